@@ -1,0 +1,206 @@
+"""Benchmark of the CP tensor-product layer forward pass on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--no-cpu-baseline] [--backward]
+
+One step is one call of tdn_cp_tp_forward on the headline workload (64
+molecules x 50 atoms, 3200 nodes, ~151k edges within 6 A, L=4, C=128,
+R=128, float32, edges pre-sorted by destination): segment offsets, the fused
+harmonics/radial/Khatri-Rao MFMA edge pass with the per-node output factor,
+and the shared channel-mix GEMM.  Inputs are resident in HBM before timing.
+Prints one JSON line.  The metric is edge tensor products per second.
+
+The roofline object reports the dominant kernel (the edge pass): its
+algorithmic flops per launch, E (2RdC + 2Rd + 17R + RC) + N 2dRC, over its
+average launch time from HIP events recorded on its launch stream, against
+the fp32 MFMA peak of 157.3 TFLOP/s.  The CPU baseline times the oracle (the
+plain float64 per-edge implementation) on a bounded sample of the same
+workload on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "edge tensor products/sec, CP-TP fwd at L=4,C=128,R=128; % MFMA/HBM roofline"
+PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_BF16_MFMA_TFLOPS = 2500.0
+FACTORS = os.path.join(ROOT, "tests", "golden", "factors")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cp_edge_fwd.json")
+
+
+def edge_kernel_flops(N, E, d, C, R):
+    return E * (2 * R * d * C + 2 * R * d + 17 * R + R * C) + N * 2 * d * R * C
+
+
+def forward_flops(N, E, d, C, R):
+    return edge_kernel_flops(N, E, d, C, R) + N * 2 * d * C * C
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("cp_edge.hip", "sh_device.hpp", "common.hpp"):
+        h.update(open(os.path.join(ROOT, "paper_2507_01131_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(workload):
+    """HBM bytes per launch of the edge kernel from the committed rocprofv3
+    counter summary, if it was taken on the current kernel source."""
+    try:
+        t = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_hash") != kernel_source_hash() or t.get("workload") != workload:
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, A, B, D, budget_s=12.0):
+    """Oracle forward on seeded batches of 64 destination nodes until about
+    budget_s seconds of work; edges/s over the sample."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import layer
+
+    rng = np.random.default_rng(0)
+    order = rng.permutation(w["N"])
+    dst = w["edge_index"][1]
+    edges = nodes = 0
+    t0 = time.perf_counter()
+    for i in range(0, w["N"], 64):
+        batch = order[i:i + 64]
+        layer.forward_at_nodes(batch, w["x"], w["edge_index"], w["edge_vec"], A, B, D, w["W"], w["radial_w"],
+                               w["r_cut"], w["L"])
+        edges += int(np.isin(dst, batch).sum())
+        nodes += len(batch)
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": edges / dt, "unit": "edge tensor products/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{nodes} of {w['N']} destination nodes ({edges} of {w['E']} edges), float64 per-edge "
+                      f"direct summation, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="molecules3200_L4_C128_R128")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--backward", action="store_true", help="also time tdn_cp_tp_backward (extra field)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the multi-GPU layout is a design "
+              "note, not a measured path", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2507_01131_amd as tdn
+    import workloads
+
+    if not os.path.exists(tdn.LIB_PATH):
+        from paper_2507_01131_amd import build as _b
+        _b.build()
+    dev = torch.device("cuda:0")
+    w = workloads.make_workload(args.workload)
+    z = np.load(os.path.join(FACTORS, f"cp_L{w['L']}_R{w['R']}.npz"))
+    A, B, D = z["A"], z["B"], z["D"]
+    N, E, d, C, R = w["N"], w["E"], w["d"], w["C"], w["R"]
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    if w["feat_dtype"] == "bf16":
+        x = t(w["x_bf16"].view(np.int16)).view(torch.bfloat16)
+        W = t(w["W_bf16"].view(np.int16)).view(torch.bfloat16)
+    else:
+        x, W = t(w["x"]), t(w["W"])
+    vec, ei, rw = t(w["edge_vec"]), t(w["edge_index"]), t(w["radial_w"])
+    At, Bt, Dt = t(A), t(B), t(D)
+    p = tdn.make_problem(w["L"], C, R, N, E, w["r_cut"], w["n_radial"],
+                         tdn.TDN_BF16 if w["feat_dtype"] == "bf16" else tdn.TDN_F32, w["presorted"])
+    fwd_bytes, bwd_bytes = tdn.workspace_size(p)
+    ws = torch.empty(fwd_bytes, dtype=torch.uint8, device=dev)
+    out = torch.empty((N, d, C), dtype=torch.float32, device=dev)
+    zsave = torch.empty((N, d, C), dtype=torch.float32, device=dev)
+    perm = torch.empty(E, dtype=torch.int32, device=dev)
+    offsets = torch.empty(N + 1, dtype=torch.int32, device=dev)
+
+    def step():
+        return tdn.forward(x, vec, ei, At, Bt, Dt, W, rw, L=w["L"], r_cut=w["r_cut"], edges_sorted=w["presorted"],
+                           workspace=ws, out=out, z=zsave, perm=perm, offsets=offsets)
+
+    for _ in range(args.warmup):
+        res = step()
+    torch.cuda.synchronize()
+    tdn.timer_enable(True)
+    for k in ("cp_edge_fwd", "node_gemm", "sort"):
+        tdn.timer_read(k, reset=True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        res = step()
+    ev1.record()
+    torch.cuda.synchronize()
+    tdn.timer_enable(False)
+    total_ms = ev0.elapsed_time(ev1)
+    ms_step = total_ms / args.steps
+    kern = {k: tdn.timer_read(k, reset=True) for k in ("cp_edge_fwd", "node_gemm", "sort")}
+    edge_ms = kern["cp_edge_fwd"][0] / max(1, kern["cp_edge_fwd"][1])
+
+    bf16 = w["feat_dtype"] == "bf16"
+    f_edge = edge_kernel_flops(N, E, d, C, R)
+    achieved = f_edge / (edge_ms * 1e-3) / 1e12
+    peak = PEAK_FP32_MFMA_TFLOPS  # the edge pass runs fp32 MFMA for both feature dtypes
+    line = {
+        "metric": METRIC,
+        "value": E / (ms_step * 1e-3),
+        "unit": "edge tensor products/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16-in/f32" if bf16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": w["name"], "N": N, "E": E, "L": w["L"], "d": d, "C": C, "R": R,
+                   "edges_presorted": bool(w["presorted"]), "pass": "forward"},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": traffic_for(w["name"]),
+                     "kernel": "cp_edge_fwd", "kernel_ms": edge_ms, "flops_per_launch": f_edge},
+        "kernel_ms_per_step": {k: v[0] / max(1, v[1]) for k, v in kern.items()},
+        "forward_tflops": forward_flops(N, E, d, C, R) / (ms_step * 1e-3) / 1e12,
+    }
+    if args.backward:
+        G = torch.from_numpy(w["grad_out"]).to(dev)
+        wsb = torch.empty(bwd_bytes, dtype=torch.uint8, device=dev)
+        for _ in range(3):
+            tdn.backward(res, G, workspace=wsb)
+        torch.cuda.synchronize()
+        ev0.record()
+        for _ in range(10):
+            tdn.backward(res, G, workspace=wsb)
+        ev1.record()
+        torch.cuda.synchronize()
+        line["backward_ms"] = ev0.elapsed_time(ev1) / 10
+        line["backward_edges_per_s"] = E / (line["backward_ms"] * 1e-3)
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, A, B, D)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,155 @@
+/*
+ * tdn.h -- C ABI of the MI355X (gfx950) CP tensor-product message-passing
+ * layer of Tensor Decomposition Networks (arXiv 2507.01131).
+ *
+ * The layer replaces the Clebsch-Gordan tensor product of an equivariant
+ * message-passing layer by its rank-R CP decomposition (Sec. 3.1, eq. cp and
+ * eq. approximate) with one channel-mixing weight shared by every path
+ * (Sec. 3.2).  For an edge e = (s, t) with vector r_e:
+ *
+ *   Y_e   = Y(r_e/|r_e|)              real spherical harmonics, degrees 0..L
+ *   phi_e = exp(-(|r_e|-mu_q)^2/(2 sigma^2)),  mu_q = q r_cut/(n_radial-1),
+ *           sigma = r_cut/(n_radial-1),  q = 0..n_radial-1
+ *   g_e   = (B^T Y_e) * (phi_e radial_w)          (elementwise, length R)
+ *   m_e   = D diag(g_e) A^T x[s] W                ([d, C])
+ *   out[t] = sum over edges e into t of m_e
+ *
+ * Factor names: D is the output-mode factor (the paper's A), A acts on the
+ * node features (the paper's B), B acts on the harmonics (the paper's C).
+ *
+ * Basis of the harmonics: index l*l + l + m (m = -l..l), real functions
+ * without the Condon-Shortley phase, z the polar axis, m > 0 from
+ * Re((x+iy)^m), m < 0 from Im((x+iy)^|m|), normalised so that Y_00 = 1 and
+ * sum_m Y_lm^2 = 2l+1 on the unit sphere.
+ *
+ * Conventions for every entry point
+ *  - Tensor pointers are DEVICE pointers owned by the caller, row-major and
+ *    contiguous, 16-byte aligned.  The library allocates nothing; scratch
+ *    space comes from the caller's workspace (size from tdn_workspace_size).
+ *  - Work is enqueued asynchronously on `stream`; the return value reports
+ *    argument validation and launch status.  With problem->validate = 1 the
+ *    call also checks the edge data on the device and synchronises `stream`.
+ *  - Outputs are overwritten, never accumulated.  A node without incoming
+ *    edges gets a zero row.  E = 0 is valid.
+ *  - Summation order is fixed (sorted-edge order, no floating-point
+ *    atomics): repeated calls give bitwise identical results.
+ *  - No exception or abort crosses the ABI.  Calls on different streams with
+ *    different workspaces may run concurrently.
+ */
+#ifndef TDN_H
+#define TDN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TDN_OK = 0,
+  TDN_ERR_NULL_POINTER = 1,        /* a required pointer is NULL                 */
+  TDN_ERR_BAD_SHAPE = 2,           /* L, C, R, N, E, n_radial or r_cut invalid    */
+  TDN_ERR_BAD_DTYPE = 3,           /* feat_dtype not a tdn_dtype                  */
+  TDN_ERR_WORKSPACE_TOO_SMALL = 4, /* workspace_bytes below tdn_workspace_size    */
+  TDN_ERR_INDEX_OUT_OF_RANGE = 5,  /* validate=1: src or dst outside [0, N)       */
+  TDN_ERR_NOT_SORTED = 6,          /* validate=1: edges_sorted=1 but dst decreases */
+  TDN_ERR_DEGENERATE_EDGE = 7,     /* validate=1: zero-length or non-finite r_e   */
+  TDN_ERR_UNSUPPORTED_DEVICE = 8,  /* current device is not gfx950                */
+  TDN_ERR_HIP = 9                  /* a HIP call failed, see tdn_last_hip_error   */
+} tdn_status;
+
+typedef enum { TDN_F32 = 0, TDN_BF16 = 1 } tdn_dtype;
+
+typedef struct {
+  int32_t L;            /* maximum degree, 0..6; d = (L+1)^2 components          */
+  int32_t C;            /* channels (shared multiplicity), multiple of 16, <= 1024 */
+  int32_t R;            /* CP rank, 1..256                                          */
+  int32_t n_nodes;      /* N >= 0                                                   */
+  int32_t n_edges;      /* E >= 0 (E > 0 needs N > 0)                              */
+  int32_t n_radial;     /* Gaussian radial functions, 2..16                        */
+  float r_cut;          /* cutoff setting the Gaussian centres and width, > 0      */
+  tdn_dtype feat_dtype; /* dtype of x and W (TDN_F32 or TDN_BF16); all else f32     */
+  int32_t edges_sorted; /* 1: edge_index already stably sorted by dst (perm is the
+                           identity); 0: the call sorts                            */
+  int32_t validate;     /* 1: check indices, order and edge vectors on the device */
+} tdn_problem;
+
+/* Workspace bytes needed by tdn_cp_tp_forward (*fwd_bytes) and
+ * tdn_cp_tp_backward (*bwd_bytes); either pointer may be NULL.  The sizes
+ * assume z_save == NULL (forward) and z_save == NULL (backward), i.e. the
+ * largest case. */
+tdn_status tdn_workspace_size(const tdn_problem* p, size_t* fwd_bytes, size_t* bwd_bytes);
+
+/* Forward pass (Sec. 3.1 eq. approximate per edge, Sec. 3.2 shared W, summed
+ * into the destination nodes).
+ *   x          [N, d, C]  feat_dtype   node features, channel fastest
+ *   edge_vec   [E, 3]     f32          r_e = pos[src] - pos[dst] (+ image shift)
+ *   edge_index [2, E]     int32        row 0 = src, row 1 = dst
+ *   A, B, D    [d, R]     f32          CP factors (constants)
+ *   W          [C, C]     feat_dtype   out = Z W, W[c_in, c_out]
+ *   radial_w   [n_radial, R] f32
+ *   out        [N, d, C]  f32          overwritten
+ *   z_save     [N, d, C]  f32 or NULL  Z = per-node sum of D diag(g) A^T x[s]
+ *                                      (the layer before W), kept for backward
+ *   perm       [E]        int32        sorted slot -> original edge id (stable
+ *                                      by dst; ties keep the original order)
+ *   offsets    [N+1]      int32        first sorted slot of each dst node,
+ *                                      offsets[N] = E
+ * perm and offsets are always written (bit-exact integer results). */
+tdn_status tdn_cp_tp_forward(const tdn_problem* p, const void* x, const float* edge_vec,
+                             const int32_t* edge_index, const float* A, const float* B,
+                             const float* D, const void* W, const float* radial_w, float* out,
+                             float* z_save, int32_t* perm, int32_t* offsets, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+/* Backward pass for the scalar <grad_out, out>.  perm and offsets are the
+ * forward's outputs; z_save is the forward's saved Z or NULL (then Z is
+ * recomputed).  Each gradient pointer may be NULL to skip it; grads are f32
+ * for any feat_dtype:
+ *   grad_x        [N, d, C]  dL/dx
+ *   grad_W        [C, C]     dL/dW
+ *   grad_edge_vec [E, 3]     dL/dr_e, in the caller's original edge order
+ * The factors and radial_w are constants (no gradient). */
+tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* edge_vec,
+                              const int32_t* edge_index, const float* A, const float* B,
+                              const float* D, const void* W, const float* radial_w,
+                              const int32_t* perm, const int32_t* offsets, const float* z_save,
+                              const float* grad_out, float* grad_x, float* grad_W,
+                              float* grad_edge_vec, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+
+/* Stable sort of E integer keys in [0, n_keys): perm[p] = original index of
+ * the p-th smallest key (equal keys keep their original order), offsets[k] =
+ * number of keys < k, offsets[n_keys] = E.  Keys outside the range give
+ * undefined perm/offsets (no memory fault).  Workspace from
+ * tdn_sort_workspace_size. */
+tdn_status tdn_sort_workspace_size(int32_t n_keys, int32_t E, size_t* bytes);
+tdn_status tdn_sort_by_key(int32_t n_keys, int32_t E, const int32_t* keys, int32_t* perm,
+                           int32_t* offsets, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream);
+
+/* Real spherical harmonics of edge directions (basis as above):
+ *   Y  [E, d]     Y(r_e/|r_e|)
+ *   dY [E, d, 3]  dY/dr_e (or NULL) */
+tdn_status tdn_spherical_harmonics(int32_t L, int32_t E, const float* edge_vec, float* Y,
+                                   float* dY, hipStream_t stream);
+
+/* Per-kernel timing with HIP events recorded on the launch stream.
+ * tdn_timer_enable(1) starts recording every launch of the layer's edge
+ * kernels; tdn_timer_read synchronises on the recorded events and returns
+ * the summed milliseconds and launch count of the kernel named `kernel`
+ * ("cp_edge_fwd", "cp_edge_bwd_src", "cp_bwd_dst", "node_gemm", "sort");
+ * reset = 1 clears that kernel's record. */
+tdn_status tdn_timer_enable(int32_t enable);
+tdn_status tdn_timer_read(const char* kernel, double* total_ms, int32_t* launches, int32_t reset);
+
+const char* tdn_status_string(tdn_status s);
+int32_t tdn_last_hip_error(void); /* hipError_t behind the calling thread's last TDN_ERR_HIP */
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TDN_H */

@@ -1,0 +1,240 @@
+"""MI355X (gfx950) CP tensor-product message-passing layer of Tensor
+Decomposition Networks (arXiv 2507.01131).
+
+This module is the Python binding of ``libtdn.so`` (ctypes).  It only
+marshals arguments: every step of the layer runs in the library's HIP
+kernels; torch provides device memory and the current stream.  It raises if
+the library is not built -- there is no fallback implementation.
+
+    import paper_2507_01131_amd as tdn
+    res = tdn.forward(x, edge_vec, edge_index, A, B, D, W, radial_w, L=4, r_cut=6.0)
+    grads = tdn.backward(res, grad_out)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+__all__ = ["forward", "backward", "sort_by_key", "spherical_harmonics", "workspace_size", "Problem",
+           "TdnError", "lib", "timer_enable", "timer_read", "LIB_PATH", "status_string"]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtdn.so")
+
+TDN_F32, TDN_BF16 = 0, 1
+STATUS = {0: "TDN_OK", 1: "TDN_ERR_NULL_POINTER", 2: "TDN_ERR_BAD_SHAPE", 3: "TDN_ERR_BAD_DTYPE",
+          4: "TDN_ERR_WORKSPACE_TOO_SMALL", 5: "TDN_ERR_INDEX_OUT_OF_RANGE", 6: "TDN_ERR_NOT_SORTED",
+          7: "TDN_ERR_DEGENERATE_EDGE", 8: "TDN_ERR_UNSUPPORTED_DEVICE", 9: "TDN_ERR_HIP"}
+
+
+class TdnError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        extra = ""
+        if status == 9:
+            extra = f" (hipError {lib().tdn_last_hip_error()})"
+        super().__init__(f"{where}: {STATUS.get(status, status)}{extra}")
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("L", ctypes.c_int32), ("C", ctypes.c_int32), ("R", ctypes.c_int32),
+                ("n_nodes", ctypes.c_int32), ("n_edges", ctypes.c_int32), ("n_radial", ctypes.c_int32),
+                ("r_cut", ctypes.c_float), ("feat_dtype", ctypes.c_int32), ("edges_sorted", ctypes.c_int32),
+                ("validate", ctypes.c_int32)]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_SZ = ctypes.c_size_t
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libtdn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2507_01131_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        PP = ctypes.POINTER(Problem)
+        L.tdn_workspace_size.argtypes = [PP, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)]
+        L.tdn_cp_tp_forward.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
+        L.tdn_cp_tp_backward.argtypes = [PP] + [_P] * 16 + [_SZ, _P]
+        L.tdn_sort_workspace_size.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_SZ)]
+        L.tdn_sort_by_key.argtypes = [ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P, _SZ, _P]
+        L.tdn_spherical_harmonics.argtypes = [ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P]
+        L.tdn_timer_enable.argtypes = [ctypes.c_int32]
+        L.tdn_timer_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                     ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]
+        L.tdn_status_string.argtypes = [ctypes.c_int]
+        L.tdn_status_string.restype = ctypes.c_char_p
+        L.tdn_last_hip_error.restype = ctypes.c_int32
+        for f in ("tdn_workspace_size", "tdn_cp_tp_forward", "tdn_cp_tp_backward", "tdn_sort_workspace_size",
+                  "tdn_sort_by_key", "tdn_spherical_harmonics", "tdn_timer_enable", "tdn_timer_read"):
+            getattr(L, f).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(s: int) -> str:
+    return lib().tdn_status_string(s).decode()
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise TdnError(status, where)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def make_problem(L, C, R, n_nodes, n_edges, r_cut, n_radial=8, feat_dtype=TDN_F32, edges_sorted=False,
+                 validate=False) -> Problem:
+    return Problem(int(L), int(C), int(R), int(n_nodes), int(n_edges), int(n_radial), float(r_cut),
+                   int(feat_dtype), int(bool(edges_sorted)), int(bool(validate)))
+
+
+def workspace_size(p: Problem) -> tuple[int, int]:
+    f, b = _SZ(), _SZ()
+    _check(lib().tdn_workspace_size(ctypes.byref(p), ctypes.byref(f), ctypes.byref(b)), "tdn_workspace_size")
+    return f.value, b.value
+
+
+def _need(t, name, dtype, shape, device):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.device != device:
+        raise ValueError(f"{name}: on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+@dataclass
+class ForwardResult:
+    out: torch.Tensor
+    z: torch.Tensor | None
+    perm: torch.Tensor
+    offsets: torch.Tensor
+    problem: Problem
+    inputs: dict
+
+
+def forward(x, edge_vec, edge_index, A, B, D, W, radial_w, *, L: int, r_cut: float, edges_sorted=False,
+            validate=False, save_z=True, workspace=None, out=None, z=None, perm=None, offsets=None,
+            stream=None) -> ForwardResult:
+    """Runs tdn_cp_tp_forward.  x [N,d,C] and W [C,C] are float32 or bfloat16
+    (both the same); edge_index [2,E] int32 (int64 is converted); everything
+    else float32 on the same device.  out, z, perm, offsets and workspace may
+    be passed preallocated; otherwise they are allocated here."""
+    dev = x.device
+    N, d, C = x.shape
+    E = edge_vec.shape[0]
+    R = A.shape[1]
+    if edge_index.dtype != torch.int32:
+        edge_index = edge_index.to(torch.int32)
+    edge_index = edge_index.contiguous()
+    fd = TDN_BF16 if x.dtype == torch.bfloat16 else TDN_F32
+    for t, n, dt, sh in [(x, "x", x.dtype, (N, d, C)), (edge_vec, "edge_vec", torch.float32, (E, 3)),
+                         (edge_index, "edge_index", torch.int32, (2, E)), (A, "A", torch.float32, (d, R)),
+                         (B, "B", torch.float32, (d, R)), (D, "D", torch.float32, (d, R)),
+                         (W, "W", x.dtype, (C, C)), (radial_w, "radial_w", torch.float32, (radial_w.shape[0], R))]:
+        _need(t, n, dt, sh, dev)
+    if x.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("x must be float32 or bfloat16")
+    p = make_problem(L, C, R, N, E, r_cut, radial_w.shape[0], fd, edges_sorted, validate)
+    fwd_bytes, _ = workspace_size(p)
+    if workspace is None or workspace.numel() < fwd_bytes:
+        workspace = torch.empty(max(fwd_bytes, 1), dtype=torch.uint8, device=dev)
+    if out is None:
+        out = torch.empty((N, d, C), dtype=torch.float32, device=dev)
+    if z is None and save_z:
+        z = torch.empty((N, d, C), dtype=torch.float32, device=dev)
+    if perm is None:
+        perm = torch.empty(max(E, 1), dtype=torch.int32, device=dev)[:E]
+    if offsets is None:
+        offsets = torch.empty(N + 1, dtype=torch.int32, device=dev)
+    _need(out, "out", torch.float32, (N, d, C), dev)
+    if z is not None:
+        _need(z, "z", torch.float32, (N, d, C), dev)
+    _need(perm, "perm", torch.int32, (E,), dev)
+    _need(offsets, "offsets", torch.int32, (N + 1,), dev)
+    st = lib().tdn_cp_tp_forward(ctypes.byref(p), _ptr(x), _ptr(edge_vec), _ptr(edge_index), _ptr(A), _ptr(B),
+                                 _ptr(D), _ptr(W), _ptr(radial_w), _ptr(out), _ptr(z), _ptr(perm), _ptr(offsets),
+                                 _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "tdn_cp_tp_forward")
+    return ForwardResult(out, z, perm, offsets, p,
+                         dict(x=x, edge_vec=edge_vec, edge_index=edge_index, A=A, B=B, D=D, W=W, radial_w=radial_w))
+
+
+def backward(res: ForwardResult, grad_out, *, need_x=True, need_W=True, need_vec=True, use_saved_z=True,
+             workspace=None, stream=None):
+    """Runs tdn_cp_tp_backward; returns (grad_x, grad_W, grad_edge_vec), each
+    float32 or None."""
+    i = res.inputs
+    x = i["x"]
+    dev = x.device
+    N, d, C = x.shape
+    E = i["edge_vec"].shape[0]
+    _need(grad_out, "grad_out", torch.float32, (N, d, C), dev)
+    p = res.problem
+    _, bwd_bytes = workspace_size(p)
+    if workspace is None or workspace.numel() < bwd_bytes:
+        workspace = torch.empty(max(bwd_bytes, 1), dtype=torch.uint8, device=dev)
+    gx = torch.empty((N, d, C), dtype=torch.float32, device=dev) if need_x else None
+    gW = torch.empty((C, C), dtype=torch.float32, device=dev) if need_W else None
+    gv = torch.empty((E, 3), dtype=torch.float32, device=dev) if need_vec else None
+    z = res.z if use_saved_z else None
+    st = lib().tdn_cp_tp_backward(ctypes.byref(p), _ptr(x), _ptr(i["edge_vec"]), _ptr(i["edge_index"]), _ptr(i["A"]),
+                                  _ptr(i["B"]), _ptr(i["D"]), _ptr(i["W"]), _ptr(i["radial_w"]), _ptr(res.perm),
+                                  _ptr(res.offsets), _ptr(z), _ptr(grad_out), _ptr(gx), _ptr(gW), _ptr(gv),
+                                  _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "tdn_cp_tp_backward")
+    return gx, gW, gv
+
+
+def sort_by_key(keys: torch.Tensor, n_keys: int, stream=None):
+    """Stable sort of int32 keys in [0, n_keys): returns (perm, offsets)."""
+    if keys.dtype != torch.int32 or not keys.is_contiguous():
+        raise TypeError("keys must be contiguous int32")
+    E = keys.numel()
+    nb = _SZ()
+    _check(lib().tdn_sort_workspace_size(int(n_keys), int(E), ctypes.byref(nb)), "tdn_sort_workspace_size")
+    ws = torch.empty(max(nb.value, 1), dtype=torch.uint8, device=keys.device)
+    perm = torch.empty(max(E, 1), dtype=torch.int32, device=keys.device)[:E]
+    offsets = torch.empty(n_keys + 1, dtype=torch.int32, device=keys.device)
+    _check(lib().tdn_sort_by_key(int(n_keys), int(E), _ptr(keys), _ptr(perm), _ptr(offsets), _ptr(ws), ws.numel(),
+                                 _stream(stream)), "tdn_sort_by_key")
+    return perm, offsets
+
+
+def spherical_harmonics(edge_vec: torch.Tensor, L: int, jacobian=False, stream=None):
+    E = edge_vec.shape[0]
+    _need(edge_vec, "edge_vec", torch.float32, (E, 3), edge_vec.device)
+    d = (L + 1) ** 2
+    Y = torch.empty((E, d), dtype=torch.float32, device=edge_vec.device)
+    J = torch.empty((E, d, 3), dtype=torch.float32, device=edge_vec.device) if jacobian else None
+    _check(lib().tdn_spherical_harmonics(int(L), int(E), _ptr(edge_vec), _ptr(Y), _ptr(J), _stream(stream)),
+           "tdn_spherical_harmonics")
+    return (Y, J) if jacobian else Y
+
+
+def timer_enable(on: bool = True):
+    _check(lib().tdn_timer_enable(int(bool(on))), "tdn_timer_enable")
+
+
+def timer_read(kernel: str, reset=True) -> tuple[float, int]:
+    ms, n = ctypes.c_double(), ctypes.c_int32()
+    _check(lib().tdn_timer_read(kernel.encode(), ctypes.byref(ms), ctypes.byref(n), int(reset)), "tdn_timer_read")
+    return ms.value, n.value

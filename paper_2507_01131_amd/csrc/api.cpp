@@ -1,0 +1,398 @@
+// C ABI of the CP tensor-product layer: argument validation, workspace
+// layout, launch sequence and status reporting.  No allocation happens here:
+// every scratch buffer is carved from the caller's workspace.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "kernels.h"
+#include "tdn.h"
+
+namespace tdn {
+size_t bwd_dst_lds_bytes(int R, int d, int n_radial, int C);
+}
+
+namespace {
+
+thread_local int32_t g_last_hip = 0;
+
+size_t al(size_t b) { return (b + 255) & ~size_t(255); }
+
+tdn_status hip_fail(hipError_t e) {
+  g_last_hip = int32_t(e);
+  return TDN_ERR_HIP;
+}
+
+#define TDN_HIP(expr)                           \
+  do {                                          \
+    hipError_t e_ = (expr);                     \
+    if (e_ != hipSuccess) return hip_fail(e_);  \
+  } while (0)
+
+int dim_of(int L) { return (L + 1) * (L + 1); }
+
+tdn_status check_problem(const tdn_problem* p) {
+  if (!p) return TDN_ERR_NULL_POINTER;
+  if (p->feat_dtype != TDN_F32 && p->feat_dtype != TDN_BF16) return TDN_ERR_BAD_DTYPE;
+  if (p->L < 0 || p->L > 6) return TDN_ERR_BAD_SHAPE;
+  if (p->C < 16 || p->C > 256 || p->C % 16 != 0) return TDN_ERR_BAD_SHAPE;
+  if (p->R < 1 || p->R > 256) return TDN_ERR_BAD_SHAPE;
+  if (p->n_nodes < 0 || p->n_edges < 0) return TDN_ERR_BAD_SHAPE;
+  if (p->n_edges > 0 && p->n_nodes == 0) return TDN_ERR_BAD_SHAPE;
+  if (p->n_radial < 2 || p->n_radial > 16) return TDN_ERR_BAD_SHAPE;
+  if (!(p->r_cut > 0.f) || !std::isfinite(p->r_cut)) return TDN_ERR_BAD_SHAPE;
+  if (int64_t(p->n_nodes) * dim_of(p->L) * p->C >= (int64_t(1) << 40)) return TDN_ERR_BAD_SHAPE;
+  if (int64_t(p->n_nodes) * dim_of(p->L) >= (int64_t(1) << 31) - 1) return TDN_ERR_BAD_SHAPE;
+  if (p->edges_sorted != 0 && p->edges_sorted != 1) return TDN_ERR_BAD_SHAPE;
+  return TDN_OK;
+}
+
+struct FwdLayout {
+  size_t z, sort, flags, total;
+};
+FwdLayout fwd_layout(const tdn_problem& p) {
+  FwdLayout f{};
+  const size_t ndc = size_t(p.n_nodes) * dim_of(p.L) * p.C * 4;
+  size_t o = 0;
+  f.z = o;
+  o += al(ndc);
+  f.sort = o;
+  o += al(p.edges_sorted ? 0 : tdn::sort_plan(p.n_nodes, p.n_edges).bytes);
+  f.flags = o;
+  o += 256;
+  f.total = o;
+  return f;
+}
+
+struct BwdLayout {
+  size_t gz, z, parts, perm_src, off_src, sort, flags, total;
+};
+BwdLayout bwd_layout(const tdn_problem& p) {
+  BwdLayout b{};
+  const size_t ndc = size_t(p.n_nodes) * dim_of(p.L) * p.C * 4;
+  size_t o = 0;
+  b.gz = o;
+  o += al(ndc);
+  b.z = o;
+  o += al(ndc);
+  b.parts = o;
+  o += al(size_t(tdn::gram_parts(p.n_nodes * dim_of(p.L))) * p.C * p.C * 4);
+  b.perm_src = o;
+  o += al(size_t(p.n_edges) * 4);
+  b.off_src = o;
+  o += al(size_t(p.n_nodes + 1) * 4);
+  b.sort = o;
+  o += al(tdn::sort_plan(p.n_nodes, p.n_edges).bytes);
+  b.flags = o;
+  o += 256;
+  b.total = o;
+  return b;
+}
+
+tdn_status check_device() {
+  int dev = 0;
+  TDN_HIP(hipGetDevice(&dev));
+  static std::mutex mu;
+  static std::map<int, bool> known;
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = known.find(dev);
+  if (it == known.end()) {
+    hipDeviceProp_t prop;
+    TDN_HIP(hipGetDeviceProperties(&prop, dev));
+    it = known.emplace(dev, std::strncmp(prop.gcnArchName, "gfx950", 6) == 0).first;
+  }
+  return it->second ? TDN_OK : TDN_ERR_UNSUPPORTED_DEVICE;
+}
+
+// --------------------------------------------------------------- timing
+struct Timer {
+  bool on = false;
+  std::mutex mu;
+  std::map<std::string, std::vector<std::pair<hipEvent_t, hipEvent_t>>> pending;
+  std::map<std::string, std::pair<double, int>> done;
+};
+Timer& timer() {
+  static Timer t;
+  return t;
+}
+
+class Timed {
+ public:
+  Timed(const char* name, hipStream_t s) : name_(name), s_(s) {
+    Timer& t = timer();
+    std::lock_guard<std::mutex> lk(t.mu);
+    if (!t.on) return;
+    if (hipEventCreate(&a_) != hipSuccess || hipEventCreate(&b_) != hipSuccess) return;
+    hipEventRecord(a_, s_);
+  }
+  ~Timed() {
+    if (!a_ || !b_) return;
+    hipEventRecord(b_, s_);
+    Timer& t = timer();
+    std::lock_guard<std::mutex> lk(t.mu);
+    t.pending[name_].emplace_back(a_, b_);
+  }
+
+ private:
+  const char* name_;
+  hipStream_t s_;
+  hipEvent_t a_ = nullptr, b_ = nullptr;
+};
+
+tdn_status run_validation(const tdn_problem& p, const int32_t* edge_index, const float* edge_vec, char* ws,
+                          size_t flags_off, int check_sorted, hipStream_t s) {
+  int32_t* flags = reinterpret_cast<int32_t*>(ws + flags_off);
+  TDN_HIP(tdn::launch_validate(p.n_nodes, p.n_edges, edge_index, edge_vec, check_sorted, flags, s));
+  int32_t host[4] = {0, 0, 0, 0};
+  TDN_HIP(hipMemcpyAsync(host, flags, sizeof(host), hipMemcpyDeviceToHost, s));
+  TDN_HIP(hipStreamSynchronize(s));
+  if (host[0]) return TDN_ERR_INDEX_OUT_OF_RANGE;
+  if (host[1]) return TDN_ERR_NOT_SORTED;
+  if (host[2]) return TDN_ERR_DEGENERATE_EDGE;
+  return TDN_OK;
+}
+
+tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int32_t* perm, const int32_t* gather,
+                        const float* edge_vec, const float* KF, const float* EF, const float* B, const float* radial_w,
+                        const void* feat, float* out) {
+  tdn::EdgeArgs a{};
+  a.n_seg = p.n_nodes;
+  a.E = p.n_edges;
+  a.L = p.L;
+  a.d = dim_of(p.L);
+  a.C = p.C;
+  a.R = p.R;
+  a.n_radial = p.n_radial;
+  a.sigma = p.r_cut / float(p.n_radial - 1);
+  a.offsets = offsets;
+  a.perm = perm;
+  a.gather = gather;
+  a.edge_vec = edge_vec;
+  a.KF = KF;
+  a.EF = EF;
+  a.Bf = B;
+  a.radial_w = radial_w;
+  a.feat = feat;
+  a.out = out;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tdn_status_string(tdn_status s) {
+  switch (s) {
+    case TDN_OK: return "ok";
+    case TDN_ERR_NULL_POINTER: return "null pointer";
+    case TDN_ERR_BAD_SHAPE: return "bad shape";
+    case TDN_ERR_BAD_DTYPE: return "bad dtype";
+    case TDN_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case TDN_ERR_INDEX_OUT_OF_RANGE: return "edge index out of range";
+    case TDN_ERR_NOT_SORTED: return "edges not sorted by destination";
+    case TDN_ERR_DEGENERATE_EDGE: return "zero-length or non-finite edge vector";
+    case TDN_ERR_UNSUPPORTED_DEVICE: return "unsupported device (needs gfx950)";
+    case TDN_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+int32_t tdn_last_hip_error(void) { return g_last_hip; }
+
+tdn_status tdn_workspace_size(const tdn_problem* p, size_t* fwd_bytes, size_t* bwd_bytes) {
+  const tdn_status st = check_problem(p);
+  if (st != TDN_OK) return st;
+  if (fwd_bytes) *fwd_bytes = fwd_layout(*p).total;
+  if (bwd_bytes) *bwd_bytes = bwd_layout(*p).total;
+  return TDN_OK;
+}
+
+tdn_status tdn_cp_tp_forward(const tdn_problem* p, const void* x, const float* edge_vec, const int32_t* edge_index,
+                             const float* A, const float* B, const float* D, const void* W, const float* radial_w,
+                             float* out, float* z_save, int32_t* perm, int32_t* offsets, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  tdn_status st = check_problem(p);
+  if (st != TDN_OK) return st;
+  const int N = p->n_nodes, E = p->n_edges, d = dim_of(p->L), C = p->C;
+  if (!A || !B || !D || !W || !radial_w || !offsets || !workspace) return TDN_ERR_NULL_POINTER;
+  if (N > 0 && (!x || !out)) return TDN_ERR_NULL_POINTER;
+  if (E > 0 && (!edge_vec || !edge_index || !perm)) return TDN_ERR_NULL_POINTER;
+  const FwdLayout lay = fwd_layout(*p);
+  if (workspace_bytes < lay.total) return TDN_ERR_WORKSPACE_TOO_SMALL;
+  st = check_device();
+  if (st != TDN_OK) return st;
+  char* ws = static_cast<char*>(workspace);
+  if (p->validate) {
+    st = run_validation(*p, edge_index, edge_vec, ws, lay.flags, p->edges_sorted, stream);
+    if (st != TDN_OK) return st;
+  }
+  const int32_t* src = edge_index;
+  const int32_t* dst = E > 0 ? edge_index + E : nullptr;
+  {
+    Timed t("sort", stream);
+    if (p->edges_sorted || E == 0)
+      TDN_HIP(tdn::launch_offsets_presorted(N, E, dst, perm, offsets, stream));
+    else
+      TDN_HIP(tdn::launch_sort(tdn::sort_plan(N, E), dst, 1, perm, offsets, ws + lay.sort, stream));
+  }
+  if (N == 0) return TDN_OK;
+  float* Z = z_save ? z_save : reinterpret_cast<float*>(ws + lay.z);
+  const bool bf16 = p->feat_dtype == TDN_BF16;
+  {
+    Timed t("cp_edge_fwd", stream);
+    TDN_HIP(tdn::launch_cp_edge(edge_args(*p, offsets, perm, src, edge_vec, A, D, B, radial_w, x, Z), bf16, stream));
+  }
+  {
+    Timed t("node_gemm", stream);
+    TDN_HIP(tdn::launch_node_gemm(N * d, C, Z, W, bf16, 0, out, stream));
+  }
+  return TDN_OK;
+}
+
+tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* edge_vec, const int32_t* edge_index,
+                              const float* A, const float* B, const float* D, const void* W, const float* radial_w,
+                              const int32_t* perm, const int32_t* offsets, const float* z_save,
+                              const float* grad_out, float* grad_x, float* grad_W, float* grad_edge_vec,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  tdn_status st = check_problem(p);
+  if (st != TDN_OK) return st;
+  const int N = p->n_nodes, E = p->n_edges, d = dim_of(p->L), C = p->C;
+  if (!A || !B || !D || !W || !radial_w || !offsets || !workspace) return TDN_ERR_NULL_POINTER;
+  if (N > 0 && (!x || !grad_out)) return TDN_ERR_NULL_POINTER;
+  if (E > 0 && (!edge_vec || !edge_index || !perm)) return TDN_ERR_NULL_POINTER;
+  const BwdLayout lay = bwd_layout(*p);
+  if (workspace_bytes < lay.total) return TDN_ERR_WORKSPACE_TOO_SMALL;
+  st = check_device();
+  if (st != TDN_OK) return st;
+  char* ws = static_cast<char*>(workspace);
+  if (p->validate) {
+    st = run_validation(*p, edge_index, edge_vec, ws, lay.flags, 0, stream);
+    if (st != TDN_OK) return st;
+  }
+  const bool bf16 = p->feat_dtype == TDN_BF16;
+  const int32_t* src = edge_index;
+  const int32_t* dst = E > 0 ? edge_index + E : nullptr;
+  if (N == 0) {
+    if (grad_W) TDN_HIP(tdn::launch_zero(grad_W, size_t(C) * C * 4, stream));
+    return TDN_OK;
+  }
+  float* Gz = reinterpret_cast<float*>(ws + lay.gz);
+  {
+    Timed t("node_gemm", stream);
+    TDN_HIP(tdn::launch_node_gemm(N * d, C, grad_out, W, bf16, 1, Gz, stream));
+  }
+  if (grad_W) {
+    const float* Z = z_save;
+    if (!Z) {
+      float* Zw = reinterpret_cast<float*>(ws + lay.z);
+      Timed t("cp_edge_fwd", stream);
+      TDN_HIP(tdn::launch_cp_edge(edge_args(*p, offsets, perm, src, edge_vec, A, D, B, radial_w, x, Zw), bf16, stream));
+      Z = Zw;
+    }
+    Timed t("gram", stream);
+    TDN_HIP(tdn::launch_gram(N * d, C, Z, grad_out, reinterpret_cast<float*>(ws + lay.parts), grad_W, stream));
+  }
+  if (grad_edge_vec && E > 0) {
+    tdn::BwdDstArgs a{};
+    a.n_seg = N;
+    a.E = E;
+    a.L = p->L;
+    a.d = d;
+    a.C = C;
+    a.R = p->R;
+    a.n_radial = p->n_radial;
+    a.sigma = p->r_cut / float(p->n_radial - 1);
+    a.offsets = offsets;
+    a.perm = perm;
+    a.src = src;
+    a.edge_vec = edge_vec;
+    a.A = A;
+    a.Bf = B;
+    a.D = D;
+    a.radial_w = radial_w;
+    a.x = x;
+    a.Gz = Gz;
+    a.grad_vec = grad_edge_vec;
+    Timed t("cp_bwd_dst", stream);
+    TDN_HIP(tdn::launch_bwd_dst(a, bf16, stream));
+  }
+  if (grad_x) {
+    int32_t* perm_src = reinterpret_cast<int32_t*>(ws + lay.perm_src);
+    int32_t* off_src = reinterpret_cast<int32_t*>(ws + lay.off_src);
+    {
+      Timed t("sort", stream);
+      TDN_HIP(tdn::launch_sort(tdn::sort_plan(N, E), src, 1, perm_src, off_src, ws + lay.sort, stream));
+    }
+    Timed t("cp_edge_bwd_src", stream);
+    TDN_HIP(tdn::launch_cp_edge(edge_args(*p, off_src, perm_src, dst, edge_vec, D, A, B, radial_w, Gz, grad_x), false,
+                                stream));
+  }
+  return TDN_OK;
+}
+
+tdn_status tdn_sort_workspace_size(int32_t n_keys, int32_t E, size_t* bytes) {
+  if (!bytes) return TDN_ERR_NULL_POINTER;
+  if (n_keys < 0 || E < 0 || (E > 0 && n_keys == 0)) return TDN_ERR_BAD_SHAPE;
+  *bytes = tdn::sort_plan(n_keys, E).bytes + 256;
+  return TDN_OK;
+}
+
+tdn_status tdn_sort_by_key(int32_t n_keys, int32_t E, const int32_t* keys, int32_t* perm, int32_t* offsets,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (n_keys < 0 || E < 0 || (E > 0 && n_keys == 0)) return TDN_ERR_BAD_SHAPE;
+  if (!offsets || !workspace || (E > 0 && (!keys || !perm))) return TDN_ERR_NULL_POINTER;
+  const tdn::SortPlan plan = tdn::sort_plan(n_keys, E);
+  if (workspace_bytes < plan.bytes + 256) return TDN_ERR_WORKSPACE_TOO_SMALL;
+  tdn_status st = check_device();
+  if (st != TDN_OK) return st;
+  Timed t("sort", stream);
+  TDN_HIP(tdn::launch_sort(plan, keys, 1, perm, offsets, workspace, stream));
+  return TDN_OK;
+}
+
+tdn_status tdn_spherical_harmonics(int32_t L, int32_t E, const float* edge_vec, float* Y, float* dY,
+                                   hipStream_t stream) {
+  if (L < 0 || L > 6 || E < 0) return TDN_ERR_BAD_SHAPE;
+  if (E > 0 && (!edge_vec || !Y)) return TDN_ERR_NULL_POINTER;
+  tdn_status st = check_device();
+  if (st != TDN_OK) return st;
+  TDN_HIP(tdn::launch_sh(L, E, edge_vec, Y, dY, stream));
+  return TDN_OK;
+}
+
+tdn_status tdn_timer_enable(int32_t enable) {
+  Timer& t = timer();
+  std::lock_guard<std::mutex> lk(t.mu);
+  t.on = enable != 0;
+  return TDN_OK;
+}
+
+tdn_status tdn_timer_read(const char* kernel, double* total_ms, int32_t* launches, int32_t reset) {
+  if (!kernel || !total_ms || !launches) return TDN_ERR_NULL_POINTER;
+  Timer& t = timer();
+  std::lock_guard<std::mutex> lk(t.mu);
+  auto& pend = t.pending[kernel];
+  auto& acc = t.done[kernel];
+  for (auto& ev : pend) {
+    TDN_HIP(hipEventSynchronize(ev.second));
+    float ms = 0.f;
+    TDN_HIP(hipEventElapsedTime(&ms, ev.first, ev.second));
+    acc.first += ms;
+    acc.second += 1;
+    hipEventDestroy(ev.first);
+    hipEventDestroy(ev.second);
+  }
+  pend.clear();
+  *total_ms = acc.first;
+  *launches = acc.second;
+  if (reset) acc = {0.0, 0};
+  return TDN_OK;
+}
+
+}  // extern "C"

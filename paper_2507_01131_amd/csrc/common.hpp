@@ -1,0 +1,44 @@
+// Shared device helpers for the gfx950 kernels of the CP tensor-product layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tdn {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kTile = 32;  // MFMA 32x32 output tile
+constexpr int kNumXcd = 8;  // MI355X: 8 accelerator complex dies, blocks dealt round-robin
+
+// One 32x32x2 fp32 MFMA.  Lane l supplies a = A[l%32][l/32] and
+// b = B[l/32][l%32]; the 32x32 result is spread so that accumulator
+// register v of lane l holds row acc_row(v, l/32), column l%32.
+__device__ __forceinline__ f32x16 mfma32(float a, float b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ int acc_row(int v, int half) { return 8 * (v >> 2) + 4 * half + (v & 3); }
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }
+
+template <typename T>
+__device__ __forceinline__ float load_feat(const T* p);
+template <>
+__device__ __forceinline__ float load_feat<float>(const float* p) { return *p; }
+template <>
+__device__ __forceinline__ float load_feat<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
+
+// Blocks of a 1-D grid are dealt to the XCDs round-robin (block b runs on XCD
+// b % 8).  Remap so that each XCD walks one contiguous range of logical work
+// items: neighbouring destination nodes share source nodes, and then share
+// that XCD's L2.  The map is a bijection on [0, total).
+__device__ __forceinline__ int xcd_remap(int b, int total) {
+  const int per = total / kNumXcd, rem = total % kNumXcd;
+  const int xcd = b % kNumXcd, j = b / kNumXcd;
+  return xcd < rem ? xcd * (per + 1) + j : rem * (per + 1) + (xcd - rem) * per + j;
+}
+
+}  // namespace tdn

@@ -1,0 +1,82 @@
+// Internal launch interface between the C ABI (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tdn {
+
+// ---------------------------------------------------------------- sorting
+// Stable LSD radix sort of int keys in [0, n_keys) with 8-bit digits.
+struct SortPlan {
+  int n_keys, E, passes, n_blocks;
+  size_t bytes;  // workspace bytes
+};
+SortPlan sort_plan(int n_keys, int E);
+// keys: [E] input; perm [E]; offsets [n_keys+1]; ws from sort_plan.
+hipError_t launch_sort(const SortPlan& plan, const int32_t* keys, int key_stride, int32_t* perm,
+                       int32_t* offsets, void* ws, hipStream_t s);
+// offsets from keys already sorted (non-decreasing); perm = identity.
+hipError_t launch_offsets_presorted(int n_keys, int E, const int32_t* sorted_keys, int32_t* perm,
+                                    int32_t* offsets, hipStream_t s);
+// Device-side validation; flags (3 ints, cleared by this call): [0] index
+// range, [1] dst order, [2] degenerate edge vector.
+hipError_t launch_validate(int N, int E, const int32_t* edge_index, const float* edge_vec, int check_sorted,
+                           int32_t* flags, hipStream_t s);
+
+// ---------------------------------------------------------------- edge kernel
+// One Khatri-Rao contraction pass over segments of a sorted edge list:
+//   H_seg = sum_{e in seg} diag(g_e) KF^T feat[gather[e]]    ([R, C])
+//   out[seg] = EF H_seg                                       ([d, C])
+// forward:        KF = A, EF = D, feat = x,  gather = src, segments = dst
+// grad_x pass:    KF = D, EF = A, feat = Gz, gather = dst, segments = src
+struct EdgeArgs {
+  int n_seg, E, L, d, C, R, n_radial;
+  float sigma;               // r_cut / (n_radial - 1)
+  const int32_t* offsets;    // [n_seg + 1]
+  const int32_t* perm;       // [E] sorted slot -> edge id
+  const int32_t* gather;     // [E] by edge id: row of feat to gather
+  const float* edge_vec;     // [E, 3] by edge id
+  const float* KF;           // [d, R]
+  const float* EF;           // [d, R]
+  const float* Bf;           // [d, R]
+  const float* radial_w;     // [n_radial, R]
+  const void* feat;          // [n_feat_rows, d, C]
+  float* out;                // [n_seg, d, C]
+};
+hipError_t launch_cp_edge(const EdgeArgs& a, bool feat_bf16, hipStream_t s);
+
+// ---------------------------------------------------------------- node GEMMs
+// out[rows, C] = in[rows, C] @ W (transpose_w = 0) or in @ W^T (transpose_w = 1)
+hipError_t launch_node_gemm(int rows, int C, const float* in, const void* W, bool w_bf16, int transpose_w,
+                            float* out, hipStream_t s);
+// grad_W[C, C] = sum_rows Z[row, :]^T G[row, :], split over n_part row chunks
+// reduced in a fixed order.  partial: [n_part, C, C] floats of workspace.
+int gram_parts(int rows);
+hipError_t launch_gram(int rows, int C, const float* Z, const float* G, float* partial, float* grad_W,
+                       hipStream_t s);
+
+// ---------------------------------------------------------------- backward
+struct BwdDstArgs {
+  int n_seg, E, L, d, C, R, n_radial;
+  float sigma;
+  const int32_t* offsets;   // dst segments
+  const int32_t* perm;
+  const int32_t* src;       // [E] by edge id
+  const float* edge_vec;
+  const float* A;
+  const float* Bf;
+  const float* D;
+  const float* radial_w;
+  const void* x;            // [N, d, C]
+  const float* Gz;          // [N, d, C] = grad_out W^T
+  float* grad_vec;          // [E, 3] by edge id
+};
+hipError_t launch_bwd_dst(const BwdDstArgs& a, bool x_bf16, hipStream_t s);
+
+// ---------------------------------------------------------------- misc
+hipError_t launch_sh(int L, int E, const float* edge_vec, float* Y, float* dY, hipStream_t s);
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
+
+}  // namespace tdn

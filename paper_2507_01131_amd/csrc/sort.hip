@@ -1,0 +1,211 @@
+// Edge ordering for the segmented reduction: a stable LSD radix sort of the
+// destination (or source) index with 8-bit digits, the segment offsets by
+// binary search over the sorted keys, and device-side input validation.
+//
+// Stability: every pass is a stable counting sort; within a block the items
+// are ranked in their original order (wave ballots give the rank among equal
+// digits inside a wave, waves are ordered by index, tiles by block), so equal
+// keys keep the original edge order and perm/offsets are exact integers.
+#include "common.hpp"
+#include "kernels.h"
+
+namespace tdn {
+
+namespace {
+
+constexpr int kSortThreads = 256;
+constexpr int kItemsPerThread = 16;
+constexpr int kSortTile = kSortThreads * kItemsPerThread;
+constexpr int kDigits = 256;
+
+size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+
+__global__ __launch_bounds__(kSortThreads) void k_digit_hist(const int32_t* __restrict__ keys, int E, int shift,
+                                                            int n_blocks, int32_t* __restrict__ hist) {
+  __shared__ int32_t h[kDigits];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int base = blockIdx.x * kSortTile;
+  for (int i = 0; i < kItemsPerThread; ++i) {
+    const int idx = base + i * kSortThreads + threadIdx.x;
+    if (idx < E) atomicAdd(&h[(keys[idx] >> shift) & (kDigits - 1)], 1);
+  }
+  __syncthreads();
+  hist[threadIdx.x * n_blocks + blockIdx.x] = h[threadIdx.x];
+}
+
+// Exclusive scan of n ints in place, one block of 1024 threads.
+__global__ __launch_bounds__(1024) void k_scan_exclusive(int32_t* __restrict__ a, int n) {
+  __shared__ int32_t part[1024];
+  const int per = (n + 1023) / 1024;
+  const int lo = min(n, int(threadIdx.x) * per), hi = min(n, lo + per);
+  int32_t s = 0;
+  for (int i = lo; i < hi; ++i) s += a[i];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int32_t t = threadIdx.x >= unsigned(off) ? part[threadIdx.x - off] : 0;
+    __syncthreads();
+    part[threadIdx.x] += t;
+    __syncthreads();
+  }
+  int32_t run = part[threadIdx.x] - s;
+  for (int i = lo; i < hi; ++i) {
+    const int32_t v = a[i];
+    a[i] = run;
+    run += v;
+  }
+}
+
+__global__ __launch_bounds__(kSortThreads) void k_digit_scatter(const int32_t* __restrict__ keys_in,
+                                                               const int32_t* __restrict__ vals_in, int E,
+                                                               int shift, int n_blocks,
+                                                               const int32_t* __restrict__ hist,
+                                                               int32_t* __restrict__ keys_out,
+                                                               int32_t* __restrict__ vals_out) {
+  constexpr int kWaves = kSortThreads / kWave;
+  __shared__ int32_t run[kDigits];
+  __shared__ int32_t wcnt[kWaves][kDigits];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  run[tid] = hist[tid * n_blocks + blockIdx.x];
+  for (int w = 0; w < kWaves; ++w) wcnt[w][tid] = 0;
+  __syncthreads();
+  const uint64_t lt_mask = lane == 0 ? 0ull : (~0ull >> (kWave - lane));
+  const int base = blockIdx.x * kSortTile;
+  for (int it = 0; it < kItemsPerThread; ++it) {
+    const int idx = base + it * kSortThreads + tid;
+    const bool valid = idx < E;
+    const int32_t key = valid ? keys_in[idx] : 0;
+    const int32_t val = valid ? (vals_in ? vals_in[idx] : idx) : 0;
+    const int digit = (key >> shift) & (kDigits - 1);
+    uint64_t peers = __ballot(valid);
+    for (int bit = 0; bit < 8; ++bit) {
+      const bool on = (digit >> bit) & 1;
+      const uint64_t b = __ballot(on);
+      peers &= on ? b : ~b;
+    }
+    const int rank = __popcll(peers & lt_mask);
+    if (valid && rank == 0) wcnt[wave][digit] = __popcll(peers);
+    __syncthreads();
+    if (valid) {
+      int pos = run[digit] + rank;
+      for (int w = 0; w < wave; ++w) pos += wcnt[w][digit];
+      keys_out[pos] = key;
+      vals_out[pos] = val;
+    }
+    __syncthreads();
+    int32_t add = 0;
+    for (int w = 0; w < kWaves; ++w) {
+      add += wcnt[w][tid];
+      wcnt[w][tid] = 0;
+    }
+    run[tid] += add;
+    __syncthreads();
+  }
+}
+
+// offsets[k] = first index i with sorted_keys[i] >= k, for k in [0, n_keys].
+__global__ void k_offsets(const int32_t* __restrict__ sorted_keys, int E, int n_keys, int32_t* __restrict__ offsets) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k > n_keys) return;
+  int lo = 0, hi = E;
+  while (lo < hi) {
+    const int mid = lo + ((hi - lo) >> 1);
+    if (sorted_keys[mid] < k)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  offsets[k] = lo;
+}
+
+__global__ void k_iota(int32_t* __restrict__ p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = i;
+}
+
+__global__ void k_fill_u32(uint32_t* __restrict__ p, size_t n) {
+  const size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
+__global__ void k_validate(int N, int E, const int32_t* __restrict__ ei, const float* __restrict__ vec,
+                           int check_sorted, int32_t* __restrict__ flags) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= E) return;
+  const int s = ei[i], t = ei[E + i];
+  if (s < 0 || s >= N || t < 0 || t >= N) atomicOr(&flags[0], 1);
+  if (check_sorted && i + 1 < E && t > ei[E + i + 1]) atomicOr(&flags[1], 1);
+  const float x = vec[3 * i], y = vec[3 * i + 1], z = vec[3 * i + 2];
+  const float n2 = x * x + y * y + z * z;
+  if (!(n2 > 0.f) || !isfinite(n2)) atomicOr(&flags[2], 1);
+}
+
+}  // namespace
+
+SortPlan sort_plan(int n_keys, int E) {
+  SortPlan p{};
+  p.n_keys = n_keys;
+  p.E = E;
+  int bits = 0;
+  while (bits < 31 && (int64_t(1) << bits) < int64_t(n_keys)) ++bits;
+  p.passes = (bits + 7) / 8;
+  p.n_blocks = (E + kSortTile - 1) / kSortTile;
+  const size_t e4 = align256(size_t(E) * 4);
+  p.bytes = 4 * e4 + align256(size_t(kDigits) * p.n_blocks * 4);
+  return p;
+}
+
+hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t s) {
+  const size_t n = bytes / 4;
+  if (n == 0) return hipSuccess;
+  k_fill_u32<<<dim3(unsigned((n + 255) / 256)), dim3(256), 0, s>>>(static_cast<uint32_t*>(ptr), n);
+  return hipGetLastError();
+}
+
+hipError_t launch_offsets_presorted(int n_keys, int E, const int32_t* sorted_keys, int32_t* perm, int32_t* offsets,
+                                    hipStream_t s) {
+  if (E > 0) k_iota<<<dim3((E + 255) / 256), dim3(256), 0, s>>>(perm, E);
+  k_offsets<<<dim3((n_keys + 1 + 255) / 256), dim3(256), 0, s>>>(sorted_keys, E, n_keys, offsets);
+  return hipGetLastError();
+}
+
+hipError_t launch_sort(const SortPlan& plan, const int32_t* keys, int /*key_stride*/, int32_t* perm, int32_t* offsets,
+                       void* ws, hipStream_t s) {
+  const int E = plan.E;
+  if (E == 0 || plan.passes == 0) {
+    // no key bits: the stable order is the original order; offsets from the keys themselves
+    return launch_offsets_presorted(plan.n_keys, E, keys, perm, offsets, s);
+  }
+  char* w = static_cast<char*>(ws);
+  const size_t e4 = align256(size_t(E) * 4);
+  int32_t* kbuf[2] = {reinterpret_cast<int32_t*>(w), reinterpret_cast<int32_t*>(w + e4)};
+  int32_t* vbuf[2] = {reinterpret_cast<int32_t*>(w + 2 * e4), reinterpret_cast<int32_t*>(w + 3 * e4)};
+  int32_t* hist = reinterpret_cast<int32_t*>(w + 4 * e4);
+  const int nb = plan.n_blocks;
+  const int32_t* kin = keys;
+  const int32_t* vin = nullptr;
+  for (int pass = 0; pass < plan.passes; ++pass) {
+    const int shift = 8 * pass;
+    int32_t* kout = kbuf[pass & 1];
+    int32_t* vout = pass + 1 == plan.passes ? perm : vbuf[pass & 1];
+    k_digit_hist<<<dim3(nb), dim3(kSortThreads), 0, s>>>(kin, E, shift, nb, hist);
+    k_scan_exclusive<<<dim3(1), dim3(1024), 0, s>>>(hist, kDigits * nb);
+    k_digit_scatter<<<dim3(nb), dim3(kSortThreads), 0, s>>>(kin, vin, E, shift, nb, hist, kout, vout);
+    kin = kout;
+    vin = vout;
+  }
+  k_offsets<<<dim3((plan.n_keys + 1 + 255) / 256), dim3(256), 0, s>>>(kin, E, plan.n_keys, offsets);
+  return hipGetLastError();
+}
+
+hipError_t launch_validate(int N, int E, const int32_t* edge_index, const float* edge_vec, int check_sorted,
+                           int32_t* flags, hipStream_t s) {
+  hipError_t e = launch_zero(flags, 4 * sizeof(int32_t), s);
+  if (e != hipSuccess) return e;
+  if (E > 0)
+    k_validate<<<dim3((E + 255) / 256), dim3(256), 0, s>>>(N, E, edge_index, edge_vec, check_sorted, flags);
+  return hipGetLastError();
+}
+
+}  // namespace tdn

@@ -1,0 +1,120 @@
+"""Host-side tests of the C ABI that need no GPU: the library loads, exports
+every entry point that include/tdn.h declares, and rejects bad arguments
+before touching any device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2507_01131_amd as tdn
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    text = open(os.path.join(ROOT, "include", "tdn.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tdn_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    syms = declared_symbols()
+    assert len(syms) >= 10
+    L = tdn.lib()
+    for s in syms:
+        assert hasattr(L, s), s
+
+
+def _problem(**kw):
+    base = dict(L=4, C=128, R=128, n_nodes=100, n_edges=1000, r_cut=6.0)
+    base.update(kw)
+    return tdn.make_problem(**base)
+
+
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every case returns before any launch
+
+
+def _fwd(p, ws_bytes=1 << 40, **override):
+    args = dict(x=FAKE, vec=FAKE, ei=FAKE, A=FAKE, B=FAKE, D=FAKE, W=FAKE, rw=FAKE, out=FAKE, z=None, perm=FAKE,
+                off=FAKE, ws=FAKE)
+    args.update(override)
+    return tdn.lib().tdn_cp_tp_forward(None if p is None else ctypes.byref(p), args["x"], args["vec"], args["ei"],
+                                       args["A"], args["B"], args["D"], args["W"], args["rw"], args["out"], args["z"],
+                                       args["perm"], args["off"], args["ws"], ws_bytes, None)
+
+
+def _bwd(p, ws_bytes=1 << 40, **override):
+    args = dict(x=FAKE, vec=FAKE, ei=FAKE, A=FAKE, B=FAKE, D=FAKE, W=FAKE, rw=FAKE, perm=FAKE, off=FAKE, z=None,
+                g=FAKE, gx=FAKE, gW=FAKE, gv=FAKE, ws=FAKE)
+    args.update(override)
+    return tdn.lib().tdn_cp_tp_backward(ctypes.byref(p), args["x"], args["vec"], args["ei"], args["A"], args["B"],
+                                        args["D"], args["W"], args["rw"], args["perm"], args["off"], args["z"],
+                                        args["g"], args["gx"], args["gW"], args["gv"], args["ws"], ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(L=7), 2), (dict(L=-1), 2), (dict(C=8), 2), (dict(C=100), 2), (dict(C=512), 2), (dict(R=0), 2),
+    (dict(R=257), 2), (dict(n_nodes=-1), 2), (dict(n_edges=-5), 2), (dict(n_nodes=0, n_edges=3), 2),
+    (dict(n_radial=1), 2), (dict(r_cut=0.0), 2), (dict(r_cut=float("nan")), 2), (dict(feat_dtype=7), 3),
+])
+def test_bad_problem_is_rejected(kw, status):
+    p = _problem(**kw)
+    assert _fwd(p) == status
+    assert _bwd(p) == status
+    f, b = ctypes.c_size_t(), ctypes.c_size_t()
+    assert tdn.lib().tdn_workspace_size(ctypes.byref(p), ctypes.byref(f), ctypes.byref(b)) == status
+
+
+def test_null_problem_and_pointers():
+    assert _fwd(None) == 1
+    p = _problem()
+    for k in ["x", "vec", "ei", "A", "B", "D", "W", "rw", "out", "perm", "off", "ws"]:
+        assert _fwd(p, **{k: None}) == 1, k
+    for k in ["x", "vec", "ei", "A", "B", "D", "W", "rw", "perm", "off", "g", "ws"]:
+        assert _bwd(p, **{k: None}) == 1, k
+
+
+def test_edge_arrays_optional_without_edges():
+    # E = 0: edge pointers may be NULL; the call then proceeds to the device
+    # check, which fails on a machine without a GPU (status 8 or 9), never 1.
+    p = _problem(n_edges=0)
+    assert _fwd(p, ws_bytes=0, vec=None, ei=None, perm=None) == 4
+    f, _ = tdn.workspace_size(p)
+    assert f > 0
+
+
+def test_workspace_too_small():
+    p = _problem()
+    f, b = tdn.workspace_size(p)
+    assert _fwd(p, ws_bytes=f - 1) == 4
+    assert _bwd(p, ws_bytes=b - 1) == 4
+    # the saved-activation buffer dominates: N*d*C floats
+    assert f >= 100 * 25 * 128 * 4
+    assert b >= 2 * 100 * 25 * 128 * 4
+
+
+def test_sort_and_sh_argument_checks():
+    L = tdn.lib()
+    nb = ctypes.c_size_t()
+    assert L.tdn_sort_workspace_size(-1, 5, ctypes.byref(nb)) == 2
+    assert L.tdn_sort_workspace_size(0, 5, ctypes.byref(nb)) == 2
+    assert L.tdn_sort_workspace_size(10, 5, None) == 1
+    assert L.tdn_sort_workspace_size(10, 5, ctypes.byref(nb)) == 0 and nb.value > 0
+    assert L.tdn_sort_by_key(10, 5, FAKE, FAKE, FAKE, FAKE, 1, None) == 4
+    assert L.tdn_sort_by_key(10, 5, None, FAKE, FAKE, FAKE, 1 << 30, None) == 1
+    assert L.tdn_spherical_harmonics(7, 5, FAKE, FAKE, None, None) == 2
+    assert L.tdn_spherical_harmonics(3, 5, None, FAKE, None, None) == 1
+
+
+def test_status_strings():
+    for s in range(10):
+        assert tdn.status_string(s)
+    assert tdn.status_string(0) == "ok"
+
+
+def test_timer_bookkeeping_without_launches():
+    tdn.timer_enable(True)
+    ms, n = tdn.timer_read("cp_edge_fwd")
+    assert ms == 0.0 and n == 0
+    tdn.timer_enable(False)
