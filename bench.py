@@ -100,6 +100,8 @@ def main():
     ap.add_argument("--workload", default="molecules3200_L4_C128_R128")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--backward", action="store_true", help="also time tdn_cp_tp_backward (extra field)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run a plain 256 MiB device copy (reference for rocprofv3 byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the multi-GPU layout is a design "
@@ -140,6 +142,13 @@ def main():
         return tdn.forward(x, vec, ei, At, Bt, Dt, W, rw, L=w["L"], r_cut=w["r_cut"], edges_sorted=w["presorted"],
                            workspace=ws, out=out, z=zsave, perm=perm, offsets=offsets)
 
+    if args.calibrate_copy:
+        a = torch.empty(64 << 20, dtype=torch.float32, device=dev).fill_(1.0)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
     for _ in range(args.warmup):
         res = step()
     torch.cuda.synchronize()
