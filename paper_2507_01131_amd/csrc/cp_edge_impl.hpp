@@ -80,9 +80,17 @@ __device__ inline void stage_factor(float* dst, const float* __restrict__ src, i
   }
 }
 
+// Two waves per SIMD when the register-resident K factor fits beside the
+// accumulators; one otherwise (large R at high L), where spilling would cost
+// more than the lost occupancy.
+template <int L, int RT>
+constexpr int edge_waves_per_eu() {
+  return ((L + 1) * (L + 1) + 1) / 2 * RT <= 64 ? 2 : 1;
+}
+
 template <int L, int RT, typename TF>
-__global__ __launch_bounds__(kMaxWavesPerBlock* kWave) void k_cp_edge(EdgeArgs a, int n_cgrp, int waves,
-                                                                       int chunk) {
+__global__ __launch_bounds__(kMaxWavesPerBlock* kWave) __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu<L, RT>())))
+void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
   constexpr int d = (L + 1) * (L + 1);
   constexpr int DH = (d + 1) / 2;  // K-steps per edge
   constexpr int Rp = RT * kTile;
@@ -113,13 +121,32 @@ __global__ __launch_bounds__(kMaxWavesPerBlock* kWave) void k_cp_edge(EdgeArgs a
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x16{};
 
-  // B operand of K-step j of one edge: x[row][2j + h][c] (zero for the pad row)
+  // When it fits (DH*RT <= 64 values per lane) the K factor of this lane,
+  // KF[2j + h][rt*32 + l32], lives in registers for the whole segment, so
+  // the MFMA loop touches LDS only for g_e.
+  constexpr bool kRegK = DH * RT <= 64;
+  float kreg[kRegK ? DH : 1][kRegK ? RT : 1];
+  const float* kr = sK + h * S.kstride + l32;
+  if constexpr (kRegK) {
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < DH; ++j)
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) kreg[j][rt] = kr[2 * j * S.kstride + rt * kTile];
+  }
+
+  // B operand of K-step j of one edge: x[row][2j + h][c].  The loads are
+  // unconditional with clamped addresses and no select on the value, so
+  // nothing forces a wait before the operand is used one edge later: the pad
+  // row (2j + h == d) meets an all-zero K row in LDS, and a lane with c >= C
+  // only feeds result column c, which is never stored.
+  const int c_ld = cvalid ? c : C - 1;
   auto load_edge = [&](int row, float (&b)[DH]) {
-    const TF* p = feat + size_t(row) * d * C + size_t(h) * C + c;
+    const TF* p = feat + size_t(row) * d * C + c_ld;
 #pragma unroll
     for (int j = 0; j < DH; ++j) {
-      const bool ok = cvalid && (2 * j + h < d);
-      b[j] = ok ? load_feat<TF>(p + size_t(2 * j) * C) : 0.f;
+      const int k = 2 * j + h < d ? 2 * j + h : d - 1;
+      b[j] = load_feat<TF>(p + size_t(k) * C);
     }
   };
 
@@ -127,49 +154,93 @@ __global__ __launch_bounds__(kMaxWavesPerBlock* kWave) void k_cp_edge(EdgeArgs a
   for (int cb = e_begin; cb < e_end; cb += chunk) {
     const int n = min(chunk, e_end - cb);
     __syncthreads();  // factors staged / previous chunk consumed
-    if (tid < n) {
-      const int eid = a.perm[cb + tid];
+    // harmonics: one thread per (edge, order m) column; radial basis: one
+    // thread per (edge, function); gathered row: one thread per edge
+    for (int t = tid; t < n * (L + 1); t += blockDim.x) {
+      const int e = t / (L + 1), m = t - e * (L + 1);
+      const int eid = a.perm[cb + e];
       const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
-      const float rn = sqrtf(vx * vx + vy * vy + vz * vz);
-      const float inv = 1.f / rn;
-      sh_unit(L, vx * inv, vy * inv, vz * inv, sY + tid * d);
-      for (int q = 0; q < nr; ++q) sPhi[tid * nr + q] = radial_phi(rn, q, a.sigma);
-      sIdx[tid] = a.gather[eid];
+      const float inv = 1.f / sqrtf(vx * vx + vy * vy + vz * vz);
+      sh_unit_column(L, m, vx * inv, vy * inv, vz * inv, sY + e * d);
     }
+    for (int t = tid; t < n * nr; t += blockDim.x) {
+      const int e = t / nr, q = t - e * nr;
+      const int eid = a.perm[cb + e];
+      const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
+      sPhi[t] = radial_phi(sqrtf(vx * vx + vy * vy + vz * vz), q, a.sigma);
+    }
+    for (int t = tid; t < n; t += blockDim.x) sIdx[t] = a.gather[a.perm[cb + t]];
     __syncthreads();
-    // g_e[r] = (sum_k B[k,r] Y_e[k]) * (sum_q Wrad[q,r] phi_e[q])
-    for (int i = tid; i < n * Rp; i += blockDim.x) {
-      const int e = i / Rp, r = i - e * Rp;
-      float v = 0.f, rho = 0.f;
+    // g = (Y B) * (Phi Wrad) for the chunk's edges (rows) and all ranks
+    // (columns): two small MFMA GEMMs per 32x32 tile, one rank tile per wave.
+    const int n_et = (n + kTile - 1) / kTile;
+    for (int item = wave; item < n_et * RT; item += waves) {
+      const int et = item / RT, rt = item - et * RT;
+      const int er = et * kTile + l32;  // this lane's edge row
+      const bool row_ok = er < n;
+      f32x16 T = f32x16{};
+#pragma unroll 1
+      for (int s2 = 0; s2 < (nr + 1) / 2; ++s2) {
+        const int q = 2 * s2 + h;
+        const float av = (row_ok && q < nr) ? sPhi[er * nr + q] : 0.f;
+        const float bv = q < nr ? sBE[(d + q) * Rp + rt * kTile + l32] : 0.f;
+        T = mfma32(av, bv, T);
+      }
 #pragma unroll
-      for (int k = 0; k < d; ++k) v += sBE[k * Rp + r] * sY[e * d + k];
-      for (int q = 0; q < nr; ++q) rho += sBE[(d + q) * Rp + r] * sPhi[e * nr + q];
-      sG[e * Rp + r] = v * rho;
+      for (int v = 0; v < 16; ++v) {
+        const int e = et * kTile + acc_row(v, h);
+        if (e < n) sG[e * Rp + rt * kTile + l32] = T[v];
+      }
+      T = f32x16{};
+#pragma unroll 1
+      for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
+        const int k = 2 * s2 + h;
+        const float av = (row_ok && k < d) ? sY[er * d + k] : 0.f;
+        const float bv = k < d ? sBE[k * Rp + rt * kTile + l32] : 0.f;
+        T = mfma32(av, bv, T);
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int e = et * kTile + acc_row(v, h);
+        if (e < n) sG[e * Rp + rt * kTile + l32] *= T[v];
+      }
     }
     __syncthreads();
 
-    float bcur[DH], bnext[DH];
-    load_edge(sIdx[0], bcur);
-    for (int e = 0; e < n; ++e) {
-      if (e + 1 < n) {
-        load_edge(sIdx[e + 1], bnext);
-      } else {
-#pragma unroll
-        for (int j = 0; j < DH; ++j) bnext[j] = 0.f;
-      }
+    // Two operand buffers used alternately: the loads for edge e+1 are issued
+    // before the MFMAs of edge e, and the scheduling barriers keep the
+    // compiler from sinking them next to their use.
+    auto edge_mfma = [&](int e, const float (&b)[DH]) {
       float g[RT];
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) g[rt] = sG[e * Rp + rt * kTile + l32];
-      const float* kr = sK + h * S.kstride + l32;
 #pragma unroll
       for (int j = 0; j < DH; ++j) {
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-          acc[rt] = mfma32(g[rt] * kr[2 * j * S.kstride + rt * kTile], bcur[j], acc[rt]);
+        for (int rt = 0; rt < RT; ++rt) {
+          float kv;
+          if constexpr (kRegK)
+            kv = kreg[j][rt];
+          else
+            kv = kr[2 * j * S.kstride + rt * kTile];
+          acc[rt] = mfma32(g[rt] * kv, b[j], acc[rt]);
+        }
       }
-#pragma unroll
-      for (int j = 0; j < DH; ++j) bcur[j] = bnext[j];
+    };
+    float b0[DH], b1[DH];
+    load_edge(sIdx[0], b0);
+    int e = 0;
+    for (; e + 1 < n; e += 2) {
+      load_edge(sIdx[e + 1], b1);
+      __builtin_amdgcn_sched_barrier(0);
+      edge_mfma(e, b0);
+      __builtin_amdgcn_sched_barrier(0);
+      load_edge(sIdx[e + 2 < n ? e + 2 : e + 1], b0);  // the last pair reloads; unused
+      __builtin_amdgcn_sched_barrier(0);
+      edge_mfma(e + 1, b1);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    if (e < n) edge_mfma(e, b0);
   }
 
   // Epilogue: out[seg][m][c] = sum_r EF[m][r] H[r][c].  The contraction over r
@@ -210,9 +281,10 @@ hipError_t launch_l_rt(const EdgeArgs& a, bool bf16, hipStream_t s) {
   const int ntiles = (a.C + kTile - 1) / kTile;
   const int waves = ntiles < kMaxWavesPerBlock ? ntiles : kMaxWavesPerBlock;
   const int n_cgrp = (ntiles + waves - 1) / waves;
-  // largest edge chunk (<= 32) that keeps LDS within 52 KB (three blocks per CU), at least 4
-  int chunk = 32;
-  while (chunk > 4 && edge_smem(RT, d, a.n_radial, chunk).floats * 4 > 52 * 1024) chunk >>= 1;
+  // largest edge chunk (<= 64) that keeps LDS within 80 KB (two blocks per
+  // CU), at least 8: typical in-degrees then need a single chunk per segment
+  int chunk = 64;
+  while (chunk > 8 && edge_smem(RT, d, a.n_radial, chunk).floats * 4 > 80 * 1024) chunk >>= 1;
   const size_t lds = size_t(edge_smem(RT, d, a.n_radial, chunk).floats) * 4;
   const int total = a.n_seg * n_cgrp;
   if (total == 0) return hipSuccess;
