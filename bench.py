@@ -48,7 +48,7 @@ def forward_flops(N, E, d, C, R):
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in ("cp_edge.hip", "sh_device.hpp", "common.hpp"):
+    for f in ("cp_edge_impl.hpp", "cp_edge.hip", "sh_device.hpp", "common.hpp"):
         h.update(open(os.path.join(ROOT, "paper_2507_01131_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
@@ -199,11 +199,17 @@ def main():
         for _ in range(3):
             tdn.backward(res, G, workspace=wsb)
         torch.cuda.synchronize()
+        bk = ("node_gemm", "gram", "cp_bwd_dst", "sort", "cp_edge_bwd_src")
+        tdn.timer_enable(True)
+        for k in bk:
+            tdn.timer_read(k, reset=True)
         ev0.record()
         for _ in range(10):
             tdn.backward(res, G, workspace=wsb)
         ev1.record()
         torch.cuda.synchronize()
+        tdn.timer_enable(False)
+        line["backward_kernel_ms_per_step"] = {k: tdn.timer_read(k, reset=True)[0] / 10 for k in bk}
         line["backward_ms"] = ev0.elapsed_time(ev1) / 10
         line["backward_edges_per_s"] = E / (line["backward_ms"] * 1e-3)
     if not args.no_cpu_baseline:
