@@ -14,9 +14,6 @@
 #include "kernels.h"
 #include "tdn.h"
 
-namespace tdn {
-size_t bwd_dst_lds_bytes(int R, int d, int n_radial, int C);
-}
 
 namespace {
 
