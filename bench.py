@@ -13,7 +13,8 @@ Prints one JSON line.  The metric is edge tensor products per second.
 The roofline object reports the dominant kernel (the edge pass): its
 algorithmic flops per launch, E (2RdC + 2Rd + 17R + RC) + N 2dRC, over its
 average launch time from HIP events recorded on its launch stream, against
-the fp32 MFMA peak of 157.3 TFLOP/s.  The CPU baseline times the oracle (the
+the MFMA peak of the dtype it runs in (fp32 157.3 TFLOP/s; bf16 2.5 PFLOP/s
+for bfloat16 features).  The CPU baseline times the oracle (the
 plain float64 per-edge implementation) on a bounded sample of the same
 workload on this host's cores.
 """
@@ -153,7 +154,8 @@ def main():
         res = step()
     torch.cuda.synchronize()
     tdn.timer_enable(True)
-    for k in ("cp_edge_fwd", "node_gemm", "sort"):
+    fwd_kernels = ("cp_edge_fwd", "transpose_bf16", "node_gemm", "sort")
+    for k in fwd_kernels:
         tdn.timer_read(k, reset=True)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -165,13 +167,14 @@ def main():
     tdn.timer_enable(False)
     total_ms = ev0.elapsed_time(ev1)
     ms_step = total_ms / args.steps
-    kern = {k: tdn.timer_read(k, reset=True) for k in ("cp_edge_fwd", "node_gemm", "sort")}
+    kern = {k: tdn.timer_read(k, reset=True) for k in fwd_kernels}
     edge_ms = kern["cp_edge_fwd"][0] / max(1, kern["cp_edge_fwd"][1])
 
     bf16 = w["feat_dtype"] == "bf16"
     f_edge = edge_kernel_flops(N, E, d, C, R)
     achieved = f_edge / (edge_ms * 1e-3) / 1e12
-    peak = PEAK_FP32_MFMA_TFLOPS  # the edge pass runs fp32 MFMA for both feature dtypes
+    # bf16 features run the edge pass on bf16 MFMA (fp32 accumulation)
+    peak = PEAK_BF16_MFMA_TFLOPS if bf16 else PEAK_FP32_MFMA_TFLOPS
     line = {
         "metric": METRIC,
         "value": E / (ms_step * 1e-3),
@@ -183,7 +186,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16-in/f32" if bf16 else "f32",
+        "dtype": "bf16" if bf16 else "f32",
         "data": "synthetic",
         "config": {"workload": w["name"], "N": N, "E": E, "L": w["L"], "d": d, "C": C, "R": R,
                    "edges_presorted": bool(w["presorted"]), "pass": "forward"},

@@ -50,8 +50,12 @@ tdn_status check_problem(const tdn_problem* p) {
   return TDN_OK;
 }
 
+size_t xt_bytes(const tdn_problem& p) {
+  return p.feat_dtype == TDN_BF16 ? size_t(p.n_nodes) * p.C * tdn::bf16_kpad(dim_of(p.L)) * 2 : 0;
+}
+
 struct FwdLayout {
-  size_t z, sort, flags, total;
+  size_t z, xt, sort, flags, total;
 };
 FwdLayout fwd_layout(const tdn_problem& p) {
   FwdLayout f{};
@@ -59,6 +63,8 @@ FwdLayout fwd_layout(const tdn_problem& p) {
   size_t o = 0;
   f.z = o;
   o += al(ndc);
+  f.xt = o;
+  o += al(xt_bytes(p));
   f.sort = o;
   o += al(p.edges_sorted ? 0 : tdn::sort_plan(p.n_nodes, p.n_edges).bytes);
   f.flags = o;
@@ -68,7 +74,7 @@ FwdLayout fwd_layout(const tdn_problem& p) {
 }
 
 struct BwdLayout {
-  size_t gz, z, parts, perm_src, off_src, sort, flags, total;
+  size_t gz, z, xt, parts, perm_src, off_src, sort, flags, total;
 };
 BwdLayout bwd_layout(const tdn_problem& p) {
   BwdLayout b{};
@@ -78,6 +84,8 @@ BwdLayout bwd_layout(const tdn_problem& p) {
   o += al(ndc);
   b.z = o;
   o += al(ndc);
+  b.xt = o;
+  o += al(xt_bytes(p));
   b.parts = o;
   o += al(size_t(tdn::gram_parts(p.n_nodes * dim_of(p.L))) * p.C * p.C * 4);
   b.perm_src = o;
@@ -180,6 +188,24 @@ tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int3
   return a;
 }
 
+// The forward edge pass Z = per-node D diag(g) A^T x sums, for either
+// feature dtype (bf16 goes through the transposed copy in the workspace).
+hipError_t forward_edge_pass(const tdn_problem& p, const int32_t* offsets, const int32_t* perm, const int32_t* src,
+                             const float* edge_vec, const float* A, const float* B, const float* D,
+                             const float* radial_w, const void* x, void* xt, float* Z, hipStream_t s) {
+  if (p.feat_dtype == TDN_BF16) {
+    {
+      Timed t("transpose_bf16", s);
+      hipError_t e = tdn::launch_transpose_bf16(p.n_nodes, dim_of(p.L), p.C, x, xt, s);
+      if (e != hipSuccess) return e;
+    }
+    Timed t("cp_edge_fwd", s);
+    return tdn::launch_cp_edge_bf16(edge_args(p, offsets, perm, src, edge_vec, A, D, B, radial_w, xt, Z), s);
+  }
+  Timed t("cp_edge_fwd", s);
+  return tdn::launch_cp_edge(edge_args(p, offsets, perm, src, edge_vec, A, D, B, radial_w, x, Z), false, s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -241,10 +267,7 @@ tdn_status tdn_cp_tp_forward(const tdn_problem* p, const void* x, const float* e
   if (N == 0) return TDN_OK;
   float* Z = z_save ? z_save : reinterpret_cast<float*>(ws + lay.z);
   const bool bf16 = p->feat_dtype == TDN_BF16;
-  {
-    Timed t("cp_edge_fwd", stream);
-    TDN_HIP(tdn::launch_cp_edge(edge_args(*p, offsets, perm, src, edge_vec, A, D, B, radial_w, x, Z), bf16, stream));
-  }
+  TDN_HIP(forward_edge_pass(*p, offsets, perm, src, edge_vec, A, B, D, radial_w, x, ws + lay.xt, Z, stream));
   {
     Timed t("node_gemm", stream);
     TDN_HIP(tdn::launch_node_gemm(N * d, C, Z, W, bf16, 0, out, stream));
@@ -288,8 +311,7 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
     const float* Z = z_save;
     if (!Z) {
       float* Zw = reinterpret_cast<float*>(ws + lay.z);
-      Timed t("cp_edge_fwd", stream);
-      TDN_HIP(tdn::launch_cp_edge(edge_args(*p, offsets, perm, src, edge_vec, A, D, B, radial_w, x, Zw), bf16, stream));
+      TDN_HIP(forward_edge_pass(*p, offsets, perm, src, edge_vec, A, B, D, radial_w, x, ws + lay.xt, Zw, stream));
       Z = Zw;
     }
     Timed t("gram", stream);

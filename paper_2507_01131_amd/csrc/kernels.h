@@ -46,6 +46,12 @@ struct EdgeArgs {
   float* out;                // [n_seg, d, C]
 };
 hipError_t launch_cp_edge(const EdgeArgs& a, bool feat_bf16, hipStream_t s);
+// bfloat16 features: x [N, d, C] is first transposed to xT [N, C, kpad(d)]
+// (kpad = 32 for d <= 32, else 64; zero padded), which the bf16 edge pass
+// gathers (EdgeArgs::feat = xT).
+int bf16_kpad(int d);
+hipError_t launch_transpose_bf16(int N, int d, int C, const void* x, void* xT, hipStream_t s);
+hipError_t launch_cp_edge_bf16(const EdgeArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- node GEMMs
 // out[rows, C] = in[rows, C] @ W (transpose_w = 0) or in @ W^T (transpose_w = 1)
