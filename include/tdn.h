@@ -64,13 +64,16 @@ typedef enum { TDN_F32 = 0, TDN_BF16 = 1 } tdn_dtype;
 
 typedef struct {
   int32_t L;            /* maximum degree, 0..6; d = (L+1)^2 components          */
-  int32_t C;            /* channels (shared multiplicity), multiple of 16, <= 1024 */
+  int32_t C;            /* channels (shared multiplicity), multiple of 16, <= 256  */
   int32_t R;            /* CP rank, 1..256                                          */
   int32_t n_nodes;      /* N >= 0                                                   */
   int32_t n_edges;      /* E >= 0 (E > 0 needs N > 0)                              */
   int32_t n_radial;     /* Gaussian radial functions, 2..16                        */
   float r_cut;          /* cutoff setting the Gaussian centres and width, > 0      */
-  tdn_dtype feat_dtype; /* dtype of x and W (TDN_F32 or TDN_BF16); all else f32     */
+  tdn_dtype feat_dtype; /* dtype of x and W (TDN_F32 or TDN_BF16); all else f32.
+                           With TDN_BF16 the edge contractions run on bf16 MFMA:
+                           the K operand g*A (and, in the backward, G W^T) is
+                           rounded to bf16, accumulation stays fp32            */
   int32_t edges_sorted; /* 1: edge_index already stably sorted by dst (perm is the
                            identity); 0: the call sorts                            */
   int32_t validate;     /* 1: check indices, order and edge vectors on the device */

@@ -196,7 +196,7 @@ hipError_t forward_edge_pass(const tdn_problem& p, const int32_t* offsets, const
   if (p.feat_dtype == TDN_BF16) {
     {
       Timed t("transpose_bf16", s);
-      hipError_t e = tdn::launch_transpose_bf16(p.n_nodes, dim_of(p.L), p.C, x, xt, s);
+      hipError_t e = tdn::launch_transpose_bf16(p.n_nodes, dim_of(p.L), p.C, x, false, xt, s);
       if (e != hipSuccess) return e;
     }
     Timed t("cp_edge_fwd", s);
@@ -348,9 +348,20 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
       Timed t("sort", stream);
       TDN_HIP(tdn::launch_sort(tdn::sort_plan(N, E), src, 1, perm_src, off_src, ws + lay.sort, stream));
     }
-    Timed t("cp_edge_bwd_src", stream);
-    TDN_HIP(tdn::launch_cp_edge(edge_args(*p, off_src, perm_src, dst, edge_vec, D, A, B, radial_w, Gz, grad_x), false,
-                                stream));
+    if (bf16) {
+      // bf16 problems run the grad_x pass on bf16 MFMA too: Gz rounded to bf16
+      {
+        Timed t("transpose_bf16", stream);
+        TDN_HIP(tdn::launch_transpose_bf16(N, d, C, Gz, true, ws + lay.xt, stream));
+      }
+      Timed t("cp_edge_bwd_src", stream);
+      TDN_HIP(tdn::launch_cp_edge_bf16(
+          edge_args(*p, off_src, perm_src, dst, edge_vec, D, A, B, radial_w, ws + lay.xt, grad_x), stream));
+    } else {
+      Timed t("cp_edge_bwd_src", stream);
+      TDN_HIP(tdn::launch_cp_edge(edge_args(*p, off_src, perm_src, dst, edge_vec, D, A, B, radial_w, Gz, grad_x),
+                                  false, stream));
+    }
   }
   return TDN_OK;
 }

@@ -32,14 +32,20 @@ constexpr int ctw() {
   return RT <= 4 ? 2 : 1;
 }
 
-// xT[n][c][k] = x[n][k][c] for k < d, 0 for d <= k < DP.  One block per node.
-template <int DP>
-__global__ __launch_bounds__(256) void k_transpose_bf16(int d, int C, const uint16_t* __restrict__ x,
+__device__ __forceinline__ uint16_t to_bf16_bits(uint16_t v) { return v; }
+__device__ __forceinline__ uint16_t to_bf16_bits(float v) {
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));  // round to nearest even
+}
+
+// xT[n][c][k] = x[n][k][c] for k < d, 0 for d <= k < DP, as bf16 (float
+// input is rounded to nearest even).  One block per node.
+template <int DP, typename TI>
+__global__ __launch_bounds__(256) void k_transpose_bf16(int d, int C, const TI* __restrict__ x,
                                                         uint16_t* __restrict__ xT) {
   extern __shared__ uint16_t tile[];  // [d][C]
   const int n = blockIdx.x;
-  const uint16_t* src = x + size_t(n) * d * C;
-  for (int i = threadIdx.x; i < d * C; i += blockDim.x) tile[i] = src[i];
+  const TI* src = x + size_t(n) * d * C;
+  for (int i = threadIdx.x; i < d * C; i += blockDim.x) tile[i] = to_bf16_bits(src[i]);
   __syncthreads();
   uint16_t* dst = xT + size_t(n) * C * DP;
   for (int i = threadIdx.x; i < C * (DP / 8); i += blockDim.x) {

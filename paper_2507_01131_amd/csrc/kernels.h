@@ -46,11 +46,11 @@ struct EdgeArgs {
   float* out;                // [n_seg, d, C]
 };
 hipError_t launch_cp_edge(const EdgeArgs& a, bool feat_bf16, hipStream_t s);
-// bfloat16 features: x [N, d, C] is first transposed to xT [N, C, kpad(d)]
-// (kpad = 32 for d <= 32, else 64; zero padded), which the bf16 edge pass
-// gathers (EdgeArgs::feat = xT).
+// bfloat16 features: x [N, d, C] (bf16, or float rounded to bf16) is first
+// transposed to xT [N, C, kpad(d)] (kpad = 32 for d <= 32, else 64; zero
+// padded), which the bf16 edge pass gathers (EdgeArgs::feat = xT).
 int bf16_kpad(int d);
-hipError_t launch_transpose_bf16(int N, int d, int C, const void* x, void* xT, hipStream_t s);
+hipError_t launch_transpose_bf16(int N, int d, int C, const void* x, bool x_is_f32, void* xT, hipStream_t s);
 hipError_t launch_cp_edge_bf16(const EdgeArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- node GEMMs
