@@ -101,6 +101,9 @@ BwdLayout bwd_layout(const tdn_problem& p) {
 }
 
 tdn_status check_device() {
+  // an error left pending by earlier, unrelated HIP work must not be
+  // reported as this call's launch failure
+  (void)hipGetLastError();
   int dev = 0;
   TDN_HIP(hipGetDevice(&dev));
   static std::mutex mu;

@@ -1,4 +1,6 @@
-// Backward of the CP tensor-product layer with respect to the edge vectors.
+// Backward of the CP tensor-product layer with respect to the edge vectors,
+// direct form (used for d > 32; d <= 32 takes the factored form in
+// cp_bwd_sg_impl.hpp).
 //
 // With Gz = grad_out W^T and Gh_t = D^T Gz[t] (per destination node, [R, C]),
 // the cotangent of g_e (eq. approximate, Sec. 3.1) is
@@ -284,249 +286,6 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
   }
 }
 
-// Variant for d <= 32 through the factored form of dg.  Since
-// Gh_t = D^T Gz[t],
-//   dg_e[r] = sum_{k,j} S_e[k, j] A[k, r] D[j, r],   S_e = x[s_e] Gz[t]^T
-// (d x d, contraction over C), so an edge costs d*d*C + d*d*R MACs instead
-// of R*d*C.  S_e is one 32x32 MFMA tile (K = C, operands x[s_e] and Gz[t],
-// both float4-loadable under the permuted channel contraction; Gz[t] stays in
-// registers for the whole segment).  In accumulator layout lane l holds
-// S_e[acc_row(v, l/32)][l%32], which is exactly the A operand of
-// T_e = S_e^T A (K = k), so S never leaves the registers; then
-// dg_e[r] = sum_j D[j, r] T_e[j, r] is a 16-term dot product plus one
-// cross-half add.  Each wave takes whole edges (e = wave, wave + waves, ...),
-// so the MFMA loop has no barriers.
-struct SgSmem {
-  int Rp, off_b, off_a, off_d, off_v, off_rho, off_dg, off_y, off_phi, off_dy, off_dphi, off_j, off_idx, floats;
-};
-
-__host__ __device__ inline SgSmem sg_smem(int RT, int d, int n_radial) {
-  SgSmem s{};
-  s.Rp = RT * kTile;
-  int o = 0;
-  s.off_b = o;  // B [d][Rp] then Wrad [n_radial][Rp]
-  o += (d + n_radial) * s.Rp;
-  s.off_a = o;  // A [32][Rp], rows >= d zero
-  o += kTile * s.Rp;
-  s.off_d = o;  // D [32][Rp], rows >= d zero
-  o += kTile * s.Rp;
-  s.off_v = o;
-  o += kChunk * s.Rp;
-  s.off_rho = o;
-  o += kChunk * s.Rp;
-  s.off_dg = o;
-  o += kChunk * s.Rp;
-  s.off_y = o;
-  o += kChunk * d;
-  s.off_phi = o;
-  o += kChunk * n_radial;
-  s.off_dy = o;
-  o += kChunk * d;
-  s.off_dphi = o;
-  o += kChunk * n_radial;
-  s.off_j = o;
-  o += kChunk * 3 * d;
-  s.off_idx = o;
-  o += 2 * kChunk;
-  s.floats = o;
-  return s;
-}
-
-constexpr int kSgWaves = 4;
-
-template <int RT, int NCT, typename TX>
-__global__ __launch_bounds__(kSgWaves* kWave) void k_bwd_dst_sg(BwdDstArgs a) {
-  extern __shared__ float smem[];
-  const SgSmem S = sg_smem(RT, a.d, a.n_radial);
-  constexpr int Rp = RT * kTile;
-  float* sB = smem + S.off_b;
-  float* sWr = sB + a.d * Rp;
-  float* sA = smem + S.off_a;
-  float* sD = smem + S.off_d;
-  float* sV = smem + S.off_v;
-  float* sRho = smem + S.off_rho;
-  float* sDG = smem + S.off_dg;
-  float* sY = smem + S.off_y;
-  float* sPhi = smem + S.off_phi;
-  float* sDY = smem + S.off_dy;
-  float* sDPhi = smem + S.off_dphi;
-  float* sJ = smem + S.off_j;
-  int* sIdx = reinterpret_cast<int*>(smem + S.off_idx);
-  int* sEid = sIdx + kChunk;
-
-  const int seg = xcd_remap(blockIdx.x, a.n_seg);
-  const int e_begin = a.offsets[seg], e_end = a.offsets[seg + 1];
-  if (e_begin == e_end) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int h = lane >> 5, l32 = lane & 31;
-  const int d = a.d, C = a.C, nr = a.n_radial, R = a.R;
-  const TX* __restrict__ x = static_cast<const TX*>(a.x);
-
-  for (int i = tid; i < (d + nr) * Rp; i += blockDim.x) {
-    const int k = i / Rp, rr = i - k * Rp;
-    sB[i] = rr < R ? (k < d ? a.Bf[k * R + rr] : a.radial_w[(k - d) * R + rr]) : 0.f;
-  }
-  for (int i = tid; i < kTile * Rp; i += blockDim.x) {
-    const int k = i / Rp, rr = i - k * Rp;
-    const bool ok = rr < R && k < d;
-    sA[i] = ok ? a.A[k * R + rr] : 0.f;
-    sD[i] = ok ? a.D[k * R + rr] : 0.f;
-  }
-  // Gz[seg] as the B operand of S: gz[ct][v] = Gz[seg][l32][ct*32 + acc_row(v, h)]
-  float gz[NCT][16];
-  {
-    const int jr = l32 < d ? l32 : d - 1;
-    const bool jok = l32 < d;
-    const float* p = a.Gz + (size_t(seg) * d + jr) * C;
-#pragma unroll
-    for (int ct = 0; ct < NCT; ++ct)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int c0 = ct * kTile + 8 * q + 4 * h;
-        const bool cok = c0 < C;
-        const f32x4 v = *reinterpret_cast<const f32x4*>(p + (cok ? c0 : C - 4));
-#pragma unroll
-        for (int i = 0; i < 4; ++i) gz[ct][4 * q + i] = (jok && cok) ? v[i] : 0.f;
-      }
-  }
-  // x[row] as the A operand of S for channel tile ct (rows past d clamped:
-  // they meet zero rows of Gz in S and of A, D afterwards)
-  auto load_step = [&](int row, int ct, float (&xb)[16]) {
-    const int kr = l32 < d ? l32 : d - 1;
-    const TX* p = x + (size_t(row) * d + kr) * C;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int c0 = ct * kTile + 8 * q + 4 * h;
-      load4<TX>(p + (c0 < C ? c0 : C - 4), &xb[4 * q]);
-    }
-  };
-
-  for (int cb = e_begin; cb < e_end; cb += kChunk) {
-    const int n = min(kChunk, e_end - cb);
-    __syncthreads();
-    // harmonics and Jacobian per (edge, order m) column; radial basis per
-    // (edge, function); indices per edge
-    for (int t = tid; t < n * (a.L + 1); t += blockDim.x) {
-      const int e = t / (a.L + 1), m = t - e * (a.L + 1);
-      const int eid = a.perm[cb + e];
-      const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
-      const float inv = 1.f / sqrtf(vx * vx + vy * vy + vz * vz);
-      sh_unit_jacobian_column(a.L, m, vx * inv, vy * inv, vz * inv, inv, sY + e * d, sJ + e * 3 * d);
-    }
-    for (int t = tid; t < n * nr; t += blockDim.x) {
-      const int e = t / nr, q = t - e * nr;
-      const int eid = a.perm[cb + e];
-      const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
-      sPhi[t] = radial_phi(sqrtf(vx * vx + vy * vy + vz * vz), q, a.sigma);
-    }
-    for (int t = tid; t < n; t += blockDim.x) {
-      const int eid = a.perm[cb + t];
-      sEid[t] = eid;
-      sIdx[t] = a.src[eid];
-    }
-    __syncthreads();
-    for (int i = tid; i < n * Rp; i += blockDim.x) {
-      const int e = i / Rp, rr = i - e * Rp;
-      float v = 0.f, rho = 0.f;
-      for (int k = 0; k < d; ++k) v += sB[k * Rp + rr] * sY[e * d + k];
-      for (int q = 0; q < nr; ++q) rho += sWr[q * Rp + rr] * sPhi[e * nr + q];
-      sV[i] = v;
-      sRho[i] = rho;
-    }
-
-    float xb0[16], xb1[16];
-    if (wave < n) load_step(sIdx[wave], 0, xb0);
-    for (int e = wave; e < n; e += kSgWaves) {
-      const int en = e + kSgWaves < n ? e + kSgWaves : e;  // last edge reloads itself; unused
-      f32x16 Sacc = f32x16{};
-#pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) {
-        if (ct + 1 < NCT) {
-          if ((ct + 1) & 1)
-            load_step(sIdx[e], ct + 1, xb1);
-          else
-            load_step(sIdx[e], ct + 1, xb0);
-        } else {
-          load_step(sIdx[en], 0, xb0);  // NCT is even: step 0 of the next edge uses buffer 0
-        }
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) Sacc = mfma32(ct & 1 ? xb1[v] : xb0[v], gz[ct][v], Sacc);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        f32x16 T = f32x16{};
-#pragma unroll
-        for (int v = 0; v < 16; ++v) T = mfma32(Sacc[v], sA[acc_row(v, h) * Rp + rt * kTile + l32], T);
-        float part = 0.f;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) part += sD[acc_row(v, h) * Rp + rt * kTile + l32] * T[v];
-        part += __shfl_xor(part, 32);
-        if (h == 0) sDG[e * Rp + rt * kTile + l32] = part;
-      }
-    }
-    __syncthreads();
-    for (int i = tid; i < n * Rp; i += blockDim.x) {
-      const float dg = sDG[i];
-      const float dv = dg * sRho[i], drho = dg * sV[i];
-      sV[i] = dv;
-      sRho[i] = drho;
-    }
-    __syncthreads();
-    for (int i = tid; i < n * (d + nr); i += blockDim.x) {
-      const int e = i / (d + nr), k = i - e * (d + nr);
-      // each thread starts at its own rank so that a wave's LDS reads of the
-      // factor rows (stride Rp) fall in distinct banks
-      const float* fr = k < d ? sB + k * Rp : sWr + (k - d) * Rp;
-      const float* vr = (k < d ? sV : sRho) + e * Rp;
-      float s2 = 0.f;
-      int rr = k % Rp;
-      for (int j = 0; j < Rp; ++j) {
-        s2 += fr[rr] * vr[rr];
-        rr = rr + 1 == Rp ? 0 : rr + 1;
-      }
-      if (k < d)
-        sDY[e * d + k] = s2;
-      else
-        sDPhi[e * nr + (k - d)] = s2;
-    }
-    __syncthreads();
-    if (tid < n) {
-      const int eid = sEid[tid];
-      const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
-      const float rn = sqrtf(vx * vx + vy * vy + vz * vz);
-      float gx = 0.f, gy = 0.f, gzv = 0.f;
-      for (int k = 0; k < d; ++k) {
-        const float dy = sDY[tid * d + k];
-        gx += dy * sJ[tid * 3 * d + 3 * k];
-        gy += dy * sJ[tid * 3 * d + 3 * k + 1];
-        gzv += dy * sJ[tid * 3 * d + 3 * k + 2];
-      }
-      float dr = 0.f;
-      for (int q = 0; q < nr; ++q) {
-        const float t = (rn - float(q) * a.sigma) / a.sigma;
-        dr += sDPhi[tid * nr + q] * (-t / a.sigma) * sPhi[tid * nr + q];
-      }
-      const float inv = 1.f / rn;
-      a.grad_vec[3 * eid] = gx + dr * vx * inv;
-      a.grad_vec[3 * eid + 1] = gy + dr * vy * inv;
-      a.grad_vec[3 * eid + 2] = gzv + dr * vz * inv;
-    }
-  }
-}
-
-template <int RT, int NCT, typename TX>
-hipError_t launch_sg(const BwdDstArgs& a, hipStream_t s) {
-  const size_t lds = size_t(sg_smem(RT, a.d, a.n_radial).floats) * 4;
-  auto k = k_bwd_dst_sg<RT, NCT, TX>;
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     int(lds));
-  if (e != hipSuccess) return e;
-  k<<<dim3(a.n_seg), dim3(kSgWaves * kWave), lds, s>>>(a);
-  return hipGetLastError();
-}
-
 template <int MT, int RT, int NCT, typename TX>
 hipError_t launch_k(const BwdDstArgs& a, hipStream_t s) {
   const size_t lds = size_t(dst_smem(RT, a.d, a.n_radial).floats) * 4;
@@ -543,17 +302,10 @@ hipError_t launch_mt(const BwdDstArgs& a, hipStream_t s) {
   const int rt = (a.R + kTile - 1) / kTile;
   const int nct = (a.C + kTile - 1) / kTile;
   const int NC = nct <= 2 ? 2 : (nct <= 4 ? 4 : 8);
-  // d <= 32: the factored form (fewer MFMAs whenever R, C >= 64); else the
-  // direct P_e = x[s_e] Gh^T form
-#define TDN_BWD_CASE(RTV)                                                          \
-  case RTV:                                                                        \
-    if (MT == 1) {                                                                 \
-      if (NC == 2) return launch_sg<RTV, 2, TX>(a, s);                             \
-      if (NC == 4) return launch_sg<RTV, 4, TX>(a, s);                             \
-      return launch_sg<RTV, 8, TX>(a, s);                                          \
-    }                                                                              \
-    if (NC == 2) return launch_k<MT, RTV, 2, TX>(a, s);                            \
-    if (NC == 4) return launch_k<MT, RTV, 4, TX>(a, s);                            \
+#define TDN_BWD_CASE(RTV)                                   \
+  case RTV:                                                 \
+    if (NC == 2) return launch_k<MT, RTV, 2, TX>(a, s);     \
+    if (NC == 4) return launch_k<MT, RTV, 4, TX>(a, s);     \
     return launch_k<MT, RTV, 8, TX>(a, s);
   switch (rt) {
     TDN_BWD_CASE(1)

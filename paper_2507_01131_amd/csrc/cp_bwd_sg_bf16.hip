@@ -1,0 +1,4 @@
+// Factored destination-side backward (d <= 32) instantiated for bf16 features.
+#include "cp_bwd_sg_impl.hpp"
+
+template hipError_t tdn::bwd_sg_detail::launch_sg_any<true>(const tdn::BwdDstArgs&, hipStream_t);
