@@ -318,7 +318,7 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
       Z = Zw;
     }
     Timed t("gram", stream);
-    TDN_HIP(tdn::launch_gram(N * d, C, Z, grad_out, reinterpret_cast<float*>(ws + lay.parts), grad_W, stream));
+    TDN_HIP(tdn::launch_gram(N * d, C, Z, grad_out, bf16, reinterpret_cast<float*>(ws + lay.parts), grad_W, stream));
   }
   if (grad_edge_vec && E > 0) {
     tdn::BwdDstArgs a{};

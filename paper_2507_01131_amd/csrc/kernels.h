@@ -54,13 +54,15 @@ hipError_t launch_transpose_bf16(int N, int d, int C, const void* x, bool x_is_f
 hipError_t launch_cp_edge_bf16(const EdgeArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- node GEMMs
-// out[rows, C] = in[rows, C] @ W (transpose_w = 0) or in @ W^T (transpose_w = 1)
+// out[rows, C] = in[rows, C] @ W (transpose_w = 0) or in @ W^T (transpose_w = 1);
+// with w_bf16 the fp32 operand is rounded to bf16 for bf16 MFMA
 hipError_t launch_node_gemm(int rows, int C, const float* in, const void* W, bool w_bf16, int transpose_w,
                             float* out, hipStream_t s);
-// grad_W[C, C] = sum_rows Z[row, :]^T G[row, :], split over n_part row chunks
-// reduced in a fixed order.  partial: [n_part, C, C] floats of workspace.
+// grad_W[C, C] = sum_rows Z[row, :]^T G[row, :], split over gram_parts(rows)
+// row chunks reduced in a fixed order.  partial: [n_part, C, C] floats of
+// workspace.  bf16 = 1 rounds Z and G to bf16 for the MFMA (bf16 problems).
 int gram_parts(int rows);
-hipError_t launch_gram(int rows, int C, const float* Z, const float* G, float* partial, float* grad_W,
+hipError_t launch_gram(int rows, int C, const float* Z, const float* G, bool bf16, float* partial, float* grad_W,
                        hipStream_t s);
 
 // ---------------------------------------------------------------- backward

@@ -6,6 +6,12 @@
 // backward, Gz = grad_out W^T (same kernel, W read transposed) and
 // grad_W = sum_rows Z^T grad_out, split over fixed row chunks whose partial
 // C x C products are summed in a fixed order (deterministic, no atomics).
+//
+// All three share one LDS-staged MFMA micro-kernel: a 128 x 128 output tile
+// per workgroup, four waves of 64 x 64 (2 x 2 MFMA tiles, so every operand
+// read from LDS feeds two MFMAs), contraction staged in chunks of 32.  fp32
+// problems use 32x32x2 fp32 MFMA; bf16 problems (bf16 W) use 32x32x16 bf16
+// MFMA with the fp32 operand rounded to bf16 while it is staged.
 #include "common.hpp"
 #include "kernels.h"
 
@@ -13,94 +19,209 @@ namespace tdn {
 
 namespace {
 
-constexpr int kBM = 64;   // rows per block
-constexpr int kBN = 128;  // columns per block
-constexpr int kBK = 32;   // contraction chunk staged in LDS
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-template <typename TW>
-__global__ __launch_bounds__(256) void k_node_gemm(int rows, int C, const float* __restrict__ in,
-                                                   const TW* __restrict__ W, int transpose_w,
-                                                   float* __restrict__ out) {
-  __shared__ float sA[kBM][kBK + 1];
-  __shared__ float sW[kBK][kBN + 4];
+constexpr int kBM = 128;  // output rows per block
+constexpr int kBN = 128;  // output columns per block
+constexpr int kBK = 32;   // contraction chunk
+constexpr int kSF = kBK + 1;  // fp32 LDS row stride (floats)
+constexpr int kSH = kBK + 8;  // bf16 LDS row stride (halves): 80-byte rows
+
+__device__ __forceinline__ uint16_t bf16_bits(float v) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v)); }
+
+template <typename T>
+__device__ __forceinline__ float to_f32(T v);
+template <>
+__device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <>
+__device__ __forceinline__ float to_f32<uint16_t>(uint16_t v) { return __uint_as_float(uint32_t(v) << 16); }
+
+__device__ __forceinline__ f32x16 mfma32_bf16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// 16 consecutive elements as floats (zero when out of range; `n_ok` of them
+// valid).  Element types: float (four float4 loads) or bf16 bits (two 16-byte
+// loads).
+template <typename T>
+__device__ __forceinline__ void load16(const T* p, int n_ok, float (&v)[16]);
+template <>
+__device__ __forceinline__ void load16<float>(const float* p, int n_ok, float (&v)[16]) {
+  if (n_ok >= 16) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 t = *reinterpret_cast<const f32x4*>(p + 4 * q);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[4 * q + i] = t[i];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = i < n_ok ? p[i] : 0.f;
+  }
+}
+template <>
+__device__ __forceinline__ void load16<uint16_t>(const uint16_t* p, int n_ok, float (&v)[16]) {
+  if (n_ok >= 16) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const u32x4 t = *reinterpret_cast<const u32x4*>(p + 8 * q);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v[8 * q + 2 * i] = __uint_as_float(t[i] << 16);
+        v[8 * q + 2 * i + 1] = __uint_as_float(t[i] & 0xffff0000u);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = i < n_ok ? __uint_as_float(uint32_t(p[i]) << 16) : 0.f;
+  }
+}
+
+// out[m][n] = sum_k L(m, k) R(k, n) for one 128 x 128 tile, k in
+// [k_begin, k_end):
+//   L(m, k) = lhs[(m0 + m) * ldl + k]  (LT = false)   or lhs[k * ldl + m0 + m]  (LT = true)
+//   R(k, n) = rhs[k * ldr + n0 + n]    (RT = false)   or rhs[(n0 + n) * ldr + k] (RT = true)
+// Each 32-deep chunk is staged "contraction-fastest" in LDS (sa[m][k],
+// sb[n][k]); every thread brings 16 consecutive elements of each operand with
+// vector loads, and the next chunk's loads are issued before the current
+// chunk's MFMAs (register double buffer).  BF16 rounds both operands to bf16
+// at staging and runs 32x32x16 bf16 MFMA; otherwise 32x32x2 fp32 MFMA.
+template <bool BF16, bool LT, bool RT, typename TL, typename TR>
+__device__ inline void gemm_tile(const TL* __restrict__ lhs, int ldl, int M, const TR* __restrict__ rhs, int ldr,
+                                 int Ncols, int k_begin, int k_end, int m0, int n0, f32x16 (&acc)[2][2], void* smem) {
+  constexpr int SS = BF16 ? kSH : kSF;  // LDS row stride in elements
+  float* sa_f = static_cast<float*>(smem);
+  float* sb_f = sa_f + kBM * kSF;
+  uint16_t* sa_h = static_cast<uint16_t*>(smem);
+  uint16_t* sb_h = sa_h + kBM * kSH;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, l32 = lane & 31;
-  const int r0 = blockIdx.x * kBM, c0 = blockIdx.y * kBN;
   const int wr = wave >> 1, wc = wave & 1;
-  f32x16 acc[2] = {f32x16{}, f32x16{}};
-  for (int k0 = 0; k0 < C; k0 += kBK) {
-    {  // 64 x 32 tile of `in`: thread -> (row, 8 consecutive columns)
-      const int row = tid >> 2, kq = (tid & 3) * 8;
-      const int gr = r0 + row, gk = k0 + kq;
-      for (int i = 0; i < 8; ++i) sA[row][kq + i] = (gr < rows && gk + i < C) ? in[size_t(gr) * C + gk + i] : 0.f;
+  // this thread's 16-element runs: along k (rows of 32 -> 2 runs per row) or
+  // along m/n (k fixed, 128 wide -> 8 runs per k)
+  const int a_r = LT ? tid / 8 : tid / 2, a_c = LT ? (tid % 8) * 16 : (tid % 2) * 16;
+  const int b_r = RT ? tid / 2 : tid / 8, b_c = RT ? (tid % 2) * 16 : (tid % 8) * 16;
+  float va[16], vb[16];
+  auto fetch = [&](int k0) {
+    if constexpr (LT) {  // run: k = k0 + a_r, m = m0 + a_c .. +15
+      const int gk = k0 + a_r;
+      const int n_ok = gk < k_end ? min(16, M - (m0 + a_c)) : 0;
+      load16<TL>(lhs + size_t(gk < k_end ? gk : k_begin) * ldl + (m0 + a_c < M ? m0 + a_c : 0), n_ok, va);
+    } else {             // run: m = m0 + a_r, k = k0 + a_c .. +15
+      const int gm = m0 + a_r;
+      const int n_ok = gm < M ? min(16, k_end - (k0 + a_c)) : 0;
+      load16<TL>(lhs + size_t(gm < M ? gm : 0) * ldl + (k0 + a_c < k_end ? k0 + a_c : k_begin), n_ok, va);
     }
-    if (!transpose_w) {  // sW[k][n] = W[k0+k][c0+n]
-      const int kr = tid >> 3, n0 = (tid & 7) * 16;
-      const int gk = k0 + kr;
-      for (int i = 0; i < 16; ++i) {
-        const int gn = c0 + n0 + i;
-        sW[kr][n0 + i] = (gk < C && gn < C) ? load_feat<TW>(W + size_t(gk) * C + gn) : 0.f;
+    if constexpr (RT) {  // run: n = n0 + b_r, k = k0 + b_c .. +15
+      const int gn = n0 + b_r;
+      const int n_ok = gn < Ncols ? min(16, k_end - (k0 + b_c)) : 0;
+      load16<TR>(rhs + size_t(gn < Ncols ? gn : 0) * ldr + (k0 + b_c < k_end ? k0 + b_c : k_begin), n_ok, vb);
+    } else {             // run: k = k0 + b_r, n = n0 + b_c .. +15
+      const int gk = k0 + b_r;
+      const int n_ok = gk < k_end ? min(16, Ncols - (n0 + b_c)) : 0;
+      load16<TR>(rhs + size_t(gk < k_end ? gk : k_begin) * ldr + (n0 + b_c < Ncols ? n0 + b_c : 0), n_ok, vb);
+    }
+  };
+  auto put = [&]() {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int am = LT ? a_c + i : a_r, ak = LT ? a_r : a_c + i;
+      const int bn = RT ? b_r : b_c + i, bk = RT ? b_c + i : b_r;
+      if constexpr (BF16) {
+        sa_h[am * SS + ak] = bf16_bits(va[i]);
+        sb_h[bn * SS + bk] = bf16_bits(vb[i]);
+      } else {
+        sa_f[am * SS + ak] = va[i];
+        sb_f[bn * SS + bk] = vb[i];
       }
-    } else {  // sW[k][n] = W[c0+n][k0+k]
-      const int n = tid >> 1, kk = (tid & 1) * 16;
-      const int gn = c0 + n;
-      for (int i = 0; i < 16; ++i) {
-        const int gk = k0 + kk + i;
-        sW[kk + i][n] = (gk < C && gn < C) ? load_feat<TW>(W + size_t(gn) * C + gk) : 0.f;
+    }
+  };
+  if (k_begin >= k_end) return;
+  fetch(k_begin);
+  for (int k0 = k_begin; k0 < k_end; k0 += kBK) {
+    __syncthreads();  // the previous chunk's operands are consumed
+    put();
+    __syncthreads();
+    if (k0 + kBK < k_end) fetch(k0 + kBK);
+    if constexpr (BF16) {
+#pragma unroll
+      for (int s = 0; s < kBK / 16; ++s) {
+        bf16x8 av[2], bv[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          av[i] = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4*>(sa_h + (wr * 64 + i * 32 + l32) * SS + 16 * s + 8 * h));
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          bv[j] = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4*>(sb_h + (wc * 64 + j * 32 + l32) * SS + 16 * s + 8 * h));
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) acc[i][j] = mfma32_bf16(av[i], bv[j], acc[i][j]);
       }
-    }
-    __syncthreads();
+    } else {
 #pragma unroll
-    for (int s = 0; s < kBK / 2; ++s) {
-      const float av = sA[wr * 32 + l32][2 * s + h];
+      for (int s = 0; s < kBK / 2; ++s) {
+        const int k = 2 * s + h;
+        float av[2], bv[2];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) acc[t] = mfma32(av, sW[2 * s + h][wc * 64 + t * 32 + l32], acc[t]);
-    }
-    __syncthreads();
-  }
+        for (int i = 0; i < 2; ++i) av[i] = sa_f[(wr * 64 + i * 32 + l32) * SS + k];
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int col = c0 + wc * 64 + t * 32 + l32;
-    if (col >= C) continue;
+        for (int j = 0; j < 2; ++j) bv[j] = sb_f[(wc * 64 + j * 32 + l32) * SS + k];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int row = r0 + wr * 32 + acc_row(v, h);
-      if (row < rows) out[size_t(row) * C + col] = acc[t][v];
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(av[i], bv[j], acc[i][j]);
+      }
     }
   }
 }
 
-// partial[p][ci][co] = sum over rows of chunk p of Z[row][ci] G[row][co].
-// One wave per (chunk, ci tile, group of up to 4 co tiles).
-__global__ __launch_bounds__(64) void k_gram_partial(int rows, int C, int rows_per_part, const float* __restrict__ Z,
-                                                     const float* __restrict__ G, float* __restrict__ partial) {
-  const int p = blockIdx.x, cit = blockIdx.y, cog = blockIdx.z;
-  const int lane = threadIdx.x, h = lane >> 5, l32 = lane & 31;
+__device__ inline void store_tile(const f32x16 (&acc)[2][2], float* __restrict__ out, int ldo, int M, int Ncols, int m0,
+                                  int n0) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int h = lane >> 5, l32 = lane & 31;
+  const int wr = wave >> 1, wc = wave & 1;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = n0 + wc * 64 + j * 32 + l32;
+      if (col >= Ncols) continue;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = m0 + wr * 64 + i * 32 + acc_row(v, h);
+        if (row < M) out[size_t(row) * ldo + col] = acc[i][j][v];
+      }
+    }
+}
+
+// out[rows, C] = in[rows, C] @ W   (TW: W[k][n])   or   in @ W^T   (W[n][k])
+template <typename TW, bool BF16, bool WT>
+__global__ __launch_bounds__(256) void k_node_gemm(int rows, int C, const float* __restrict__ in,
+                                                   const TW* __restrict__ W, float* __restrict__ out) {
+  __shared__ __align__(16) float smem[2 * kBM * kSF];
+  const int m0 = blockIdx.x * kBM, n0 = blockIdx.y * kBN;
+  f32x16 acc[2][2] = {{f32x16{}, f32x16{}}, {f32x16{}, f32x16{}}};
+  gemm_tile<BF16, false, WT>(in, C, rows, W, C, C, 0, C, m0, n0, acc, smem);
+  store_tile(acc, out, C, rows, C, m0, n0);
+}
+
+// partial[p][ci][co] = sum over rows of chunk p of Z[row][ci] G[row][co]:
+// L(m = ci, k = row) = Z[row][ci] (transposed left operand),
+// R(k = row, n = co) = G[row][co].
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_gram_partial(int rows, int C, int rows_per_part, const float* __restrict__ Z,
+                                                      const float* __restrict__ G, float* __restrict__ partial) {
+  __shared__ __align__(16) float smem[2 * kBM * kSF];
+  const int p = blockIdx.x;
+  const int m0 = blockIdx.y * kBM, n0 = blockIdx.z * kBN;
   const int lo = p * rows_per_part, hi = min(rows, lo + rows_per_part);
-  const int ci = cit * kTile + l32;
-  f32x16 acc[4] = {f32x16{}, f32x16{}, f32x16{}, f32x16{}};
-  for (int r = lo; r < hi; r += 2) {
-    const int row = r + h;
-    const bool ok = row < hi;
-    const float av = (ok && ci < C) ? Z[size_t(row) * C + ci] : 0.f;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int co = (cog * 4 + t) * kTile + l32;
-      const float bv = (ok && co < C) ? G[size_t(row) * C + co] : 0.f;
-      acc[t] = mfma32(av, bv, acc[t]);
-    }
-  }
-  float* out = partial + size_t(p) * C * C;
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int co = (cog * 4 + t) * kTile + l32;
-    if (co >= C) continue;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int r = cit * kTile + acc_row(v, h);
-      if (r < C) out[size_t(r) * C + co] = acc[t][v];
-    }
-  }
+  f32x16 acc[2][2] = {{f32x16{}, f32x16{}}, {f32x16{}, f32x16{}}};
+  gemm_tile<BF16, true, false>(Z, C, C, G, C, C, lo, hi, m0, n0, acc, smem);
+  store_tile(acc, partial + size_t(p) * C * C, C, C, C, m0, n0);
 }
 
 __global__ void k_sum_parts(int n_part, int CC, const float* __restrict__ partial, float* __restrict__ out) {
@@ -117,25 +238,38 @@ hipError_t launch_node_gemm(int rows, int C, const float* in, const void* W, boo
                             hipStream_t s) {
   if (rows == 0) return hipSuccess;
   const dim3 grid((rows + kBM - 1) / kBM, (C + kBN - 1) / kBN);
-  if (w_bf16)
-    k_node_gemm<uint16_t><<<grid, dim3(256), 0, s>>>(rows, C, in, static_cast<const uint16_t*>(W), transpose_w, out);
-  else
-    k_node_gemm<float><<<grid, dim3(256), 0, s>>>(rows, C, in, static_cast<const float*>(W), transpose_w, out);
+  const uint16_t* wh = static_cast<const uint16_t*>(W);
+  const float* wf = static_cast<const float*>(W);
+  if (w_bf16) {
+    if (transpose_w)
+      k_node_gemm<uint16_t, true, true><<<grid, dim3(256), 0, s>>>(rows, C, in, wh, out);
+    else
+      k_node_gemm<uint16_t, true, false><<<grid, dim3(256), 0, s>>>(rows, C, in, wh, out);
+  } else {
+    if (transpose_w)
+      k_node_gemm<float, false, true><<<grid, dim3(256), 0, s>>>(rows, C, in, wf, out);
+    else
+      k_node_gemm<float, false, false><<<grid, dim3(256), 0, s>>>(rows, C, in, wf, out);
+  }
   return hipGetLastError();
 }
 
 int gram_parts(int rows) {
-  int p = (rows + 255) / 256;
-  return p < 1 ? 1 : (p > 256 ? 256 : p);
+  int p = (rows + 511) / 512;
+  return p < 1 ? 1 : (p > 128 ? 128 : p);
 }
 
-hipError_t launch_gram(int rows, int C, const float* Z, const float* G, float* partial, float* grad_W, hipStream_t s) {
+hipError_t launch_gram(int rows, int C, const float* Z, const float* G, bool bf16, float* partial, float* grad_W,
+                       hipStream_t s) {
+  if (rows <= 0) return launch_zero(grad_W, size_t(C) * C * 4, s);
   const int parts = gram_parts(rows);
   int rpp = (rows + parts - 1) / parts;
-  rpp += rpp & 1;
-  const int ct = (C + kTile - 1) / kTile;
-  if (rows > 0) k_gram_partial<<<dim3(parts, ct, (ct + 3) / 4), dim3(64), 0, s>>>(rows, C, rpp, Z, G, partial);
-  else return launch_zero(grad_W, size_t(C) * C * 4, s);
+  rpp = (rpp + kBK - 1) / kBK * kBK;
+  const dim3 grid(parts, (C + kBM - 1) / kBM, (C + kBN - 1) / kBN);
+  if (bf16)
+    k_gram_partial<true><<<grid, dim3(256), 0, s>>>(rows, C, rpp, Z, G, partial);
+  else
+    k_gram_partial<false><<<grid, dim3(256), 0, s>>>(rows, C, rpp, Z, G, partial);
   k_sum_parts<<<dim3((C * C + 255) / 256), dim3(256), 0, s>>>(parts, C * C, partial, grad_W);
   return hipGetLastError();
 }
