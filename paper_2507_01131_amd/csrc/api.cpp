@@ -54,8 +54,13 @@ size_t xt_bytes(const tdn_problem& p) {
   return p.feat_dtype == TDN_BF16 ? size_t(p.n_nodes) * p.C * tdn::bf16_kpad(dim_of(p.L)) * 2 : 0;
 }
 
+// partial slots of the fp32 edge pass: two [d, C] rows per edge range
+size_t partial_bytes(const tdn_problem& p) {
+  return size_t(tdn::edge_ranges(p.L, p.R, p.C, p.n_radial, p.n_edges)) * 2 * dim_of(p.L) * p.C * 4;
+}
+
 struct FwdLayout {
-  size_t z, xt, sort, flags, total;
+  size_t z, xt, part, sort, flags, total;
 };
 FwdLayout fwd_layout(const tdn_problem& p) {
   FwdLayout f{};
@@ -65,6 +70,8 @@ FwdLayout fwd_layout(const tdn_problem& p) {
   o += al(ndc);
   f.xt = o;
   o += al(xt_bytes(p));
+  f.part = o;
+  o += al(partial_bytes(p));
   f.sort = o;
   o += al(p.edges_sorted ? 0 : tdn::sort_plan(p.n_nodes, p.n_edges).bytes);
   f.flags = o;
@@ -74,7 +81,7 @@ FwdLayout fwd_layout(const tdn_problem& p) {
 }
 
 struct BwdLayout {
-  size_t gz, z, xt, parts, perm_src, off_src, sort, flags, total;
+  size_t gz, z, xt, part, parts, perm_src, off_src, sort, flags, total;
 };
 BwdLayout bwd_layout(const tdn_problem& p) {
   BwdLayout b{};
@@ -86,6 +93,8 @@ BwdLayout bwd_layout(const tdn_problem& p) {
   o += al(ndc);
   b.xt = o;
   o += al(xt_bytes(p));
+  b.part = o;
+  o += al(partial_bytes(p));
   b.parts = o;
   o += al(size_t(tdn::gram_parts(p.n_nodes * dim_of(p.L))) * p.C * p.C * 4);
   b.perm_src = o;
@@ -167,8 +176,8 @@ tdn_status run_validation(const tdn_problem& p, const int32_t* edge_index, const
 }
 
 tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int32_t* perm, const int32_t* gather,
-                        const float* edge_vec, const float* KF, const float* EF, const float* B, const float* radial_w,
-                        const void* feat, float* out) {
+                        const int32_t* key, const float* edge_vec, const float* KF, const float* EF, const float* B,
+                        const float* radial_w, const void* feat, float* out, float* partial) {
   tdn::EdgeArgs a{};
   a.n_seg = p.n_nodes;
   a.E = p.n_edges;
@@ -181,6 +190,7 @@ tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int3
   a.offsets = offsets;
   a.perm = perm;
   a.gather = gather;
+  a.key = key;
   a.edge_vec = edge_vec;
   a.KF = KF;
   a.EF = EF;
@@ -188,14 +198,17 @@ tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int3
   a.radial_w = radial_w;
   a.feat = feat;
   a.out = out;
+  a.n_range = tdn::edge_ranges(p.L, p.R, p.C, p.n_radial, p.n_edges);
+  a.partial = partial;
   return a;
 }
 
 // The forward edge pass Z = per-node D diag(g) A^T x sums, for either
 // feature dtype (bf16 goes through the transposed copy in the workspace).
 hipError_t forward_edge_pass(const tdn_problem& p, const int32_t* offsets, const int32_t* perm, const int32_t* src,
-                             const float* edge_vec, const float* A, const float* B, const float* D,
-                             const float* radial_w, const void* x, void* xt, float* Z, hipStream_t s) {
+                             const int32_t* dst, const float* edge_vec, const float* A, const float* B, const float* D,
+                             const float* radial_w, const void* x, void* xt, float* partial, float* Z,
+                             hipStream_t s) {
   if (p.feat_dtype == TDN_BF16) {
     {
       Timed t("transpose_bf16", s);
@@ -203,10 +216,11 @@ hipError_t forward_edge_pass(const tdn_problem& p, const int32_t* offsets, const
       if (e != hipSuccess) return e;
     }
     Timed t("cp_edge_fwd", s);
-    return tdn::launch_cp_edge_bf16(edge_args(p, offsets, perm, src, edge_vec, A, D, B, radial_w, xt, Z), s);
+    return tdn::launch_cp_edge_bf16(
+        edge_args(p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, xt, Z, partial), s);
   }
   Timed t("cp_edge_fwd", s);
-  return tdn::launch_cp_edge(edge_args(p, offsets, perm, src, edge_vec, A, D, B, radial_w, x, Z), false, s);
+  return tdn::launch_cp_edge(edge_args(p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, x, Z, partial), s);
 }
 
 }  // namespace
@@ -270,7 +284,8 @@ tdn_status tdn_cp_tp_forward(const tdn_problem* p, const void* x, const float* e
   if (N == 0) return TDN_OK;
   float* Z = z_save ? z_save : reinterpret_cast<float*>(ws + lay.z);
   const bool bf16 = p->feat_dtype == TDN_BF16;
-  TDN_HIP(forward_edge_pass(*p, offsets, perm, src, edge_vec, A, B, D, radial_w, x, ws + lay.xt, Z, stream));
+  TDN_HIP(forward_edge_pass(*p, offsets, perm, src, dst, edge_vec, A, B, D, radial_w, x, ws + lay.xt,
+                            reinterpret_cast<float*>(ws + lay.part), Z, stream));
   {
     Timed t("node_gemm", stream);
     TDN_HIP(tdn::launch_node_gemm(N * d, C, Z, W, bf16, 0, out, stream));
@@ -314,7 +329,8 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
     const float* Z = z_save;
     if (!Z) {
       float* Zw = reinterpret_cast<float*>(ws + lay.z);
-      TDN_HIP(forward_edge_pass(*p, offsets, perm, src, edge_vec, A, B, D, radial_w, x, ws + lay.xt, Zw, stream));
+      TDN_HIP(forward_edge_pass(*p, offsets, perm, src, dst, edge_vec, A, B, D, radial_w, x, ws + lay.xt,
+                                reinterpret_cast<float*>(ws + lay.part), Zw, stream));
       Z = Zw;
     }
     Timed t("gram", stream);
@@ -359,11 +375,14 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
       }
       Timed t("cp_edge_bwd_src", stream);
       TDN_HIP(tdn::launch_cp_edge_bf16(
-          edge_args(*p, off_src, perm_src, dst, edge_vec, D, A, B, radial_w, ws + lay.xt, grad_x), stream));
+          edge_args(*p, off_src, perm_src, dst, src, edge_vec, D, A, B, radial_w, ws + lay.xt, grad_x,
+                    reinterpret_cast<float*>(ws + lay.part)),
+          stream));
     } else {
       Timed t("cp_edge_bwd_src", stream);
-      TDN_HIP(tdn::launch_cp_edge(edge_args(*p, off_src, perm_src, dst, edge_vec, D, A, B, radial_w, Gz, grad_x),
-                                  false, stream));
+      TDN_HIP(tdn::launch_cp_edge(edge_args(*p, off_src, perm_src, dst, src, edge_vec, D, A, B, radial_w, Gz, grad_x,
+                                            reinterpret_cast<float*>(ws + lay.part)),
+                                  stream));
     }
   }
   return TDN_OK;

@@ -29,14 +29,18 @@ hipError_t launch_validate(int N, int E, const int32_t* edge_index, const float*
 // One Khatri-Rao contraction pass over segments of a sorted edge list:
 //   H_seg = sum_{e in seg} diag(g_e) KF^T feat[gather[e]]    ([R, C])
 //   out[seg] = EF H_seg                                       ([d, C])
-// forward:        KF = A, EF = D, feat = x,  gather = src, segments = dst
-// grad_x pass:    KF = D, EF = A, feat = Gz, gather = dst, segments = src
+// forward:        KF = A, EF = D, feat = x,  gather = src, key = dst
+// grad_x pass:    KF = D, EF = A, feat = Gz, gather = dst, key = src
+// The fp32 pass splits the sorted edges into n_range equal ranges (one
+// workgroup each per channel group); segments spanning ranges are summed
+// from `partial` ([n_range, 2, d, C] floats of workspace).
 struct EdgeArgs {
   int n_seg, E, L, d, C, R, n_radial;
   float sigma;               // r_cut / (n_radial - 1)
   const int32_t* offsets;    // [n_seg + 1]
   const int32_t* perm;       // [E] sorted slot -> edge id
   const int32_t* gather;     // [E] by edge id: row of feat to gather
+  const int32_t* key;        // [E] by edge id: segment of the edge
   const float* edge_vec;     // [E, 3] by edge id
   const float* KF;           // [d, R]
   const float* EF;           // [d, R]
@@ -44,8 +48,14 @@ struct EdgeArgs {
   const float* radial_w;     // [n_radial, R]
   const void* feat;          // [n_feat_rows, d, C]
   float* out;                // [n_seg, d, C]
+  int n_range;               // edge ranges (fp32 pass), from edge_ranges
+  float* partial;            // [n_range, 2, d, C]
 };
-hipError_t launch_cp_edge(const EdgeArgs& a, bool feat_bf16, hipStream_t s);
+// Edge ranges of the fp32 pass for this problem on the current device: the
+// number of workgroups the device holds at once, over the channel groups,
+// capped at E (0 when E = 0).
+int edge_ranges(int L, int R, int C, int n_radial, int E);
+hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
 // bfloat16 features: x [N, d, C] (bf16, or float rounded to bf16) is first
 // transposed to xT [N, C, kpad(d)] (kpad = 32 for d <= 32, else 64; zero
 // padded), which the bf16 edge pass gathers (EdgeArgs::feat = xT).
