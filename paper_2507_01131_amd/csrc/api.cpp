@@ -50,13 +50,18 @@ tdn_status check_problem(const tdn_problem* p) {
   return TDN_OK;
 }
 
+// transposed features for the edge pass: bf16 copy (bf16 problems) or the
+// three-part bf16 split (fp32 problems)
 size_t xt_bytes(const tdn_problem& p) {
-  return p.feat_dtype == TDN_BF16 ? size_t(p.n_nodes) * p.C * tdn::bf16_kpad(dim_of(p.L)) * 2 : 0;
+  const size_t nc = size_t(p.n_nodes) * p.C;
+  return p.feat_dtype == TDN_BF16 ? nc * tdn::bf16_kpad(dim_of(p.L)) * 2 : nc * 3 * tdn::x3_kpad(dim_of(p.L)) * 2;
 }
 
-// partial slots of the fp32 edge pass: two [d, C] rows per edge range
+// partial slots of the fp32 edge pass (two [d, C] rows per edge range) and
+// its zero-padded output factor [d, RT*32]
+size_t ef_pad_bytes(const tdn_problem& p) { return al(size_t(dim_of(p.L)) * ((p.R + 31) / 32 * 32) * 4); }
 size_t partial_bytes(const tdn_problem& p) {
-  return size_t(tdn::edge_ranges(p.L, p.R, p.C, p.n_radial, p.n_edges)) * 2 * dim_of(p.L) * p.C * 4;
+  return ef_pad_bytes(p) + size_t(tdn::edge_ranges(p.L, p.R, p.C, p.n_radial, p.n_edges)) * 2 * dim_of(p.L) * p.C * 4;
 }
 
 struct FwdLayout {
@@ -199,7 +204,8 @@ tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int3
   a.feat = feat;
   a.out = out;
   a.n_range = tdn::edge_ranges(p.L, p.R, p.C, p.n_radial, p.n_edges);
-  a.partial = partial;
+  a.ef_pad = partial;
+  a.partial = partial ? reinterpret_cast<float*>(reinterpret_cast<char*>(partial) + ef_pad_bytes(p)) : nullptr;
   return a;
 }
 
@@ -219,8 +225,13 @@ hipError_t forward_edge_pass(const tdn_problem& p, const int32_t* offsets, const
     return tdn::launch_cp_edge_bf16(
         edge_args(p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, xt, Z, partial), s);
   }
+  {
+    Timed t("split_x3", s);
+    hipError_t e = tdn::launch_split_x3(p.n_nodes, dim_of(p.L), p.C, static_cast<const float*>(x), xt, s);
+    if (e != hipSuccess) return e;
+  }
   Timed t("cp_edge_fwd", s);
-  return tdn::launch_cp_edge(edge_args(p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, x, Z, partial), s);
+  return tdn::launch_cp_edge(edge_args(p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, xt, Z, partial), s);
 }
 
 }  // namespace
@@ -379,8 +390,12 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
                     reinterpret_cast<float*>(ws + lay.part)),
           stream));
     } else {
+      {
+        Timed t("split_x3", stream);
+        TDN_HIP(tdn::launch_split_x3(N, d, C, Gz, ws + lay.xt, stream));
+      }
       Timed t("cp_edge_bwd_src", stream);
-      TDN_HIP(tdn::launch_cp_edge(edge_args(*p, off_src, perm_src, dst, src, edge_vec, D, A, B, radial_w, Gz, grad_x,
+      TDN_HIP(tdn::launch_cp_edge(edge_args(*p, off_src, perm_src, dst, src, edge_vec, D, A, B, radial_w, ws + lay.xt, grad_x,
                                             reinterpret_cast<float*>(ws + lay.part)),
                                   stream));
     }

@@ -31,6 +31,20 @@ __device__ __forceinline__ float load_feat<float>(const float* p) { return *p; }
 template <>
 __device__ __forceinline__ float load_feat<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
 
+// Exact three-way bfloat16 split of a float: v = hi + mid + lo with each
+// part a bfloat16 (round to nearest even at every step; the residuals
+// v - hi and v - hi - mid are exact in fp32, and the last one has at most
+// eight significant bits, so lo holds it exactly).  Products of two parts
+// are exact in fp32, which lets bf16 MFMA reproduce fp32 contractions.
+__device__ __forceinline__ uint16_t bf16_rne_bits(float v) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v)); }
+__device__ __forceinline__ void split_bf16x3(float v, uint16_t& hi, uint16_t& mid, uint16_t& lo) {
+  hi = bf16_rne_bits(v);
+  const float r1 = v - bf16_to_f32(hi);
+  mid = bf16_rne_bits(r1);
+  const float r2 = r1 - bf16_to_f32(mid);
+  lo = bf16_rne_bits(r2);
+}
+
 // Blocks of a 1-D grid are dealt to the XCDs round-robin (block b runs on XCD
 // b % 8).  Remap so that each XCD walks one contiguous range of logical work
 // items: neighbouring destination nodes share source nodes, and then share

@@ -35,6 +35,15 @@ __global__ __launch_bounds__(256) void k_range_fixup(int E, int n_range, int dC,
   }
 }
 
+// dst[k][r] = src[k][r] for r < R, 0 for R <= r < Rp
+__global__ __launch_bounds__(256) void k_pad_rows(int rows, int R, int Rp, const float* __restrict__ src,
+                                                  float* __restrict__ dst) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * Rp) return;
+  const int k = i / Rp, r = i - k * Rp;
+  dst[i] = r < R ? src[k * R + r] : 0.f;
+}
+
 int device_cus() {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 256;
@@ -72,8 +81,14 @@ int edge_ranges(int L, int R, int C, int n_radial, int E) {
 
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s) {
   using namespace edge_detail;
-  if (a.E > 0 && (a.n_range < 1 || a.n_range > a.E)) return hipErrorInvalidValue;
+  if (a.E > 0 && (a.n_range < 1 || a.n_range > a.E || !a.ef_pad)) return hipErrorInvalidValue;
   hipError_t e = hipSuccess;
+  if (a.E > 0) {
+    const int Rp = (a.R + kTile - 1) / kTile * kTile;
+    k_pad_rows<<<dim3((a.d * Rp + 255) / 256), dim3(256), 0, s>>>(a.d, a.R, Rp, a.EF, a.ef_pad);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   switch (a.L) {
     case 0: e = launch_cp_edge_l<0>(a, s); break;
     case 1: e = launch_cp_edge_l<1>(a, s); break;

@@ -1,20 +1,28 @@
-// The CP tensor-product edge pass as one Khatri-Rao GEMM per segment.
+// The CP tensor-product edge pass for fp32 features.
 //
 // For a destination node t with incoming edges e (eq. approximate of
 // Sec. 3.1 per channel, radial weight on the rank index):
-//   H_t[r, c] = sum_e g_e[r] sum_k A[k, r] x[s_e][k, c]
-//             = (K_t^T X_t)[r, c],  K_t[(e,k), r] = g_e[r] A[k, r],
-//                                    X_t[(e,k), c] = x[s_e][k, c]
-// so the projection A^T x, the Hadamard product with g_e = (B^T Y_e)*rho_e
-// and the sum over the segment are a single fp32 MFMA contraction of length
-// n_t * d whose partial sums never leave the accumulators (no atomics, fixed
-// order).  The output factor is applied once per node, Z_t = D H_t, because D
-// commutes with the sum over edges; the shared channel mix W (Sec. 3.2) is a
-// separate node GEMM.
+//   H_t[r, c] = sum_e g_e[r] U_e[r, c],   U_e = A^T x[s_e]   ([R, C], K = d)
+// with g_e = (B^T Y_e) * rho_e.  The output factor is applied once per node,
+// Z_t = D H_t, because D commutes with the sum over edges; the shared
+// channel mix W (Sec. 3.2) is a separate node GEMM.  The sum over the
+// segment stays in registers (no atomics, fixed order).
 //
 // The same kernel computes grad_x on the source-sorted graph:
 //   grad_x[s] = A sum_{e: s_e = s} diag(g_e) D^T Gz[t_e],  Gz = grad_out W^T,
-// i.e. K uses D, the epilogue uses A and the gathered rows are Gz[t_e].
+// i.e. the contraction uses D, the epilogue uses A and the gathered rows are
+// Gz[t_e].
+//
+// Arithmetic.  U_e runs on bf16 MFMA (v_mfma_f32_32x32x16_bf16) with fp32
+// accumulation and fp32 accuracy: both operands are split exactly into three
+// bfloat16 parts (a = a1 + a2 + a3, x = x1 + x2 + x3, every part product
+// exact in fp32) and the six products a_i x_j with i + j <= 4 are summed,
+// smallest first; the dropped ones are below 2^-22 of |a x|.  The features
+// arrive pre-split and transposed (xs [N, C, 3, DP], k fastest, zero padded
+// to DP = 32 or 64), so one lane's operand for eight consecutive k is one
+// 16-byte load; the split factor sits in LDS in MFMA operand order.  Then
+// acc[r, c] += g_e[r] U_e[r, c] in
+// fp32 on the VALU, with g read from LDS four rows at a time.
 //
 // Work decomposition.  The sorted edge list is cut into n_range equal ranges,
 // as many as the device holds workgroups at once (over the channel groups),
@@ -24,22 +32,17 @@
 // rank rows, so its accumulators are RT = ceil(R/32) MFMA tiles of 32x32.
 // Per chunk of edges the block evaluates the harmonics and radial basis, then
 // g_e[r] for every rank, into LDS, and marks where in the chunk a new segment
-// starts.  The MFMA loop then walks the chunk edge by edge: each edge's
-// contraction over its d feature rows is padded to an even length (a zero row
-// when d is odd), so one 32x32x2 K-step always covers rows 2j and 2j+1 of one
-// edge; g_e is held in registers for the edge, the K operand is
-// g_e[r] * KF[k][r], and the B operand x[s_e][k][c] comes straight from
-// global memory (each half-wave reads one contiguous 128-byte row slice),
-// loaded one edge ahead.  Where a segment ends the epilogue Z = EF H runs on
-// the accumulators and they restart from zero.  A segment wholly inside the
-// range is written to its output row; the first segment of a range, when it
-// began in an earlier range, and the last one, when it continues into a later
-// range, go to two per-range partial slots that a small second kernel adds
-// up in range order (fixed order, deterministic); that kernel also writes the
-// zero rows of segments without edges.
+// starts.  The MFMA loop then walks the chunk edge by edge, loading the next
+// edge's feature operands one edge ahead.  Where a segment ends the epilogue
+// Z = EF H runs on the accumulators and they restart from zero.  A segment
+// wholly inside the range is written to its output row; the first segment of
+// a range, when it began in an earlier range, and the last one, when it
+// continues into a later range, go to two per-range partial slots that a
+// small second kernel adds up in range order (fixed order, deterministic);
+// that kernel also writes the zero rows of segments without edges.
 //
-// The degree L is a template parameter so that the per-edge K-step count
-// DH = ceil(d/2) and the harmonic recurrences are compile-time constants.
+// The degree L is a template parameter so that the K-block count and the
+// harmonic recurrences are compile-time constants.
 #pragma once
 
 #include "common.hpp"
@@ -50,44 +53,44 @@ namespace tdn {
 
 namespace edge_detail {
 
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x16 mfma_bf16(u32x4 a, u32x4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                 0, 0);
+}
+
 constexpr int kMaxWavesPerBlock = 4;
 
-// Whether this lane's share of the K factor, KF[2j + h][rt*32 + l32] for all
-// K-steps j and rank tiles rt, fits in registers beside the accumulators.
-__host__ __device__ constexpr bool edge_reg_k(int d, int RT) { return (d + 1) / 2 * RT <= 64; }
+__host__ __device__ constexpr int edge_dp(int d) { return d <= 32 ? 32 : 64; }
 
-// Two waves per SIMD (two workgroups per CU) when the K factor is register
-// resident; one otherwise (large R at high L), where spilling would cost more
-// than the lost occupancy.
+// K-blocks of 16 degree rows per edge
+__host__ __device__ constexpr int edge_kb(int d) { return edge_dp(d) / 16; }
+
+// Two waves per SIMD (two workgroups per CU) when the accumulators (16 RT),
+// the double-buffered feature and factor operands (48 KB) and the rest fit in
+// 256 registers without spilling in the edge loop: two K-blocks and at most
+// four rank tiles; one wave otherwise.
 __host__ __device__ constexpr int edge_waves_per_eu(int L, int RT) {
-  return edge_reg_k((L + 1) * (L + 1), RT) ? 2 : 1;
+  return edge_kb((L + 1) * (L + 1)) == 2 && RT <= 4 ? 2 : 1;
 }
 
 struct EdgeSmem {
-  int Rp, kstride, estride, off_k, off_be, off_ef, off_g, off_y, off_vec, off_phi, off_idx, off_bnd, floats;
+  int Rp, off_a, off_g, off_y, off_vec, off_phi, off_idx, off_bnd, floats;
 };
 
-// LDS regions: the K factor (only when it is not register resident), the
-// harmonic and radial factors B and radial_w, the output factor EF (only
-// when the K factor is in registers; otherwise the epilogue reads EF from
-// global memory), g for a chunk of edges (rows rounded up to a whole 32-row
+// LDS regions (in floats): the split factor operands [KB][RT][3][64 lanes]
+// x 16 bytes, g for a chunk of edges (rows rounded up to a whole 32-row
 // tile), harmonics, normalised edge vectors with their lengths, radial basis,
 // gathered rows, and the segment starts of the chunk (positions, keys, count
 // and the two partial-segment flags).
 __host__ __device__ inline EdgeSmem edge_smem(int RT, int d, int n_radial, int chunk) {
   EdgeSmem s{};
-  const int dpad = d + (d & 1);
-  const bool reg_k = edge_reg_k(d, RT);
   s.Rp = RT * kTile;
-  s.kstride = s.Rp + 32;  // rows 2j and 2j+1 land 32 banks apart
-  s.estride = s.Rp + 1;   // the epilogue reads a column across 32 rows
   int o = 0;
-  s.off_k = o;
-  if (!reg_k) o += dpad * s.kstride;
-  s.off_be = o;
-  o += (d + n_radial) * s.Rp;
-  s.off_ef = o;
-  if (reg_k) o += d * s.estride;
+  s.off_a = o;
+  o += edge_kb(d) * RT * 3 * kWave * 4;
   s.off_g = o;
   o += (chunk + kTile - 1) / kTile * kTile * s.Rp;
   s.off_y = o;
@@ -105,45 +108,17 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, int d, int n_radial, int c
   return s;
 }
 
-// Stage a [rows_src, R] factor into LDS rows of `stride` floats; zero beyond
-// R and for rows rows_src..rows_dst-1.  Eight loads per thread are in flight
-// at once (clamped addresses, zeroing by select) before any store.
-__device__ inline void stage_factor(float* dst, const float* __restrict__ src, int rows_src, int rows_dst, int R,
-                                    int Rp, int stride) {
-  constexpr int U = 8;
-  const int total = rows_dst * Rp;
-  for (int i0 = threadIdx.x; i0 < total; i0 += U * blockDim.x) {
-    float v[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int i = i0 + u * blockDim.x;
-      const int k = i / Rp, r = i - k * Rp;
-      const int kc = k < rows_src ? k : rows_src - 1, rc = r < R ? r : R - 1;
-      v[u] = src[kc * R + rc];
-      v[u] = (k < rows_src && r < R) ? v[u] : 0.f;
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int i = i0 + u * blockDim.x;
-      const int k = i / Rp, r = i - k * Rp;
-      if (i < total) dst[k * stride + r] = v[u];
-    }
-  }
-}
-
 template <int L, int RT>
 __global__ __launch_bounds__(kMaxWavesPerBlock* kWave) __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT))))
 void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
   constexpr int d = (L + 1) * (L + 1);
-  constexpr int DH = (d + 1) / 2;  // K-steps per edge
+  constexpr int DP = edge_dp(d);
+  constexpr int KB = edge_kb(d);
   constexpr int Rp = RT * kTile;
   constexpr int MT = (d + kTile - 1) / kTile;
-  constexpr bool kRegK = edge_reg_k(d, RT);
   extern __shared__ float smem[];
   const EdgeSmem S = edge_smem(RT, d, a.n_radial, chunk);
-  float* sK = smem + S.off_k;
-  float* sBE = smem + S.off_be;
-  float* sEF = smem + S.off_ef;
+  u32x4* sA = reinterpret_cast<u32x4*>(smem + S.off_a);
   float* sG = smem + S.off_g;
   float* sY = smem + S.off_y;
   float4* sVec = reinterpret_cast<float4*>(smem + S.off_vec);
@@ -162,57 +137,63 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
   const int C = a.C, nr = a.n_radial, R = a.R;
   const int c = (cgrp * waves + wave) * kTile + l32;
   const bool cvalid = c < C;
-  const float* __restrict__ feat = static_cast<const float*>(a.feat);
 
-  // When it fits (DH*RT <= 64 values per lane) the K factor of this lane
-  // lives in registers for the whole range, read straight from global
-  // memory; the pad row (2j + h == d) and ranks beyond R are zero.
-  // Otherwise the factor is staged in LDS and read per K-step.
-  float kreg[kRegK ? DH : 1][kRegK ? RT : 1];
-  const float* kr = sK + h * S.kstride + l32;
-  if constexpr (kRegK) {
+  // Factor operands: lane (l32, h) of K-block b, rank tile rt holds
+  // KF[16b + 8h + i][rt*32 + l32], i = 0..7, zero past d and R, as its three
+  // bf16 parts.  One thread per (b, rt, lane).
+  for (int t = tid; t < KB * RT * kWave; t += blockDim.x) {
+    const int ln = t % kWave, brt = t / kWave;
+    const int b = brt / RT, rt = brt - b * RT;
+    const int r = rt * kTile + (ln & 31), k0 = 16 * b + 8 * (ln >> 5);
+    uint32_t w[3][4];
 #pragma unroll
-    for (int j = 0; j < DH; ++j)
+    for (int p = 0; p < 4; ++p) {
+      uint16_t part[3][2];
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        const int k = 2 * j + h, r = rt * kTile + l32;
-        const float v = a.KF[(k < d ? k : d - 1) * R + (r < R ? r : R - 1)];
-        kreg[j][rt] = (k < d && r < R) ? v : 0.f;
+      for (int q = 0; q < 2; ++q) {
+        const int k = k0 + 2 * p + q;
+        split_bf16x3(k < d && r < R ? a.KF[k * R + r] : 0.f, part[0][q], part[1][q], part[2][q]);
       }
-    stage_factor(sEF, a.EF, d, d, R, Rp, S.estride);
-  } else {
-    stage_factor(sK, a.KF, d, d + (d & 1), R, Rp, S.kstride);
+#pragma unroll
+      for (int s = 0; s < 3; ++s) w[s][p] = uint32_t(part[s][0]) | (uint32_t(part[s][1]) << 16);
+    }
+#pragma unroll
+    for (int s = 0; s < 3; ++s) sA[(brt * 3 + s) * kWave + ln] = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
   }
-  stage_factor(sBE, a.Bf, d, d, R, Rp, Rp);
-  stage_factor(sBE + d * Rp, a.radial_w, nr, nr, R, Rp, Rp);
+  __syncthreads();
+  // Factor operands are read where they are used: their index goes through
+  // an opaque copy (zero added in inline asm) so that the compiler does not
+  // hoist all of them out of the edge loop into registers; the pointer
+  // itself stays a known LDS pointer.
+  auto a_op = [&](int base, int b, int rt, int s) -> u32x4 { return sA[base + ((b * RT + rt) * 3 + s) * kWave]; };
 
   f32x16 acc[RT];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x16{};
 
-  // Segment epilogue: Z[m][c] = sum_r EF[m][r] H[r][c].  The contraction over
-  // r pairs accumulator register v of the two half-waves: lanes 0-31
-  // contribute rank rt*32 + acc_row(v,0), lanes 32-63 rank rt*32 +
+  // Segment epilogue: Z[m][c] = sum_r EF[m][r] H[r][c] on fp32 MFMA.  The
+  // contraction over r pairs accumulator register v of the two half-waves:
+  // lanes 0-31 contribute rank rt*32 + acc_row(v,0), lanes 32-63 rank rt*32 +
   // acc_row(v,1), which is exactly the B-operand layout, so H never leaves
-  // the registers.  The A operand comes in groups of 16 values, one group per
-  // (row tile mt, rank tile rt), the next group loaded while the current
-  // one's MFMAs run; EF is read from LDS when staged there, else from global
-  // memory.  slot < 0 writes the segment's output row, slot 0 or 1 the
-  // range's partial slot; the accumulators restart from zero.
+  // the registers.  The A operand (EF, read from global memory, where it
+  // stays cached) comes in groups of 16 values, one group per (row tile mt,
+  // rank tile rt), the next group loaded while the current one's MFMAs run.
+  // slot < 0 writes the segment's output row, slot 0 or 1 the range's partial
+  // slot; the accumulators restart from zero.
   auto finish = [&](int seg, int slot) {
     float* dst = slot < 0 ? a.out + size_t(seg) * d * C : a.partial + (size_t(range) * 2 + slot) * d * C;
     constexpr int NG = MT * RT;
+    // EF zero-padded to [d][Rp] (ef_pad): a lane's 16 values of a group sit
+    // at fixed offsets from one row pointer
+    int ef_off = 0;
+    asm volatile("" : "+s"(ef_off));
+    const float* ef = a.ef_pad + ef_off;
     auto ef_load = [&](int g, float (&ev)[16]) {
       const int mt = g / RT, rt = g - mt * RT;
-      const int row = mt * kTile + l32, rowc = row < d ? row : d - 1;
+      const int row = mt * kTile + l32;
+      const float* er = ef + (row < d ? row : d - 1) * Rp + rt * kTile + 4 * h;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int r = rt * kTile + acc_row(v, h);
-        if constexpr (kRegK)
-          ev[v] = sEF[rowc * S.estride + r];  // zero beyond R
-        else
-          ev[v] = a.EF[rowc * R + (r < R ? r : R - 1)];
-      }
+      for (int v = 0; v < 16; ++v) ev[v] = er[8 * (v >> 2) + (v & 3)];
     };
     f32x16 z = f32x16{};
     auto ef_mfma = [&](int g, const float (&ev)[16]) {
@@ -220,10 +201,7 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
       const int row = mt * kTile + l32;
       if (rt == 0) z = f32x16{};
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int r = rt * kTile + acc_row(v, h);
-        z = mfma32((row < d && r < R) ? ev[v] : 0.f, acc[rt][v], z);
-      }
+      for (int v = 0; v < 16; ++v) z = mfma32(row < d ? ev[v] : 0.f, acc[rt][v], z);
       if (rt == RT - 1 && cvalid) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
@@ -251,39 +229,81 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
     for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x16{};
   };
 
-  // B operand of K-step j of one edge: x[row][2j + h][c].  The gathered row
-  // is wave-uniform, so the row base lives in scalar registers and each load
-  // takes one 32-bit lane offset.  The loads are unconditional with clamped
-  // addresses and no select on the value, so nothing forces a wait before
-  // the operand is used one edge later: the pad row (2j + h == d) meets an
-  // all-zero K row, and a lane with c >= C only feeds result column c, which
-  // is never stored.
-  const uint32_t c_ld = cvalid ? c : C - 1;
-  auto load_edge = [&](int row, float (&b)[DH]) {
-    const char* p = reinterpret_cast<const char*>(feat + size_t(row) * (d * C));
+  // Feature operands of one edge: split s, K-block b is the 16-byte run
+  // xs[row][c][s][16b + 8h .. +7].  The gathered row is wave-uniform (row
+  // base in scalar registers, one 32-bit lane offset per load).  Lanes with
+  // c >= C read channel C - 1; their results are never stored.
+  const char* __restrict__ xs = static_cast<const char*>(a.feat);
+  const uint32_t lane_off = ((uint32_t(cvalid ? c : C - 1) * 3) * DP + 8 * h) * 2;
+  auto load_x = [&](int row, u32x4 (&xb)[3][KB]) {
+    const char* p = xs + size_t(row) * (size_t(C) * 3 * DP * 2);
 #pragma unroll
-    for (int j = 0; j < DH; ++j) {
-      const uint32_t k = 2 * j + h < d ? 2 * j + h : d - 1;
-      b[j] = *reinterpret_cast<const float*>(p + (k * uint32_t(C) + c_ld) * 4u);
-    }
+    for (int s = 0; s < 3; ++s)
+#pragma unroll
+      for (int b = 0; b < KB; ++b)
+        xb[s][b] = *reinterpret_cast<const u32x4*>(p + lane_off + uint32_t((s * DP + 16 * b) * 2));
   };
-  auto load_g = [&](int e, float (&g)[RT]) {
+  // U_e = KF^T x[row] for one rank tile from the six part products (smallest
+  // first), then acc += g_e * U_e with g for this lane's rows
+  // rt*32 + 8q + 4h + i read four at a time.  The rank tiles are pipelined:
+  // step rt issues the LDS reads of the factor parts of tile rt+1 and of g
+  // for tile rt-1, runs the MFMA chain of tile rt into one of two U buffers,
+  // and the VALU multiply-adds of tile rt-1 from the other, so that neither
+  // LDS latency nor the MFMA drain stalls the chain.
+  auto edge_compute = [&](int e, const u32x4 (&xb)[3][KB]) {
+    int ab = lane;
+    asm volatile("" : "+v"(ab));
+    const float* gb = sG + e * Rp + 4 * h;
+    u32x4 am[2][3][KB];  // [buffer][part][K-block]
+    float4 gv[4];        // [row group]
+    f32x16 U[2];
+    auto load_a = [&](int rt, int buf) {
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) g[rt] = sG[e * Rp + rt * kTile + l32];
-  };
-  auto edge_mfma = [&](const float (&g)[RT], const float (&b)[DH]) {
+      for (int sp = 0; sp < 3; ++sp)
 #pragma unroll
-    for (int j = 0; j < DH; ++j) {
+        for (int b = 0; b < KB; ++b) am[buf][sp][b] = a_op(ab, b, rt, sp);
+    };
+    auto load_g = [&](int rt) {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        float kv;
-        if constexpr (kRegK)
-          kv = kreg[j][rt];
-        else
-          kv = kr[2 * j * S.kstride + rt * kTile];
-        acc[rt] = mfma32(g[rt] * kv, b[j], acc[rt]);
+      for (int q = 0; q < 4; ++q) gv[q] = *reinterpret_cast<const float4*>(gb + rt * kTile + 8 * q);
+    };
+    auto chain = [&](int buf) {
+      f32x16 u = f32x16{};
+#pragma unroll
+      for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][0][b], xb[2][b], u);
+#pragma unroll
+      for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][2][b], xb[0][b], u);
+#pragma unroll
+      for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][1][b], xb[1][b], u);
+#pragma unroll
+      for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][0][b], xb[1][b], u);
+#pragma unroll
+      for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][1][b], xb[0][b], u);
+#pragma unroll
+      for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][0][b], xb[0][b], u);
+      U[buf] = u;
+    };
+    auto fma_rt = [&](int rt, int buf) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc[rt][4 * q + 0] += gv[q].x * U[buf][4 * q + 0];
+        acc[rt][4 * q + 1] += gv[q].y * U[buf][4 * q + 1];
+        acc[rt][4 * q + 2] += gv[q].z * U[buf][4 * q + 2];
+        acc[rt][4 * q + 3] += gv[q].w * U[buf][4 * q + 3];
       }
+    };
+    load_a(0, 0);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      if (rt + 1 < RT) load_a(rt + 1, (rt + 1) & 1);
+      if (rt > 0) load_g(rt - 1);
+      __builtin_amdgcn_sched_barrier(0);
+      chain(rt & 1);
+      if (rt > 0) fma_rt(rt - 1, (rt - 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    load_g(RT - 1);
+    fma_rt(RT - 1, (RT - 1) & 1);
   };
 
   int cur = -1;           // segment in the accumulators
@@ -337,27 +357,29 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
     }
     __syncthreads();
     // g = (Y B) * (Phi Wrad) for the chunk's edges (rows) and all ranks
-    // (columns): two small MFMA GEMMs per 32x32 tile, one rank tile per wave.
-    // Rows beyond n hold zeros (their A operand is masked) and are never read.
+    // (columns): two small fp32 MFMA GEMMs per 32x32 tile, one rank tile per
+    // wave, with B and Wrad read from global memory (cached).  Rows beyond n
+    // hold zeros (their A operand is masked) and are never read.
     const int n_et = (n + kTile - 1) / kTile;
     for (int item = wave; item < n_et * RT; item += waves) {
       const int et = item / RT, rt = item - et * RT;
       const int er = et * kTile + l32;  // this lane's edge row
       const bool row_ok = er < n;
+      const int r = rt * kTile + l32, rc = r < R ? r : R - 1;
       f32x16 Tr = f32x16{}, Ty = f32x16{};
 #pragma unroll 1
       for (int s2 = 0; s2 < (nr + 1) / 2; ++s2) {
-        const int q = 2 * s2 + h;
+        const int q = 2 * s2 + h, qc = q < nr ? q : nr - 1;
         const float av = (row_ok && q < nr) ? sPhi[er * nr + q] : 0.f;
-        const float bv = q < nr ? sBE[(d + q) * Rp + rt * kTile + l32] : 0.f;
-        Tr = mfma32(av, bv, Tr);
+        const float bw = a.radial_w[qc * R + rc];
+        Tr = mfma32(av, (q < nr && r < R) ? bw : 0.f, Tr);
       }
 #pragma unroll
       for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
-        const int k = 2 * s2 + h;
+        const int k = 2 * s2 + h, kc = k < d ? k : d - 1;
         const float av = (row_ok && k < d) ? sY[er * d + k] : 0.f;
-        const float bv = k < d ? sBE[k * Rp + rt * kTile + l32] : 0.f;
-        Ty = mfma32(av, bv, Ty);
+        const float bw = a.Bf[kc * R + rc];
+        Ty = mfma32(av, (k < d && r < R) ? bw : 0.f, Ty);
       }
 #pragma unroll
       for (int v = 0; v < 16; ++v) sG[(et * kTile + acc_row(v, h)) * Rp + rt * kTile + l32] = Tr[v] * Ty[v];
@@ -383,33 +405,23 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
         next = bi < nb ? __builtin_amdgcn_readfirstlane(sBnd[bi]) : n;
       }
       const int pe = next;
-      // Two operand buffers used alternately: the loads of edge f+1 (its
-      // feature rows and g) are issued before the MFMAs of edge f, and the
-      // gathered row of each edge is read from LDS one edge earlier still,
-      // so no wait falls between the MFMA chains of consecutive edges; the
-      // scheduling barriers keep the compiler from sinking the loads next to
-      // their use.
-      float b0[DH], b1[DH], g0[RT], g1[RT];
-      load_edge(__builtin_amdgcn_readfirstlane(sIdx[e]), b0);
-      load_g(e, g0);
-      int row_a = sIdx[e + 1 < pe ? e + 1 : e];
+      // Two operand buffers used alternately: the loads of edge f+1 are
+      // issued before the MFMAs of edge f, and the scheduling barriers keep
+      // the compiler from sinking them next to their use.
+      u32x4 x0[3][KB], x1[3][KB];
+      load_x(__builtin_amdgcn_readfirstlane(sIdx[e]), x0);
       int f = e;
       for (; f + 1 < pe; f += 2) {
-        load_edge(__builtin_amdgcn_readfirstlane(row_a), b1);
-        load_g(f + 1, g1);
-        const int f2 = f + 2 < pe ? f + 2 : f + 1, f3 = f + 3 < pe ? f + 3 : f2;  // past the end: reloads, unused
-        const int row_b = sIdx[f2];
+        load_x(__builtin_amdgcn_readfirstlane(sIdx[f + 1]), x1);
         __builtin_amdgcn_sched_barrier(0);
-        edge_mfma(g0, b0);
+        edge_compute(f, x0);
         __builtin_amdgcn_sched_barrier(0);
-        load_edge(__builtin_amdgcn_readfirstlane(row_b), b0);
-        load_g(f2, g0);
-        row_a = sIdx[f3];
+        load_x(__builtin_amdgcn_readfirstlane(sIdx[f + 2 < pe ? f + 2 : f + 1]), x0);  // past the end: unused
         __builtin_amdgcn_sched_barrier(0);
-        edge_mfma(g1, b1);
+        edge_compute(f + 1, x1);
         __builtin_amdgcn_sched_barrier(0);
       }
-      if (f < pe) edge_mfma(g0, b0);
+      if (f < pe) edge_compute(f, x0);
       e = pe;
     }
   }

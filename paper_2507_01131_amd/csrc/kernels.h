@@ -50,11 +50,17 @@ struct EdgeArgs {
   float* out;                // [n_seg, d, C]
   int n_range;               // edge ranges (fp32 pass), from edge_ranges
   float* partial;            // [n_range, 2, d, C]
+  float* ef_pad;             // [d, RT*32] fp32 pass: EF zero-padded (workspace, written by launch_cp_edge)
 };
 // Edge ranges of the fp32 pass for this problem on the current device: the
 // number of workgroups the device holds at once, over the channel groups,
 // capped at E (0 when E = 0).
 int edge_ranges(int L, int R, int C, int n_radial, int E);
+// fp32 features for the fp32 pass: x [N, d, C] -> xs [N, C, 3, x3_kpad(d)]
+// bfloat16, the exact split x = hi + mid + lo along the last axis groups
+// (EdgeArgs::feat = xs); x3_kpad(d) = 32 for d <= 32, else 64.
+int x3_kpad(int d);
+hipError_t launch_split_x3(int N, int d, int C, const float* x, void* xs, hipStream_t s);
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
 // bfloat16 features: x [N, d, C] (bf16, or float rounded to bf16) is first
 // transposed to xT [N, C, kpad(d)] (kpad = 32 for d <= 32, else 64; zero
