@@ -154,7 +154,7 @@ def main():
         res = step()
     torch.cuda.synchronize()
     tdn.timer_enable(True)
-    fwd_kernels = ("cp_edge_fwd", "split_x3", "transpose_bf16", "node_gemm", "sort")
+    fwd_kernels = ("cp_edge_fwd", "feature_layout", "node_gemm", "sort")
     for k in fwd_kernels:
         tdn.timer_read(k, reset=True)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -202,7 +202,7 @@ def main():
         for _ in range(3):
             tdn.backward(res, G, workspace=wsb)
         torch.cuda.synchronize()
-        bk = ("node_gemm", "gram", "cp_bwd_dst", "sort", "split_x3", "cp_edge_bwd_src")
+        bk = ("node_gemm", "gram", "cp_bwd_dst", "sort", "feature_layout", "cp_edge_bwd_src")
         tdn.timer_enable(True)
         for k in bk:
             tdn.timer_read(k, reset=True)

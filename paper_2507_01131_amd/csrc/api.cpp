@@ -50,17 +50,20 @@ tdn_status check_problem(const tdn_problem* p) {
   return TDN_OK;
 }
 
-// transposed features for the edge pass: bf16 copy (bf16 problems) or the
-// three-part bf16 split (fp32 problems)
+// bf16 parts per feature of the edge pass: the exact three-part split of
+// fp32 features, or the bf16 features themselves
+int feature_parts(const tdn_problem& p) { return p.feat_dtype == TDN_BF16 ? 1 : 3; }
+
+// transposed features for the edge pass
 size_t xt_bytes(const tdn_problem& p) {
-  const size_t nc = size_t(p.n_nodes) * p.C;
-  return p.feat_dtype == TDN_BF16 ? nc * tdn::bf16_kpad(dim_of(p.L)) * 2 : nc * 3 * tdn::x3_kpad(dim_of(p.L)) * 2;
+  return size_t(p.n_nodes) * p.C * feature_parts(p) * tdn::edge_kpad(dim_of(p.L)) * 2;
 }
 
 // partial slots of the fp32 edge pass (two [d, C] rows per edge range) and
 // its zero-padded output factor [d, RT*32]
 size_t ef_pad_bytes(const tdn_problem& p) { return al(size_t(dim_of(p.L)) * ((p.R + 31) / 32 * 32) * 4); }
 size_t partial_bytes(const tdn_problem& p) {
+  if (p.feat_dtype == TDN_BF16) return 0;
   return ef_pad_bytes(p) + size_t(tdn::edge_ranges(p.L, p.R, p.C, p.n_radial, p.n_edges)) * 2 * dim_of(p.L) * p.C * 4;
 }
 
@@ -203,8 +206,9 @@ tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int3
   a.radial_w = radial_w;
   a.feat = feat;
   a.out = out;
-  a.n_range = tdn::edge_ranges(p.L, p.R, p.C, p.n_radial, p.n_edges);
+  a.n_range = p.feat_dtype == TDN_BF16 ? 0 : tdn::edge_ranges(p.L, p.R, p.C, p.n_radial, p.n_edges);
   a.ef_pad = partial;
+  a.parts = feature_parts(p);
   a.partial = partial ? reinterpret_cast<float*>(reinterpret_cast<char*>(partial) + ef_pad_bytes(p)) : nullptr;
   return a;
 }
@@ -215,19 +219,10 @@ hipError_t forward_edge_pass(const tdn_problem& p, const int32_t* offsets, const
                              const int32_t* dst, const float* edge_vec, const float* A, const float* B, const float* D,
                              const float* radial_w, const void* x, void* xt, float* partial, float* Z,
                              hipStream_t s) {
-  if (p.feat_dtype == TDN_BF16) {
-    {
-      Timed t("transpose_bf16", s);
-      hipError_t e = tdn::launch_transpose_bf16(p.n_nodes, dim_of(p.L), p.C, x, false, xt, s);
-      if (e != hipSuccess) return e;
-    }
-    Timed t("cp_edge_fwd", s);
-    return tdn::launch_cp_edge_bf16(
-        edge_args(p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, xt, Z, partial), s);
-  }
   {
-    Timed t("split_x3", s);
-    hipError_t e = tdn::launch_split_x3(p.n_nodes, dim_of(p.L), p.C, static_cast<const float*>(x), xt, s);
+    Timed t("feature_layout", s);
+    hipError_t e = tdn::launch_feature_layout(p.n_nodes, dim_of(p.L), p.C, x, p.feat_dtype == TDN_F32,
+                                              feature_parts(p), xt, s);
     if (e != hipSuccess) return e;
   }
   Timed t("cp_edge_fwd", s);
@@ -378,27 +373,16 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
       Timed t("sort", stream);
       TDN_HIP(tdn::launch_sort(tdn::sort_plan(N, E), src, 1, perm_src, off_src, ws + lay.sort, stream));
     }
-    if (bf16) {
-      // bf16 problems run the grad_x pass on bf16 MFMA too: Gz rounded to bf16
-      {
-        Timed t("transpose_bf16", stream);
-        TDN_HIP(tdn::launch_transpose_bf16(N, d, C, Gz, true, ws + lay.xt, stream));
-      }
-      Timed t("cp_edge_bwd_src", stream);
-      TDN_HIP(tdn::launch_cp_edge_bf16(
-          edge_args(*p, off_src, perm_src, dst, src, edge_vec, D, A, B, radial_w, ws + lay.xt, grad_x,
-                    reinterpret_cast<float*>(ws + lay.part)),
-          stream));
-    } else {
-      {
-        Timed t("split_x3", stream);
-        TDN_HIP(tdn::launch_split_x3(N, d, C, Gz, ws + lay.xt, stream));
-      }
-      Timed t("cp_edge_bwd_src", stream);
-      TDN_HIP(tdn::launch_cp_edge(edge_args(*p, off_src, perm_src, dst, src, edge_vec, D, A, B, radial_w, ws + lay.xt, grad_x,
-                                            reinterpret_cast<float*>(ws + lay.part)),
-                                  stream));
+    // bf16 problems run the grad_x pass on bf16 MFMA too (Gz rounded to
+    // bf16); fp32 problems on the exact three-part split of Gz
+    {
+      Timed t("feature_layout", stream);
+      TDN_HIP(tdn::launch_feature_layout(N, d, C, Gz, true, feature_parts(*p), ws + lay.xt, stream));
     }
+    Timed t("cp_edge_bwd_src", stream);
+    TDN_HIP(tdn::launch_cp_edge(edge_args(*p, off_src, perm_src, dst, src, edge_vec, D, A, B, radial_w, ws + lay.xt,
+                                          grad_x, reinterpret_cast<float*>(ws + lay.part)),
+                                stream));
   }
   return TDN_OK;
 }

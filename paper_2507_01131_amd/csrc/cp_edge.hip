@@ -1,7 +1,8 @@
 // Dispatch of the edge pass on the maximum degree L (each L is instantiated
 // in its own translation unit, cp_edge_l<L>.hip, to keep compile units
-// small), the choice of edge ranges, and the kernel that combines the
-// partial slots of segments spanning ranges.
+// small), the choice of edge ranges, the zero padding of the output factor,
+// and the kernel that combines the partial slots of segments spanning
+// ranges.
 #include "cp_edge_impl.hpp"
 
 #include <map>
@@ -81,6 +82,8 @@ int edge_ranges(int L, int R, int C, int n_radial, int E) {
 
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s) {
   using namespace edge_detail;
+  if (a.parts == 1) return launch_cp_edge_bf16(a, s);
+  if (a.parts != 3) return hipErrorInvalidValue;
   if (a.E > 0 && (a.n_range < 1 || a.n_range > a.E || !a.ef_pad)) return hipErrorInvalidValue;
   hipError_t e = hipSuccess;
   if (a.E > 0) {

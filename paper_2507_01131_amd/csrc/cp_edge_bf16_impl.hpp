@@ -4,8 +4,9 @@
 // on bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation).  The K operand
 // g_e[r] KF[k, r] is formed in fp32 and rounded to bf16 once; x is already
 // bf16.  A bf16 32x32x16 step wants eight consecutive contraction rows per
-// lane, so x is first transposed to xT[n][c][k] (k padded to 32 or 64 with
-// zeros): then one lane's operand is a single 16-byte load.  Each wave owns
+// lane, so x arrives transposed as xT[n][c][k] (k padded to 32 or 64 with
+// zeros, launch_feature_layout with one part): then one lane's operand is a
+// single 16-byte load.  Each wave owns
 // two 32-channel tiles so that every K operand built in registers feeds two
 // MFMAs.  The per-node output factor runs in fp32 as in the fp32 kernel.
 #pragma once
@@ -30,36 +31,6 @@ constexpr int kWavesMax = 4;
 template <int RT>
 constexpr int ctw() {
   return RT <= 4 ? 2 : 1;
-}
-
-__device__ __forceinline__ uint16_t to_bf16_bits(uint16_t v) { return v; }
-__device__ __forceinline__ uint16_t to_bf16_bits(float v) {
-  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));  // round to nearest even
-}
-
-// xT[n][c][k] = x[n][k][c] for k < d, 0 for d <= k < DP, as bf16 (float
-// input is rounded to nearest even).  One block per node.
-template <int DP, typename TI>
-__global__ __launch_bounds__(256) void k_transpose_bf16(int d, int C, const TI* __restrict__ x,
-                                                        uint16_t* __restrict__ xT) {
-  extern __shared__ uint16_t tile[];  // [d][C]
-  const int n = blockIdx.x;
-  const TI* src = x + size_t(n) * d * C;
-  for (int i = threadIdx.x; i < d * C; i += blockDim.x) tile[i] = to_bf16_bits(src[i]);
-  __syncthreads();
-  uint16_t* dst = xT + size_t(n) * C * DP;
-  for (int i = threadIdx.x; i < C * (DP / 8); i += blockDim.x) {
-    const int c = i / (DP / 8), g = i - c * (DP / 8);
-    uint32_t w[4];
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const int k0 = 8 * g + 2 * p, k1 = k0 + 1;
-      const uint32_t lo = k0 < d ? tile[k0 * C + c] : 0u;
-      const uint32_t hi = k1 < d ? tile[k1 * C + c] : 0u;
-      w[p] = lo | (hi << 16);
-    }
-    *reinterpret_cast<u32x4*>(dst + size_t(c) * DP + 8 * g) = u32x4{w[0], w[1], w[2], w[3]};
-  }
 }
 
 struct Bf16Smem {

@@ -68,20 +68,22 @@ __host__ __device__ constexpr int edge_dp(int d) { return d <= 32 ? 32 : 64; }
 // K-blocks of 16 degree rows per edge
 __host__ __device__ constexpr int edge_kb(int d) { return edge_dp(d) / 16; }
 
+// Bf16 parts per operand (the exact three-way split).
+constexpr int XP = 3;
+
 // Two waves per SIMD (two workgroups per CU) when the accumulators (16 RT),
-// the double-buffered feature and factor operands (48 KB) and the rest fit in
-// 256 registers without spilling in the edge loop: two K-blocks and at most
-// four rank tiles; one wave otherwise.
+// the double-buffered feature and factor operands (16 XP KB) and the rest
+// fit in 256 registers without spilling in the edge loop; one otherwise.
 __host__ __device__ constexpr int edge_waves_per_eu(int L, int RT) {
-  return edge_kb((L + 1) * (L + 1)) == 2 && RT <= 4 ? 2 : 1;
+  return 16 * RT + 16 * XP * edge_kb((L + 1) * (L + 1)) <= 160 ? 2 : 1;
 }
 
 struct EdgeSmem {
   int Rp, off_a, off_g, off_y, off_vec, off_phi, off_idx, off_bnd, floats;
 };
 
-// LDS regions (in floats): the split factor operands [KB][RT][3][64 lanes]
-// x 16 bytes, g for a chunk of edges (rows rounded up to a whole 32-row
+// LDS regions (in floats): the factor operands [KB][RT][XP][64 lanes] x 16
+// bytes, g for a chunk of edges (rows rounded up to a whole 32-row
 // tile), harmonics, normalised edge vectors with their lengths, radial basis,
 // gathered rows, and the segment starts of the chunk (positions, keys, count
 // and the two partial-segment flags).
@@ -90,7 +92,7 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, int d, int n_radial, int c
   s.Rp = RT * kTile;
   int o = 0;
   s.off_a = o;
-  o += edge_kb(d) * RT * 3 * kWave * 4;
+  o += edge_kb(d) * RT * XP * kWave * 4;
   s.off_g = o;
   o += (chunk + kTile - 1) / kTile * kTile * s.Rp;
   s.off_y = o;
@@ -145,27 +147,27 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
     const int ln = t % kWave, brt = t / kWave;
     const int b = brt / RT, rt = brt - b * RT;
     const int r = rt * kTile + (ln & 31), k0 = 16 * b + 8 * (ln >> 5);
-    uint32_t w[3][4];
+    uint32_t w[XP][4];
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
-      uint16_t part[3][2];
+      uint16_t part[XP][2];
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
         const int k = k0 + 2 * p + q;
         split_bf16x3(k < d && r < R ? a.KF[k * R + r] : 0.f, part[0][q], part[1][q], part[2][q]);
       }
 #pragma unroll
-      for (int s = 0; s < 3; ++s) w[s][p] = uint32_t(part[s][0]) | (uint32_t(part[s][1]) << 16);
+      for (int s = 0; s < XP; ++s) w[s][p] = uint32_t(part[s][0]) | (uint32_t(part[s][1]) << 16);
     }
 #pragma unroll
-    for (int s = 0; s < 3; ++s) sA[(brt * 3 + s) * kWave + ln] = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
+    for (int s = 0; s < XP; ++s) sA[(brt * XP + s) * kWave + ln] = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
   }
   __syncthreads();
   // Factor operands are read where they are used: their index goes through
   // an opaque copy (zero added in inline asm) so that the compiler does not
   // hoist all of them out of the edge loop into registers; the pointer
   // itself stays a known LDS pointer.
-  auto a_op = [&](int base, int b, int rt, int s) -> u32x4 { return sA[base + ((b * RT + rt) * 3 + s) * kWave]; };
+  auto a_op = [&](int base, int b, int rt, int s) -> u32x4 { return sA[base + ((b * RT + rt) * XP + s) * kWave]; };
 
   f32x16 acc[RT];
 #pragma unroll
@@ -229,16 +231,16 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
     for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x16{};
   };
 
-  // Feature operands of one edge: split s, K-block b is the 16-byte run
+  // Feature operands of one edge: part s, K-block b is the 16-byte run
   // xs[row][c][s][16b + 8h .. +7].  The gathered row is wave-uniform (row
   // base in scalar registers, one 32-bit lane offset per load).  Lanes with
   // c >= C read channel C - 1; their results are never stored.
   const char* __restrict__ xs = static_cast<const char*>(a.feat);
-  const uint32_t lane_off = ((uint32_t(cvalid ? c : C - 1) * 3) * DP + 8 * h) * 2;
-  auto load_x = [&](int row, u32x4 (&xb)[3][KB]) {
-    const char* p = xs + size_t(row) * (size_t(C) * 3 * DP * 2);
+  const uint32_t lane_off = ((uint32_t(cvalid ? c : C - 1) * XP) * DP + 8 * h) * 2;
+  auto load_x = [&](int row, u32x4 (&xb)[XP][KB]) {
+    const char* p = xs + size_t(row) * (size_t(C) * XP * DP * 2);
 #pragma unroll
-    for (int s = 0; s < 3; ++s)
+    for (int s = 0; s < XP; ++s)
 #pragma unroll
       for (int b = 0; b < KB; ++b)
         xb[s][b] = *reinterpret_cast<const u32x4*>(p + lane_off + uint32_t((s * DP + 16 * b) * 2));
@@ -250,16 +252,16 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
   // for tile rt-1, runs the MFMA chain of tile rt into one of two U buffers,
   // and the VALU multiply-adds of tile rt-1 from the other, so that neither
   // LDS latency nor the MFMA drain stalls the chain.
-  auto edge_compute = [&](int e, const u32x4 (&xb)[3][KB]) {
+  auto edge_compute = [&](int e, const u32x4 (&xb)[XP][KB]) {
     int ab = lane;
     asm volatile("" : "+v"(ab));
     const float* gb = sG + e * Rp + 4 * h;
-    u32x4 am[2][3][KB];  // [buffer][part][K-block]
+    u32x4 am[2][XP][KB];  // [buffer][part][K-block]
     float4 gv[4];        // [row group]
     f32x16 U[2];
     auto load_a = [&](int rt, int buf) {
 #pragma unroll
-      for (int sp = 0; sp < 3; ++sp)
+      for (int sp = 0; sp < XP; ++sp)
 #pragma unroll
         for (int b = 0; b < KB; ++b) am[buf][sp][b] = a_op(ab, b, rt, sp);
     };
@@ -408,7 +410,7 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
       // Two operand buffers used alternately: the loads of edge f+1 are
       // issued before the MFMAs of edge f, and the scheduling barriers keep
       // the compiler from sinking them next to their use.
-      u32x4 x0[3][KB], x1[3][KB];
+      u32x4 x0[XP][KB], x1[XP][KB];
       load_x(__builtin_amdgcn_readfirstlane(sIdx[e]), x0);
       int f = e;
       for (; f + 1 < pe; f += 2) {

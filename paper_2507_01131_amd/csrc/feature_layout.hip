@@ -1,0 +1,89 @@
+// Feature layout for the edge pass: x [N, d, C] becomes
+// xs [N, C, P, DP] bfloat16 with the degree index k fastest, zero padded to
+// DP = 32 (d <= 32) or 64, so that a lane of the 32x32x16 bf16 MFMA reads
+// the eight consecutive k it needs with one 16-byte load.
+//   P = 3 (fp32 problems): the exact three-way split hi/mid/lo of every fp32
+//         value, x = hi + mid + lo;
+//   P = 1 (bf16 problems): x itself (bf16 input), or an fp32 input (the
+//         backward's Gz) rounded to bf16.
+// One block per node: the node's [d, C] rows are staged in LDS, then each
+// thread writes groups of eight k for one channel and all P parts.
+#include "common.hpp"
+#include "kernels.h"
+
+namespace tdn {
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
+
+template <int DP, int P, typename TI>
+__global__ __launch_bounds__(256) void k_feature_layout(int d, int C, const TI* __restrict__ x,
+                                                        uint16_t* __restrict__ xs) {
+  extern __shared__ float tile[];  // [d][C]
+  const int n = blockIdx.x;
+  const TI* src = x + size_t(n) * d * C;
+  for (int i = threadIdx.x; i < d * C; i += blockDim.x) tile[i] = to_f32(src[i]);
+  __syncthreads();
+  uint16_t* dst = xs + size_t(n) * C * P * DP;
+  for (int i = threadIdx.x; i < C * (DP / 8); i += blockDim.x) {
+    const int c = i / (DP / 8), g = i - c * (DP / 8);
+    uint32_t w[P][4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      uint16_t part[3][2];
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int k = 8 * g + 2 * p + q;
+        const float v = k < d ? tile[k * C + c] : 0.f;
+        if constexpr (P == 3)
+          split_bf16x3(v, part[0][q], part[1][q], part[2][q]);
+        else
+          part[0][q] = bf16_rne_bits(v);  // exact for bf16 input
+      }
+#pragma unroll
+      for (int s = 0; s < P; ++s) w[s][p] = uint32_t(part[s][0]) | (uint32_t(part[s][1]) << 16);
+    }
+#pragma unroll
+    for (int s = 0; s < P; ++s)
+      *reinterpret_cast<u32x4*>(dst + (size_t(c) * P + s) * DP + 8 * g) = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
+  }
+}
+
+template <int DP, int P, typename TI>
+hipError_t launch_dp(int N, int d, int C, const TI* x, uint16_t* xs, hipStream_t s) {
+  const size_t lds = size_t(d) * C * 4;
+  auto k = k_feature_layout<DP, P, TI>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     int(lds));
+  if (e != hipSuccess) return e;
+  k<<<dim3(N), dim3(256), lds, s>>>(d, C, x, xs);
+  return hipGetLastError();
+}
+
+template <int P, typename TI>
+hipError_t launch_p(int N, int d, int C, const TI* x, void* xs, hipStream_t s) {
+  uint16_t* o = static_cast<uint16_t*>(xs);
+  return edge_kpad(d) == 32 ? launch_dp<32, P>(N, d, C, x, o, s) : launch_dp<64, P>(N, d, C, x, o, s);
+}
+
+}  // namespace
+
+int edge_kpad(int d) { return d <= 32 ? 32 : 64; }
+
+hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,
+                                 hipStream_t s) {
+  if (N == 0) return hipSuccess;
+  if (parts == 3) {
+    if (!x_is_f32) return hipErrorInvalidValue;
+    return launch_p<3>(N, d, C, static_cast<const float*>(x), xs, s);
+  }
+  if (parts != 1) return hipErrorInvalidValue;
+  return x_is_f32 ? launch_p<1>(N, d, C, static_cast<const float*>(x), xs, s)
+                  : launch_p<1>(N, d, C, static_cast<const uint16_t*>(x), xs, s);
+}
+
+}  // namespace tdn

@@ -31,9 +31,9 @@ hipError_t launch_validate(int N, int E, const int32_t* edge_index, const float*
 //   out[seg] = EF H_seg                                       ([d, C])
 // forward:        KF = A, EF = D, feat = x,  gather = src, key = dst
 // grad_x pass:    KF = D, EF = A, feat = Gz, gather = dst, key = src
-// The fp32 pass splits the sorted edges into n_range equal ranges (one
-// workgroup each per channel group); segments spanning ranges are summed
-// from `partial` ([n_range, 2, d, C] floats of workspace).
+// The pass splits the sorted edges into n_range equal ranges (one workgroup
+// each per channel group); segments spanning ranges are summed from
+// `partial` ([n_range, 2, d, C] floats of workspace).
 struct EdgeArgs {
   int n_seg, E, L, d, C, R, n_radial;
   float sigma;               // r_cut / (n_radial - 1)
@@ -48,25 +48,27 @@ struct EdgeArgs {
   const float* radial_w;     // [n_radial, R]
   const void* feat;          // [n_feat_rows, d, C]
   float* out;                // [n_seg, d, C]
-  int n_range;               // edge ranges (fp32 pass), from edge_ranges
-  float* partial;            // [n_range, 2, d, C]
-  float* ef_pad;             // [d, RT*32] fp32 pass: EF zero-padded (workspace, written by launch_cp_edge)
+  int n_range;               // edge ranges, from edge_ranges
+  float* partial;            // [n_range, 2, d, C] workspace
+  float* ef_pad;             // [d, RT*32] workspace: EF zero-padded (written by launch_cp_edge)
+  int parts;                 // bf16 parts per feature in feat (3: fp32 features, 1: bf16 features)
 };
 // Edge ranges of the fp32 pass for this problem on the current device: the
 // number of workgroups the device holds at once, over the channel groups,
 // capped at E (0 when E = 0).
 int edge_ranges(int L, int R, int C, int n_radial, int E);
-// fp32 features for the fp32 pass: x [N, d, C] -> xs [N, C, 3, x3_kpad(d)]
-// bfloat16, the exact split x = hi + mid + lo along the last axis groups
-// (EdgeArgs::feat = xs); x3_kpad(d) = 32 for d <= 32, else 64.
-int x3_kpad(int d);
-hipError_t launch_split_x3(int N, int d, int C, const float* x, void* xs, hipStream_t s);
+// Features for the edge pass: x [N, d, C] -> xs [N, C, parts, edge_kpad(d)]
+// bfloat16 (k fastest, zero padded; EdgeArgs::feat = xs): parts = 3 holds
+// the exact split x = hi + mid + lo of fp32 features, parts = 1 holds bf16
+// features (an fp32 input is rounded to bf16).  edge_kpad(d) = 32 for
+// d <= 32, else 64.
+int edge_kpad(int d);
+hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,
+                                 hipStream_t s);
+// parts = 3: the fp32 pass below; parts = 1: launch_cp_edge_bf16
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
-// bfloat16 features: x [N, d, C] (bf16, or float rounded to bf16) is first
-// transposed to xT [N, C, kpad(d)] (kpad = 32 for d <= 32, else 64; zero
-// padded), which the bf16 edge pass gathers (EdgeArgs::feat = xT).
-int bf16_kpad(int d);
-hipError_t launch_transpose_bf16(int N, int d, int C, const void* x, bool x_is_f32, void* xT, hipStream_t s);
+// bf16 features (feat = xs with one part): one workgroup per segment and
+// channel group, K operand g * KF rounded to bf16 (no ranges or partials)
 hipError_t launch_cp_edge_bf16(const EdgeArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- node GEMMs
