@@ -45,6 +45,9 @@ __global__ __launch_bounds__(256) void k_pad_rows(int rows, int R, int Rp, const
   dst[i] = r < R ? src[k * R + r] : 0.f;
 }
 
+constexpr int kRangesPerBlock = 2;
+constexpr int kMinRangeEdges = 48;
+
 int device_cus() {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 256;
@@ -63,9 +66,9 @@ int device_cus() {
 }  // namespace
 }  // namespace edge_detail
 
-int edge_ranges(int L, int R, int C, int n_radial, int E) {
+EdgePlan edge_plan(int L, int R, int C, int n_radial, int E) {
   using namespace edge_detail;
-  if (E <= 0) return 0;
+  if (E <= 0) return EdgePlan{0, 0};
   const int ntiles = (C + kTile - 1) / kTile;
   const int n_cgrp = (ntiles + kMaxWavesPerBlock - 1) / kMaxWavesPerBlock;
   const int RT = (R + kTile - 1) / kTile, d = (L + 1) * (L + 1);
@@ -75,16 +78,22 @@ int edge_ranges(int L, int R, int C, int n_radial, int E) {
   int per_cu = 160 * 1024 / lds;
   const int by_waves = 4 * edge_waves_per_eu(L, RT) / waves;
   if (per_cu > by_waves) per_cu = by_waves;
-  const int resident = device_cus() * (per_cu < 1 ? 1 : per_cu);
-  const int n = resident / n_cgrp;
-  return n < 1 ? 1 : (n > E ? E : n);
+  int nb = device_cus() * (per_cu < 1 ? 1 : per_cu) / n_cgrp;
+  nb = nb < 1 ? 1 : (nb > E ? E : nb);
+  // ranges per workgroup: kRangesPerBlock while each range keeps at least
+  // kMinRangeEdges edges
+  int S = E / (nb * kMinRangeEdges);
+  S = S < 1 ? 1 : (S > kRangesPerBlock ? kRangesPerBlock : S);
+  return EdgePlan{nb * S, S};
 }
 
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s) {
   using namespace edge_detail;
   if (a.parts == 1) return launch_cp_edge_bf16(a, s);
   if (a.parts != 3) return hipErrorInvalidValue;
-  if (a.E > 0 && (a.n_range < 1 || a.n_range > a.E || !a.ef_pad)) return hipErrorInvalidValue;
+  if (a.E > 0 && (a.n_range < 1 || a.n_range > a.E || a.pieces_per_block < 1 || a.n_range % a.pieces_per_block ||
+                  !a.ef_pad))
+    return hipErrorInvalidValue;
   hipError_t e = hipSuccess;
   if (a.E > 0) {
     const int Rp = (a.R + kTile - 1) / kTile * kTile;

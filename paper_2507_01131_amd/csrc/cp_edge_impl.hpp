@@ -130,10 +130,9 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
   int* sBndKey = sBnd + chunk;                          // [chunk] that segment
   int* sMeta = sBndKey + chunk;                         // start count, first partial, last partial
 
-  const int total = a.n_range * n_cgrp;
-  const int logical = xcd_remap(blockIdx.x, total);
-  const int range = logical / n_cgrp, cgrp = logical - range * n_cgrp;
-  const int e_lo = int(int64_t(range) * a.E / a.n_range), e_hi = int(int64_t(range + 1) * a.E / a.n_range);
+  const int n_blocks = a.n_range / a.pieces_per_block;
+  const int logical = xcd_remap(blockIdx.x, n_blocks * n_cgrp);
+  const int slot = logical / n_cgrp, cgrp = logical - slot * n_cgrp;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int h = lane >> 5, l32 = lane & 31;
   const int C = a.C, nr = a.n_radial, R = a.R;
@@ -180,10 +179,11 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
   // the registers.  The A operand (EF, read from global memory, where it
   // stays cached) comes in groups of 16 values, one group per (row tile mt,
   // rank tile rt), the next group loaded while the current one's MFMAs run.
-  // slot < 0 writes the segment's output row, slot 0 or 1 the range's partial
-  // slot; the accumulators restart from zero.
-  auto finish = [&](int seg, int slot) {
-    float* dst = slot < 0 ? a.out + size_t(seg) * d * C : a.partial + (size_t(range) * 2 + slot) * d * C;
+  // part < 0 writes the segment's output row, part 0 or 1 the range's
+  // partial slot; the accumulators restart from zero.
+  int range = 0;
+  auto finish = [&](int seg, int part) {
+    float* dst = part < 0 ? a.out + size_t(seg) * d * C : a.partial + (size_t(range) * 2 + part) * d * C;
     constexpr int NG = MT * RT;
     // EF zero-padded to [d][Rp] (ef_pad): a lane's 16 values of a group sit
     // at fixed offsets from one row pointer
@@ -308,126 +308,132 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
     fma_rt(RT - 1, (RT - 1) & 1);
   };
 
-  int cur = -1;           // segment in the accumulators
-  bool first_seg = true;  // cur is the range's first segment
-  int first_partial = 0, last_partial = 0;
-  for (int cb = e_lo; cb < e_hi; cb += chunk) {
-    const int n = min(chunk, e_hi - cb);
-    __syncthreads();  // factors staged / previous chunk consumed
-    // wave 0, one lane per edge: gathered row, unit direction and length,
-    // and the segment starts (a key differing from the previous edge's, and
-    // the range's first edge)
-    if (wave == 0) {
-      const int t = lane;
-      int key = -1;
-      if (t < n) {
-        const int eid = a.perm[cb + t];
-        sIdx[t] = a.gather[eid];
-        key = a.key[eid];
-        const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
-        const float len = sqrtf(vx * vx + vy * vy + vz * vz);
-        const float inv = 1.f / len;
-        sVec[t] = make_float4(vx * inv, vy * inv, vz * inv, len);
-      }
-      int prev = __shfl_up(key, 1);
-      if (t == 0) prev = cb > 0 ? a.key[a.perm[cb - 1]] : -1;
-      const int last_key = __shfl(key, n - 1);
-      const bool start = t < n && (key != prev || (cb == e_lo && t == 0));
-      const unsigned long long m = __ballot(start);
-      if (start) {
-        const int pos = __popcll(m & ((1ull << t) - 1));
-        sBnd[pos] = t;
-        sBndKey[pos] = key;
-      }
-      if (t == 0) {
-        sMeta[0] = __popcll(m);
-        sMeta[1] = cb == e_lo && cb > 0 && key == prev;
-        sMeta[2] = cb + n == e_hi && e_hi < a.E && a.key[a.perm[e_hi]] == last_key;
-      }
-    }
-    __syncthreads();
-    // harmonics: one thread per (edge, order m) column; radial basis: one
-    // thread per (edge, function)
-    for (int t = tid; t < n * (L + 1); t += blockDim.x) {
-      const int e = t / (L + 1), m = t - e * (L + 1);
-      const float4 u = sVec[e];
-      sh_unit_column(L, m, u.x, u.y, u.z, sY + e * d);
-    }
-    for (int t = tid; t < n * nr; t += blockDim.x) {
-      const int e = t / nr, q = t - e * nr;
-      sPhi[t] = radial_phi(sVec[e].w, q, a.sigma);
-    }
-    __syncthreads();
-    // g = (Y B) * (Phi Wrad) for the chunk's edges (rows) and all ranks
-    // (columns): two small fp32 MFMA GEMMs per 32x32 tile, one rank tile per
-    // wave, with B and Wrad read from global memory (cached).  Rows beyond n
-    // hold zeros (their A operand is masked) and are never read.
-    const int n_et = (n + kTile - 1) / kTile;
-    for (int item = wave; item < n_et * RT; item += waves) {
-      const int et = item / RT, rt = item - et * RT;
-      const int er = et * kTile + l32;  // this lane's edge row
-      const bool row_ok = er < n;
-      const int r = rt * kTile + l32, rc = r < R ? r : R - 1;
-      f32x16 Tr = f32x16{}, Ty = f32x16{};
-#pragma unroll 1
-      for (int s2 = 0; s2 < (nr + 1) / 2; ++s2) {
-        const int q = 2 * s2 + h, qc = q < nr ? q : nr - 1;
-        const float av = (row_ok && q < nr) ? sPhi[er * nr + q] : 0.f;
-        const float bw = a.radial_w[qc * R + rc];
-        Tr = mfma32(av, (q < nr && r < R) ? bw : 0.f, Tr);
-      }
-#pragma unroll
-      for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
-        const int k = 2 * s2 + h, kc = k < d ? k : d - 1;
-        const float av = (row_ok && k < d) ? sY[er * d + k] : 0.f;
-        const float bw = a.Bf[kc * R + rc];
-        Ty = mfma32(av, (k < d && r < R) ? bw : 0.f, Ty);
-      }
-#pragma unroll
-      for (int v = 0; v < 16; ++v) sG[(et * kTile + acc_row(v, h)) * Rp + rt * kTile + l32] = Tr[v] * Ty[v];
-    }
-    __syncthreads();
-
-    const int nb = __builtin_amdgcn_readfirstlane(sMeta[0]);
-    if (cb == e_lo) first_partial = __builtin_amdgcn_readfirstlane(sMeta[1]);
-    if (cb + n == e_hi) last_partial = __builtin_amdgcn_readfirstlane(sMeta[2]);
-    int bi = 0;
-    int next = nb > 0 ? __builtin_amdgcn_readfirstlane(sBnd[0]) : n;
-    // The chunk in pieces that each lie in one segment; the segment in the
-    // accumulators is closed where the next one starts, before any operand
-    // of the next piece is loaded.
-    for (int e = 0; e < n;) {
-      if (e == next) {
-        if (cur >= 0) {
-          finish(cur, first_seg && first_partial ? 0 : -1);
-          first_seg = false;
+  // The workgroup's ranges are slot, slot + n_blocks, ...: at any time the
+  // workgroups of one XCD work on neighbouring edges.
+  for (int sp = 0; sp < a.pieces_per_block; ++sp) {
+    range = sp * n_blocks + slot;
+    const int e_lo = int(int64_t(range) * a.E / a.n_range), e_hi = int(int64_t(range + 1) * a.E / a.n_range);
+    int cur = -1;           // segment in the accumulators
+    bool first_seg = true;  // cur is the range's first segment
+    int first_partial = 0, last_partial = 0;
+    for (int cb = e_lo; cb < e_hi; cb += chunk) {
+      const int n = min(chunk, e_hi - cb);
+      __syncthreads();  // factors staged / previous chunk consumed
+      // wave 0, one lane per edge: gathered row, unit direction and length,
+      // and the segment starts (a key differing from the previous edge's, and
+      // the range's first edge)
+      if (wave == 0) {
+        const int t = lane;
+        int key = -1;
+        if (t < n) {
+          const int eid = a.perm[cb + t];
+          sIdx[t] = a.gather[eid];
+          key = a.key[eid];
+          const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
+          const float len = sqrtf(vx * vx + vy * vy + vz * vz);
+          const float inv = 1.f / len;
+          sVec[t] = make_float4(vx * inv, vy * inv, vz * inv, len);
         }
-        cur = __builtin_amdgcn_readfirstlane(sBndKey[bi]);
-        ++bi;
-        next = bi < nb ? __builtin_amdgcn_readfirstlane(sBnd[bi]) : n;
+        int prev = __shfl_up(key, 1);
+        if (t == 0) prev = cb > 0 ? a.key[a.perm[cb - 1]] : -1;
+        const int last_key = __shfl(key, n - 1);
+        const bool start = t < n && (key != prev || (cb == e_lo && t == 0));
+        const unsigned long long m = __ballot(start);
+        if (start) {
+          const int pos = __popcll(m & ((1ull << t) - 1));
+          sBnd[pos] = t;
+          sBndKey[pos] = key;
+        }
+        if (t == 0) {
+          sMeta[0] = __popcll(m);
+          sMeta[1] = cb == e_lo && cb > 0 && key == prev;
+          sMeta[2] = cb + n == e_hi && e_hi < a.E && a.key[a.perm[e_hi]] == last_key;
+        }
       }
-      const int pe = next;
-      // Two operand buffers used alternately: the loads of edge f+1 are
-      // issued before the MFMAs of edge f, and the scheduling barriers keep
-      // the compiler from sinking them next to their use.
-      u32x4 x0[XP][KB], x1[XP][KB];
-      load_x(__builtin_amdgcn_readfirstlane(sIdx[e]), x0);
-      int f = e;
-      for (; f + 1 < pe; f += 2) {
-        load_x(__builtin_amdgcn_readfirstlane(sIdx[f + 1]), x1);
-        __builtin_amdgcn_sched_barrier(0);
-        edge_compute(f, x0);
-        __builtin_amdgcn_sched_barrier(0);
-        load_x(__builtin_amdgcn_readfirstlane(sIdx[f + 2 < pe ? f + 2 : f + 1]), x0);  // past the end: unused
-        __builtin_amdgcn_sched_barrier(0);
-        edge_compute(f + 1, x1);
-        __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+      // harmonics: one thread per (edge, order m) column; radial basis: one
+      // thread per (edge, function)
+      for (int t = tid; t < n * (L + 1); t += blockDim.x) {
+        const int e = t / (L + 1), m = t - e * (L + 1);
+        const float4 u = sVec[e];
+        sh_unit_column(L, m, u.x, u.y, u.z, sY + e * d);
       }
-      if (f < pe) edge_compute(f, x0);
-      e = pe;
+      for (int t = tid; t < n * nr; t += blockDim.x) {
+        const int e = t / nr, q = t - e * nr;
+        sPhi[t] = radial_phi(sVec[e].w, q, a.sigma);
+      }
+      __syncthreads();
+      // g = (Y B) * (Phi Wrad) for the chunk's edges (rows) and all ranks
+      // (columns): two small fp32 MFMA GEMMs per 32x32 tile, one rank tile per
+      // wave, with B and Wrad read from global memory (cached).  Rows beyond n
+      // hold zeros (their A operand is masked) and are never read.
+      const int n_et = (n + kTile - 1) / kTile;
+      for (int item = wave; item < n_et * RT; item += waves) {
+        const int et = item / RT, rt = item - et * RT;
+        const int er = et * kTile + l32;  // this lane's edge row
+        const bool row_ok = er < n;
+        const int r = rt * kTile + l32, rc = r < R ? r : R - 1;
+        f32x16 Tr = f32x16{}, Ty = f32x16{};
+  #pragma unroll 1
+        for (int s2 = 0; s2 < (nr + 1) / 2; ++s2) {
+          const int q = 2 * s2 + h, qc = q < nr ? q : nr - 1;
+          const float av = (row_ok && q < nr) ? sPhi[er * nr + q] : 0.f;
+          const float bw = a.radial_w[qc * R + rc];
+          Tr = mfma32(av, (q < nr && r < R) ? bw : 0.f, Tr);
+        }
+  #pragma unroll
+        for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
+          const int k = 2 * s2 + h, kc = k < d ? k : d - 1;
+          const float av = (row_ok && k < d) ? sY[er * d + k] : 0.f;
+          const float bw = a.Bf[kc * R + rc];
+          Ty = mfma32(av, (k < d && r < R) ? bw : 0.f, Ty);
+        }
+  #pragma unroll
+        for (int v = 0; v < 16; ++v) sG[(et * kTile + acc_row(v, h)) * Rp + rt * kTile + l32] = Tr[v] * Ty[v];
+      }
+      __syncthreads();
+
+      const int nb = __builtin_amdgcn_readfirstlane(sMeta[0]);
+      if (cb == e_lo) first_partial = __builtin_amdgcn_readfirstlane(sMeta[1]);
+      if (cb + n == e_hi) last_partial = __builtin_amdgcn_readfirstlane(sMeta[2]);
+      int bi = 0;
+      int next = nb > 0 ? __builtin_amdgcn_readfirstlane(sBnd[0]) : n;
+      // The chunk in pieces that each lie in one segment; the segment in the
+      // accumulators is closed where the next one starts, before any operand
+      // of the next piece is loaded.
+      for (int e = 0; e < n;) {
+        if (e == next) {
+          if (cur >= 0) {
+            finish(cur, first_seg && first_partial ? 0 : -1);
+            first_seg = false;
+          }
+          cur = __builtin_amdgcn_readfirstlane(sBndKey[bi]);
+          ++bi;
+          next = bi < nb ? __builtin_amdgcn_readfirstlane(sBnd[bi]) : n;
+        }
+        const int pe = next;
+        // Two operand buffers used alternately: the loads of edge f+1 are
+        // issued before the MFMAs of edge f, and the scheduling barriers keep
+        // the compiler from sinking them next to their use.
+        u32x4 x0[XP][KB], x1[XP][KB];
+        load_x(__builtin_amdgcn_readfirstlane(sIdx[e]), x0);
+        int f = e;
+        for (; f + 1 < pe; f += 2) {
+          load_x(__builtin_amdgcn_readfirstlane(sIdx[f + 1]), x1);
+          __builtin_amdgcn_sched_barrier(0);
+          edge_compute(f, x0);
+          __builtin_amdgcn_sched_barrier(0);
+          load_x(__builtin_amdgcn_readfirstlane(sIdx[f + 2 < pe ? f + 2 : f + 1]), x0);  // past the end: unused
+          __builtin_amdgcn_sched_barrier(0);
+          edge_compute(f + 1, x1);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        if (f < pe) edge_compute(f, x0);
+        e = pe;
+      }
     }
+    if (cur >= 0) finish(cur, first_seg && first_partial ? 0 : (last_partial ? 1 : -1));
   }
-  if (cur >= 0) finish(cur, first_seg && first_partial ? 0 : (last_partial ? 1 : -1));
 }
 
 // Edge chunk of a block: the largest power of two <= 64 (at least 8) whose
@@ -453,7 +459,7 @@ hipError_t launch_l_rt(const EdgeArgs& a, hipStream_t s) {
     hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
-    k<<<dim3(a.n_range * n_cgrp), dim3(waves * kWave), lds, s>>>(a, n_cgrp, waves, chunk);
+    k<<<dim3(a.n_range / a.pieces_per_block * n_cgrp), dim3(waves * kWave), lds, s>>>(a, n_cgrp, waves, chunk);
   }
   return hipGetLastError();
 }

@@ -31,9 +31,9 @@ hipError_t launch_validate(int N, int E, const int32_t* edge_index, const float*
 //   out[seg] = EF H_seg                                       ([d, C])
 // forward:        KF = A, EF = D, feat = x,  gather = src, key = dst
 // grad_x pass:    KF = D, EF = A, feat = Gz, gather = dst, key = src
-// The pass splits the sorted edges into n_range equal ranges (one workgroup
-// each per channel group); segments spanning ranges are summed from
-// `partial` ([n_range, 2, d, C] floats of workspace).
+// The fp32 pass splits the sorted edges into n_range equal ranges, several
+// per workgroup; segments spanning ranges are summed from `partial`
+// ([n_range, 2, d, C] floats of workspace).
 struct EdgeArgs {
   int n_seg, E, L, d, C, R, n_radial;
   float sigma;               // r_cut / (n_radial - 1)
@@ -48,15 +48,20 @@ struct EdgeArgs {
   const float* radial_w;     // [n_radial, R]
   const void* feat;          // [n_feat_rows, d, C]
   float* out;                // [n_seg, d, C]
-  int n_range;               // edge ranges, from edge_ranges
+  int n_range;               // edge ranges (EdgePlan::n_range)
+  int pieces_per_block;      // ranges per workgroup (EdgePlan::per_block)
   float* partial;            // [n_range, 2, d, C] workspace
   float* ef_pad;             // [d, RT*32] workspace: EF zero-padded (written by launch_cp_edge)
   int parts;                 // bf16 parts per feature in feat (3: fp32 features, 1: bf16 features)
 };
-// Edge ranges of the fp32 pass for this problem on the current device: the
-// number of workgroups the device holds at once, over the channel groups,
-// capped at E (0 when E = 0).
-int edge_ranges(int L, int R, int C, int n_radial, int E);
+// Edge ranges of the fp32 pass for this problem on the current device:
+// n_range = per_block x the number of workgroups the device holds at once
+// over the channel groups (capped at E; 0 when E = 0).  Workgroup b takes
+// ranges b, b + n_range / per_block, ...
+struct EdgePlan {
+  int n_range, per_block;
+};
+EdgePlan edge_plan(int L, int R, int C, int n_radial, int E);
 // Features for the edge pass: x [N, d, C] -> xs [N, C, parts, edge_kpad(d)]
 // bfloat16 (k fastest, zero padded; EdgeArgs::feat = xs): parts = 3 holds
 // the exact split x = hi + mid + lo of fp32 features, parts = 1 holds bf16
