@@ -73,7 +73,10 @@ typedef struct {
   tdn_dtype feat_dtype; /* dtype of x and W (TDN_F32 or TDN_BF16); all else f32.
                            With TDN_BF16 the edge contractions run on bf16 MFMA:
                            the K operand g*A (and, in the backward, G W^T) is
-                           rounded to bf16, accumulation stays fp32            */
+                           rounded to bf16, accumulation stays fp32.  With
+                           TDN_F32 results keep fp32 accuracy (the edge
+                           contraction uses bf16 MFMA only on exact three-part
+                           splits of both operands)                          */
   int32_t edges_sorted; /* 1: edge_index already stably sorted by dst (perm is the
                            identity); 0: the call sorts                            */
   int32_t validate;     /* 1: check indices, order and edge vectors on the device */
