@@ -63,8 +63,8 @@ size_t xt_bytes(const tdn_problem& p) {
 // its zero-padded output factor [d, RT*32]
 size_t ef_pad_bytes(const tdn_problem& p) { return al(size_t(dim_of(p.L)) * ((p.R + 31) / 32 * 32) * 4); }
 size_t partial_bytes(const tdn_problem& p) {
-  if (p.feat_dtype == TDN_BF16) return 0;
-  return ef_pad_bytes(p) + size_t(tdn::edge_plan(p.L, p.R, p.C, p.n_radial, p.n_edges).n_range) * 2 * dim_of(p.L) * p.C * 4;
+  const tdn::EdgePlan pl = tdn::edge_plan(p.L, p.R, p.C, p.n_radial, p.feat_dtype == TDN_BF16, p.n_edges);
+  return ef_pad_bytes(p) + size_t(pl.n_range) * 2 * dim_of(p.L) * p.C * 4;
 }
 
 struct FwdLayout {
@@ -206,8 +206,7 @@ tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int3
   a.radial_w = radial_w;
   a.feat = feat;
   a.out = out;
-  const tdn::EdgePlan pl =
-      p.feat_dtype == TDN_BF16 ? tdn::EdgePlan{0, 0} : tdn::edge_plan(p.L, p.R, p.C, p.n_radial, p.n_edges);
+  const tdn::EdgePlan pl = tdn::edge_plan(p.L, p.R, p.C, p.n_radial, p.feat_dtype == TDN_BF16, p.n_edges);
   a.n_range = pl.n_range;
   a.pieces_per_block = pl.per_block;
   a.ef_pad = partial;

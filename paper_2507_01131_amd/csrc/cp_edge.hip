@@ -45,7 +45,6 @@ __global__ __launch_bounds__(256) void k_pad_rows(int rows, int R, int Rp, const
   dst[i] = r < R ? src[k * R + r] : 0.f;
 }
 
-constexpr int kRangesPerBlock = 2;
 constexpr int kMinRangeEdges = 48;
 
 int device_cus() {
@@ -66,31 +65,29 @@ int device_cus() {
 }  // namespace
 }  // namespace edge_detail
 
-EdgePlan edge_plan(int L, int R, int C, int n_radial, int E) {
+EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E) {
   using namespace edge_detail;
   if (E <= 0) return EdgePlan{0, 0};
-  const int ntiles = (C + kTile - 1) / kTile;
-  const int n_cgrp = (ntiles + kMaxWavesPerBlock - 1) / kMaxWavesPerBlock;
   const int RT = (R + kTile - 1) / kTile, d = (L + 1) * (L + 1);
+  const EdgeGrid gr = edge_grid(C, RT, bf16);
   // workgroups per CU: as many as the wave slots (four SIMDs) and LDS allow
-  const int waves = ntiles < kMaxWavesPerBlock ? ntiles : kMaxWavesPerBlock;
-  const int lds = edge_smem(RT, d, n_radial, edge_chunk(L, RT, n_radial)).floats * 4;
+  const int lds = edge_smem(RT, bf16, d, n_radial, edge_chunk(L, RT, bf16, n_radial)).floats * 4;
   int per_cu = 160 * 1024 / lds;
-  const int by_waves = 4 * edge_waves_per_eu(L, RT) / waves;
+  const int by_waves = 4 * edge_waves_per_eu(L, RT, bf16) / gr.waves;
   if (per_cu > by_waves) per_cu = by_waves;
-  int nb = device_cus() * (per_cu < 1 ? 1 : per_cu) / n_cgrp;
+  int nb = device_cus() * (per_cu < 1 ? 1 : per_cu) / gr.n_cgrp;
   nb = nb < 1 ? 1 : (nb > E ? E : nb);
-  // ranges per workgroup: kRangesPerBlock while each range keeps at least
-  // kMinRangeEdges edges
+  // ranges per workgroup: up to edge_max_ranges while each range keeps at
+  // least kMinRangeEdges edges
+  const int smax = edge_max_ranges(L, RT, bf16);
   int S = E / (nb * kMinRangeEdges);
-  S = S < 1 ? 1 : (S > kRangesPerBlock ? kRangesPerBlock : S);
+  S = S < 1 ? 1 : (S > smax ? smax : S);
   return EdgePlan{nb * S, S};
 }
 
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s) {
   using namespace edge_detail;
-  if (a.parts == 1) return launch_cp_edge_bf16(a, s);
-  if (a.parts != 3) return hipErrorInvalidValue;
+  if (a.parts != 1 && a.parts != 3) return hipErrorInvalidValue;
   if (a.E > 0 && (a.n_range < 1 || a.n_range > a.E || a.pieces_per_block < 1 || a.n_range % a.pieces_per_block ||
                   !a.ef_pad))
     return hipErrorInvalidValue;

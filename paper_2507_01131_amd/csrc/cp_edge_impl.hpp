@@ -63,36 +63,60 @@ __device__ __forceinline__ f32x16 mfma_bf16(u32x4 a, u32x4 b, f32x16 c) {
 
 constexpr int kMaxWavesPerBlock = 4;
 
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return uint32_t(bf16_rne_bits(lo)) | (uint32_t(bf16_rne_bits(hi)) << 16);
+}
+
 __host__ __device__ constexpr int edge_dp(int d) { return d <= 32 ? 32 : 64; }
 
 // K-blocks of 16 degree rows per edge
 __host__ __device__ constexpr int edge_kb(int d) { return edge_dp(d) / 16; }
 
-// Bf16 parts per operand (the exact three-way split).
-constexpr int XP = 3;
+// Two modes of the edge contraction:
+//  split (fp32 features): U_e = KF^T x from six exact bf16 part products,
+//    then acc += g * U_e; one 32-channel tile per wave;
+//  bf16 (bf16 features): the K operand g_e[r] KF[k, r] is formed in fp32 and
+//    rounded to bf16, one MFMA per K-block straight into acc; two channel
+//    tiles per wave (while R <= 128) so every K operand feeds two MFMAs.
+// Bf16 parts per feature value and channel tiles per wave:
+__host__ __device__ constexpr int edge_xp(bool bf) { return bf ? 1 : 3; }
+__host__ __device__ constexpr int edge_ct(bool bf, int RT) { return bf && RT <= 4 ? 2 : 1; }
 
-// Two waves per SIMD (two workgroups per CU) when the accumulators (16 RT),
-// the double-buffered feature and factor operands (16 XP KB) and the rest
-// fit in 256 registers without spilling in the edge loop; one otherwise.
-__host__ __device__ constexpr int edge_waves_per_eu(int L, int RT) {
-  return 16 * RT + 16 * XP * edge_kb((L + 1) * (L + 1)) <= 160 ? 2 : 1;
+// Two waves per SIMD (two workgroups per CU) when the accumulators and the
+// double-buffered operands fit in 256 registers without spilling in the edge
+// loop; one otherwise.
+__host__ __device__ constexpr int edge_waves_per_eu(int L, int RT, bool bf) {
+  return bf ? (16 * RT * edge_ct(bf, RT) + 8 * edge_ct(bf, RT) * edge_kb((L + 1) * (L + 1)) <= 144 ? 2 : 1)
+            : (16 * RT + 48 * edge_kb((L + 1) * (L + 1)) <= 160 ? 2 : 1);
 }
+
+// Most ranges a workgroup takes: two where two workgroups share a CU (their
+// gathered rows then stay in L2), one otherwise (the extra loop level costs
+// registers that a one-wave kernel spends on accumulators).
+__host__ __device__ constexpr int edge_max_ranges(int L, int RT, bool bf) {
+  return edge_waves_per_eu(L, RT, bf) == 2 ? 2 : 1;
+}
+
+// bf16 mode: whether this lane's K factor values (KB * RT * 8 floats) stay
+// in registers instead of LDS.
+__host__ __device__ constexpr bool edge_reg_kf(int d, int RT) { return edge_kb(d) * RT * 8 <= 64; }
 
 struct EdgeSmem {
   int Rp, off_a, off_g, off_y, off_vec, off_phi, off_idx, off_bnd, floats;
 };
 
-// LDS regions (in floats): the factor operands [KB][RT][XP][64 lanes] x 16
-// bytes, g for a chunk of edges (rows rounded up to a whole 32-row
+// LDS regions (in floats): the factor operands, split mode
+// [KB][RT][3 parts][64 lanes] x 16 bytes of bf16, bf16 mode
+// [KB][RT][64 lanes] x 32 bytes of fp32, g for a chunk of edges (rows rounded up to a whole 32-row
 // tile), harmonics, normalised edge vectors with their lengths, radial basis,
 // gathered rows, and the segment starts of the chunk (positions, keys, count
 // and the two partial-segment flags).
-__host__ __device__ inline EdgeSmem edge_smem(int RT, int d, int n_radial, int chunk) {
+__host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radial, int chunk) {
   EdgeSmem s{};
   s.Rp = RT * kTile;
   int o = 0;
   s.off_a = o;
-  o += edge_kb(d) * RT * XP * kWave * 4;
+  o += edge_kb(d) * RT * (bf ? 2 : 3) * kWave * 4;
   s.off_g = o;
   o += (chunk + kTile - 1) / kTile * kTile * s.Rp;
   s.off_y = o;
@@ -110,17 +134,22 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, int d, int n_radial, int c
   return s;
 }
 
-template <int L, int RT>
-__global__ __launch_bounds__(kMaxWavesPerBlock* kWave) __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT))))
-void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
+template <int L, int RT, bool BF>
+__global__ __launch_bounds__(kMaxWavesPerBlock* kWave)
+__attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edge(EdgeArgs a, int n_cgrp, int waves,
+                                                                                  int chunk) {
+  constexpr int XP = edge_xp(BF);
+  constexpr int CT = edge_ct(BF, RT);
+  constexpr int kMaxRanges = edge_max_ranges(L, RT, BF);
   constexpr int d = (L + 1) * (L + 1);
   constexpr int DP = edge_dp(d);
   constexpr int KB = edge_kb(d);
   constexpr int Rp = RT * kTile;
   constexpr int MT = (d + kTile - 1) / kTile;
   extern __shared__ float smem[];
-  const EdgeSmem S = edge_smem(RT, d, a.n_radial, chunk);
+  const EdgeSmem S = edge_smem(RT, BF, d, a.n_radial, chunk);
   u32x4* sA = reinterpret_cast<u32x4*>(smem + S.off_a);
+  float4* sAf = reinterpret_cast<float4*>(smem + S.off_a);
   float* sG = smem + S.off_g;
   float* sY = smem + S.off_y;
   float4* sVec = reinterpret_cast<float4*>(smem + S.off_vec);
@@ -136,30 +165,41 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int h = lane >> 5, l32 = lane & 31;
   const int C = a.C, nr = a.n_radial, R = a.R;
-  const int c = (cgrp * waves + wave) * kTile + l32;
-  const bool cvalid = c < C;
+  const int c0 = (cgrp * waves + wave) * CT * kTile + l32;  // this lane's channel in tile 0
 
   // Factor operands: lane (l32, h) of K-block b, rank tile rt holds
   // KF[16b + 8h + i][rt*32 + l32], i = 0..7, zero past d and R, as its three
-  // bf16 parts.  One thread per (b, rt, lane).
+  // bf16 parts (split mode) or in fp32 (bf16 mode).  One thread per
+  // (b, rt, lane).
   for (int t = tid; t < KB * RT * kWave; t += blockDim.x) {
-    const int ln = t % kWave, brt = t / kWave;
-    const int b = brt / RT, rt = brt - b * RT;
-    const int r = rt * kTile + (ln & 31), k0 = 16 * b + 8 * (ln >> 5);
-    uint32_t w[XP][4];
+    if constexpr (BF) {
+      const int ln = t % kWave, brt = t / kWave;
+      const int b = brt / RT, rt = brt - b * RT;
+      const int r = rt * kTile + (ln & 31), k0 = 16 * b + 8 * (ln >> 5);
+      float v[8];
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      uint16_t part[XP][2];
+      for (int i = 0; i < 8; ++i) v[i] = k0 + i < d && r < R ? a.KF[(k0 + i) * R + r] : 0.f;
+      sAf[2 * t] = make_float4(v[0], v[1], v[2], v[3]);
+      sAf[2 * t + 1] = make_float4(v[4], v[5], v[6], v[7]);
+    } else {
+      const int ln = t % kWave, brt = t / kWave;
+      const int b = brt / RT, rt = brt - b * RT;
+      const int r = rt * kTile + (ln & 31), k0 = 16 * b + 8 * (ln >> 5);
+      uint32_t w[XP][4];
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        const int k = k0 + 2 * p + q;
-        split_bf16x3(k < d && r < R ? a.KF[k * R + r] : 0.f, part[0][q], part[1][q], part[2][q]);
+      for (int p = 0; p < 4; ++p) {
+        uint16_t part[XP][2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int k = k0 + 2 * p + q;
+          split_bf16x3(k < d && r < R ? a.KF[k * R + r] : 0.f, part[0][q], part[1][q], part[2][q]);
+        }
+#pragma unroll
+        for (int s = 0; s < XP; ++s) w[s][p] = uint32_t(part[s][0]) | (uint32_t(part[s][1]) << 16);
       }
 #pragma unroll
-      for (int s = 0; s < XP; ++s) w[s][p] = uint32_t(part[s][0]) | (uint32_t(part[s][1]) << 16);
+      for (int s = 0; s < XP; ++s) sA[(brt * XP + s) * kWave + ln] = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
     }
-#pragma unroll
-    for (int s = 0; s < XP; ++s) sA[(brt * XP + s) * kWave + ln] = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
   }
   __syncthreads();
   // Factor operands are read where they are used: their index goes through
@@ -168,9 +208,11 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
   // itself stays a known LDS pointer.
   auto a_op = [&](int base, int b, int rt, int s) -> u32x4 { return sA[base + ((b * RT + rt) * XP + s) * kWave]; };
 
-  f32x16 acc[RT];
+  f32x16 acc[RT][CT];
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x16{};
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int t = 0; t < CT; ++t) acc[rt][t] = f32x16{};
 
   // Segment epilogue: Z[m][c] = sum_r EF[m][r] H[r][c] on fp32 MFMA.  The
   // contraction over r pairs accumulator register v of the two half-waves:
@@ -197,18 +239,22 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) ev[v] = er[8 * (v >> 2) + (v & 3)];
     };
-    f32x16 z = f32x16{};
+    f32x16 z[CT];
     auto ef_mfma = [&](int g, const float (&ev)[16]) {
       const int mt = g / RT, rt = g - mt * RT;
       const int row = mt * kTile + l32;
-      if (rt == 0) z = f32x16{};
 #pragma unroll
-      for (int v = 0; v < 16; ++v) z = mfma32(row < d ? ev[v] : 0.f, acc[rt][v], z);
-      if (rt == RT - 1 && cvalid) {
+      for (int t = 0; t < CT; ++t) {
+        if (rt == 0) z[t] = f32x16{};
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int m = mt * kTile + acc_row(v, h);
-          if (m < d) dst[size_t(m) * C + c] = z[v];
+        for (int v = 0; v < 16; ++v) z[t] = mfma32(row < d ? ev[v] : 0.f, acc[rt][t][v], z[t]);
+        const int c = c0 + t * kTile;
+        if (rt == RT - 1 && c < C) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int m = mt * kTile + acc_row(v, h);
+            if (m < d) dst[size_t(m) * C + c] = z[t][v];
+          }
         }
       }
     };
@@ -228,22 +274,32 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
       }
     }
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x16{};
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int t = 0; t < CT; ++t) acc[rt][t] = f32x16{};
   };
 
-  // Feature operands of one edge: part s, K-block b is the 16-byte run
-  // xs[row][c][s][16b + 8h .. +7].  The gathered row is wave-uniform (row
-  // base in scalar registers, one 32-bit lane offset per load).  Lanes with
-  // c >= C read channel C - 1; their results are never stored.
+  // Feature operands of one edge: part s (split mode) or channel tile t
+  // (bf16 mode), K-block b is the 16-byte run xs[row][c][s][16b + 8h .. +7].
+  // The gathered row is wave-uniform (row base in scalar registers, one
+  // 32-bit lane offset per load).  Lanes with c >= C read channel C - 1;
+  // their results are never stored.
+  constexpr int XB = BF ? CT : XP;  // operand rows per edge
   const char* __restrict__ xs = static_cast<const char*>(a.feat);
-  const uint32_t lane_off = ((uint32_t(cvalid ? c : C - 1) * XP) * DP + 8 * h) * 2;
-  auto load_x = [&](int row, u32x4 (&xb)[XP][KB]) {
+  uint32_t lane_off[CT];
+#pragma unroll
+  for (int t = 0; t < CT; ++t) {
+    const int c = c0 + t * kTile;
+    lane_off[t] = ((uint32_t(c < C ? c : C - 1) * XP) * DP + 8 * h) * 2;
+  }
+  auto load_x = [&](int row, u32x4 (&xb)[XB][KB]) {
     const char* p = xs + size_t(row) * (size_t(C) * XP * DP * 2);
 #pragma unroll
-    for (int s = 0; s < XP; ++s)
+    for (int s = 0; s < XB; ++s)
 #pragma unroll
       for (int b = 0; b < KB; ++b)
-        xb[s][b] = *reinterpret_cast<const u32x4*>(p + lane_off + uint32_t((s * DP + 16 * b) * 2));
+        xb[s][b] = BF ? *reinterpret_cast<const u32x4*>(p + lane_off[s] + uint32_t(16 * b * 2))
+                      : *reinterpret_cast<const u32x4*>(p + lane_off[0] + uint32_t((s * DP + 16 * b) * 2));
   };
   // U_e = KF^T x[row] for one rank tile from the six part products (smallest
   // first), then acc += g_e * U_e with g for this lane's rows
@@ -252,65 +308,100 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
   // for tile rt-1, runs the MFMA chain of tile rt into one of two U buffers,
   // and the VALU multiply-adds of tile rt-1 from the other, so that neither
   // LDS latency nor the MFMA drain stalls the chain.
-  auto edge_compute = [&](int e, const u32x4 (&xb)[XP][KB]) {
-    int ab = lane;
-    asm volatile("" : "+v"(ab));
-    const float* gb = sG + e * Rp + 4 * h;
-    u32x4 am[2][XP][KB];  // [buffer][part][K-block]
-    float4 gv[4];        // [row group]
-    f32x16 U[2];
-    auto load_a = [&](int rt, int buf) {
+  // bf16 mode: per (K-block, rank tile) the K operand bf16(g_e[r] KF[k][r])
+  // for this lane's eight k, built once and fed to the CT channel tiles; the
+  // K factor values come from registers when they fit, else from LDS.
+  constexpr bool kRegKF = BF && edge_reg_kf(d, RT);
+  float4 kf[kRegKF ? KB * RT * 2 : 1];
+  if constexpr (kRegKF) {
 #pragma unroll
-      for (int sp = 0; sp < XP; ++sp)
-#pragma unroll
-        for (int b = 0; b < KB; ++b) am[buf][sp][b] = a_op(ab, b, rt, sp);
-    };
-    auto load_g = [&](int rt) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) gv[q] = *reinterpret_cast<const float4*>(gb + rt * kTile + 8 * q);
-    };
-    auto chain = [&](int buf) {
-      f32x16 u = f32x16{};
-#pragma unroll
-      for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][0][b], xb[2][b], u);
-#pragma unroll
-      for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][2][b], xb[0][b], u);
-#pragma unroll
-      for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][1][b], xb[1][b], u);
-#pragma unroll
-      for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][0][b], xb[1][b], u);
-#pragma unroll
-      for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][1][b], xb[0][b], u);
-#pragma unroll
-      for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][0][b], xb[0][b], u);
-      U[buf] = u;
-    };
-    auto fma_rt = [&](int rt, int buf) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        acc[rt][4 * q + 0] += gv[q].x * U[buf][4 * q + 0];
-        acc[rt][4 * q + 1] += gv[q].y * U[buf][4 * q + 1];
-        acc[rt][4 * q + 2] += gv[q].z * U[buf][4 * q + 2];
-        acc[rt][4 * q + 3] += gv[q].w * U[buf][4 * q + 3];
-      }
-    };
-    load_a(0, 0);
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      if (rt + 1 < RT) load_a(rt + 1, (rt + 1) & 1);
-      if (rt > 0) load_g(rt - 1);
-      __builtin_amdgcn_sched_barrier(0);
-      chain(rt & 1);
-      if (rt > 0) fma_rt(rt - 1, (rt - 1) & 1);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int i = 0; i < KB * RT; ++i) {
+      kf[2 * i] = sAf[(i * kWave + lane) * 2];
+      kf[2 * i + 1] = sAf[(i * kWave + lane) * 2 + 1];
     }
-    load_g(RT - 1);
-    fma_rt(RT - 1, (RT - 1) & 1);
+  }
+  auto edge_compute_bf = [&](int e, const u32x4 (&xb)[XB][KB]) {
+    int ab = 2 * lane;
+    asm volatile("" : "+v"(ab));
+    float g[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) g[rt] = sG[e * Rp + rt * kTile + l32];
+#pragma unroll
+    for (int b = 0; b < KB; ++b)
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const int i = b * RT + rt;
+        const float4 f0 = kRegKF ? kf[2 * i] : sAf[ab + i * 2 * kWave];
+        const float4 f1 = kRegKF ? kf[2 * i + 1] : sAf[ab + i * 2 * kWave + 1];
+        const u32x4 kop = {pack_bf16x2(g[rt] * f0.x, g[rt] * f0.y), pack_bf16x2(g[rt] * f0.z, g[rt] * f0.w),
+                           pack_bf16x2(g[rt] * f1.x, g[rt] * f1.y), pack_bf16x2(g[rt] * f1.z, g[rt] * f1.w)};
+#pragma unroll
+        for (int t = 0; t < CT; ++t) acc[rt][t] = mfma_bf16(kop, xb[t][b], acc[rt][t]);
+      }
+  };
+  auto edge_compute = [&](int e, const u32x4 (&xb)[XB][KB]) {
+    if constexpr (BF) {
+      edge_compute_bf(e, xb);
+    } else {
+      int ab = lane;
+      asm volatile("" : "+v"(ab));
+      const float* gb = sG + e * Rp + 4 * h;
+      u32x4 am[2][XP][KB];  // [buffer][part][K-block]
+      float4 gv[4];        // [row group]
+      f32x16 U[2];
+      auto load_a = [&](int rt, int buf) {
+#pragma unroll
+        for (int sp = 0; sp < XP; ++sp)
+#pragma unroll
+          for (int b = 0; b < KB; ++b) am[buf][sp][b] = a_op(ab, b, rt, sp);
+      };
+      auto load_g = [&](int rt) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) gv[q] = *reinterpret_cast<const float4*>(gb + rt * kTile + 8 * q);
+      };
+      auto chain = [&](int buf) {
+        f32x16 u = f32x16{};
+#pragma unroll
+        for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][0][b], xb[2][b], u);
+#pragma unroll
+        for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][2][b], xb[0][b], u);
+#pragma unroll
+        for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][1][b], xb[1][b], u);
+#pragma unroll
+        for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][0][b], xb[1][b], u);
+#pragma unroll
+        for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][1][b], xb[0][b], u);
+#pragma unroll
+        for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][0][b], xb[0][b], u);
+        U[buf] = u;
+      };
+      auto fma_rt = [&](int rt, int buf) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[rt][0][4 * q + 0] += gv[q].x * U[buf][4 * q + 0];
+          acc[rt][0][4 * q + 1] += gv[q].y * U[buf][4 * q + 1];
+          acc[rt][0][4 * q + 2] += gv[q].z * U[buf][4 * q + 2];
+          acc[rt][0][4 * q + 3] += gv[q].w * U[buf][4 * q + 3];
+        }
+      };
+      load_a(0, 0);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        if (rt + 1 < RT) load_a(rt + 1, (rt + 1) & 1);
+        if (rt > 0) load_g(rt - 1);
+        __builtin_amdgcn_sched_barrier(0);
+        chain(rt & 1);
+        if (rt > 0) fma_rt(rt - 1, (rt - 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      load_g(RT - 1);
+      fma_rt(RT - 1, (RT - 1) & 1);
+    }
   };
 
   // The workgroup's ranges are slot, slot + n_blocks, ...: at any time the
   // workgroups of one XCD work on neighbouring edges.
-  for (int sp = 0; sp < a.pieces_per_block; ++sp) {
+  for (int sp = 0; sp < (kMaxRanges == 1 ? 1 : a.pieces_per_block); ++sp) {
     range = sp * n_blocks + slot;
     const int e_lo = int(int64_t(range) * a.E / a.n_range), e_hi = int(int64_t(range + 1) * a.E / a.n_range);
     int cur = -1;           // segment in the accumulators
@@ -415,7 +506,7 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
         // Two operand buffers used alternately: the loads of edge f+1 are
         // issued before the MFMAs of edge f, and the scheduling barriers keep
         // the compiler from sinking them next to their use.
-        u32x4 x0[XP][KB], x1[XP][KB];
+        u32x4 x0[XB][KB], x1[XB][KB];
         load_x(__builtin_amdgcn_readfirstlane(sIdx[e]), x0);
         int f = e;
         for (; f + 1 < pe; f += 2) {
@@ -438,30 +529,46 @@ void k_cp_edge(EdgeArgs a, int n_cgrp, int waves, int chunk) {
 
 // Edge chunk of a block: the largest power of two <= 64 (at least 8) whose
 // LDS fits the block's share of the CU (160 KB over the blocks per CU).
-inline int edge_chunk(int L, int RT, int n_radial) {
+inline int edge_chunk(int L, int RT, bool bf, int n_radial) {
   const int d = (L + 1) * (L + 1);
-  const int budget = 160 * 1024 / edge_waves_per_eu(L, RT);
+  const int budget = 160 * 1024 / edge_waves_per_eu(L, RT, bf);
   int chunk = 64;
-  while (chunk > 8 && edge_smem(RT, d, n_radial, chunk).floats * 4 > budget) chunk >>= 1;
+  while (chunk > 8 && edge_smem(RT, bf, d, n_radial, chunk).floats * 4 > budget) chunk >>= 1;
   return chunk;
 }
 
-template <int L, int RT>
-hipError_t launch_l_rt(const EdgeArgs& a, hipStream_t s) {
+// Waves per workgroup and channel groups: a wave takes CT channel tiles, a
+// workgroup up to four waves.
+struct EdgeGrid {
+  int waves, n_cgrp;
+};
+inline EdgeGrid edge_grid(int C, int RT, bool bf) {
+  const int ct = edge_ct(bf, RT);
+  const int wave_tiles = (C + ct * kTile - 1) / (ct * kTile);
+  const int waves = wave_tiles < kMaxWavesPerBlock ? wave_tiles : kMaxWavesPerBlock;
+  return EdgeGrid{waves, (wave_tiles + waves - 1) / waves};
+}
+
+template <int L, int RT, bool BF>
+hipError_t launch_l_rt_m(const EdgeArgs& a, hipStream_t s) {
   constexpr int d = (L + 1) * (L + 1);
-  const int ntiles = (a.C + kTile - 1) / kTile;
-  const int waves = ntiles < kMaxWavesPerBlock ? ntiles : kMaxWavesPerBlock;
-  const int n_cgrp = (ntiles + waves - 1) / waves;
+  const EdgeGrid gr = edge_grid(a.C, RT, BF);
+  const int waves = gr.waves, n_cgrp = gr.n_cgrp;
   if (a.E > 0) {
-    const int chunk = edge_chunk(L, RT, a.n_radial);
-    const size_t lds = size_t(edge_smem(RT, d, a.n_radial, chunk).floats) * 4;
-    auto k = k_cp_edge<L, RT>;
+    const int chunk = edge_chunk(L, RT, BF, a.n_radial);
+    const size_t lds = size_t(edge_smem(RT, BF, d, a.n_radial, chunk).floats) * 4;
+    auto k = k_cp_edge<L, RT, BF>;
     hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
     k<<<dim3(a.n_range / a.pieces_per_block * n_cgrp), dim3(waves * kWave), lds, s>>>(a, n_cgrp, waves, chunk);
   }
   return hipGetLastError();
+}
+
+template <int L, int RT>
+hipError_t launch_l_rt(const EdgeArgs& a, hipStream_t s) {
+  return a.parts == 1 ? launch_l_rt_m<L, RT, true>(a, s) : launch_l_rt_m<L, RT, false>(a, s);
 }
 
 template <int L>

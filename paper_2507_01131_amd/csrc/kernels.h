@@ -31,8 +31,8 @@ hipError_t launch_validate(int N, int E, const int32_t* edge_index, const float*
 //   out[seg] = EF H_seg                                       ([d, C])
 // forward:        KF = A, EF = D, feat = x,  gather = src, key = dst
 // grad_x pass:    KF = D, EF = A, feat = Gz, gather = dst, key = src
-// The fp32 pass splits the sorted edges into n_range equal ranges, several
-// per workgroup; segments spanning ranges are summed from `partial`
+// The pass splits the sorted edges into n_range equal ranges, several per
+// workgroup; segments spanning ranges are summed from `partial`
 // ([n_range, 2, d, C] floats of workspace).
 struct EdgeArgs {
   int n_seg, E, L, d, C, R, n_radial;
@@ -54,14 +54,14 @@ struct EdgeArgs {
   float* ef_pad;             // [d, RT*32] workspace: EF zero-padded (written by launch_cp_edge)
   int parts;                 // bf16 parts per feature in feat (3: fp32 features, 1: bf16 features)
 };
-// Edge ranges of the fp32 pass for this problem on the current device:
+// Edge ranges of the pass for this problem on the current device:
 // n_range = per_block x the number of workgroups the device holds at once
 // over the channel groups (capped at E; 0 when E = 0).  Workgroup b takes
 // ranges b, b + n_range / per_block, ...
 struct EdgePlan {
   int n_range, per_block;
 };
-EdgePlan edge_plan(int L, int R, int C, int n_radial, int E);
+EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E);
 // Features for the edge pass: x [N, d, C] -> xs [N, C, parts, edge_kpad(d)]
 // bfloat16 (k fastest, zero padded; EdgeArgs::feat = xs): parts = 3 holds
 // the exact split x = hi + mid + lo of fp32 features, parts = 1 holds bf16
@@ -70,11 +70,8 @@ EdgePlan edge_plan(int L, int R, int C, int n_radial, int E);
 int edge_kpad(int d);
 hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,
                                  hipStream_t s);
-// parts = 3: the fp32 pass below; parts = 1: launch_cp_edge_bf16
+// parts = 3: fp32 features (exact split), parts = 1: bf16 features
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
-// bf16 features (feat = xs with one part): one workgroup per segment and
-// channel group, K operand g * KF rounded to bf16 (no ranges or partials)
-hipError_t launch_cp_edge_bf16(const EdgeArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- node GEMMs
 // out[rows, C] = in[rows, C] @ W (transpose_w = 0) or in @ W^T (transpose_w = 1);
