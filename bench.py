@@ -218,7 +218,7 @@ def main():
         for _ in range(3):
             tdn.backward(res, G, workspace=wsb)
         torch.cuda.synchronize()
-        bk = ("node_gemm", "gram", "cp_bwd_dst", "sort", "feature_layout", "cp_edge_bwd_src")
+        bk = ("node_gemm", "gram", "channel_layout", "cp_bwd_dst", "sort", "feature_layout", "cp_edge_bwd_src")
         tdn.timer_enable(True)
         for k in bk:
             tdn.timer_read(k, reset=True)

@@ -146,7 +146,7 @@ tdn_status tdn_spherical_harmonics(int32_t L, int32_t E, const float* edge_vec, 
  * tdn_timer_enable(1) starts recording every launch of the layer's edge
  * kernels; tdn_timer_read synchronises on the recorded events and returns
  * the summed milliseconds and launch count of the kernel named `kernel`
- * ("cp_edge_fwd", "feature_layout", "cp_edge_bwd_src", "cp_bwd_dst", "node_gemm", "gram",
+ * ("cp_edge_fwd", "feature_layout", "channel_layout", "cp_edge_bwd_src", "cp_bwd_dst", "node_gemm", "gram",
  * "sort");
  * reset = 1 clears that kernel's record. */
 tdn_status tdn_timer_enable(int32_t enable);

@@ -365,6 +365,15 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
     a.x = x;
     a.Gz = Gz;
     a.grad_vec = grad_edge_vec;
+    a.dst = dst;
+    a.n_range = tdn::bwd_dst_plan(p->L, p->R, C, p->n_radial, bf16, E);
+    if (a.n_range > 0) {
+      // x with the channel fastest, in parts, for the contraction over channels
+      // (the region is free until the grad_x pass lays out Gz there)
+      Timed t("channel_layout", stream);
+      TDN_HIP(tdn::launch_channel_layout(N, d, C, x, !bf16, feature_parts(*p), ws + lay.xt, stream));
+      a.xc = ws + lay.xt;
+    }
     Timed t("cp_bwd_dst", stream);
     TDN_HIP(tdn::launch_bwd_dst(a, bf16, stream));
   }

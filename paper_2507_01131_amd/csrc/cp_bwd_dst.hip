@@ -1,7 +1,9 @@
-// Dispatch of the destination-side backward kernel: the factored form for
-// d <= 32 (cp_bwd_sg_<dtype>.hip), the direct form on the k-tile count 2 for
-// d <= 64 (cp_bwd_dst_m2_<dtype>.hip); each in its own translation unit.
-#include "kernels.h"
+// Dispatch of the destination-side backward kernel: for d <= 32 the range
+// kernel on bf16 MFMA (cp_bwd_dst2_l<L>.hip), else, or where its LDS layout
+// does not fit, the per-segment kernels: the factored form for d <= 32
+// (cp_bwd_sg_<dtype>.hip), the direct form on the k-tile count 2 for d <= 64
+// (cp_bwd_dst_m2_<dtype>.hip); each in its own translation unit.
+#include "cp_bwd_dst2_impl.hpp"
 
 namespace tdn {
 namespace bwd_detail {
@@ -13,8 +15,48 @@ template <bool BF16>
 hipError_t launch_sg_any(const BwdDstArgs& a, hipStream_t s);
 }
 
+namespace bwd2_detail {
+#define TDN_DST2_EXTERN(LV)                                                              \
+  extern template hipError_t launch_l<LV, false>(const BwdDstArgs&, int, hipStream_t); \
+  extern template hipError_t launch_l<LV, true>(const BwdDstArgs&, int, hipStream_t);
+TDN_DST2_EXTERN(0)
+TDN_DST2_EXTERN(1)
+TDN_DST2_EXTERN(2)
+TDN_DST2_EXTERN(3)
+TDN_DST2_EXTERN(4)
+#undef TDN_DST2_EXTERN
+}  // namespace bwd2_detail
+
+int bwd_dst_plan(int L, int R, int C, int n_radial, bool bf16, int E) {
+  using namespace bwd2_detail;
+  const int d = (L + 1) * (L + 1);
+  const int RT = (R + kTile - 1) / kTile;
+  if (E <= 0 || d > 32 || RT > 8) return 0;
+  const int chunk = dst2_chunk(RT, bf16, d, n_radial, C);
+  const int lds = dst2_smem(RT, bf16 ? 1 : 3, d, n_radial, C, chunk).floats * 4;
+  if (lds > 160 * 1024) return 0;
+  int per_cu = 160 * 1024 / lds;
+  per_cu = per_cu > 2 ? 2 : per_cu;  // eight waves per workgroup, two per SIMD
+  const int nb = device_cus() * per_cu;
+  return nb < E ? nb : E;
+}
+
 hipError_t launch_bwd_dst(const BwdDstArgs& a, bool x_bf16, hipStream_t s) {
-  if (a.n_seg == 0) return hipSuccess;
+  if (a.n_seg == 0 || a.E == 0) return hipSuccess;
+  if (a.n_range > 0) {
+    if (a.d > 32 || a.n_range > a.E || !a.xc || !a.dst) return hipErrorInvalidValue;
+    switch (a.L) {
+#define TDN_DST2_CASE(LV) \
+  case LV: return x_bf16 ? bwd2_detail::launch_l<LV, true>(a, a.n_range, s) : bwd2_detail::launch_l<LV, false>(a, a.n_range, s);
+      TDN_DST2_CASE(0)
+      TDN_DST2_CASE(1)
+      TDN_DST2_CASE(2)
+      TDN_DST2_CASE(3)
+      TDN_DST2_CASE(4)
+#undef TDN_DST2_CASE
+      default: return hipErrorInvalidValue;
+    }
+  }
   if (a.d <= 32)
     return x_bf16 ? bwd_sg_detail::launch_sg_any<true>(a, s) : bwd_sg_detail::launch_sg_any<false>(a, s);
   return x_bf16 ? bwd_detail::launch_mt<2, uint16_t>(a, s) : bwd_detail::launch_mt<2, float>(a, s);

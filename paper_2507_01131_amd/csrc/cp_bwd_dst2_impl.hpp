@@ -1,0 +1,425 @@
+// Destination-side backward (the edge-vector gradient) for d <= 32 through
+// the factored form of dg, on bf16 MFMA.
+//
+// With Gz = grad_out W^T and Gh_t = D^T Gz[t], the cotangent of g_e
+// (eq. approximate, Sec. 3.1) factors as
+//   dg_e[r] = sum_{k,j} S_e[k, j] A[k, r] D[j, r],   S_e = x[s_e] Gz[t]^T
+// (d x d, contraction over the C channels): T_e = S_e^T A ([d, R], K = d)
+// and dg_e[r] = sum_j D[j, r] T_e[j, r].  Then dv = dg * rho,
+// drho = dg * v, dY = B dv, dphi = Wrad drho and
+//   grad r_e = J_Y(r_e)^T dY + (sum_q dphi_q phi'_q(|r_e|)) r_e/|r_e|.
+//
+// Arithmetic.  fp32 problems: S_e and T_e run on v_mfma_f32_32x32x16_bf16
+// with exact three-way bf16 splits of both operands and the six part
+// products a_i b_j with i + j <= 4 (as in the forward edge pass), fp32
+// accumulation.  S_e is split again (exactly) before it feeds T_e.  bf16
+// problems: x is bf16, Gz, S_e and A are rounded to bf16, one product each.
+//
+// Work decomposition.  No sum runs over edges here, so the sorted edge list
+// is cut into equal ranges anywhere, one per workgroup of eight waves (two
+// per SIMD).  Per chunk of up to 32 edges: harmonics with their Jacobian per
+// (edge, order m) column and the radial basis per (edge, function); v = Y B
+// and rho = Phi Wrad as small fp32 MFMA GEMMs; then the chunk in segment
+// pieces: the piece's Gz[t] is split into LDS once, and each wave takes whole
+// edges: S_e (K-steps of 16 channels; the x operand comes straight from
+// global memory in the channel-fastest layout xc [N, 32, P, C], one 16-byte
+// load per part), T_e per rank tile (the accumulator registers of S regroup
+// into the A operand of a 32x32x16 step, so the factor A is stored with the
+// same row permutation), dg, dv and drho.  Last dY = dV B^T and
+// dphi = dRho Wrad^T (fp32 MFMA) and the gradient per edge.
+#pragma once
+
+#include "common.hpp"
+#include "kernels.h"
+#include "sh_device.hpp"
+
+namespace tdn {
+
+namespace bwd2_detail {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 8;
+constexpr int kMaxChunk = 32;
+
+__device__ __forceinline__ f32x16 mfma_bf16(u32x4 a, u32x4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                 0, 0);
+}
+
+// Contraction row of K-step q (0, 1), half h, element i of T = S^T A: the S
+// rows that lane half h holds in accumulator registers 8q .. 8q+7.
+__host__ __device__ constexpr int t_row(int q, int h, int i) { return 16 * q + 8 * (i / 4) + 4 * h + (i % 4); }
+
+struct Smem {
+  int Rp, bs, gzs, off_b, off_wr, off_ap, off_d, off_gz, off_v, off_rho, off_y, off_phi, off_dy, off_dphi, off_j,
+      off_idx, floats;
+};
+
+// LDS regions (floats): B and Wrad rows (padded stride bs so row-wise
+// operand reads across lanes hit distinct banks), the factor A parts in T
+// operand order [q][rank tile][part][64 lanes] x 16 bytes, D [32][Rp], the
+// staged Gz parts [32 rows][gzs halves] (gzs = P*C + 8: rows 16 bytes apart
+// in bank terms), and the chunk's v, rho, Y, Phi, dY, dPhi, Jacobian and
+// per-edge indices.
+__host__ __device__ inline Smem dst2_smem(int RT, int P, int d, int n_radial, int C, int chunk) {
+  Smem s{};
+  s.Rp = RT * kTile;
+  s.bs = s.Rp + 1;
+  s.gzs = P * C + 8;
+  int o = 0;
+  s.off_b = o;
+  o += d * s.bs;
+  s.off_wr = o;
+  o += n_radial * s.bs;
+  o = (o + 3) & ~3;
+  s.off_ap = o;
+  o += 2 * RT * P * kWave * 4;
+  s.off_d = o;
+  o += kTile * s.Rp;
+  s.off_gz = o;
+  o += kTile * s.gzs / 2;
+  s.off_v = o;
+  o += chunk * s.bs;
+  s.off_rho = o;
+  o += chunk * s.bs;
+  s.off_y = o;
+  o += chunk * d;
+  s.off_phi = o;
+  o += chunk * n_radial;
+  s.off_dy = o;
+  o += chunk * d;
+  s.off_dphi = o;
+  o += chunk * n_radial;
+  s.off_j = o;
+  o += chunk * 3 * d;
+  s.off_idx = o;
+  o += 3 * chunk;
+  s.floats = o;
+  return s;
+}
+
+__device__ __forceinline__ uint32_t pack2(uint16_t lo, uint16_t hi) { return uint32_t(lo) | (uint32_t(hi) << 16); }
+
+template <int L, int RT, bool BF>
+__global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_range, int chunk) {
+  constexpr int d = (L + 1) * (L + 1);
+  constexpr int P = BF ? 1 : 3;
+  constexpr int Rp = RT * kTile;
+  extern __shared__ float smem[];
+  const Smem S = dst2_smem(RT, P, d, a.n_radial, a.C, chunk);
+  const int bs = S.bs, gzs = S.gzs;
+  float* sB = smem + S.off_b;
+  float* sWr = smem + S.off_wr;
+  u32x4* sAp = reinterpret_cast<u32x4*>(smem + S.off_ap);
+  float* sD = smem + S.off_d;
+  uint16_t* sGz = reinterpret_cast<uint16_t*>(smem + S.off_gz);
+  float* sV = smem + S.off_v;
+  float* sRho = smem + S.off_rho;
+  float* sY = smem + S.off_y;
+  float* sPhi = smem + S.off_phi;
+  float* sDY = smem + S.off_dy;
+  float* sDPhi = smem + S.off_dphi;
+  float* sJ = smem + S.off_j;
+  int* sIdx = reinterpret_cast<int*>(smem + S.off_idx);  // gathered row
+  int* sEid = sIdx + chunk;                             // edge id
+  int* sKey = sEid + chunk;                             // destination segment
+
+  const int range = xcd_remap(blockIdx.x, n_range);
+  const int e_lo = int(int64_t(range) * a.E / n_range), e_hi = int(int64_t(range + 1) * a.E / n_range);
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int h = lane >> 5, l32 = lane & 31;
+  const int C = a.C, nr = a.n_radial, R = a.R;
+
+  // ---- factors, once per workgroup
+  for (int i = tid; i < (d + nr) * Rp; i += blockDim.x) {
+    const int k = i / Rp, r = i - k * Rp;
+    const float v = r < R ? (k < d ? a.Bf[k * R + r] : a.radial_w[(k - d) * R + r]) : 0.f;
+    (k < d ? sB + k * bs : sWr + (k - d) * bs)[r] = v;
+  }
+  for (int i = tid; i < kTile * Rp; i += blockDim.x) {
+    const int j = i / Rp, r = i - j * Rp;
+    sD[i] = (j < d && r < R) ? a.D[j * R + r] : 0.f;
+  }
+  // sAp[((q*RT + rt)*P + p)*64 + lane'] = part p of A[t_row(q, h', i)][rt*32 + l32'], i = 0..7
+  for (int t = tid; t < 2 * RT * kWave; t += blockDim.x) {
+    const int ln = t % kWave, qrt = t / kWave;
+    const int q = qrt / RT, rt = qrt - q * RT;
+    const int r = rt * kTile + (ln & 31), hh = ln >> 5;
+    uint32_t w[P][4];
+#pragma unroll
+    for (int p2 = 0; p2 < 4; ++p2) {
+      uint16_t part[3][2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int k = t_row(q, hh, 2 * p2 + e);
+        const float v = (k < d && r < R) ? a.A[k * R + r] : 0.f;
+        if constexpr (P == 3)
+          split_bf16x3(v, part[0][e], part[1][e], part[2][e]);
+        else
+          part[0][e] = bf16_rne_bits(v);
+      }
+#pragma unroll
+      for (int p = 0; p < P; ++p) w[p][p2] = pack2(part[p][0], part[p][1]);
+    }
+#pragma unroll
+    for (int p = 0; p < P; ++p) sAp[(qrt * P + p) * kWave + ln] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
+  }
+
+  // ---- per edge: S_e, T_e, dg -> dv, drho (in place in sV, sRho)
+  const char* __restrict__ xc = static_cast<const char*>(a.xc);
+  const uint32_t xlane = uint32_t((l32 * P * C + 8 * h) * 2);  // lane's row k = l32, channels 8h..
+  const uint16_t* gzl = sGz + l32 * gzs + 8 * h;               // lane's Gz row j = l32
+  auto edge_work = [&](int e) {
+    const int row = __builtin_amdgcn_readfirstlane(sIdx[e]);
+    const char* xr = xc + size_t(row) * (size_t(kTile) * P * C * 2) + xlane;
+    f32x16 Sacc = f32x16{};
+    auto ks = [&](int s2, const u32x4 (&xp)[P]) {
+      u32x4 gp[P];
+#pragma unroll
+      for (int p = 0; p < P; ++p) gp[p] = *reinterpret_cast<const u32x4*>(gzl + p * C + 16 * s2);
+      if constexpr (P == 3) {
+        Sacc = mfma_bf16(xp[0], gp[2], Sacc);
+        Sacc = mfma_bf16(xp[2], gp[0], Sacc);
+        Sacc = mfma_bf16(xp[1], gp[1], Sacc);
+        Sacc = mfma_bf16(xp[0], gp[1], Sacc);
+        Sacc = mfma_bf16(xp[1], gp[0], Sacc);
+      }
+      Sacc = mfma_bf16(xp[0], gp[0], Sacc);
+    };
+    auto load_xp = [&](int s2, u32x4 (&xp)[P]) {
+#pragma unroll
+      for (int p = 0; p < P; ++p) xp[p] = *reinterpret_cast<const u32x4*>(xr + (p * C + 16 * s2) * 2);
+    };
+    // K-steps of 16 channels, the next step's x loads issued one step ahead
+    const int nks = C / 16;
+    u32x4 x0[P], x1[P];
+    load_xp(0, x0);
+    int s2 = 0;
+    for (; s2 + 1 < nks; s2 += 2) {
+      load_xp(s2 + 1, x1);
+      __builtin_amdgcn_sched_barrier(0);
+      ks(s2, x0);
+      __builtin_amdgcn_sched_barrier(0);
+      load_xp(s2 + 2 < nks ? s2 + 2 : s2 + 1, x0);  // past the end: reloads, unused
+      __builtin_amdgcn_sched_barrier(0);
+      ks(s2 + 1, x1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (s2 < nks) ks(s2, x0);
+    // S in parts, regrouped as the A operand of T's two K-steps
+    u32x4 sp[2][P];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      uint32_t w[P][4];
+#pragma unroll
+      for (int p2 = 0; p2 < 4; ++p2) {
+        uint16_t part[3][2];
+#pragma unroll
+        for (int e2 = 0; e2 < 2; ++e2) {
+          const float v = Sacc[8 * q + 2 * p2 + e2];
+          if constexpr (P == 3)
+            split_bf16x3(v, part[0][e2], part[1][e2], part[2][e2]);
+          else
+            part[0][e2] = bf16_rne_bits(v);
+        }
+#pragma unroll
+        for (int p = 0; p < P; ++p) w[p][p2] = pack2(part[p][0], part[p][1]);
+      }
+#pragma unroll
+      for (int p = 0; p < P; ++p) sp[q][p] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
+    }
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      f32x16 T = f32x16{};
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        u32x4 ap[P];
+#pragma unroll
+        for (int p = 0; p < P; ++p) ap[p] = sAp[((q * RT + rt) * P + p) * kWave + lane];
+        if constexpr (P == 3) {
+          T = mfma_bf16(sp[q][0], ap[2], T);
+          T = mfma_bf16(sp[q][2], ap[0], T);
+          T = mfma_bf16(sp[q][1], ap[1], T);
+          T = mfma_bf16(sp[q][0], ap[1], T);
+          T = mfma_bf16(sp[q][1], ap[0], T);
+        }
+        T = mfma_bf16(sp[q][0], ap[0], T);
+      }
+      const int r = rt * kTile + l32;
+      float part = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) part += sD[acc_row(v, h) * Rp + r] * T[v];
+      part += __shfl_xor(part, 32);
+      if (h == 0) {
+        const float dv = part * sRho[e * bs + r], drho = part * sV[e * bs + r];
+        sV[e * bs + r] = dv;
+        sRho[e * bs + r] = drho;
+      }
+    }
+  };
+
+  int cur = -1;  // segment whose Gz parts are in sGz
+  for (int cb = e_lo; cb < e_hi; cb += chunk) {
+    const int n = min(chunk, e_hi - cb);
+    __syncthreads();  // factors staged / previous chunk consumed
+    for (int t = tid; t < n; t += blockDim.x) {
+      const int eid = a.perm[cb + t];
+      sEid[t] = eid;
+      sIdx[t] = a.src[eid];
+      sKey[t] = a.dst[eid];
+    }
+    // ---- geometry: harmonics and Jacobian per (edge, order m) column,
+    // radial basis per (edge, function)
+    for (int t = tid; t < n * (L + 1); t += blockDim.x) {
+      const int e = t / (L + 1), m = t - e * (L + 1);
+      const int eid = a.perm[cb + e];
+      const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
+      const float inv = 1.f / sqrtf(vx * vx + vy * vy + vz * vz);
+      sh_unit_jacobian_column(L, m, vx * inv, vy * inv, vz * inv, inv, sY + e * d, sJ + e * 3 * d);
+    }
+    for (int t = tid; t < n * nr; t += blockDim.x) {
+      const int e = t / nr, q = t - e * nr;
+      const int eid = a.perm[cb + e];
+      const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
+      sPhi[t] = radial_phi(sqrtf(vx * vx + vy * vy + vz * vz), q, a.sigma);
+    }
+    __syncthreads();
+    // ---- v = Y B, rho = Phi Wrad (rows: edges, columns: ranks), fp32 MFMA
+    for (int item = wave; item < 2 * RT; item += kWaves) {
+      const int rt = item >> 1;
+      const bool is_v = (item & 1) == 0;
+      const int K = is_v ? d : nr;
+      const float* src = is_v ? sY : sPhi;
+      const float* fac = is_v ? sB : sWr;
+      f32x16 T = f32x16{};
+      for (int s2 = 0; s2 < (K + 1) / 2; ++s2) {
+        const int k = 2 * s2 + h;
+        const float av = (l32 < n && k < K) ? src[l32 * K + k] : 0.f;
+        const float bv = k < K ? fac[k * bs + rt * kTile + l32] : 0.f;
+        T = mfma32(av, bv, T);
+      }
+      float* dstp = is_v ? sV : sRho;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int e = acc_row(v, h);
+        if (e < n) dstp[e * bs + rt * kTile + l32] = T[v];
+      }
+    }
+    // ---- the chunk in segment pieces
+    for (int p0 = 0; p0 < n;) {
+      __syncthreads();  // v/rho written; the previous piece's edges done with sGz
+      const int seg = __builtin_amdgcn_readfirstlane(sKey[p0]);
+      int p1 = p0 + 1;
+      while (p1 < n && sKey[p1] == seg) ++p1;
+      p1 = __builtin_amdgcn_readfirstlane(p1);
+      if (seg != cur) {
+        // Gz[seg] rows j < 32 (zero from d) in parts: one thread per pair of channels
+        for (int i = tid; i < kTile * (C / 2); i += blockDim.x) {
+          const int j = i / (C / 2), c2 = 2 * (i - j * (C / 2));
+          float2 g = make_float2(0.f, 0.f);
+          if (j < d) g = *reinterpret_cast<const float2*>(a.Gz + (size_t(seg) * d + j) * C + c2);
+          uint16_t part[3][2];
+          if constexpr (P == 3) {
+            split_bf16x3(g.x, part[0][0], part[1][0], part[2][0]);
+            split_bf16x3(g.y, part[0][1], part[1][1], part[2][1]);
+          } else {
+            part[0][0] = bf16_rne_bits(g.x);
+            part[0][1] = bf16_rne_bits(g.y);
+          }
+#pragma unroll
+          for (int p = 0; p < P; ++p)
+            *reinterpret_cast<uint32_t*>(sGz + j * gzs + p * C + c2) = pack2(part[p][0], part[p][1]);
+        }
+        cur = seg;
+        __syncthreads();
+      }
+      for (int e = p0 + wave; e < p1; e += kWaves) edge_work(e);
+      p0 = p1;
+    }
+    __syncthreads();
+    // ---- dY = dV B^T (k < d), dphi = dRho Wrad^T (q < nr); K = ranks
+    for (int item = wave; item < 2; item += kWaves) {
+      const bool is_y = item == 0;
+      const int K2 = is_y ? d : nr;
+      const float* src = is_y ? sV : sRho;
+      const float* fac = is_y ? sB : sWr;
+      f32x16 T = f32x16{};
+      for (int s2 = 0; s2 < Rp / 2; ++s2) {
+        const int r = 2 * s2 + h;
+        const float av = l32 < n ? src[l32 * bs + r] : 0.f;
+        const float bv = l32 < K2 ? fac[l32 * bs + r] : 0.f;
+        T = mfma32(av, bv, T);
+      }
+      float* dstp = is_y ? sDY : sDPhi;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int ee = acc_row(v, h);
+        if (ee < n && l32 < K2) dstp[ee * K2 + l32] = T[v];
+      }
+    }
+    __syncthreads();
+    for (int t = tid; t < n; t += blockDim.x) {
+      const int eid = sEid[t];
+      const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
+      const float rn = sqrtf(vx * vx + vy * vy + vz * vz);
+      float gx = 0.f, gy = 0.f, gzv = 0.f;
+      for (int k = 0; k < d; ++k) {
+        const float dy = sDY[t * d + k];
+        gx += dy * sJ[t * 3 * d + 3 * k];
+        gy += dy * sJ[t * 3 * d + 3 * k + 1];
+        gzv += dy * sJ[t * 3 * d + 3 * k + 2];
+      }
+      float dr = 0.f;
+      for (int q = 0; q < nr; ++q) {
+        const float u = (rn - float(q) * a.sigma) / a.sigma;
+        dr += sDPhi[t * nr + q] * (-u / a.sigma) * sPhi[t * nr + q];
+      }
+      const float inv = 1.f / rn;
+      a.grad_vec[3 * eid] = gx + dr * vx * inv;
+      a.grad_vec[3 * eid + 1] = gy + dr * vy * inv;
+      a.grad_vec[3 * eid + 2] = gzv + dr * vz * inv;
+    }
+  }
+}
+
+// Chunk: the largest of 32, 16, 8 edges whose layout fits the 160 KB of LDS.
+inline int dst2_chunk(int RT, bool bf, int d, int n_radial, int C) {
+  int chunk = kMaxChunk;
+  while (chunk > 8 && dst2_smem(RT, bf ? 1 : 3, d, n_radial, C, chunk).floats * 4 > 160 * 1024) chunk >>= 1;
+  return chunk;
+}
+
+template <int L, int RT, bool BF>
+hipError_t launch_l_rt(const BwdDstArgs& a, int n_range, hipStream_t s) {
+  constexpr int d = (L + 1) * (L + 1);
+  const int chunk = dst2_chunk(RT, BF, d, a.n_radial, a.C);
+  const size_t lds = size_t(dst2_smem(RT, BF ? 1 : 3, d, a.n_radial, a.C, chunk).floats) * 4;
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  auto k = k_bwd_dst2<L, RT, BF>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     int(lds));
+  if (e != hipSuccess) return e;
+  k<<<dim3(n_range), dim3(kWaves * kWave), lds, s>>>(a, n_range, chunk);
+  return hipGetLastError();
+}
+
+template <int L, bool BF>
+hipError_t launch_l(const BwdDstArgs& a, int n_range, hipStream_t s) {
+  switch ((a.R + kTile - 1) / kTile) {
+    case 1: return launch_l_rt<L, 1, BF>(a, n_range, s);
+    case 2: return launch_l_rt<L, 2, BF>(a, n_range, s);
+    case 3: return launch_l_rt<L, 3, BF>(a, n_range, s);
+    case 4: return launch_l_rt<L, 4, BF>(a, n_range, s);
+    case 5: return launch_l_rt<L, 5, BF>(a, n_range, s);
+    case 6: return launch_l_rt<L, 6, BF>(a, n_range, s);
+    case 7: return launch_l_rt<L, 7, BF>(a, n_range, s);
+    case 8: return launch_l_rt<L, 8, BF>(a, n_range, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace bwd2_detail
+
+}  // namespace tdn

@@ -1,0 +1,5 @@
+// Destination-side backward on bf16 MFMA (d <= 32) instantiated for L = 1.
+#include "cp_bwd_dst2_impl.hpp"
+
+template hipError_t tdn::bwd2_detail::launch_l<1, false>(const tdn::BwdDstArgs&, int, hipStream_t);
+template hipError_t tdn::bwd2_detail::launch_l<1, true>(const tdn::BwdDstArgs&, int, hipStream_t);

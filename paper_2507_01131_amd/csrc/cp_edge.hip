@@ -47,6 +47,9 @@ __global__ __launch_bounds__(256) void k_pad_rows(int rows, int R, int Rp, const
 
 constexpr int kMinRangeEdges = 48;
 
+}  // namespace
+}  // namespace edge_detail
+
 int device_cus() {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 256;
@@ -61,9 +64,6 @@ int device_cus() {
   }
   return it->second;
 }
-
-}  // namespace
-}  // namespace edge_detail
 
 EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E) {
   using namespace edge_detail;

@@ -70,6 +70,10 @@ EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E);
 int edge_kpad(int d);
 hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,
                                  hipStream_t s);
+// The same parts with the channel fastest: xc [N, edge_kpad(d), parts, C]
+// bfloat16 (rows from d zero), for contractions over channels.
+hipError_t launch_channel_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xc,
+                                 hipStream_t s);
 // parts = 3: fp32 features (exact split), parts = 1: bf16 features
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
 
@@ -92,6 +96,7 @@ struct BwdDstArgs {
   const int32_t* offsets;   // dst segments
   const int32_t* perm;
   const int32_t* src;       // [E] by edge id
+  const int32_t* dst;       // [E] by edge id
   const float* edge_vec;
   const float* A;
   const float* Bf;
@@ -100,10 +105,17 @@ struct BwdDstArgs {
   const void* x;            // [N, d, C]
   const float* Gz;          // [N, d, C] = grad_out W^T
   float* grad_vec;          // [E, 3] by edge id
+  const void* xc;           // [N, 32, parts, C] bf16 (launch_channel_layout of x), d <= 32
+  int n_range;              // equal edge ranges, one per workgroup (bwd_dst_plan)
 };
+// Edge ranges of the destination-side kernel on the current device (0 when
+// the problem takes the per-segment kernels: d > 32 or no LDS fit).
+int bwd_dst_plan(int L, int R, int C, int n_radial, bool bf16, int E);
 hipError_t launch_bwd_dst(const BwdDstArgs& a, bool x_bf16, hipStream_t s);
 
 // ---------------------------------------------------------------- misc
+// Compute units of the current device (cached per device).
+int device_cus();
 hipError_t launch_sh(int L, int E, const float* edge_vec, float* Y, float* dY, hipStream_t s);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 
