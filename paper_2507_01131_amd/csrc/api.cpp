@@ -3,6 +3,7 @@
 // every scratch buffer is carved from the caller's workspace.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <map>
@@ -58,6 +59,13 @@ int feature_parts(const tdn_problem& p) { return p.feat_dtype == TDN_BF16 ? 1 : 
 size_t xt_bytes(const tdn_problem& p) {
   return size_t(p.n_nodes) * p.C * feature_parts(p) * tdn::edge_kpad(dim_of(p.L)) * 2;
 }
+// the same region holds, in the backward, x with the channel fastest for
+// the destination-side kernel
+size_t xt_xc_bytes(const tdn_problem& p) {
+  const size_t xc =
+      size_t(p.n_nodes) * dim_of(p.L) * feature_parts(p) * tdn::bwd_dst_cpad(p.C, p.feat_dtype == TDN_BF16) * 2;
+  return std::max(xt_bytes(p), xc);
+}
 
 // partial slots of the fp32 edge pass (two [d, C] rows per edge range) and
 // its zero-padded output factor [d, RT*32]
@@ -100,7 +108,7 @@ BwdLayout bwd_layout(const tdn_problem& p) {
   b.z = o;
   o += al(ndc);
   b.xt = o;
-  o += al(xt_bytes(p));
+  o += al(xt_xc_bytes(p));
   b.part = o;
   o += al(partial_bytes(p));
   b.parts = o;
@@ -366,12 +374,15 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
     a.Gz = Gz;
     a.grad_vec = grad_edge_vec;
     a.dst = dst;
-    a.n_range = tdn::bwd_dst_plan(p->L, p->R, C, p->n_radial, bf16, E);
+    const tdn::EdgePlan dp = tdn::bwd_dst_plan(p->L, p->R, C, p->n_radial, bf16, E);
+    a.n_range = dp.n_range;
+    a.pieces_per_block = dp.per_block;
     if (a.n_range > 0) {
       // x with the channel fastest, in parts, for the contraction over channels
       // (the region is free until the grad_x pass lays out Gz there)
       Timed t("channel_layout", stream);
-      TDN_HIP(tdn::launch_channel_layout(N, d, C, x, !bf16, feature_parts(*p), ws + lay.xt, stream));
+      TDN_HIP(tdn::launch_channel_layout(N, d, C, tdn::bwd_dst_cpad(C, bf16), x, !bf16, feature_parts(*p), ws + lay.xt,
+                                         stream));
       a.xc = ws + lay.xt;
     }
     Timed t("cp_bwd_dst", stream);

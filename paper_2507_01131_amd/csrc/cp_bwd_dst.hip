@@ -27,19 +27,28 @@ TDN_DST2_EXTERN(4)
 #undef TDN_DST2_EXTERN
 }  // namespace bwd2_detail
 
-int bwd_dst_plan(int L, int R, int C, int n_radial, bool bf16, int E) {
+constexpr int kMinPieceEdges = 96, kMaxPieces = 2;
+
+EdgePlan bwd_dst_plan(int L, int R, int C, int n_radial, bool bf16, int E) {
   using namespace bwd2_detail;
   const int d = (L + 1) * (L + 1);
   const int RT = (R + kTile - 1) / kTile;
-  if (E <= 0 || d > 32 || RT > 8) return 0;
+  if (E <= 0 || d > 32 || RT > 8) return EdgePlan{0, 0};
   const int chunk = dst2_chunk(RT, bf16, d, n_radial, C);
   const int lds = dst2_smem(RT, bf16 ? 1 : 3, d, n_radial, C, chunk).floats * 4;
-  if (lds > 160 * 1024) return 0;
+  if (lds > 160 * 1024) return EdgePlan{0, 0};
   int per_cu = 160 * 1024 / lds;
   per_cu = per_cu > 2 ? 2 : per_cu;  // eight waves per workgroup, two per SIMD
-  const int nb = device_cus() * per_cu;
-  return nb < E ? nb : E;
+  int nb = device_cus() * per_cu;
+  nb = nb < E ? nb : E;
+  // several ranges per workgroup (there is no sum across ranges here) while
+  // each keeps at least kMinPieceEdges edges
+  int S = E / (nb * kMinPieceEdges);
+  S = S < 1 ? 1 : (S > kMaxPieces ? kMaxPieces : S);
+  return EdgePlan{nb * S, S};
 }
+
+int bwd_dst_cpad(int C, bool bf16) { return bwd2_detail::dst2_cpad(C, bf16 ? 1 : 3); }
 
 hipError_t launch_bwd_dst(const BwdDstArgs& a, bool x_bf16, hipStream_t s) {
   if (a.n_seg == 0 || a.E == 0) return hipSuccess;

@@ -16,17 +16,19 @@
 // problems: x is bf16, Gz, S_e and A are rounded to bf16, one product each.
 //
 // Work decomposition.  No sum runs over edges here, so the sorted edge list
-// is cut into equal ranges anywhere, one per workgroup of eight waves (two
-// per SIMD).  Per chunk of up to 32 edges: harmonics with their Jacobian per
-// (edge, order m) column and the radial basis per (edge, function); v = Y B
-// and rho = Phi Wrad as small fp32 MFMA GEMMs; then the chunk in segment
-// pieces: the piece's Gz[t] is split into LDS once, and each wave takes whole
-// edges: S_e (K-steps of 16 channels; the x operand comes straight from
-// global memory in the channel-fastest layout xc [N, 32, P, C], one 16-byte
-// load per part), T_e per rank tile (the accumulator registers of S regroup
-// into the A operand of a 32x32x16 step, so the factor A is stored with the
-// same row permutation), dg, dv and drho.  Last dY = dV B^T and
-// dphi = dRho Wrad^T (fp32 MFMA) and the gradient per edge.
+// is cut into equal ranges anywhere, several per workgroup of eight waves
+// (two per SIMD), interleaved so that the workgroups of one XCD work in one
+// stretch of destinations at a time.  Per chunk of up to 32 edges: harmonics
+// with their Jacobian per (edge, order m) column and the radial basis per
+// (edge, function); v = Y B and rho = Phi Wrad as small fp32 MFMA GEMMs; then
+// the chunk in segment pieces: the piece's Gz[t] is split into LDS once, and
+// each wave takes whole edges: S_e (K-steps of 16 channels; the x operand
+// comes straight from global memory in the channel-fastest layout
+// xc [N, d, P, Cp], one 16-byte load per part, through a per-wave prefetch
+// ring), T_e per rank tile (the accumulator registers of S regroup into the
+// A operand of a 32x32x16 step, so the factor A is stored with the same row
+// permutation), dg, dv and drho.  Last dY = dV B^T and dphi = dRho Wrad^T
+// (fp32 MFMA) and the gradient per edge.
 #pragma once
 
 #include "common.hpp"
@@ -42,6 +44,18 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 8;
 constexpr int kMaxChunk = 32;
+constexpr int kRing = 4;  // x slots per wave in the S loop
+constexpr int kMaxRadial = 16;
+constexpr int kBufferWord3 = 0x00020000;  // raw buffer resource, fourth word (gfx9 family)
+
+// K-steps of 16 channels per ring slot: one for the three-part (fp32)
+// operands, two for bf16
+__host__ __device__ constexpr int dst2_kps(int P) { return P == 3 ? 1 : 2; }
+// channels padded to whole ring turns
+__host__ __device__ inline int dst2_cpad(int C, int P) {
+  const int turn = 16 * dst2_kps(P) * kRing;
+  return (C + turn - 1) / turn * turn;
+}
 
 __device__ __forceinline__ f32x16 mfma_bf16(u32x4 a, u32x4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
@@ -67,7 +81,7 @@ __host__ __device__ inline Smem dst2_smem(int RT, int P, int d, int n_radial, in
   Smem s{};
   s.Rp = RT * kTile;
   s.bs = s.Rp + 1;
-  s.gzs = P * C + 8;
+  s.gzs = P * dst2_cpad(C, P) + 8;
   int o = 0;
   s.off_b = o;
   o += d * s.bs;
@@ -89,13 +103,13 @@ __host__ __device__ inline Smem dst2_smem(int RT, int P, int d, int n_radial, in
   s.off_phi = o;
   o += chunk * n_radial;
   s.off_dy = o;
-  o += chunk * d;
+  o += 4 * chunk * d;  // four rank-quarter partials
   s.off_dphi = o;
-  o += chunk * n_radial;
+  o += 4 * chunk * n_radial;
   s.off_j = o;
   o += chunk * 3 * d;
   s.off_idx = o;
-  o += 3 * chunk;
+  o += 6 * chunk;
   s.floats = o;
   return s;
 }
@@ -106,6 +120,7 @@ template <int L, int RT, bool BF>
 __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_range, int chunk) {
   constexpr int d = (L + 1) * (L + 1);
   constexpr int P = BF ? 1 : 3;
+  constexpr int KPS = dst2_kps(P);
   constexpr int Rp = RT * kTile;
   extern __shared__ float smem[];
   const Smem S = dst2_smem(RT, P, d, a.n_radial, a.C, chunk);
@@ -125,10 +140,15 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
   int* sIdx = reinterpret_cast<int*>(smem + S.off_idx);  // gathered row
   int* sEid = sIdx + chunk;                             // edge id
   int* sKey = sEid + chunk;                             // destination segment
+  float* sVec = reinterpret_cast<float*>(sKey + chunk);  // edge vectors [chunk][3]
 
-  const int range = xcd_remap(blockIdx.x, n_range);
-  const int e_lo = int(int64_t(range) * a.E / n_range), e_hi = int(int64_t(range + 1) * a.E / n_range);
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  // ranges slot, slot + n_blocks, ...: at any time the workgroups of one XCD
+  // work in one stretch of the destination-sorted edges, and their gathered
+  // source rows overlap in that XCD's L2
+  const int n_blocks = gridDim.x, per_block = n_range / n_blocks;
+  const int slot = xcd_remap(blockIdx.x, n_blocks);
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform over the wave
   const int h = lane >> 5, l32 = lane & 31;
   const int C = a.C, nr = a.n_radial, R = a.R;
 
@@ -168,17 +188,43 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
   }
 
   // ---- per edge: S_e, T_e, dg -> dv, drho (in place in sV, sRho)
+  // The x operand streams through a ring of kRing slots per wave, kRing - 1
+  // slots ahead of the MFMA and on into the wave's next edge of the piece, so
+  // that edge's first loads are in flight while this edge's T runs.  A slot
+  // is KPS K-steps of 16 channels; the channel count is padded to whole ring
+  // turns (zero channels in x and in the staged Gz), so every edge starts on
+  // slot 0.  The loads are buffer loads over one node's row of xc: lanes of
+  // rows k >= d and a missing next edge (a record of no bytes) read zeros
+  // through the range check, with no branch that would drain the ring.  The
+  // Gz operand is read from LDS one slot ahead.
+  const int Cp = dst2_cpad(C, P), nsl = Cp / (16 * KPS);
   const char* __restrict__ xc = static_cast<const char*>(a.xc);
-  const uint32_t xlane = uint32_t((l32 * P * C + 8 * h) * 2);  // lane's row k = l32, channels 8h..
-  const uint16_t* gzl = sGz + l32 * gzs + 8 * h;               // lane's Gz row j = l32
-  auto edge_work = [&](int e) {
-    const int row = __builtin_amdgcn_readfirstlane(sIdx[e]);
-    const char* xr = xc + size_t(row) * (size_t(kTile) * P * C * 2) + xlane;
-    f32x16 Sacc = f32x16{};
-    auto ks = [&](int s2, const u32x4 (&xp)[P]) {
-      u32x4 gp[P];
+  const int xrow = d * P * Cp * 2;  // bytes per node
+  const uint32_t xoff = l32 < d ? uint32_t((l32 * P * Cp + 8 * h) * 2) : 0x80000000u;
+  const uint16_t* gzl = sGz + l32 * gzs + 8 * h;  // lane's Gz row j = l32
+  auto row_rsrc = [&](int row, bool valid) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(xc) + size_t(row) * xrow, 0, valid ? xrow : 0,
+                                             kBufferWord3);
+  };
+  auto load_slot = [&](__amdgpu_buffer_rsrc_t rs, int sl, u32x4 (&xb)[KPS][P]) {
 #pragma unroll
-      for (int p = 0; p < P; ++p) gp[p] = *reinterpret_cast<const u32x4*>(gzl + p * C + 16 * s2);
+    for (int kk = 0; kk < KPS; ++kk)
+#pragma unroll
+      for (int p = 0; p < P; ++p)
+        xb[kk][p] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, xoff, (p * Cp + 16 * (sl * KPS + kk)) * 2, 0));
+  };
+  auto load_g = [&](int sl, u32x4 (&g)[KPS][P]) {
+#pragma unroll
+    for (int kk = 0; kk < KPS; ++kk)
+#pragma unroll
+      for (int p = 0; p < P; ++p) g[kk][p] = *reinterpret_cast<const u32x4*>(gzl + p * Cp + 16 * (sl * KPS + kk));
+  };
+  auto mma_slot = [&](const u32x4 (&xb)[KPS][P], const u32x4 (&g)[KPS][P], f32x16& Sacc) {
+#pragma unroll
+    for (int kk = 0; kk < KPS; ++kk) {
+      const u32x4(&xp)[P] = xb[kk];
+      const u32x4(&gp)[P] = g[kk];
       if constexpr (P == 3) {
         Sacc = mfma_bf16(xp[0], gp[2], Sacc);
         Sacc = mfma_bf16(xp[2], gp[0], Sacc);
@@ -187,27 +233,9 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
         Sacc = mfma_bf16(xp[1], gp[0], Sacc);
       }
       Sacc = mfma_bf16(xp[0], gp[0], Sacc);
-    };
-    auto load_xp = [&](int s2, u32x4 (&xp)[P]) {
-#pragma unroll
-      for (int p = 0; p < P; ++p) xp[p] = *reinterpret_cast<const u32x4*>(xr + (p * C + 16 * s2) * 2);
-    };
-    // K-steps of 16 channels, the next step's x loads issued one step ahead
-    const int nks = C / 16;
-    u32x4 x0[P], x1[P];
-    load_xp(0, x0);
-    int s2 = 0;
-    for (; s2 + 1 < nks; s2 += 2) {
-      load_xp(s2 + 1, x1);
-      __builtin_amdgcn_sched_barrier(0);
-      ks(s2, x0);
-      __builtin_amdgcn_sched_barrier(0);
-      load_xp(s2 + 2 < nks ? s2 + 2 : s2 + 1, x0);  // past the end: reloads, unused
-      __builtin_amdgcn_sched_barrier(0);
-      ks(s2 + 1, x1);
-      __builtin_amdgcn_sched_barrier(0);
     }
-    if (s2 < nks) ks(s2, x0);
+  };
+  auto finish_edge = [&](int e, const f32x16& Sacc) {
     // S in parts, regrouped as the A operand of T's two K-steps
     u32x4 sp[2][P];
 #pragma unroll
@@ -260,126 +288,225 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
     }
   };
 
-  int cur = -1;  // segment whose Gz parts are in sGz
-  for (int cb = e_lo; cb < e_hi; cb += chunk) {
-    const int n = min(chunk, e_hi - cb);
-    __syncthreads();  // factors staged / previous chunk consumed
-    for (int t = tid; t < n; t += blockDim.x) {
-      const int eid = a.perm[cb + t];
-      sEid[t] = eid;
-      sIdx[t] = a.src[eid];
-      sKey[t] = a.dst[eid];
-    }
-    // ---- geometry: harmonics and Jacobian per (edge, order m) column,
-    // radial basis per (edge, function)
-    for (int t = tid; t < n * (L + 1); t += blockDim.x) {
-      const int e = t / (L + 1), m = t - e * (L + 1);
-      const int eid = a.perm[cb + e];
-      const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
-      const float inv = 1.f / sqrtf(vx * vx + vy * vy + vz * vz);
-      sh_unit_jacobian_column(L, m, vx * inv, vy * inv, vz * inv, inv, sY + e * d, sJ + e * 3 * d);
-    }
-    for (int t = tid; t < n * nr; t += blockDim.x) {
-      const int e = t / nr, q = t - e * nr;
-      const int eid = a.perm[cb + e];
-      const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
-      sPhi[t] = radial_phi(sqrtf(vx * vx + vy * vy + vz * vz), q, a.sigma);
-    }
-    __syncthreads();
-    // ---- v = Y B, rho = Phi Wrad (rows: edges, columns: ranks), fp32 MFMA
-    for (int item = wave; item < 2 * RT; item += kWaves) {
-      const int rt = item >> 1;
-      const bool is_v = (item & 1) == 0;
-      const int K = is_v ? d : nr;
-      const float* src = is_v ? sY : sPhi;
-      const float* fac = is_v ? sB : sWr;
-      f32x16 T = f32x16{};
-      for (int s2 = 0; s2 < (K + 1) / 2; ++s2) {
-        const int k = 2 * s2 + h;
-        const float av = (l32 < n && k < K) ? src[l32 * K + k] : 0.f;
-        const float bv = k < K ? fac[k * bs + rt * kTile + l32] : 0.f;
-        T = mfma32(av, bv, T);
-      }
-      float* dstp = is_v ? sV : sRho;
+  // this wave's edges of the piece [p0, p1): p0 + wave, p0 + wave + kWaves, ...
+  auto wave_edges = [&](int p0, int p1) {
+    int e = p0 + wave;
+    if (e >= p1) return;
+    u32x4 ring[kRing][KPS][P];
+    u32x4 g2[2][KPS][P];
+    __amdgpu_buffer_rsrc_t rs = row_rsrc(__builtin_amdgcn_readfirstlane(sIdx[e]), true);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int e = acc_row(v, h);
-        if (e < n) dstp[e * bs + rt * kTile + l32] = T[v];
-      }
-    }
-    // ---- the chunk in segment pieces
-    for (int p0 = 0; p0 < n;) {
-      __syncthreads();  // v/rho written; the previous piece's edges done with sGz
-      const int seg = __builtin_amdgcn_readfirstlane(sKey[p0]);
-      int p1 = p0 + 1;
-      while (p1 < n && sKey[p1] == seg) ++p1;
-      p1 = __builtin_amdgcn_readfirstlane(p1);
-      if (seg != cur) {
-        // Gz[seg] rows j < 32 (zero from d) in parts: one thread per pair of channels
-        for (int i = tid; i < kTile * (C / 2); i += blockDim.x) {
-          const int j = i / (C / 2), c2 = 2 * (i - j * (C / 2));
-          float2 g = make_float2(0.f, 0.f);
-          if (j < d) g = *reinterpret_cast<const float2*>(a.Gz + (size_t(seg) * d + j) * C + c2);
-          uint16_t part[3][2];
-          if constexpr (P == 3) {
-            split_bf16x3(g.x, part[0][0], part[1][0], part[2][0]);
-            split_bf16x3(g.y, part[0][1], part[1][1], part[2][1]);
-          } else {
-            part[0][0] = bf16_rne_bits(g.x);
-            part[0][1] = bf16_rne_bits(g.y);
-          }
+    for (int j = 0; j + 1 < kRing; ++j) load_slot(rs, j, ring[j]);
+    load_g(0, g2[0]);
+    for (; e < p1; e += kWaves) {
+      const bool has_next = e + kWaves < p1;
+      const __amdgpu_buffer_rsrc_t nrs =
+          row_rsrc(__builtin_amdgcn_readfirstlane(sIdx[has_next ? e + kWaves : e]), has_next);
+      f32x16 Sacc = f32x16{};
+      for (int u0 = 0; u0 < nsl; u0 += kRing) {
 #pragma unroll
-          for (int p = 0; p < P; ++p)
-            *reinterpret_cast<uint32_t*>(sGz + j * gzs + p * C + c2) = pack2(part[p][0], part[p][1]);
+        for (int j = 0; j < kRing; ++j) {
+          const int fs = u0 + j + kRing - 1;  // slot loaded now, into ring[(j + kRing - 1) % kRing]
+          load_slot(fs < nsl ? rs : nrs, fs < nsl ? fs : fs - nsl, ring[(j + kRing - 1) % kRing]);
+          const int gs = u0 + j + 1;
+          load_g(gs < nsl ? gs : 0, g2[(j + 1) & 1]);
+          __builtin_amdgcn_sched_barrier(0);
+          mma_slot(ring[j], g2[j & 1], Sacc);
+          __builtin_amdgcn_sched_barrier(0);
         }
-        cur = seg;
-        __syncthreads();
       }
-      for (int e = p0 + wave; e < p1; e += kWaves) edge_work(e);
-      p0 = p1;
+      finish_edge(e, Sacc);
+      rs = nrs;
     }
-    __syncthreads();
-    // ---- dY = dV B^T (k < d), dphi = dRho Wrad^T (q < nr); K = ranks
-    for (int item = wave; item < 2; item += kWaves) {
-      const bool is_y = item == 0;
-      const int K2 = is_y ? d : nr;
-      const float* src = is_y ? sV : sRho;
-      const float* fac = is_y ? sB : sWr;
-      f32x16 T = f32x16{};
-      for (int s2 = 0; s2 < Rp / 2; ++s2) {
-        const int r = 2 * s2 + h;
-        const float av = l32 < n ? src[l32 * bs + r] : 0.f;
-        const float bv = l32 < K2 ? fac[l32 * bs + r] : 0.f;
-        T = mfma32(av, bv, T);
+  };
+
+  // The workgroup's chunks: ranges pc = 0 .. per_block - 1, each in chunks
+  // of up to `chunk` edges.  The records (edge id, source, destination,
+  // edge vector) of the next chunk are fetched by threads t < chunk while
+  // this chunk runs: the edge ids during the geometry, the rest during the
+  // edge work, so no chunk starts on a chain of dependent global loads.
+  // range pc * n_blocks + slot of this workgroup: [range_lo(pc), range_hi(pc))
+  auto range_lo = [&](int pc) { return int(int64_t(pc * n_blocks + slot) * a.E / n_range); };
+  auto range_hi = [&](int pc) { return int(int64_t(pc * n_blocks + slot + 1) * a.E / n_range); };
+  struct EdgeRec {
+    int eid, src, dst;
+    float vx, vy, vz;
+  };
+  auto load_rec = [&](int eid, int cnt, EdgeRec& r) {
+    if (tid < cnt) {
+      r.eid = eid;
+      r.src = a.src[eid];
+      r.dst = a.dst[eid];
+      r.vx = a.edge_vec[3 * eid];
+      r.vy = a.edge_vec[3 * eid + 1];
+      r.vz = a.edge_vec[3 * eid + 2];
+    }
+  };
+  int pc = 0, cb = range_lo(0), hi = range_hi(0);
+  EdgeRec rec{};
+  {
+    const int n0 = min(chunk, hi - cb);
+    load_rec(tid < n0 ? a.perm[cb + tid] : 0, n0, rec);
+  }
+  int cur = -1;  // segment whose Gz parts are in sGz
+  for (;;) {
+    {
+      const int n = min(chunk, hi - cb);
+      int npc = pc, ncb = cb + chunk, nhi = hi;
+      if (ncb >= hi) {
+        npc = pc + 1;
+        ncb = npc < per_block ? range_lo(npc) : 0;
+        nhi = npc < per_block ? range_hi(npc) : 0;
       }
-      float* dstp = is_y ? sDY : sDPhi;
+      const int nn = npc < per_block ? min(chunk, nhi - ncb) : 0;
+      __syncthreads();  // factors staged / previous chunk consumed
+      if (tid < n) {
+        sEid[tid] = rec.eid;
+        sIdx[tid] = rec.src;
+        sKey[tid] = rec.dst;
+        sVec[3 * tid] = rec.vx;
+        sVec[3 * tid + 1] = rec.vy;
+        sVec[3 * tid + 2] = rec.vz;
+      }
+      const int next_eid = tid < nn ? a.perm[ncb + tid] : 0;
+      __syncthreads();
+      // ---- geometry: harmonics and Jacobian per (edge, order m) column,
+      // radial basis per (edge, function)
+      for (int t = tid; t < n * (L + 1); t += blockDim.x) {
+        const int e = t / (L + 1), m = t - e * (L + 1);
+        const float vx = sVec[3 * e], vy = sVec[3 * e + 1], vz = sVec[3 * e + 2];
+        const float inv = 1.f / sqrtf(vx * vx + vy * vy + vz * vz);
+        sh_unit_jacobian_column(L, m, vx * inv, vy * inv, vz * inv, inv, sY + e * d, sJ + e * 3 * d);
+      }
+      for (int t = tid; t < n * nr; t += blockDim.x) {
+        const int e = t / nr, q = t - e * nr;
+        const float vx = sVec[3 * e], vy = sVec[3 * e + 1], vz = sVec[3 * e + 2];
+        sPhi[t] = radial_phi(sqrtf(vx * vx + vy * vy + vz * vz), q, a.sigma);
+      }
+      __syncthreads();
+      // ---- v = Y B, rho = Phi Wrad (rows: edges, columns: ranks), fp32 MFMA
+      // (fully unrolled: every LDS operand read is issued ahead of the chain)
+      for (int item = wave; item < 2 * RT; item += kWaves) {
+        const int rt = item >> 1;
+        const bool is_v = (item & 1) == 0;
+        f32x16 T = f32x16{};
+        if (is_v) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int ee = acc_row(v, h);
-        if (ee < n && l32 < K2) dstp[ee * K2 + l32] = T[v];
+          for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
+            const int k = 2 * s2 + h;
+            const float av = (l32 < n && k < d) ? sY[l32 * d + k] : 0.f;
+            const float bv = k < d ? sB[k * bs + rt * kTile + l32] : 0.f;
+            T = mfma32(av, bv, T);
+          }
+        } else {
+#pragma unroll
+          for (int s2 = 0; s2 < kMaxRadial / 2; ++s2) {
+            if (2 * s2 < nr) {
+              const int q = 2 * s2 + h;
+              const float av = (l32 < n && q < nr) ? sPhi[l32 * nr + q] : 0.f;
+              const float bv = q < nr ? sWr[q * bs + rt * kTile + l32] : 0.f;
+              T = mfma32(av, bv, T);
+            }
+          }
+        }
+        float* dstp = is_v ? sV : sRho;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int e = acc_row(v, h);
+          if (e < n) dstp[e * bs + rt * kTile + l32] = T[v];
+        }
       }
-    }
-    __syncthreads();
-    for (int t = tid; t < n; t += blockDim.x) {
-      const int eid = sEid[t];
-      const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
-      const float rn = sqrtf(vx * vx + vy * vy + vz * vz);
-      float gx = 0.f, gy = 0.f, gzv = 0.f;
-      for (int k = 0; k < d; ++k) {
-        const float dy = sDY[t * d + k];
-        gx += dy * sJ[t * 3 * d + 3 * k];
-        gy += dy * sJ[t * 3 * d + 3 * k + 1];
-        gzv += dy * sJ[t * 3 * d + 3 * k + 2];
+      EdgeRec next{};
+      load_rec(next_eid, nn, next);
+      // ---- the chunk in segment pieces
+      for (int p0 = 0; p0 < n;) {
+        __syncthreads();  // v/rho written; the previous piece's edges done with sGz
+        const int seg = __builtin_amdgcn_readfirstlane(sKey[p0]);
+        int p1 = p0 + 1;
+        while (p1 < n && sKey[p1] == seg) ++p1;
+        p1 = __builtin_amdgcn_readfirstlane(p1);
+        if (seg != cur) {
+          // Gz[seg] rows j < 32 in parts, zero from row d and from channel C:
+          // one thread per pair of channels
+          for (int i = tid; i < kTile * (Cp / 2); i += blockDim.x) {
+            const int j = i / (Cp / 2), c2 = 2 * (i - j * (Cp / 2));
+            float2 g = make_float2(0.f, 0.f);
+            if (j < d && c2 < C) g = *reinterpret_cast<const float2*>(a.Gz + (size_t(seg) * d + j) * C + c2);
+            uint16_t part[3][2];
+            if constexpr (P == 3) {
+              split_bf16x3(g.x, part[0][0], part[1][0], part[2][0]);
+              split_bf16x3(g.y, part[0][1], part[1][1], part[2][1]);
+            } else {
+              part[0][0] = bf16_rne_bits(g.x);
+              part[0][1] = bf16_rne_bits(g.y);
+            }
+#pragma unroll
+            for (int p = 0; p < P; ++p)
+              *reinterpret_cast<uint32_t*>(sGz + j * gzs + p * Cp + c2) = pack2(part[p][0], part[p][1]);
+          }
+          cur = seg;
+          __syncthreads();
+        }
+        wave_edges(p0, p1);
+        p0 = p1;
       }
-      float dr = 0.f;
-      for (int q = 0; q < nr; ++q) {
-        const float u = (rn - float(q) * a.sigma) / a.sigma;
-        dr += sDPhi[t * nr + q] * (-u / a.sigma) * sPhi[t * nr + q];
+      __syncthreads();
+      // ---- dY = dV B^T (k < d), dphi = dRho Wrad^T (q < nr); K = ranks,
+      // one quarter of the ranks per wave, partial products summed in a
+      // fixed order by the gradient below
+      {
+        static_assert(kWaves == 8 && kRing % 2 == 0, "two products x four rank quarters");
+        const bool is_y = wave < 4;
+        const int rq = wave & 3;
+        const int K2 = is_y ? d : nr;
+        const float* src = is_y ? sV : sRho;
+        const float* fac = is_y ? sB : sWr;
+        f32x16 T = f32x16{};
+#pragma unroll
+        for (int s2 = 0; s2 < RT * 4; ++s2) {
+          const int r = rq * (RT * 8) + 2 * s2 + h;
+          const float av = l32 < n ? src[l32 * bs + r] : 0.f;
+          const float bv = l32 < K2 ? fac[l32 * bs + r] : 0.f;
+          T = mfma32(av, bv, T);
+        }
+        float* dstp = is_y ? sDY + rq * chunk * d : sDPhi + rq * chunk * nr;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int ee = acc_row(v, h);
+          if (ee < n && l32 < K2) dstp[ee * K2 + l32] = T[v];
+        }
       }
-      const float inv = 1.f / rn;
-      a.grad_vec[3 * eid] = gx + dr * vx * inv;
-      a.grad_vec[3 * eid + 1] = gy + dr * vy * inv;
-      a.grad_vec[3 * eid + 2] = gzv + dr * vz * inv;
+      __syncthreads();
+      for (int t = tid; t < n; t += blockDim.x) {
+        const int eid = sEid[t];
+        const float vx = sVec[3 * t], vy = sVec[3 * t + 1], vz = sVec[3 * t + 2];
+        const float rn = sqrtf(vx * vx + vy * vy + vz * vz);
+        float gx = 0.f, gy = 0.f, gzv = 0.f;
+        for (int k = 0; k < d; ++k) {
+          const int i = t * d + k;
+          const float dy = ((sDY[i] + sDY[chunk * d + i]) + sDY[2 * chunk * d + i]) + sDY[3 * chunk * d + i];
+          gx += dy * sJ[t * 3 * d + 3 * k];
+          gy += dy * sJ[t * 3 * d + 3 * k + 1];
+          gzv += dy * sJ[t * 3 * d + 3 * k + 2];
+        }
+        float dr = 0.f;
+        for (int q = 0; q < nr; ++q) {
+          const float u = (rn - float(q) * a.sigma) / a.sigma;
+          const int i = t * nr + q;
+          const float dphi =
+              ((sDPhi[i] + sDPhi[chunk * nr + i]) + sDPhi[2 * chunk * nr + i]) + sDPhi[3 * chunk * nr + i];
+          dr += dphi * (-u / a.sigma) * sPhi[i];
+        }
+        const float inv = 1.f / rn;
+        a.grad_vec[3 * eid] = gx + dr * vx * inv;
+        a.grad_vec[3 * eid + 1] = gy + dr * vy * inv;
+        a.grad_vec[3 * eid + 2] = gzv + dr * vz * inv;
+      }
+      if (npc >= per_block) break;
+      pc = npc;
+      cb = ncb;
+      hi = nhi;
+      rec = next;
     }
   }
 }
@@ -393,6 +520,7 @@ inline int dst2_chunk(int RT, bool bf, int d, int n_radial, int C) {
 
 template <int L, int RT, bool BF>
 hipError_t launch_l_rt(const BwdDstArgs& a, int n_range, hipStream_t s) {
+  if (a.pieces_per_block < 1 || n_range % a.pieces_per_block) return hipErrorInvalidValue;
   constexpr int d = (L + 1) * (L + 1);
   const int chunk = dst2_chunk(RT, BF, d, a.n_radial, a.C);
   const size_t lds = size_t(dst2_smem(RT, BF ? 1 : 3, d, a.n_radial, a.C, chunk).floats) * 4;
@@ -401,7 +529,7 @@ hipError_t launch_l_rt(const BwdDstArgs& a, int n_range, hipStream_t s) {
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      int(lds));
   if (e != hipSuccess) return e;
-  k<<<dim3(n_range), dim3(kWaves * kWave), lds, s>>>(a, n_range, chunk);
+  k<<<dim3(n_range / a.pieces_per_block), dim3(kWaves * kWave), lds, s>>>(a, n_range, chunk);
   return hipGetLastError();
 }
 

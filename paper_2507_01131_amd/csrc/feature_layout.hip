@@ -72,25 +72,24 @@ hipError_t launch_p(int N, int d, int C, const TI* x, void* xs, hipStream_t s) {
   return edge_kpad(d) == 32 ? launch_dp<32, P>(N, d, C, x, o, s) : launch_dp<64, P>(N, d, C, x, o, s);
 }
 
-// xc[n][k][p][c] for k < DP (zero rows from d), p < P, c < C: the bf16 parts
-// with the channel fastest, one thread per run of eight channels.
+// xc[n][k][p][c] for k < d, p < P, c < Cp (zero channels from C): the bf16
+// parts with the channel fastest, one thread per run of eight channels.
 template <int P, typename TI>
-__global__ __launch_bounds__(256) void k_channel_layout(int N, int d, int DP, int C, const TI* __restrict__ x,
+__global__ __launch_bounds__(256) void k_channel_layout(int N, int d, int C, int Cp, const TI* __restrict__ x,
                                                         uint16_t* __restrict__ xc) {
-  const int groups = C / 8;
+  const int groups = Cp / 8;
   const size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= size_t(N) * DP * groups) return;
+  if (i >= size_t(N) * d * groups) return;
   const int g = int(i % groups);
-  const size_t nk = i / groups;
-  const int k = int(nk % DP);
-  const size_t n = nk / DP;
+  const size_t nk = i / groups;  // n * d + k
   uint32_t w[P][4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     uint16_t part[3][2];
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      const float v = k < d ? to_f32(x[(n * d + k) * C + 8 * g + 2 * q + e]) : 0.f;
+      const int c = 8 * g + 2 * q + e;
+      const float v = c < C ? to_f32(x[nk * C + c]) : 0.f;
       if constexpr (P == 3)
         split_bf16x3(v, part[0][e], part[1][e], part[2][e]);
       else
@@ -99,17 +98,17 @@ __global__ __launch_bounds__(256) void k_channel_layout(int N, int d, int DP, in
 #pragma unroll
     for (int s = 0; s < P; ++s) w[s][q] = uint32_t(part[s][0]) | (uint32_t(part[s][1]) << 16);
   }
-  uint16_t* dst = xc + (nk * P) * C + 8 * g;
+  uint16_t* dst = xc + (nk * P) * Cp + 8 * g;
 #pragma unroll
   for (int s = 0; s < P; ++s)
-    *reinterpret_cast<u32x4*>(dst + size_t(s) * C) = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
+    *reinterpret_cast<u32x4*>(dst + size_t(s) * Cp) = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
 }
 
 template <int P, typename TI>
-hipError_t launch_channel_p(int N, int d, int C, const TI* x, void* xc, hipStream_t s) {
-  const size_t items = size_t(N) * edge_kpad(d) * (C / 8);
-  k_channel_layout<P, TI><<<dim3(unsigned((items + 255) / 256)), dim3(256), 0, s>>>(
-      N, d, edge_kpad(d), C, x, static_cast<uint16_t*>(xc));
+hipError_t launch_channel_p(int N, int d, int C, int Cp, const TI* x, void* xc, hipStream_t s) {
+  const size_t items = size_t(N) * d * (Cp / 8);
+  k_channel_layout<P, TI><<<dim3(unsigned((items + 255) / 256)), dim3(256), 0, s>>>(N, d, C, Cp, x,
+                                                                                    static_cast<uint16_t*>(xc));
   return hipGetLastError();
 }
 
@@ -117,16 +116,17 @@ hipError_t launch_channel_p(int N, int d, int C, const TI* x, void* xc, hipStrea
 
 int edge_kpad(int d) { return d <= 32 ? 32 : 64; }
 
-hipError_t launch_channel_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xc,
+hipError_t launch_channel_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xc,
                                  hipStream_t s) {
   if (N == 0) return hipSuccess;
+  if (Cp < C || Cp % 8 || C % 2) return hipErrorInvalidValue;
   if (parts == 3) {
     if (!x_is_f32) return hipErrorInvalidValue;
-    return launch_channel_p<3>(N, d, C, static_cast<const float*>(x), xc, s);
+    return launch_channel_p<3>(N, d, C, Cp, static_cast<const float*>(x), xc, s);
   }
   if (parts != 1) return hipErrorInvalidValue;
-  return x_is_f32 ? launch_channel_p<1>(N, d, C, static_cast<const float*>(x), xc, s)
-                  : launch_channel_p<1>(N, d, C, static_cast<const uint16_t*>(x), xc, s);
+  return x_is_f32 ? launch_channel_p<1>(N, d, C, Cp, static_cast<const float*>(x), xc, s)
+                  : launch_channel_p<1>(N, d, C, Cp, static_cast<const uint16_t*>(x), xc, s);
 }
 
 hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,

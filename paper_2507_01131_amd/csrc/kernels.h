@@ -70,9 +70,10 @@ EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E);
 int edge_kpad(int d);
 hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,
                                  hipStream_t s);
-// The same parts with the channel fastest: xc [N, edge_kpad(d), parts, C]
-// bfloat16 (rows from d zero), for contractions over channels.
-hipError_t launch_channel_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xc,
+// The same parts with the channel fastest: xc [N, d, parts, Cp] bfloat16
+// (channels from C zero, Cp >= C a multiple of 8), for contractions over
+// channels.
+hipError_t launch_channel_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xc,
                                  hipStream_t s);
 // parts = 3: fp32 features (exact split), parts = 1: bf16 features
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
@@ -105,12 +106,17 @@ struct BwdDstArgs {
   const void* x;            // [N, d, C]
   const float* Gz;          // [N, d, C] = grad_out W^T
   float* grad_vec;          // [E, 3] by edge id
-  const void* xc;           // [N, 32, parts, C] bf16 (launch_channel_layout of x), d <= 32
-  int n_range;              // equal edge ranges, one per workgroup (bwd_dst_plan)
+  const void* xc;           // [N, d, parts, bwd_dst_cpad(C, bf16)] bf16 (launch_channel_layout of x)
+  int n_range;              // equal edge ranges (bwd_dst_plan)
+  int pieces_per_block;     // ranges per workgroup
 };
-// Edge ranges of the destination-side kernel on the current device (0 when
-// the problem takes the per-segment kernels: d > 32 or no LDS fit).
-int bwd_dst_plan(int L, int R, int C, int n_radial, bool bf16, int E);
+// Edge ranges of the destination-side kernel on the current device
+// (n_range = 0 when the problem takes the per-segment kernels: d > 32 or no
+// LDS fit): per_block ranges per workgroup, workgroup b taking ranges
+// b, b + n_range / per_block, ...
+EdgePlan bwd_dst_plan(int L, int R, int C, int n_radial, bool bf16, int E);
+// channel count of its x layout: C padded to the kernel's ring turn
+int bwd_dst_cpad(int C, bool bf16);
 hipError_t launch_bwd_dst(const BwdDstArgs& a, bool x_bf16, hipStream_t s);
 
 // ---------------------------------------------------------------- misc
