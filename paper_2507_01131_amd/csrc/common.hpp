@@ -45,6 +45,23 @@ __device__ __forceinline__ void split_bf16x3(float v, uint16_t& hi, uint16_t& mi
   lo = bf16_rne_bits(r2);
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+// Two floats rounded to bfloat16 (nearest even) and packed, a in the low
+// half: one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16x2_rne(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
+}
+// split_bf16x3 of two floats at once, each part packed as by pack_bf16x2_rne
+// (the same parts, bit for bit, in half the conversions).
+__device__ __forceinline__ void split_bf16x3_pair(float a, float b, uint32_t& hi, uint32_t& mid, uint32_t& lo) {
+  hi = pack_bf16x2_rne(a, b);
+  const float ra = a - __uint_as_float(hi << 16), rb = b - __uint_as_float(hi & 0xffff0000u);
+  mid = pack_bf16x2_rne(ra, rb);
+  const float sa = ra - __uint_as_float(mid << 16), sb = rb - __uint_as_float(mid & 0xffff0000u);
+  lo = pack_bf16x2_rne(sa, sb);
+}
+
 // Blocks of a 1-D grid are dealt to the XCDs round-robin (block b runs on XCD
 // b % 8).  Remap so that each XCD walks one contiguous range of logical work
 // items: neighbouring destination nodes share source nodes, and then share

@@ -73,10 +73,10 @@ struct Smem {
 
 // LDS regions (floats): B and Wrad rows (padded stride bs so row-wise
 // operand reads across lanes hit distinct banks), the factor A parts in T
-// operand order [q][rank tile][part][64 lanes] x 16 bytes, D [32][Rp], the
-// staged Gz parts [32 rows][gzs halves] (gzs = P*C + 8: rows 16 bytes apart
-// in bank terms), and the chunk's v, rho, Y, Phi, dY, dPhi, Jacobian and
-// per-edge indices.
+// operand order [q][rank tile][part][64 lanes] x 16 bytes, D in accumulator
+// order [rank tile][4][64 lanes] x 16 bytes, the staged Gz parts
+// [32 rows][gzs halves] (gzs = P*Cp + 8: rows 16 bytes apart in bank terms),
+// and the chunk's v, rho, Y, Phi, dY, dPhi, Jacobian and per-edge records.
 __host__ __device__ inline Smem dst2_smem(int RT, int P, int d, int n_radial, int C, int chunk) {
   Smem s{};
   s.Rp = RT * kTile;
@@ -114,7 +114,6 @@ __host__ __device__ inline Smem dst2_smem(int RT, int P, int d, int n_radial, in
   return s;
 }
 
-__device__ __forceinline__ uint32_t pack2(uint16_t lo, uint16_t hi) { return uint32_t(lo) | (uint32_t(hi) << 16); }
 
 template <int L, int RT, bool BF>
 __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_range, int chunk) {
@@ -128,7 +127,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
   float* sB = smem + S.off_b;
   float* sWr = smem + S.off_wr;
   u32x4* sAp = reinterpret_cast<u32x4*>(smem + S.off_ap);
-  float* sD = smem + S.off_d;
+  f32x4* sDl = reinterpret_cast<f32x4*>(smem + S.off_d);
   uint16_t* sGz = reinterpret_cast<uint16_t*>(smem + S.off_gz);
   float* sV = smem + S.off_v;
   float* sRho = smem + S.off_rho;
@@ -158,10 +157,6 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
     const float v = r < R ? (k < d ? a.Bf[k * R + r] : a.radial_w[(k - d) * R + r]) : 0.f;
     (k < d ? sB + k * bs : sWr + (k - d) * bs)[r] = v;
   }
-  for (int i = tid; i < kTile * Rp; i += blockDim.x) {
-    const int j = i / Rp, r = i - j * Rp;
-    sD[i] = (j < d && r < R) ? a.D[j * R + r] : 0.f;
-  }
   // sAp[((q*RT + rt)*P + p)*64 + lane'] = part p of A[t_row(q, h', i)][rt*32 + l32'], i = 0..7
   for (int t = tid; t < 2 * RT * kWave; t += blockDim.x) {
     const int ln = t % kWave, qrt = t / kWave;
@@ -170,21 +165,30 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
     uint32_t w[P][4];
 #pragma unroll
     for (int p2 = 0; p2 < 4; ++p2) {
-      uint16_t part[3][2];
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int k = t_row(q, hh, 2 * p2 + e);
-        const float v = (k < d && r < R) ? a.A[k * R + r] : 0.f;
-        if constexpr (P == 3)
-          split_bf16x3(v, part[0][e], part[1][e], part[2][e]);
-        else
-          part[0][e] = bf16_rne_bits(v);
-      }
-#pragma unroll
-      for (int p = 0; p < P; ++p) w[p][p2] = pack2(part[p][0], part[p][1]);
+      const int k0 = t_row(q, hh, 2 * p2), k1 = t_row(q, hh, 2 * p2 + 1);
+      const float v0 = (k0 < d && r < R) ? a.A[k0 * R + r] : 0.f;
+      const float v1 = (k1 < d && r < R) ? a.A[k1 * R + r] : 0.f;
+      if constexpr (P == 3)
+        split_bf16x3_pair(v0, v1, w[0][p2], w[1][p2], w[2][p2]);
+      else
+        w[0][p2] = pack_bf16x2_rne(v0, v1);
     }
 #pragma unroll
     for (int p = 0; p < P; ++p) sAp[(qrt * P + p) * kWave + ln] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
+  }
+  // sDl[(rt*4 + qq)*64 + lane'][i] = D[acc_row(4 qq + i, h')][rt*32 + l32']: the D
+  // values lane' weighs its T accumulators with, one 16-byte read per quarter
+  for (int t = tid; t < RT * 4 * kWave; t += blockDim.x) {
+    const int ln = t % kWave, rq = t / kWave;
+    const int rt = rq / 4, qq = rq % 4;
+    const int r = rt * kTile + (ln & 31);
+    f32x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = acc_row(4 * qq + i, ln >> 5);
+      v[i] = (j < d && r < R) ? a.D[j * R + r] : 0.f;
+    }
+    sDl[t] = v;
   }
 
   // ---- per edge: S_e, T_e, dg -> dv, drho (in place in sV, sRho)
@@ -243,47 +247,55 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
       uint32_t w[P][4];
 #pragma unroll
       for (int p2 = 0; p2 < 4; ++p2) {
-        uint16_t part[3][2];
-#pragma unroll
-        for (int e2 = 0; e2 < 2; ++e2) {
-          const float v = Sacc[8 * q + 2 * p2 + e2];
-          if constexpr (P == 3)
-            split_bf16x3(v, part[0][e2], part[1][e2], part[2][e2]);
-          else
-            part[0][e2] = bf16_rne_bits(v);
-        }
-#pragma unroll
-        for (int p = 0; p < P; ++p) w[p][p2] = pack2(part[p][0], part[p][1]);
+        const float v0 = Sacc[8 * q + 2 * p2], v1 = Sacc[8 * q + 2 * p2 + 1];
+        if constexpr (P == 3)
+          split_bf16x3_pair(v0, v1, w[0][p2], w[1][p2], w[2][p2]);
+        else
+          w[0][p2] = pack_bf16x2_rne(v0, v1);
       }
 #pragma unroll
       for (int p = 0; p < P; ++p) sp[q][p] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
     }
+    // the factor operands one rank tile ahead of the MFMA; D values and the
+    // edge's v and rho ahead of the tile's MFMA
+    u32x4 ap[2][2][P];
+    auto load_a = [&](int rt, int b) {
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int p = 0; p < P; ++p) ap[b][q][p] = sAp[((q * RT + rt) * P + p) * kWave + lane];
+    };
+    load_a(0, 0);
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
+      if (rt + 1 < RT) load_a(rt + 1, (rt + 1) & 1);
+      f32x4 dl[4];
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq) dl[qq] = sDl[(rt * 4 + qq) * kWave + lane];
+      const float v_e = sV[e * bs + rt * kTile + l32], rho_e = sRho[e * bs + rt * kTile + l32];
       f32x16 T = f32x16{};
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
-        u32x4 ap[P];
-#pragma unroll
-        for (int p = 0; p < P; ++p) ap[p] = sAp[((q * RT + rt) * P + p) * kWave + lane];
+        const u32x4(&a_)[P] = ap[rt & 1][q];
         if constexpr (P == 3) {
-          T = mfma_bf16(sp[q][0], ap[2], T);
-          T = mfma_bf16(sp[q][2], ap[0], T);
-          T = mfma_bf16(sp[q][1], ap[1], T);
-          T = mfma_bf16(sp[q][0], ap[1], T);
-          T = mfma_bf16(sp[q][1], ap[0], T);
+          T = mfma_bf16(sp[q][0], a_[2], T);
+          T = mfma_bf16(sp[q][2], a_[0], T);
+          T = mfma_bf16(sp[q][1], a_[1], T);
+          T = mfma_bf16(sp[q][0], a_[1], T);
+          T = mfma_bf16(sp[q][1], a_[0], T);
         }
-        T = mfma_bf16(sp[q][0], ap[0], T);
+        T = mfma_bf16(sp[q][0], a_[0], T);
       }
-      const int r = rt * kTile + l32;
+      // dg[r] = sum_j D[j, r] T[j, r]: this lane's 16 rows, then the other half
       float part = 0.f;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) part += sD[acc_row(v, h) * Rp + r] * T[v];
-      part += __shfl_xor(part, 32);
+      for (int v = 0; v < 16; ++v) part += dl[v / 4][v % 4] * T[v];
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(part), __float_as_uint(part), false, false);
+      part = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
       if (h == 0) {
-        const float dv = part * sRho[e * bs + r], drho = part * sV[e * bs + r];
-        sV[e * bs + r] = dv;
-        sRho[e * bs + r] = drho;
+        const int r = rt * kTile + l32;
+        sV[e * bs + r] = part * rho_e;  // dv
+        sRho[e * bs + r] = part * v_e;  // drho
       }
     }
   };
@@ -432,17 +444,13 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
             const int j = i / (Cp / 2), c2 = 2 * (i - j * (Cp / 2));
             float2 g = make_float2(0.f, 0.f);
             if (j < d && c2 < C) g = *reinterpret_cast<const float2*>(a.Gz + (size_t(seg) * d + j) * C + c2);
-            uint16_t part[3][2];
-            if constexpr (P == 3) {
-              split_bf16x3(g.x, part[0][0], part[1][0], part[2][0]);
-              split_bf16x3(g.y, part[0][1], part[1][1], part[2][1]);
-            } else {
-              part[0][0] = bf16_rne_bits(g.x);
-              part[0][1] = bf16_rne_bits(g.y);
-            }
+            uint32_t w[3];
+            if constexpr (P == 3)
+              split_bf16x3_pair(g.x, g.y, w[0], w[1], w[2]);
+            else
+              w[0] = pack_bf16x2_rne(g.x, g.y);
 #pragma unroll
-            for (int p = 0; p < P; ++p)
-              *reinterpret_cast<uint32_t*>(sGz + j * gzs + p * Cp + c2) = pack2(part[p][0], part[p][1]);
+            for (int p = 0; p < P; ++p) *reinterpret_cast<uint32_t*>(sGz + j * gzs + p * Cp + c2) = w[p];
           }
           cur = seg;
           __syncthreads();

@@ -64,7 +64,7 @@ __device__ __forceinline__ f32x16 mfma_bf16(u32x4 a, u32x4 b, f32x16 c) {
 constexpr int kMaxWavesPerBlock = 4;
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return uint32_t(bf16_rne_bits(lo)) | (uint32_t(bf16_rne_bits(hi)) << 16);
+  return pack_bf16x2_rne(lo, hi);
 }
 
 __host__ __device__ constexpr int edge_dp(int d) { return d <= 32 ? 32 : 64; }
