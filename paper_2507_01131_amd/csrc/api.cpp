@@ -59,7 +59,7 @@ int feature_parts(const tdn_problem& p) { return p.feat_dtype == TDN_BF16 ? 1 : 
 size_t xt_bytes(const tdn_problem& p) {
   return size_t(p.n_nodes) * p.C * feature_parts(p) * tdn::edge_kpad(dim_of(p.L)) * 2;
 }
-// the same region holds, in the backward, x with the channel fastest for
+// the same region holds, in the backward, x blocked over channels for
 // the destination-side kernel
 size_t xt_xc_bytes(const tdn_problem& p) {
   const size_t xc =
@@ -378,7 +378,7 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
     a.n_range = dp.n_range;
     a.pieces_per_block = dp.per_block;
     if (a.n_range > 0) {
-      // x with the channel fastest, in parts, for the contraction over channels
+      // x in parts, blocked as MFMA operands for the contraction over channels
       // (the region is free until the grad_x pass lays out Gz there)
       Timed t("channel_layout", stream);
       TDN_HIP(tdn::launch_channel_layout(N, d, C, tdn::bwd_dst_cpad(C, bf16), x, !bf16, feature_parts(*p), ws + lay.xt,

@@ -23,9 +23,9 @@
 // (edge, function); v = Y B and rho = Phi Wrad as small fp32 MFMA GEMMs; then
 // the chunk in segment pieces: the piece's Gz[t] is split into LDS once, and
 // each wave takes whole edges: S_e (K-steps of 16 channels; the x operand
-// comes straight from global memory in the channel-fastest layout
-// xc [N, d, P, Cp], one 16-byte load per part, through a per-wave prefetch
-// ring), T_e per rank tile (the accumulator registers of S regroup into the
+// comes straight from global memory, laid out in MFMA operand blocks per
+// node, part and K-step, one contiguous 16-byte-per-lane load per part,
+// through a per-wave prefetch ring), T_e per rank tile (the accumulator registers of S regroup into the
 // A operand of a 32x32x16 step, so the factor A is stored with the same row
 // permutation), dg, dv and drho.  Last dY = dV B^T and dphi = dRho Wrad^T
 // (fp32 MFMA) and the gradient per edge.
@@ -197,14 +197,15 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
   // that edge's first loads are in flight while this edge's T runs.  A slot
   // is KPS K-steps of 16 channels; the channel count is padded to whole ring
   // turns (zero channels in x and in the staged Gz), so every edge starts on
-  // slot 0.  The loads are buffer loads over one node's row of xc: lanes of
+  // slot 0.  The loads are buffer loads over one node's blocks of xc: lanes of
   // rows k >= d and a missing next edge (a record of no bytes) read zeros
   // through the range check, with no branch that would drain the ring.  The
   // Gz operand is read from LDS one slot ahead.
   const int Cp = dst2_cpad(C, P), nsl = Cp / (16 * KPS);
   const char* __restrict__ xc = static_cast<const char*>(a.xc);
   const int xrow = d * P * Cp * 2;  // bytes per node
-  const uint32_t xoff = l32 < d ? uint32_t((l32 * P * Cp + 8 * h) * 2) : 0x80000000u;
+  const int xstep = 2 * d * 16;     // bytes per MFMA operand block (part, K-step)
+  const uint32_t xoff = l32 < d ? uint32_t((h * d + l32) * 16) : 0x80000000u;
   const uint16_t* gzl = sGz + l32 * gzs + 8 * h;  // lane's Gz row j = l32
   auto row_rsrc = [&](int row, bool valid) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(xc) + size_t(row) * xrow, 0, valid ? xrow : 0,
@@ -216,7 +217,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
 #pragma unroll
       for (int p = 0; p < P; ++p)
         xb[kk][p] = __builtin_bit_cast(
-            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, xoff, (p * Cp + 16 * (sl * KPS + kk)) * 2, 0));
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, xoff, (p * (Cp / 16) + sl * KPS + kk) * xstep, 0));
   };
   auto load_g = [&](int sl, u32x4 (&g)[KPS][P]) {
 #pragma unroll

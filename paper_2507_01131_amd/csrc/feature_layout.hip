@@ -9,7 +9,7 @@
 // One block per node: the node's [d, C] rows are staged in LDS, then each
 // thread writes groups of eight k for one channel and all P parts.
 // The backward's destination kernel contracts over channels instead and reads
-// the channel-fastest layout xc [N, DP, P, C] (launch_channel_layout).
+// x in MFMA operand blocks over channels (launch_channel_layout).
 #include "common.hpp"
 #include "kernels.h"
 
@@ -72,41 +72,45 @@ hipError_t launch_p(int N, int d, int C, const TI* x, void* xs, hipStream_t s) {
   return edge_kpad(d) == 32 ? launch_dp<32, P>(N, d, C, x, o, s) : launch_dp<64, P>(N, d, C, x, o, s);
 }
 
-// xc[n][k][p][c] for k < d, p < P, c < Cp (zero channels from C): the bf16
-// parts with the channel fastest, one thread per run of eight channels.
+// xc[n][p][s][h][k][i] = part p of x[n][k][16 s + 8 h + i] (zero from
+// channel C): for every node, part and K-step s of 16 channels, the operand
+// block of a 32x32x16 MFMA with the rows k < d, so that the 64 lanes of a
+// wave read one contiguous block.  One thread per (node, s, h, k), k fastest.
 template <int P, typename TI>
 __global__ __launch_bounds__(256) void k_channel_layout(int N, int d, int C, int Cp, const TI* __restrict__ x,
                                                         uint16_t* __restrict__ xc) {
-  const int groups = Cp / 8;
+  const int nks = Cp / 16;
   const size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= size_t(N) * d * groups) return;
-  const int g = int(i % groups);
-  const size_t nk = i / groups;  // n * d + k
+  if (i >= size_t(N) * nks * 2 * d) return;
+  const int k = int(i % d);
+  size_t rest = i / d;
+  const int h = int(rest % 2);
+  rest /= 2;
+  const int st = int(rest % nks);
+  const size_t n = rest / nks;
+  const int c0 = 16 * st + 8 * h;
+  const TI* src = x + (n * d + k) * C;
   uint32_t w[P][4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    uint16_t part[3][2];
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int c = 8 * g + 2 * q + e;
-      const float v = c < C ? to_f32(x[nk * C + c]) : 0.f;
-      if constexpr (P == 3)
-        split_bf16x3(v, part[0][e], part[1][e], part[2][e]);
-      else
-        part[0][e] = bf16_rne_bits(v);
-    }
-#pragma unroll
-    for (int s = 0; s < P; ++s) w[s][q] = uint32_t(part[s][0]) | (uint32_t(part[s][1]) << 16);
+    const int c = c0 + 2 * q;
+    const float v0 = c < C ? to_f32(src[c]) : 0.f;
+    const float v1 = c + 1 < C ? to_f32(src[c + 1]) : 0.f;
+    if constexpr (P == 3)
+      split_bf16x3_pair(v0, v1, w[0][q], w[1][q], w[2][q]);
+    else
+      w[0][q] = pack_bf16x2_rne(v0, v1);
   }
-  uint16_t* dst = xc + (nk * P) * Cp + 8 * g;
 #pragma unroll
-  for (int s = 0; s < P; ++s)
-    *reinterpret_cast<u32x4*>(dst + size_t(s) * Cp) = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
+  for (int p = 0; p < P; ++p) {
+    uint16_t* dst = xc + ((((n * P + p) * nks + st) * 2 + h) * d + k) * 8;
+    *reinterpret_cast<u32x4*>(dst) = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
+  }
 }
 
 template <int P, typename TI>
 hipError_t launch_channel_p(int N, int d, int C, int Cp, const TI* x, void* xc, hipStream_t s) {
-  const size_t items = size_t(N) * d * (Cp / 8);
+  const size_t items = size_t(N) * (Cp / 16) * 2 * d;
   k_channel_layout<P, TI><<<dim3(unsigned((items + 255) / 256)), dim3(256), 0, s>>>(N, d, C, Cp, x,
                                                                                     static_cast<uint16_t*>(xc));
   return hipGetLastError();
@@ -119,7 +123,7 @@ int edge_kpad(int d) { return d <= 32 ? 32 : 64; }
 hipError_t launch_channel_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xc,
                                  hipStream_t s) {
   if (N == 0) return hipSuccess;
-  if (Cp < C || Cp % 8 || C % 2) return hipErrorInvalidValue;
+  if (Cp < C || Cp % 16) return hipErrorInvalidValue;
   if (parts == 3) {
     if (!x_is_f32) return hipErrorInvalidValue;
     return launch_channel_p<3>(N, d, C, Cp, static_cast<const float*>(x), xc, s);

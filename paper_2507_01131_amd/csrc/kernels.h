@@ -70,9 +70,11 @@ EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E);
 int edge_kpad(int d);
 hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,
                                  hipStream_t s);
-// The same parts with the channel fastest: xc [N, d, parts, Cp] bfloat16
-// (channels from C zero, Cp >= C a multiple of 8), for contractions over
-// channels.
+// The same parts blocked for contractions over channels:
+// xc [N, parts, Cp / 16, 2, d, 8] bfloat16, element [n][p][s][h][k][i] = part
+// p of x[n][k][16 s + 8 h + i] (zero from channel C; Cp >= C a multiple of
+// 16): per node, part and K-step of 16 channels one 32x32x16 MFMA operand
+// block of rows k < d.
 hipError_t launch_channel_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xc,
                                  hipStream_t s);
 // parts = 3: fp32 features (exact split), parts = 1: bf16 features
@@ -106,7 +108,7 @@ struct BwdDstArgs {
   const void* x;            // [N, d, C]
   const float* Gz;          // [N, d, C] = grad_out W^T
   float* grad_vec;          // [E, 3] by edge id
-  const void* xc;           // [N, d, parts, bwd_dst_cpad(C, bf16)] bf16 (launch_channel_layout of x)
+  const void* xc;           // x blocked by launch_channel_layout with Cp = bwd_dst_cpad(C, bf16)
   int n_range;              // equal edge ranges (bwd_dst_plan)
   int pieces_per_block;     // ranges per workgroup
 };
