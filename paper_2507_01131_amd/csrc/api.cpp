@@ -57,7 +57,7 @@ int feature_parts(const tdn_problem& p) { return p.feat_dtype == TDN_BF16 ? 1 : 
 
 // transposed features for the edge pass
 size_t xt_bytes(const tdn_problem& p) {
-  return size_t(p.n_nodes) * p.C * feature_parts(p) * tdn::edge_kpad(dim_of(p.L)) * 2;
+  return size_t(p.n_nodes) * ((p.C + 31) / 32 * 32) * feature_parts(p) * tdn::edge_kpad(dim_of(p.L)) * 2;
 }
 // the same region holds, in the backward, x blocked over channels for
 // the destination-side kernel

@@ -280,26 +280,28 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   };
 
   // Feature operands of one edge: part s (split mode) or channel tile t
-  // (bf16 mode), K-block b is the 16-byte run xs[row][c][s][16b + 8h .. +7].
-  // The gathered row is wave-uniform (row base in scalar registers, one
-  // 32-bit lane offset per load).  Lanes with c >= C read channel C - 1;
-  // their results are never stored.
+  // (bf16 mode), K-block b is the lane's 16 bytes of the operand block
+  // xs[row][tile][s][b]: the 64 lanes of a load read one contiguous
+  // kilobyte.  The gathered row is wave-uniform (row base in scalar
+  // registers, one 32-bit lane offset per tile).  Channel tiles past the
+  // layout's last read that tile; their results are never stored.
   constexpr int XB = BF ? CT : XP;  // operand rows per edge
   const char* __restrict__ xs = static_cast<const char*>(a.feat);
+  const int n_ct = (C + kTile - 1) / kTile;  // channel tiles of the layout
   uint32_t lane_off[CT];
 #pragma unroll
   for (int t = 0; t < CT; ++t) {
-    const int c = c0 + t * kTile;
-    lane_off[t] = ((uint32_t(c < C ? c : C - 1) * XP) * DP + 8 * h) * 2;
+    const int ct = min((cgrp * waves + wave) * CT + t, n_ct - 1);
+    lane_off[t] = uint32_t(ct * XP * KB * 1024 + h * 512 + l32 * 16);
   }
   auto load_x = [&](int row, u32x4 (&xb)[XB][KB]) {
-    const char* p = xs + size_t(row) * (size_t(C) * XP * DP * 2);
+    const char* p = xs + size_t(row) * (size_t(n_ct) * XP * KB * 1024);
 #pragma unroll
     for (int s = 0; s < XB; ++s)
 #pragma unroll
       for (int b = 0; b < KB; ++b)
-        xb[s][b] = BF ? *reinterpret_cast<const u32x4*>(p + lane_off[s] + uint32_t(16 * b * 2))
-                      : *reinterpret_cast<const u32x4*>(p + lane_off[0] + uint32_t((s * DP + 16 * b) * 2));
+        xb[s][b] = BF ? *reinterpret_cast<const u32x4*>(p + lane_off[s] + uint32_t(b * 1024))
+                      : *reinterpret_cast<const u32x4*>(p + lane_off[0] + uint32_t((s * KB + b) * 1024));
   };
   // U_e = KF^T x[row] for one rank tile from the six part products (smallest
   // first), then acc += g_e * U_e with g for this lane's rows

@@ -1,13 +1,15 @@
-// Feature layout for the edge pass: x [N, d, C] becomes
-// xs [N, C, P, DP] bfloat16 with the degree index k fastest, zero padded to
-// DP = 32 (d <= 32) or 64, so that a lane of the 32x32x16 bf16 MFMA reads
-// the eight consecutive k it needs with one 16-byte load.
+// Feature layout for the edge pass: x [N, d, C] becomes bfloat16 operand
+// blocks of the 32x32x16 MFMA, xs [N, Cq/32, P, DP/16, 2, 32, 8]: element
+// [n][ct][s][b][h][c][i] is part s of x[n][16 b + 8 h + i][32 ct + c], zero
+// for k >= d (DP = 32 for d <= 32, else 64) and for channels from C (Cq is C
+// rounded up to 32).  Lane (h, c) of a wave reads its eight k with one
+// 16-byte load, and the 64 lanes read one contiguous kilobyte.
 //   P = 3 (fp32 problems): the exact three-way split hi/mid/lo of every fp32
 //         value, x = hi + mid + lo;
 //   P = 1 (bf16 problems): x itself (bf16 input), or an fp32 input (the
 //         backward's Gz) rounded to bf16.
 // One block per node: the node's [d, C] rows are staged in LDS, then each
-// thread writes groups of eight k for one channel and all P parts.
+// thread writes a group of eight k of one channel in all P parts.
 // The backward's destination kernel contracts over channels instead and reads
 // x in MFMA operand blocks over channels (launch_channel_layout).
 #include "common.hpp"
@@ -30,28 +32,28 @@ __global__ __launch_bounds__(256) void k_feature_layout(int d, int C, const TI* 
   const TI* src = x + size_t(n) * d * C;
   for (int i = threadIdx.x; i < d * C; i += blockDim.x) tile[i] = to_f32(src[i]);
   __syncthreads();
-  uint16_t* dst = xs + size_t(n) * C * P * DP;
-  for (int i = threadIdx.x; i < C * (DP / 8); i += blockDim.x) {
-    const int c = i / (DP / 8), g = i - c * (DP / 8);
+  constexpr int KB = DP / 16;
+  const int Cq = (C + 31) / 32 * 32;
+  uint16_t* dst = xs + size_t(n) * Cq * P * DP;
+  // thread (g, c), c fastest: the eight k = 8 g .. 8 g + 7 of channel c
+  for (int i = threadIdx.x; i < Cq * (DP / 8); i += blockDim.x) {
+    const int g = i / Cq, c = i - g * Cq;
     uint32_t w[P][4];
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      uint16_t part[3][2];
-#pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        const int k = 8 * g + 2 * p + q;
-        const float v = k < d ? tile[k * C + c] : 0.f;
-        if constexpr (P == 3)
-          split_bf16x3(v, part[0][q], part[1][q], part[2][q]);
-        else
-          part[0][q] = bf16_rne_bits(v);  // exact for bf16 input
-      }
-#pragma unroll
-      for (int s = 0; s < P; ++s) w[s][p] = uint32_t(part[s][0]) | (uint32_t(part[s][1]) << 16);
+    for (int q = 0; q < 4; ++q) {
+      const int k = 8 * g + 2 * q;
+      const float v0 = (k < d && c < C) ? tile[k * C + c] : 0.f;
+      const float v1 = (k + 1 < d && c < C) ? tile[(k + 1) * C + c] : 0.f;
+      if constexpr (P == 3)
+        split_bf16x3_pair(v0, v1, w[0][q], w[1][q], w[2][q]);
+      else
+        w[0][q] = pack_bf16x2_rne(v0, v1);  // exact for bf16 input
     }
+    const int ct = c / 32, c32 = c % 32, b = g / 2, h = g % 2;
 #pragma unroll
     for (int s = 0; s < P; ++s)
-      *reinterpret_cast<u32x4*>(dst + (size_t(c) * P + s) * DP + 8 * g) = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
+      *reinterpret_cast<u32x4*>(dst + (((((ct * P + s) * KB + b) * 2 + h) * 32 + c32) * 8)) =
+          u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
   }
 }
 

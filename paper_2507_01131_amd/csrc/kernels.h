@@ -62,8 +62,10 @@ struct EdgePlan {
   int n_range, per_block;
 };
 EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E);
-// Features for the edge pass: x [N, d, C] -> xs [N, C, parts, edge_kpad(d)]
-// bfloat16 (k fastest, zero padded; EdgeArgs::feat = xs): parts = 3 holds
+// Features for the edge pass: x [N, d, C] -> 32x32x16 MFMA operand blocks
+// xs [N, ceil(C/32), parts, edge_kpad(d)/16, 2, 32, 8] bfloat16, element
+// [n][ct][s][b][h][c][i] = part s of x[n][16b + 8h + i][32ct + c], zero
+// padded in k and c (EdgeArgs::feat = xs): parts = 3 holds
 // the exact split x = hi + mid + lo of fp32 features, parts = 1 holds bf16
 // features (an fp32 input is rounded to bf16).  edge_kpad(d) = 32 for
 // d <= 32, else 64.
