@@ -15,9 +15,10 @@ algorithmic flops per launch, E (2RdC + 2Rd + 17R + RC) + N 2dRC, over its
 average launch time from HIP events recorded on its launch stream, against
 the MFMA peak of the arithmetic type of the problem (fp32 157.3 TFLOP/s;
 bf16 2.5 PFLOP/s for bfloat16 features).  For fp32 problems the edge
-contraction runs on bf16 MFMA as six exact part products (fp32 accuracy),
-so the fraction of the fp32 peak can pass 1; the "executed" object then
-gives the bf16 MFMA work the kernel issues against the bf16 peak.  The CPU baseline times the oracle (the
+contraction runs on fp16 MFMA as three products of two-part fp16 splits
+(fp32-level accuracy), so the fraction of the fp32 peak can pass 1; the
+"executed" object then gives the fp16 MFMA work the kernel issues against
+the fp16 peak (2.5 PFLOP/s).  The CPU baseline times the oracle (the
 plain float64 per-edge implementation) on a bounded sample of the same
 workload on this host's cores.
 """
@@ -38,6 +39,7 @@ sys.path.insert(0, ROOT)
 METRIC = "edge tensor products/sec, CP-TP fwd at L=4,C=128,R=128; % MFMA/HBM roofline"
 PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_BF16_MFMA_TFLOPS = 2500.0
+PEAK_FP16_MFMA_TFLOPS = 2500.0
 FACTORS = os.path.join(ROOT, "tests", "golden", "factors")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cp_edge_fwd.json")
 
@@ -203,15 +205,15 @@ def main():
         "forward_tflops": forward_flops(N, E, d, C, R) / (ms_step * 1e-3) / 1e12,
     }
     if not bf16:
-        # bf16 MFMA work issued by the edge contraction: per edge and 32-channel
-        # tile, (K-blocks of 16 degree rows) x (32-rank tiles) x 6 part products
+        # fp16 MFMA work issued by the edge contraction: per edge and 32-channel
+        # tile, (K-blocks of 16 degree rows) x (32-rank tiles) x 3 part products
         # of 2*32*32*16 flops
         kb = 2 if d <= 32 else 4
-        executed = E * ((C + 31) // 32) * kb * ((R + 31) // 32) * 6 * 2 * 32 * 32 * 16
+        executed = E * ((C + 31) // 32) * kb * ((R + 31) // 32) * 3 * 2 * 32 * 32 * 16
         line["roofline"]["executed"] = {
-            "mfma": "v_mfma_f32_32x32x16_bf16, six exact bf16 part products per fp32 product",
+            "mfma": "v_mfma_f32_32x32x16_f16, three products of two-part fp16 splits per fp32 product",
             "flops_per_launch": executed, "achieved": executed / (edge_ms * 1e-3) / 1e12,
-            "peak": PEAK_BF16_MFMA_TFLOPS, "frac": executed / (edge_ms * 1e-3) / 1e12 / PEAK_BF16_MFMA_TFLOPS}
+            "peak": PEAK_FP16_MFMA_TFLOPS, "frac": executed / (edge_ms * 1e-3) / 1e12 / PEAK_FP16_MFMA_TFLOPS}
     if args.backward:
         G = torch.from_numpy(w["grad_out"]).to(dev)
         wsb = torch.empty(bwd_bytes, dtype=torch.uint8, device=dev)

@@ -74,9 +74,10 @@ typedef struct {
                            With TDN_BF16 the edge contractions run on bf16 MFMA:
                            the K operand g*A (and, in the backward, G W^T) is
                            rounded to bf16, accumulation stays fp32.  With
-                           TDN_F32 results keep fp32 accuracy (the edge
-                           contraction uses bf16 MFMA only on exact three-part
-                           splits of both operands)                          */
+                           TDN_F32 results keep fp32-level accuracy (the
+                           edge contractions run on 16-bit MFMA over exact
+                           splits: two fp16 parts of power-of-two scaled
+                           operands, or three bf16 parts)                    */
   int32_t edges_sorted; /* 1: edge_index already stably sorted by dst (perm is the
                            identity); 0: the call sorts                            */
   int32_t validate;     /* 1: check indices, order and edge vectors on the device */

@@ -51,19 +51,26 @@ tdn_status check_problem(const tdn_problem* p) {
   return TDN_OK;
 }
 
-// bf16 parts per feature of the edge pass: the exact three-part split of
+// 16-bit parts per feature of the edge pass: the fp16 two-part split of
 // fp32 features, or the bf16 features themselves
-int feature_parts(const tdn_problem& p) { return p.feat_dtype == TDN_BF16 ? 1 : 3; }
+int feature_parts(const tdn_problem& p) { return p.feat_dtype == TDN_BF16 ? 1 : 2; }
+// bf16 parts per feature of the backward's destination kernel: the exact
+// three-part split of fp32 features, or the bf16 features
+int dst_parts(const tdn_problem& p) { return p.feat_dtype == TDN_BF16 ? 1 : 3; }
 
-// transposed features for the edge pass
-size_t xt_bytes(const tdn_problem& p) {
+// features of the edge pass in MFMA operand blocks, then their row scales
+size_t xs_bytes(const tdn_problem& p) {
   return size_t(p.n_nodes) * ((p.C + 31) / 32 * 32) * feature_parts(p) * tdn::edge_kpad(dim_of(p.L)) * 2;
+}
+size_t xt_bytes(const tdn_problem& p) { return al(xs_bytes(p)) + size_t(p.n_nodes) * 4; }
+float* row_scales(const tdn_problem& p, void* xt) {
+  return reinterpret_cast<float*>(static_cast<char*>(xt) + al(xs_bytes(p)));
 }
 // the same region holds, in the backward, x blocked over channels for
 // the destination-side kernel
 size_t xt_xc_bytes(const tdn_problem& p) {
   const size_t xc =
-      size_t(p.n_nodes) * dim_of(p.L) * feature_parts(p) * tdn::bwd_dst_cpad(p.C, p.feat_dtype == TDN_BF16) * 2;
+      size_t(p.n_nodes) * dim_of(p.L) * dst_parts(p) * tdn::bwd_dst_cpad(p.C, p.feat_dtype == TDN_BF16) * 2;
   return std::max(xt_bytes(p), xc);
 }
 
@@ -219,6 +226,7 @@ tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int3
   a.pieces_per_block = pl.per_block;
   a.ef_pad = partial;
   a.parts = feature_parts(p);
+  a.row_scale = a.parts == 2 ? row_scales(p, const_cast<void*>(feat)) : nullptr;
   a.partial = partial ? reinterpret_cast<float*>(reinterpret_cast<char*>(partial) + ef_pad_bytes(p)) : nullptr;
   return a;
 }
@@ -232,7 +240,7 @@ hipError_t forward_edge_pass(const tdn_problem& p, const int32_t* offsets, const
   {
     Timed t("feature_layout", s);
     hipError_t e = tdn::launch_feature_layout(p.n_nodes, dim_of(p.L), p.C, x, p.feat_dtype == TDN_F32,
-                                              feature_parts(p), xt, s);
+                                              feature_parts(p), xt, row_scales(p, xt), s);
     if (e != hipSuccess) return e;
   }
   Timed t("cp_edge_fwd", s);
@@ -381,7 +389,7 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
       // x in parts, blocked as MFMA operands for the contraction over channels
       // (the region is free until the grad_x pass lays out Gz there)
       Timed t("channel_layout", stream);
-      TDN_HIP(tdn::launch_channel_layout(N, d, C, tdn::bwd_dst_cpad(C, bf16), x, !bf16, feature_parts(*p), ws + lay.xt,
+      TDN_HIP(tdn::launch_channel_layout(N, d, C, tdn::bwd_dst_cpad(C, bf16), x, !bf16, dst_parts(*p), ws + lay.xt,
                                          stream));
       a.xc = ws + lay.xt;
     }
@@ -396,10 +404,11 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
       TDN_HIP(tdn::launch_sort(tdn::sort_plan(N, E), src, 1, perm_src, off_src, ws + lay.sort, stream));
     }
     // bf16 problems run the grad_x pass on bf16 MFMA too (Gz rounded to
-    // bf16); fp32 problems on the exact three-part split of Gz
+    // bf16); fp32 problems on the fp16 two-part split of Gz
     {
       Timed t("feature_layout", stream);
-      TDN_HIP(tdn::launch_feature_layout(N, d, C, Gz, true, feature_parts(*p), ws + lay.xt, stream));
+      TDN_HIP(tdn::launch_feature_layout(N, d, C, Gz, true, feature_parts(*p), ws + lay.xt,
+                                         row_scales(*p, ws + lay.xt), stream));
     }
     Timed t("cp_edge_bwd_src", stream);
     TDN_HIP(tdn::launch_cp_edge(edge_args(*p, off_src, perm_src, dst, src, edge_vec, D, A, B, radial_w, ws + lay.xt,

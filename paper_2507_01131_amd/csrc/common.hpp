@@ -52,6 +52,33 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2_rne(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
 }
+// Two-way half-precision split of a pair of floats, for fp32-accurate
+// contractions on fp16 MFMA: v = hi + lo + r with hi = fp16(v) and
+// lo = fp16(v - hi) (round to nearest even; v - hi is exact in fp32), so
+// |r| <= 2^-22 |v| + 2^-25 (the second term from fp16 subnormals) for
+// |v| < 2^15.  Callers scale each row by a power of two that puts its largest
+// |v| in [2^13, 2^14), which makes the absolute term 2^-38 of that largest
+// value.  Each part is packed as a pair, a in the low half: one
+// v_cvt_pk_f16_f32 per part.
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_f16x2_rne(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, f16x2_t));
+}
+__device__ __forceinline__ void split_f16x2_pair(float a, float b, uint32_t& hi, uint32_t& lo) {
+  hi = pack_f16x2_rne(a, b);
+  const f16x2_t h2 = __builtin_bit_cast(f16x2_t, hi);
+  lo = pack_f16x2_rne(a - float(h2[0]), b - float(h2[1]));
+}
+// Power-of-two exponent e with max_abs * 2^-e in [2^13, 2^14) (0 for 0 or
+// non-finite input), clamped so that 2^e and 2^-e are normal floats.
+__device__ __forceinline__ int f16_split_exponent(float max_abs) {
+  if (!(max_abs > 0.f) || !(max_abs < 3.0e38f)) return 0;
+  int E;
+  (void)frexpf(max_abs, &E);  // max_abs = m 2^E, m in [0.5, 1)
+  const int e = E - 14;
+  return e < -125 ? -125 : (e > 125 ? 125 : e);
+}
+
 // split_bf16x3 of two floats at once, each part packed as by pack_bf16x2_rne
 // (the same parts, bit for bit, in half the conversions).
 __device__ __forceinline__ void split_bf16x3_pair(float a, float b, uint32_t& hi, uint32_t& mid, uint32_t& lo) {

@@ -87,7 +87,8 @@ EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E) {
 
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s) {
   using namespace edge_detail;
-  if (a.parts != 1 && a.parts != 3) return hipErrorInvalidValue;
+  if (a.parts != 1 && a.parts != 2) return hipErrorInvalidValue;
+  if (a.parts == 2 && a.E > 0 && !a.row_scale) return hipErrorInvalidValue;
   if (a.E > 0 && (a.n_range < 1 || a.n_range > a.E || a.pieces_per_block < 1 || a.n_range % a.pieces_per_block ||
                   !a.ef_pad))
     return hipErrorInvalidValue;

@@ -13,16 +13,18 @@
 // i.e. the contraction uses D, the epilogue uses A and the gathered rows are
 // Gz[t_e].
 //
-// Arithmetic.  U_e runs on bf16 MFMA (v_mfma_f32_32x32x16_bf16) with fp32
-// accumulation and fp32 accuracy: both operands are split exactly into three
-// bfloat16 parts (a = a1 + a2 + a3, x = x1 + x2 + x3, every part product
-// exact in fp32) and the six products a_i x_j with i + j <= 4 are summed,
-// smallest first; the dropped ones are below 2^-22 of |a x|.  The features
-// arrive pre-split and transposed (xs [N, C, 3, DP], k fastest, zero padded
-// to DP = 32 or 64), so one lane's operand for eight consecutive k is one
-// 16-byte load; the split factor sits in LDS in MFMA operand order.  Then
-// acc[r, c] += g_e[r] U_e[r, c] in
-// fp32 on the VALU, with g read from LDS four rows at a time.
+// Arithmetic.  U_e runs on fp16 MFMA (v_mfma_f32_32x32x16_f16) with fp32
+// accumulation and fp32-level accuracy: every feature row and the factor are
+// scaled by powers of two (exact) that put their largest magnitude in
+// [2^13, 2^14), then split into two fp16 parts, a = a1 + a2 and x = x1 + x2,
+// each to 2^-22 of the value; the part products are exact in fp32 and the
+// three with i + j <= 3 are summed, smallest first (the dropped a2 x2 is
+// below 2^-22 of |a x|).  g_e carries the two scales back, exactly.  The
+// features arrive pre-split in MFMA operand blocks (launch_feature_layout),
+// so one lane's operand for eight consecutive k is one 16-byte load; the
+// split factor sits in LDS in MFMA operand order.  Then
+// acc[r, c] += g_e[r] U_e[r, c] in fp32 on the VALU, with g read from LDS
+// four rows at a time.  bf16 features take the bf16 mode described below.
 //
 // Work decomposition.  The sorted edge list is cut into n_range equal ranges,
 // as many as the device holds workgroups at once (over the channel groups),
@@ -54,11 +56,16 @@ namespace tdn {
 namespace edge_detail {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f32x16 mfma_bf16(u32x4 a, u32x4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
                                                  0, 0);
+}
+__device__ __forceinline__ f32x16 mfma_f16(u32x4 a, u32x4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0,
+                                                0);
 }
 
 constexpr int kMaxWavesPerBlock = 4;
@@ -73,13 +80,13 @@ __host__ __device__ constexpr int edge_dp(int d) { return d <= 32 ? 32 : 64; }
 __host__ __device__ constexpr int edge_kb(int d) { return edge_dp(d) / 16; }
 
 // Two modes of the edge contraction:
-//  split (fp32 features): U_e = KF^T x from six exact bf16 part products,
-//    then acc += g * U_e; one 32-channel tile per wave;
+//  split (fp32 features): U_e = KF^T x from three fp16 part products, then
+//    acc += g * U_e; one 32-channel tile per wave;
 //  bf16 (bf16 features): the K operand g_e[r] KF[k, r] is formed in fp32 and
 //    rounded to bf16, one MFMA per K-block straight into acc; two channel
 //    tiles per wave (while R <= 128) so every K operand feeds two MFMAs.
-// Bf16 parts per feature value and channel tiles per wave:
-__host__ __device__ constexpr int edge_xp(bool bf) { return bf ? 1 : 3; }
+// 16-bit parts per feature value and channel tiles per wave:
+__host__ __device__ constexpr int edge_xp(bool bf) { return bf ? 1 : 2; }
 __host__ __device__ constexpr int edge_ct(bool bf, int RT) { return bf && RT <= 4 ? 2 : 1; }
 
 // Two waves per SIMD (two workgroups per CU) when the accumulators and the
@@ -87,7 +94,7 @@ __host__ __device__ constexpr int edge_ct(bool bf, int RT) { return bf && RT <= 
 // loop; one otherwise.
 __host__ __device__ constexpr int edge_waves_per_eu(int L, int RT, bool bf) {
   return bf ? (16 * RT * edge_ct(bf, RT) + 8 * edge_ct(bf, RT) * edge_kb((L + 1) * (L + 1)) <= 144 ? 2 : 1)
-            : (16 * RT + 48 * edge_kb((L + 1) * (L + 1)) <= 160 ? 2 : 1);
+            : (16 * RT + 24 * edge_xp(bf) * edge_kb((L + 1) * (L + 1)) <= 160 ? 2 : 1);
 }
 
 // Most ranges a workgroup takes: two where two workgroups share a CU (their
@@ -102,21 +109,22 @@ __host__ __device__ constexpr int edge_max_ranges(int L, int RT, bool bf) {
 __host__ __device__ constexpr bool edge_reg_kf(int d, int RT) { return edge_kb(d) * RT * 8 <= 64; }
 
 struct EdgeSmem {
-  int Rp, off_a, off_g, off_y, off_vec, off_phi, off_idx, off_bnd, floats;
+  int Rp, off_a, off_g, off_y, off_vec, off_phi, off_idx, off_sc, off_bnd, floats;
 };
 
 // LDS regions (in floats): the factor operands, split mode
-// [KB][RT][3 parts][64 lanes] x 16 bytes of bf16, bf16 mode
-// [KB][RT][64 lanes] x 32 bytes of fp32, g for a chunk of edges (rows rounded up to a whole 32-row
-// tile), harmonics, normalised edge vectors with their lengths, radial basis,
-// gathered rows, and the segment starts of the chunk (positions, keys, count
-// and the two partial-segment flags).
+// [KB][RT][2 parts][64 lanes] x 16 bytes of fp16, bf16 mode
+// [KB][RT][64 lanes] x 32 bytes of fp32, g for a chunk of edges (rows
+// rounded up to a whole 32-row tile), harmonics, normalised edge vectors with
+// their lengths, radial basis, gathered rows, the edges' operand scales, and
+// the segment starts of the chunk (positions, keys, count and the two
+// partial-segment flags).
 __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radial, int chunk) {
   EdgeSmem s{};
   s.Rp = RT * kTile;
   int o = 0;
   s.off_a = o;
-  o += edge_kb(d) * RT * (bf ? 2 : 3) * kWave * 4;
+  o += edge_kb(d) * RT * 2 * kWave * 4;
   s.off_g = o;
   o += (chunk + kTile - 1) / kTile * kTile * s.Rp;
   s.off_y = o;
@@ -127,6 +135,8 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radi
   s.off_phi = o;
   o += chunk * n_radial;
   s.off_idx = o;
+  o += chunk;
+  s.off_sc = o;
   o += chunk;
   s.off_bnd = o;
   o += 2 * chunk + 4;
@@ -155,6 +165,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   float4* sVec = reinterpret_cast<float4*>(smem + S.off_vec);
   float* sPhi = smem + S.off_phi;
   int* sIdx = reinterpret_cast<int*>(smem + S.off_idx);
+  float* sSc = smem + S.off_sc;                          // [chunk] 2^e of the edge's operands (split mode)
   int* sBnd = reinterpret_cast<int*>(smem + S.off_bnd);  // [chunk] chunk positions where a segment starts
   int* sBndKey = sBnd + chunk;                          // [chunk] that segment
   int* sMeta = sBndKey + chunk;                         // start count, first partial, last partial
@@ -167,36 +178,41 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   const int C = a.C, nr = a.n_radial, R = a.R;
   const int c0 = (cgrp * waves + wave) * CT * kTile + l32;  // this lane's channel in tile 0
 
+  // Split mode: the power of two 2^-e_K that puts the factor's largest |KF|
+  // in [2^13, 2^14) for its fp16 parts (a block maximum through sG, which
+  // the chunk loop overwrites only after its first barrier); the edges' g
+  // carry 2^e_K back.
+  float kf_sc = 1.f, kf_unsc = 1.f;
+  if constexpr (!BF) {
+    float mx = 0.f;
+    for (int i = tid; i < d * R; i += blockDim.x) mx = fmaxf(mx, fabsf(a.KF[i]));
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    if (lane == 0) sG[wave] = mx;
+    __syncthreads();
+    for (int w = 0; w < int(blockDim.x / kWave); ++w) mx = fmaxf(mx, sG[w]);
+    const int e = f16_split_exponent(mx);
+    kf_sc = ldexpf(1.f, -e);
+    kf_unsc = ldexpf(1.f, e);
+  }
   // Factor operands: lane (l32, h) of K-block b, rank tile rt holds
-  // KF[16b + 8h + i][rt*32 + l32], i = 0..7, zero past d and R, as its three
-  // bf16 parts (split mode) or in fp32 (bf16 mode).  One thread per
+  // KF[16b + 8h + i][rt*32 + l32], i = 0..7, zero past d and R, as the fp16
+  // parts of KF 2^-e_K (split mode) or in fp32 (bf16 mode).  One thread per
   // (b, rt, lane).
   for (int t = tid; t < KB * RT * kWave; t += blockDim.x) {
-    if constexpr (BF) {
-      const int ln = t % kWave, brt = t / kWave;
-      const int b = brt / RT, rt = brt - b * RT;
-      const int r = rt * kTile + (ln & 31), k0 = 16 * b + 8 * (ln >> 5);
-      float v[8];
+    const int ln = t % kWave, brt = t / kWave;
+    const int b = brt / RT, rt = brt - b * RT;
+    const int r = rt * kTile + (ln & 31), k0 = 16 * b + 8 * (ln >> 5);
+    float v[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = k0 + i < d && r < R ? a.KF[(k0 + i) * R + r] : 0.f;
+    for (int i = 0; i < 8; ++i) v[i] = k0 + i < d && r < R ? a.KF[(k0 + i) * R + r] : 0.f;
+    if constexpr (BF) {
       sAf[2 * t] = make_float4(v[0], v[1], v[2], v[3]);
       sAf[2 * t + 1] = make_float4(v[4], v[5], v[6], v[7]);
     } else {
-      const int ln = t % kWave, brt = t / kWave;
-      const int b = brt / RT, rt = brt - b * RT;
-      const int r = rt * kTile + (ln & 31), k0 = 16 * b + 8 * (ln >> 5);
       uint32_t w[XP][4];
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        uint16_t part[XP][2];
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const int k = k0 + 2 * p + q;
-          split_bf16x3(k < d && r < R ? a.KF[k * R + r] : 0.f, part[0][q], part[1][q], part[2][q]);
-        }
-#pragma unroll
-        for (int s = 0; s < XP; ++s) w[s][p] = uint32_t(part[s][0]) | (uint32_t(part[s][1]) << 16);
-      }
+      for (int p = 0; p < 4; ++p) split_f16x2_pair(v[2 * p] * kf_sc, v[2 * p + 1] * kf_sc, w[0][p], w[1][p]);
 #pragma unroll
       for (int s = 0; s < XP; ++s) sA[(brt * XP + s) * kWave + ln] = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
     }
@@ -303,8 +319,9 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
         xb[s][b] = BF ? *reinterpret_cast<const u32x4*>(p + lane_off[s] + uint32_t(b * 1024))
                       : *reinterpret_cast<const u32x4*>(p + lane_off[0] + uint32_t((s * KB + b) * 1024));
   };
-  // U_e = KF^T x[row] for one rank tile from the six part products (smallest
-  // first), then acc += g_e * U_e with g for this lane's rows
+  // U_e = KF^T x[row] for one rank tile from the three part products lo hi,
+  // hi lo, hi hi (smallest first), then acc += g_e * U_e with g (which
+  // carries the operands' scales) for this lane's rows
   // rt*32 + 8q + 4h + i read four at a time.  The rank tiles are pipelined:
   // step rt issues the LDS reads of the factor parts of tile rt+1 and of g
   // for tile rt-1, runs the MFMA chain of tile rt into one of two U buffers,
@@ -364,17 +381,11 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
       auto chain = [&](int buf) {
         f32x16 u = f32x16{};
 #pragma unroll
-        for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][0][b], xb[2][b], u);
+        for (int b = 0; b < KB; ++b) u = mfma_f16(am[buf][1][b], xb[0][b], u);
 #pragma unroll
-        for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][2][b], xb[0][b], u);
+        for (int b = 0; b < KB; ++b) u = mfma_f16(am[buf][0][b], xb[1][b], u);
 #pragma unroll
-        for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][1][b], xb[1][b], u);
-#pragma unroll
-        for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][0][b], xb[1][b], u);
-#pragma unroll
-        for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][1][b], xb[0][b], u);
-#pragma unroll
-        for (int b = 0; b < KB; ++b) u = mfma_bf16(am[buf][0][b], xb[0][b], u);
+        for (int b = 0; b < KB; ++b) u = mfma_f16(am[buf][0][b], xb[0][b], u);
         U[buf] = u;
       };
       auto fma_rt = [&](int rt, int buf) {
@@ -420,7 +431,9 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
         int key = -1;
         if (t < n) {
           const int eid = a.perm[cb + t];
-          sIdx[t] = a.gather[eid];
+          const int row = a.gather[eid];
+          sIdx[t] = row;
+          if constexpr (!BF) sSc[t] = a.row_scale[row] * kf_unsc;
           key = a.key[eid];
           const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
           const float len = sqrtf(vx * vx + vy * vy + vz * vz);
@@ -482,7 +495,10 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
           Ty = mfma32(av, (k < d && r < R) ? bw : 0.f, Ty);
         }
   #pragma unroll
-        for (int v = 0; v < 16; ++v) sG[(et * kTile + acc_row(v, h)) * Rp + rt * kTile + l32] = Tr[v] * Ty[v];
+        for (int v = 0; v < 16; ++v) {
+          const int e = et * kTile + acc_row(v, h);
+          sG[e * Rp + rt * kTile + l32] = BF ? Tr[v] * Ty[v] : Tr[v] * Ty[v] * (e < n ? sSc[e] : 0.f);
+        }
       }
       __syncthreads();
 

@@ -1,17 +1,19 @@
-// Feature layout for the edge pass: x [N, d, C] becomes bfloat16 operand
+// Feature layout for the edge pass: x [N, d, C] becomes 16-bit operand
 // blocks of the 32x32x16 MFMA, xs [N, Cq/32, P, DP/16, 2, 32, 8]: element
 // [n][ct][s][b][h][c][i] is part s of x[n][16 b + 8 h + i][32 ct + c], zero
 // for k >= d (DP = 32 for d <= 32, else 64) and for channels from C (Cq is C
 // rounded up to 32).  Lane (h, c) of a wave reads its eight k with one
 // 16-byte load, and the 64 lanes read one contiguous kilobyte.
-//   P = 3 (fp32 problems): the exact three-way split hi/mid/lo of every fp32
-//         value, x = hi + mid + lo;
+//   P = 2 (fp32 problems): fp16 parts hi, lo of x[n] 2^-e_n, the power of
+//         two that puts the node's largest |x| in [2^13, 2^14); the factor
+//         2^e_n goes to row_scale[n];
 //   P = 1 (bf16 problems): x itself (bf16 input), or an fp32 input (the
 //         backward's Gz) rounded to bf16.
-// One block per node: the node's [d, C] rows are staged in LDS, then each
-// thread writes a group of eight k of one channel in all P parts.
+// One block per node: the node's [d, C] rows are staged in LDS (with their
+// largest magnitude), then each thread writes a group of eight k of one
+// channel in all P parts.
 // The backward's destination kernel contracts over channels instead and reads
-// x in MFMA operand blocks over channels (launch_channel_layout).
+// x in bf16 MFMA operand blocks over channels (launch_channel_layout).
 #include "common.hpp"
 #include "kernels.h"
 
@@ -26,12 +28,30 @@ __device__ __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
 
 template <int DP, int P, typename TI>
 __global__ __launch_bounds__(256) void k_feature_layout(int d, int C, const TI* __restrict__ x,
-                                                        uint16_t* __restrict__ xs) {
-  extern __shared__ float tile[];  // [d][C]
+                                                        uint16_t* __restrict__ xs, float* __restrict__ row_scale) {
+  extern __shared__ float tile[];  // [d][C], then four floats for the row maximum
+  float* red = tile + d * C;
   const int n = blockIdx.x;
   const TI* src = x + size_t(n) * d * C;
-  for (int i = threadIdx.x; i < d * C; i += blockDim.x) tile[i] = to_f32(src[i]);
+  float mx = 0.f;
+  for (int i = threadIdx.x; i < d * C; i += blockDim.x) {
+    const float v = to_f32(src[i]);
+    tile[i] = v;
+    mx = fmaxf(mx, fabsf(v));
+  }
+  float sc = 1.f;  // 2^-e_n: the row's largest |x| to [2^13, 2^14) (fp16 parts)
+  if constexpr (P == 2) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+  }
   __syncthreads();
+  if constexpr (P == 2) {
+    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    const int e = f16_split_exponent(mx);
+    sc = ldexpf(1.f, -e);
+    if (threadIdx.x == 0) row_scale[n] = ldexpf(1.f, e);
+  }
   constexpr int KB = DP / 16;
   const int Cq = (C + 31) / 32 * 32;
   uint16_t* dst = xs + size_t(n) * Cq * P * DP;
@@ -44,8 +64,8 @@ __global__ __launch_bounds__(256) void k_feature_layout(int d, int C, const TI* 
       const int k = 8 * g + 2 * q;
       const float v0 = (k < d && c < C) ? tile[k * C + c] : 0.f;
       const float v1 = (k + 1 < d && c < C) ? tile[(k + 1) * C + c] : 0.f;
-      if constexpr (P == 3)
-        split_bf16x3_pair(v0, v1, w[0][q], w[1][q], w[2][q]);
+      if constexpr (P == 2)
+        split_f16x2_pair(v0 * sc, v1 * sc, w[0][q], w[1][q]);
       else
         w[0][q] = pack_bf16x2_rne(v0, v1);  // exact for bf16 input
     }
@@ -58,20 +78,21 @@ __global__ __launch_bounds__(256) void k_feature_layout(int d, int C, const TI* 
 }
 
 template <int DP, int P, typename TI>
-hipError_t launch_dp(int N, int d, int C, const TI* x, uint16_t* xs, hipStream_t s) {
-  const size_t lds = size_t(d) * C * 4;
+hipError_t launch_dp(int N, int d, int C, const TI* x, uint16_t* xs, float* row_scale, hipStream_t s) {
+  const size_t lds = (size_t(d) * C + 4) * 4;
   auto k = k_feature_layout<DP, P, TI>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      int(lds));
   if (e != hipSuccess) return e;
-  k<<<dim3(N), dim3(256), lds, s>>>(d, C, x, xs);
+  k<<<dim3(N), dim3(256), lds, s>>>(d, C, x, xs, row_scale);
   return hipGetLastError();
 }
 
 template <int P, typename TI>
-hipError_t launch_p(int N, int d, int C, const TI* x, void* xs, hipStream_t s) {
+hipError_t launch_p(int N, int d, int C, const TI* x, void* xs, float* row_scale, hipStream_t s) {
   uint16_t* o = static_cast<uint16_t*>(xs);
-  return edge_kpad(d) == 32 ? launch_dp<32, P>(N, d, C, x, o, s) : launch_dp<64, P>(N, d, C, x, o, s);
+  return edge_kpad(d) == 32 ? launch_dp<32, P>(N, d, C, x, o, row_scale, s)
+                            : launch_dp<64, P>(N, d, C, x, o, row_scale, s);
 }
 
 // xc[n][p][s][h][k][i] = part p of x[n][k][16 s + 8 h + i] (zero from
@@ -136,15 +157,15 @@ hipError_t launch_channel_layout(int N, int d, int C, int Cp, const void* x, boo
 }
 
 hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,
-                                 hipStream_t s) {
+                                 float* row_scale, hipStream_t s) {
   if (N == 0) return hipSuccess;
-  if (parts == 3) {
-    if (!x_is_f32) return hipErrorInvalidValue;
-    return launch_p<3>(N, d, C, static_cast<const float*>(x), xs, s);
+  if (parts == 2) {
+    if (!x_is_f32 || !row_scale) return hipErrorInvalidValue;
+    return launch_p<2>(N, d, C, static_cast<const float*>(x), xs, row_scale, s);
   }
   if (parts != 1) return hipErrorInvalidValue;
-  return x_is_f32 ? launch_p<1>(N, d, C, static_cast<const float*>(x), xs, s)
-                  : launch_p<1>(N, d, C, static_cast<const uint16_t*>(x), xs, s);
+  return x_is_f32 ? launch_p<1>(N, d, C, static_cast<const float*>(x), xs, nullptr, s)
+                  : launch_p<1>(N, d, C, static_cast<const uint16_t*>(x), xs, nullptr, s);
 }
 
 }  // namespace tdn

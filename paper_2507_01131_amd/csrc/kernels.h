@@ -52,7 +52,8 @@ struct EdgeArgs {
   int pieces_per_block;      // ranges per workgroup (EdgePlan::per_block)
   float* partial;            // [n_range, 2, d, C] workspace
   float* ef_pad;             // [d, RT*32] workspace: EF zero-padded (written by launch_cp_edge)
-  int parts;                 // bf16 parts per feature in feat (3: fp32 features, 1: bf16 features)
+  int parts;                 // 16-bit parts per feature in feat (2: fp32 features as fp16 hi + lo, 1: bf16)
+  const float* row_scale;    // [n_feat_rows] 2^e of each feat row (parts = 2), from launch_feature_layout
 };
 // Edge ranges of the pass for this problem on the current device:
 // n_range = per_block x the number of workgroups the device holds at once
@@ -63,23 +64,25 @@ struct EdgePlan {
 };
 EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E);
 // Features for the edge pass: x [N, d, C] -> 32x32x16 MFMA operand blocks
-// xs [N, ceil(C/32), parts, edge_kpad(d)/16, 2, 32, 8] bfloat16, element
-// [n][ct][s][b][h][c][i] = part s of x[n][16b + 8h + i][32ct + c], zero
-// padded in k and c (EdgeArgs::feat = xs): parts = 3 holds
-// the exact split x = hi + mid + lo of fp32 features, parts = 1 holds bf16
-// features (an fp32 input is rounded to bf16).  edge_kpad(d) = 32 for
-// d <= 32, else 64.
+// xs [N, ceil(C/32), parts, edge_kpad(d)/16, 2, 32, 8] of 16-bit values,
+// element [n][ct][s][b][h][c][i] = part s of x[n][16b + 8h + i][32ct + c],
+// zero padded in k and c (EdgeArgs::feat = xs).  parts = 2 (fp32 features):
+// fp16 hi and lo of x[n] 2^-e_n with x[n] 2^-e_n = hi + lo to 2^-22, e_n
+// putting the row's largest |x| in [2^13, 2^14), and row_scale[n] = 2^e_n;
+// parts = 1: bf16 features (an fp32 input is rounded to bf16; row_scale is
+// not used).  edge_kpad(d) = 32 for d <= 32, else 64.
 int edge_kpad(int d);
 hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,
-                                 hipStream_t s);
-// The same parts blocked for contractions over channels:
+                                 float* row_scale, hipStream_t s);
+// Features in bf16 parts blocked for contractions over channels (parts = 3:
+// the exact split x = hi + mid + lo of fp32 features, parts = 1: bf16):
 // xc [N, parts, Cp / 16, 2, d, 8] bfloat16, element [n][p][s][h][k][i] = part
 // p of x[n][k][16 s + 8 h + i] (zero from channel C; Cp >= C a multiple of
 // 16): per node, part and K-step of 16 channels one 32x32x16 MFMA operand
 // block of rows k < d.
 hipError_t launch_channel_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xc,
                                  hipStream_t s);
-// parts = 3: fp32 features (exact split), parts = 1: bf16 features
+// parts = 2: fp32 features (fp16 two-part split), parts = 1: bf16 features
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- node GEMMs
