@@ -49,11 +49,19 @@ def device_inputs(w: dict, A, B, D, dev="cuda"):
 
 
 def rel_err(gpu, ref) -> float:
+    """Relative Frobenius error; with TDN_PARITY_LOG set, each value is also
+    appended to that file with the running test's id."""
     gpu = np.asarray(gpu, np.float64)
     ref = np.asarray(ref, np.float64)
     assert np.all(np.isfinite(gpu)), "non-finite values in GPU output"
     nrm = np.linalg.norm(ref)
-    return float(np.linalg.norm(gpu - ref) / (nrm if nrm > 0 else 1.0))
+    err = float(np.linalg.norm(gpu - ref) / (nrm if nrm > 0 else 1.0))
+    log = os.environ.get("TDN_PARITY_LOG")
+    if log:
+        test = os.environ.get("PYTEST_CURRENT_TEST", "?").split(" ")[0]
+        with open(log, "a") as f:
+            f.write(f"{test}\t{gpu.shape}\t{err:.3e}\n")
+    return err
 
 
 def tol(w: dict) -> float:
