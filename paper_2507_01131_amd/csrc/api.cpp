@@ -68,10 +68,16 @@ float* row_scales(const tdn_problem& p, void* xt) {
 }
 // the same region holds, in the backward, x blocked over channels for
 // the destination-side kernel
+// x in the direct destination kernel's operand blocks (d > 32), then its row
+// scales
+size_t xd_bytes(const tdn_problem& p) {
+  return size_t(p.n_nodes) * dim_of(p.L) * feature_parts(p) * tdn::bwd_direct_cpad(p.C) * 2;
+}
 size_t xt_xc_bytes(const tdn_problem& p) {
   const size_t xc =
       size_t(p.n_nodes) * dim_of(p.L) * dst_parts(p) * tdn::bwd_dst_cpad(p.C, p.feat_dtype == TDN_BF16) * 2;
-  return std::max(xt_bytes(p), xc);
+  const size_t xd = al(xd_bytes(p)) + size_t(p.n_nodes) * 4;
+  return std::max(xt_bytes(p), std::max(xc, xd));
 }
 
 // partial slots of the fp32 edge pass (two [d, C] rows per edge range) and
@@ -392,6 +398,15 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
       TDN_HIP(tdn::launch_channel_layout(N, d, C, tdn::bwd_dst_cpad(C, bf16), x, !bf16, dst_parts(*p), ws + lay.xt,
                                          stream));
       a.xc = ws + lay.xt;
+    } else if (d > 32) {
+      // x in the direct kernel's operand blocks, fp16 parts with row scales
+      // (fp32 problems) or bf16
+      float* xscale = reinterpret_cast<float*>(ws + lay.xt + al(xd_bytes(*p)));
+      Timed t("channel_layout", stream);
+      TDN_HIP(tdn::launch_direct_layout(N, d, C, tdn::bwd_direct_cpad(C), x, !bf16, feature_parts(*p), ws + lay.xt,
+                                        bf16 ? nullptr : xscale, stream));
+      a.xc = ws + lay.xt;
+      a.x_scale = bf16 ? nullptr : xscale;
     }
     Timed t("cp_bwd_dst", stream);
     TDN_HIP(tdn::launch_bwd_dst(a, bf16, stream));

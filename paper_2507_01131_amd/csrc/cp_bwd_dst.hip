@@ -7,7 +7,7 @@
 
 namespace tdn {
 namespace bwd_detail {
-template <int MT, typename TX>
+template <int MT, bool BF>
 hipError_t launch_mt(const BwdDstArgs& a, hipStream_t s);
 }
 namespace bwd_sg_detail {
@@ -68,7 +68,8 @@ hipError_t launch_bwd_dst(const BwdDstArgs& a, bool x_bf16, hipStream_t s) {
   }
   if (a.d <= 32)
     return x_bf16 ? bwd_sg_detail::launch_sg_any<true>(a, s) : bwd_sg_detail::launch_sg_any<false>(a, s);
-  return x_bf16 ? bwd_detail::launch_mt<2, uint16_t>(a, s) : bwd_detail::launch_mt<2, float>(a, s);
+  if (!a.xc || (!x_bf16 && !a.x_scale)) return hipErrorInvalidValue;
+  return x_bf16 ? bwd_detail::launch_mt<2, true>(a, s) : bwd_detail::launch_mt<2, false>(a, s);
 }
 
 }  // namespace tdn

@@ -1,6 +1,6 @@
 // Backward of the CP tensor-product layer with respect to the edge vectors,
-// direct form (used for d > 32; d <= 32 takes the factored form in
-// cp_bwd_sg_impl.hpp).
+// direct form (used for d > 32; d <= 32 takes the factored forms in
+// cp_bwd_dst2_impl.hpp and cp_bwd_sg_impl.hpp).
 //
 // With Gz = grad_out W^T and Gh_t = D^T Gz[t] (per destination node, [R, C]),
 // the cotangent of g_e (eq. approximate, Sec. 3.1) is
@@ -10,16 +10,21 @@
 //   grad r_e = J_Y(r_e)^T dY + (sum_q dphi_q phi'_q(|r_e|)) r_e/|r_e|.
 //
 // One workgroup per destination segment, one wave per 32-rank tile.  Each
-// wave forms its Gh^T tiles once (MFMA, K = d) and keeps them in registers:
-// in accumulator layout lane l holds Gh^T[ct*32 + acc_row(v, l/32)]
-// [rt*32 + l%32], which is exactly the B operand of P_e^T = x[s_e] Gh^T when
-// K-step (ct, v) contracts channel ct*32 + acc_row(v, half) in each
-// half-wave.  The matching A operand, x[s_e][k][ct*32 + acc_row(v, half)],
-// is four groups of four consecutive channels per lane, so it is loaded
-// straight from global memory with float4 loads (no LDS staging), one
-// (edge, channel tile) step ahead into alternating register buffers.  dg is
-// then a 16-term dot product with A held in registers plus one cross-half
-// add.  The channel-tile count NCT and k-tile count MT are compile-time.
+// wave forms its Gh^T tiles once (fp32 MFMA, K = d); in accumulator layout
+// lane l holds Gh^T[ct*32 + acc_row(v, l/32)][rt*32 + l%32], so registers
+// 8q .. 8q+7 are the B operand of one 32x32x16 step of P_e = x[s_e] Gh^T
+// that contracts channels ct*32 + 16q + 8(i/4) + 4h + i%4 (i = 0..7) in
+// half-wave h.  The x operand comes in that channel order from the xd layout
+// (launch_direct_layout): per edge and channel tile one 16-byte load per
+// k tile, K-step and part, one channel tile ahead.
+//
+// Arithmetic.  fp32 problems: x[n] 2^-e_n and the wave's Gh^T tiles scaled by
+// a power of two (largest magnitude to [2^13, 2^14)) are split into two fp16
+// parts each (to 2^-22) and P_e sums the three part products with i + j <= 3
+// on v_mfma_f32_32x32x16_f16, fp32 accumulation; dg carries both scales back
+// (exactly).  bf16 problems: x is bf16 and Gh^T is rounded to bf16, one
+// product on v_mfma_f32_32x32x16_bf16.  dg is a 32-term dot product with A
+// held in registers plus one cross-half add.
 #pragma once
 
 #include "common.hpp"
@@ -33,7 +38,7 @@ namespace bwd_detail {
 constexpr int kChunk = 16;  // edges per chunk
 
 struct DstSmem {
-  int Rp, off_b, off_v, off_rho, off_dg, off_y, off_phi, off_dy, off_dphi, off_j, off_idx, floats;
+  int Rp, off_b, off_v, off_rho, off_dg, off_y, off_phi, off_dy, off_dphi, off_j, off_idx, off_sc, floats;
 };
 
 __host__ __device__ inline DstSmem dst_smem(int RT, int d, int n_radial) {
@@ -60,31 +65,30 @@ __host__ __device__ inline DstSmem dst_smem(int RT, int d, int n_radial) {
   o += kChunk * 3 * d;
   s.off_idx = o;
   o += 2 * kChunk;
+  s.off_sc = o;
+  o += kChunk;
   s.floats = o;
   return s;
 }
 
-template <typename TX>
-__device__ __forceinline__ void load4(const TX* p, float* out);
-template <>
-__device__ __forceinline__ void load4<float>(const float* p, float* out) {
-  const f32x4 v = *reinterpret_cast<const f32x4*>(p);
-  out[0] = v[0];
-  out[1] = v[1];
-  out[2] = v[2];
-  out[3] = v[3];
-}
-template <>
-__device__ __forceinline__ void load4<uint16_t>(const uint16_t* p, float* out) {
-  const uint2 v = *reinterpret_cast<const uint2*>(p);
-  out[0] = __uint_as_float(v.x << 16);
-  out[1] = __uint_as_float(v.x & 0xffff0000u);
-  out[2] = __uint_as_float(v.y << 16);
-  out[3] = __uint_as_float(v.y & 0xffff0000u);
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <bool BF>
+__device__ __forceinline__ f32x16 mfma16(u32x4 a, u32x4 b, f32x16 c) {
+  if constexpr (BF)
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                   0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                  0, 0);
 }
 
-template <int MT, int RT, int NCT, typename TX>
+template <int MT, int RT, int NCT, bool BF>
 __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
+  constexpr int P = BF ? 1 : 2;    // 16-bit parts per operand value
+  constexpr int NS = 2 * NCT;      // K-steps of 16 channels (xd blocks per part)
   extern __shared__ float smem[];
   const DstSmem S = dst_smem(RT, a.d, a.n_radial);
   constexpr int Rp = RT * kTile;
@@ -100,6 +104,7 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
   float* sJ = smem + S.off_j;
   int* sIdx = reinterpret_cast<int*>(smem + S.off_idx);
   int* sEid = sIdx + kChunk;
+  float* sSc = smem + S.off_sc;  // 2^e of the edge's x row (fp32 problems)
 
   const int seg = xcd_remap(blockIdx.x, a.n_seg);
   const int e_begin = a.offsets[seg], e_end = a.offsets[seg + 1];
@@ -108,13 +113,12 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
   const int h = lane >> 5, l32 = lane & 31;
   const int d = a.d, C = a.C, nr = a.n_radial, R = a.R;
   const int r = rt * kTile + l32;
-  const TX* __restrict__ x = static_cast<const TX*>(a.x);
 
   for (int i = tid; i < (d + nr) * Rp; i += blockDim.x) {
     const int k = i / Rp, rr = i - k * Rp;
     sB[i] = rr < R ? (k < d ? a.Bf[k * R + rr] : a.radial_w[(k - d) * R + rr]) : 0.f;
   }
-  // factor A in registers, in P^T accumulator layout: Areg[kt][v] = A[kt*32 + acc_row(v,h)][r]
+  // factor A in registers, in P accumulator layout: Areg[kt][v] = A[kt*32 + acc_row(v,h)][r]
   float Areg[MT][16];
 #pragma unroll
   for (int kt = 0; kt < MT; ++kt)
@@ -125,34 +129,74 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
     }
 
   // Gh^T tiles: gh[ct] = Gz[seg]^T D restricted to (channel tile ct, rank tile rt)
-  f32x16 gh[NCT];
+  u32x4 ghp[NCT][2][P];  // [channel tile][K-step][part]
+  float gh_unscale = 1.f;
+  {
+    f32x16 gh[NCT];
 #pragma unroll
-  for (int ct = 0; ct < NCT; ++ct) {
-    gh[ct] = f32x16{};
-    const int cc = ct * kTile + l32;
-    for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
-      const int k = 2 * s2 + h;
-      const float av = (k < d && cc < C) ? a.Gz[(size_t(seg) * d + k) * C + cc] : 0.f;
-      const float bv = (k < d && r < R) ? a.D[k * R + r] : 0.f;
-      gh[ct] = mfma32(av, bv, gh[ct]);
-    }
-  }
-
-  // A operand of step (edge row `row`, channel tile ct): for k tile kt,
-  // x[row][kt*32 + l32][ct*32 + 8q + 4h + i] -> xb[kt*16 + 4q + i].  Rows past
-  // d are clamped (their P rows meet A = 0); channels past C are clamped
-  // (they meet Gh = 0).
-  auto load_step = [&](int row, int ct, float (&xb)[MT * 16]) {
-#pragma unroll
-    for (int kt = 0; kt < MT; ++kt) {
-      const int kr = kt * kTile + l32 < d ? kt * kTile + l32 : d - 1;
-      const TX* p = x + (size_t(row) * d + kr) * C;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int c0 = ct * kTile + 8 * q + 4 * h;
-        load4<TX>(p + (c0 < C ? c0 : C - 4), &xb[kt * 16 + 4 * q]);
+    for (int ct = 0; ct < NCT; ++ct) {
+      gh[ct] = f32x16{};
+      const int cc = ct * kTile + l32;
+      for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
+        const int k = 2 * s2 + h;
+        const float av = (k < d && cc < C) ? a.Gz[(size_t(seg) * d + k) * C + cc] : 0.f;
+        const float bv = (k < d && r < R) ? a.D[k * R + r] : 0.f;
+        gh[ct] = mfma32(av, bv, gh[ct]);
       }
     }
+    float sc = 1.f;
+    if constexpr (!BF) {
+      // the wave's largest |Gh^T| to [2^13, 2^14)
+      float mx = 0.f;
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, fabsf(gh[ct][v]));
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      const int e = f16_split_exponent(mx);
+      sc = ldexpf(1.f, -e);
+      gh_unscale = ldexpf(1.f, e);
+    }
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        uint32_t w[P][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float v0 = gh[ct][8 * q + 2 * i] * sc, v1 = gh[ct][8 * q + 2 * i + 1] * sc;
+          if constexpr (BF)
+            w[0][i] = pack_bf16x2_rne(v0, v1);
+          else
+            split_f16x2_pair(v0, v1, w[0][i], w[1][i]);
+        }
+#pragma unroll
+        for (int p = 0; p < P; ++p) ghp[ct][q][p] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
+      }
+  }
+
+  // x operand of channel tile ct for an edge row: xb[kt][q][p] is lane (h,
+  // row kt*32 + l32) of block (part p, K-step 2ct + q) of xd.  Rows past d are
+  // clamped (their P rows meet A = 0).
+  const char* __restrict__ xd = static_cast<const char*>(a.xc);
+  const size_t node_bytes = size_t(P) * NS * 2 * d * 16;
+  uint32_t lane_off[MT];
+#pragma unroll
+  for (int kt = 0; kt < MT; ++kt) {
+    const int kr = kt * kTile + l32 < d ? kt * kTile + l32 : d - 1;
+    lane_off[kt] = uint32_t((h * d + kr) * 16);
+  }
+  auto load_step = [&](int row, int ct, u32x4 (&xb)[MT][2][P]) {
+    const char* base = xd + size_t(row) * node_bytes;
+#pragma unroll
+    for (int kt = 0; kt < MT; ++kt)
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+          xb[kt][q][p] =
+              *reinterpret_cast<const u32x4*>(base + lane_off[kt] + uint32_t((p * NS + 2 * ct + q) * 2 * d * 16));
   };
 
   for (int cb = e_begin; cb < e_end; cb += kChunk) {
@@ -175,8 +219,10 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
     }
     for (int t = tid; t < n; t += blockDim.x) {
       const int eid = a.perm[cb + t];
+      const int row = a.src[eid];
       sEid[t] = eid;
-      sIdx[t] = a.src[eid];
+      sIdx[t] = row;
+      sSc[t] = BF ? 1.f : a.x_scale[row];
     }
     __syncthreads();
     for (int i = tid; i < n * Rp; i += blockDim.x) {
@@ -188,12 +234,12 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
       sRho[i] = rho;
     }
 
-    // P_e^T tiles and dg, edges in pairs so that the buffer of every
+    // P_e tiles and dg, edges in pairs so that the buffer of every
     // (edge, ct) step is a compile-time choice; an odd last edge is paired
     // with a copy of itself whose result is dropped.
-    float xb0[MT * 16], xb1[MT * 16];
+    u32x4 xb0[MT][2][P], xb1[MT][2][P];
     f32x16 p[MT];
-    load_step(sIdx[0], 0, xb0);
+    load_step(__builtin_amdgcn_readfirstlane(sIdx[0]), 0, xb0);
     for (int e0 = 0; e0 < n; e0 += 2) {
       const int e1 = e0 + 1 < n ? e0 + 1 : e0;
       const int e2 = e0 + 2 < n ? e0 + 2 : e1;
@@ -207,7 +253,7 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
           // issue the loads of the next step
           {
             const bool last_ct = ct + 1 == NCT;
-            const int nrow = last_ct ? sIdx[half_e ? e2 : e1] : sIdx[e];
+            const int nrow = __builtin_amdgcn_readfirstlane(last_ct ? sIdx[half_e ? e2 : e1] : sIdx[e]);
             const int nct = last_ct ? 0 : ct + 1;
             if ((s + 1) & 1)
               load_step(nrow, nct, xb1);
@@ -220,9 +266,17 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
             for (int kt = 0; kt < MT; ++kt) p[kt] = f32x16{};
           }
 #pragma unroll
-          for (int kt = 0; kt < MT; ++kt)
+          for (int q = 0; q < 2; ++q)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) p[kt] = mfma32(s & 1 ? xb1[kt * 16 + v] : xb0[kt * 16 + v], gh[ct][v], p[kt]);
+            for (int kt = 0; kt < MT; ++kt) {
+              const u32x4(&xq)[P] = s & 1 ? xb1[kt][q] : xb0[kt][q];
+              const u32x4(&gq)[P] = ghp[ct][q];
+              if constexpr (!BF) {
+                p[kt] = mfma16<BF>(xq[1], gq[0], p[kt]);
+                p[kt] = mfma16<BF>(xq[0], gq[1], p[kt]);
+              }
+              p[kt] = mfma16<BF>(xq[0], gq[0], p[kt]);
+            }
           __builtin_amdgcn_sched_barrier(0);
           if (ct + 1 == NCT && (half_e == 0 || e1 != e0)) {
             float part = 0.f;
@@ -231,7 +285,7 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
 #pragma unroll
               for (int v = 0; v < 16; ++v) part += Areg[kt][v] * p[kt][v];
             part += __shfl_xor(part, 32);
-            if (h == 0) sDG[e * Rp + r] = part;
+            if (h == 0) sDG[e * Rp + r] = part * (sSc[e] * gh_unscale);
           }
         }
       }
@@ -286,10 +340,10 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
   }
 }
 
-template <int MT, int RT, int NCT, typename TX>
+template <int MT, int RT, int NCT, bool BF>
 hipError_t launch_k(const BwdDstArgs& a, hipStream_t s) {
   const size_t lds = size_t(dst_smem(RT, a.d, a.n_radial).floats) * 4;
-  auto k = k_bwd_dst<MT, RT, NCT, TX>;
+  auto k = k_bwd_dst<MT, RT, NCT, BF>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      int(lds));
   if (e != hipSuccess) return e;
@@ -297,16 +351,15 @@ hipError_t launch_k(const BwdDstArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int MT, typename TX>
+template <int MT, bool BF>
 hipError_t launch_mt(const BwdDstArgs& a, hipStream_t s) {
   const int rt = (a.R + kTile - 1) / kTile;
-  const int nct = (a.C + kTile - 1) / kTile;
-  const int NC = nct <= 2 ? 2 : (nct <= 4 ? 4 : 8);
+  const int NC = bwd_direct_cpad(a.C) / kTile;
 #define TDN_BWD_CASE(RTV)                                   \
   case RTV:                                                 \
-    if (NC == 2) return launch_k<MT, RTV, 2, TX>(a, s);     \
-    if (NC == 4) return launch_k<MT, RTV, 4, TX>(a, s);     \
-    return launch_k<MT, RTV, 8, TX>(a, s);
+    if (NC == 2) return launch_k<MT, RTV, 2, BF>(a, s);     \
+    if (NC == 4) return launch_k<MT, RTV, 4, BF>(a, s);     \
+    return launch_k<MT, RTV, 8, BF>(a, s);
   switch (rt) {
     TDN_BWD_CASE(1)
     TDN_BWD_CASE(2)

@@ -139,6 +139,74 @@ hipError_t launch_channel_p(int N, int d, int C, int Cp, const TI* x, void* xc, 
   return hipGetLastError();
 }
 
+// xd[n][p][s][h][k][i] = part p of x[n][k][16 s + 8 (i/4) + 4 h + i%4] (zero
+// from channel C): the operand blocks of a 32x32x16 MFMA contracting
+// channels in the order in which the backward's direct kernel holds
+// Gh^T in accumulator registers.  P = 2: fp16 hi and lo of x[n] 2^-e_n with
+// 2^e_n (the row's largest |x| to [2^13, 2^14)) in row_scale[n]; P = 1:
+// bf16.  One block per node: its [d, C] rows staged in LDS with their
+// maximum, then one thread per (s, h, k) run of eight channels.
+template <int P, typename TI>
+__global__ __launch_bounds__(256) void k_direct_layout(int d, int C, int Cp, const TI* __restrict__ x,
+                                                       uint16_t* __restrict__ xd, float* __restrict__ row_scale) {
+  extern __shared__ float tile[];  // [d][C], then four floats for the row maximum
+  float* red = tile + d * C;
+  const int n = blockIdx.x;
+  const TI* src = x + size_t(n) * d * C;
+  float mx = 0.f;
+  for (int i = threadIdx.x; i < d * C; i += blockDim.x) {
+    const float v = to_f32(src[i]);
+    tile[i] = v;
+    mx = fmaxf(mx, fabsf(v));
+  }
+  float sc = 1.f;
+  if constexpr (P == 2) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+  }
+  __syncthreads();
+  if constexpr (P == 2) {
+    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    const int e = f16_split_exponent(mx);
+    sc = ldexpf(1.f, -e);
+    if (threadIdx.x == 0) row_scale[n] = ldexpf(1.f, e);
+  }
+  const int ns = Cp / 16;
+  uint16_t* dst = xd + size_t(n) * P * ns * 2 * d * 8;
+  // thread (s, h, k), k fastest: consecutive threads write consecutive 16 bytes
+  for (int i = threadIdx.x; i < ns * 2 * d; i += blockDim.x) {
+    const int k = i % d, sh = i / d, h = sh & 1, st = sh >> 1;
+    uint32_t w[P][4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i0 = 2 * q;  // elements i0, i0 + 1 of the run
+      const int c0 = 16 * st + 8 * (i0 / 4) + 4 * h + i0 % 4;
+      const float v0 = c0 < C ? tile[k * C + c0] : 0.f;
+      const float v1 = c0 + 1 < C ? tile[k * C + c0 + 1] : 0.f;
+      if constexpr (P == 2)
+        split_f16x2_pair(v0 * sc, v1 * sc, w[0][q], w[1][q]);
+      else
+        w[0][q] = pack_bf16x2_rne(v0, v1);
+    }
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+      *reinterpret_cast<u32x4*>(dst + ((size_t(p) * ns * 2 + sh) * d + k) * 8) =
+          u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
+  }
+}
+
+template <int P, typename TI>
+hipError_t launch_direct_p(int N, int d, int C, int Cp, const TI* x, void* xd, float* row_scale, hipStream_t s) {
+  const size_t lds = (size_t(d) * C + 4) * 4;
+  auto k = k_direct_layout<P, TI>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     int(lds));
+  if (e != hipSuccess) return e;
+  k<<<dim3(N), dim3(256), lds, s>>>(d, C, Cp, x, static_cast<uint16_t*>(xd), row_scale);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 int edge_kpad(int d) { return d <= 32 ? 32 : 64; }
@@ -154,6 +222,19 @@ hipError_t launch_channel_layout(int N, int d, int C, int Cp, const void* x, boo
   if (parts != 1) return hipErrorInvalidValue;
   return x_is_f32 ? launch_channel_p<1>(N, d, C, Cp, static_cast<const float*>(x), xc, s)
                   : launch_channel_p<1>(N, d, C, Cp, static_cast<const uint16_t*>(x), xc, s);
+}
+
+hipError_t launch_direct_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xd,
+                                float* row_scale, hipStream_t s) {
+  if (N == 0) return hipSuccess;
+  if (Cp < C || Cp % 16 || size_t(d) * C * 4 + 16 > 160 * 1024) return hipErrorInvalidValue;
+  if (parts == 2) {
+    if (!x_is_f32 || !row_scale) return hipErrorInvalidValue;
+    return launch_direct_p<2>(N, d, C, Cp, static_cast<const float*>(x), xd, row_scale, s);
+  }
+  if (parts != 1) return hipErrorInvalidValue;
+  return x_is_f32 ? launch_direct_p<1>(N, d, C, Cp, static_cast<const float*>(x), xd, nullptr, s)
+                  : launch_direct_p<1>(N, d, C, Cp, static_cast<const uint16_t*>(x), xd, nullptr, s);
 }
 
 hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,

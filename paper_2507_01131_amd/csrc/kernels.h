@@ -82,6 +82,14 @@ hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f
 // block of rows k < d.
 hipError_t launch_channel_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xc,
                                  hipStream_t s);
+// Features for the backward's direct destination kernel (d > 32): xd
+// [N, parts, Cp / 16, 2, d, 8] of 16-bit values, element [n][p][s][h][k][i] =
+// part p of x[n][k][16 s + 8 (i / 4) + 4 h + i % 4] (zero from channel C, Cp a
+// multiple of 16): the contraction over channels in the order of the
+// kernel's accumulator registers.  parts = 2: fp16 hi and lo of x[n] 2^-e_n
+// and row_scale[n] = 2^e_n as for the edge pass; parts = 1: bf16.
+hipError_t launch_direct_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xd,
+                                float* row_scale, hipStream_t s);
 // parts = 2: fp32 features (fp16 two-part split), parts = 1: bf16 features
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
 
@@ -113,7 +121,9 @@ struct BwdDstArgs {
   const void* x;            // [N, d, C]
   const float* Gz;          // [N, d, C] = grad_out W^T
   float* grad_vec;          // [E, 3] by edge id
-  const void* xc;           // x blocked by launch_channel_layout with Cp = bwd_dst_cpad(C, bf16)
+  const void* xc;           // x blocked by launch_channel_layout (Cp = bwd_dst_cpad(C, bf16)), or for
+                            // the direct kernel (d > 32) by launch_direct_layout (Cp = 32 ceil(C / 32))
+  const float* x_scale;     // direct kernel, fp32 problems: row_scale of launch_direct_layout
   int n_range;              // equal edge ranges (bwd_dst_plan)
   int pieces_per_block;     // ranges per workgroup
 };
@@ -124,6 +134,9 @@ struct BwdDstArgs {
 EdgePlan bwd_dst_plan(int L, int R, int C, int n_radial, bool bf16, int E);
 // channel count of its x layout: C padded to the kernel's ring turn
 int bwd_dst_cpad(int C, bool bf16);
+// Channels of the direct kernel's xd layout (d > 32): C rounded up to 64, 128
+// or 256 (two, four or eight 32-channel tiles).
+__host__ __device__ inline int bwd_direct_cpad(int C) { return C <= 64 ? 64 : (C <= 128 ? 128 : 256); }
 hipError_t launch_bwd_dst(const BwdDstArgs& a, bool x_bf16, hipStream_t s);
 
 // ---------------------------------------------------------------- misc
