@@ -36,6 +36,7 @@ namespace tdn {
 namespace bwd_detail {
 
 constexpr int kChunk = 16;  // edges per chunk
+static_assert(kChunk <= kTile, "one 32-row MFMA tile of edges");
 
 struct DstSmem {
   int Rp, off_b, off_v, off_rho, off_dg, off_y, off_phi, off_dy, off_dphi, off_j, off_idx, off_sc, floats;
@@ -225,13 +226,31 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
       sSc[t] = BF ? 1.f : a.x_scale[row];
     }
     __syncthreads();
-    for (int i = tid; i < n * Rp; i += blockDim.x) {
-      const int e = i / Rp, rr = i - e * Rp;
-      float v = 0.f, rho = 0.f;
-      for (int k = 0; k < d; ++k) v += sB[k * Rp + rr] * sY[e * d + k];
-      for (int q = 0; q < nr; ++q) rho += sWr[q * Rp + rr] * sPhi[e * nr + q];
-      sV[i] = v;
-      sRho[i] = rho;
+    // v = Y B and rho = Phi Wrad for this wave's rank tile on fp32 MFMA (rows:
+    // the chunk's edges, padded to a 32-row tile)
+    {
+      f32x16 tv = f32x16{}, tr = f32x16{};
+#pragma unroll 4
+      for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
+        const int k = 2 * s2 + h;
+        const float av = (l32 < n && k < d) ? sY[l32 * d + k] : 0.f;
+        const float bv = k < d ? sB[k * Rp + r] : 0.f;
+        tv = mfma32(av, bv, tv);
+      }
+      for (int s2 = 0; s2 < (nr + 1) / 2; ++s2) {
+        const int q = 2 * s2 + h;
+        const float av = (l32 < n && q < nr) ? sPhi[l32 * nr + q] : 0.f;
+        const float bv = q < nr ? sWr[q * Rp + r] : 0.f;
+        tr = mfma32(av, bv, tr);
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int e = acc_row(v, h);
+        if (e < n) {
+          sV[e * Rp + r] = tv[v];
+          sRho[e * Rp + r] = tr[v];
+        }
+      }
     }
 
     // P_e tiles and dg, edges in pairs so that the buffer of every
@@ -298,22 +317,45 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
       sRho[i] = drho;
     }
     __syncthreads();
-    for (int i = tid; i < n * (d + nr); i += blockDim.x) {
-      const int e = i / (d + nr), k = i - e * (d + nr);
-      // each thread starts at its own rank so that a wave's LDS reads of the
-      // factor rows (stride Rp) fall in distinct banks
-      const float* fr = k < d ? sB + k * Rp : sWr + (k - d) * Rp;
-      const float* vr = (k < d ? sV : sRho) + e * Rp;
-      float s2 = 0.f;
-      int rr = k % Rp;
-      for (int j = 0; j < Rp; ++j) {
-        s2 += fr[rr] * vr[rr];
-        rr = rr + 1 == Rp ? 0 : rr + 1;
+    // dY = dV B^T (k < d <= 64: two output tiles) and dphi = dRho Wrad^T (one
+    // tile) on fp32 MFMA with this wave's rank tile as the contraction range;
+    // the per-wave partials go to the v/rho/dg region (3 x kChunk x Rp floats
+    // = RT waves x 3 tiles x kChunk rows x 32) and are summed over the rank
+    // tiles in a fixed order.
+    {
+      f32x16 py[3] = {f32x16{}, f32x16{}, f32x16{}};
+#pragma unroll 4
+      for (int s2 = 0; s2 < kTile / 2; ++s2) {
+        const int rr = rt * kTile + 2 * s2 + h;
+        const float a_v = l32 < n ? sV[l32 * Rp + rr] : 0.f;
+        const float a_r = l32 < n ? sRho[l32 * Rp + rr] : 0.f;
+        const float b0 = l32 < d ? sB[l32 * Rp + rr] : 0.f;
+        const float b1 = kTile + l32 < d ? sB[(kTile + l32) * Rp + rr] : 0.f;
+        const float b2 = l32 < nr ? sWr[l32 * Rp + rr] : 0.f;
+        py[0] = mfma32(a_v, b0, py[0]);
+        py[1] = mfma32(a_v, b1, py[1]);
+        py[2] = mfma32(a_r, b2, py[2]);
       }
-      if (k < d)
-        sDY[e * d + k] = s2;
-      else
-        sDPhi[e * nr + (k - d)] = s2;
+      __syncthreads();  // every wave has read dv and drho
+      float* sPart = sV;
+#pragma unroll
+      for (int t3 = 0; t3 < 3; ++t3)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int e = acc_row(v, h);
+          if (e < n) sPart[((rt * 3 + t3) * kChunk + e) * kTile + l32] = py[t3][v];
+        }
+      __syncthreads();
+      for (int i = tid; i < n * 3 * kTile; i += blockDim.x) {
+        const int e = i / (3 * kTile), c = i - e * 3 * kTile, t3 = c / kTile, col = c - t3 * kTile;
+        float sum = 0.f;
+        for (int w = 0; w < RT; ++w) sum += sPart[((w * 3 + t3) * kChunk + e) * kTile + col];
+        if (t3 < 2) {
+          if (t3 * kTile + col < d) sDY[e * d + t3 * kTile + col] = sum;
+        } else if (col < nr) {
+          sDPhi[e * nr + col] = sum;
+        }
+      }
     }
     __syncthreads();
     if (tid < n) {
