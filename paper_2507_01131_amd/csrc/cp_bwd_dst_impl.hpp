@@ -36,24 +36,24 @@ namespace tdn {
 namespace bwd_detail {
 
 constexpr int kChunk = 16;  // edges per chunk
-static_assert(kChunk <= kTile, "one 32-row MFMA tile of edges");
+static_assert(kChunk <= kTile, "a chunk's edges fit one 32-row MFMA tile");
 
 struct DstSmem {
   int Rp, off_b, off_v, off_rho, off_dg, off_y, off_phi, off_dy, off_dphi, off_j, off_idx, off_sc, floats;
 };
 
-__host__ __device__ inline DstSmem dst_smem(int RT, int d, int n_radial) {
+__host__ __device__ inline DstSmem dst_smem(int RT, int MT, int d, int n_radial) {
   DstSmem s{};
   s.Rp = RT * kTile;
   int o = 0;
-  s.off_b = o;  // B [d][Rp] then Wrad [n_radial][Rp]
-  o += (d + n_radial) * s.Rp;
+  s.off_b = o;  // A in accumulator order: [MT][RT][4][64 lanes] x float4
+  o += MT * RT * 4 * kWave * 4;
   s.off_v = o;
   o += kChunk * s.Rp;
   s.off_rho = o;
   o += kChunk * s.Rp;
   s.off_dg = o;
-  o += kChunk * s.Rp;
+  o += MT * kChunk * s.Rp;
   s.off_y = o;
   o += kChunk * d;
   s.off_phi = o;
@@ -86,18 +86,21 @@ __device__ __forceinline__ f32x16 mfma16(u32x4 a, u32x4 b, f32x16 c) {
                                                   0, 0);
 }
 
+// Waves of the workgroup: MT k tiles x ceil(RT / 2) pairs of rank tiles.
+__host__ __device__ constexpr int direct_waves(int MT, int RT) { return MT * ((RT + 1) / 2); }
+
 template <int MT, int RT, int NCT, bool BF>
-__global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
-  constexpr int P = BF ? 1 : 2;    // 16-bit parts per operand value
-  constexpr int NS = 2 * NCT;      // K-steps of 16 channels (xd blocks per part)
+__global__ __launch_bounds__(direct_waves(MT, RT)* kWave) void k_bwd_dst(BwdDstArgs a) {
+  constexpr int P = BF ? 1 : 2;  // 16-bit parts per operand value
+  constexpr int NS = 2 * NCT;    // K-steps of 16 channels (xd blocks per part)
+  constexpr int NW = direct_waves(MT, RT);
   extern __shared__ float smem[];
-  const DstSmem S = dst_smem(RT, a.d, a.n_radial);
+  const DstSmem S = dst_smem(RT, MT, a.d, a.n_radial);
   constexpr int Rp = RT * kTile;
-  float* sB = smem + S.off_b;
-  float* sWr = sB + a.d * Rp;
+  f32x4* sAl = reinterpret_cast<f32x4*>(smem + S.off_b);
   float* sV = smem + S.off_v;
   float* sRho = smem + S.off_rho;
-  float* sDG = smem + S.off_dg;
+  float* sDG = smem + S.off_dg;  // [MT][kChunk][Rp]: dg over each k tile
   float* sY = smem + S.off_y;
   float* sPhi = smem + S.off_phi;
   float* sDY = smem + S.off_dy;
@@ -110,29 +113,39 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
   const int seg = xcd_remap(blockIdx.x, a.n_seg);
   const int e_begin = a.offsets[seg], e_end = a.offsets[seg + 1];
   if (e_begin == e_end) return;
-  const int tid = threadIdx.x, lane = tid & 63, rt = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, l32 = lane & 31;
   const int d = a.d, C = a.C, nr = a.n_radial, R = a.R;
-  const int r = rt * kTile + l32;
+  // the P_e tiles of this wave: k tile kt, rank tiles 2j and 2j + 1
+  const int kt = wave % MT, pj = wave / MT;
+  int rtw[2];
+  rtw[0] = 2 * pj;
+  rtw[1] = 2 * pj + 1 < RT ? 2 * pj + 1 : 2 * pj;  // a lone last tile runs twice; the copy is dropped
+  const bool has2 = 2 * pj + 1 < RT;
 
-  for (int i = tid; i < (d + nr) * Rp; i += blockDim.x) {
-    const int k = i / Rp, rr = i - k * Rp;
-    sB[i] = rr < R ? (k < d ? a.Bf[k * R + rr] : a.radial_w[(k - d) * R + rr]) : 0.f;
-  }
-  // factor A in registers, in P accumulator layout: Areg[kt][v] = A[kt*32 + acc_row(v,h)][r]
-  float Areg[MT][16];
+  // sAl[((kt*RT + rt)*4 + qq)*64 + lane'] = A[kt*32 + acc_row(4 qq + i, h')][rt*32 + l32']:
+  // the A values lane' weighs its P accumulators with, one 16-byte read per quarter
+  for (int t = tid; t < MT * RT * 4 * kWave; t += blockDim.x) {
+    const int ln = t % kWave, q4 = t / kWave;
+    const int qq = q4 % 4, krt = q4 / 4, rt = krt % RT, kt2 = krt / RT;
+    const int r = rt * kTile + (ln & 31);
+    f32x4 v;
 #pragma unroll
-  for (int kt = 0; kt < MT; ++kt)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int k = kt * kTile + acc_row(v, h);
-      Areg[kt][v] = (k < d && r < R) ? a.A[k * R + r] : 0.f;
+    for (int i = 0; i < 4; ++i) {
+      const int k = kt2 * kTile + acc_row(4 * qq + i, ln >> 5);
+      v[i] = (k < d && r < R) ? a.A[k * R + r] : 0.f;
     }
+    sAl[t] = v;
+  }
 
-  // Gh^T tiles: gh[ct] = Gz[seg]^T D restricted to (channel tile ct, rank tile rt)
-  u32x4 ghp[NCT][2][P];  // [channel tile][K-step][part]
-  float gh_unscale = 1.f;
-  {
+  // Gh^T tiles of the wave's two rank tiles, each scaled by its own power of
+  // two (fp32 problems) and split: ghp[t][ct][q][p]
+  u32x4 ghp[2][NCT][2][P];
+  float gh_unscale[2] = {1.f, 1.f};
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int r = rtw[t] * kTile + l32;
     f32x16 gh[NCT];
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct) {
@@ -147,7 +160,6 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
     }
     float sc = 1.f;
     if constexpr (!BF) {
-      // the wave's largest |Gh^T| to [2^13, 2^14)
       float mx = 0.f;
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct)
@@ -157,7 +169,7 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
       for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
       const int e = f16_split_exponent(mx);
       sc = ldexpf(1.f, -e);
-      gh_unscale = ldexpf(1.f, e);
+      gh_unscale[t] = ldexpf(1.f, e);
     }
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct)
@@ -173,31 +185,24 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
             split_f16x2_pair(v0, v1, w[0][i], w[1][i]);
         }
 #pragma unroll
-        for (int p = 0; p < P; ++p) ghp[ct][q][p] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
+        for (int p = 0; p < P; ++p) ghp[t][ct][q][p] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
       }
   }
 
-  // x operand of channel tile ct for an edge row: xb[kt][q][p] is lane (h,
-  // row kt*32 + l32) of block (part p, K-step 2ct + q) of xd.  Rows past d are
+  // x operand of channel tile ct for an edge row: xb[q][p] is lane (h, row
+  // kt*32 + l32) of block (part p, K-step 2ct + q) of xd.  Rows past d are
   // clamped (their P rows meet A = 0).
   const char* __restrict__ xd = static_cast<const char*>(a.xc);
   const size_t node_bytes = size_t(P) * NS * 2 * d * 16;
-  uint32_t lane_off[MT];
-#pragma unroll
-  for (int kt = 0; kt < MT; ++kt) {
-    const int kr = kt * kTile + l32 < d ? kt * kTile + l32 : d - 1;
-    lane_off[kt] = uint32_t((h * d + kr) * 16);
-  }
-  auto load_step = [&](int row, int ct, u32x4 (&xb)[MT][2][P]) {
+  const int kr = kt * kTile + l32 < d ? kt * kTile + l32 : d - 1;
+  const uint32_t lane_off = uint32_t((h * d + kr) * 16);
+  auto load_step = [&](int row, int ct, u32x4 (&xb)[2][P]) {
     const char* base = xd + size_t(row) * node_bytes;
 #pragma unroll
-    for (int kt = 0; kt < MT; ++kt)
+    for (int q = 0; q < 2; ++q)
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
-#pragma unroll
-        for (int p = 0; p < P; ++p)
-          xb[kt][q][p] =
-              *reinterpret_cast<const u32x4*>(base + lane_off[kt] + uint32_t((p * NS + 2 * ct + q) * 2 * d * 16));
+      for (int p = 0; p < P; ++p)
+        xb[q][p] = *reinterpret_cast<const u32x4*>(base + lane_off + uint32_t((p * NS + 2 * ct + q) * 2 * d * 16));
   };
 
   for (int cb = e_begin; cb < e_end; cb += kChunk) {
@@ -226,21 +231,22 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
       sSc[t] = BF ? 1.f : a.x_scale[row];
     }
     __syncthreads();
-    // v = Y B and rho = Phi Wrad for this wave's rank tile on fp32 MFMA (rows:
-    // the chunk's edges, padded to a 32-row tile)
-    {
+    // v = Y B and rho = Phi Wrad per rank tile on fp32 MFMA (rows: the chunk's
+    // edges, padded to a 32-row tile), one rank tile per wave at a time
+    for (int rt = wave; rt < RT; rt += NW) {
+      const int r = rt * kTile + l32;
       f32x16 tv = f32x16{}, tr = f32x16{};
 #pragma unroll 4
       for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
         const int k = 2 * s2 + h;
         const float av = (l32 < n && k < d) ? sY[l32 * d + k] : 0.f;
-        const float bv = k < d ? sB[k * Rp + r] : 0.f;
+        const float bv = (k < d && r < R) ? a.Bf[k * R + r] : 0.f;
         tv = mfma32(av, bv, tv);
       }
       for (int s2 = 0; s2 < (nr + 1) / 2; ++s2) {
         const int q = 2 * s2 + h;
         const float av = (l32 < n && q < nr) ? sPhi[l32 * nr + q] : 0.f;
-        const float bv = q < nr ? sWr[q * Rp + r] : 0.f;
+        const float bv = (q < nr && r < R) ? a.radial_w[q * R + r] : 0.f;
         tr = mfma32(av, bv, tr);
       }
 #pragma unroll
@@ -253,11 +259,11 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
       }
     }
 
-    // P_e tiles and dg, edges in pairs so that the buffer of every
-    // (edge, ct) step is a compile-time choice; an odd last edge is paired
-    // with a copy of itself whose result is dropped.
-    u32x4 xb0[MT][2][P], xb1[MT][2][P];
-    f32x16 p[MT];
+    // P_e tiles and dg over this wave's k tile, edges in pairs so that the
+    // buffer of every (edge, ct) step is a compile-time choice; an odd last
+    // edge is paired with a copy of itself whose result is dropped.
+    u32x4 xb0[2][P], xb1[2][P];
+    f32x16 pacc[2];
     load_step(__builtin_amdgcn_readfirstlane(sIdx[0]), 0, xb0);
     for (int e0 = 0; e0 < n; e0 += 2) {
       const int e1 = e0 + 1 < n ? e0 + 1 : e0;
@@ -281,70 +287,85 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
           }
           __builtin_amdgcn_sched_barrier(0);
           if (ct == 0) {
-#pragma unroll
-            for (int kt = 0; kt < MT; ++kt) p[kt] = f32x16{};
+            pacc[0] = f32x16{};
+            pacc[1] = f32x16{};
           }
 #pragma unroll
           for (int q = 0; q < 2; ++q)
 #pragma unroll
-            for (int kt = 0; kt < MT; ++kt) {
-              const u32x4(&xq)[P] = s & 1 ? xb1[kt][q] : xb0[kt][q];
-              const u32x4(&gq)[P] = ghp[ct][q];
+            for (int t = 0; t < 2; ++t) {
+              const u32x4(&xq)[P] = s & 1 ? xb1[q] : xb0[q];
+              const u32x4(&gq)[P] = ghp[t][ct][q];
               if constexpr (!BF) {
-                p[kt] = mfma16<BF>(xq[1], gq[0], p[kt]);
-                p[kt] = mfma16<BF>(xq[0], gq[1], p[kt]);
+                pacc[t] = mfma16<BF>(xq[1], gq[0], pacc[t]);
+                pacc[t] = mfma16<BF>(xq[0], gq[1], pacc[t]);
               }
-              p[kt] = mfma16<BF>(xq[0], gq[0], p[kt]);
+              pacc[t] = mfma16<BF>(xq[0], gq[0], pacc[t]);
             }
           __builtin_amdgcn_sched_barrier(0);
           if (ct + 1 == NCT && (half_e == 0 || e1 != e0)) {
-            float part = 0.f;
+            const float sc = sSc[e];
 #pragma unroll
-            for (int kt = 0; kt < MT; ++kt)
+            for (int t = 0; t < 2; ++t) {
+              float part = 0.f;
 #pragma unroll
-              for (int v = 0; v < 16; ++v) part += Areg[kt][v] * p[kt][v];
-            part += __shfl_xor(part, 32);
-            if (h == 0) sDG[e * Rp + r] = part * (sSc[e] * gh_unscale);
+              for (int qq = 0; qq < 4; ++qq) {
+                const f32x4 av = sAl[((kt * RT + rtw[t]) * 4 + qq) * kWave + lane];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) part += av[i] * pacc[t][4 * qq + i];
+              }
+              part += __shfl_xor(part, 32);
+              if (h == 0 && (t == 0 || has2))
+                sDG[(kt * kChunk + e) * Rp + rtw[t] * kTile + l32] = part * (sc * gh_unscale[t]);
+            }
           }
         }
       }
     }
     __syncthreads();
     for (int i = tid; i < n * Rp; i += blockDim.x) {
-      const float dg = sDG[i];
+      float dg = sDG[i];
+#pragma unroll
+      for (int k2 = 1; k2 < MT; ++k2) dg += sDG[k2 * kChunk * Rp + i];
       const float dv = dg * sRho[i], drho = dg * sV[i];
       sV[i] = dv;
       sRho[i] = drho;
     }
     __syncthreads();
     // dY = dV B^T (k < d <= 64: two output tiles) and dphi = dRho Wrad^T (one
-    // tile) on fp32 MFMA with this wave's rank tile as the contraction range;
-    // the per-wave partials go to the v/rho/dg region (3 x kChunk x Rp floats
-    // = RT waves x 3 tiles x kChunk rows x 32) and are summed over the rank
-    // tiles in a fixed order.
+    // tile) on fp32 MFMA with one rank tile as the contraction range; the
+    // per-tile partials (RT tiles x 3 outputs x kChunk rows x 32 floats =
+    // 3 kChunk Rp) go to the v/rho/dg region ((2 + MT) kChunk Rp floats) and
+    // are summed over the rank tiles in a fixed order.
     {
       f32x16 py[3] = {f32x16{}, f32x16{}, f32x16{}};
+      const int rt = wave;  // RT <= NW: one rank tile per wave at most
+      if (rt < RT) {
 #pragma unroll 4
-      for (int s2 = 0; s2 < kTile / 2; ++s2) {
-        const int rr = rt * kTile + 2 * s2 + h;
-        const float a_v = l32 < n ? sV[l32 * Rp + rr] : 0.f;
-        const float a_r = l32 < n ? sRho[l32 * Rp + rr] : 0.f;
-        const float b0 = l32 < d ? sB[l32 * Rp + rr] : 0.f;
-        const float b1 = kTile + l32 < d ? sB[(kTile + l32) * Rp + rr] : 0.f;
-        const float b2 = l32 < nr ? sWr[l32 * Rp + rr] : 0.f;
-        py[0] = mfma32(a_v, b0, py[0]);
-        py[1] = mfma32(a_v, b1, py[1]);
-        py[2] = mfma32(a_r, b2, py[2]);
+        for (int s2 = 0; s2 < kTile / 2; ++s2) {
+          const int rr = rt * kTile + 2 * s2 + h;
+          const float a_v = l32 < n ? sV[l32 * Rp + rr] : 0.f;
+          const float a_r = l32 < n ? sRho[l32 * Rp + rr] : 0.f;
+          const bool rok = rr < R;
+          const float b0 = (rok && l32 < d) ? a.Bf[l32 * R + rr] : 0.f;
+          const float b1 = (rok && kTile + l32 < d) ? a.Bf[(kTile + l32) * R + rr] : 0.f;
+          const float b2 = (rok && l32 < nr) ? a.radial_w[l32 * R + rr] : 0.f;
+          py[0] = mfma32(a_v, b0, py[0]);
+          py[1] = mfma32(a_v, b1, py[1]);
+          py[2] = mfma32(a_r, b2, py[2]);
+        }
       }
       __syncthreads();  // every wave has read dv and drho
       float* sPart = sV;
+      if (rt < RT) {
 #pragma unroll
-      for (int t3 = 0; t3 < 3; ++t3)
+        for (int t3 = 0; t3 < 3; ++t3)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int e = acc_row(v, h);
-          if (e < n) sPart[((rt * 3 + t3) * kChunk + e) * kTile + l32] = py[t3][v];
-        }
+          for (int v = 0; v < 16; ++v) {
+            const int e = acc_row(v, h);
+            if (e < n) sPart[((rt * 3 + t3) * kChunk + e) * kTile + l32] = py[t3][v];
+          }
+      }
       __syncthreads();
       for (int i = tid; i < n * 3 * kTile; i += blockDim.x) {
         const int e = i / (3 * kTile), c = i - e * 3 * kTile, t3 = c / kTile, col = c - t3 * kTile;
@@ -384,12 +405,12 @@ __global__ __launch_bounds__(RT* kWave) void k_bwd_dst(BwdDstArgs a) {
 
 template <int MT, int RT, int NCT, bool BF>
 hipError_t launch_k(const BwdDstArgs& a, hipStream_t s) {
-  const size_t lds = size_t(dst_smem(RT, a.d, a.n_radial).floats) * 4;
+  const size_t lds = size_t(dst_smem(RT, MT, a.d, a.n_radial).floats) * 4;
   auto k = k_bwd_dst<MT, RT, NCT, BF>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      int(lds));
   if (e != hipSuccess) return e;
-  k<<<dim3(a.n_seg), dim3(RT * kWave), lds, s>>>(a);
+  k<<<dim3(a.n_seg), dim3(direct_waves(MT, RT) * kWave), lds, s>>>(a);
   return hipGetLastError();
 }
 
