@@ -73,6 +73,11 @@ SMALL = [
     dict(seed=5, N=64, E=2000, L=4, C=128, R=128, sort=False),
     dict(seed=6, N=25, E=500, L=4, C=256, R=256, sort=True),
     dict(seed=7, N=40, E=800, L=3, C=64, R=64, sort=False, feat_dtype="bf16"),
+    # d > 32 (direct destination kernel): channels not a multiple of 32, one
+    # rank-tile pair; bf16 with padded channel tiles; eight channel tiles
+    dict(seed=8, N=33, E=600, L=5, C=48, R=40, sort=False),
+    dict(seed=9, N=30, E=500, L=5, C=96, R=100, sort=True, feat_dtype="bf16"),
+    dict(seed=10, N=20, E=300, L=6, C=160, R=64, sort=False),
 ]
 
 
