@@ -54,9 +54,6 @@ tdn_status check_problem(const tdn_problem* p) {
 // 16-bit parts per feature of the edge pass: the fp16 two-part split of
 // fp32 features, or the bf16 features themselves
 int feature_parts(const tdn_problem& p) { return p.feat_dtype == TDN_BF16 ? 1 : 2; }
-// bf16 parts per feature of the backward's destination kernel: the exact
-// three-part split of fp32 features, or the bf16 features
-int dst_parts(const tdn_problem& p) { return p.feat_dtype == TDN_BF16 ? 1 : 3; }
 
 // features of the edge pass in MFMA operand blocks, then their row scales
 size_t xs_bytes(const tdn_problem& p) {
@@ -73,9 +70,11 @@ float* row_scales(const tdn_problem& p, void* xt) {
 size_t xd_bytes(const tdn_problem& p) {
   return size_t(p.n_nodes) * dim_of(p.L) * feature_parts(p) * tdn::bwd_direct_cpad(p.C) * 2;
 }
+size_t xc_bytes(const tdn_problem& p) {
+  return size_t(p.n_nodes) * dim_of(p.L) * feature_parts(p) * tdn::bwd_dst_cpad(p.C, p.feat_dtype == TDN_BF16) * 2;
+}
 size_t xt_xc_bytes(const tdn_problem& p) {
-  const size_t xc =
-      size_t(p.n_nodes) * dim_of(p.L) * dst_parts(p) * tdn::bwd_dst_cpad(p.C, p.feat_dtype == TDN_BF16) * 2;
+  const size_t xc = al(xc_bytes(p)) + size_t(p.n_nodes) * 4;
   const size_t xd = al(xd_bytes(p)) + size_t(p.n_nodes) * 4;
   return std::max(xt_bytes(p), std::max(xc, xd));
 }
@@ -392,19 +391,22 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
     a.n_range = dp.n_range;
     a.pieces_per_block = dp.per_block;
     if (a.n_range > 0) {
-      // x in parts, blocked as MFMA operands for the contraction over channels
-      // (the region is free until the grad_x pass lays out Gz there)
+      // x in parts (fp16 with row scales for fp32 problems, bf16), blocked as
+      // MFMA operands for the contraction over channels (the region is free
+      // until the grad_x pass lays out Gz there)
+      float* xscale = reinterpret_cast<float*>(ws + lay.xt + al(xc_bytes(*p)));
       Timed t("channel_layout", stream);
-      TDN_HIP(tdn::launch_channel_layout(N, d, C, tdn::bwd_dst_cpad(C, bf16), x, !bf16, dst_parts(*p), ws + lay.xt,
-                                         stream));
+      TDN_HIP(tdn::launch_direct_layout(N, d, C, tdn::bwd_dst_cpad(C, bf16), x, !bf16, feature_parts(*p), ws + lay.xt,
+                                        bf16 ? nullptr : xscale, false, stream));
       a.xc = ws + lay.xt;
+      a.x_scale = bf16 ? nullptr : xscale;
     } else if (d > 32) {
-      // x in the direct kernel's operand blocks, fp16 parts with row scales
-      // (fp32 problems) or bf16
+      // x in the direct kernel's operand blocks, channels in its accumulator
+      // order
       float* xscale = reinterpret_cast<float*>(ws + lay.xt + al(xd_bytes(*p)));
       Timed t("channel_layout", stream);
       TDN_HIP(tdn::launch_direct_layout(N, d, C, tdn::bwd_direct_cpad(C), x, !bf16, feature_parts(*p), ws + lay.xt,
-                                        bf16 ? nullptr : xscale, stream));
+                                        bf16 ? nullptr : xscale, true, stream));
       a.xc = ws + lay.xt;
       a.x_scale = bf16 ? nullptr : xscale;
     }

@@ -35,7 +35,7 @@ EdgePlan bwd_dst_plan(int L, int R, int C, int n_radial, bool bf16, int E) {
   const int RT = (R + kTile - 1) / kTile;
   if (E <= 0 || d > 32 || RT > 8) return EdgePlan{0, 0};
   const int chunk = dst2_chunk(RT, bf16, d, n_radial, C);
-  const int lds = dst2_smem(RT, bf16 ? 1 : 3, d, n_radial, C, chunk).floats * 4;
+  const int lds = dst2_smem(RT, bf16 ? 1 : 2, d, n_radial, C, chunk).floats * 4;
   if (lds > 160 * 1024) return EdgePlan{0, 0};
   int per_cu = 160 * 1024 / lds;
   per_cu = per_cu > 2 ? 2 : per_cu;  // eight waves per workgroup, two per SIMD
@@ -48,12 +48,12 @@ EdgePlan bwd_dst_plan(int L, int R, int C, int n_radial, bool bf16, int E) {
   return EdgePlan{nb * S, S};
 }
 
-int bwd_dst_cpad(int C, bool bf16) { return bwd2_detail::dst2_cpad(C, bf16 ? 1 : 3); }
+int bwd_dst_cpad(int C, bool bf16) { return bwd2_detail::dst2_cpad(C, bf16 ? 1 : 2); }
 
 hipError_t launch_bwd_dst(const BwdDstArgs& a, bool x_bf16, hipStream_t s) {
   if (a.n_seg == 0 || a.E == 0) return hipSuccess;
   if (a.n_range > 0) {
-    if (a.d > 32 || a.n_range > a.E || !a.xc || !a.dst) return hipErrorInvalidValue;
+    if (a.d > 32 || a.n_range > a.E || !a.xc || !a.dst || (!x_bf16 && !a.x_scale)) return hipErrorInvalidValue;
     switch (a.L) {
 #define TDN_DST2_CASE(LV) \
   case LV: return x_bf16 ? bwd2_detail::launch_l<LV, true>(a, a.n_range, s) : bwd2_detail::launch_l<LV, false>(a, a.n_range, s);

@@ -48,18 +48,26 @@ constexpr int kRing = 4;  // x slots per wave in the S loop
 constexpr int kMaxRadial = 16;
 constexpr int kBufferWord3 = 0x00020000;  // raw buffer resource, fourth word (gfx9 family)
 
-// K-steps of 16 channels per ring slot: one for the three-part (fp32)
+// K-steps of 16 channels per ring slot: one for the two-part (fp32)
 // operands, two for bf16
-__host__ __device__ constexpr int dst2_kps(int P) { return P == 3 ? 1 : 2; }
+__host__ __device__ constexpr int dst2_kps(int P) { return P == 2 ? 1 : 2; }
 // channels padded to whole ring turns
 __host__ __device__ inline int dst2_cpad(int C, int P) {
   const int turn = 16 * dst2_kps(P) * kRing;
   return (C + turn - 1) / turn * turn;
 }
 
-__device__ __forceinline__ f32x16 mfma_bf16(u32x4 a, u32x4 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
-                                                 0, 0);
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// 32x32x16 MFMA on fp16 operands (fp32 problems) or bf16 operands
+template <bool BF>
+__device__ __forceinline__ f32x16 mfma16(u32x4 a, u32x4 b, f32x16 c) {
+  if constexpr (BF)
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                   0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                  0, 0);
 }
 
 // Contraction row of K-step q (0, 1), half h, element i of T = S^T A: the S
@@ -109,7 +117,7 @@ __host__ __device__ inline Smem dst2_smem(int RT, int P, int d, int n_radial, in
   s.off_j = o;
   o += chunk * 3 * d;
   s.off_idx = o;
-  o += 6 * chunk;
+  o += 7 * chunk;
   s.floats = o;
   return s;
 }
@@ -118,7 +126,7 @@ __host__ __device__ inline Smem dst2_smem(int RT, int P, int d, int n_radial, in
 template <int L, int RT, bool BF>
 __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_range, int chunk) {
   constexpr int d = (L + 1) * (L + 1);
-  constexpr int P = BF ? 1 : 3;
+  constexpr int P = BF ? 1 : 2;
   constexpr int KPS = dst2_kps(P);
   constexpr int Rp = RT * kTile;
   extern __shared__ float smem[];
@@ -140,6 +148,8 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
   int* sEid = sIdx + chunk;                             // edge id
   int* sKey = sEid + chunk;                             // destination segment
   float* sVec = reinterpret_cast<float*>(sKey + chunk);  // edge vectors [chunk][3]
+  float* sXs = sVec + 3 * chunk;                         // 2^e of the edge's x row (fp32 problems)
+  float* sRed = smem + S.off_dy;                         // block maxima (free outside the dY phase)
 
   // ranges slot, slot + n_blocks, ...: at any time the workgroups of one XCD
   // work in one stretch of the destination-sorted edges, and their gathered
@@ -157,6 +167,22 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
     const float v = r < R ? (k < d ? a.Bf[k * R + r] : a.radial_w[(k - d) * R + r]) : 0.f;
     (k < d ? sB + k * bs : sWr + (k - d) * bs)[r] = v;
   }
+  // fp32 problems: the power of two 2^-e_A that puts A's largest |A| in
+  // [2^13, 2^14) for its fp16 parts; dg carries 2^e_A back
+  float a_sc = 1.f, a_unscale = 1.f;
+  if constexpr (!BF) {
+    float mx = 0.f;
+    for (int i = tid; i < d * R; i += blockDim.x) mx = fmaxf(mx, fabsf(a.A[i]));
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    if (lane == 0) sRed[wave] = mx;
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, sRed[w]);
+    const int e = f16_split_exponent(mx);
+    a_sc = ldexpf(1.f, -e);
+    a_unscale = ldexpf(1.f, e);
+  }
   // sAp[((q*RT + rt)*P + p)*64 + lane'] = part p of A[t_row(q, h', i)][rt*32 + l32'], i = 0..7
   for (int t = tid; t < 2 * RT * kWave; t += blockDim.x) {
     const int ln = t % kWave, qrt = t / kWave;
@@ -168,8 +194,8 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
       const int k0 = t_row(q, hh, 2 * p2), k1 = t_row(q, hh, 2 * p2 + 1);
       const float v0 = (k0 < d && r < R) ? a.A[k0 * R + r] : 0.f;
       const float v1 = (k1 < d && r < R) ? a.A[k1 * R + r] : 0.f;
-      if constexpr (P == 3)
-        split_bf16x3_pair(v0, v1, w[0][p2], w[1][p2], w[2][p2]);
+      if constexpr (P == 2)
+        split_f16x2_pair(v0 * a_sc, v1 * a_sc, w[0][p2], w[1][p2]);
       else
         w[0][p2] = pack_bf16x2_rne(v0, v1);
     }
@@ -191,6 +217,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
     sDl[t] = v;
   }
 
+  float gz_unscale = 1.f;  // 2^e_g of the staged Gz (fp32 problems)
   // ---- per edge: S_e, T_e, dg -> dv, drho (in place in sV, sRho)
   // The x operand streams through a ring of kRing slots per wave, kRing - 1
   // slots ahead of the MFMA and on into the wave's next edge of the piece, so
@@ -230,18 +257,28 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
     for (int kk = 0; kk < KPS; ++kk) {
       const u32x4(&xp)[P] = xb[kk];
       const u32x4(&gp)[P] = g[kk];
-      if constexpr (P == 3) {
-        Sacc = mfma_bf16(xp[0], gp[2], Sacc);
-        Sacc = mfma_bf16(xp[2], gp[0], Sacc);
-        Sacc = mfma_bf16(xp[1], gp[1], Sacc);
-        Sacc = mfma_bf16(xp[0], gp[1], Sacc);
-        Sacc = mfma_bf16(xp[1], gp[0], Sacc);
+      if constexpr (P == 2) {
+        Sacc = mfma16<BF>(xp[1], gp[0], Sacc);
+        Sacc = mfma16<BF>(xp[0], gp[1], Sacc);
       }
-      Sacc = mfma_bf16(xp[0], gp[0], Sacc);
+      Sacc = mfma16<BF>(xp[0], gp[0], Sacc);
     }
   };
   auto finish_edge = [&](int e, const f32x16& Sacc) {
-    // S in parts, regrouped as the A operand of T's two K-steps
+    // S in parts, regrouped as the A operand of T's two K-steps; fp32
+    // problems scale the tile by the power of two that puts its largest |S|
+    // in [2^13, 2^14) first, and dg takes back all four scales
+    float s_sc = 1.f, unscale = 1.f;
+    if constexpr (P == 2) {
+      float mx = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, fabsf(Sacc[v]));
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      const int es = f16_split_exponent(mx);
+      s_sc = ldexpf(1.f, -es);
+      unscale = ldexpf(sXs[e] * gz_unscale * a_unscale, es);
+    }
     u32x4 sp[2][P];
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
@@ -249,8 +286,8 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
 #pragma unroll
       for (int p2 = 0; p2 < 4; ++p2) {
         const float v0 = Sacc[8 * q + 2 * p2], v1 = Sacc[8 * q + 2 * p2 + 1];
-        if constexpr (P == 3)
-          split_bf16x3_pair(v0, v1, w[0][p2], w[1][p2], w[2][p2]);
+        if constexpr (P == 2)
+          split_f16x2_pair(v0 * s_sc, v1 * s_sc, w[0][p2], w[1][p2]);
         else
           w[0][p2] = pack_bf16x2_rne(v0, v1);
       }
@@ -278,21 +315,18 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
         const u32x4(&a_)[P] = ap[rt & 1][q];
-        if constexpr (P == 3) {
-          T = mfma_bf16(sp[q][0], a_[2], T);
-          T = mfma_bf16(sp[q][2], a_[0], T);
-          T = mfma_bf16(sp[q][1], a_[1], T);
-          T = mfma_bf16(sp[q][0], a_[1], T);
-          T = mfma_bf16(sp[q][1], a_[0], T);
+        if constexpr (P == 2) {
+          T = mfma16<BF>(sp[q][1], a_[0], T);
+          T = mfma16<BF>(sp[q][0], a_[1], T);
         }
-        T = mfma_bf16(sp[q][0], a_[0], T);
+        T = mfma16<BF>(sp[q][0], a_[0], T);
       }
       // dg[r] = sum_j D[j, r] T[j, r]: this lane's 16 rows, then the other half
       float part = 0.f;
 #pragma unroll
       for (int v = 0; v < 16; ++v) part += dl[v / 4][v % 4] * T[v];
       const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(part), __float_as_uint(part), false, false);
-      part = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+      part = (__uint_as_float(sw[0]) + __uint_as_float(sw[1])) * unscale;
       if (h == 0) {
         const int r = rt * kTile + l32;
         sV[e * bs + r] = part * rho_e;  // dv
@@ -343,7 +377,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
   auto range_hi = [&](int pc) { return int(int64_t(pc * n_blocks + slot + 1) * a.E / n_range); };
   struct EdgeRec {
     int eid, src, dst;
-    float vx, vy, vz;
+    float vx, vy, vz, xs;
   };
   auto load_rec = [&](int eid, int cnt, EdgeRec& r) {
     if (tid < cnt) {
@@ -353,6 +387,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
       r.vx = a.edge_vec[3 * eid];
       r.vy = a.edge_vec[3 * eid + 1];
       r.vz = a.edge_vec[3 * eid + 2];
+      r.xs = BF ? 1.f : a.x_scale[r.src];
     }
   };
   int pc = 0, cb = range_lo(0), hi = range_hi(0);
@@ -380,6 +415,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
         sVec[3 * tid] = rec.vx;
         sVec[3 * tid + 1] = rec.vy;
         sVec[3 * tid + 2] = rec.vz;
+        sXs[tid] = rec.xs;
       }
       const int next_eid = tid < nn ? a.perm[ncb + tid] : 0;
       __syncthreads();
@@ -439,15 +475,32 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
         while (p1 < n && sKey[p1] == seg) ++p1;
         p1 = __builtin_amdgcn_readfirstlane(p1);
         if (seg != cur) {
+          // fp32 problems: Gz[seg] scaled by the power of two that puts its
+          // largest magnitude in [2^13, 2^14)
+          float g_sc = 1.f;
+          if constexpr (P == 2) {
+            float mx = 0.f;
+            for (int i = tid; i < d * C; i += blockDim.x) mx = fmaxf(mx, fabsf(a.Gz[size_t(seg) * d * C + i]));
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+            if (lane == 0) sRed[wave] = mx;
+            __syncthreads();
+            mx = 0.f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, sRed[w]);
+            const int eg = f16_split_exponent(mx);
+            g_sc = ldexpf(1.f, -eg);
+            gz_unscale = ldexpf(1.f, eg);
+          }
           // Gz[seg] rows j < 32 in parts, zero from row d and from channel C:
           // one thread per pair of channels
           for (int i = tid; i < kTile * (Cp / 2); i += blockDim.x) {
             const int j = i / (Cp / 2), c2 = 2 * (i - j * (Cp / 2));
             float2 g = make_float2(0.f, 0.f);
             if (j < d && c2 < C) g = *reinterpret_cast<const float2*>(a.Gz + (size_t(seg) * d + j) * C + c2);
-            uint32_t w[3];
-            if constexpr (P == 3)
-              split_bf16x3_pair(g.x, g.y, w[0], w[1], w[2]);
+            uint32_t w[2];
+            if constexpr (P == 2)
+              split_f16x2_pair(g.x * g_sc, g.y * g_sc, w[0], w[1]);
             else
               w[0] = pack_bf16x2_rne(g.x, g.y);
 #pragma unroll
@@ -523,7 +576,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
 // Chunk: the largest of 32, 16, 8 edges whose layout fits the 160 KB of LDS.
 inline int dst2_chunk(int RT, bool bf, int d, int n_radial, int C) {
   int chunk = kMaxChunk;
-  while (chunk > 8 && dst2_smem(RT, bf ? 1 : 3, d, n_radial, C, chunk).floats * 4 > 160 * 1024) chunk >>= 1;
+  while (chunk > 8 && dst2_smem(RT, bf ? 1 : 2, d, n_radial, C, chunk).floats * 4 > 160 * 1024) chunk >>= 1;
   return chunk;
 }
 
@@ -532,7 +585,7 @@ hipError_t launch_l_rt(const BwdDstArgs& a, int n_range, hipStream_t s) {
   if (a.pieces_per_block < 1 || n_range % a.pieces_per_block) return hipErrorInvalidValue;
   constexpr int d = (L + 1) * (L + 1);
   const int chunk = dst2_chunk(RT, BF, d, a.n_radial, a.C);
-  const size_t lds = size_t(dst2_smem(RT, BF ? 1 : 3, d, a.n_radial, a.C, chunk).floats) * 4;
+  const size_t lds = size_t(dst2_smem(RT, BF ? 1 : 2, d, a.n_radial, a.C, chunk).floats) * 4;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
   auto k = k_bwd_dst2<L, RT, BF>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,

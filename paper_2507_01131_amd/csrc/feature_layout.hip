@@ -12,8 +12,8 @@
 // One block per node: the node's [d, C] rows are staged in LDS (with their
 // largest magnitude), then each thread writes a group of eight k of one
 // channel in all P parts.
-// The backward's destination kernel contracts over channels instead and reads
-// x in bf16 MFMA operand blocks over channels (launch_channel_layout).
+// The backward's destination kernels contract over channels instead and read
+// x in MFMA operand blocks over channels (launch_direct_layout).
 #include "common.hpp"
 #include "kernels.h"
 
@@ -95,58 +95,15 @@ hipError_t launch_p(int N, int d, int C, const TI* x, void* xs, float* row_scale
                             : launch_dp<64, P>(N, d, C, x, o, row_scale, s);
 }
 
-// xc[n][p][s][h][k][i] = part p of x[n][k][16 s + 8 h + i] (zero from
-// channel C): for every node, part and K-step s of 16 channels, the operand
-// block of a 32x32x16 MFMA with the rows k < d, so that the 64 lanes of a
-// wave read one contiguous block.  One thread per (node, s, h, k), k fastest.
-template <int P, typename TI>
-__global__ __launch_bounds__(256) void k_channel_layout(int N, int d, int C, int Cp, const TI* __restrict__ x,
-                                                        uint16_t* __restrict__ xc) {
-  const int nks = Cp / 16;
-  const size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= size_t(N) * nks * 2 * d) return;
-  const int k = int(i % d);
-  size_t rest = i / d;
-  const int h = int(rest % 2);
-  rest /= 2;
-  const int st = int(rest % nks);
-  const size_t n = rest / nks;
-  const int c0 = 16 * st + 8 * h;
-  const TI* src = x + (n * d + k) * C;
-  uint32_t w[P][4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int c = c0 + 2 * q;
-    const float v0 = c < C ? to_f32(src[c]) : 0.f;
-    const float v1 = c + 1 < C ? to_f32(src[c + 1]) : 0.f;
-    if constexpr (P == 3)
-      split_bf16x3_pair(v0, v1, w[0][q], w[1][q], w[2][q]);
-    else
-      w[0][q] = pack_bf16x2_rne(v0, v1);
-  }
-#pragma unroll
-  for (int p = 0; p < P; ++p) {
-    uint16_t* dst = xc + ((((n * P + p) * nks + st) * 2 + h) * d + k) * 8;
-    *reinterpret_cast<u32x4*>(dst) = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
-  }
-}
-
-template <int P, typename TI>
-hipError_t launch_channel_p(int N, int d, int C, int Cp, const TI* x, void* xc, hipStream_t s) {
-  const size_t items = size_t(N) * (Cp / 16) * 2 * d;
-  k_channel_layout<P, TI><<<dim3(unsigned((items + 255) / 256)), dim3(256), 0, s>>>(N, d, C, Cp, x,
-                                                                                    static_cast<uint16_t*>(xc));
-  return hipGetLastError();
-}
-
-// xd[n][p][s][h][k][i] = part p of x[n][k][16 s + 8 (i/4) + 4 h + i%4] (zero
-// from channel C): the operand blocks of a 32x32x16 MFMA contracting
-// channels in the order in which the backward's direct kernel holds
-// Gh^T in accumulator registers.  P = 2: fp16 hi and lo of x[n] 2^-e_n with
+// xd[n][p][s][h][k][i] = part p of x[n][k][c(s, h, i)] (zero from channel C):
+// the operand blocks of a 32x32x16 MFMA contracting channels, lane (h, k)
+// holding eight channels of K-step s.  c(s, h, i) = 16 s + 8 h + i (plain),
+// or with PERM 16 s + 8 (i/4) + 4 h + i%4, the order in which the backward's
+// direct kernel holds Gh^T in accumulator registers.  P = 2: fp16 hi and lo of x[n] 2^-e_n with
 // 2^e_n (the row's largest |x| to [2^13, 2^14)) in row_scale[n]; P = 1:
 // bf16.  One block per node: its [d, C] rows staged in LDS with their
 // maximum, then one thread per (s, h, k) run of eight channels.
-template <int P, typename TI>
+template <int P, typename TI, bool PERM>
 __global__ __launch_bounds__(256) void k_direct_layout(int d, int C, int Cp, const TI* __restrict__ x,
                                                        uint16_t* __restrict__ xd, float* __restrict__ row_scale) {
   extern __shared__ float tile[];  // [d][C], then four floats for the row maximum
@@ -181,7 +138,7 @@ __global__ __launch_bounds__(256) void k_direct_layout(int d, int C, int Cp, con
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int i0 = 2 * q;  // elements i0, i0 + 1 of the run
-      const int c0 = 16 * st + 8 * (i0 / 4) + 4 * h + i0 % 4;
+      const int c0 = PERM ? 16 * st + 8 * (i0 / 4) + 4 * h + i0 % 4 : 16 * st + 8 * h + i0;
       const float v0 = c0 < C ? tile[k * C + c0] : 0.f;
       const float v1 = c0 + 1 < C ? tile[k * C + c0 + 1] : 0.f;
       if constexpr (P == 2)
@@ -197,9 +154,10 @@ __global__ __launch_bounds__(256) void k_direct_layout(int d, int C, int Cp, con
 }
 
 template <int P, typename TI>
-hipError_t launch_direct_p(int N, int d, int C, int Cp, const TI* x, void* xd, float* row_scale, hipStream_t s) {
+hipError_t launch_direct_p(int N, int d, int C, int Cp, const TI* x, void* xd, float* row_scale, bool perm,
+                           hipStream_t s) {
   const size_t lds = (size_t(d) * C + 4) * 4;
-  auto k = k_direct_layout<P, TI>;
+  auto k = perm ? k_direct_layout<P, TI, true> : k_direct_layout<P, TI, false>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      int(lds));
   if (e != hipSuccess) return e;
@@ -211,30 +169,18 @@ hipError_t launch_direct_p(int N, int d, int C, int Cp, const TI* x, void* xd, f
 
 int edge_kpad(int d) { return d <= 32 ? 32 : 64; }
 
-hipError_t launch_channel_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xc,
-                                 hipStream_t s) {
-  if (N == 0) return hipSuccess;
-  if (Cp < C || Cp % 16) return hipErrorInvalidValue;
-  if (parts == 3) {
-    if (!x_is_f32) return hipErrorInvalidValue;
-    return launch_channel_p<3>(N, d, C, Cp, static_cast<const float*>(x), xc, s);
-  }
-  if (parts != 1) return hipErrorInvalidValue;
-  return x_is_f32 ? launch_channel_p<1>(N, d, C, Cp, static_cast<const float*>(x), xc, s)
-                  : launch_channel_p<1>(N, d, C, Cp, static_cast<const uint16_t*>(x), xc, s);
-}
-
 hipError_t launch_direct_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xd,
-                                float* row_scale, hipStream_t s) {
+                                float* row_scale, bool perm_channels, hipStream_t s) {
   if (N == 0) return hipSuccess;
   if (Cp < C || Cp % 16 || size_t(d) * C * 4 + 16 > 160 * 1024) return hipErrorInvalidValue;
+  const bool pm = perm_channels;
   if (parts == 2) {
     if (!x_is_f32 || !row_scale) return hipErrorInvalidValue;
-    return launch_direct_p<2>(N, d, C, Cp, static_cast<const float*>(x), xd, row_scale, s);
+    return launch_direct_p<2>(N, d, C, Cp, static_cast<const float*>(x), xd, row_scale, pm, s);
   }
   if (parts != 1) return hipErrorInvalidValue;
-  return x_is_f32 ? launch_direct_p<1>(N, d, C, Cp, static_cast<const float*>(x), xd, nullptr, s)
-                  : launch_direct_p<1>(N, d, C, Cp, static_cast<const uint16_t*>(x), xd, nullptr, s);
+  return x_is_f32 ? launch_direct_p<1>(N, d, C, Cp, static_cast<const float*>(x), xd, nullptr, pm, s)
+                  : launch_direct_p<1>(N, d, C, Cp, static_cast<const uint16_t*>(x), xd, nullptr, pm, s);
 }
 
 hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,

@@ -74,22 +74,15 @@ EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E);
 int edge_kpad(int d);
 hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,
                                  float* row_scale, hipStream_t s);
-// Features in bf16 parts blocked for contractions over channels (parts = 3:
-// the exact split x = hi + mid + lo of fp32 features, parts = 1: bf16):
-// xc [N, parts, Cp / 16, 2, d, 8] bfloat16, element [n][p][s][h][k][i] = part
-// p of x[n][k][16 s + 8 h + i] (zero from channel C; Cp >= C a multiple of
-// 16): per node, part and K-step of 16 channels one 32x32x16 MFMA operand
-// block of rows k < d.
-hipError_t launch_channel_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xc,
-                                 hipStream_t s);
-// Features for the backward's direct destination kernel (d > 32): xd
-// [N, parts, Cp / 16, 2, d, 8] of 16-bit values, element [n][p][s][h][k][i] =
-// part p of x[n][k][16 s + 8 (i / 4) + 4 h + i % 4] (zero from channel C, Cp a
-// multiple of 16): the contraction over channels in the order of the
-// kernel's accumulator registers.  parts = 2: fp16 hi and lo of x[n] 2^-e_n
-// and row_scale[n] = 2^e_n as for the edge pass; parts = 1: bf16.
+// Features for the backward's destination kernels, blocked for contractions
+// over channels: xd [N, parts, Cp / 16, 2, d, 8] of 16-bit values, element
+// [n][p][s][h][k][i] = part p of x[n][k][c(s, h, i)] with c = 16 s + 8 h + i,
+// or with perm_channels c = 16 s + 8 (i / 4) + 4 h + i % 4 (the direct
+// kernel's accumulator order); zero from channel C, Cp a multiple of 16.
+// parts = 2: fp16 hi and lo of x[n] 2^-e_n and row_scale[n] = 2^e_n as for
+// the edge pass; parts = 1: bf16.
 hipError_t launch_direct_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xd,
-                                float* row_scale, hipStream_t s);
+                                float* row_scale, bool perm_channels, hipStream_t s);
 // parts = 2: fp32 features (fp16 two-part split), parts = 1: bf16 features
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
 
@@ -121,9 +114,9 @@ struct BwdDstArgs {
   const void* x;            // [N, d, C]
   const float* Gz;          // [N, d, C] = grad_out W^T
   float* grad_vec;          // [E, 3] by edge id
-  const void* xc;           // x blocked by launch_channel_layout (Cp = bwd_dst_cpad(C, bf16)), or for
-                            // the direct kernel (d > 32) by launch_direct_layout (Cp = 32 ceil(C / 32))
-  const float* x_scale;     // direct kernel, fp32 problems: row_scale of launch_direct_layout
+  const void* xc;           // x blocked by launch_direct_layout: plain order, Cp = bwd_dst_cpad(C, bf16)
+                            // (d <= 32); accumulator order, Cp = bwd_direct_cpad(C) (d > 32)
+  const float* x_scale;     // fp32 problems: row_scale of launch_direct_layout
   int n_range;              // equal edge ranges (bwd_dst_plan)
   int pieces_per_block;     // ranges per workgroup
 };
