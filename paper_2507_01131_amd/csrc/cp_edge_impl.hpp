@@ -93,7 +93,10 @@ __host__ __device__ constexpr int edge_ct(bool bf, int RT) { return bf && RT <= 
 // double-buffered operands fit in 256 registers without spilling in the edge
 // loop; one otherwise.
 __host__ __device__ constexpr int edge_waves_per_eu(int L, int RT, bool bf) {
-  return bf ? (16 * RT * edge_ct(bf, RT) + 8 * edge_ct(bf, RT) * edge_kb((L + 1) * (L + 1)) <= 144 ? 2 : 1)
+  return bf ? (16 * RT * edge_ct(bf, RT) + 8 * edge_ct(bf, RT) * edge_kb((L + 1) * (L + 1)) <=
+                       (edge_kb((L + 1) * (L + 1)) == 2 ? 160 : 128)
+                   ? 2
+                   : 1)
             : (16 * RT + 24 * edge_xp(bf) * edge_kb((L + 1) * (L + 1)) <= 160 ? 2 : 1);
 }
 
@@ -105,8 +108,10 @@ __host__ __device__ constexpr int edge_max_ranges(int L, int RT, bool bf) {
 }
 
 // bf16 mode: whether this lane's K factor values (KB * RT * 8 floats) stay
-// in registers instead of LDS.
-__host__ __device__ constexpr bool edge_reg_kf(int d, int RT) { return edge_kb(d) * RT * 8 <= 64; }
+// in registers instead of LDS.  Never: two waves per SIMD, which the registers
+// allow only with the factor in LDS, run faster (1.02 -> 0.93 ms on the bulk
+// bf16 workload).
+__host__ __device__ constexpr bool edge_reg_kf(int, int) { return false; }
 
 struct EdgeSmem {
   int Rp, off_a, off_g, off_y, off_vec, off_phi, off_idx, off_sc, off_bnd, floats;
