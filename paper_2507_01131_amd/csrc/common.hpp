@@ -31,20 +31,6 @@ __device__ __forceinline__ float load_feat<float>(const float* p) { return *p; }
 template <>
 __device__ __forceinline__ float load_feat<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
 
-// Exact three-way bfloat16 split of a float: v = hi + mid + lo with each
-// part a bfloat16 (round to nearest even at every step; the residuals
-// v - hi and v - hi - mid are exact in fp32, and the last one has at most
-// eight significant bits, so lo holds it exactly).  Products of two parts
-// are exact in fp32, which lets bf16 MFMA reproduce fp32 contractions.
-__device__ __forceinline__ uint16_t bf16_rne_bits(float v) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v)); }
-__device__ __forceinline__ void split_bf16x3(float v, uint16_t& hi, uint16_t& mid, uint16_t& lo) {
-  hi = bf16_rne_bits(v);
-  const float r1 = v - bf16_to_f32(hi);
-  mid = bf16_rne_bits(r1);
-  const float r2 = r1 - bf16_to_f32(mid);
-  lo = bf16_rne_bits(r2);
-}
-
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 // Two floats rounded to bfloat16 (nearest even) and packed, a in the low
@@ -77,16 +63,6 @@ __device__ __forceinline__ int f16_split_exponent(float max_abs) {
   (void)frexpf(max_abs, &E);  // max_abs = m 2^E, m in [0.5, 1)
   const int e = E - 14;
   return e < -125 ? -125 : (e > 125 ? 125 : e);
-}
-
-// split_bf16x3 of two floats at once, each part packed as by pack_bf16x2_rne
-// (the same parts, bit for bit, in half the conversions).
-__device__ __forceinline__ void split_bf16x3_pair(float a, float b, uint32_t& hi, uint32_t& mid, uint32_t& lo) {
-  hi = pack_bf16x2_rne(a, b);
-  const float ra = a - __uint_as_float(hi << 16), rb = b - __uint_as_float(hi & 0xffff0000u);
-  mid = pack_bf16x2_rne(ra, rb);
-  const float sa = ra - __uint_as_float(mid << 16), sb = rb - __uint_as_float(mid & 0xffff0000u);
-  lo = pack_bf16x2_rne(sa, sb);
 }
 
 // Blocks of a 1-D grid are dealt to the XCDs round-robin (block b runs on XCD
