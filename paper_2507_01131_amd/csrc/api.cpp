@@ -79,9 +79,9 @@ size_t xt_xc_bytes(const tdn_problem& p) {
   return std::max(xt_bytes(p), std::max(xc, xd));
 }
 
-// partial slots of the fp32 edge pass (two [d, C] rows per edge range) and
-// its zero-padded output factor [d, RT*32]
-size_t ef_pad_bytes(const tdn_problem& p) { return al(size_t(dim_of(p.L)) * ((p.R + 31) / 32 * 32) * 4); }
+// the output factor's epilogue operand blocks and scale, then the partial
+// slots of the edge pass (two [d, C] rows per edge range)
+size_t ef_pad_bytes(const tdn_problem& p) { return al(tdn::edge_ef_bytes(dim_of(p.L), p.R)); }
 size_t partial_bytes(const tdn_problem& p) {
   const tdn::EdgePlan pl = tdn::edge_plan(p.L, p.R, p.C, p.n_radial, p.feat_dtype == TDN_BF16, p.n_edges);
   return ef_pad_bytes(p) + size_t(pl.n_range) * 2 * dim_of(p.L) * p.C * 4;
@@ -229,7 +229,10 @@ tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int3
   const tdn::EdgePlan pl = tdn::edge_plan(p.L, p.R, p.C, p.n_radial, p.feat_dtype == TDN_BF16, p.n_edges);
   a.n_range = pl.n_range;
   a.pieces_per_block = pl.per_block;
-  a.ef_pad = partial;
+  a.ef_ops = partial;
+  a.ef_scale = partial ? reinterpret_cast<float*>(reinterpret_cast<char*>(partial) +
+                                                 tdn::edge_ef_bytes(dim_of(p.L), p.R) - 256)
+                       : nullptr;
   a.parts = feature_parts(p);
   a.row_scale = a.parts == 2 ? row_scales(p, const_cast<void*>(feat)) : nullptr;
   a.partial = partial ? reinterpret_cast<float*>(reinterpret_cast<char*>(partial) + ef_pad_bytes(p)) : nullptr;

@@ -65,6 +65,12 @@ __device__ __forceinline__ int f16_split_exponent(float max_abs) {
   return e < -125 ? -125 : (e > 125 ? 125 : e);
 }
 
+// A 32x32 MFMA accumulator tile as the K operand of a 32x32x16 step: K-step
+// q (0, 1) of lane half h takes the rows held in accumulator registers
+// 8q .. 8q+7, i.e. row acc_krow(q, h, i) for element i = 0..7.  The other
+// operand is laid out with the same row order.
+__host__ __device__ constexpr int acc_krow(int q, int h, int i) { return 16 * q + 8 * (i / 4) + 4 * h + (i % 4); }
+
 // Blocks of a 1-D grid are dealt to the XCDs round-robin (block b runs on XCD
 // b % 8).  Remap so that each XCD walks one contiguous range of logical work
 // items: neighbouring destination nodes share source nodes, and then share

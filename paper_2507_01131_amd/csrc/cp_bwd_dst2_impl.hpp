@@ -1,5 +1,5 @@
 // Destination-side backward (the edge-vector gradient) for d <= 32 through
-// the factored form of dg, on bf16 MFMA.
+// the factored form of dg, on 16-bit MFMA.
 //
 // With Gz = grad_out W^T and Gh_t = D^T Gz[t], the cotangent of g_e
 // (eq. approximate, Sec. 3.1) factors as
@@ -9,11 +9,13 @@
 // drho = dg * v, dY = B dv, dphi = Wrad drho and
 //   grad r_e = J_Y(r_e)^T dY + (sum_q dphi_q phi'_q(|r_e|)) r_e/|r_e|.
 //
-// Arithmetic.  fp32 problems: S_e and T_e run on v_mfma_f32_32x32x16_bf16
-// with exact three-way bf16 splits of both operands and the six part
-// products a_i b_j with i + j <= 4 (as in the forward edge pass), fp32
-// accumulation.  S_e is split again (exactly) before it feeds T_e.  bf16
-// problems: x is bf16, Gz, S_e and A are rounded to bf16, one product each.
+// Arithmetic.  fp32 problems: S_e and T_e run on v_mfma_f32_32x32x16_f16
+// with both operands scaled by powers of two (x per node, Gz per segment,
+// S_e per edge tile, A once: each largest magnitude to [2^13, 2^14)) and
+// split into two fp16 parts (to 2^-22); the three part products with
+// i + j <= 3 are summed in fp32 and dg multiplies the four scales back.
+// bf16 problems: x is bf16; Gz, S_e and A are rounded to bf16, one product
+// each on v_mfma_f32_32x32x16_bf16.
 //
 // Work decomposition.  No sum runs over edges here, so the sorted edge list
 // is cut into equal ranges anywhere, several per workgroup of eight waves
@@ -25,9 +27,9 @@
 // each wave takes whole edges: S_e (K-steps of 16 channels; the x operand
 // comes straight from global memory, laid out in MFMA operand blocks per
 // node, part and K-step, one contiguous 16-byte-per-lane load per part,
-// through a per-wave prefetch ring), T_e per rank tile (the accumulator registers of S regroup into the
-// A operand of a 32x32x16 step, so the factor A is stored with the same row
-// permutation), dg, dv and drho.  Last dY = dV B^T and dphi = dRho Wrad^T
+// through a per-wave prefetch ring), T_e per rank tile (the accumulator
+// registers of S regroup into the A operand of a 32x32x16 step, so the
+// factor A is stored with the same row permutation), dg, dv and drho.  Last dY = dV B^T and dphi = dRho Wrad^T
 // (fp32 MFMA) and the gradient per edge.
 #pragma once
 

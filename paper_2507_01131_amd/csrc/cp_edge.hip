@@ -1,8 +1,8 @@
 // Dispatch of the edge pass on the maximum degree L (each L is instantiated
 // in its own translation unit, cp_edge_l<L>.hip, to keep compile units
-// small), the choice of edge ranges, the zero padding of the output factor,
-// and the kernel that combines the partial slots of segments spanning
-// ranges.
+// small), the choice of edge ranges, the output factor's operand blocks for
+// the segment epilogue, and the kernel that combines the partial slots of
+// segments spanning ranges.
 #include "cp_edge_impl.hpp"
 
 #include <map>
@@ -36,13 +36,48 @@ __global__ __launch_bounds__(256) void k_range_fixup(int E, int n_range, int dC,
   }
 }
 
-// dst[k][r] = src[k][r] for r < R, 0 for R <= r < Rp
-__global__ __launch_bounds__(256) void k_pad_rows(int rows, int R, int Rp, const float* __restrict__ src,
-                                                  float* __restrict__ dst) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= rows * Rp) return;
-  const int k = i / Rp, r = i - k * Rp;
-  dst[i] = r < R ? src[k * R + r] : 0.f;
+// The output factor EF [d, R] in the operand blocks of the segment
+// epilogue's 32x32x16 MFMA: block (mt, rt, q), lane l holds
+// EF[mt*32 + l%32][rt*32 + acc_krow(q, l/32, i)], i = 0..7 (zero past d and
+// R), the ranks in the order the accumulators hold them.  P = 2: fp16 hi and
+// lo of EF 2^-e with 2^e (EF's largest |EF| to [2^13, 2^14)) to ef_scale;
+// P = 1: bf16.  One block.
+template <int P>
+__global__ __launch_bounds__(256) void k_ef_blocks(int d, int R, int RT, int MT, const float* __restrict__ EF,
+                                                   u32x4* __restrict__ out, float* __restrict__ ef_scale) {
+  __shared__ float red[4];
+  const int tid = threadIdx.x;
+  float sc = 1.f;
+  if constexpr (P == 2) {
+    float mx = 0.f;
+    for (int i = tid; i < d * R; i += blockDim.x) mx = fmaxf(mx, fabsf(EF[i]));
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    if ((tid & 63) == 0) red[tid >> 6] = mx;
+    __syncthreads();
+    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    const int e = f16_split_exponent(mx);
+    sc = ldexpf(1.f, -e);
+    if (tid == 0) *ef_scale = ldexpf(1.f, e);
+  }
+  for (int t = tid; t < MT * RT * 2 * kWave; t += blockDim.x) {
+    const int ln = t % kWave, blk = t / kWave;
+    const int q = blk % 2, rt = (blk / 2) % RT, mt = blk / (2 * RT);
+    const int m = mt * kTile + (ln & 31), hh = ln >> 5;
+    uint32_t w[P][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r0 = rt * kTile + acc_krow(q, hh, 2 * i), r1 = rt * kTile + acc_krow(q, hh, 2 * i + 1);
+      const float v0 = (m < d && r0 < R) ? EF[m * R + r0] : 0.f;
+      const float v1 = (m < d && r1 < R) ? EF[m * R + r1] : 0.f;
+      if constexpr (P == 2)
+        split_f16x2_pair(v0 * sc, v1 * sc, w[0][i], w[1][i]);
+      else
+        w[0][i] = pack_bf16x2_rne(v0, v1);
+    }
+#pragma unroll
+    for (int p = 0; p < P; ++p) out[t * P + p] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
+  }
 }
 
 constexpr int kMinRangeEdges = 48;
@@ -63,6 +98,11 @@ int device_cus() {
     it = cus.emplace(dev, n).first;
   }
   return it->second;
+}
+
+size_t edge_ef_bytes(int d, int R) {
+  const size_t blocks = size_t((d + kTile - 1) / kTile) * ((R + kTile - 1) / kTile) * 2 * 2 * kWave * 16;
+  return blocks + 256;
 }
 
 EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E) {
@@ -90,12 +130,16 @@ hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s) {
   if (a.parts != 1 && a.parts != 2) return hipErrorInvalidValue;
   if (a.parts == 2 && a.E > 0 && !a.row_scale) return hipErrorInvalidValue;
   if (a.E > 0 && (a.n_range < 1 || a.n_range > a.E || a.pieces_per_block < 1 || a.n_range % a.pieces_per_block ||
-                  !a.ef_pad))
+                  !a.ef_ops || !a.ef_scale))
     return hipErrorInvalidValue;
   hipError_t e = hipSuccess;
   if (a.E > 0) {
-    const int Rp = (a.R + kTile - 1) / kTile * kTile;
-    k_pad_rows<<<dim3((a.d * Rp + 255) / 256), dim3(256), 0, s>>>(a.d, a.R, Rp, a.EF, a.ef_pad);
+    const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
+    u32x4* blocks = static_cast<u32x4*>(a.ef_ops);
+    if (a.parts == 2)
+      k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, blocks, a.ef_scale);
+    else
+      k_ef_blocks<1><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, blocks, a.ef_scale);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

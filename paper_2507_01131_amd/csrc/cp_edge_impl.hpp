@@ -235,63 +235,90 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
 #pragma unroll
     for (int t = 0; t < CT; ++t) acc[rt][t] = f32x16{};
 
-  // Segment epilogue: Z[m][c] = sum_r EF[m][r] H[r][c] on fp32 MFMA.  The
-  // contraction over r pairs accumulator register v of the two half-waves:
-  // lanes 0-31 contribute rank rt*32 + acc_row(v,0), lanes 32-63 rank rt*32 +
-  // acc_row(v,1), which is exactly the B-operand layout, so H never leaves
-  // the registers.  The A operand (EF, read from global memory, where it
-  // stays cached) comes in groups of 16 values, one group per (row tile mt,
-  // rank tile rt), the next group loaded while the current one's MFMAs run.
-  // part < 0 writes the segment's output row, part 0 or 1 the range's
-  // partial slot; the accumulators restart from zero.
+  // Segment epilogue: Z[m][c] = sum_r EF[m][r] H[r][c] on 32x32x16 MFMA.  The
+  // accumulators are the K operand as they stand (K-step (rt, q) of lane half
+  // h contracts the ranks rt*32 + acc_krow(q, h, i) that its registers
+  // 8q .. 8q+7 hold), and EF comes in operand blocks with the same rank order
+  // (k_ef_blocks, read from global memory, where they stay cached).  fp32
+  // problems: the wave's H scaled by a power of two into [2^13, 2^14) and
+  // split into two fp16 parts, three part products, the scales of H and EF
+  // multiplied back into Z; bf16 problems: H and EF rounded to bf16, one
+  // product.  part < 0 writes the segment's output row, part 0 or 1 the
+  // range's partial slot; the accumulators restart from zero.
+  const u32x4* __restrict__ efb = static_cast<const u32x4*>(a.ef_ops);
+  const float ef_unscale = BF ? 1.f : *a.ef_scale;
   int range = 0;
   auto finish = [&](int seg, int part) {
     float* dst = part < 0 ? a.out + size_t(seg) * d * C : a.partial + (size_t(range) * 2 + part) * d * C;
-    constexpr int NG = MT * RT;
-    // EF zero-padded to [d][Rp] (ef_pad): a lane's 16 values of a group sit
-    // at fixed offsets from one row pointer
-    int ef_off = 0;
-    asm volatile("" : "+s"(ef_off));
-    const float* ef = a.ef_pad + ef_off;
-    auto ef_load = [&](int g, float (&ev)[16]) {
-      const int mt = g / RT, rt = g - mt * RT;
-      const int row = mt * kTile + l32;
-      const float* er = ef + (row < d ? row : d - 1) * Rp + rt * kTile + 4 * h;
+    constexpr int P16 = BF ? 1 : 2;
+    float hsc = 1.f, zsc = 1.f;
+    if constexpr (!BF) {
+      float mx = 0.f;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) ev[v] = er[8 * (v >> 2) + (v & 3)];
-    };
-    f32x16 z[CT];
-    auto ef_mfma = [&](int g, const float (&ev)[16]) {
-      const int mt = g / RT, rt = g - mt * RT;
-      const int row = mt * kTile + l32;
+      for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int t = 0; t < CT; ++t) {
-        if (rt == 0) z[t] = f32x16{};
+        for (int t = 0; t < CT; ++t)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) z[t] = mfma32(row < d ? ev[v] : 0.f, acc[rt][t][v], z[t]);
-        const int c = c0 + t * kTile;
-        if (rt == RT - 1 && c < C) {
+          for (int v = 0; v < 16; ++v) mx = fmaxf(mx, fabsf(acc[rt][t][v]));
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      const int e = f16_split_exponent(mx);
+      hsc = ldexpf(1.f, -e);
+      zsc = ldexpf(ef_unscale, e);
+    }
+    f32x16 z[CT][MT];
+#pragma unroll
+    for (int t = 0; t < CT; ++t)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) z[t][mt] = f32x16{};
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        u32x4 hp[CT][P16];
+#pragma unroll
+        for (int t = 0; t < CT; ++t) {
+          uint32_t w[P16][4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float v0 = acc[rt][t][8 * q + 2 * i] * hsc, v1 = acc[rt][t][8 * q + 2 * i + 1] * hsc;
+            if constexpr (BF)
+              w[0][i] = pack_bf16x2_rne(v0, v1);
+            else
+              split_f16x2_pair(v0, v1, w[0][i], w[1][i]);
+          }
+#pragma unroll
+          for (int p = 0; p < P16; ++p) hp[t][p] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          u32x4 ea[P16];
+#pragma unroll
+          for (int p = 0; p < P16; ++p) ea[p] = efb[((((mt * RT + rt) * 2 + q) * kWave) + lane) * P16 + p];
+#pragma unroll
+          for (int t = 0; t < CT; ++t) {
+            if constexpr (BF) {
+              z[t][mt] = mfma_bf16(ea[0], hp[t][0], z[t][mt]);
+            } else {
+              z[t][mt] = mfma_f16(ea[1], hp[t][0], z[t][mt]);
+              z[t][mt] = mfma_f16(ea[0], hp[t][1], z[t][mt]);
+              z[t][mt] = mfma_f16(ea[0], hp[t][0], z[t][mt]);
+            }
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);  // one (rt, q) step's operands live at a time
+      }
+#pragma unroll
+    for (int t = 0; t < CT; ++t) {
+      const int c = c0 + t * kTile;
+      if (c < C) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int m = mt * kTile + acc_row(v, h);
-            if (m < d) dst[size_t(m) * C + c] = z[t][v];
+            if (m < d) dst[size_t(m) * C + c] = z[t][mt][v] * zsc;
           }
-        }
-      }
-    };
-    float ev0[16], ev1[16];
-    ef_load(0, ev0);
-#pragma unroll
-    for (int g = 0; g < NG; g += 2) {
-      if (g + 1 < NG) ef_load(g + 1, ev1);
-      __builtin_amdgcn_sched_barrier(0);
-      ef_mfma(g, ev0);
-      __builtin_amdgcn_sched_barrier(0);
-      if (g + 1 < NG) {
-        if (g + 2 < NG) ef_load(g + 2, ev0);
-        __builtin_amdgcn_sched_barrier(0);
-        ef_mfma(g + 1, ev1);
-        __builtin_amdgcn_sched_barrier(0);
       }
     }
 #pragma unroll

@@ -51,7 +51,9 @@ struct EdgeArgs {
   int n_range;               // edge ranges (EdgePlan::n_range)
   int pieces_per_block;      // ranges per workgroup (EdgePlan::per_block)
   float* partial;            // [n_range, 2, d, C] workspace
-  float* ef_pad;             // [d, RT*32] workspace: EF zero-padded (written by launch_cp_edge)
+  void* ef_ops;              // workspace of edge_ef_bytes(d, R): EF in the epilogue's operand blocks
+                             // and its scale (written by launch_cp_edge)
+  float* ef_scale;           // inside ef_ops: 2^e of EF's fp16 parts (parts = 2)
   int parts;                 // 16-bit parts per feature in feat (2: fp32 features as fp16 hi + lo, 1: bf16)
   const float* row_scale;    // [n_feat_rows] 2^e of each feat row (parts = 2), from launch_feature_layout
 };
@@ -85,6 +87,10 @@ hipError_t launch_direct_layout(int N, int d, int C, int Cp, const void* x, bool
                                 float* row_scale, bool perm_channels, hipStream_t s);
 // parts = 2: fp32 features (fp16 two-part split), parts = 1: bf16 features
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
+// Workspace bytes of EdgeArgs::ef_ops: the output factor in 32x32x16 operand
+// blocks [ceil(d/32)][ceil(R/32)][2][parts][64 lanes] x 16 bytes (parts <= 2)
+// and, after them, its scale.
+size_t edge_ef_bytes(int d, int R);
 
 // ---------------------------------------------------------------- node GEMMs
 // out[rows, C] = in[rows, C] @ W (transpose_w = 0) or in @ W^T (transpose_w = 1);
