@@ -88,7 +88,7 @@ size_t partial_bytes(const tdn_problem& p) {
 }
 
 struct FwdLayout {
-  size_t z, xt, part, sort, flags, total;
+  size_t z, xt, part, sort, wp, flags, total;
 };
 FwdLayout fwd_layout(const tdn_problem& p) {
   FwdLayout f{};
@@ -102,6 +102,8 @@ FwdLayout fwd_layout(const tdn_problem& p) {
   o += al(partial_bytes(p));
   f.sort = o;
   o += al(p.edges_sorted ? 0 : tdn::sort_plan(p.n_nodes, p.n_edges).bytes);
+  f.wp = o;
+  o += al(tdn::node_gemm_ws_bytes(p.C));
   f.flags = o;
   o += 256;
   f.total = o;
@@ -109,7 +111,7 @@ FwdLayout fwd_layout(const tdn_problem& p) {
 }
 
 struct BwdLayout {
-  size_t gz, z, xt, part, parts, perm_src, off_src, sort, flags, total;
+  size_t gz, z, xt, part, parts, perm_src, off_src, sort, wp, flags, total;
 };
 BwdLayout bwd_layout(const tdn_problem& p) {
   BwdLayout b{};
@@ -131,6 +133,8 @@ BwdLayout bwd_layout(const tdn_problem& p) {
   o += al(size_t(p.n_nodes + 1) * 4);
   b.sort = o;
   o += al(tdn::sort_plan(p.n_nodes, p.n_edges).bytes);
+  b.wp = o;
+  o += al(tdn::node_gemm_ws_bytes(p.C));
   b.flags = o;
   o += 256;
   b.total = o;
@@ -320,7 +324,7 @@ tdn_status tdn_cp_tp_forward(const tdn_problem* p, const void* x, const float* e
                             reinterpret_cast<float*>(ws + lay.part), Z, stream));
   {
     Timed t("node_gemm", stream);
-    TDN_HIP(tdn::launch_node_gemm(N * d, C, Z, W, bf16, 0, out, stream));
+    TDN_HIP(tdn::launch_node_gemm(N * d, C, Z, W, bf16, 0, out, ws + lay.wp, stream));
   }
   return TDN_OK;
 }
@@ -355,7 +359,7 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
   float* Gz = reinterpret_cast<float*>(ws + lay.gz);
   {
     Timed t("node_gemm", stream);
-    TDN_HIP(tdn::launch_node_gemm(N * d, C, grad_out, W, bf16, 1, Gz, stream));
+    TDN_HIP(tdn::launch_node_gemm(N * d, C, grad_out, W, bf16, 1, Gz, ws + lay.wp, stream));
   }
   if (grad_W) {
     const float* Z = z_save;

@@ -93,10 +93,14 @@ hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
 size_t edge_ef_bytes(int d, int R);
 
 // ---------------------------------------------------------------- node GEMMs
-// out[rows, C] = in[rows, C] @ W (transpose_w = 0) or in @ W^T (transpose_w = 1);
-// with w_bf16 the fp32 operand is rounded to bf16 for bf16 MFMA
+// out[rows, C] = in[rows, C] @ W (transpose_w = 0) or in @ W^T (transpose_w = 1).
+// fp32 W: fp16 MFMA over power-of-two scaled two-part splits of W and of each
+// row of `in` (fp32-level accuracy), W's parts in ws (node_gemm_ws_bytes(C)
+// bytes); w_bf16: bf16 MFMA with `in` rounded to bf16 (ws unused).  C is a
+// multiple of 16.
+size_t node_gemm_ws_bytes(int C);
 hipError_t launch_node_gemm(int rows, int C, const float* in, const void* W, bool w_bf16, int transpose_w,
-                            float* out, hipStream_t s);
+                            float* out, void* ws, hipStream_t s);
 // grad_W[C, C] = sum_rows Z[row, :]^T G[row, :], split over gram_parts(rows)
 // row chunks reduced in a fixed order.  partial: [n_part, C, C] floats of
 // workspace.  bf16 = 1 rounds Z and G to bf16 for the MFMA (bf16 problems).

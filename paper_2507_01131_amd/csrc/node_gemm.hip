@@ -7,11 +7,13 @@
 // grad_W = sum_rows Z^T grad_out, split over fixed row chunks whose partial
 // C x C products are summed in a fixed order (deterministic, no atomics).
 //
-// All three share one LDS-staged MFMA micro-kernel: a 128 x 128 output tile
+// All of them stage operands through LDS for MFMA: a 128 x 128 output tile
 // per workgroup, four waves of 64 x 64 (2 x 2 MFMA tiles, so every operand
-// read from LDS feeds two MFMAs), contraction staged in chunks of 32.  fp32
-// problems use 32x32x2 fp32 MFMA; bf16 problems (bf16 W) use 32x32x16 bf16
-// MFMA with the fp32 operand rounded to bf16 while it is staged.
+// read from LDS feeds two MFMAs), contraction staged in chunks of 32.  The
+// fp32 node GEMMs run on 32x32x16 fp16 MFMA over scaled two-part splits
+// (k_node_gemm_f16); the Gram products of fp32 problems use 32x32x2 fp32
+// MFMA; bf16 problems (bf16 W) use 32x32x16 bf16 MFMA with the fp32 operand
+// rounded to bf16 while it is staged.
 #include "common.hpp"
 #include "kernels.h"
 
@@ -198,6 +200,171 @@ __device__ inline void store_tile(const f32x16 (&acc)[2][2], float* __restrict__
     }
 }
 
+// ---- fp32 problems: the node GEMM on fp16 MFMA over two-part splits.
+// W (or W^T) is split once per call into wp[p][n][k] (fp16 parts of
+// W 2^-e_W, contraction fastest; 2^e_W after them); every row of `in` is
+// scaled by the power of two that puts its largest |value| in [2^13, 2^14)
+// and split while it is staged; out = (sum of the three part products with
+// i + j <= 3) x 2^(e_row + e_W).
+__global__ __launch_bounds__(1024) void k_w_parts(int C, int transpose_w, const float* __restrict__ W,
+                                                  uint16_t* __restrict__ wp) {
+  __shared__ float red[16];
+  const int tid = threadIdx.x;
+  // every block finds W's largest magnitude itself (C*C <= 65536 floats,
+  // float4 loads, independent iterations), then splits its slice of pairs
+  float mx = 0.f;
+  const int n4 = C * C / 4;
+#pragma unroll 4
+  for (int i = tid; i < n4; i += blockDim.x) {
+    const f32x4 v = reinterpret_cast<const f32x4*>(W)[i];
+    mx = fmaxf(mx, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  if ((tid & 63) == 0) red[tid >> 6] = mx;
+  __syncthreads();
+  for (int w = 0; w < int(blockDim.x >> 6); ++w) mx = fmaxf(mx, red[w]);
+  const int e = f16_split_exponent(mx);
+  const float sc = ldexpf(1.f, -e);
+  // pair i: element (n, k), (n, k + 1) of the B operand: W[k][n] (out = in W)
+  // or W[n][k] (in W^T)
+  const int i = blockIdx.x * blockDim.x + tid;
+  if (i < C * C / 2) {
+    const int n = (2 * i) / C, k = (2 * i) % C;
+    const float v0 = transpose_w ? W[n * C + k] : W[k * C + n];
+    const float v1 = transpose_w ? W[n * C + k + 1] : W[(k + 1) * C + n];
+    uint32_t hi, lo;
+    split_f16x2_pair(v0 * sc, v1 * sc, hi, lo);
+    reinterpret_cast<uint32_t*>(wp)[i] = hi;
+    reinterpret_cast<uint32_t*>(wp)[C * C / 2 + i] = lo;
+  }
+  if (blockIdx.x == 0 && tid == 0) *reinterpret_cast<float*>(wp + 2 * C * C) = ldexpf(1.f, e);
+}
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ f32x16 mfma32_f16(u32x4 a, u32x4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0,
+                                                0);
+}
+
+// out[rows, C] = in[rows, C] B with B given as the parts wp (k_w_parts), for
+// C <= 32 NCH.  128 x 128 output tile per workgroup, four waves of 64 x 64.
+// The block loads all NCH 32-wide chunks of its rows at once (coalesced,
+// straight into registers), so each row's largest magnitude needs one
+// memory latency; then per 32-deep chunk both operands are staged in LDS as
+// fp16 parts (the row parts split on the way, W's next chunk loaded one
+// chunk ahead) and every 16-deep step runs the three part products.
+template <int NCH>
+__global__ __launch_bounds__(256) void k_node_gemm_f16(int rows, int C, const float* __restrict__ in,
+                                                       const uint16_t* __restrict__ wp, float* __restrict__ out) {
+  __shared__ __align__(16) uint16_t sa[2][kBM * kSH];
+  __shared__ __align__(16) uint16_t sb[2][kBN * kSH];
+  __shared__ float s_unscale[kBM];
+  const int m0 = blockIdx.x * kBM, n0 = blockIdx.y * kBN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = lane >> 5, l32 = lane & 31;
+  const int wr = wave >> 1, wc = wave & 1;
+  // row chunk loads, coalesced: per 32-wide chunk the block's 128 x 32
+  // floats are 1024 float4, thread t taking float4 f = t + 256 j (j = 0..3):
+  // row (t >> 3) + 32 j, columns 4 (t & 7) .. +3; eight consecutive lanes
+  // cover one row's 128 bytes
+  const int c4 = tid & 7;
+  f32x4 va[NCH][4];
+#pragma unroll
+  for (int it = 0; it < NCH; ++it)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = (tid >> 3) + 32 * j, k = it * kBK + 4 * c4;
+      va[it][j] = (m0 + r < rows && k < C) ? *reinterpret_cast<const f32x4*>(in + size_t(m0 + r) * C + k) : f32x4{};
+    }
+  float rsc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float mx = 0.f;
+#pragma unroll
+    for (int it = 0; it < NCH; ++it)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mx = fmaxf(mx, fabsf(va[it][j][i]));
+    mx = fmaxf(mx, __shfl_xor(mx, 1));
+    mx = fmaxf(mx, __shfl_xor(mx, 2));
+    mx = fmaxf(mx, __shfl_xor(mx, 4));
+    const int er = f16_split_exponent(mx);
+    rsc[j] = ldexpf(1.f, -er);
+    if (c4 == 0) s_unscale[(tid >> 3) + 32 * j] = ldexpf(1.f, er);
+  }
+  const float w_unscale = *reinterpret_cast<const float*>(wp + 2 * C * C);
+  // B runs: n = n0 + tid / 2, k = k0 + (tid % 2) * 16 .. +15, both parts
+  const int b_r = tid / 2, b_c = (tid % 2) * 16;
+  const int gn = n0 + b_r;
+  f32x16 acc[2][2] = {{f32x16{}, f32x16{}}, {f32x16{}, f32x16{}}};
+  u32x4 vb[2][2][2];  // [buffer][part][half of the run]
+  auto fetch_b = [&](int k0, u32x4 (&b)[2][2]) {
+    const int kb = k0 + b_c;
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+        b[p][q] = (gn < C && kb + 8 * q < C)
+                      ? *reinterpret_cast<const u32x4*>(wp + size_t(p) * C * C + size_t(gn) * C + kb + 8 * q)
+                      : u32x4{};
+  };
+  fetch_b(0, vb[0]);
+#pragma unroll
+  for (int it = 0; it < NCH; ++it) {
+    const int k0 = it * kBK;
+    if (k0 >= C) break;
+    __syncthreads();  // the previous chunk's operands are consumed
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t hi[2], lo[2];
+      split_f16x2_pair(va[it][j][0] * rsc[j], va[it][j][1] * rsc[j], hi[0], lo[0]);
+      split_f16x2_pair(va[it][j][2] * rsc[j], va[it][j][3] * rsc[j], hi[1], lo[1]);
+      const int r = (tid >> 3) + 32 * j;
+      *reinterpret_cast<uint2*>(&sa[0][r * kSH + 4 * c4]) = make_uint2(hi[0], hi[1]);
+      *reinterpret_cast<uint2*>(&sa[1][r * kSH + 4 * c4]) = make_uint2(lo[0], lo[1]);
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int p = 0; p < 2; ++p) *reinterpret_cast<u32x4*>(&sb[p][b_r * kSH + b_c + 8 * q]) = vb[it & 1][p][q];
+    __syncthreads();
+    if (it + 1 < NCH && k0 + kBK < C) fetch_b(k0 + kBK, vb[(it + 1) & 1]);
+#pragma unroll
+    for (int s2 = 0; s2 < kBK / 16; ++s2) {
+      u32x4 av[2][2], bv[2][2];  // [part][tile]
+#pragma unroll
+      for (int p = 0; p < 2; ++p)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          av[p][i] = *reinterpret_cast<const u32x4*>(&sa[p][(wr * 64 + i * 32 + l32) * kSH + 16 * s2 + 8 * h]);
+          bv[p][i] = *reinterpret_cast<const u32x4*>(&sb[p][(wc * 64 + i * 32 + l32) * kSH + 16 * s2 + 8 * h]);
+        }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          acc[i][j] = mfma32_f16(av[1][i], bv[0][j], acc[i][j]);
+          acc[i][j] = mfma32_f16(av[0][i], bv[1][j], acc[i][j]);
+          acc[i][j] = mfma32_f16(av[0][i], bv[0][j], acc[i][j]);
+        }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = n0 + wc * 64 + j * 32 + l32;
+      if (col >= C) continue;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int rl = wr * 64 + i * 32 + acc_row(v, h);
+        if (m0 + rl < rows) out[size_t(m0 + rl) * C + col] = acc[i][j][v] * (s_unscale[rl] * w_unscale);
+      }
+    }
+}
+
 // out[rows, C] = in[rows, C] @ W   (TW: W[k][n])   or   in @ W^T   (W[n][k])
 template <typename TW, bool BF16, bool WT>
 __global__ __launch_bounds__(256) void k_node_gemm(int rows, int C, const float* __restrict__ in,
@@ -234,23 +401,35 @@ __global__ void k_sum_parts(int n_part, int CC, const float* __restrict__ partia
 
 }  // namespace
 
+size_t node_gemm_ws_bytes(int C) { return size_t(2) * C * C * 2 + 256; }
+
 hipError_t launch_node_gemm(int rows, int C, const float* in, const void* W, bool w_bf16, int transpose_w, float* out,
-                            hipStream_t s) {
+                            void* ws, hipStream_t s) {
   if (rows == 0) return hipSuccess;
+  if (C % 16) return hipErrorInvalidValue;
   const dim3 grid((rows + kBM - 1) / kBM, (C + kBN - 1) / kBN);
-  const uint16_t* wh = static_cast<const uint16_t*>(W);
-  const float* wf = static_cast<const float*>(W);
   if (w_bf16) {
+    const uint16_t* wh = static_cast<const uint16_t*>(W);
     if (transpose_w)
       k_node_gemm<uint16_t, true, true><<<grid, dim3(256), 0, s>>>(rows, C, in, wh, out);
     else
       k_node_gemm<uint16_t, true, false><<<grid, dim3(256), 0, s>>>(rows, C, in, wh, out);
-  } else {
-    if (transpose_w)
-      k_node_gemm<float, false, true><<<grid, dim3(256), 0, s>>>(rows, C, in, wf, out);
-    else
-      k_node_gemm<float, false, false><<<grid, dim3(256), 0, s>>>(rows, C, in, wf, out);
+    return hipGetLastError();
   }
+  if (!ws) return hipErrorInvalidValue;
+  uint16_t* wp = static_cast<uint16_t*>(ws);
+  k_w_parts<<<dim3((C * C / 2 + 1023) / 1024), dim3(1024), 0, s>>>(C, transpose_w, static_cast<const float*>(W), wp);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int nch = (C + kBK - 1) / kBK;
+  if (nch <= 1)
+    k_node_gemm_f16<1><<<grid, dim3(256), 0, s>>>(rows, C, in, wp, out);
+  else if (nch <= 2)
+    k_node_gemm_f16<2><<<grid, dim3(256), 0, s>>>(rows, C, in, wp, out);
+  else if (nch <= 4)
+    k_node_gemm_f16<4><<<grid, dim3(256), 0, s>>>(rows, C, in, wp, out);
+  else
+    k_node_gemm_f16<8><<<grid, dim3(256), 0, s>>>(rows, C, in, wp, out);
   return hipGetLastError();
 }
 
