@@ -42,7 +42,7 @@ struct DstSmem {
   int Rp, off_b, off_v, off_rho, off_dg, off_y, off_phi, off_dy, off_dphi, off_j, off_idx, off_sc, floats;
 };
 
-__host__ __device__ inline DstSmem dst_smem(int RT, int MT, int d, int n_radial) {
+__host__ __device__ inline DstSmem dst_smem(int RT, int MT, int d, int n_radial, int C) {
   DstSmem s{};
   s.Rp = RT * kTile;
   int o = 0;
@@ -54,6 +54,7 @@ __host__ __device__ inline DstSmem dst_smem(int RT, int MT, int d, int n_radial)
   o += kChunk * s.Rp;
   s.off_dg = o;
   o += MT * kChunk * s.Rp;
+  if (o < s.off_v + d * C) o = s.off_v + d * C;  // the region also holds Gz[seg] while Gh^T is formed
   s.off_y = o;
   o += kChunk * d;
   s.off_phi = o;
@@ -95,7 +96,7 @@ __global__ __launch_bounds__(direct_waves(MT, RT)* kWave) void k_bwd_dst(BwdDstA
   constexpr int NS = 2 * NCT;    // K-steps of 16 channels (xd blocks per part)
   constexpr int NW = direct_waves(MT, RT);
   extern __shared__ float smem[];
-  const DstSmem S = dst_smem(RT, MT, a.d, a.n_radial);
+  const DstSmem S = dst_smem(RT, MT, a.d, a.n_radial, a.C);
   constexpr int Rp = RT * kTile;
   f32x4* sAl = reinterpret_cast<f32x4*>(smem + S.off_b);
   float* sV = smem + S.off_v;
@@ -139,8 +140,17 @@ __global__ __launch_bounds__(direct_waves(MT, RT)* kWave) void k_bwd_dst(BwdDstA
     sAl[t] = v;
   }
 
+  // Gz[seg] staged in LDS ([d][C], coalesced float4 loads) in the v/rho/dg
+  // region, which the chunk loop uses only after its first barrier
+  float* sGzf = sV;
+  {
+    const f32x4* g4 = reinterpret_cast<const f32x4*>(a.Gz + size_t(seg) * d * C);
+    for (int i = tid; i < d * C / 4; i += blockDim.x) reinterpret_cast<f32x4*>(sGzf)[i] = g4[i];
+  }
+  __syncthreads();
   // Gh^T tiles of the wave's two rank tiles, each scaled by its own power of
-  // two (fp32 problems) and split: ghp[t][ct][q][p]
+  // two (fp32 problems) and split: ghp[t][ct][q][p].  One D value per lane
+  // and step feeds all channel tiles.
   u32x4 ghp[2][NCT][2][P];
   float gh_unscale[2] = {1.f, 1.f};
 #pragma unroll
@@ -148,13 +158,15 @@ __global__ __launch_bounds__(direct_waves(MT, RT)* kWave) void k_bwd_dst(BwdDstA
     const int r = rtw[t] * kTile + l32;
     f32x16 gh[NCT];
 #pragma unroll
-    for (int ct = 0; ct < NCT; ++ct) {
-      gh[ct] = f32x16{};
-      const int cc = ct * kTile + l32;
-      for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
-        const int k = 2 * s2 + h;
-        const float av = (k < d && cc < C) ? a.Gz[(size_t(seg) * d + k) * C + cc] : 0.f;
-        const float bv = (k < d && r < R) ? a.D[k * R + r] : 0.f;
+    for (int ct = 0; ct < NCT; ++ct) gh[ct] = f32x16{};
+#pragma unroll 5
+    for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
+      const int k = 2 * s2 + h;
+      const float bv = (k < d && r < R) ? a.D[k * R + r] : 0.f;
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) {
+        const int cc = ct * kTile + l32;
+        const float av = (k < d && cc < C) ? sGzf[k * C + cc] : 0.f;
         gh[ct] = mfma32(av, bv, gh[ct]);
       }
     }
@@ -405,7 +417,8 @@ __global__ __launch_bounds__(direct_waves(MT, RT)* kWave) void k_bwd_dst(BwdDstA
 
 template <int MT, int RT, int NCT, bool BF>
 hipError_t launch_k(const BwdDstArgs& a, hipStream_t s) {
-  const size_t lds = size_t(dst_smem(RT, MT, a.d, a.n_radial).floats) * 4;
+  const size_t lds = size_t(dst_smem(RT, MT, a.d, a.n_radial, a.C).floats) * 4;
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
   auto k = k_bwd_dst<MT, RT, NCT, BF>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      int(lds));
