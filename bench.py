@@ -106,6 +106,8 @@ def main():
     ap.add_argument("--workload", default="molecules3200_L4_C128_R128")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--backward", action="store_true", help="also time tdn_cp_tp_backward (extra field)")
+    ap.add_argument("--ablation-atomics", action="store_true",
+                    help="also time the atomic scatter-add forward (extra field; fp32 workloads with 2 <= L <= 4)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 256 MiB device copy (reference for rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -214,6 +216,31 @@ def main():
             "mfma": "v_mfma_f32_32x32x16_f16, three products of two-part fp16 splits per fp32 product",
             "flops_per_launch": executed, "achieved": executed / (edge_ms * 1e-3) / 1e12,
             "peak": PEAK_FP16_MFMA_TFLOPS, "frac": executed / (edge_ms * 1e-3) / 1e12 / PEAK_FP16_MFMA_TFLOPS}
+    if args.ablation_atomics:
+        # the same forward with the segmented sum replaced by per-edge
+        # application of D and float atomics into Z
+        def step_atomic():
+            return tdn.forward(x, vec, ei, At, Bt, Dt, W, rw, L=w["L"], r_cut=w["r_cut"],
+                               edges_sorted=w["presorted"], workspace=ws, out=out, z=zsave, perm=perm,
+                               offsets=offsets, atomics_ablation=True)
+
+        for _ in range(3):
+            step_atomic()
+        torch.cuda.synchronize()
+        tdn.timer_enable(True)
+        tdn.timer_read("cp_edge_fwd_atomic", reset=True)
+        ev0.record()
+        for _ in range(args.steps):
+            step_atomic()
+        ev1.record()
+        torch.cuda.synchronize()
+        tdn.timer_enable(False)
+        a_ms, a_n = tdn.timer_read("cp_edge_fwd_atomic", reset=True)
+        a_step = ev0.elapsed_time(ev1) / args.steps
+        line["ablation_atomics"] = {
+            "edge_kernel_ms": a_ms / max(1, a_n), "segmented_edge_kernel_ms": edge_ms,
+            "edge_kernel_slowdown": a_ms / max(1, a_n) / edge_ms,
+            "ms_per_step": a_step, "value": E / (a_step * 1e-3)}
     if args.backward:
         G = torch.from_numpy(w["grad_out"]).to(dev)
         wsb = torch.empty(bwd_bytes, dtype=torch.uint8, device=dev)

@@ -111,6 +111,21 @@ tdn_status tdn_cp_tp_forward(const tdn_problem* p, const void* x, const float* e
                              float* z_save, int32_t* perm, int32_t* offsets, void* workspace,
                              size_t workspace_bytes, hipStream_t stream);
 
+/* Measurement ablation of the forward's segmented sum (Sec. 3.1: the layer
+ * sums the per-edge messages into each destination node).  Same arguments,
+ * workspace and results as tdn_cp_tp_forward, within floating-point
+ * reordering: the edge pass applies D to every edge's message on its own and
+ * adds the d x C result into z_save (or the workspace's Z) with float atomics,
+ * instead of summing each node's edges before one application of D and one
+ * plain store.  The order of the additions is not fixed, so results may
+ * differ between calls in the last bits.  Only fp32 features and 2 <= L <= 4
+ * (TDN_ERR_BAD_DTYPE / TDN_ERR_BAD_SHAPE otherwise). */
+tdn_status tdn_ablation_forward_atomics(const tdn_problem* p, const void* x, const float* edge_vec,
+                                        const int32_t* edge_index, const float* A, const float* B,
+                                        const float* D, const void* W, const float* radial_w,
+                                        float* out, float* z_save, int32_t* perm, int32_t* offsets,
+                                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Backward pass for the scalar <grad_out, out>.  perm and offsets are the
  * forward's outputs; z_save is the forward's saved Z or NULL (then Z is
  * recomputed).  Each gradient pointer may be NULL to skip it; grads are f32
@@ -147,7 +162,7 @@ tdn_status tdn_spherical_harmonics(int32_t L, int32_t E, const float* edge_vec, 
  * tdn_timer_enable(1) starts recording every launch of the layer's edge
  * kernels; tdn_timer_read synchronises on the recorded events and returns
  * the summed milliseconds and launch count of the kernel named `kernel`
- * ("cp_edge_fwd", "feature_layout", "channel_layout", "cp_edge_bwd_src", "cp_bwd_dst", "node_gemm", "gram",
+ * ("cp_edge_fwd", "cp_edge_fwd_atomic", "feature_layout", "channel_layout", "cp_edge_bwd_src", "cp_bwd_dst", "node_gemm", "gram",
  * "sort");
  * reset = 1 clears that kernel's record. */
 tdn_status tdn_timer_enable(int32_t enable);

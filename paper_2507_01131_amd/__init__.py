@@ -60,6 +60,7 @@ def lib() -> ctypes.CDLL:
         PP = ctypes.POINTER(Problem)
         L.tdn_workspace_size.argtypes = [PP, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)]
         L.tdn_cp_tp_forward.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
+        L.tdn_ablation_forward_atomics.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
         L.tdn_cp_tp_backward.argtypes = [PP] + [_P] * 16 + [_SZ, _P]
         L.tdn_sort_workspace_size.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_SZ)]
         L.tdn_sort_by_key.argtypes = [ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P, _SZ, _P]
@@ -70,8 +71,9 @@ def lib() -> ctypes.CDLL:
         L.tdn_status_string.argtypes = [ctypes.c_int]
         L.tdn_status_string.restype = ctypes.c_char_p
         L.tdn_last_hip_error.restype = ctypes.c_int32
-        for f in ("tdn_workspace_size", "tdn_cp_tp_forward", "tdn_cp_tp_backward", "tdn_sort_workspace_size",
-                  "tdn_sort_by_key", "tdn_spherical_harmonics", "tdn_timer_enable", "tdn_timer_read"):
+        for f in ("tdn_workspace_size", "tdn_cp_tp_forward", "tdn_ablation_forward_atomics", "tdn_cp_tp_backward",
+                  "tdn_sort_workspace_size", "tdn_sort_by_key", "tdn_spherical_harmonics", "tdn_timer_enable",
+                  "tdn_timer_read"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -133,11 +135,13 @@ class ForwardResult:
 
 def forward(x, edge_vec, edge_index, A, B, D, W, radial_w, *, L: int, r_cut: float, edges_sorted=False,
             validate=False, save_z=True, workspace=None, out=None, z=None, perm=None, offsets=None,
-            stream=None) -> ForwardResult:
+            stream=None, atomics_ablation=False) -> ForwardResult:
     """Runs tdn_cp_tp_forward.  x [N,d,C] and W [C,C] are float32 or bfloat16
     (both the same); edge_index [2,E] int32 (int64 is converted); everything
     else float32 on the same device.  out, z, perm, offsets and workspace may
-    be passed preallocated; otherwise they are allocated here."""
+    be passed preallocated; otherwise they are allocated here.
+    atomics_ablation=True runs tdn_ablation_forward_atomics instead (the
+    per-edge atomic scatter-add the segmented sum replaces; fp32, 2 <= L <= 4)."""
     dev = x.device
     N, d, C = x.shape
     E = edge_vec.shape[0]
@@ -170,10 +174,11 @@ def forward(x, edge_vec, edge_index, A, B, D, W, radial_w, *, L: int, r_cut: flo
         _need(z, "z", torch.float32, (N, d, C), dev)
     _need(perm, "perm", torch.int32, (E,), dev)
     _need(offsets, "offsets", torch.int32, (N + 1,), dev)
-    st = lib().tdn_cp_tp_forward(ctypes.byref(p), _ptr(x), _ptr(edge_vec), _ptr(edge_index), _ptr(A), _ptr(B),
-                                 _ptr(D), _ptr(W), _ptr(radial_w), _ptr(out), _ptr(z), _ptr(perm), _ptr(offsets),
-                                 _ptr(workspace), workspace.numel(), _stream(stream))
-    _check(st, "tdn_cp_tp_forward")
+    name = "tdn_ablation_forward_atomics" if atomics_ablation else "tdn_cp_tp_forward"
+    st = getattr(lib(), name)(ctypes.byref(p), _ptr(x), _ptr(edge_vec), _ptr(edge_index), _ptr(A), _ptr(B),
+                              _ptr(D), _ptr(W), _ptr(radial_w), _ptr(out), _ptr(z), _ptr(perm), _ptr(offsets),
+                              _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, name)
     return ForwardResult(out, z, perm, offsets, p,
                          dict(x=x, edge_vec=edge_vec, edge_index=edge_index, A=A, B=B, D=D, W=W, radial_w=radial_w))
 

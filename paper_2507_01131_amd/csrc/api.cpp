@@ -248,15 +248,16 @@ tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int3
 hipError_t forward_edge_pass(const tdn_problem& p, const int32_t* offsets, const int32_t* perm, const int32_t* src,
                              const int32_t* dst, const float* edge_vec, const float* A, const float* B, const float* D,
                              const float* radial_w, const void* x, void* xt, float* partial, float* Z,
-                             hipStream_t s) {
+                             hipStream_t s, bool atomic = false) {
   {
     Timed t("feature_layout", s);
     hipError_t e = tdn::launch_feature_layout(p.n_nodes, dim_of(p.L), p.C, x, p.feat_dtype == TDN_F32,
                                               feature_parts(p), xt, row_scales(p, xt), s);
     if (e != hipSuccess) return e;
   }
-  Timed t("cp_edge_fwd", s);
-  return tdn::launch_cp_edge(edge_args(p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, xt, Z, partial), s);
+  Timed t(atomic ? "cp_edge_fwd_atomic" : "cp_edge_fwd", s);
+  const tdn::EdgeArgs a = edge_args(p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, xt, Z, partial);
+  return atomic ? tdn::launch_cp_edge_atomic(a, s) : tdn::launch_cp_edge(a, s);
 }
 
 }  // namespace
@@ -289,12 +290,15 @@ tdn_status tdn_workspace_size(const tdn_problem* p, size_t* fwd_bytes, size_t* b
   return TDN_OK;
 }
 
-tdn_status tdn_cp_tp_forward(const tdn_problem* p, const void* x, const float* edge_vec, const int32_t* edge_index,
-                             const float* A, const float* B, const float* D, const void* W, const float* radial_w,
-                             float* out, float* z_save, int32_t* perm, int32_t* offsets, void* workspace,
-                             size_t workspace_bytes, hipStream_t stream) {
+namespace {
+tdn_status forward_impl(const tdn_problem* p, const void* x, const float* edge_vec, const int32_t* edge_index,
+                        const float* A, const float* B, const float* D, const void* W, const float* radial_w,
+                        float* out, float* z_save, int32_t* perm, int32_t* offsets, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream, bool atomic) {
   tdn_status st = check_problem(p);
   if (st != TDN_OK) return st;
+  if (atomic && p->feat_dtype != TDN_F32) return TDN_ERR_BAD_DTYPE;
+  if (atomic && (p->L < 2 || p->L > 4)) return TDN_ERR_BAD_SHAPE;
   const int N = p->n_nodes, E = p->n_edges, d = dim_of(p->L), C = p->C;
   if (!A || !B || !D || !W || !radial_w || !offsets || !workspace) return TDN_ERR_NULL_POINTER;
   if (N > 0 && (!x || !out)) return TDN_ERR_NULL_POINTER;
@@ -321,12 +325,30 @@ tdn_status tdn_cp_tp_forward(const tdn_problem* p, const void* x, const float* e
   float* Z = z_save ? z_save : reinterpret_cast<float*>(ws + lay.z);
   const bool bf16 = p->feat_dtype == TDN_BF16;
   TDN_HIP(forward_edge_pass(*p, offsets, perm, src, dst, edge_vec, A, B, D, radial_w, x, ws + lay.xt,
-                            reinterpret_cast<float*>(ws + lay.part), Z, stream));
+                            reinterpret_cast<float*>(ws + lay.part), Z, stream, atomic));
   {
     Timed t("node_gemm", stream);
     TDN_HIP(tdn::launch_node_gemm(N * d, C, Z, W, bf16, 0, out, ws + lay.wp, stream));
   }
   return TDN_OK;
+}
+}  // namespace
+
+tdn_status tdn_cp_tp_forward(const tdn_problem* p, const void* x, const float* edge_vec, const int32_t* edge_index,
+                             const float* A, const float* B, const float* D, const void* W, const float* radial_w,
+                             float* out, float* z_save, int32_t* perm, int32_t* offsets, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  return forward_impl(p, x, edge_vec, edge_index, A, B, D, W, radial_w, out, z_save, perm, offsets, workspace,
+                      workspace_bytes, stream, false);
+}
+
+tdn_status tdn_ablation_forward_atomics(const tdn_problem* p, const void* x, const float* edge_vec,
+                                        const int32_t* edge_index, const float* A, const float* B, const float* D,
+                                        const void* W, const float* radial_w, float* out, float* z_save,
+                                        int32_t* perm, int32_t* offsets, void* workspace, size_t workspace_bytes,
+                                        hipStream_t stream) {
+  return forward_impl(p, x, edge_vec, edge_index, A, B, D, W, radial_w, out, z_save, perm, offsets, workspace,
+                      workspace_bytes, stream, true);
 }
 
 tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* edge_vec, const int32_t* edge_index,

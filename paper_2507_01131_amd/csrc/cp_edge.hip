@@ -12,6 +12,8 @@ namespace tdn {
 namespace edge_detail {
 template <int L>
 hipError_t launch_cp_edge_l(const EdgeArgs& a, hipStream_t s);
+template <int L>
+hipError_t launch_cp_edge_atomic_l(const EdgeArgs& a, hipStream_t s);
 
 namespace {
 
@@ -157,6 +159,25 @@ hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s) {
   if (a.n_seg > 0)
     k_range_fixup<<<dim3(a.n_seg), dim3(256), 0, s>>>(a.E, a.n_range, a.d * a.C, a.offsets, a.partial, a.out);
   return hipGetLastError();
+}
+
+hipError_t launch_cp_edge_atomic(const EdgeArgs& a, hipStream_t s) {
+  using namespace edge_detail;
+  if (a.parts != 2 || a.L < 2 || a.L > 4) return hipErrorInvalidValue;
+  if (a.E > 0 && (a.n_range < 1 || a.n_range > a.E || a.pieces_per_block < 1 || a.n_range % a.pieces_per_block ||
+                  !a.ef_ops || !a.ef_scale || !a.row_scale))
+    return hipErrorInvalidValue;
+  hipError_t e = launch_zero(a.out, size_t(a.n_seg) * a.d * a.C * 4, s);
+  if (e != hipSuccess || a.E == 0) return e;
+  const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
+  k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops), a.ef_scale);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  switch (a.L) {
+    case 2: return launch_cp_edge_atomic_l<2>(a, s);
+    case 3: return launch_cp_edge_atomic_l<3>(a, s);
+    default: return launch_cp_edge_atomic_l<4>(a, s);
+  }
 }
 
 }  // namespace tdn

@@ -149,7 +149,11 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radi
   return s;
 }
 
-template <int L, int RT, bool BF>
+// ATOM (measurement ablation only): every edge is its own segment, so the
+// epilogue applies EF per edge, and it adds Z into `out` with float atomics
+// instead of storing the segment sums (`out` zeroed beforehand; no partial
+// slots, no fix-up) -- the naive scatter-add the segmented sum replaces.
+template <int L, int RT, bool BF, bool ATOM = false>
 __global__ __launch_bounds__(kMaxWavesPerBlock* kWave)
 __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edge(EdgeArgs a, int n_cgrp, int waves,
                                                                                   int chunk) {
@@ -249,7 +253,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   const float ef_unscale = BF ? 1.f : *a.ef_scale;
   int range = 0;
   auto finish = [&](int seg, int part) {
-    float* dst = part < 0 ? a.out + size_t(seg) * d * C : a.partial + (size_t(range) * 2 + part) * d * C;
+    float* dst = (ATOM || part < 0) ? a.out + size_t(seg) * d * C : a.partial + (size_t(range) * 2 + part) * d * C;
     constexpr int P16 = BF ? 1 : 2;
     float hsc = 1.f, zsc = 1.f;
     if constexpr (!BF) {
@@ -317,7 +321,12 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int m = mt * kTile + acc_row(v, h);
-            if (m < d) dst[size_t(m) * C + c] = z[t][mt][v] * zsc;
+            if (m < d) {
+              if constexpr (ATOM)
+                unsafeAtomicAdd(dst + size_t(m) * C + c, z[t][mt][v] * zsc);  // hardware float add
+              else
+                dst[size_t(m) * C + c] = z[t][mt][v] * zsc;
+            }
           }
       }
     }
@@ -475,7 +484,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
         int prev = __shfl_up(key, 1);
         if (t == 0) prev = cb > 0 ? a.key[a.perm[cb - 1]] : -1;
         const int last_key = __shfl(key, n - 1);
-        const bool start = t < n && (key != prev || (cb == e_lo && t == 0));
+        const bool start = t < n && (ATOM || key != prev || (cb == e_lo && t == 0));
         const unsigned long long m = __ballot(start);
         if (start) {
           const int pos = __popcll(m & ((1ull << t) - 1));
@@ -484,8 +493,8 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
         }
         if (t == 0) {
           sMeta[0] = __popcll(m);
-          sMeta[1] = cb == e_lo && cb > 0 && key == prev;
-          sMeta[2] = cb + n == e_hi && e_hi < a.E && a.key[a.perm[e_hi]] == last_key;
+          sMeta[1] = !ATOM && cb == e_lo && cb > 0 && key == prev;
+          sMeta[2] = !ATOM && cb + n == e_hi && e_hi < a.E && a.key[a.perm[e_hi]] == last_key;
         }
       }
       __syncthreads();
@@ -599,7 +608,7 @@ inline EdgeGrid edge_grid(int C, int RT, bool bf) {
   return EdgeGrid{waves, (wave_tiles + waves - 1) / waves};
 }
 
-template <int L, int RT, bool BF>
+template <int L, int RT, bool BF, bool ATOM = false>
 hipError_t launch_l_rt_m(const EdgeArgs& a, hipStream_t s) {
   constexpr int d = (L + 1) * (L + 1);
   const EdgeGrid gr = edge_grid(a.C, RT, BF);
@@ -607,7 +616,7 @@ hipError_t launch_l_rt_m(const EdgeArgs& a, hipStream_t s) {
   if (a.E > 0) {
     const int chunk = edge_chunk(L, RT, BF, a.n_radial);
     const size_t lds = size_t(edge_smem(RT, BF, d, a.n_radial, chunk).floats) * 4;
-    auto k = k_cp_edge<L, RT, BF>;
+    auto k = k_cp_edge<L, RT, BF, ATOM>;
     hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
@@ -632,6 +641,22 @@ hipError_t launch_cp_edge_l(const EdgeArgs& a, hipStream_t s) {
     case 6: return launch_l_rt<L, 6>(a, s);
     case 7: return launch_l_rt<L, 7>(a, s);
     case 8: return launch_l_rt<L, 8>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// The ablation's dispatch on the rank tiles (fp32 features only).
+template <int L>
+hipError_t launch_cp_edge_atomic_l(const EdgeArgs& a, hipStream_t s) {
+  switch ((a.R + kTile - 1) / kTile) {
+    case 1: return launch_l_rt_m<L, 1, false, true>(a, s);
+    case 2: return launch_l_rt_m<L, 2, false, true>(a, s);
+    case 3: return launch_l_rt_m<L, 3, false, true>(a, s);
+    case 4: return launch_l_rt_m<L, 4, false, true>(a, s);
+    case 5: return launch_l_rt_m<L, 5, false, true>(a, s);
+    case 6: return launch_l_rt_m<L, 6, false, true>(a, s);
+    case 7: return launch_l_rt_m<L, 7, false, true>(a, s);
+    case 8: return launch_l_rt_m<L, 8, false, true>(a, s);
     default: return hipErrorInvalidValue;
   }
 }

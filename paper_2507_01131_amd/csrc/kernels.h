@@ -87,6 +87,11 @@ hipError_t launch_direct_layout(int N, int d, int C, int Cp, const void* x, bool
                                 float* row_scale, bool perm_channels, hipStream_t s);
 // parts = 2: fp32 features (fp16 two-part split), parts = 1: bf16 features
 hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
+// Measurement ablation of the segmented sum (fp32 features, 2 <= L <= 4): the
+// same contraction with every edge its own segment, the output factor applied
+// per edge and Z accumulated into `out` (zeroed first) with float atomics;
+// nondeterministic in the order of the additions.
+hipError_t launch_cp_edge_atomic(const EdgeArgs& a, hipStream_t s);
 // Workspace bytes of EdgeArgs::ef_ops: the output factor in 32x32x16 operand
 // blocks [ceil(d/32)][ceil(R/32)][2][parts][64 lanes] x 16 bytes (parts <= 2)
 // and, after them, its scale.

@@ -279,3 +279,48 @@ def test_validation_passes_on_good_input_and_timer_counts_launches():
     assert n == 1 and ms > 0
     ref = _oracle_fwd(w, A, B, D)
     assert rel_err(res.out.cpu(), ref) < TOL_F32
+
+
+# ------------------------------------------------------------ atomic scatter-add ablation
+ATOMIC_SMALL = [c for c in SMALL if c.get("feat_dtype", "f32") == "f32" and 2 <= c["L"] <= 4]
+
+
+@pytest.mark.parametrize("cfg", ATOMIC_SMALL, ids=lambda c: f"L{c['L']}C{c['C']}R{c['R']}s{c['seed']}")
+def test_atomics_ablation_small_full(cfg):
+    w, (A, B, D) = _small(cfg)
+    res = _fwd(w, A, B, D, atomics_ablation=True)
+    ref, zref = layer.forward(w["x"], w["edge_index"], w["edge_vec"], A, B, D, w["W"], w["radial_w"], w["r_cut"],
+                              w["L"], return_z=True)
+    rp, ro = layer.stable_sort_by_key(w["edge_index"][1], w["N"])
+    np.testing.assert_array_equal(res.perm.cpu().numpy(), rp)
+    np.testing.assert_array_equal(res.offsets.cpu().numpy(), ro)
+    assert rel_err(res.out.cpu(), ref) < TOL_F32
+    assert rel_err(res.z.cpu(), zref) < TOL_F32
+
+
+def test_atomics_ablation_headline_size_sampled():
+    w = workload("molecules3200_L4_C128_R128")
+    A, B, D = load_factors(w["L"], w["R"])
+    seg = _fwd(w, A, B, D)
+    res = _fwd(w, A, B, D, atomics_ablation=True)
+    out = res.out.cpu().numpy()
+    assert np.all(np.isfinite(out))
+    nodes = sample_nodes(w, 24)
+    ref = layer.forward_at_nodes(nodes, w["x"], w["edge_index"], w["edge_vec"], A, B, D, w["W"], w["radial_w"],
+                                 w["r_cut"], w["L"])
+    assert rel_err(out[nodes], ref) < TOL_F32
+    # the two summation orders agree to the fp32 tolerance everywhere
+    assert rel_err(res.out.cpu(), seg.out.cpu().numpy().astype(np.float64)) < TOL_F32
+
+
+def test_atomics_ablation_rejects_unsupported_problems():
+    w = workloads.random_graph(11, n_nodes=10, n_edges=50, L=5, C=32, R=32)
+    A, B, D = random_factors(5, 32, 11)
+    with pytest.raises(tdn.TdnError) as ei:
+        _fwd(w, A, B, D, atomics_ablation=True)
+    assert ei.value.status == 2
+    w = workloads.random_graph(12, n_nodes=10, n_edges=50, L=3, C=32, R=32, feat_dtype="bf16")
+    A, B, D = random_factors(3, 32, 12)
+    with pytest.raises(tdn.TdnError) as ei:
+        _fwd(w, A, B, D, atomics_ablation=True)
+    assert ei.value.status == 3
