@@ -19,6 +19,11 @@ Modules
             Sec. 3.3, Sec. 3.4, Sec. 4.1, App. B)
   layer     the message-passing layer by direct per-edge summation and its
             backward (Sec. 3.1 eq. approximate, Sec. 3.2)
+  radius_graph
+            the edges the layer consumes: every atom pair of a system (and
+            its periodic images) closer than the cutoff, with an optional
+            nearest-neighbour cap, by brute force in float32 (App. "Model and
+            Training Configurations")
 
 Parity status: every function is pinned by the tests in tests/test_oracle_*.py
 against closed forms, library routines, invariants or brute force, except the

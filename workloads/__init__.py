@@ -76,21 +76,12 @@ def _streams(seed: int):
     return {n: np.random.default_rng(k) for n, k in zip(names, kids)}
 
 
-def _batch_of_molecules(rng, n_graphs, n_atoms, r_cut, sphere):
-    srcs, dsts, vecs = [], [], []
-    for g in range(n_graphs):
-        pos = geometry.molecule_walk(rng, n_atoms, sphere=sphere, ring_start=bool(g % 2))
-        s, t, v = geometry.radius_graph(pos, r_cut)
-        srcs.append(s + g * n_atoms)
-        dsts.append(t + g * n_atoms)
-        vecs.append(v)
-    return (n_graphs * n_atoms, np.concatenate(srcs), np.concatenate(dsts),
-            np.concatenate(vecs))
+def _batch_of_molecules(rng, n_graphs, n_atoms, sphere):
+    return [geometry.molecule_walk(rng, n_atoms, sphere=sphere, ring_start=bool(g % 2)) for g in range(n_graphs)]
 
 
-def _slabs(rng, n_slabs, r_cut):
-    srcs, dsts, vecs = [], [], []
-    base = 0
+def _slabs(rng, n_slabs):
+    graphs, cells = [], []
     for _ in range(n_slabs):
         slab, cell_xy = geometry.fcc_slab(rng)
         ads = geometry.molecule_walk(rng, 10, sphere=3.0)
@@ -99,39 +90,57 @@ def _slabs(rng, n_slabs, r_cut):
                           top + 2.0 - ads[:, 2].min()])
         ads = ads - ads[0] * np.array([1.0, 1.0, 0.0]) + shift
         ads[:, :2] %= cell_xy
-        pos = np.concatenate([slab, ads])
-        cell = np.array([cell_xy[0], cell_xy[1], 0.0])
-        s, t, v = geometry.radius_graph(pos, r_cut, cell, (True, True, False))
-        srcs.append(s + base)
-        dsts.append(t + base)
-        vecs.append(v)
-        base += pos.shape[0]
-    return base, np.concatenate(srcs), np.concatenate(dsts), np.concatenate(vecs)
+        graphs.append(np.concatenate([slab, ads]))
+        cells.append(np.array([cell_xy[0], cell_xy[1], 0.0]))
+    return graphs, cells
 
 
-def _bulk(rng, n_atoms, density, r_cut):
-    box = (n_atoms / density) ** (1.0 / 3.0)
-    pos = geometry.random_sequential_addition(rng, n_atoms, box)
-    s, t, v = geometry.radius_graph(pos, r_cut, np.array([box, box, box]), (True, True, True))
-    return n_atoms, s, t, v
+def make_geometry(w: Workload) -> dict:
+    """The atoms behind a workload's graph: a batch of independent graphs.
+
+    Returns pos float64 [N,3] (graphs one after another), graph_ptr int64
+    [G+1] (graph g holds atoms graph_ptr[g] .. graph_ptr[g+1]-1), cell
+    float64 [G,3] (box lengths; 0 on non-periodic axes), periodic (3 bools)
+    and r_cut.  Periodic coordinates are as generated (slab atoms may lie up
+    to a few tenths of an Angstrom outside [0, L))."""
+    rng = _streams(w.seed)["pos"]
+    if w.name.startswith("cube64"):
+        graphs, cells, per = [rng.uniform(0.0, 6.0, size=(64, 3))], [np.zeros(3)], (False, False, False)
+    elif w.name.startswith("molecules960"):
+        graphs = _batch_of_molecules(rng, 32, 30, sphere=3.5)
+        cells, per = [np.zeros(3)] * 32, (False, False, False)
+    elif w.name.startswith("molecules3200"):
+        graphs = _batch_of_molecules(rng, 64, 50, sphere=3.5)
+        cells, per = [np.zeros(3)] * 64, (False, False, False)
+    elif w.name.startswith("slabs4960"):
+        graphs, cells = _slabs(rng, 16)
+        per = (True, True, False)
+    elif w.name.startswith("bulk4096"):
+        box = (4096 / 0.1) ** (1.0 / 3.0)
+        graphs = [geometry.random_sequential_addition(rng, 4096, box)]
+        cells, per = [np.array([box, box, box])], (True, True, True)
+    else:
+        raise KeyError(w.name)
+    ptr = np.concatenate([[0], np.cumsum([g.shape[0] for g in graphs])]).astype(np.int64)
+    return dict(pos=np.concatenate(graphs), graph_ptr=ptr, cell=np.stack(cells), periodic=per, r_cut=float(w.r_cut))
 
 
 def make_graph(w: Workload):
-    """Returns (n_nodes, src, dst, edge_vec) for a workload (float64 vectors)."""
-    rng = _streams(w.seed)["pos"]
-    if w.name.startswith("cube64"):
-        pos = rng.uniform(0.0, 6.0, size=(64, 3))
-        s, t, v = geometry.radius_graph(pos, w.r_cut)
-        return 64, s, t, v
-    if w.name.startswith("molecules960"):
-        return _batch_of_molecules(rng, 32, 30, w.r_cut, sphere=3.5)
-    if w.name.startswith("molecules3200"):
-        return _batch_of_molecules(rng, 64, 50, w.r_cut, sphere=3.5)
-    if w.name.startswith("slabs4960"):
-        return _slabs(rng, 16, w.r_cut)
-    if w.name.startswith("bulk4096"):
-        return _bulk(rng, 4096, 0.1, w.r_cut)
-    raise KeyError(w.name)
+    """Returns (n_nodes, src, dst, edge_vec) for a workload (float64 vectors):
+    the radius graph of every graph of ``make_geometry``, concatenated."""
+    g = make_geometry(w)
+    pos, ptr, per = g["pos"], g["graph_ptr"], g["periodic"]
+    srcs, dsts, vecs = [], [], []
+    for k in range(len(ptr) - 1):
+        a, b = int(ptr[k]), int(ptr[k + 1])
+        if any(per):
+            s, t, v = geometry.radius_graph(pos[a:b], g["r_cut"], g["cell"][k], per)
+        else:
+            s, t, v = geometry.radius_graph(pos[a:b], g["r_cut"])
+        srcs.append(s + a)
+        dsts.append(t + a)
+        vecs.append(v)
+    return int(ptr[-1]), np.concatenate(srcs), np.concatenate(dsts), np.concatenate(vecs)
 
 
 def make_workload(name: str) -> dict:
