@@ -57,7 +57,10 @@ typedef enum {
   TDN_ERR_NOT_SORTED = 6,          /* validate=1: edges_sorted=1 but dst decreases */
   TDN_ERR_DEGENERATE_EDGE = 7,     /* validate=1: zero-length or non-finite r_e   */
   TDN_ERR_UNSUPPORTED_DEVICE = 8,  /* current device is not gfx950                */
-  TDN_ERR_HIP = 9                  /* a HIP call failed, see tdn_last_hip_error   */
+  TDN_ERR_HIP = 9,                 /* a HIP call failed, see tdn_last_hip_error   */
+  TDN_ERR_BAD_GEOMETRY = 10,       /* radius graph: graph_ptr, positions or box   */
+  TDN_ERR_EDGE_CAPACITY = 11,      /* radius graph: more edges than buffer room   */
+  TDN_ERR_NEIGHBOUR_LIMIT = 12     /* radius graph: > 2048 candidates for an atom */
 } tdn_status;
 
 typedef enum { TDN_F32 = 0, TDN_BF16 = 1 } tdn_dtype;
@@ -142,6 +145,57 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
                               float* grad_edge_vec, void* workspace, size_t workspace_bytes,
                               hipStream_t stream);
 
+/* Radius graph of a batch of atomic systems (App. "Model and Training
+ * Configurations": the edges are built on the fly from a cutoff, with a cap
+ * on the neighbours per atom -- 5.0 and 500 for OC20, 12.0 and 20 for OC22).
+ * System g owns atoms graph_ptr[g] .. graph_ptr[g+1]-1; on a periodic axis a
+ * it is a box of length cell[g][a] >= r_cut holding its atoms in [0, L).
+ * Edge (src, dst, n), same system, source image n in {-1,0,1} per periodic
+ * axis (0 elsewhere):
+ *   r = (pos[src] - pos[dst]) + n * L      float32, each operation rounded
+ *   kept when (rx*rx + ry*ry) + rz*rz < r_cut*r_cut (no fused multiply-add),
+ *   except src == dst with n = 0,
+ * so the edge set and vectors are exact functions of the float32 inputs.
+ * max_neighbors > 0 keeps, per destination, the candidates smallest in
+ * (|r|^2, src, image code).  Edges are ordered by (dst, src, image code),
+ * code = (nx+1)*9 + (ny+1)*3 + (nz+1): edges_sorted = 1 input for
+ * tdn_cp_tp_forward. */
+typedef struct {
+  int32_t n_nodes;       /* N atoms over all systems, 0 <= N < 2^26          */
+  int32_t n_graphs;      /* G systems (>= 1 when N > 0)                      */
+  float r_cut;           /* cutoff, > 0                                       */
+  int32_t max_neighbors; /* 0 = no cap                                        */
+  int32_t periodic[3];   /* 1 = the axis is periodic (every system)          */
+} tdn_graph_problem;
+
+tdn_status tdn_radius_graph_workspace_size(const tdn_graph_problem* g, size_t* bytes);
+
+/*   pos        [N, 3]   f32    device
+ *   graph_ptr  [G+1]    int32  device, graph_ptr[0] = 0, non-decreasing,
+ *                              graph_ptr[G] = N
+ *   cell       [G, 3]   f32    device box lengths (read on periodic axes
+ *                              only; may be NULL when no axis is periodic)
+ *   edge_index [2, E]   int32  row 0 = src, row 1 = dst (row stride E, the
+ *                              edge count, not the capacity)
+ *   edge_vec   [E, 3]   f32    r as above
+ *   edge_image [E, 3]   int32  n (or NULL)
+ *   offsets    [N+1]    int32  first edge of each dst, offsets[N] = E (or NULL)
+ *   n_edges    host int64: E
+ * edge buffers hold edge_capacity edges.  The call counts the edges first and
+ * synchronises the stream once to read E and the checks; then, if
+ * E <= edge_capacity, it writes the edges (asynchronously, on the stream).
+ * E > edge_capacity returns TDN_ERR_EDGE_CAPACITY with *n_edges = E and
+ * writes nothing (capacity 0 with NULL edge buffers asks for the count).
+ * TDN_ERR_BAD_GEOMETRY: graph_ptr inconsistent, a non-finite position, a box
+ * shorter than r_cut, or a periodic coordinate outside [0, L).
+ * TDN_ERR_NEIGHBOUR_LIMIT: an atom has more than 2048 candidates within the
+ * cutoff (before the cap).  Workspace from tdn_radius_graph_workspace_size;
+ * not for capture in a HIP graph (it synchronises). */
+tdn_status tdn_radius_graph(const tdn_graph_problem* g, const float* pos, const int32_t* graph_ptr,
+                            const float* cell, int64_t edge_capacity, int32_t* edge_index,
+                            float* edge_vec, int32_t* edge_image, int32_t* offsets, int64_t* n_edges,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Stable sort of E integer keys in [0, n_keys): perm[p] = original index of
  * the p-th smallest key (equal keys keep their original order), offsets[k] =
  * number of keys < k, offsets[n_keys] = E.  Keys outside the range give
@@ -162,7 +216,7 @@ tdn_status tdn_spherical_harmonics(int32_t L, int32_t E, const float* edge_vec, 
  * tdn_timer_enable(1) starts recording every launch of the layer's edge
  * kernels; tdn_timer_read synchronises on the recorded events and returns
  * the summed milliseconds and launch count of the kernel named `kernel`
- * ("cp_edge_fwd", "cp_edge_fwd_atomic", "feature_layout", "channel_layout", "cp_edge_bwd_src", "cp_bwd_dst", "node_gemm", "gram",
+ * ("cp_edge_fwd", "cp_edge_fwd_atomic", "radius_graph", "feature_layout", "channel_layout", "cp_edge_bwd_src", "cp_bwd_dst", "node_gemm", "gram",
  * "sort");
  * reset = 1 clears that kernel's record. */
 tdn_status tdn_timer_enable(int32_t enable);

@@ -26,7 +26,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtdn.so")
 TDN_F32, TDN_BF16 = 0, 1
 STATUS = {0: "TDN_OK", 1: "TDN_ERR_NULL_POINTER", 2: "TDN_ERR_BAD_SHAPE", 3: "TDN_ERR_BAD_DTYPE",
           4: "TDN_ERR_WORKSPACE_TOO_SMALL", 5: "TDN_ERR_INDEX_OUT_OF_RANGE", 6: "TDN_ERR_NOT_SORTED",
-          7: "TDN_ERR_DEGENERATE_EDGE", 8: "TDN_ERR_UNSUPPORTED_DEVICE", 9: "TDN_ERR_HIP"}
+          7: "TDN_ERR_DEGENERATE_EDGE", 8: "TDN_ERR_UNSUPPORTED_DEVICE", 9: "TDN_ERR_HIP",
+          10: "TDN_ERR_BAD_GEOMETRY", 11: "TDN_ERR_EDGE_CAPACITY", 12: "TDN_ERR_NEIGHBOUR_LIMIT"}
+TDN_ERR_EDGE_CAPACITY = 11
 
 
 class TdnError(RuntimeError):
@@ -36,6 +38,11 @@ class TdnError(RuntimeError):
         if status == 9:
             extra = f" (hipError {lib().tdn_last_hip_error()})"
         super().__init__(f"{where}: {STATUS.get(status, status)}{extra}")
+
+
+class GraphProblem(ctypes.Structure):
+    _fields_ = [("n_nodes", ctypes.c_int32), ("n_graphs", ctypes.c_int32), ("r_cut", ctypes.c_float),
+                ("max_neighbors", ctypes.c_int32), ("periodic", ctypes.c_int32 * 3)]
 
 
 class Problem(ctypes.Structure):
@@ -62,6 +69,10 @@ def lib() -> ctypes.CDLL:
         L.tdn_cp_tp_forward.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
         L.tdn_ablation_forward_atomics.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
         L.tdn_cp_tp_backward.argtypes = [PP] + [_P] * 16 + [_SZ, _P]
+        GP = ctypes.POINTER(GraphProblem)
+        L.tdn_radius_graph_workspace_size.argtypes = [GP, ctypes.POINTER(_SZ)]
+        L.tdn_radius_graph.argtypes = [GP, _P, _P, _P, ctypes.c_int64, _P, _P, _P, _P,
+                                       ctypes.POINTER(ctypes.c_int64), _P, _SZ, _P]
         L.tdn_sort_workspace_size.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_SZ)]
         L.tdn_sort_by_key.argtypes = [ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P, _SZ, _P]
         L.tdn_spherical_harmonics.argtypes = [ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P]
@@ -73,7 +84,7 @@ def lib() -> ctypes.CDLL:
         L.tdn_last_hip_error.restype = ctypes.c_int32
         for f in ("tdn_workspace_size", "tdn_cp_tp_forward", "tdn_ablation_forward_atomics", "tdn_cp_tp_backward",
                   "tdn_sort_workspace_size", "tdn_sort_by_key", "tdn_spherical_harmonics", "tdn_timer_enable",
-                  "tdn_timer_read"):
+                  "tdn_timer_read", "tdn_radius_graph_workspace_size", "tdn_radius_graph"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -222,6 +233,55 @@ def sort_by_key(keys: torch.Tensor, n_keys: int, stream=None):
     _check(lib().tdn_sort_by_key(int(n_keys), int(E), _ptr(keys), _ptr(perm), _ptr(offsets), _ptr(ws), ws.numel(),
                                  _stream(stream)), "tdn_sort_by_key")
     return perm, offsets
+
+
+@dataclass
+class RadiusGraph:
+    edge_index: torch.Tensor      # [2, E] int32, row 0 = src, row 1 = dst, sorted by (dst, src, image)
+    edge_vec: torch.Tensor        # [E, 3] float32
+    edge_image: torch.Tensor | None  # [E, 3] int32
+    offsets: torch.Tensor         # [N+1] int32
+
+
+def radius_graph(pos, graph_ptr, *, r_cut: float, cell=None, periodic=(False, False, False), max_neighbors=0,
+                 capacity=None, want_image=False, workspace=None, stream=None) -> RadiusGraph:
+    """Runs tdn_radius_graph.  pos [N,3] float32, graph_ptr [G+1] int32 (int64
+    is converted), cell [G,3] float32 when an axis is periodic.  capacity:
+    edge buffer size to try first (default: ask for the count, then build);
+    a call with too small a capacity is repeated once with the exact count."""
+    dev = pos.device
+    N = pos.shape[0]
+    if graph_ptr.dtype != torch.int32:
+        graph_ptr = graph_ptr.to(torch.int32)
+    graph_ptr = graph_ptr.contiguous()
+    G = graph_ptr.numel() - 1
+    _need(pos, "pos", torch.float32, (N, 3), dev)
+    _need(graph_ptr, "graph_ptr", torch.int32, (G + 1,), dev)
+    if cell is not None:
+        _need(cell, "cell", torch.float32, (G, 3), dev)
+    per = (ctypes.c_int32 * 3)(*[int(bool(p)) for p in periodic])
+    g = GraphProblem(int(N), int(G), float(r_cut), int(max_neighbors), per)
+    nb = _SZ()
+    _check(lib().tdn_radius_graph_workspace_size(ctypes.byref(g), ctypes.byref(nb)), "tdn_radius_graph_workspace_size")
+    if workspace is None or workspace.numel() < nb.value:
+        workspace = torch.empty(max(nb.value, 1), dtype=torch.uint8, device=dev)
+    offsets = torch.empty(N + 1, dtype=torch.int32, device=dev)
+    n_edges = ctypes.c_int64()
+    cap = 0 if capacity is None else int(capacity)
+    for _ in range(2):
+        ei = torch.empty(max(2 * cap, 1), dtype=torch.int32, device=dev)
+        ev = torch.empty((max(cap, 1), 3), dtype=torch.float32, device=dev)
+        im = torch.empty((max(cap, 1), 3), dtype=torch.int32, device=dev) if want_image else None
+        st = lib().tdn_radius_graph(ctypes.byref(g), _ptr(pos), _ptr(graph_ptr), _ptr(cell), cap,
+                                    _ptr(ei) if cap else None, _ptr(ev) if cap else None,
+                                    _ptr(im) if cap and want_image else None, _ptr(offsets), ctypes.byref(n_edges),
+                                    _ptr(workspace), workspace.numel(), _stream(stream))
+        if st != TDN_ERR_EDGE_CAPACITY:
+            break
+        cap = n_edges.value
+    _check(st, "tdn_radius_graph")
+    E = n_edges.value
+    return RadiusGraph(ei[:2 * E].view(2, E), ev[:E], im[:E] if want_image else None, offsets)
 
 
 def spherical_harmonics(edge_vec: torch.Tensor, L: int, jacobian=False, stream=None):

@@ -276,6 +276,9 @@ const char* tdn_status_string(tdn_status s) {
     case TDN_ERR_DEGENERATE_EDGE: return "zero-length or non-finite edge vector";
     case TDN_ERR_UNSUPPORTED_DEVICE: return "unsupported device (needs gfx950)";
     case TDN_ERR_HIP: return "HIP error";
+    case TDN_ERR_BAD_GEOMETRY: return "invalid graph_ptr, position or periodic box";
+    case TDN_ERR_EDGE_CAPACITY: return "edge buffers smaller than the edge count";
+    case TDN_ERR_NEIGHBOUR_LIMIT: return "more than 2048 neighbours of one atom within the cutoff";
   }
   return "unknown status";
 }
@@ -481,6 +484,70 @@ tdn_status tdn_sort_by_key(int32_t n_keys, int32_t E, const int32_t* keys, int32
   if (st != TDN_OK) return st;
   Timed t("sort", stream);
   TDN_HIP(tdn::launch_sort(plan, keys, 1, perm, offsets, workspace, stream));
+  return TDN_OK;
+}
+
+namespace {
+tdn_status check_graph_problem(const tdn_graph_problem* g) {
+  if (!g) return TDN_ERR_NULL_POINTER;
+  if (g->n_nodes < 0 || g->n_nodes >= (1 << 26) || g->n_graphs < 0 || g->max_neighbors < 0)
+    return TDN_ERR_BAD_SHAPE;
+  if (g->n_nodes > 0 && g->n_graphs == 0) return TDN_ERR_BAD_SHAPE;
+  if (g->n_graphs > (1 << 26)) return TDN_ERR_BAD_SHAPE;
+  if (!(g->r_cut > 0.f) || !std::isfinite(g->r_cut)) return TDN_ERR_BAD_SHAPE;
+  for (int k = 0; k < 3; ++k)
+    if (g->periodic[k] != 0 && g->periodic[k] != 1) return TDN_ERR_BAD_SHAPE;
+  return TDN_OK;
+}
+}  // namespace
+
+tdn_status tdn_radius_graph_workspace_size(const tdn_graph_problem* g, size_t* bytes) {
+  const tdn_status st = check_graph_problem(g);
+  if (st != TDN_OK) return st;
+  if (!bytes) return TDN_ERR_NULL_POINTER;
+  *bytes = tdn::radius_graph_layout(g->n_nodes, g->n_graphs).total;
+  return TDN_OK;
+}
+
+tdn_status tdn_radius_graph(const tdn_graph_problem* g, const float* pos, const int32_t* graph_ptr,
+                            const float* cell, int64_t edge_capacity, int32_t* edge_index, float* edge_vec,
+                            int32_t* edge_image, int32_t* offsets, int64_t* n_edges, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+  tdn_status st = check_graph_problem(g);
+  if (st != TDN_OK) return st;
+  if (!n_edges || !graph_ptr || !workspace || (g->n_nodes > 0 && !pos)) return TDN_ERR_NULL_POINTER;
+  const bool periodic = g->periodic[0] || g->periodic[1] || g->periodic[2];
+  if (periodic && g->n_graphs > 0 && !cell) return TDN_ERR_NULL_POINTER;
+  if (edge_capacity < 0) return TDN_ERR_BAD_SHAPE;
+  if (edge_capacity > 0 && (!edge_index || !edge_vec)) return TDN_ERR_NULL_POINTER;
+  const tdn::RadiusGraphLayout lay = tdn::radius_graph_layout(g->n_nodes, g->n_graphs);
+  if (workspace_bytes < lay.total) return TDN_ERR_WORKSPACE_TOO_SMALL;
+  st = check_device();
+  if (st != TDN_OK) return st;
+  tdn::RadiusGraphArgs a{};
+  a.N = g->n_nodes;
+  a.G = g->n_graphs;
+  a.r_cut = g->r_cut;
+  a.max_neighbors = g->max_neighbors;
+  for (int k = 0; k < 3; ++k) a.periodic[k] = g->periodic[k];
+  a.pos = pos;
+  a.graph_ptr = graph_ptr;
+  a.cell = cell;
+  char* ws = static_cast<char*>(workspace);
+  Timed t("radius_graph", stream);
+  TDN_HIP(tdn::launch_radius_count(a, ws, stream));
+  int32_t flags[5] = {0, 0, 0, 0, 0}, total = 0;
+  TDN_HIP(hipMemcpyAsync(flags, ws + lay.flags, sizeof(flags), hipMemcpyDeviceToHost, stream));
+  TDN_HIP(hipMemcpyAsync(&total, ws + lay.offs + size_t(a.N) * 4, 4, hipMemcpyDeviceToHost, stream));
+  TDN_HIP(hipStreamSynchronize(stream));
+  if (flags[0] || flags[1]) return TDN_ERR_BAD_GEOMETRY;
+  if (flags[2]) return TDN_ERR_NEIGHBOUR_LIMIT;
+  *n_edges = total;
+  if (offsets)
+    TDN_HIP(hipMemcpyAsync(offsets, ws + lay.offs, (size_t(a.N) + 1) * 4, hipMemcpyDeviceToDevice, stream));
+  if (int64_t(total) > edge_capacity) return TDN_ERR_EDGE_CAPACITY;
+  if (total > 0)
+    TDN_HIP(tdn::launch_radius_emit(a, ws, flags[4], edge_index, edge_vec, edge_image, stream));
   return TDN_OK;
 }
 

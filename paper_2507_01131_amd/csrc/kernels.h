@@ -20,6 +20,8 @@ hipError_t launch_sort(const SortPlan& plan, const int32_t* keys, int key_stride
 // offsets from keys already sorted (non-decreasing); perm = identity.
 hipError_t launch_offsets_presorted(int n_keys, int E, const int32_t* sorted_keys, int32_t* perm,
                                     int32_t* offsets, hipStream_t s);
+// Exclusive prefix sum of n ints in place (one workgroup).
+hipError_t launch_scan_exclusive(int32_t* a, int n, hipStream_t s);
 // Device-side validation; flags (3 ints, cleared by this call): [0] index
 // range, [1] dst order, [2] degenerate edge vector.
 hipError_t launch_validate(int N, int E, const int32_t* edge_index, const float* edge_vec, int check_sorted,
@@ -152,5 +154,32 @@ hipError_t launch_bwd_dst(const BwdDstArgs& a, bool x_bf16, hipStream_t s);
 int device_cus();
 hipError_t launch_sh(int L, int E, const float* edge_vec, float* Y, float* dY, hipStream_t s);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
+
+// ---------------------------------------------------------------- radius graph
+// Cell-list radius graph of a batch of systems (radius_graph.hip).
+struct RadiusGraphArgs {
+  int N, G;
+  float r_cut;
+  int max_neighbors;  // 0 = no cap
+  int periodic[3];
+  const float* pos;         // [N,3]
+  const int32_t* graph_ptr; // [G+1]
+  const float* cell;        // [G,3] (periodic axes only)
+};
+struct RadiusGraphLayout {
+  size_t params, keys, gid, perm, cell_off, spos, offs, flags, sort, total;
+  int n_keys;
+};
+RadiusGraphLayout radius_graph_layout(int N, int G);
+// Maximum candidates (atoms and images within the cutoff) of one atom.
+constexpr int kRadiusMaxNeighbours = 2048;
+// Count pass: cells, sort by cell, per-atom neighbour counts, their prefix
+// sum in ws.offs ([N+1], offs[N] = E) and the flags in ws.flags (int32:
+// [0] graph_ptr invalid, [1] geometry invalid, [2] neighbour limit exceeded,
+// [3] unused, [4] largest candidate count).
+hipError_t launch_radius_count(const RadiusGraphArgs& a, char* ws, hipStream_t s);
+// Emit pass (after the count pass on the same workspace; E = offs[N]).
+hipError_t launch_radius_emit(const RadiusGraphArgs& a, char* ws, int max_candidates, int32_t* edge_index,
+                              float* edge_vec, int32_t* edge_image, hipStream_t s);
 
 }  // namespace tdn

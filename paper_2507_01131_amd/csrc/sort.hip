@@ -156,6 +156,12 @@ SortPlan sort_plan(int n_keys, int E) {
   return p;
 }
 
+hipError_t launch_scan_exclusive(int32_t* a, int n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  k_scan_exclusive<<<dim3(1), dim3(1024), 0, s>>>(a, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t s) {
   const size_t n = bytes / 4;
   if (n == 0) return hipSuccess;

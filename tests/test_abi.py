@@ -107,8 +107,49 @@ def test_sort_and_sh_argument_checks():
     assert L.tdn_spherical_harmonics(3, 5, None, FAKE, None, None) == 1
 
 
+def _gp(N=100, G=2, r_cut=5.0, cap=0, per=(0, 0, 0)):
+    return tdn.GraphProblem(N, G, r_cut, cap, (ctypes.c_int32 * 3)(*per))
+
+
+def _rg(g, ws_bytes=1 << 40, capacity=0, **override):
+    args = dict(pos=FAKE, ptr=FAKE, cell=None, ei=None, ev=None, im=None, off=None, ws=FAKE)
+    args.update(override)
+    n = ctypes.c_int64(-1)
+    st = tdn.lib().tdn_radius_graph(None if g is None else ctypes.byref(g), args["pos"], args["ptr"], args["cell"],
+                                    capacity, args["ei"], args["ev"], args["im"], args["off"], ctypes.byref(n),
+                                    args["ws"], ws_bytes, None)
+    return st, n.value
+
+
+@pytest.mark.parametrize("g,status", [
+    (None, 1),
+    (_gp(N=-1), 2), (_gp(N=1 << 26), 2), (_gp(G=0), 2), (_gp(r_cut=0.0), 2), (_gp(r_cut=float("nan")), 2),
+    (_gp(cap=-1), 2), (_gp(per=(0, 2, 0)), 2),
+])
+def test_radius_graph_problem_checks(g, status):
+    assert _rg(g)[0] == status
+    if g is not None:
+        nb = ctypes.c_size_t()
+        assert tdn.lib().tdn_radius_graph_workspace_size(ctypes.byref(g), ctypes.byref(nb)) == status
+
+
+def test_radius_graph_argument_checks():
+    L = tdn.lib()
+    nb = ctypes.c_size_t()
+    assert L.tdn_radius_graph_workspace_size(ctypes.byref(_gp()), None) == 1
+    assert L.tdn_radius_graph_workspace_size(ctypes.byref(_gp()), ctypes.byref(nb)) == 0 and nb.value > 0
+    assert _rg(_gp(), pos=None)[0] == 1
+    assert _rg(_gp(), ptr=None)[0] == 1
+    assert _rg(_gp(), ws=None)[0] == 1
+    assert _rg(_gp(per=(1, 0, 0)))[0] == 1                    # periodic needs cell
+    assert _rg(_gp(), capacity=-5)[0] == 2
+    assert _rg(_gp(), capacity=10)[0] == 1                    # capacity without buffers
+    assert _rg(_gp(), capacity=10, ei=FAKE)[0] == 1
+    assert _rg(_gp(), ws_bytes=nb.value - 1)[0] == 4
+
+
 def test_status_strings():
-    for s in range(10):
+    for s in range(13):
         assert tdn.status_string(s)
     assert tdn.status_string(0) == "ok"
 

@@ -92,27 +92,12 @@ def test_scalar_brute_force_on_a_tiny_batch():
     assert got == want and len(want) > 10
 
 
-def _wrap(pos, L, per):
-    p = pos.copy()
-    for a in range(3):
-        if per[a]:
-            p[:, a] = np.mod(p[:, a], L[a])
-    p32 = p.astype(np.float32)
-    for a in range(3):
-        if per[a]:
-            p32[p32[:, a] >= np.float32(L[a]), a] = 0.0
-    return p32
-
-
 @pytest.mark.parametrize("name,n_dst", [("cube64_L2_C16_R32", None), ("molecules960_L3_C64_R64", None),
                                         ("slabs4960_L6_C128_R256", 400), ("bulk4096_L4_C256_R128_bf16", 200)])
 def test_matches_the_float64_fixture_builder_away_from_the_cutoff(name, n_dst):
     w = workloads.WORKLOADS[name]
-    geo = workloads.make_geometry(w)
-    per = geo["periodic"]
-    ptr = geo["graph_ptr"]
-    cell32 = geo["cell"].astype(np.float32)
-    pos32 = np.concatenate([_wrap(geo["pos"][ptr[g]:ptr[g + 1]], geo["cell"][g], per) for g in range(len(ptr) - 1)])
+    geo = workloads.graph_inputs(name)
+    per, ptr, cell32, pos32 = geo["periodic"], geo["graph_ptr"], geo["cell"], geo["pos"]
     n_all, fs, fd, fv = workloads.make_graph(w)
     rng = np.random.default_rng(0)
     dsts = np.arange(n_all) if n_dst is None else np.sort(rng.choice(n_all, n_dst, replace=False))

@@ -125,6 +125,33 @@ def make_geometry(w: Workload) -> dict:
     return dict(pos=np.concatenate(graphs), graph_ptr=ptr, cell=np.stack(cells), periodic=per, r_cut=float(w.r_cut))
 
 
+def graph_inputs(name: str) -> dict:
+    """A workload's geometry as the radius-graph builder takes it: float32
+    positions wrapped into [0, L) on periodic axes (a coordinate that rounds
+    up to L becomes 0), int32 graph_ptr, float32 cell, periodic, r_cut."""
+    g = make_geometry(WORKLOADS[name])
+    return wrap_inputs(g["pos"], g["graph_ptr"], g["cell"], g["periodic"], g["r_cut"])
+
+
+def wrap_inputs(pos, graph_ptr, cell, periodic, r_cut) -> dict:
+    ptr = np.asarray(graph_ptr, dtype=np.int64)
+    cell = np.asarray(cell, dtype=np.float64).reshape(len(ptr) - 1, 3)
+    p = np.array(pos, dtype=np.float64)
+    for k in range(len(ptr) - 1):
+        for a in range(3):
+            if periodic[a]:
+                p[ptr[k]:ptr[k + 1], a] = np.mod(p[ptr[k]:ptr[k + 1], a], cell[k, a])
+    p32 = p.astype(np.float32)
+    cell32 = cell.astype(np.float32)
+    for k in range(len(ptr) - 1):
+        for a in range(3):
+            if periodic[a]:
+                col = p32[ptr[k]:ptr[k + 1], a]
+                col[col >= cell32[k, a]] = 0.0
+    return dict(pos=p32, graph_ptr=ptr.astype(np.int32), cell=cell32, periodic=tuple(bool(x) for x in periodic),
+                r_cut=float(r_cut))
+
+
 def make_graph(w: Workload):
     """Returns (n_nodes, src, dst, edge_vec) for a workload (float64 vectors):
     the radius graph of every graph of ``make_geometry``, concatenated."""
