@@ -108,6 +108,8 @@ def main():
     ap.add_argument("--backward", action="store_true", help="also time tdn_cp_tp_backward (extra field)")
     ap.add_argument("--ablation-atomics", action="store_true",
                     help="also time the atomic scatter-add forward (extra field; fp32 workloads with 2 <= L <= 4)")
+    ap.add_argument("--radius-graph", action="store_true",
+                    help="also time tdn_radius_graph on the workload's geometry (extra field)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 256 MiB device copy (reference for rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -241,6 +243,35 @@ def main():
             "edge_kernel_ms": a_ms / max(1, a_n), "segmented_edge_kernel_ms": edge_ms,
             "edge_kernel_slowdown": a_ms / max(1, a_n) / edge_ms,
             "ms_per_step": a_step, "value": E / (a_step * 1e-3)}
+    if args.radius_graph:
+        # the edges of this workload rebuilt on the device from its atoms
+        gi = workloads.graph_inputs(w["name"])
+        per = gi["periodic"]
+        gp, gg, gc = t(gi["pos"]), t(gi["graph_ptr"]), t(gi["cell"]) if any(per) else None
+        first = tdn.radius_graph(gp, gg, r_cut=gi["r_cut"], cell=gc, periodic=per)
+        E_rg = first.edge_index.shape[1]
+
+        def build_graph():
+            return tdn.radius_graph(gp, gg, r_cut=gi["r_cut"], cell=gc, periodic=per, capacity=E_rg)
+
+        for _ in range(3):
+            build_graph()
+        torch.cuda.synchronize()
+        tdn.timer_enable(True)
+        tdn.timer_read("radius_graph", reset=True)
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            build_graph()
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) / args.steps
+        tdn.timer_enable(False)
+        g_ms, g_n = tdn.timer_read("radius_graph", reset=True)
+        n_at = gi["pos"].shape[0]
+        line["radius_graph"] = {
+            "atoms": n_at, "systems": len(gi["graph_ptr"]) - 1, "r_cut": gi["r_cut"], "periodic": list(per),
+            "edges": E_rg, "edges_match_fixture": E_rg == E, "ms_per_call_wall": wall * 1e3,
+            "ms_per_call_events": g_ms / max(1, g_n), "edges_per_s": E_rg / wall,
+            "algorithmic_bytes": 12 * n_at + 20 * E_rg + 4 * (n_at + 1)}
     if args.backward:
         G = torch.from_numpy(w["grad_out"]).to(dev)
         wsb = torch.empty(bwd_bytes, dtype=torch.uint8, device=dev)

@@ -167,16 +167,16 @@ struct RadiusGraphArgs {
   const float* cell;        // [G,3] (periodic axes only)
 };
 struct RadiusGraphLayout {
-  size_t params, keys, gid, perm, cell_off, spos, offs, flags, sort, total;
+  size_t params, keys, gid, rank, flags, cell_off, spos, offs, tot, total;
   int n_keys;
 };
 RadiusGraphLayout radius_graph_layout(int N, int G);
 // Maximum candidates (atoms and images within the cutoff) of one atom.
 constexpr int kRadiusMaxNeighbours = 2048;
-// Count pass: cells, sort by cell, per-atom neighbour counts, their prefix
-// sum in ws.offs ([N+1], offs[N] = E) and the flags in ws.flags (int32:
-// [0] graph_ptr invalid, [1] geometry invalid, [2] neighbour limit exceeded,
-// [3] unused, [4] largest candidate count).
+// Count pass: cells, atoms in cell order, per-atom neighbour counts, their
+// prefix sum in ws.offs ([N+1], offs[N] = E) and the flags in ws.flags
+// (int32: [0] graph_ptr invalid, [1] geometry invalid, [2] neighbour limit
+// exceeded, [3] unused, [4] largest candidate count).
 hipError_t launch_radius_count(const RadiusGraphArgs& a, char* ws, hipStream_t s);
 // Emit pass (after the count pass on the same workspace; E = offs[N]).
 hipError_t launch_radius_emit(const RadiusGraphArgs& a, char* ws, int max_candidates, int32_t* edge_index,

@@ -20,14 +20,16 @@
 // rounding of the cell coordinate, whose error stays below 1024 * 2^-23 cell
 // widths); adjacency wraps on periodic axes, the wrap giving the image.  Cell
 // ids are system-major (system g's cells start at 2 ptr[g] + g, so no
-// prefix sum over systems is needed); atoms are ordered by cell with the
-// library's stable radix sort, whose offsets are the cell ranges.
+// prefix sum over systems is needed); atoms are placed in cell order by a
+// counting scatter (atomic per-cell counts, their prefix sum, one scatter).
 //
-// Passes: per-system grids; per-atom cell ids; the sort; positions in cell
-// order; a count pass (one wave per destination over the 27 adjacent cells);
-// its prefix sum; and an emit pass (one wave per destination) that gathers
-// the candidates into LDS, sorts them there (bitonic; first by (|r|^2, key)
-// when the cap binds) and writes the edges.
+// Passes: per-system grids; per-atom cell ids and cell counts; their prefix
+// sum; positions in cell order; a count pass (one wave per destination, the
+// 27 adjacent cells flattened over the lanes); a prefix sum of the kept
+// counts with their maximum; and an emit pass (one wave per destination)
+// that gathers the candidates into LDS, sorts them there (bitonic; first by
+// (|r|^2, key) when the cap binds) and writes the edges in (src, image)
+// order, so the output does not depend on the order of atoms inside a cell.
 #include "common.hpp"
 #include "kernels.h"
 
@@ -137,9 +139,13 @@ __device__ __forceinline__ int cell_coord(float x, float lo, float inv, int n) {
   return min(c, n - 1);
 }
 
-// One thread per atom: its system (binary search over graph_ptr) and cell id.
+// One thread per atom: its system (binary search over graph_ptr), cell id,
+// and a slot in the cell (the cell's atom count, zeroed beforehand, counted
+// up with atomics: the order inside a cell is arbitrary, which the emit
+// pass's sort makes irrelevant).
 __global__ __launch_bounds__(256) void k_rg_keys(RadiusGraphArgs a, const GridParams* __restrict__ params,
                                                  int n_keys, int32_t* __restrict__ keys, int32_t* __restrict__ gid,
+                                                 int32_t* __restrict__ cell_cnt, int32_t* __restrict__ rank,
                                                  int32_t* __restrict__ flags) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= a.N) return;
@@ -160,17 +166,22 @@ __global__ __launch_bounds__(256) void k_rg_keys(RadiusGraphArgs a, const GridPa
     c[k] = cell_coord(p[k], P.lo[k], P.inv[k], P.n[k]);
   }
   if (bad) atomicOr(&flags[1], 1);
-  const int key = P.base + (c[2] * P.n[1] + c[1]) * P.n[0] + c[0];
-  keys[i] = min(max(key, 0), n_keys - 1);
+  const int key = min(max(P.base + (c[2] * P.n[1] + c[1]) * P.n[0] + c[0], 0), n_keys - 1);
+  keys[i] = key;
   gid[i] = g;
+  rank[i] = atomicAdd(&cell_cnt[key], 1);
 }
 
-// Positions in cell order, the atom id in .w.
-__global__ __launch_bounds__(256) void k_rg_sorted(int N, const float* __restrict__ pos,
-                                                   const int32_t* __restrict__ perm, float4* __restrict__ spos) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= N) return;
-  const int i = perm[j];
+// Positions in cell order (cell_off: exclusive prefix of the cell counts),
+// the atom id in .w.
+__global__ __launch_bounds__(256) void k_rg_scatter(int N, const float* __restrict__ pos,
+                                                    const int32_t* __restrict__ keys,
+                                                    const int32_t* __restrict__ rank,
+                                                    const int32_t* __restrict__ cell_off,
+                                                    float4* __restrict__ spos) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= N) return;
+  const int j = cell_off[keys[i]] + rank[i];
   spos[j] = make_float4(pos[3 * size_t(i)], pos[3 * size_t(i) + 1], pos[3 * size_t(i) + 2], __int_as_float(i));
 }
 
@@ -199,77 +210,133 @@ __device__ __forceinline__ DstCtx dst_ctx(const RadiusGraphArgs& a, const GridPa
   return d;
 }
 
-// Calls visit(hit, key, r2, rx, ry, rz) once per candidate slot of the wave
-// (all lanes together; hit false on idle lanes), over the 27 adjacent cells
-// in a fixed order.  key = src * 32 + image code.
+// Calls visit(hit, key, r2) once per candidate slot of the wave (all lanes
+// together, hit false on idle lanes).  The 27 adjacent cells are flattened
+// into one slot range: lane k < 27 takes cell k (its atom range, image and
+// whether it exists), a lane prefix sum gives each cell's first slot, and
+// each slot finds its cell by a five-step search over the prefix.  Wraps on
+// periodic axes give the image; cells past a non-periodic edge are empty.
+// key = src * 32 + image code.
 template <typename Visit>
 __device__ __forceinline__ void for_each_candidate(const RadiusGraphArgs& a, const DstCtx& d,
                                                    const int32_t* __restrict__ cell_off, int n_keys,
                                                    const float4* __restrict__ spos, float rc2, int lane,
                                                    Visit&& visit) {
-  for (int oz = -1; oz <= 1; ++oz)
-    for (int oy = -1; oy <= 1; ++oy)
-      for (int ox = -1; ox <= 1; ++ox) {
-        const int o[3] = {ox, oy, oz};
-        int cc[3], img[3];
-        bool skip = false;
+  int beg = 0, cnt = 0, code = 13;
+  if (lane < 27) {
+    const int o[3] = {lane % 3 - 1, (lane / 3) % 3 - 1, lane / 9 - 1};
+    int cc[3], img[3];
+    bool skip = false;
 #pragma unroll
-        for (int k = 0; k < 3; ++k) {
-          int v = d.c[k] + o[k];
-          img[k] = 0;
-          if (a.periodic[k]) {
-            if (v < 0) { v += d.P.n[k]; img[k] = -1; }
-            else if (v >= d.P.n[k]) { v -= d.P.n[k]; img[k] = 1; }
-          } else if (v < 0 || v >= d.P.n[k]) {
-            skip = true;
-          }
-          cc[k] = v;
-        }
-        if (skip) continue;
-        const int key = min(max(d.P.base + (cc[2] * d.P.n[1] + cc[1]) * d.P.n[0] + cc[0], 0), n_keys - 1);
-        const int beg = cell_off[key], end = cell_off[key + 1];
-        const float sx = float(img[0]) * d.P.L[0], sy = float(img[1]) * d.P.L[1], sz = float(img[2]) * d.P.L[2];
-        const bool self_img = img[0] == 0 && img[1] == 0 && img[2] == 0;
-        const int code = (img[0] + 1) * 9 + (img[1] + 1) * 3 + (img[2] + 1);
-        for (int jb = beg; jb < end; jb += kWave) {
-          const int j = jb + lane;
-          bool hit = false;
-          uint32_t ekey = 0;
-          float r2 = 0.f, rx = 0.f, ry = 0.f, rz = 0.f;
-          if (j < end) {
-            const float4 q = spos[j];
-            const int src = __float_as_int(q.w);
-            rx = __fadd_rn(__fsub_rn(q.x, d.px), sx);
-            ry = __fadd_rn(__fsub_rn(q.y, d.py), sy);
-            rz = __fadd_rn(__fsub_rn(q.z, d.pz), sz);
-            r2 = __fadd_rn(__fadd_rn(__fmul_rn(rx, rx), __fmul_rn(ry, ry)), __fmul_rn(rz, rz));
-            hit = r2 < rc2 && !(self_img && src == d.i);
-            ekey = uint32_t(src) * 32u + uint32_t(code);
-          }
-          visit(hit, ekey, r2, rx, ry, rz);
-        }
+    for (int k = 0; k < 3; ++k) {
+      int v = d.c[k] + o[k];
+      img[k] = 0;
+      if (a.periodic[k]) {
+        if (v < 0) { v += d.P.n[k]; img[k] = -1; }
+        else if (v >= d.P.n[k]) { v -= d.P.n[k]; img[k] = 1; }
+      } else if (v < 0 || v >= d.P.n[k]) {
+        skip = true;
       }
+      cc[k] = v;
+    }
+    if (!skip) {
+      const int key = min(max(d.P.base + (cc[2] * d.P.n[1] + cc[1]) * d.P.n[0] + cc[0], 0), n_keys - 1);
+      beg = cell_off[key];
+      cnt = cell_off[key + 1] - beg;
+    }
+    code = (img[0] + 1) * 9 + (img[1] + 1) * 3 + (img[2] + 1);
+  }
+  int incl = cnt;
+#pragma unroll
+  for (int o = 1; o < 32; o <<= 1) {
+    const int t = __shfl_up(incl, o);
+    if (lane >= o) incl += t;
+  }
+  const int excl = incl - cnt;
+  const int total = __shfl(incl, 26);
+  for (int sb = 0; sb < total; sb += kWave) {
+    const int slot = sb + lane;
+    int c = 0;  // cells before the slot's: lanes k < 27 with incl[k] <= slot
+#pragma unroll
+    for (int step = 16; step > 0; step >>= 1) {
+      const int v = __shfl(incl, min(c + step - 1, 26));
+      if (c + step <= 27 && v <= slot) c += step;
+    }
+    c = min(c, 26);
+    const int cb = __shfl(beg, c), ce = __shfl(excl, c), cd = __shfl(code, c);
+    bool hit = false;
+    uint32_t ekey = 0;
+    float r2 = 0.f;
+    if (slot < total) {
+      const float4 q = spos[cb + (slot - ce)];
+      const int src = __float_as_int(q.w);
+      const float sx = float(cd / 9 - 1) * d.P.L[0], sy = float((cd / 3) % 3 - 1) * d.P.L[1],
+                  sz = float(cd % 3 - 1) * d.P.L[2];
+      const float rx = __fadd_rn(__fsub_rn(q.x, d.px), sx);
+      const float ry = __fadd_rn(__fsub_rn(q.y, d.py), sy);
+      const float rz = __fadd_rn(__fsub_rn(q.z, d.pz), sz);
+      r2 = __fadd_rn(__fadd_rn(__fmul_rn(rx, rx), __fmul_rn(ry, ry)), __fmul_rn(rz, rz));
+      hit = r2 < rc2 && !(cd == 13 && src == d.i);
+      ekey = uint32_t(src) * 32u + uint32_t(cd);
+    }
+    visit(hit, ekey, r2);
+  }
 }
 
-// One wave per destination atom: candidates within the cutoff.
+// One wave per destination atom: candidates within the cutoff (tot) and the
+// edges kept (offs, before the prefix sum).
 __global__ __launch_bounds__(256) void k_rg_count(RadiusGraphArgs a, const GridParams* __restrict__ params,
                                                   const int32_t* __restrict__ keys, const int32_t* __restrict__ gid,
                                                   const int32_t* __restrict__ cell_off, int n_keys,
                                                   const float4* __restrict__ spos, float rc2,
-                                                  int32_t* __restrict__ offs, int32_t* __restrict__ flags) {
-  if (blockIdx.x == 0 && threadIdx.x == 0) offs[a.N] = 0;
+                                                  int32_t* __restrict__ offs, int32_t* __restrict__ tot) {
   const int lane = threadIdx.x & (kWave - 1);
   const int i = __builtin_amdgcn_readfirstlane(int(blockIdx.x * 4 + threadIdx.x / kWave));
   if (i >= a.N) return;
   const DstCtx d = dst_ctx(a, params, keys, gid, i);
   int total = 0;
   for_each_candidate(a, d, cell_off, n_keys, spos, rc2, lane,
-                     [&](bool hit, uint32_t, float, float, float, float) { total += __popcll(__ballot(hit)); });
+                     [&](bool hit, uint32_t, float) { total += __popcll(__ballot(hit)); });
   if (lane == 0) {
-    const int keep = a.max_neighbors > 0 ? min(total, a.max_neighbors) : total;
-    offs[i] = keep;
-    if (total > kRadiusMaxNeighbours) atomicOr(&flags[2], 1);
-    atomicMax(&flags[4], total);
+    offs[i] = a.max_neighbors > 0 ? min(total, a.max_neighbors) : total;
+    tot[i] = total;
+  }
+}
+
+// One workgroup: offs[0..N-1] -> exclusive prefix sum with offs[N] = E, and
+// the largest candidate count and the neighbour-limit flag into flags.
+__global__ __launch_bounds__(1024) void k_rg_scan(int N, int32_t* __restrict__ offs,
+                                                  const int32_t* __restrict__ tot, int32_t* __restrict__ flags) {
+  __shared__ int32_t part[1024], pmax[1024];
+  const int t = threadIdx.x;
+  const int per = (N + 1023) / 1024;
+  const int lo = min(N, t * per), hi = min(N, lo + per);
+  int32_t sum = 0, mx = 0;
+  for (int i = lo; i < hi; ++i) {
+    sum += offs[i];
+    mx = max(mx, tot[i]);
+  }
+  part[t] = sum;
+  pmax[t] = mx;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int32_t v = t >= off ? part[t - off] : 0;
+    const int32_t m = t >= off ? pmax[t - off] : 0;
+    __syncthreads();
+    part[t] += v;
+    pmax[t] = max(pmax[t], m);
+    __syncthreads();
+  }
+  int32_t run = part[t] - sum;
+  for (int i = lo; i < hi; ++i) {
+    const int32_t v = offs[i];
+    offs[i] = run;
+    run += v;
+  }
+  if (t == 1023) {
+    offs[N] = part[1023];
+    flags[4] = pmax[1023];
+    flags[2] = pmax[1023] > kRadiusMaxNeighbours;
   }
 }
 
@@ -307,7 +374,7 @@ __global__ __launch_bounds__(kWave) void k_rg_emit(RadiusGraphArgs a, const Grid
   int n = 0;
   const bool capped = a.max_neighbors > 0;
   for_each_candidate(a, d, cell_off, n_keys, spos, rc2, lane,
-                     [&](bool hit, uint32_t key, float r2, float, float, float) {
+                     [&](bool hit, uint32_t key, float r2) {
                        const uint64_t m = __ballot(hit);
                        if (hit) {
                          const int pos = n + __popcll(m & ((1ull << lane) - 1));
@@ -358,12 +425,12 @@ RadiusGraphLayout radius_graph_layout(int N, int G) {
   l.params = o; o += al(size_t(G) * sizeof(GridParams));
   l.keys = o; o += al(size_t(N) * 4);
   l.gid = o; o += al(size_t(N) * 4);
-  l.perm = o; o += al(size_t(N) * 4);
+  l.rank = o; o += al(size_t(N) * 4);
+  l.flags = o; o += 256;  // flags, then the cell counts: cleared together
   l.cell_off = o; o += al((size_t(l.n_keys) + 1) * 4);
   l.spos = o; o += al(size_t(N) * 16);
   l.offs = o; o += al((size_t(N) + 1) * 4);
-  l.flags = o; o += 256;
-  l.sort = o; o += al(sort_plan(l.n_keys, N).bytes);
+  l.tot = o; o += al(size_t(N) * 4);
   l.total = o;
   return l;
 }
@@ -371,30 +438,34 @@ RadiusGraphLayout radius_graph_layout(int N, int G) {
 hipError_t launch_radius_count(const RadiusGraphArgs& a, char* ws, hipStream_t s) {
   const RadiusGraphLayout l = radius_graph_layout(a.N, a.G);
   int32_t* flags = reinterpret_cast<int32_t*>(ws + l.flags);
-  hipError_t e = launch_zero(flags, 64, s);
-  if (e != hipSuccess) return e;
   int32_t* offs = reinterpret_cast<int32_t*>(ws + l.offs);
-  if (a.N == 0) return launch_zero(offs, 4, s);
+  if (a.N == 0) {
+    hipError_t e = launch_zero(flags, 64, s);
+    return e != hipSuccess ? e : launch_zero(offs, 4, s);
+  }
+  // flags and cell counts are adjacent: one clear
+  hipError_t e = launch_zero(flags, 256 + (size_t(l.n_keys) + 1) * 4, s);
+  if (e != hipSuccess) return e;
   auto* params = reinterpret_cast<GridParams*>(ws + l.params);
   auto* keys = reinterpret_cast<int32_t*>(ws + l.keys);
   auto* gid = reinterpret_cast<int32_t*>(ws + l.gid);
-  auto* perm = reinterpret_cast<int32_t*>(ws + l.perm);
+  auto* rank = reinterpret_cast<int32_t*>(ws + l.rank);
   auto* cell_off = reinterpret_cast<int32_t*>(ws + l.cell_off);
   auto* spos = reinterpret_cast<float4*>(ws + l.spos);
+  auto* tot = reinterpret_cast<int32_t*>(ws + l.tot);
   const unsigned nb = unsigned((a.N + 255) / 256);
   k_rg_grid<<<dim3(a.G), dim3(256), 0, s>>>(a, params, flags);
-  k_rg_keys<<<dim3(nb), dim3(256), 0, s>>>(a, params, l.n_keys, keys, gid, flags);
+  k_rg_keys<<<dim3(nb), dim3(256), 0, s>>>(a, params, l.n_keys, keys, gid, cell_off, rank, flags);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = launch_sort(sort_plan(l.n_keys, a.N), keys, 1, perm, cell_off, ws + l.sort, s);
+  e = launch_scan_exclusive(cell_off, l.n_keys + 1, s);
   if (e != hipSuccess) return e;
-  k_rg_sorted<<<dim3(nb), dim3(256), 0, s>>>(a.N, a.pos, perm, spos);
+  k_rg_scatter<<<dim3(nb), dim3(256), 0, s>>>(a.N, a.pos, keys, rank, cell_off, spos);
   const float rc2 = a.r_cut * a.r_cut;
   k_rg_count<<<dim3(unsigned((a.N + 3) / 4)), dim3(256), 0, s>>>(a, params, keys, gid, cell_off, l.n_keys, spos,
-                                                                   rc2, offs, flags);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return launch_scan_exclusive(offs, a.N + 1, s);
+                                                                   rc2, offs, tot);
+  k_rg_scan<<<dim3(1), dim3(1024), 0, s>>>(a.N, offs, tot, flags);
+  return hipGetLastError();
 }
 
 hipError_t launch_radius_emit(const RadiusGraphArgs& a, char* ws, int max_candidates, int32_t* edge_index,
