@@ -101,9 +101,10 @@ def forward(x, edge_index, edge_vec, A, B, D, W, radial_w, r_cut, L,
 
 # ----------------------------------------------------------------- backward
 def backward(x, edge_index, edge_vec, A, B, D, W, radial_w, r_cut, L, grad_out,
-             perm=None):
+             perm=None, return_radial=False):
     """Returns (grad_x [N,d,C], grad_W [C,C], grad_edge_vec [E,3]) for the
-    scalar <grad_out, out>."""
+    scalar <grad_out, out>, and with return_radial also grad_radial_w
+    [n_radial, R] (rho_e = phi_e Wrad, so dL/dWrad = sum_e phi_e^T drho_e)."""
     x, A, B, D, W, G = _f64(x, A, B, D, W, grad_out)
     Wrad = np.asarray(radial_w, np.float64)
     N, d, C = x.shape
@@ -116,6 +117,7 @@ def backward(x, edge_index, edge_vec, A, B, D, W, radial_w, r_cut, L, grad_out,
     grad_x = np.zeros_like(x)
     grad_W = np.zeros((C, C))
     grad_vec = np.zeros((E, 3))
+    grad_wrad = np.zeros_like(Wrad)
     for c0 in range(0, E, CHUNK):
         ids = perm[c0:c0 + CHUNK]
         vec = np.asarray(edge_vec, np.float64)[ids]
@@ -134,12 +136,15 @@ def backward(x, edge_index, edge_vec, A, B, D, W, radial_w, r_cut, L, grad_out,
         dg = np.sum(Gh * u, axis=2)                        # dL/dg  [e, R]
         dv = dg * rho
         drho = dg * v
+        grad_wrad += phi.T @ drho                          # [n, R]
         dY = dv @ B.T                                      # [e, d]
         dphi_w = drho @ Wrad.T                             # dL/dphi [e, n]
         J = spherical_harmonics_jacobian(L, vec)           # [e, d, 3]
         gv = np.einsum("ek,ekx->ex", dY, J)
         gv += (np.sum(dphi_w * dphi, axis=1) / dist)[:, None] * vec
         grad_vec[ids] = gv
+    if return_radial:
+        return grad_x, grad_W, grad_vec, grad_wrad
     return grad_x, grad_W, grad_vec
 
 

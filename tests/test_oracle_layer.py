@@ -144,15 +144,23 @@ def test_backward_finite_differences():
     L = 2
     ei = w["edge_index"]
 
-    def loss(x=None, W=None, vec=None):
+    def loss(x=None, W=None, vec=None, Wr=None):
         o = layer.forward(f["x"] if x is None else x, ei, f["edge_vec"] if vec is None else vec, A, B, D,
-                          f["W"] if W is None else W, f["radial_w"], w["r_cut"], L)
+                          f["W"] if W is None else W, f["radial_w"] if Wr is None else Wr, w["r_cut"], L)
         return np.sum(o * f["grad_out"])
 
-    gx, gW, gv = layer.backward(f["x"], ei, f["edge_vec"], A, B, D, f["W"], f["radial_w"], w["r_cut"], L,
-                                f["grad_out"])
+    gx, gW, gv, gr = layer.backward(f["x"], ei, f["edge_vec"], A, B, D, f["W"], f["radial_w"], w["r_cut"], L,
+                                    f["grad_out"], return_radial=True)
     h = 1e-6
     rng = np.random.default_rng(0)
+    assert gr.shape == f["radial_w"].shape
+    for q in range(gr.shape[0]):
+        for r in range(0, gr.shape[1], 5):
+            Rp, Rm = f["radial_w"].astype(np.float64), f["radial_w"].astype(np.float64)
+            Rp[q, r] += h
+            Rm[q, r] -= h
+            fd = (loss(Wr=Rp) - loss(Wr=Rm)) / (2 * h)
+            assert abs(fd - gr[q, r]) < 1e-6 * max(1, abs(gr[q, r])), (q, r, fd, gr[q, r])
     for _ in range(6):
         idx = tuple(rng.integers(0, s) for s in f["x"].shape)
         xp, xm = f["x"].copy(), f["x"].copy()
