@@ -105,7 +105,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="molecules3200_L4_C128_R128")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--backward", action="store_true", help="also time tdn_cp_tp_backward (extra field)")
+    ap.add_argument("--backward", action="store_true", help="also time tdn_cp_tp_backward with every gradient (x, W, edge vectors, radial weights; extra field)")
     ap.add_argument("--ablation-atomics", action="store_true",
                     help="also time the atomic scatter-add forward (extra field; fp32 workloads with 2 <= L <= 4)")
     ap.add_argument("--radius-graph", action="store_true",
@@ -285,15 +285,16 @@ def main():
         G = torch.from_numpy(w["grad_out"]).to(dev)
         wsb = torch.empty(bwd_bytes, dtype=torch.uint8, device=dev)
         for _ in range(3):
-            tdn.backward(res, G, workspace=wsb)
+            tdn.backward(res, G, workspace=wsb, need_radial=True)
         torch.cuda.synchronize()
-        bk = ("node_gemm", "gram", "channel_layout", "cp_bwd_dst", "sort", "feature_layout", "cp_edge_bwd_src")
+        bk = ("node_gemm", "gram", "channel_layout", "cp_bwd_dst", "radial_grad", "sort", "feature_layout",
+              "cp_edge_bwd_src")
         tdn.timer_enable(True)
         for k in bk:
             tdn.timer_read(k, reset=True)
         ev0.record()
         for _ in range(10):
-            tdn.backward(res, G, workspace=wsb)
+            tdn.backward(res, G, workspace=wsb, need_radial=True)
         ev1.record()
         torch.cuda.synchronize()
         tdn.timer_enable(False)

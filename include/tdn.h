@@ -133,17 +133,20 @@ tdn_status tdn_ablation_forward_atomics(const tdn_problem* p, const void* x, con
  * forward's outputs; z_save is the forward's saved Z or NULL (then Z is
  * recomputed).  Each gradient pointer may be NULL to skip it; grads are f32
  * for any feat_dtype:
- *   grad_x        [N, d, C]  dL/dx
- *   grad_W        [C, C]     dL/dW
- *   grad_edge_vec [E, 3]     dL/dr_e, in the caller's original edge order
- * The factors and radial_w are constants (no gradient). */
+ *   grad_x        [N, d, C]         dL/dx
+ *   grad_W        [C, C]            dL/dW
+ *   grad_edge_vec [E, 3]            dL/dr_e, in the caller's original edge order
+ *   grad_radial_w [n_radial, R]     dL/dWrad = sum_e phi_e^T (dL/dg_e * v_e),
+ *                                   summed in a fixed order (deterministic)
+ * The CP factors are constants (no gradient; the paper caches them once per
+ * L and keeps them fixed in training, Sec. 4.1). */
 tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* edge_vec,
                               const int32_t* edge_index, const float* A, const float* B,
                               const float* D, const void* W, const float* radial_w,
                               const int32_t* perm, const int32_t* offsets, const float* z_save,
                               const float* grad_out, float* grad_x, float* grad_W,
-                              float* grad_edge_vec, void* workspace, size_t workspace_bytes,
-                              hipStream_t stream);
+                              float* grad_edge_vec, float* grad_radial_w, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream);
 
 /* Radius graph of a batch of atomic systems (App. "Model and Training
  * Configurations": the edges are built on the fly from a cutoff, with a cap
@@ -216,7 +219,8 @@ tdn_status tdn_spherical_harmonics(int32_t L, int32_t E, const float* edge_vec, 
  * tdn_timer_enable(1) starts recording every launch of the layer's edge
  * kernels; tdn_timer_read synchronises on the recorded events and returns
  * the summed milliseconds and launch count of the kernel named `kernel`
- * ("cp_edge_fwd", "cp_edge_fwd_atomic", "radius_graph", "feature_layout", "channel_layout", "cp_edge_bwd_src", "cp_bwd_dst", "node_gemm", "gram",
+ * ("cp_edge_fwd", "cp_edge_fwd_atomic", "radius_graph", "feature_layout",
+ * "channel_layout", "cp_edge_bwd_src", "cp_bwd_dst", "radial_grad", "node_gemm", "gram",
  * "sort");
  * reset = 1 clears that kernel's record. */
 tdn_status tdn_timer_enable(int32_t enable);

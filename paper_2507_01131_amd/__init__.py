@@ -68,7 +68,7 @@ def lib() -> ctypes.CDLL:
         L.tdn_workspace_size.argtypes = [PP, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)]
         L.tdn_cp_tp_forward.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
         L.tdn_ablation_forward_atomics.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
-        L.tdn_cp_tp_backward.argtypes = [PP] + [_P] * 16 + [_SZ, _P]
+        L.tdn_cp_tp_backward.argtypes = [PP] + [_P] * 17 + [_SZ, _P]
         GP = ctypes.POINTER(GraphProblem)
         L.tdn_radius_graph_workspace_size.argtypes = [GP, ctypes.POINTER(_SZ)]
         L.tdn_radius_graph.argtypes = [GP, _P, _P, _P, ctypes.c_int64, _P, _P, _P, _P,
@@ -194,10 +194,11 @@ def forward(x, edge_vec, edge_index, A, B, D, W, radial_w, *, L: int, r_cut: flo
                          dict(x=x, edge_vec=edge_vec, edge_index=edge_index, A=A, B=B, D=D, W=W, radial_w=radial_w))
 
 
-def backward(res: ForwardResult, grad_out, *, need_x=True, need_W=True, need_vec=True, use_saved_z=True,
-             workspace=None, stream=None):
+def backward(res: ForwardResult, grad_out, *, need_x=True, need_W=True, need_vec=True, need_radial=False,
+             use_saved_z=True, workspace=None, stream=None):
     """Runs tdn_cp_tp_backward; returns (grad_x, grad_W, grad_edge_vec), each
-    float32 or None."""
+    float32 or None, and grad_radial_w [n_radial, R] as a fourth value when
+    need_radial is set."""
     i = res.inputs
     x = i["x"]
     dev = x.device
@@ -211,13 +212,14 @@ def backward(res: ForwardResult, grad_out, *, need_x=True, need_W=True, need_vec
     gx = torch.empty((N, d, C), dtype=torch.float32, device=dev) if need_x else None
     gW = torch.empty((C, C), dtype=torch.float32, device=dev) if need_W else None
     gv = torch.empty((E, 3), dtype=torch.float32, device=dev) if need_vec else None
+    gr = torch.empty(tuple(i["radial_w"].shape), dtype=torch.float32, device=dev) if need_radial else None
     z = res.z if use_saved_z else None
     st = lib().tdn_cp_tp_backward(ctypes.byref(p), _ptr(x), _ptr(i["edge_vec"]), _ptr(i["edge_index"]), _ptr(i["A"]),
                                   _ptr(i["B"]), _ptr(i["D"]), _ptr(i["W"]), _ptr(i["radial_w"]), _ptr(res.perm),
                                   _ptr(res.offsets), _ptr(z), _ptr(grad_out), _ptr(gx), _ptr(gW), _ptr(gv),
-                                  _ptr(workspace), workspace.numel(), _stream(stream))
+                                  _ptr(gr), _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, "tdn_cp_tp_backward")
-    return gx, gW, gv
+    return (gx, gW, gv, gr) if need_radial else (gx, gW, gv)
 
 
 def sort_by_key(keys: torch.Tensor, n_keys: int, stream=None):

@@ -111,7 +111,7 @@ FwdLayout fwd_layout(const tdn_problem& p) {
 }
 
 struct BwdLayout {
-  size_t gz, z, xt, part, parts, perm_src, off_src, sort, wp, flags, total;
+  size_t gz, z, xt, part, parts, perm_src, off_src, sort, wp, drho, wrad_part, gv, flags, total;
 };
 BwdLayout bwd_layout(const tdn_problem& p) {
   BwdLayout b{};
@@ -135,6 +135,12 @@ BwdLayout bwd_layout(const tdn_problem& p) {
   o += al(tdn::sort_plan(p.n_nodes, p.n_edges).bytes);
   b.wp = o;
   o += al(tdn::node_gemm_ws_bytes(p.C));
+  b.drho = o;  // radial-weight gradient: dL/drho per edge, block partials, and a
+  o += al(size_t(p.n_edges) * p.R * 4);  // grad_edge_vec stand-in when only grad_radial_w is asked for
+  b.wrad_part = o;
+  o += al(size_t(tdn::radial_grad_blocks(p.n_edges)) * p.n_radial * p.R * 4);
+  b.gv = o;
+  o += al(size_t(p.n_edges) * 12);
   b.flags = o;
   o += 256;
   b.total = o;
@@ -358,7 +364,8 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
                               const float* A, const float* B, const float* D, const void* W, const float* radial_w,
                               const int32_t* perm, const int32_t* offsets, const float* z_save,
                               const float* grad_out, float* grad_x, float* grad_W, float* grad_edge_vec,
-                              void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                              float* grad_radial_w, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
   tdn_status st = check_problem(p);
   if (st != TDN_OK) return st;
   const int N = p->n_nodes, E = p->n_edges, d = dim_of(p->L), C = p->C;
@@ -377,6 +384,9 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
   const bool bf16 = p->feat_dtype == TDN_BF16;
   const int32_t* src = edge_index;
   const int32_t* dst = E > 0 ? edge_index + E : nullptr;
+  if (N == 0 || E == 0) {
+    if (grad_radial_w) TDN_HIP(tdn::launch_zero(grad_radial_w, size_t(p->n_radial) * p->R * 4, stream));
+  }
   if (N == 0) {
     if (grad_W) TDN_HIP(tdn::launch_zero(grad_W, size_t(C) * C * 4, stream));
     return TDN_OK;
@@ -397,7 +407,7 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
     Timed t("gram", stream);
     TDN_HIP(tdn::launch_gram(N * d, C, Z, grad_out, bf16, reinterpret_cast<float*>(ws + lay.parts), grad_W, stream));
   }
-  if (grad_edge_vec && E > 0) {
+  if ((grad_edge_vec || grad_radial_w) && E > 0) {
     tdn::BwdDstArgs a{};
     a.n_seg = N;
     a.E = E;
@@ -417,7 +427,8 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
     a.radial_w = radial_w;
     a.x = x;
     a.Gz = Gz;
-    a.grad_vec = grad_edge_vec;
+    a.grad_vec = grad_edge_vec ? grad_edge_vec : reinterpret_cast<float*>(ws + lay.gv);
+    a.drho = grad_radial_w ? reinterpret_cast<float*>(ws + lay.drho) : nullptr;
     a.dst = dst;
     const tdn::EdgePlan dp = tdn::bwd_dst_plan(p->L, p->R, C, p->n_radial, bf16, E);
     a.n_range = dp.n_range;
@@ -442,8 +453,15 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
       a.xc = ws + lay.xt;
       a.x_scale = bf16 ? nullptr : xscale;
     }
-    Timed t("cp_bwd_dst", stream);
-    TDN_HIP(tdn::launch_bwd_dst(a, bf16, stream));
+    {
+      Timed t("cp_bwd_dst", stream);
+      TDN_HIP(tdn::launch_bwd_dst(a, bf16, stream));
+    }
+    if (grad_radial_w) {
+      Timed t("radial_grad", stream);
+      TDN_HIP(tdn::launch_radial_grad(E, p->R, p->n_radial, a.sigma, edge_vec, a.drho,
+                                      reinterpret_cast<float*>(ws + lay.wrad_part), grad_radial_w, stream));
+    }
   }
   if (grad_x) {
     int32_t* perm_src = reinterpret_cast<int32_t*>(ws + lay.perm_src);

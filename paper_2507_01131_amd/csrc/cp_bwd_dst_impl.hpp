@@ -342,6 +342,10 @@ __global__ __launch_bounds__(direct_waves(MT, RT)* kWave) void k_bwd_dst(BwdDstA
       const float dv = dg * sRho[i], drho = dg * sV[i];
       sV[i] = dv;
       sRho[i] = drho;
+      if (a.drho) {  // drho rows for the radial-weight gradient
+        const int e = i / Rp, r = i - e * Rp;
+        if (r < R) a.drho[size_t(sEid[e]) * R + r] = drho;
+      }
     }
     __syncthreads();
     // dY = dV B^T (k < d <= 64: two output tiles) and dphi = dRho Wrad^T (one

@@ -390,6 +390,12 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst_sg(BwdDstArgs a, int 
       a.grad_vec[3 * eid + 1] = gy + dr * vy * inv;
       a.grad_vec[3 * eid + 2] = gzv + dr * vz * inv;
     }
+    if (a.drho) {  // drho rows for the radial-weight gradient (sRho is rewritten after the next barrier)
+      for (int i = tid; i < n * R; i += blockDim.x) {
+        const int t = i / R, r = i - t * R;
+        a.drho[size_t(sEid[t]) * R + r] = sRho[t * bs + r];
+      }
+    }
   }
 }
 

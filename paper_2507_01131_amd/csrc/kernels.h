@@ -136,6 +136,7 @@ struct BwdDstArgs {
   const float* x_scale;     // fp32 problems: row_scale of launch_direct_layout
   int n_range;              // equal edge ranges (bwd_dst_plan)
   int pieces_per_block;     // ranges per workgroup
+  float* drho;              // [E, R] by edge id: dL/drho_e, or nullptr (not stored)
 };
 // Edge ranges of the destination-side kernel on the current device
 // (n_range = 0 when the problem takes the per-segment kernels: d > 32 or no
@@ -154,6 +155,13 @@ hipError_t launch_bwd_dst(const BwdDstArgs& a, bool x_bf16, hipStream_t s);
 int device_cus();
 hipError_t launch_sh(int L, int E, const float* edge_vec, float* Y, float* dY, hipStream_t s);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
+
+// ---------------------------------------------------------------- radial weights
+// grad_Wrad[q, r] = sum_e phi_e[q] drho[e, r] (radial_grad.hip): per-block
+// partial sums over fixed edge ranges, then their sum in block order.
+int radial_grad_blocks(int E);
+hipError_t launch_radial_grad(int E, int R, int n_radial, float sigma, const float* edge_vec, const float* drho,
+                              float* partial, float* grad_radial_w, hipStream_t s);
 
 // ---------------------------------------------------------------- radius graph
 // Cell-list radius graph of a batch of systems (radius_graph.hip).

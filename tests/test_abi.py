@@ -46,11 +46,12 @@ def _fwd(p, ws_bytes=1 << 40, **override):
 
 def _bwd(p, ws_bytes=1 << 40, **override):
     args = dict(x=FAKE, vec=FAKE, ei=FAKE, A=FAKE, B=FAKE, D=FAKE, W=FAKE, rw=FAKE, perm=FAKE, off=FAKE, z=None,
-                g=FAKE, gx=FAKE, gW=FAKE, gv=FAKE, ws=FAKE)
+                g=FAKE, gx=FAKE, gW=FAKE, gv=FAKE, gr=FAKE, ws=FAKE)
     args.update(override)
     return tdn.lib().tdn_cp_tp_backward(ctypes.byref(p), args["x"], args["vec"], args["ei"], args["A"], args["B"],
                                         args["D"], args["W"], args["rw"], args["perm"], args["off"], args["z"],
-                                        args["g"], args["gx"], args["gW"], args["gv"], args["ws"], ws_bytes, None)
+                                        args["g"], args["gx"], args["gW"], args["gv"], args["gr"], args["ws"],
+                                        ws_bytes, None)
 
 
 @pytest.mark.parametrize("kw,status", [

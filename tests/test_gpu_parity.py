@@ -107,15 +107,18 @@ def test_backward_small_full(cfg):
     w, (A, B, D) = _small(cfg)
     res = _fwd(w, A, B, D)
     G = torch.from_numpy(w["grad_out"]).cuda()
-    gx, gW, gv = tdn.backward(res, G)
+    gx, gW, gv, gr = tdn.backward(res, G, need_radial=True)
     gx2, gW2, gv2 = tdn.backward(res, G, use_saved_z=False)
+    _, _, _, gr2 = tdn.backward(res, G, need_x=False, need_W=False, need_vec=False, need_radial=True)
     torch.cuda.synchronize()
-    rx, rW, rv = layer.backward(w["x"], w["edge_index"], w["edge_vec"], A, B, D, w["W"], w["radial_w"], w["r_cut"],
-                                w["L"], w["grad_out"])
+    rx, rW, rv, rr = layer.backward(w["x"], w["edge_index"], w["edge_vec"], A, B, D, w["W"], w["radial_w"],
+                                    w["r_cut"], w["L"], w["grad_out"], return_radial=True)
     t = tol(w)
     assert rel_err(gx.cpu(), rx) < t
     assert rel_err(gW.cpu(), rW) < t
     assert rel_err(gv.cpu(), rv) < t
+    assert rel_err(gr.cpu(), rr) < t
+    assert torch.equal(gr, gr2)            # alone (no grad_edge_vec) it takes the same fixed-order sums
     assert torch.equal(gx, gx2) and torch.equal(gv, gv2)
     assert rel_err(gW2.cpu(), rW) < t
 
@@ -162,17 +165,24 @@ def test_backward_full_size_sampled(name):
     tn = sample_nodes(w, 6, seed=3)
     Gm = np.zeros_like(w["grad_out"])
     Gm[tn] = w["grad_out"][tn]
-    _, gWm, _ = tdn.backward(res, torch.from_numpy(Gm).cuda(), need_x=False, need_vec=False)
+    _, gWm, _, grm = tdn.backward(res, torch.from_numpy(Gm).cuda(), need_x=False, need_vec=False,
+                                  need_radial=True)
     torch.cuda.synchronize()
     sel = np.nonzero(np.isin(dst, tn))[0]
-    _, rW, _ = layer.backward(*args, Gm, perm=sel)
+    _, rW, _, rr = layer.backward(*args, Gm, perm=sel, return_radial=True)
     assert rel_err(gWm.cpu(), rW) < t
+    assert rel_err(grm.cpu(), rr) < t
     # full-size identity: <G, out> = <grad_x, x> = <grad_W, W>
     s = float(torch.sum(G.double() * res.out.double()))
     xf = torch.from_numpy(w["x"]).cuda().double()
     Wf = torch.from_numpy(w["W"]).cuda().double()
     assert abs(float(torch.sum(gx.double() * xf)) - s) < 10 * t * max(1.0, abs(s))
     assert abs(float(torch.sum(gW.double() * Wf)) - s) < 10 * t * max(1.0, abs(s))
+    # and <grad_Wrad, Wrad> = <G, out>: out is linear in the radial weights too
+    _, _, _, gr = tdn.backward(res, G, need_x=False, need_W=False, need_vec=False, need_radial=True)
+    torch.cuda.synchronize()
+    Rf = torch.from_numpy(w["radial_w"]).cuda().double()
+    assert abs(float(torch.sum(gr.double() * Rf)) - s) < 10 * t * max(1.0, abs(s))
 
 
 def test_repeat_calls_are_bitwise_identical():
@@ -226,9 +236,10 @@ def test_no_edges_gives_zero_output():
     res = _fwd(w, A, B, D)
     assert torch.count_nonzero(res.out) == 0
     assert res.offsets.cpu().tolist() == [0] * 13
-    gx, gW, gv = tdn.backward(res, torch.from_numpy(w["grad_out"]).cuda())
+    gx, gW, gv, gr = tdn.backward(res, torch.from_numpy(w["grad_out"]).cuda(), need_radial=True)
     torch.cuda.synchronize()
     assert torch.count_nonzero(gx) == 0 and torch.count_nonzero(gW) == 0 and gv.numel() == 0
+    assert gr.shape == (8, 32) and torch.count_nonzero(gr) == 0
 
 
 def test_skewed_degrees_star_graph_and_isolated_nodes():
