@@ -105,7 +105,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="molecules3200_L4_C128_R128")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--backward", action="store_true", help="also time tdn_cp_tp_backward with every gradient (x, W, edge vectors, radial weights; extra field)")
+    ap.add_argument("--backward", action="store_true",
+                    help="also time tdn_cp_tp_backward with every gradient (x, W, edge vectors, radial weights; "
+                         "extra field)")
     ap.add_argument("--ablation-atomics", action="store_true",
                     help="also time the atomic scatter-add forward (extra field; fp32 workloads with 2 <= L <= 4)")
     ap.add_argument("--radius-graph", action="store_true",
