@@ -3,7 +3,8 @@
 // [n_radial, R], one weight per rank of the CP product of Sec. 3.1), so
 //   grad_Wrad[q, r] = sum_e phi_e[q] drho_e[r],
 // with drho_e = dg_e * v_e stored per edge by the backward destination pass.
-// Workgroup b takes the edge range [b E / B, (b+1) E / B) in chunks of 64:
+// Workgroup b takes the edge range [b E / B, (b+1) E / B) (B = E / 256, at
+// most 2048) in chunks of 64:
 // phi for the chunk into LDS, then fp32 MFMA (rows: radial functions, columns:
 // ranks, contraction over the chunk's edges, two per step), one 32-rank tile
 // per wave (two for R > 128).  The partial sums are added in block order by a
@@ -17,7 +18,7 @@ namespace tdn {
 namespace {
 
 constexpr int kGradChunk = 64;
-constexpr int kEdgesPerBlock = 512;
+constexpr int kEdgesPerBlock = 256;
 constexpr int kMaxBlocks = 2048;
 
 __global__ __launch_bounds__(256) void k_wrad_partial(int E, int n_blocks, int R, int nr, float sigma,
@@ -44,11 +45,18 @@ __global__ __launch_bounds__(256) void k_wrad_partial(int E, int n_blocks, int R
       const int rt = wave + 4 * j;
       if (rt < RT) {
         const int r = rt * kTile + l32;
+        // every drho load of the chunk issued before the first product
+        float bv[kGradChunk / 2];
+#pragma unroll
+        for (int s2 = 0; s2 < kGradChunk / 2; ++s2) {
+          const int e = 2 * s2 + h;
+          bv[s2] = (e < n && r < R) ? drho[size_t(cb + e) * R + r] : 0.f;
+        }
+#pragma unroll
         for (int s2 = 0; s2 < kGradChunk / 2; ++s2) {
           const int e = 2 * s2 + h;
           const float av = (e < n && l32 < nr) ? sPhi[e * nr + l32] : 0.f;
-          const float bv = (e < n && r < R) ? drho[size_t(cb + e) * R + r] : 0.f;
-          acc[j] = mfma32(av, bv, acc[j]);
+          acc[j] = mfma32(av, bv[s2], acc[j]);
         }
       }
     }
@@ -67,13 +75,24 @@ __global__ __launch_bounds__(256) void k_wrad_partial(int E, int n_blocks, int R
   }
 }
 
+// 16 outputs per workgroup, 16 slices per output: slice k sums the partials
+// of blocks k, k + 16, ... in order, then the slices are added in order.
 __global__ __launch_bounds__(256) void k_wrad_reduce(int n_blocks, int n_out, const float* __restrict__ partial,
                                                      float* __restrict__ grad) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= n_out) return;
+  __shared__ float sSum[16][17];
+  const int o = threadIdx.x & 15, k = threadIdx.x >> 4;
+  const int i = blockIdx.x * 16 + o;
   float s = 0.f;
-  for (int b = 0; b < n_blocks; ++b) s += partial[size_t(b) * n_out + i];
-  grad[i] = s;
+  if (i < n_out)
+    for (int b = k; b < n_blocks; b += 16) s += partial[size_t(b) * n_out + i];
+  sSum[k][o] = s;
+  __syncthreads();
+  if (k == 0 && i < n_out) {
+    float t = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) t += sSum[j][o];
+    grad[i] = t;
+  }
 }
 
 }  // namespace
@@ -90,7 +109,7 @@ hipError_t launch_radial_grad(int E, int R, int n_radial, float sigma, const flo
   if (E == 0) return launch_zero(grad_radial_w, size_t(n_out) * 4, s);
   const int nb = radial_grad_blocks(E);
   k_wrad_partial<<<dim3(nb), dim3(256), 0, s>>>(E, nb, R, n_radial, sigma, edge_vec, drho, partial);
-  k_wrad_reduce<<<dim3((n_out + 255) / 256), dim3(256), 0, s>>>(nb, n_out, partial, grad_radial_w);
+  k_wrad_reduce<<<dim3((n_out + 15) / 16), dim3(256), 0, s>>>(nb, n_out, partial, grad_radial_w);
   return hipGetLastError();
 }
 
