@@ -1,14 +1,20 @@
 """Benchmark of the CP tensor-product layer forward pass on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                    [--no-cpu-baseline] [--backward]
+                    [--no-cpu-baseline] [--backward] [--eager] [--radius-graph]
+                    [--ablation-atomics] [--calibrate-copy]
 
 One step is one call of tdn_cp_tp_forward on the headline workload (64
 molecules x 50 atoms, 3200 nodes, ~151k edges within 6 A, L=4, C=128,
 R=128, float32, edges pre-sorted by destination): segment offsets, the fused
 harmonics/radial/Khatri-Rao MFMA edge pass with the per-node output factor,
 and the shared channel-mix GEMM.  Inputs are resident in HBM before timing.
-Prints one JSON line.  The metric is edge tensor products per second.
+Prints one JSON line.  The metric is edge tensor products per second.  The
+step is timed twice: launched eagerly (with per-kernel HIP events, which give
+the roofline's kernel time) and captured once in a HIP graph and replayed
+(every kernel of every step still runs, without per-launch host cost); value
+and ms_per_step come from the replay, value_eager and ms_per_step_eager from
+the eager loop (--eager times the eager step only).
 
 The roofline object reports the dominant kernel (the edge pass): its
 algorithmic flops per launch, E (2RdC + 2Rd + 17R + RC) + N 2dRC, over its
@@ -110,6 +116,9 @@ def main():
                          "extra field)")
     ap.add_argument("--ablation-atomics", action="store_true",
                     help="also time the atomic scatter-add forward (extra field; fp32 workloads with 2 <= L <= 4)")
+    ap.add_argument("--eager", action="store_true",
+                    help="time the eagerly launched step only (default: the step captured once in a HIP graph "
+                         "and replayed, with the eager step timed beside it)")
     ap.add_argument("--radius-graph", action="store_true",
                     help="also time tdn_radius_graph on the workload's geometry (extra field)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -182,6 +191,36 @@ def main():
     per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
     kern = {k: tdn.timer_read(k, reset=True) for k in fwd_kernels}
     edge_ms = kern["cp_edge_fwd"][0] / max(1, kern["cp_edge_fwd"][1])
+    ms_step_eager = ms_step
+    launch = "eager"
+    if not args.eager:
+        # The same step (offsets, feature layout, edge pass, node GEMM)
+        # captured once in a HIP graph and replayed: every kernel of every step
+        # still runs, without the per-launch host cost.  The eager loop above
+        # gave the per-kernel durations.
+        try:
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                step()
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                step()
+            for _ in range(args.warmup):
+                graph.replay()
+            torch.cuda.synchronize()
+            for i in range(args.steps):
+                evs[i].record()
+                graph.replay()
+            ev1.record()
+            torch.cuda.synchronize()
+            ms_step = ev0.elapsed_time(ev1) / args.steps
+            per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+            launch = "hip_graph_replay"
+        except RuntimeError as exc:  # capture unavailable: report the eager step
+            print(f"graph capture failed ({exc}); timing the eager step", file=sys.stderr)
 
     bf16 = w["feat_dtype"] == "bf16"
     f_edge = edge_kernel_flops(N, E, d, C, R)
@@ -197,6 +236,9 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": ms_step,
         "ms_per_step_p10_p50_p90": [float(np.percentile(per_step, q)) for q in (10, 50, 90)],
+        "launch": launch,
+        "ms_per_step_eager": ms_step_eager,
+        "value_eager": E / (ms_step_eager * 1e-3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
