@@ -183,3 +183,44 @@ def test_built_graph_feeds_the_layer():
     torch.cuda.synchronize()
     ref = layer.forward(x, np.stack([s, d]).astype(np.int32), v, A, B, D, W, rw, 3.5, L)
     assert rel_err(out.cpu(), ref) < TOL_F32
+
+
+def test_grid_limits_and_cell_boundaries():
+    rng = np.random.default_rng(21)
+    # (a) clusters spread over 1e5 A: the 1024-cells-per-axis and 2 n + 1
+    # cells-per-system bounds widen the cells far beyond the cutoff
+    centres = rng.uniform(0, 1e5, size=(20, 3))
+    pos = np.concatenate([c + rng.uniform(0, 6.0, size=(25, 3)) for c in centres])
+    inp = workloads.wrap_inputs(pos, [0, len(pos)], np.zeros((1, 3)), (False, False, False), 3.0)
+    _assert_same(_gpu(inp), _oracle(inp))
+    # (b) a lattice whose spacing is the smallest cell width the grid allows
+    # (1.001 r_cut), so atoms sit on cell boundaries, plus the same lattice
+    # shifted by half a spacing along x (two neighbours at 1.001 per atom);
+    # periodic and open axes
+    r_cut = 2.0
+    a = np.float32(r_cut * 1.001)
+    n = 9
+    g = np.stack(np.meshgrid(*[np.arange(n)] * 3, indexing="ij"), -1).reshape(-1, 3) * float(a)
+    g2 = np.concatenate([g, g + np.array([0.5 * float(a), 0.0, 0.0])])
+    jitter = rng.choice([0.0, 1e-6, -1e-6], size=g2.shape)
+    L = float(np.float32(n * a))
+    for per in [(True, True, True), (True, False, False)]:
+        inp = workloads.wrap_inputs(g2 + jitter, [0, len(g2)], np.array([[L, L, L]]), per, r_cut)
+        ref = _oracle(inp)
+        assert len(ref[0]) > 0
+        _assert_same(_gpu(inp), ref)
+    # (c) spacing just under the cutoff: every lattice neighbour is an edge
+    inp = workloads.wrap_inputs(g * (1.9 / float(a)), [0, len(g)], np.array([[9 * 1.9] * 3]), (True,) * 3, r_cut)
+    res = _gpu(inp)
+    assert res.edge_index.shape[1] == 6 * len(g)
+    _assert_same(res, _oracle(inp))
+
+
+def test_large_periodic_system_sampled():
+    rng = np.random.default_rng(22)
+    N, box = 20000, 58.0
+    inp = workloads.wrap_inputs(rng.uniform(0, box, size=(N, 3)), [0, N], np.array([[box, box, box]]),
+                                (True, True, True), 4.0)
+    res = _gpu(inp, max_neighbors=24)
+    dsts = np.sort(rng.choice(N, 64, replace=False))
+    _assert_same(res, _oracle(inp, max_neighbors=24, dst_nodes=dsts), dsts)
