@@ -55,8 +55,10 @@ hipError_t launch_bwd_dst(const BwdDstArgs& a, bool x_bf16, hipStream_t s) {
   if (a.n_range > 0) {
     if (a.d > 32 || a.n_range > a.E || !a.xc || !a.dst || (!x_bf16 && !a.x_scale)) return hipErrorInvalidValue;
     switch (a.L) {
-#define TDN_DST2_CASE(LV) \
-  case LV: return x_bf16 ? bwd2_detail::launch_l<LV, true>(a, a.n_range, s) : bwd2_detail::launch_l<LV, false>(a, a.n_range, s);
+#define TDN_DST2_CASE(LV)                                                  \
+  case LV:                                                                 \
+    return x_bf16 ? bwd2_detail::launch_l<LV, true>(a, a.n_range, s)      \
+                  : bwd2_detail::launch_l<LV, false>(a, a.n_range, s);
       TDN_DST2_CASE(0)
       TDN_DST2_CASE(1)
       TDN_DST2_CASE(2)
