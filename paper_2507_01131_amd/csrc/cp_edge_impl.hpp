@@ -498,12 +498,11 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
         }
       }
       __syncthreads();
-      // harmonics: one thread per (edge, order m) column; radial basis: one
+      // harmonics: one thread per edge (all degrees, unrolled); radial basis: one
       // thread per (edge, function)
-      for (int t = tid; t < n * (L + 1); t += blockDim.x) {
-        const int e = t / (L + 1), m = t - e * (L + 1);
-        const float4 u = sVec[e];
-        sh_unit_column(L, m, u.x, u.y, u.z, sY + e * d);
+      for (int t = tid; t < n; t += blockDim.x) {
+        const float4 u = sVec[t];
+        sh_unit_all<L>(u.x, u.y, u.z, sY + t * d);
       }
       for (int t = tid; t < n * nr; t += blockDim.x) {
         const int e = t / nr, q = t - e * nr;
