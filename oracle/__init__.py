@@ -19,6 +19,9 @@ Modules
             Sec. 3.3, Sec. 3.4, Sec. 4.1, App. B)
   layer     the message-passing layer by direct per-edge summation and its
             backward (Sec. 3.1 eq. approximate, Sec. 3.2)
+  dense_layer
+            the exact CG tensor-product layer path by path, the comparator
+            of the CP layer (Sec. 2 eq. clebsch_gordan, Sec. 3.2)
   radius_graph
             the edges the layer consumes: every atom pair of a system (and
             its periodic images) closer than the cutoff, with an optional
