@@ -129,6 +129,33 @@ tdn_status tdn_ablation_forward_atomics(const tdn_problem* p, const void* x, con
                                         float* out, float* z_save, int32_t* perm, int32_t* offsets,
                                         void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* The exact CG tensor product over the same edges, as the comparator of the
+ * CP layer (Sec. 2 eq. clebsch_gordan summed over every path (l1, l2, l3)
+ * with l1, l2 <= L and |l1 - l2| <= l3 <= min(l1 + l2, L); Sec. 3.2 for the
+ * per-path weight and the one channel weight W that all paths share):
+ *   Z[n] = sum over edges e into n of K_e x[src_e],
+ *   K_e[k, i] = sum_j C[k, i, j] Y_e[j] rho_e[path(k, i, j)],
+ *   rho_e = phi_e path_w,   out = Z W.
+ * Arguments as tdn_cp_tp_forward, with p->R the number of paths of degree L
+ * (1, 5, 15, 34, 65, 111, 175 for L = 0..6; TDN_ERR_BAD_SHAPE otherwise) and
+ * fp32 features only (TDN_ERR_BAD_DTYPE); the same workspace size.  The
+ * coefficients C (device memory, read only) are rows over (k, i) pairs,
+ * q = k d + i:
+ *   cg_row [d*d + 1] int32   entries cg_row[q] .. cg_row[q+1] - 1 of row q
+ *   cg_col [cg_nnz]  int32   j | path << 16 (path: index of the path in the
+ *                            order l1, then l2, then l3 ascending)
+ *   cg_val [cg_nnz]  f32     the coefficient
+ *   path_w [n_radial, R] f32 radial weights of the paths
+ * Rows are clamped to [0, cg_nnz] and entries with j >= d or path >= R are
+ * skipped (a malformed table gives wrong values, never an out-of-bounds
+ * read).  z_save, if not NULL, receives Z.  Deterministic: each node's edges
+ * are summed in sorted order. */
+tdn_status tdn_dense_tp_forward(const tdn_problem* p, const void* x, const float* edge_vec,
+                                const int32_t* edge_index, const int32_t* cg_row, const int32_t* cg_col,
+                                const float* cg_val, int32_t cg_nnz, const float* path_w, const void* W,
+                                float* out, float* z_save, int32_t* perm, int32_t* offsets, void* workspace,
+                                size_t workspace_bytes, hipStream_t stream);
+
 /* Backward pass for the scalar <grad_out, out>.  perm and offsets are the
  * forward's outputs; z_save is the forward's saved Z or NULL (then Z is
  * recomputed).  Each gradient pointer may be NULL to skip it; grads are f32
@@ -219,7 +246,7 @@ tdn_status tdn_spherical_harmonics(int32_t L, int32_t E, const float* edge_vec, 
  * tdn_timer_enable(1) starts recording every launch of the layer's edge
  * kernels; tdn_timer_read synchronises on the recorded events and returns
  * the summed milliseconds and launch count of the kernel named `kernel`
- * ("cp_edge_fwd", "cp_edge_fwd_atomic", "radius_graph", "feature_layout",
+ * ("cp_edge_fwd", "cp_edge_fwd_atomic", "dense_edge_fwd", "radius_graph", "feature_layout",
  * "channel_layout", "cp_edge_bwd_src", "cp_bwd_dst", "radial_grad", "node_gemm", "gram",
  * "sort");
  * reset = 1 clears that kernel's record. */

@@ -69,6 +69,7 @@ def lib() -> ctypes.CDLL:
         L.tdn_cp_tp_forward.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
         L.tdn_ablation_forward_atomics.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
         L.tdn_cp_tp_backward.argtypes = [PP] + [_P] * 17 + [_SZ, _P]
+        L.tdn_dense_tp_forward.argtypes = [PP] + [_P] * 6 + [ctypes.c_int32] + [_P] * 7 + [_SZ, _P]
         GP = ctypes.POINTER(GraphProblem)
         L.tdn_radius_graph_workspace_size.argtypes = [GP, ctypes.POINTER(_SZ)]
         L.tdn_radius_graph.argtypes = [GP, _P, _P, _P, ctypes.c_int64, _P, _P, _P, _P,
@@ -84,7 +85,7 @@ def lib() -> ctypes.CDLL:
         L.tdn_last_hip_error.restype = ctypes.c_int32
         for f in ("tdn_workspace_size", "tdn_cp_tp_forward", "tdn_ablation_forward_atomics", "tdn_cp_tp_backward",
                   "tdn_sort_workspace_size", "tdn_sort_by_key", "tdn_spherical_harmonics", "tdn_timer_enable",
-                  "tdn_timer_read", "tdn_radius_graph_workspace_size", "tdn_radius_graph"):
+                  "tdn_timer_read", "tdn_radius_graph_workspace_size", "tdn_radius_graph", "tdn_dense_tp_forward"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -192,6 +193,89 @@ def forward(x, edge_vec, edge_index, A, B, D, W, radial_w, *, L: int, r_cut: flo
     _check(st, name)
     return ForwardResult(out, z, perm, offsets, p,
                          dict(x=x, edge_vec=edge_vec, edge_index=edge_index, A=A, B=B, D=D, W=W, radial_w=radial_w))
+
+
+@dataclass
+class CGTable:
+    """The coefficient tensor in tdn_dense_tp_forward's row format (device
+    tensors): row q = k d + i holds the entries (j | path << 16, value) of
+    every nonzero C[k, i, j], in increasing j."""
+    L: int
+    n_path: int
+    row: torch.Tensor
+    col: torch.Tensor
+    val: torch.Tensor
+
+
+def cg_table(M, path, device) -> CGTable:
+    """Marshals a dense coefficient tensor M [d, d, d] (index order k, i, j)
+    and the path index of each entry ([d, d, d], -1 where M is zero) into the
+    row format of tdn_dense_tp_forward."""
+    import numpy as np
+
+    M = np.asarray(M)
+    path = np.asarray(path, np.int64)
+    d = M.shape[0]
+    L = int(round(d ** 0.5)) - 1
+    if M.shape != (d, d, d) or path.shape != M.shape or (L + 1) ** 2 != d:
+        raise ValueError("M and path must be [d, d, d] with d = (L + 1)^2")
+    k, i, j = np.nonzero(M)                     # row-major: sorted by (k, i, j)
+    p = path[k, i, j]
+    if np.any(p < 0) or np.any(p >= 1 << 15):
+        raise ValueError("every nonzero coefficient needs a path index in [0, 2^15)")
+    q = k * d + i
+    row = np.zeros(d * d + 1, np.int64)
+    np.add.at(row, q + 1, 1)
+    row = np.cumsum(row)
+    col = (j | (p << 16)).astype(np.int32)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)  # noqa: E731
+    return CGTable(L, int(path.max()) + 1 if path.size else 0, t(row.astype(np.int32)), t(col),
+                   t(M[k, i, j].astype(np.float32)))
+
+
+def dense_forward(x, edge_vec, edge_index, table: CGTable, path_w, W, *, r_cut: float, edges_sorted=False,
+                  validate=False, workspace=None, out=None, z=None, perm=None, offsets=None,
+                  stream=None) -> ForwardResult:
+    """Runs tdn_dense_tp_forward, the exact CG tensor product over the same
+    edges (float32 features).  path_w [n_radial, n_path] float32; the other
+    arguments as in forward()."""
+    dev = x.device
+    N, d, C = x.shape
+    E = edge_vec.shape[0]
+    L = table.L
+    P = path_w.shape[1]
+    if edge_index.dtype != torch.int32:
+        edge_index = edge_index.to(torch.int32)
+    edge_index = edge_index.contiguous()
+    for t, n, dt, sh in [(x, "x", torch.float32, (N, (L + 1) ** 2, C)), (edge_vec, "edge_vec", torch.float32, (E, 3)),
+                         (edge_index, "edge_index", torch.int32, (2, E)), (W, "W", torch.float32, (C, C)),
+                         (path_w, "path_w", torch.float32, (path_w.shape[0], P)),
+                         (table.row, "table.row", torch.int32, (d * d + 1,)),
+                         (table.col, "table.col", torch.int32, (table.col.shape[0],)),
+                         (table.val, "table.val", torch.float32, (table.col.shape[0],))]:
+        _need(t, n, dt, sh, dev)
+    p = make_problem(L, C, P, N, E, r_cut, path_w.shape[0], TDN_F32, edges_sorted, validate)
+    fwd_bytes, _ = workspace_size(p)
+    if workspace is None or workspace.numel() < fwd_bytes:
+        workspace = torch.empty(max(fwd_bytes, 1), dtype=torch.uint8, device=dev)
+    if out is None:
+        out = torch.empty((N, d, C), dtype=torch.float32, device=dev)
+    if perm is None:
+        perm = torch.empty(max(E, 1), dtype=torch.int32, device=dev)[:E]
+    if offsets is None:
+        offsets = torch.empty(N + 1, dtype=torch.int32, device=dev)
+    _need(out, "out", torch.float32, (N, d, C), dev)
+    if z is not None:
+        _need(z, "z", torch.float32, (N, d, C), dev)
+    _need(perm, "perm", torch.int32, (E,), dev)
+    _need(offsets, "offsets", torch.int32, (N + 1,), dev)
+    st = lib().tdn_dense_tp_forward(ctypes.byref(p), _ptr(x), _ptr(edge_vec), _ptr(edge_index), _ptr(table.row),
+                                    _ptr(table.col), _ptr(table.val), int(table.col.shape[0]), _ptr(path_w), _ptr(W),
+                                    _ptr(out), _ptr(z), _ptr(perm), _ptr(offsets), _ptr(workspace),
+                                    workspace.numel(), _stream(stream))
+    _check(st, "tdn_dense_tp_forward")
+    return ForwardResult(out, z, perm, offsets, p, dict(x=x, edge_vec=edge_vec, edge_index=edge_index, W=W,
+                                                        path_w=path_w))
 
 
 def backward(res: ForwardResult, grad_out, *, need_x=True, need_W=True, need_vec=True, need_radial=False,

@@ -1,0 +1,306 @@
+// The exact CG tensor product over the edges, the comparator of the CP edge
+// pass: for every destination node n,
+//   Z[n] = sum over edges e into n of K_e x[s_e],
+//   K_e[k][i] = sum_j C[k; i, j] Y_e[j] rho_e[path(k, i, j)],
+// with C the real CG coefficients of every path (l1, l2, l3) of degree <= L
+// (Sec. 2, eq. clebsch_gordan and the direct sum over paths), Y_e the real
+// harmonics of the edge direction and rho_e = phi_e Wpath one radial weight
+// per path (Sec. 3.2; the channel weight W is applied by the node GEMM).
+//
+// One workgroup per destination node, edges in batches of EB:
+//   1. per edge: harmonics and radial basis into LDS;
+//   2. rho_e = phi_e Wpath, one thread per (edge, path);
+//   3. K_e in LDS: thread q takes the (k, i) pairs q, q + threads, ...,
+//      loads each pair's coefficients (j, path, value) once and applies them
+//      to all edges of the batch; the largest |K_e| per edge sets the power of
+//      two that puts K_e in the fp16 split's range;
+//   4. per edge and 32-channel tile: U = K_e x[s_e] on 32x32x16 fp16 MFMA from
+//      the three part products of the two-part splits (K_e split on the fly
+//      from LDS, x from the edge pass's operand blocks), then
+//      acc += 2^(e_K + e_x) U in fp32.
+// The node's d x C sum is stored once.  Work per edge: nnz(C) multiply-adds
+// for K_e (independent of C) and 2 d^2 C flops of contraction (d padded to
+// 32 or 64).
+#include "common.hpp"
+#include "kernels.h"
+#include "sh_device.hpp"
+
+namespace tdn {
+
+namespace dense_detail {
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x16 mfma_f16(u32x4 a, u32x4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0,
+                                                0);
+}
+
+constexpr int kMaxWaves = 4;
+
+__host__ __device__ constexpr int dense_dp(int d) { return d <= 32 ? 32 : 64; }  // rows and K, padded
+__host__ __device__ constexpr int dense_ks(int d) { return dense_dp(d) + 4; }   // LDS row stride (floats)
+__host__ __device__ constexpr int dense_eb(int d) { return d <= 32 ? 8 : 4; }   // edges per batch
+
+struct DenseSmem {
+  int off_k, off_y, off_phi, off_rho, off_row, off_sc, off_ksc, off_max, floats;
+};
+__host__ __device__ inline DenseSmem dense_smem(int d, int n_path) {
+  const int eb = dense_eb(d);
+  DenseSmem s{};
+  int o = 0;
+  s.off_k = o;
+  o += eb * dense_dp(d) * dense_ks(d);
+  s.off_y = o;
+  o += eb * d;
+  s.off_phi = o;
+  o += eb * 16;
+  s.off_rho = o;
+  o += eb * n_path;
+  s.off_row = o;
+  o += eb;
+  s.off_sc = o;
+  o += eb;
+  s.off_ksc = o;
+  o += eb;
+  s.off_max = o;
+  o += kMaxWaves * eb;
+  s.floats = o;
+  return s;
+}
+
+template <int L, int CTW>
+__global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves) {
+  constexpr int d = (L + 1) * (L + 1);
+  constexpr int DP = dense_dp(d), KS = dense_ks(d), EB = dense_eb(d);
+  constexpr int KB = DP / 16, RK = DP / 32;
+  extern __shared__ float smem[];
+  const DenseSmem sm = dense_smem(d, a.n_path);
+  float* sK = smem + sm.off_k;
+  float* sY = smem + sm.off_y;
+  float* sPhi = smem + sm.off_phi;
+  float* sRho = smem + sm.off_rho;
+  int* sRow = reinterpret_cast<int*>(smem + sm.off_row);
+  float* sSc = smem + sm.off_sc;
+  float* sKsc = smem + sm.off_ksc;
+  float* sMax = smem + sm.off_max;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int h = lane >> 5, l32 = lane & 31;
+  const int nthr = blockDim.x;
+  const int n = xcd_remap(blockIdx.x, a.N);
+  const int e0 = a.offsets[n], e1 = a.offsets[n + 1];
+  const int P = a.n_path, nr = a.n_radial;
+
+  // K padding (rows and columns >= d) stays zero; every (k, i) with k, i < d
+  // is rewritten for each batch
+  for (int t = tid; t < EB * DP * KS; t += nthr) sK[t] = 0.f;
+
+  f32x16 acc[RK][CTW];
+#pragma unroll
+  for (int r = 0; r < RK; ++r)
+#pragma unroll
+    for (int c = 0; c < CTW; ++c) acc[r][c] = f32x16{};
+
+  const char* __restrict__ xs = static_cast<const char*>(a.feat);
+  const int n_ct = (a.C + kTile - 1) / kTile;
+  const size_t row_bytes = size_t(n_ct) * 2 * KB * 1024;
+  uint32_t lane_off[CTW];
+#pragma unroll
+  for (int c = 0; c < CTW; ++c) {
+    const int ct = min(wave * CTW + c, n_ct - 1);
+    lane_off[c] = uint32_t(ct * 2 * KB * 1024 + h * 512 + l32 * 16);
+  }
+  // x[row] operand blocks of this wave's channel tiles: [tile][part][K-block]
+  auto load_x = [&](int row, u32x4 (&xb)[CTW][2][KB]) {
+    const char* p = xs + size_t(row) * row_bytes;
+#pragma unroll
+    for (int c = 0; c < CTW; ++c)
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int b = 0; b < KB; ++b)
+          xb[c][s][b] = *reinterpret_cast<const u32x4*>(p + lane_off[c] + uint32_t((s * KB + b) * 1024));
+  };
+  auto edge_compute = [&](int t, const u32x4 (&xb)[CTW][2][KB]) {
+    const float ksc = sKsc[t], usc = sSc[t];
+#pragma unroll
+    for (int r = 0; r < RK; ++r) {
+      u32x4 hi[KB], lo[KB];
+      const float* kp = sK + (t * DP + r * kTile + l32) * KS + 8 * h;
+#pragma unroll
+      for (int b = 0; b < KB; ++b) {
+        const float4 f0 = *reinterpret_cast<const float4*>(kp + 16 * b);
+        const float4 f1 = *reinterpret_cast<const float4*>(kp + 16 * b + 4);
+        uint32_t h0, h1, h2, h3, m0, m1, m2, m3;
+        split_f16x2_pair(f0.x * ksc, f0.y * ksc, h0, m0);
+        split_f16x2_pair(f0.z * ksc, f0.w * ksc, h1, m1);
+        split_f16x2_pair(f1.x * ksc, f1.y * ksc, h2, m2);
+        split_f16x2_pair(f1.z * ksc, f1.w * ksc, h3, m3);
+        hi[b] = u32x4{h0, h1, h2, h3};
+        lo[b] = u32x4{m0, m1, m2, m3};
+      }
+#pragma unroll
+      for (int c = 0; c < CTW; ++c) {
+        f32x16 u = f32x16{};
+#pragma unroll
+        for (int b = 0; b < KB; ++b) u = mfma_f16(lo[b], xb[c][0][b], u);
+#pragma unroll
+        for (int b = 0; b < KB; ++b) u = mfma_f16(hi[b], xb[c][1][b], u);
+#pragma unroll
+        for (int b = 0; b < KB; ++b) u = mfma_f16(hi[b], xb[c][0][b], u);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[r][c][v] = fmaf(usc, u[v], acc[r][c][v]);
+      }
+    }
+  };
+
+  for (int b0 = e0; b0 < e1; b0 += EB) {
+    const int nb = min(EB, e1 - b0);
+    __syncthreads();  // the previous batch's K consumed (and the zero fill done)
+    // 1. per edge: gathered row, harmonics, radial basis
+    if (tid < nb) {
+      const int eid = a.perm[b0 + tid];
+      sRow[tid] = a.src[eid];
+      const float vx = a.edge_vec[3 * size_t(eid)], vy = a.edge_vec[3 * size_t(eid) + 1],
+                  vz = a.edge_vec[3 * size_t(eid) + 2];
+      const float len = sqrtf(vx * vx + vy * vy + vz * vz);
+      const float inv = 1.f / len;
+      sh_unit_all<L>(vx * inv, vy * inv, vz * inv, sY + tid * d);
+      for (int q = 0; q < nr; ++q) sPhi[tid * 16 + q] = radial_phi(len, q, a.sigma);
+    }
+    __syncthreads();
+    // 2. rho = phi Wpath
+    for (int t = tid; t < nb * P; t += nthr) {
+      const int e = t / P, p = t - e * P;
+      float s = 0.f;
+      for (int q = 0; q < nr; ++q) s = fmaf(sPhi[e * 16 + q], a.path_w[q * P + p], s);
+      sRho[e * P + p] = s;
+    }
+    __syncthreads();
+    // 3. K_e for the batch, and the largest |K_e| of each edge
+    float mx[EB];
+#pragma unroll
+    for (int e = 0; e < EB; ++e) mx[e] = 0.f;
+    for (int q = tid; q < d * d; q += nthr) {
+      const int k = q / d, i = q - k * d;
+      int s0 = a.cg_row[q], s1 = a.cg_row[q + 1];
+      s0 = max(0, min(s0, a.cg_nnz));
+      s1 = max(s0, min(s1, a.cg_nnz));
+      float v[EB];
+#pragma unroll
+      for (int e = 0; e < EB; ++e) v[e] = 0.f;
+      for (int s = s0; s < s1; ++s) {
+        const int col = a.cg_col[s];
+        const int j = col & 0xffff, p = col >> 16;
+        if (j >= d || p < 0 || p >= P) continue;  // malformed entry: ignored
+        const float c = a.cg_val[s];
+#pragma unroll
+        for (int e = 0; e < EB; ++e)
+          if (e < nb) v[e] = fmaf(c, sY[e * d + j] * sRho[e * P + p], v[e]);
+      }
+#pragma unroll
+      for (int e = 0; e < EB; ++e)
+        if (e < nb) {
+          sK[(e * DP + k) * KS + i] = v[e];
+          mx[e] = fmaxf(mx[e], fabsf(v[e]));
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < EB; ++e) {
+      float m = mx[e];
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+      if (lane == 0) sMax[wave * EB + e] = m;
+    }
+    __syncthreads();
+    if (tid < nb) {
+      float m = 0.f;
+      for (int w = 0; w < waves; ++w) m = fmaxf(m, sMax[w * EB + tid]);
+      const int ek = f16_split_exponent(m);
+      sKsc[tid] = ldexpf(1.f, -ek);
+      sSc[tid] = ldexpf(a.row_scale[sRow[tid]], ek);
+    }
+    __syncthreads();
+    // 4. the contraction, x of edge t + 1 loaded while edge t computes
+    u32x4 x0[CTW][2][KB], x1[CTW][2][KB];
+    load_x(__builtin_amdgcn_readfirstlane(sRow[0]), x0);
+    int t = 0;
+    for (; t + 1 < nb; t += 2) {
+      load_x(__builtin_amdgcn_readfirstlane(sRow[t + 1]), x1);
+      __builtin_amdgcn_sched_barrier(0);
+      edge_compute(t, x0);
+      __builtin_amdgcn_sched_barrier(0);
+      load_x(__builtin_amdgcn_readfirstlane(sRow[t + 2 < nb ? t + 2 : t + 1]), x0);  // past the end: unused
+      __builtin_amdgcn_sched_barrier(0);
+      edge_compute(t + 1, x1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (t < nb) edge_compute(t, x0);
+  }
+  // Z[n] rows k < d, channels of this wave's tiles
+#pragma unroll
+  for (int c = 0; c < CTW; ++c) {
+    const int ct = wave * CTW + c;
+    const int ch = ct * kTile + l32;
+    if (ct >= n_ct || ch >= a.C) continue;
+#pragma unroll
+    for (int r = 0; r < RK; ++r)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int k = r * kTile + acc_row(v, h);
+        if (k < d) a.out[(size_t(n) * d + k) * a.C + ch] = acc[r][c][v];
+      }
+  }
+}
+
+template <int L, int CTW>
+hipError_t launch_l_ctw(const DenseArgs& a, int waves, hipStream_t s) {
+  constexpr int d = (L + 1) * (L + 1);
+  const size_t lds = size_t(dense_smem(d, a.n_path).floats) * 4;
+  auto k = k_dense_edge<L, CTW>;
+  hipError_t e =
+      hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  if (e != hipSuccess) return e;
+  k<<<dim3(a.N), dim3(waves * kWave), lds, s>>>(a, waves);
+  return hipGetLastError();
+}
+
+template <int L>
+hipError_t launch_l(const DenseArgs& a, hipStream_t s) {
+  const int n_ct = (a.C + kTile - 1) / kTile;
+  const int waves = n_ct < kMaxWaves ? n_ct : kMaxWaves;
+  return n_ct <= kMaxWaves ? launch_l_ctw<L, 1>(a, waves, s) : launch_l_ctw<L, 2>(a, waves, s);
+}
+
+}  // namespace dense_detail
+
+int dense_path_count(int L) {
+  int n = 0;
+  for (int l1 = 0; l1 <= L; ++l1)
+    for (int l2 = 0; l2 <= L; ++l2) {
+      const int lo = l1 > l2 ? l1 - l2 : l2 - l1, hi = l1 + l2 < L ? l1 + l2 : L;
+      n += hi - lo + 1;
+    }
+  return n;
+}
+
+hipError_t launch_dense_edge(const DenseArgs& a, hipStream_t s) {
+  if (a.N == 0) return hipSuccess;
+  if (a.C < 1 || a.C > 8 * kTile || a.n_radial < 1 || a.n_radial > 16 || a.n_path != dense_path_count(a.L) ||
+      a.feat == nullptr || a.row_scale == nullptr)
+    return hipErrorInvalidValue;
+  switch (a.L) {
+    case 0: return dense_detail::launch_l<0>(a, s);
+    case 1: return dense_detail::launch_l<1>(a, s);
+    case 2: return dense_detail::launch_l<2>(a, s);
+    case 3: return dense_detail::launch_l<3>(a, s);
+    case 4: return dense_detail::launch_l<4>(a, s);
+    case 5: return dense_detail::launch_l<5>(a, s);
+    case 6: return dense_detail::launch_l<6>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace tdn

@@ -94,6 +94,33 @@ hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
 // per edge and Z accumulated into `out` (zeroed first) with float atomics;
 // nondeterministic in the order of the additions.
 hipError_t launch_cp_edge_atomic(const EdgeArgs& a, hipStream_t s);
+
+// The exact CG tensor product over the sorted edges (the comparator of the CP
+// edge pass): out[n] = sum over edges e into n of K_e x[src_e] with
+// K_e[k][i] = sum_j C[k; i, j] Y_e[j] rho_e[path], rho_e = phi_e path_w.
+// The coefficients come as rows over (k, i) pairs, q = k d + i: entries
+// cg_row[q] .. cg_row[q+1] - 1 of cg_col (j | path << 16) and cg_val.  Rows
+// are clamped to [0, cg_nnz] and entries with j >= d or path >= n_path are
+// skipped, so any table stays in bounds.  fp32 features only (feat in
+// launch_feature_layout's blocks with parts = 2, and its row scales).
+struct DenseArgs {
+  int N, E, L, d, C, n_radial, n_path, cg_nnz;
+  float sigma;             // r_cut / (n_radial - 1)
+  const int32_t* offsets;  // [N + 1]
+  const int32_t* perm;     // [E] sorted slot -> edge id
+  const int32_t* src;      // [E] by edge id
+  const float* edge_vec;   // [E, 3] by edge id
+  const int32_t* cg_row;   // [d * d + 1]
+  const int32_t* cg_col;   // [cg_nnz]
+  const float* cg_val;     // [cg_nnz]
+  const float* path_w;     // [n_radial, n_path]
+  const void* feat;        // operand blocks of x (parts = 2)
+  const float* row_scale;  // [N]
+  float* out;              // [N, d, C]
+};
+// Paths (l1, l2, l3) of the full product up to degree L.
+int dense_path_count(int L);
+hipError_t launch_dense_edge(const DenseArgs& a, hipStream_t s);
 // Workspace bytes of EdgeArgs::ef_ops: the output factor in 32x32x16 operand
 // blocks [ceil(d/32)][ceil(R/32)][2][parts][64 lanes] x 16 bytes (parts <= 2)
 // and, after them, its scale.

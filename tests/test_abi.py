@@ -160,3 +160,28 @@ def test_timer_bookkeeping_without_launches():
     ms, n = tdn.timer_read("cp_edge_fwd")
     assert ms == 0.0 and n == 0
     tdn.timer_enable(False)
+
+
+def _dense(p, ws_bytes=1 << 40, nnz=100, **override):
+    args = dict(x=FAKE, vec=FAKE, ei=FAKE, row=FAKE, col=FAKE, val=FAKE, pw=FAKE, W=FAKE, out=FAKE, z=None,
+                perm=FAKE, off=FAKE, ws=FAKE)
+    args.update(override)
+    return tdn.lib().tdn_dense_tp_forward(None if p is None else ctypes.byref(p), args["x"], args["vec"], args["ei"],
+                                          args["row"], args["col"], args["val"], nnz, args["pw"], args["W"],
+                                          args["out"], args["z"], args["perm"], args["off"], args["ws"], ws_bytes,
+                                          None)
+
+
+@pytest.mark.parametrize("L,n_path", [(0, 1), (1, 5), (2, 15), (3, 34), (4, 65), (5, 111), (6, 175)])
+def test_dense_forward_argument_checks(L, n_path):
+    # R must be the number of paths of degree L (Sec. 2: l1, l2 <= L,
+    # |l1 - l2| <= l3 <= min(l1 + l2, L))
+    good = _problem(L=L, R=n_path)
+    assert _dense(good, ws_bytes=0) == 4                       # everything else accepted
+    assert _dense(_problem(L=L, R=n_path + 1)) == 2
+    assert _dense(_problem(L=L, R=n_path, feat_dtype=tdn.TDN_BF16)) == 3
+    assert _dense(good, nnz=-1) == 2
+    assert _dense(None) == 1
+    for k in ["x", "vec", "ei", "row", "col", "val", "pw", "W", "out", "perm", "off", "ws"]:
+        assert _dense(good, **{k: None}) == 1, k
+    assert _dense(good, ws_bytes=0, nnz=0, col=None, val=None) == 4   # an empty table needs no entries
