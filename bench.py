@@ -2,7 +2,8 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--no-cpu-baseline] [--backward] [--eager] [--radius-graph]
-                    [--ablation-atomics] [--calibrate-copy]
+                    [--ablation-atomics] [--calibrate-copy] [--no-comparator]
+                    [--comparator-sweep]
 
 One step is one call of tdn_cp_tp_forward on the headline workload (64
 molecules x 50 atoms, 3200 nodes, ~151k edges within 6 A, L=4, C=128,
@@ -27,6 +28,17 @@ contraction runs on fp16 MFMA as three products of two-part fp16 splits
 the fp16 peak (2.5 PFLOP/s).  The CPU baseline times the oracle (the
 plain float64 per-edge implementation) on a bounded sample of the same
 workload on this host's cores.
+
+The "exact_cg_comparator" object (fp32 workloads; --no-comparator skips it)
+times tdn_dense_tp_forward, the exact CG tensor product with one radial
+weight per path (Sec. 2, Sec. 3.2), on the same edges, features and channel
+weight, and reports the CP edge pass's speed-up over it (edge kernel against
+edge kernel, whole forward against whole forward, eager launches).  Its
+algorithmic flops per launch are E (3 nnz(C) + 2 d^2 C): the per-edge matrix
+K_e = C x2 (Y_e rho_e) and its product with the gathered features.
+--comparator-sweep adds the same comparison for L = 1..6 on the headline
+graph (C = 128, R = 32 ceil(7 L^2 / 32) capped at 256, random factors):
+the analogue of the paper's speed-up-against-degree figure (Sec. 4.5).
 """
 from __future__ import annotations
 
@@ -47,6 +59,7 @@ PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_BF16_MFMA_TFLOPS = 2500.0
 PEAK_FP16_MFMA_TFLOPS = 2500.0
 FACTORS = os.path.join(ROOT, "tests", "golden", "factors")
+CG_TABLES = os.path.join(ROOT, "tests", "golden", "cg")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cp_edge_fwd.json")
 
 
@@ -75,6 +88,51 @@ def traffic_for(workload):
     if t.get("kernel_source_hash") != kernel_source_hash() or t.get("workload") != workload:
         return None
     return t.get("hbm_bytes_per_launch")
+
+
+def time_calls(fn, torch, tdn, kernel, steps, warmup=3):
+    """(average kernel ms from the library's HIP events, average ms per call)
+    over `steps` eager calls."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    tdn.timer_enable(True)
+    tdn.timer_read(kernel, reset=True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    tdn.timer_enable(False)
+    ms, n = tdn.timer_read(kernel, reset=True)
+    return ms / max(1, n), e0.elapsed_time(e1) / steps
+
+
+def exact_comparator(torch, tdn, L, x, vec, ei, W, r_cut, presorted, steps, n_radial, seed=0):
+    """Times tdn_dense_tp_forward on these inputs with seeded path weights."""
+    zc = np.load(os.path.join(CG_TABLES, f"cg_L{L}.npz"))
+    tab = tdn.cg_table(zc["M"], zc["path"], x.device)
+    rng = np.random.default_rng(seed)
+    pw = torch.from_numpy((rng.standard_normal((n_radial, tab.n_path)) / np.sqrt(n_radial)).astype(np.float32))
+    pw = pw.to(x.device)
+    N, d, C = x.shape
+    E = vec.shape[0]
+    ws = torch.empty(tdn.workspace_size(tdn.make_problem(L, C, tab.n_path, N, E, r_cut, n_radial))[0],
+                     dtype=torch.uint8, device=x.device)
+    out = torch.empty((N, d, C), dtype=torch.float32, device=x.device)
+    perm = torch.empty(E, dtype=torch.int32, device=x.device)
+    off = torch.empty(N + 1, dtype=torch.int32, device=x.device)
+
+    def call():
+        return tdn.dense_forward(x, vec, ei, tab, pw, W, r_cut=r_cut, edges_sorted=presorted, workspace=ws,
+                                 out=out, perm=perm, offsets=off)
+
+    k_ms, f_ms = time_calls(call, torch, tdn, "dense_edge_fwd", steps)
+    nnz = int(tab.col.shape[0])
+    flops = E * (3 * nnz + 2 * d * d * C)
+    return {"edge_kernel_ms": k_ms, "forward_ms": f_ms, "paths": tab.n_path, "cg_nnz": nnz,
+            "flops_per_launch": flops, "achieved_tflops": flops / (k_ms * 1e-3) / 1e12}
 
 
 def cpu_baseline(w, A, B, D, budget_s=12.0):
@@ -121,6 +179,10 @@ def main():
                          "and replayed, with the eager step timed beside it)")
     ap.add_argument("--radius-graph", action="store_true",
                     help="also time tdn_radius_graph on the workload's geometry (extra field)")
+    ap.add_argument("--no-comparator", action="store_true",
+                    help="skip timing the exact CG tensor product on the same edges")
+    ap.add_argument("--comparator-sweep", action="store_true",
+                    help="also compare the CP and exact forwards for L = 1..6 on this graph (extra field)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 256 MiB device copy (reference for rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -271,6 +333,42 @@ def main():
             "mfma": "v_mfma_f32_32x32x16_f16, three products of two-part fp16 splits per fp32 product",
             "flops_per_launch": executed, "achieved": executed / (edge_ms * 1e-3) / 1e12,
             "peak": PEAK_FP16_MFMA_TFLOPS, "frac": executed / (edge_ms * 1e-3) / 1e12 / PEAK_FP16_MFMA_TFLOPS}
+    if not bf16 and not args.no_comparator:
+        # the exact CG tensor product on the same edges, features and W
+        cmp_ = exact_comparator(torch, tdn, w["L"], x, vec, ei, W, w["r_cut"], w["presorted"], args.steps,
+                                w["n_radial"])
+        _, cp_fwd_ms = time_calls(step, torch, tdn, "cp_edge_fwd", args.steps)
+        cmp_.update({"kernel": "dense_edge_fwd", "cp_edge_kernel_ms": edge_ms, "cp_forward_ms": cp_fwd_ms,
+                     "cp_edge_kernel_speedup": cmp_["edge_kernel_ms"] / edge_ms,
+                     "cp_forward_speedup": cmp_["forward_ms"] / cp_fwd_ms,
+                     "frac_of_fp32_mfma_peak": cmp_["achieved_tflops"] / PEAK_FP32_MFMA_TFLOPS,
+                     "launch": "eager"})
+        line["exact_cg_comparator"] = cmp_
+    if args.comparator_sweep and not bf16:
+        rng = np.random.default_rng(1)
+        sweep = []
+        for Ls in range(1, 7):
+            ds = (Ls + 1) ** 2
+            Rs = min(256, 32 * -(-7 * Ls * Ls // 32))
+            Cs = 128
+            xs_ = t(rng.standard_normal((N, ds, Cs)).astype(np.float32))
+            Ws = t((rng.standard_normal((Cs, Cs)) / np.sqrt(Cs)).astype(np.float32))
+            fac = [t((rng.standard_normal((ds, Rs)) / np.sqrt(ds)).astype(np.float32)) for _ in range(3)]
+            rws = t((rng.standard_normal((w["n_radial"], Rs)) / np.sqrt(w["n_radial"])).astype(np.float32))
+
+            def cp_call():
+                return tdn.forward(xs_, vec, ei, fac[0], fac[1], fac[2], Ws, rws, L=Ls, r_cut=w["r_cut"],
+                                   edges_sorted=w["presorted"], save_z=False)
+
+            ck, cf = time_calls(cp_call, torch, tdn, "cp_edge_fwd", 20)
+            ex = exact_comparator(torch, tdn, Ls, xs_, vec, ei, Ws, w["r_cut"], w["presorted"], 20, w["n_radial"])
+            sweep.append({"L": Ls, "d": ds, "C": Cs, "R": Rs, "paths": ex["paths"], "cg_nnz": ex["cg_nnz"],
+                          "cp_edge_kernel_ms": ck, "exact_edge_kernel_ms": ex["edge_kernel_ms"],
+                          "cp_forward_ms": cf, "exact_forward_ms": ex["forward_ms"],
+                          "cp_edge_kernel_speedup": ex["edge_kernel_ms"] / ck,
+                          "cp_forward_speedup": ex["forward_ms"] / cf})
+            del xs_, Ws, fac, rws
+        line["comparator_sweep"] = sweep
     if args.ablation_atomics:
         # the same forward with the segmented sum replaced by per-edge
         # application of D and float atomics into Z

@@ -39,9 +39,12 @@ __device__ __forceinline__ f32x16 mfma_f16(u32x4 a, u32x4 b, f32x16 c) {
 
 constexpr int kMaxWaves = 4;
 
-__host__ __device__ constexpr int dense_dp(int d) { return d <= 32 ? 32 : 64; }  // rows and K, padded
-__host__ __device__ constexpr int dense_ks(int d) { return dense_dp(d) + 4; }   // LDS row stride (floats)
-__host__ __device__ constexpr int dense_eb(int d) { return d <= 32 ? 8 : 4; }   // edges per batch
+__host__ __device__ constexpr int dense_dp(int d) { return d <= 32 ? 32 : 64; }  // MFMA rows and K, padded
+// K_e in LDS: the d rows only, columns up to the next multiple of 8 (zero
+// past d), row stride 4 floats more (16-byte aligned, fewer bank conflicts)
+__host__ __device__ constexpr int dense_kc(int d) { return (d + 7) / 8 * 8; }
+__host__ __device__ constexpr int dense_ks(int d) { return dense_kc(d) + 4; }
+__host__ __device__ constexpr int dense_eb(int d) { return d <= 32 ? 8 : 4; }  // edges per batch
 
 struct DenseSmem {
   int off_k, off_y, off_phi, off_rho, off_row, off_sc, off_ksc, off_max, floats;
@@ -51,7 +54,7 @@ __host__ __device__ inline DenseSmem dense_smem(int d, int n_path) {
   DenseSmem s{};
   int o = 0;
   s.off_k = o;
-  o += eb * dense_dp(d) * dense_ks(d);
+  o += eb * d * dense_ks(d);
   s.off_y = o;
   o += eb * d;
   s.off_phi = o;
@@ -73,7 +76,7 @@ __host__ __device__ inline DenseSmem dense_smem(int d, int n_path) {
 template <int L, int CTW>
 __global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves) {
   constexpr int d = (L + 1) * (L + 1);
-  constexpr int DP = dense_dp(d), KS = dense_ks(d), EB = dense_eb(d);
+  constexpr int DP = dense_dp(d), KC = dense_kc(d), KS = dense_ks(d), EB = dense_eb(d);
   constexpr int KB = DP / 16, RK = DP / 32;
   extern __shared__ float smem[];
   const DenseSmem sm = dense_smem(d, a.n_path);
@@ -93,9 +96,9 @@ __global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves) {
   const int e0 = a.offsets[n], e1 = a.offsets[n + 1];
   const int P = a.n_path, nr = a.n_radial;
 
-  // K padding (rows and columns >= d) stays zero; every (k, i) with k, i < d
-  // is rewritten for each batch
-  for (int t = tid; t < EB * DP * KS; t += nthr) sK[t] = 0.f;
+  // K's padding columns (d .. KC-1) stay zero; every (k, i) with k, i < d is
+  // rewritten for each batch
+  for (int t = tid; t < EB * d * KS; t += nthr) sK[t] = 0.f;
 
   f32x16 acc[RK][CTW];
 #pragma unroll
@@ -128,11 +131,17 @@ __global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves) {
 #pragma unroll
     for (int r = 0; r < RK; ++r) {
       u32x4 hi[KB], lo[KB];
-      const float* kp = sK + (t * DP + r * kTile + l32) * KS + 8 * h;
+      const int row = r * kTile + l32;
+      const float* kp = sK + (t * d + (row < d ? row : 0)) * KS + 8 * h;
 #pragma unroll
       for (int b = 0; b < KB; ++b) {
-        const float4 f0 = *reinterpret_cast<const float4*>(kp + 16 * b);
-        const float4 f1 = *reinterpret_cast<const float4*>(kp + 16 * b + 4);
+        // rows >= d and column groups >= KC are zero (not stored)
+        const bool in = row < d && 16 * b + 8 * h < KC;
+        float4 f0 = make_float4(0.f, 0.f, 0.f, 0.f), f1 = f0;
+        if (in) {
+          f0 = *reinterpret_cast<const float4*>(kp + 16 * b);
+          f1 = *reinterpret_cast<const float4*>(kp + 16 * b + 4);
+        }
         uint32_t h0, h1, h2, h3, m0, m1, m2, m3;
         split_f16x2_pair(f0.x * ksc, f0.y * ksc, h0, m0);
         split_f16x2_pair(f0.z * ksc, f0.w * ksc, h1, m1);
@@ -191,19 +200,32 @@ __global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves) {
       float v[EB];
 #pragma unroll
       for (int e = 0; e < EB; ++e) v[e] = 0.f;
-      for (int s = s0; s < s1; ++s) {
-        const int col = a.cg_col[s];
-        const int j = col & 0xffff, p = col >> 16;
-        if (j >= d || p < 0 || p >= P) continue;  // malformed entry: ignored
-        const float c = a.cg_val[s];
+      // for d > 32 (rows of ~5 entries) four entries' loads issued together,
+      // then applied in order; one at a time below (fewer registers, more
+      // waves)
+      constexpr int U = d > 32 ? 4 : 1;
+      for (int s = s0; s < s1; s += U) {
+        int cl[U];
+        float cv[U];
 #pragma unroll
-        for (int e = 0; e < EB; ++e)
-          if (e < nb) v[e] = fmaf(c, sY[e * d + j] * sRho[e * P + p], v[e]);
+        for (int u = 0; u < U; ++u) {
+          const int su = s + u < s1 ? s + u : s0;
+          cl[u] = a.cg_col[su];
+          cv[u] = a.cg_val[su];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int j = cl[u] & 0xffff, p = cl[u] >> 16;
+          if (s + u >= s1 || j >= d || p < 0 || p >= P) continue;  // past the row, or malformed: ignored
+#pragma unroll
+          for (int e = 0; e < EB; ++e)
+            if (e < nb) v[e] = fmaf(cv[u], sY[e * d + j] * sRho[e * P + p], v[e]);
+        }
       }
 #pragma unroll
       for (int e = 0; e < EB; ++e)
         if (e < nb) {
-          sK[(e * DP + k) * KS + i] = v[e];
+          sK[(e * d + k) * KS + i] = v[e];
           mx[e] = fmaxf(mx[e], fabsf(v[e]));
         }
     }
