@@ -3,7 +3,7 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--no-cpu-baseline] [--backward] [--eager] [--radius-graph]
                     [--ablation-atomics] [--calibrate-copy] [--no-comparator]
-                    [--comparator-sweep]
+                    [--comparator-sweep] [--three-input]
 
 One step is one call of tdn_cp_tp_forward on the headline workload (64
 molecules x 50 atoms, 3200 nodes, ~151k edges within 6 A, L=4, C=128,
@@ -39,6 +39,9 @@ K_e = C x2 (Y_e rho_e) and its product with the gathered features.
 --comparator-sweep adds the same comparison for L = 1..6 on the headline
 graph (C = 128, R = 32 ceil(7 L^2 / 32) capped at 256, random factors):
 the analogue of the paper's speed-up-against-degree figure (Sec. 4.5).
+--three-input adds the three-input CP product (App. A, N = 3: source
+features, edge harmonics, destination features; tdn_cp_tp3_forward) on the
+same workload, timed beside the two-input forward.
 """
 from __future__ import annotations
 
@@ -183,6 +186,8 @@ def main():
                     help="skip timing the exact CG tensor product on the same edges")
     ap.add_argument("--comparator-sweep", action="store_true",
                     help="also compare the CP and exact forwards for L = 1..6 on this graph (extra field)")
+    ap.add_argument("--three-input", action="store_true",
+                    help="also time the three-input CP product on this workload (extra field; fp32, 2 <= L <= 4)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 256 MiB device copy (reference for rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -369,6 +374,19 @@ def main():
                           "cp_forward_speedup": ex["forward_ms"] / cf})
             del xs_, Ws, fac, rws
         line["comparator_sweep"] = sweep
+    if args.three_input and not bf16:
+        A2t = t((np.random.default_rng(5).standard_normal((d, R)) / np.sqrt(d)).astype(np.float32))
+
+        def step3():
+            return tdn.forward3(x, vec, ei, At, A2t, Bt, Dt, W, rw, L=w["L"], r_cut=w["r_cut"],
+                                edges_sorted=w["presorted"], workspace=ws, out=out, z=zsave, perm=perm,
+                                offsets=offsets)
+
+        k3, f3 = time_calls(step3, torch, tdn, "cp_edge_fwd_t3", args.steps)
+        _, f2 = time_calls(step, torch, tdn, "cp_edge_fwd", args.steps)
+        line["three_input"] = {"edge_kernel_ms": k3, "forward_ms": f3, "two_input_edge_kernel_ms": edge_ms,
+                               "two_input_forward_ms": f2, "edge_kernel_ratio": k3 / edge_ms,
+                               "value": E / (f3 * 1e-3), "launch": "eager"}
     if args.ablation_atomics:
         # the same forward with the segmented sum replaced by per-edge
         # application of D and float atomics into Z

@@ -129,6 +129,22 @@ tdn_status tdn_ablation_forward_atomics(const tdn_problem* p, const void* x, con
                                         float* out, float* z_save, int32_t* perm, int32_t* offsets,
                                         void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* The three-input CP product (App. A: an N-input multilinear map as
+ * A (B1^T x1 * ... * BN^T xN), here N = 3 with the source node's features,
+ * the edge's harmonics and the destination node's features):
+ *   Z[t] = sum over edges e = (s, t) of D (g_e * (A^T x[s]) * (A2^T x[t])),
+ *   g_e = (B^T Y_e) * (phi_e Wrad),   out = Z W.
+ * Arguments as tdn_cp_tp_forward, plus A2 [d, R] f32, the factor of the
+ * destination features; fp32 features and 2 <= L <= 4 only
+ * (TDN_ERR_BAD_DTYPE / TDN_ERR_BAD_SHAPE); the same workspace size.  Since
+ * A2^T x[t] is the same for every edge into t, it multiplies each node's
+ * summed messages once. */
+tdn_status tdn_cp_tp3_forward(const tdn_problem* p, const void* x, const float* edge_vec,
+                              const int32_t* edge_index, const float* A, const float* A2, const float* B,
+                              const float* D, const void* W, const float* radial_w, float* out, float* z_save,
+                              int32_t* perm, int32_t* offsets, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+
 /* The exact CG tensor product over the same edges, as the comparator of the
  * CP layer (Sec. 2 eq. clebsch_gordan summed over every path (l1, l2, l3)
  * with l1, l2 <= L and |l1 - l2| <= l3 <= min(l1 + l2, L); Sec. 3.2 for the
@@ -246,7 +262,7 @@ tdn_status tdn_spherical_harmonics(int32_t L, int32_t E, const float* edge_vec, 
  * tdn_timer_enable(1) starts recording every launch of the layer's edge
  * kernels; tdn_timer_read synchronises on the recorded events and returns
  * the summed milliseconds and launch count of the kernel named `kernel`
- * ("cp_edge_fwd", "cp_edge_fwd_atomic", "dense_edge_fwd", "radius_graph", "feature_layout",
+ * ("cp_edge_fwd", "cp_edge_fwd_atomic", "cp_edge_fwd_t3", "dense_edge_fwd", "radius_graph", "feature_layout",
  * "channel_layout", "cp_edge_bwd_src", "cp_bwd_dst", "radial_grad", "node_gemm", "gram",
  * "sort");
  * reset = 1 clears that kernel's record. */

@@ -99,6 +99,31 @@ def forward(x, edge_index, edge_vec, A, B, D, W, radial_w, r_cut, L,
     return (out, zsum) if return_z else out
 
 
+def forward3(x, edge_index, edge_vec, A, A2, B, D, W, radial_w, r_cut, L, perm=None):
+    """The three-input product (App. A, eq. multi-tp with N = 3 and its CP
+    form D (B1^T x1 * B2^T x2 * B3^T x3)), the inputs being the source node's
+    features, the edge's harmonics and the destination node's features:
+    per edge e = (s, t),  h_e = g_e * (A^T x[s]) * (A2^T x[t]),  z_e = D h_e,
+    m_e = z_e W,  out[t] = sum of m_e (sorted order).  Float64."""
+    x, A, A2, B, D, W = _f64(x, A, A2, B, D, W)
+    N, d, C = x.shape
+    src = np.asarray(edge_index[0], np.int64)
+    dst = np.asarray(edge_index[1], np.int64)
+    if perm is None:
+        perm, _ = stable_sort_by_key(dst, N)
+    perm = np.asarray(perm, np.int64)
+    out = np.zeros((N, d, C))
+    for c0 in range(0, perm.shape[0], CHUNK):
+        ids = perm[c0:c0 + CHUNK]
+        _, _, _, _, g = edge_terms(np.asarray(edge_vec)[ids], L, B, radial_w, r_cut)
+        u = np.matmul(A.T[None], x[src[ids]])              # [e, R, C]
+        u2 = np.matmul(A2.T[None], x[dst[ids]])            # [e, R, C]
+        h = g[:, :, None] * u * u2
+        z = np.matmul(D[None], h)
+        np.add.at(out, dst[ids], z @ W)
+    return out
+
+
 # ----------------------------------------------------------------- backward
 def backward(x, edge_index, edge_vec, A, B, D, W, radial_w, r_cut, L, grad_out,
              perm=None, return_radial=False):

@@ -69,6 +69,7 @@ def lib() -> ctypes.CDLL:
         L.tdn_cp_tp_forward.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
         L.tdn_ablation_forward_atomics.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
         L.tdn_cp_tp_backward.argtypes = [PP] + [_P] * 17 + [_SZ, _P]
+        L.tdn_cp_tp3_forward.argtypes = [PP] + [_P] * 14 + [_SZ, _P]
         L.tdn_dense_tp_forward.argtypes = [PP] + [_P] * 6 + [ctypes.c_int32] + [_P] * 7 + [_SZ, _P]
         GP = ctypes.POINTER(GraphProblem)
         L.tdn_radius_graph_workspace_size.argtypes = [GP, ctypes.POINTER(_SZ)]
@@ -85,7 +86,8 @@ def lib() -> ctypes.CDLL:
         L.tdn_last_hip_error.restype = ctypes.c_int32
         for f in ("tdn_workspace_size", "tdn_cp_tp_forward", "tdn_ablation_forward_atomics", "tdn_cp_tp_backward",
                   "tdn_sort_workspace_size", "tdn_sort_by_key", "tdn_spherical_harmonics", "tdn_timer_enable",
-                  "tdn_timer_read", "tdn_radius_graph_workspace_size", "tdn_radius_graph", "tdn_dense_tp_forward"):
+                  "tdn_timer_read", "tdn_radius_graph_workspace_size", "tdn_radius_graph", "tdn_dense_tp_forward",
+                  "tdn_cp_tp3_forward"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -193,6 +195,48 @@ def forward(x, edge_vec, edge_index, A, B, D, W, radial_w, *, L: int, r_cut: flo
     _check(st, name)
     return ForwardResult(out, z, perm, offsets, p,
                          dict(x=x, edge_vec=edge_vec, edge_index=edge_index, A=A, B=B, D=D, W=W, radial_w=radial_w))
+
+
+def forward3(x, edge_vec, edge_index, A, A2, B, D, W, radial_w, *, L: int, r_cut: float, edges_sorted=False,
+             validate=False, workspace=None, out=None, z=None, perm=None, offsets=None,
+             stream=None) -> ForwardResult:
+    """Runs tdn_cp_tp3_forward, the three-input CP product whose third input
+    is the destination node's features (A2 [d, R] its factor); float32
+    features, 2 <= L <= 4.  Other arguments as in forward()."""
+    dev = x.device
+    N, d, C = x.shape
+    E = edge_vec.shape[0]
+    R = A.shape[1]
+    if edge_index.dtype != torch.int32:
+        edge_index = edge_index.to(torch.int32)
+    edge_index = edge_index.contiguous()
+    for t, n, dt, sh in [(x, "x", torch.float32, (N, d, C)), (edge_vec, "edge_vec", torch.float32, (E, 3)),
+                         (edge_index, "edge_index", torch.int32, (2, E)), (A, "A", torch.float32, (d, R)),
+                         (A2, "A2", torch.float32, (d, R)), (B, "B", torch.float32, (d, R)),
+                         (D, "D", torch.float32, (d, R)), (W, "W", torch.float32, (C, C)),
+                         (radial_w, "radial_w", torch.float32, (radial_w.shape[0], R))]:
+        _need(t, n, dt, sh, dev)
+    p = make_problem(L, C, R, N, E, r_cut, radial_w.shape[0], TDN_F32, edges_sorted, validate)
+    fwd_bytes, _ = workspace_size(p)
+    if workspace is None or workspace.numel() < fwd_bytes:
+        workspace = torch.empty(max(fwd_bytes, 1), dtype=torch.uint8, device=dev)
+    if out is None:
+        out = torch.empty((N, d, C), dtype=torch.float32, device=dev)
+    if perm is None:
+        perm = torch.empty(max(E, 1), dtype=torch.int32, device=dev)[:E]
+    if offsets is None:
+        offsets = torch.empty(N + 1, dtype=torch.int32, device=dev)
+    _need(out, "out", torch.float32, (N, d, C), dev)
+    if z is not None:
+        _need(z, "z", torch.float32, (N, d, C), dev)
+    _need(perm, "perm", torch.int32, (E,), dev)
+    _need(offsets, "offsets", torch.int32, (N + 1,), dev)
+    st = lib().tdn_cp_tp3_forward(ctypes.byref(p), _ptr(x), _ptr(edge_vec), _ptr(edge_index), _ptr(A), _ptr(A2),
+                                  _ptr(B), _ptr(D), _ptr(W), _ptr(radial_w), _ptr(out), _ptr(z), _ptr(perm),
+                                  _ptr(offsets), _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "tdn_cp_tp3_forward")
+    return ForwardResult(out, z, perm, offsets, p, dict(x=x, edge_vec=edge_vec, edge_index=edge_index, A=A, A2=A2,
+                                                        B=B, D=D, W=W, radial_w=radial_w))
 
 
 @dataclass

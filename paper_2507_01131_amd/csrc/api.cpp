@@ -83,8 +83,11 @@ size_t xt_xc_bytes(const tdn_problem& p) {
 // slots of the edge pass (two [d, C] rows per edge range)
 size_t ef_pad_bytes(const tdn_problem& p) { return al(tdn::edge_ef_bytes(dim_of(p.L), p.R)); }
 size_t partial_bytes(const tdn_problem& p) {
-  const tdn::EdgePlan pl = tdn::edge_plan(p.L, p.R, p.C, p.n_radial, p.feat_dtype == TDN_BF16, p.n_edges);
-  return ef_pad_bytes(p) + size_t(pl.n_range) * 2 * dim_of(p.L) * p.C * 4;
+  const bool bf16 = p.feat_dtype == TDN_BF16;
+  int n_range = tdn::edge_plan(p.L, p.R, p.C, p.n_radial, bf16, p.n_edges).n_range;
+  if (!bf16 && p.L >= 2 && p.L <= 4)  // the three-input product's plan may use more ranges
+    n_range = std::max(n_range, tdn::edge_plan(p.L, p.R, p.C, p.n_radial, false, p.n_edges, true).n_range);
+  return ef_pad_bytes(p) + size_t(n_range) * 2 * dim_of(p.L) * p.C * 4;
 }
 
 struct FwdLayout {
@@ -215,7 +218,7 @@ tdn_status run_validation(const tdn_problem& p, const int32_t* edge_index, const
 
 tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int32_t* perm, const int32_t* gather,
                         const int32_t* key, const float* edge_vec, const float* KF, const float* EF, const float* B,
-                        const float* radial_w, const void* feat, float* out, float* partial) {
+                        const float* radial_w, const void* feat, float* out, float* partial, bool t3 = false) {
   tdn::EdgeArgs a{};
   a.n_seg = p.n_nodes;
   a.E = p.n_edges;
@@ -236,7 +239,7 @@ tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int3
   a.radial_w = radial_w;
   a.feat = feat;
   a.out = out;
-  const tdn::EdgePlan pl = tdn::edge_plan(p.L, p.R, p.C, p.n_radial, p.feat_dtype == TDN_BF16, p.n_edges);
+  const tdn::EdgePlan pl = tdn::edge_plan(p.L, p.R, p.C, p.n_radial, p.feat_dtype == TDN_BF16, p.n_edges, t3);
   a.n_range = pl.n_range;
   a.pieces_per_block = pl.per_block;
   a.ef_ops = partial;
@@ -358,6 +361,57 @@ tdn_status tdn_ablation_forward_atomics(const tdn_problem* p, const void* x, con
                                         hipStream_t stream) {
   return forward_impl(p, x, edge_vec, edge_index, A, B, D, W, radial_w, out, z_save, perm, offsets, workspace,
                       workspace_bytes, stream, true);
+}
+
+tdn_status tdn_cp_tp3_forward(const tdn_problem* p, const void* x, const float* edge_vec, const int32_t* edge_index,
+                              const float* A, const float* A2, const float* B, const float* D, const void* W,
+                              const float* radial_w, float* out, float* z_save, int32_t* perm, int32_t* offsets,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  tdn_status st = check_problem(p);
+  if (st != TDN_OK) return st;
+  if (p->feat_dtype != TDN_F32) return TDN_ERR_BAD_DTYPE;
+  if (p->L < 2 || p->L > 4) return TDN_ERR_BAD_SHAPE;
+  const int N = p->n_nodes, E = p->n_edges, d = dim_of(p->L), C = p->C;
+  if (!A || !A2 || !B || !D || !W || !radial_w || !offsets || !workspace) return TDN_ERR_NULL_POINTER;
+  if (N > 0 && (!x || !out)) return TDN_ERR_NULL_POINTER;
+  if (E > 0 && (!edge_vec || !edge_index || !perm)) return TDN_ERR_NULL_POINTER;
+  const FwdLayout lay = fwd_layout(*p);
+  if (workspace_bytes < lay.total) return TDN_ERR_WORKSPACE_TOO_SMALL;
+  st = check_device();
+  if (st != TDN_OK) return st;
+  char* ws = static_cast<char*>(workspace);
+  if (p->validate) {
+    st = run_validation(*p, edge_index, edge_vec, ws, lay.flags, p->edges_sorted, stream);
+    if (st != TDN_OK) return st;
+  }
+  const int32_t* src = edge_index;
+  const int32_t* dst = E > 0 ? edge_index + E : nullptr;
+  {
+    Timed t("sort", stream);
+    if (p->edges_sorted || E == 0)
+      TDN_HIP(tdn::launch_offsets_presorted(N, E, dst, perm, offsets, stream));
+    else
+      TDN_HIP(tdn::launch_sort(tdn::sort_plan(N, E), dst, 1, perm, offsets, ws + lay.sort, stream));
+  }
+  if (N == 0) return TDN_OK;
+  float* Z = z_save ? z_save : reinterpret_cast<float*>(ws + lay.z);
+  void* xt = ws + lay.xt;
+  {
+    Timed t("feature_layout", stream);
+    TDN_HIP(tdn::launch_feature_layout(N, d, C, x, true, 2, xt, row_scales(*p, xt), stream));
+  }
+  {
+    Timed t("cp_edge_fwd_t3", stream);
+    tdn::EdgeArgs a = edge_args(*p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, xt, Z,
+                                reinterpret_cast<float*>(ws + lay.part), true);
+    a.KF2 = A2;
+    TDN_HIP(tdn::launch_cp_edge_t3(a, stream));
+  }
+  {
+    Timed t("node_gemm", stream);
+    TDN_HIP(tdn::launch_node_gemm(N * d, C, Z, W, false, 0, out, ws + lay.wp, stream));
+  }
+  return TDN_OK;
 }
 
 tdn_status tdn_dense_tp_forward(const tdn_problem* p, const void* x, const float* edge_vec,

@@ -107,13 +107,13 @@ size_t edge_ef_bytes(int d, int R) {
   return blocks + 256;
 }
 
-EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E) {
+EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E, bool t3) {
   using namespace edge_detail;
   if (E <= 0) return EdgePlan{0, 0};
   const int RT = (R + kTile - 1) / kTile, d = (L + 1) * (L + 1);
   const EdgeGrid gr = edge_grid(C, RT, bf16);
   // workgroups per CU: as many as the wave slots (four SIMDs) and LDS allow
-  const int lds = edge_smem(RT, bf16, d, n_radial, edge_chunk(L, RT, bf16, n_radial)).floats * 4;
+  const int lds = edge_smem(RT, bf16, d, n_radial, edge_chunk(L, RT, bf16, n_radial, t3), t3).floats * 4;
   int per_cu = 160 * 1024 / lds;
   const int by_waves = 4 * edge_waves_per_eu(L, RT, bf16) / gr.waves;
   if (per_cu > by_waves) per_cu = by_waves;
@@ -178,6 +178,35 @@ hipError_t launch_cp_edge_atomic(const EdgeArgs& a, hipStream_t s) {
     case 3: return launch_cp_edge_atomic_l<3>(a, s);
     default: return launch_cp_edge_atomic_l<4>(a, s);
   }
+}
+
+}  // namespace tdn
+
+namespace tdn {
+
+hipError_t launch_cp_edge_t3(const EdgeArgs& a, hipStream_t s) {
+  using namespace edge_detail;
+  if (a.parts != 2 || a.L < 2 || a.L > 4 || !a.KF2) return hipErrorInvalidValue;
+  if (a.E > 0 && (a.n_range < 1 || a.n_range > a.E || a.pieces_per_block < 1 || a.n_range % a.pieces_per_block ||
+                  !a.ef_ops || !a.ef_scale || !a.row_scale))
+    return hipErrorInvalidValue;
+  hipError_t e = hipSuccess;
+  if (a.E > 0) {
+    const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
+    k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops),
+                                                  a.ef_scale);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  switch (a.L) {
+    case 2: e = launch_cp_edge_t3_l<2>(a, s); break;
+    case 3: e = launch_cp_edge_t3_l<3>(a, s); break;
+    default: e = launch_cp_edge_t3_l<4>(a, s); break;
+  }
+  if (e != hipSuccess) return e;
+  if (a.n_seg > 0)
+    k_range_fixup<<<dim3(a.n_seg), dim3(256), 0, s>>>(a.E, a.n_range, a.d * a.C, a.offsets, a.partial, a.out);
+  return hipGetLastError();
 }
 
 }  // namespace tdn

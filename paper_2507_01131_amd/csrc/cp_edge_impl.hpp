@@ -114,7 +114,7 @@ __host__ __device__ constexpr int edge_max_ranges(int L, int RT, bool bf) {
 __host__ __device__ constexpr bool edge_reg_kf(int, int) { return false; }
 
 struct EdgeSmem {
-  int Rp, off_a, off_g, off_y, off_vec, off_phi, off_idx, off_sc, off_bnd, floats;
+  int Rp, off_a, off_g, off_y, off_vec, off_phi, off_idx, off_sc, off_bnd, off_a2, floats;
 };
 
 // LDS regions (in floats): the factor operands, split mode
@@ -123,8 +123,9 @@ struct EdgeSmem {
 // rounded up to a whole 32-row tile), harmonics, normalised edge vectors with
 // their lengths, radial basis, gathered rows, the edges' operand scales, and
 // the segment starts of the chunk (positions, keys, count and the two
-// partial-segment flags).
-__host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radial, int chunk) {
+// partial-segment flags); with t3 (the three-input product) last the second
+// node factor's operands in the layout of the first.
+__host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radial, int chunk, bool t3 = false) {
   EdgeSmem s{};
   s.Rp = RT * kTile;
   int o = 0;
@@ -145,6 +146,9 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radi
   o += chunk;
   s.off_bnd = o;
   o += 2 * chunk + 4;
+  o = (o + 3) & ~3;
+  s.off_a2 = o;
+  if (t3) o += edge_kb(d) * RT * 2 * kWave * 4;
   s.floats = o;
   return s;
 }
@@ -153,7 +157,13 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radi
 // epilogue applies EF per edge, and it adds Z into `out` with float atomics
 // instead of storing the segment sums (`out` zeroed beforehand; no partial
 // slots, no fix-up) -- the naive scatter-add the segmented sum replaces.
-template <int L, int RT, bool BF, bool ATOM = false>
+// T3 (fp32 features, forward): the three-input product of the N-input CP
+// form (App. A) with the destination node's features as the third input,
+//   Z_t = D (V_t * sum_e g_e * U_e),  V_t = KF2^T x[t];
+// V_t is the same for every edge of the segment, so it multiplies the
+// accumulated sum once, in the epilogue (also for partial segments: the
+// epilogue is linear in the sum).
+template <int L, int RT, bool BF, bool ATOM = false, bool T3 = false>
 __global__ __launch_bounds__(kMaxWavesPerBlock* kWave)
 __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edge(EdgeArgs a, int n_cgrp, int waves,
                                                                                   int chunk) {
@@ -166,8 +176,9 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   constexpr int Rp = RT * kTile;
   constexpr int MT = (d + kTile - 1) / kTile;
   extern __shared__ float smem[];
-  const EdgeSmem S = edge_smem(RT, BF, d, a.n_radial, chunk);
+  const EdgeSmem S = edge_smem(RT, BF, d, a.n_radial, chunk, T3);
   u32x4* sA = reinterpret_cast<u32x4*>(smem + S.off_a);
+  u32x4* sA2 = reinterpret_cast<u32x4*>(smem + S.off_a2);
   float4* sAf = reinterpret_cast<float4*>(smem + S.off_a);
   float* sG = smem + S.off_g;
   float* sY = smem + S.off_y;
@@ -203,6 +214,33 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
     const int e = f16_split_exponent(mx);
     kf_sc = ldexpf(1.f, -e);
     kf_unsc = ldexpf(1.f, e);
+  }
+  // T3: the same for the second node factor (its own slots of sG)
+  float kf2_sc = 1.f, kf2_unsc = 1.f;
+  if constexpr (T3) {
+    float mx = 0.f;
+    for (int i = tid; i < d * R; i += blockDim.x) mx = fmaxf(mx, fabsf(a.KF2[i]));
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    if (lane == 0) sG[kMaxWavesPerBlock + wave] = mx;
+    __syncthreads();
+    for (int w = 0; w < int(blockDim.x / kWave); ++w) mx = fmaxf(mx, sG[kMaxWavesPerBlock + w]);
+    const int e = f16_split_exponent(mx);
+    kf2_sc = ldexpf(1.f, -e);
+    kf2_unsc = ldexpf(1.f, e);
+    for (int t = tid; t < KB * RT * kWave; t += blockDim.x) {
+      const int ln = t % kWave, brt = t / kWave;
+      const int b = brt / RT, rt = brt - b * RT;
+      const int r = rt * kTile + (ln & 31), k0 = 16 * b + 8 * (ln >> 5);
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = k0 + i < d && r < R ? a.KF2[(k0 + i) * R + r] : 0.f;
+      uint32_t w[2][4];
+#pragma unroll
+      for (int p = 0; p < 4; ++p) split_f16x2_pair(v[2 * p] * kf2_sc, v[2 * p + 1] * kf2_sc, w[0][p], w[1][p]);
+#pragma unroll
+      for (int s = 0; s < 2; ++s) sA2[(brt * 2 + s) * kWave + ln] = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
+    }
   }
   // Factor operands: lane (l32, h) of K-block b, rank tile rt holds
   // KF[16b + 8h + i][rt*32 + l32], i = 0..7, zero past d and R, as the fp16
@@ -255,6 +293,32 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   auto finish = [&](int seg, int part) {
     float* dst = (ATOM || part < 0) ? a.out + size_t(seg) * d * C : a.partial + (size_t(range) * 2 + part) * d * C;
     constexpr int P16 = BF ? 1 : 2;
+    if constexpr (T3) {
+      // V = KF2^T x[seg] for this lane's rank rows and channel, from the
+      // three part products, times the two operands' scales; H *= V
+      const int n_ct = (C + kTile - 1) / kTile;
+      const int ct = min((cgrp * waves + wave) * CT, n_ct - 1);
+      const char* p = static_cast<const char*>(a.feat) + size_t(seg) * (size_t(n_ct) * 2 * KB * 1024) +
+                      ct * 2 * KB * 1024 + h * 512 + l32 * 16;
+      u32x4 xv[2][KB];
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int b = 0; b < KB; ++b) xv[s][b] = *reinterpret_cast<const u32x4*>(p + (s * KB + b) * 1024);
+      const float vsc = a.row_scale[seg] * kf2_unsc;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        f32x16 u = f32x16{};
+#pragma unroll
+        for (int b = 0; b < KB; ++b) u = mfma_f16(sA2[((b * RT + rt) * 2 + 1) * kWave + lane], xv[0][b], u);
+#pragma unroll
+        for (int b = 0; b < KB; ++b) u = mfma_f16(sA2[((b * RT + rt) * 2 + 0) * kWave + lane], xv[1][b], u);
+#pragma unroll
+        for (int b = 0; b < KB; ++b) u = mfma_f16(sA2[((b * RT + rt) * 2 + 0) * kWave + lane], xv[0][b], u);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[rt][0][v] *= u[v] * vsc;
+      }
+    }
     float hsc = 1.f, zsc = 1.f;
     if constexpr (!BF) {
       float mx = 0.f;
@@ -587,11 +651,11 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
 
 // Edge chunk of a block: the largest power of two <= 64 (at least 8) whose
 // LDS fits the block's share of the CU (160 KB over the blocks per CU).
-inline int edge_chunk(int L, int RT, bool bf, int n_radial) {
+inline int edge_chunk(int L, int RT, bool bf, int n_radial, bool t3 = false) {
   const int d = (L + 1) * (L + 1);
   const int budget = 160 * 1024 / edge_waves_per_eu(L, RT, bf);
   int chunk = 64;
-  while (chunk > 8 && edge_smem(RT, bf, d, n_radial, chunk).floats * 4 > budget) chunk >>= 1;
+  while (chunk > 8 && edge_smem(RT, bf, d, n_radial, chunk, t3).floats * 4 > budget) chunk >>= 1;
   return chunk;
 }
 
@@ -607,15 +671,15 @@ inline EdgeGrid edge_grid(int C, int RT, bool bf) {
   return EdgeGrid{waves, (wave_tiles + waves - 1) / waves};
 }
 
-template <int L, int RT, bool BF, bool ATOM = false>
+template <int L, int RT, bool BF, bool ATOM = false, bool T3 = false>
 hipError_t launch_l_rt_m(const EdgeArgs& a, hipStream_t s) {
   constexpr int d = (L + 1) * (L + 1);
   const EdgeGrid gr = edge_grid(a.C, RT, BF);
   const int waves = gr.waves, n_cgrp = gr.n_cgrp;
   if (a.E > 0) {
-    const int chunk = edge_chunk(L, RT, BF, a.n_radial);
-    const size_t lds = size_t(edge_smem(RT, BF, d, a.n_radial, chunk).floats) * 4;
-    auto k = k_cp_edge<L, RT, BF, ATOM>;
+    const int chunk = edge_chunk(L, RT, BF, a.n_radial, T3);
+    const size_t lds = size_t(edge_smem(RT, BF, d, a.n_radial, chunk, T3).floats) * 4;
+    auto k = k_cp_edge<L, RT, BF, ATOM, T3>;
     hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
@@ -656,6 +720,22 @@ hipError_t launch_cp_edge_atomic_l(const EdgeArgs& a, hipStream_t s) {
     case 6: return launch_l_rt_m<L, 6, false, true>(a, s);
     case 7: return launch_l_rt_m<L, 7, false, true>(a, s);
     case 8: return launch_l_rt_m<L, 8, false, true>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// The three-input product's dispatch on the rank tiles (fp32 features only).
+template <int L>
+hipError_t launch_cp_edge_t3_l(const EdgeArgs& a, hipStream_t s) {
+  switch ((a.R + kTile - 1) / kTile) {
+    case 1: return launch_l_rt_m<L, 1, false, false, true>(a, s);
+    case 2: return launch_l_rt_m<L, 2, false, false, true>(a, s);
+    case 3: return launch_l_rt_m<L, 3, false, false, true>(a, s);
+    case 4: return launch_l_rt_m<L, 4, false, false, true>(a, s);
+    case 5: return launch_l_rt_m<L, 5, false, false, true>(a, s);
+    case 6: return launch_l_rt_m<L, 6, false, false, true>(a, s);
+    case 7: return launch_l_rt_m<L, 7, false, false, true>(a, s);
+    case 8: return launch_l_rt_m<L, 8, false, false, true>(a, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -48,6 +48,7 @@ struct EdgeArgs {
   const float* EF;           // [d, R]
   const float* Bf;           // [d, R]
   const float* radial_w;     // [n_radial, R]
+  const float* KF2;          // [d, R] second node factor of the three-input product (launch_cp_edge_t3 only)
   const void* feat;          // [n_feat_rows, d, C]
   float* out;                // [n_seg, d, C]
   int n_range;               // edge ranges (EdgePlan::n_range)
@@ -66,7 +67,7 @@ struct EdgeArgs {
 struct EdgePlan {
   int n_range, per_block;
 };
-EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E);
+EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E, bool t3 = false);
 // Features for the edge pass: x [N, d, C] -> 32x32x16 MFMA operand blocks
 // xs [N, ceil(C/32), parts, edge_kpad(d)/16, 2, 32, 8] of 16-bit values,
 // element [n][ct][s][b][h][c][i] = part s of x[n][16b + 8h + i][32ct + c],
@@ -94,6 +95,12 @@ hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
 // per edge and Z accumulated into `out` (zeroed first) with float atomics;
 // nondeterministic in the order of the additions.
 hipError_t launch_cp_edge_atomic(const EdgeArgs& a, hipStream_t s);
+// The three-input product (App. A, N = 3: source features, edge harmonics,
+// destination features): as launch_cp_edge, with each segment's sum
+// multiplied by V_t = KF2^T x[t] (t = the segment's node, a row of feat)
+// before EF is applied.  fp32 features, 2 <= L <= 4; the plan must come from
+// edge_plan(..., t3 = true).
+hipError_t launch_cp_edge_t3(const EdgeArgs& a, hipStream_t s);
 
 // The exact CG tensor product over the sorted edges (the comparator of the CP
 // edge pass): out[n] = sum over edges e into n of K_e x[src_e] with

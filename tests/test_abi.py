@@ -185,3 +185,25 @@ def test_dense_forward_argument_checks(L, n_path):
     for k in ["x", "vec", "ei", "row", "col", "val", "pw", "W", "out", "perm", "off", "ws"]:
         assert _dense(good, **{k: None}) == 1, k
     assert _dense(good, ws_bytes=0, nnz=0, col=None, val=None) == 4   # an empty table needs no entries
+
+
+def _tp3(p, ws_bytes=1 << 40, **override):
+    args = dict(x=FAKE, vec=FAKE, ei=FAKE, A=FAKE, A2=FAKE, B=FAKE, D=FAKE, W=FAKE, rw=FAKE, out=FAKE, z=None,
+                perm=FAKE, off=FAKE, ws=FAKE)
+    args.update(override)
+    return tdn.lib().tdn_cp_tp3_forward(None if p is None else ctypes.byref(p), args["x"], args["vec"], args["ei"],
+                                        args["A"], args["A2"], args["B"], args["D"], args["W"], args["rw"],
+                                        args["out"], args["z"], args["perm"], args["off"], args["ws"], ws_bytes, None)
+
+
+def test_three_input_forward_argument_checks():
+    good = _problem(L=4)
+    assert _tp3(good, ws_bytes=0) == 4
+    assert _tp3(_problem(L=1)) == 2 and _tp3(_problem(L=5)) == 2      # 2 <= L <= 4
+    assert _tp3(_problem(feat_dtype=tdn.TDN_BF16)) == 3
+    assert _tp3(None) == 1
+    for k in ["x", "vec", "ei", "A", "A2", "B", "D", "W", "rw", "out", "perm", "off", "ws"]:
+        assert _tp3(good, **{k: None}) == 1, k
+    # the workspace covers the three-input product's edge ranges too
+    f, _ = tdn.workspace_size(good)
+    assert _tp3(good, ws_bytes=f - 1) == 4

@@ -189,3 +189,67 @@ def test_sampled_forward_matches_full():
     sub = layer.forward_at_nodes(nodes, f["x"], w["edge_index"], f["edge_vec"], A, B, D, f["W"],
                                  f["radial_w"], w["r_cut"], L)
     np.testing.assert_array_equal(sub, out[nodes])
+
+
+# ------------------------------------------------------------ three-input product (App. A)
+def _tp3_graph(seed, L, R, N=10, E=60, C=3):
+    return workloads.random_graph(seed, n_nodes=N, n_edges=E, L=L, C=C, R=R)
+
+
+def test_three_input_with_constant_third_factor_is_the_two_input_layer():
+    # A2 = e_0 (one in the degree-0 row) and x[:, 0, :] = 1 make A2^T x[t] = 1
+    L, R = 2, 6
+    w = _tp3_graph(1, L, R)
+    rng = np.random.default_rng(2)
+    A, B, D = (rng.normal(size=((L + 1) ** 2, R)) for _ in range(3))
+    x = np.array(w["x"], np.float64)
+    x[:, 0, :] = 1.0
+    A2 = np.zeros_like(A)
+    A2[0, :] = 1.0
+    got = layer.forward3(x, w["edge_index"], w["edge_vec"], A, A2, B, D, w["W"], w["radial_w"], w["r_cut"], L)
+    want = layer.forward(x, w["edge_index"], w["edge_vec"], A, B, D, w["W"], w["radial_w"], w["r_cut"], L)
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-12 * np.max(np.abs(want)))
+
+
+def _cg3_factors(L):
+    """Exact CP factors of T[k, i, j, l] = sum_m M[k, m, l] M[m, i, j], the
+    trilinear map M(M(x, y), z): one rank per (i, j, l)."""
+    M = cg_tensor.cg_tensor(L)
+    T = np.einsum("kml,mij->kijl", M, M)
+    d = M.shape[0]
+    idx = [(i, j, l) for i in range(d) for j in range(d) for l in range(d) if np.any(T[:, i, j, l] != 0)]
+    A = np.zeros((d, len(idx)))
+    B = np.zeros((d, len(idx)))
+    A2 = np.zeros((d, len(idx)))
+    D = np.zeros((d, len(idx)))
+    for r, (i, j, l) in enumerate(idx):
+        A[i, r] = B[j, r] = A2[l, r] = 1.0
+        D[:, r] = T[:, i, j, l]
+    return T, A, A2, B, D
+
+
+def test_three_input_exact_factors_give_the_nested_cg_product_and_equivariance():
+    L = 1
+    T, A, A2, B, D = _cg3_factors(L)
+    R = A.shape[1]
+    w = _tp3_graph(3, L, R)
+    rw = np.repeat(np.random.default_rng(4).normal(size=(8, 1)), R, axis=1)   # one radial weight per edge
+    got = layer.forward3(w["x"], w["edge_index"], w["edge_vec"], A, A2, B, D, w["W"], rw, w["r_cut"], L)
+    vec = w["edge_vec"].astype(np.float64)
+    Y = sh.spherical_harmonics(L, vec)
+    phi, _ = layer.radial_basis(np.linalg.norm(vec, axis=1), w["r_cut"], 8)
+    rho = (phi @ rw)[:, 0]
+    s, t = w["edge_index"]
+    x = w["x"].astype(np.float64)
+    # brute force: M(M(x[s], Y), x[t]) channel by channel, scaled by rho
+    M = cg_tensor.cg_tensor(L)
+    inner = np.einsum("mij,eic,ej->emc", M, x[s], Y)
+    msg = np.einsum("kml,emc,elc->ekc", M, inner, x[t]) * rho[:, None, None]
+    want = np.zeros_like(got)
+    np.add.at(want, t, msg @ w["W"].astype(np.float64))
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-12 * np.max(np.abs(want)))
+    Rm = wigner.random_rotation(np.random.default_rng(5))
+    Dr = wigner.wigner_d_full(L, Rm)
+    x2 = np.einsum("ab,nbc->nac", Dr, x)
+    got2 = layer.forward3(x2, w["edge_index"], vec @ Rm.T, A, A2, B, D, w["W"], rw, w["r_cut"], L)
+    np.testing.assert_allclose(got2, np.einsum("ab,nbc->nac", Dr, got), rtol=0, atol=1e-10 * np.max(np.abs(got)))
