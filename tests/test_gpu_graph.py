@@ -76,3 +76,56 @@ def test_forward_and_backward_replays_match_eager(N, E, L, C, R, sort):
     eager = tdn.forward(*args, L=L, r_cut=w["r_cut"], edges_sorted=sort).out
     torch.cuda.synchronize()
     assert torch.equal(got, eager) and not torch.equal(got, ref[0])
+
+
+def _replays_match(call, outs, k=3):
+    """Captures call() once, replays it k times with the outputs cleared and
+    eager work in between, and compares every replay bit for bit with the
+    eager result."""
+    call()
+    torch.cuda.synchronize()
+    ref = [o.clone() for o in outs]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        call()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call()
+    for i in range(k):
+        for o in outs:
+            o.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(outs, ref):
+            assert torch.equal(a, b), i
+        other = torch.randn(700, 700, device="cuda")
+        (other @ other).sum().item()
+
+
+def test_exact_comparator_and_three_input_replays_match_eager():
+    import os
+
+    L, C, R, N, E = 3, 64, 64, 60, 1500
+    w, inp = _inputs(17, N, E, L, C, R, False)
+    d = (L + 1) ** 2
+    out = torch.empty((N, d, C), device="cuda")
+    perm = torch.empty(E, dtype=torch.int32, device="cuda")
+    off = torch.empty(N + 1, dtype=torch.int32, device="cuda")
+    A2 = torch.from_numpy(random_factors(L, R, 99)[0]).cuda()
+    p = tdn.make_problem(L, C, R, N, E, w["r_cut"], w["n_radial"], tdn.TDN_F32, False)
+    ws = torch.empty(tdn.workspace_size(p)[0], dtype=torch.uint8, device="cuda")
+    args = [inp[k] for k in ("x", "edge_vec", "edge_index", "A")] + [A2] + [inp[k] for k in ("B", "D", "W", "radial_w")]
+    _replays_match(lambda: tdn.forward3(*args, L=L, r_cut=w["r_cut"], workspace=ws, out=out, perm=perm,
+                                        offsets=off), [out, perm, off])
+    z = np.load(os.path.join(os.path.dirname(__file__), "golden", "cg", f"cg_L{L}.npz"))
+    tab = tdn.cg_table(z["M"], z["path"], "cuda")
+    pw = torch.from_numpy(np.random.default_rng(3).standard_normal((w["n_radial"], tab.n_path)).astype(np.float32))
+    pw = pw.cuda()
+    pd = tdn.make_problem(L, C, tab.n_path, N, E, w["r_cut"], w["n_radial"], tdn.TDN_F32, False)
+    wsd = torch.empty(tdn.workspace_size(pd)[0], dtype=torch.uint8, device="cuda")
+    _replays_match(lambda: tdn.dense_forward(inp["x"], inp["edge_vec"], inp["edge_index"], tab, pw, inp["W"],
+                                             r_cut=w["r_cut"], workspace=wsd, out=out, perm=perm, offsets=off),
+                   [out, perm, off])
