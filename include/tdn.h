@@ -252,6 +252,19 @@ tdn_status tdn_sort_by_key(int32_t n_keys, int32_t E, const int32_t* keys, int32
                            int32_t* offsets, void* workspace, size_t workspace_bytes,
                            hipStream_t stream);
 
+/* The equivariant linear layer with path-weight sharing (Sec. 3.2, and its
+ * use in the equivariant linear layers, Sec. 4.1 "Model Design"): one
+ * channel matrix for every degree, y^(l) = x^(l) W for l = 0..L, i.e.
+ *   y [N, d, C] = x [N, d, C] W [C, C]   (f32, channel fastest; W[c_in, c_out])
+ * the map the layer applies to Z.  w_dtype TDN_F32 (fp32-level accuracy) or
+ * TDN_BF16 (W in bf16 bits, x rounded to bf16 on the MFMA; fp32
+ * accumulation).  Workspace from tdn_ps_linear_workspace_size (W's split
+ * parts for TDN_F32, none for TDN_BF16).  n_nodes = 0 is a no-op; C in
+ * 16..256 with C % 16 = 0, 0 <= L <= 6 (TDN_ERR_BAD_SHAPE). */
+tdn_status tdn_ps_linear_workspace_size(int32_t C, int32_t w_dtype, size_t* bytes);
+tdn_status tdn_ps_linear(int32_t n_nodes, int32_t L, int32_t C, const float* x, const void* W, int32_t w_dtype,
+                         float* y, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Real spherical harmonics of edge directions (basis as above):
  *   Y  [E, d]     Y(r_e/|r_e|)
  *   dY [E, d, 3]  dY/dr_e (or NULL) */

@@ -99,6 +99,20 @@ def forward(x, edge_index, edge_vec, A, B, D, W, radial_w, r_cut, L,
     return (out, zsum) if return_z else out
 
 
+def ps_linear(x, W, L):
+    """The equivariant linear layer with path-weight sharing (Sec. 3.2; used
+    for the linear layers, Sec. 4.1): for every degree l the block
+    x^(l) [N, 2l+1, C] is multiplied by the one channel matrix W, degree by
+    degree as the per-degree layer would be with all W_l equal."""
+    x = np.asarray(x, np.float64)
+    W = np.asarray(W, np.float64)
+    y = np.zeros(x.shape[:2] + (W.shape[1],))
+    for l in range(L + 1):
+        blk = slice(l * l, (l + 1) ** 2)
+        y[:, blk, :] = np.einsum("nmc,cf->nmf", x[:, blk, :], W)
+    return y
+
+
 def forward3(x, edge_index, edge_vec, A, A2, B, D, W, radial_w, r_cut, L, perm=None):
     """The three-input product (App. A, eq. multi-tp with N = 3 and its CP
     form D (B1^T x1 * B2^T x2 * B3^T x3)), the inputs being the source node's

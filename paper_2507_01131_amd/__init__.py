@@ -69,6 +69,8 @@ def lib() -> ctypes.CDLL:
         L.tdn_cp_tp_forward.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
         L.tdn_ablation_forward_atomics.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
         L.tdn_cp_tp_backward.argtypes = [PP] + [_P] * 17 + [_SZ, _P]
+        L.tdn_ps_linear_workspace_size.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_SZ)]
+        L.tdn_ps_linear.argtypes = [ctypes.c_int32] * 3 + [_P, _P, ctypes.c_int32, _P, _P, _SZ, _P]
         L.tdn_cp_tp3_forward.argtypes = [PP] + [_P] * 14 + [_SZ, _P]
         L.tdn_dense_tp_forward.argtypes = [PP] + [_P] * 6 + [ctypes.c_int32] + [_P] * 7 + [_SZ, _P]
         GP = ctypes.POINTER(GraphProblem)
@@ -87,7 +89,7 @@ def lib() -> ctypes.CDLL:
         for f in ("tdn_workspace_size", "tdn_cp_tp_forward", "tdn_ablation_forward_atomics", "tdn_cp_tp_backward",
                   "tdn_sort_workspace_size", "tdn_sort_by_key", "tdn_spherical_harmonics", "tdn_timer_enable",
                   "tdn_timer_read", "tdn_radius_graph_workspace_size", "tdn_radius_graph", "tdn_dense_tp_forward",
-                  "tdn_cp_tp3_forward"):
+                  "tdn_cp_tp3_forward", "tdn_ps_linear_workspace_size", "tdn_ps_linear"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -237,6 +239,30 @@ def forward3(x, edge_vec, edge_index, A, A2, B, D, W, radial_w, *, L: int, r_cut
     _check(st, "tdn_cp_tp3_forward")
     return ForwardResult(out, z, perm, offsets, p, dict(x=x, edge_vec=edge_vec, edge_index=edge_index, A=A, A2=A2,
                                                         B=B, D=D, W=W, radial_w=radial_w))
+
+
+def ps_linear(x, W, *, workspace=None, out=None, stream=None):
+    """Runs tdn_ps_linear: y = x W with one W [C, C] for every degree
+    (path-weight-shared equivariant linear layer).  x [N, d, C] float32; W
+    float32 or bfloat16."""
+    dev = x.device
+    N, d, C = x.shape
+    L = int(round(d ** 0.5)) - 1
+    if (L + 1) ** 2 != d:
+        raise ValueError("x must be [N, (L+1)^2, C]")
+    wd = TDN_BF16 if W.dtype == torch.bfloat16 else TDN_F32
+    _need(x, "x", torch.float32, (N, d, C), dev)
+    _need(W, "W", W.dtype, (C, C), dev)
+    nb = _SZ()
+    _check(lib().tdn_ps_linear_workspace_size(C, wd, ctypes.byref(nb)), "tdn_ps_linear_workspace_size")
+    if workspace is None or workspace.numel() < nb.value:
+        workspace = torch.empty(max(nb.value, 1), dtype=torch.uint8, device=dev)
+    if out is None:
+        out = torch.empty((N, d, C), dtype=torch.float32, device=dev)
+    _need(out, "out", torch.float32, (N, d, C), dev)
+    _check(lib().tdn_ps_linear(N, L, C, _ptr(x), _ptr(W), wd, _ptr(out), _ptr(workspace), workspace.numel(),
+                               _stream(stream)), "tdn_ps_linear")
+    return out
 
 
 @dataclass

@@ -414,6 +414,31 @@ tdn_status tdn_cp_tp3_forward(const tdn_problem* p, const void* x, const float* 
   return TDN_OK;
 }
 
+tdn_status tdn_ps_linear_workspace_size(int32_t C, int32_t w_dtype, size_t* bytes) {
+  if (!bytes) return TDN_ERR_NULL_POINTER;
+  if (w_dtype != TDN_F32 && w_dtype != TDN_BF16) return TDN_ERR_BAD_DTYPE;
+  if (C < 16 || C > 256 || C % 16 != 0) return TDN_ERR_BAD_SHAPE;
+  *bytes = w_dtype == TDN_F32 ? tdn::node_gemm_ws_bytes(C) : 0;
+  return TDN_OK;
+}
+
+tdn_status tdn_ps_linear(int32_t n_nodes, int32_t L, int32_t C, const float* x, const void* W, int32_t w_dtype,
+                         float* y, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (w_dtype != TDN_F32 && w_dtype != TDN_BF16) return TDN_ERR_BAD_DTYPE;
+  if (n_nodes < 0 || L < 0 || L > 6 || C < 16 || C > 256 || C % 16 != 0) return TDN_ERR_BAD_SHAPE;
+  if (int64_t(n_nodes) * dim_of(L) >= (int64_t(1) << 31) - 1) return TDN_ERR_BAD_SHAPE;
+  const bool f32 = w_dtype == TDN_F32;
+  if (!W || (f32 && !workspace)) return TDN_ERR_NULL_POINTER;
+  if (n_nodes > 0 && (!x || !y)) return TDN_ERR_NULL_POINTER;
+  if (f32 && workspace_bytes < tdn::node_gemm_ws_bytes(C)) return TDN_ERR_WORKSPACE_TOO_SMALL;
+  const tdn_status st = check_device();
+  if (st != TDN_OK) return st;
+  if (n_nodes == 0) return TDN_OK;
+  Timed t("node_gemm", stream);
+  TDN_HIP(tdn::launch_node_gemm(n_nodes * dim_of(L), C, x, W, !f32, 0, y, workspace, stream));
+  return TDN_OK;
+}
+
 tdn_status tdn_dense_tp_forward(const tdn_problem* p, const void* x, const float* edge_vec,
                                 const int32_t* edge_index, const int32_t* cg_row, const int32_t* cg_col,
                                 const float* cg_val, int32_t cg_nnz, const float* path_w, const void* W, float* out,

@@ -207,3 +207,20 @@ def test_three_input_forward_argument_checks():
     # the workspace covers the three-input product's edge ranges too
     f, _ = tdn.workspace_size(good)
     assert _tp3(good, ws_bytes=f - 1) == 4
+
+
+def test_ps_linear_argument_checks():
+    L = tdn.lib()
+    nb = ctypes.c_size_t()
+    assert L.tdn_ps_linear_workspace_size(128, tdn.TDN_F32, ctypes.byref(nb)) == 0 and nb.value > 0
+    assert L.tdn_ps_linear_workspace_size(128, tdn.TDN_BF16, ctypes.byref(nb)) == 0 and nb.value == 0
+    assert L.tdn_ps_linear_workspace_size(100, tdn.TDN_F32, ctypes.byref(nb)) == 2
+    assert L.tdn_ps_linear_workspace_size(128, 9, ctypes.byref(nb)) == 3
+    assert L.tdn_ps_linear(10, 2, 64, FAKE, FAKE, 9, FAKE, FAKE, 1 << 30, None) == 3
+    assert L.tdn_ps_linear(10, 7, 64, FAKE, FAKE, tdn.TDN_F32, FAKE, FAKE, 1 << 30, None) == 2
+    assert L.tdn_ps_linear(10, 2, 40, FAKE, FAKE, tdn.TDN_F32, FAKE, FAKE, 1 << 30, None) == 2
+    assert L.tdn_ps_linear(-1, 2, 64, FAKE, FAKE, tdn.TDN_F32, FAKE, FAKE, 1 << 30, None) == 2
+    assert L.tdn_ps_linear(10, 2, 64, None, FAKE, tdn.TDN_F32, FAKE, FAKE, 1 << 30, None) == 1
+    assert L.tdn_ps_linear(10, 2, 64, FAKE, None, tdn.TDN_F32, FAKE, FAKE, 1 << 30, None) == 1
+    assert L.tdn_ps_linear(10, 2, 64, FAKE, FAKE, tdn.TDN_F32, FAKE, None, 1 << 30, None) == 1
+    assert L.tdn_ps_linear(10, 2, 64, FAKE, FAKE, tdn.TDN_F32, FAKE, FAKE, 0, None) == 4

@@ -253,3 +253,22 @@ def test_three_input_exact_factors_give_the_nested_cg_product_and_equivariance()
     x2 = np.einsum("ab,nbc->nac", Dr, x)
     got2 = layer.forward3(x2, w["edge_index"], vec @ Rm.T, A, A2, B, D, w["W"], rw, w["r_cut"], L)
     np.testing.assert_allclose(got2, np.einsum("ab,nbc->nac", Dr, got), rtol=0, atol=1e-10 * np.max(np.abs(got)))
+
+
+# ------------------------------------------------------------ path-weight-shared linear layer
+def test_ps_linear_identity_scaling_and_equivariance():
+    rng = np.random.default_rng(8)
+    L, C = 3, 5
+    d = (L + 1) ** 2
+    x = rng.normal(size=(7, d, C))
+    np.testing.assert_allclose(layer.ps_linear(x, np.eye(C), L), x, rtol=0, atol=0)
+    np.testing.assert_allclose(layer.ps_linear(x, 2.5 * np.eye(C), L), 2.5 * x, rtol=1e-15)
+    W = rng.normal(size=(C, C))
+    y = layer.ps_linear(x, W, L)
+    # it acts on channels only, so it commutes with every Wigner-D rotation
+    Dr = wigner.wigner_d_full(L, wigner.random_rotation(rng))
+    y2 = layer.ps_linear(np.einsum("ab,nbc->nac", Dr, x), W, L)
+    np.testing.assert_allclose(y2, np.einsum("ab,nbc->nac", Dr, y), rtol=0, atol=1e-12)
+    # one channel vector at a time: column f of y is x's channels against W[:, f]
+    for f in range(C):
+        np.testing.assert_allclose(y[..., f], np.tensordot(x, W[:, f], axes=([2], [0])), rtol=1e-13)
