@@ -249,38 +249,41 @@ __device__ __forceinline__ f32x16 mfma32_f16(u32x4 a, u32x4 b, f32x16 c) {
 }
 
 // out[rows, C] = in[rows, C] B with B given as the parts wp (k_w_parts), for
-// C <= 32 NCH.  128 x 128 output tile per workgroup, four waves of 64 x 64.
+// C <= 32 NCH.  BM x 128 output tile per workgroup (BM = 128 or 64), four
+// waves of BM/2 x 64.
 // The block loads all NCH 32-wide chunks of its rows at once (coalesced,
 // straight into registers), so each row's largest magnitude needs one
 // memory latency; then per 32-deep chunk both operands are staged in LDS as
 // fp16 parts (the row parts split on the way, W's next chunk loaded one
 // chunk ahead) and every 16-deep step runs the three part products.
-template <int NCH>
+template <int NCH, int BM>
 __global__ __launch_bounds__(256) void k_node_gemm_f16(int rows, int C, const float* __restrict__ in,
                                                        const uint16_t* __restrict__ wp, float* __restrict__ out) {
-  __shared__ __align__(16) uint16_t sa[2][kBM * kSH];
+  constexpr int JR = BM / 32;  // 32-row groups of the block's row loads
+  constexpr int MI = BM / 64;  // 32-row MFMA tiles per wave
+  __shared__ __align__(16) uint16_t sa[2][BM * kSH];
   __shared__ __align__(16) uint16_t sb[2][kBN * kSH];
-  __shared__ float s_unscale[kBM];
-  const int m0 = blockIdx.x * kBM, n0 = blockIdx.y * kBN;
+  __shared__ float s_unscale[BM];
+  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * kBN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, l32 = lane & 31;
   const int wr = wave >> 1, wc = wave & 1;
-  // row chunk loads, coalesced: per 32-wide chunk the block's 128 x 32
-  // floats are 1024 float4, thread t taking float4 f = t + 256 j (j = 0..3):
-  // row (t >> 3) + 32 j, columns 4 (t & 7) .. +3; eight consecutive lanes
-  // cover one row's 128 bytes
+  // row chunk loads, coalesced: per 32-wide chunk the block's BM x 32
+  // floats are BM * 8 float4, thread t taking float4 f = t + 256 j
+  // (j < BM / 32): row (t >> 3) + 32 j, columns 4 (t & 7) .. +3; eight
+  // consecutive lanes cover one row's 128 bytes
   const int c4 = tid & 7;
-  f32x4 va[NCH][4];
+  f32x4 va[NCH][JR];
 #pragma unroll
   for (int it = 0; it < NCH; ++it)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < JR; ++j) {
       const int r = (tid >> 3) + 32 * j, k = it * kBK + 4 * c4;
       va[it][j] = (m0 + r < rows && k < C) ? *reinterpret_cast<const f32x4*>(in + size_t(m0 + r) * C + k) : f32x4{};
     }
-  float rsc[4];
+  float rsc[JR];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < JR; ++j) {
     float mx = 0.f;
 #pragma unroll
     for (int it = 0; it < NCH; ++it)
@@ -297,7 +300,9 @@ __global__ __launch_bounds__(256) void k_node_gemm_f16(int rows, int C, const fl
   // B runs: n = n0 + tid / 2, k = k0 + (tid % 2) * 16 .. +15, both parts
   const int b_r = tid / 2, b_c = (tid % 2) * 16;
   const int gn = n0 + b_r;
-  f32x16 acc[2][2] = {{f32x16{}, f32x16{}}, {f32x16{}, f32x16{}}};
+  f32x16 acc[MI][2];
+#pragma unroll
+  for (int i = 0; i < MI; ++i) acc[i][0] = acc[i][1] = f32x16{};
   u32x4 vb[2][2][2];  // [buffer][part][half of the run]
   auto fetch_b = [&](int k0, u32x4 (&b)[2][2]) {
     const int kb = k0 + b_c;
@@ -316,7 +321,7 @@ __global__ __launch_bounds__(256) void k_node_gemm_f16(int rows, int C, const fl
     if (k0 >= C) break;
     __syncthreads();  // the previous chunk's operands are consumed
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < JR; ++j) {
       uint32_t hi[2], lo[2];
       split_f16x2_pair(va[it][j][0] * rsc[j], va[it][j][1] * rsc[j], hi[0], lo[0]);
       split_f16x2_pair(va[it][j][2] * rsc[j], va[it][j][3] * rsc[j], hi[1], lo[1]);
@@ -332,16 +337,18 @@ __global__ __launch_bounds__(256) void k_node_gemm_f16(int rows, int C, const fl
     if (it + 1 < NCH && k0 + kBK < C) fetch_b(k0 + kBK, vb[(it + 1) & 1]);
 #pragma unroll
     for (int s2 = 0; s2 < kBK / 16; ++s2) {
-      u32x4 av[2][2], bv[2][2];  // [part][tile]
+      u32x4 av[2][MI], bv[2][2];  // [part][tile]
 #pragma unroll
-      for (int p = 0; p < 2; ++p)
+      for (int p = 0; p < 2; ++p) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          av[p][i] = *reinterpret_cast<const u32x4*>(&sa[p][(wr * 64 + i * 32 + l32) * kSH + 16 * s2 + 8 * h]);
+        for (int i = 0; i < MI; ++i)
+          av[p][i] = *reinterpret_cast<const u32x4*>(&sa[p][(wr * (BM / 2) + i * 32 + l32) * kSH + 16 * s2 + 8 * h]);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
           bv[p][i] = *reinterpret_cast<const u32x4*>(&sb[p][(wc * 64 + i * 32 + l32) * kSH + 16 * s2 + 8 * h]);
-        }
+      }
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           acc[i][j] = mfma32_f16(av[1][i], bv[0][j], acc[i][j]);
@@ -352,14 +359,14 @@ __global__ __launch_bounds__(256) void k_node_gemm_f16(int rows, int C, const fl
   }
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int col = n0 + wc * 64 + j * 32 + l32;
       if (col >= C) continue;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int rl = wr * 64 + i * 32 + acc_row(v, h);
+        const int rl = wr * (BM / 2) + i * 32 + acc_row(v, h);
         if (m0 + rl < rows) out[size_t(m0 + rl) * C + col] = acc[i][j][v] * (s_unscale[rl] * w_unscale);
       }
     }
@@ -421,15 +428,19 @@ hipError_t launch_node_gemm(int rows, int C, const float* in, const void* W, boo
   k_w_parts<<<dim3((C * C / 2 + 1023) / 1024), dim3(1024), 0, s>>>(C, transpose_w, static_cast<const float*>(W), wp);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  // 64-row tiles: twice the workgroups of 128-row ones, so the last round of
+  // workgroups on the CUs is less uneven
+  constexpr int BM = 64;
+  const dim3 grid_f((rows + BM - 1) / BM, (C + kBN - 1) / kBN);
   const int nch = (C + kBK - 1) / kBK;
   if (nch <= 1)
-    k_node_gemm_f16<1><<<grid, dim3(256), 0, s>>>(rows, C, in, wp, out);
+    k_node_gemm_f16<1, BM><<<grid_f, dim3(256), 0, s>>>(rows, C, in, wp, out);
   else if (nch <= 2)
-    k_node_gemm_f16<2><<<grid, dim3(256), 0, s>>>(rows, C, in, wp, out);
+    k_node_gemm_f16<2, BM><<<grid_f, dim3(256), 0, s>>>(rows, C, in, wp, out);
   else if (nch <= 4)
-    k_node_gemm_f16<4><<<grid, dim3(256), 0, s>>>(rows, C, in, wp, out);
+    k_node_gemm_f16<4, BM><<<grid_f, dim3(256), 0, s>>>(rows, C, in, wp, out);
   else
-    k_node_gemm_f16<8><<<grid, dim3(256), 0, s>>>(rows, C, in, wp, out);
+    k_node_gemm_f16<8, BM><<<grid_f, dim3(256), 0, s>>>(rows, C, in, wp, out);
   return hipGetLastError();
 }
 
