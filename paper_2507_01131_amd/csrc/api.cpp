@@ -129,7 +129,7 @@ BwdLayout bwd_layout(const tdn_problem& p) {
   b.part = o;
   o += al(partial_bytes(p));
   b.parts = o;
-  o += al(size_t(tdn::gram_parts(p.n_nodes * dim_of(p.L))) * p.C * p.C * 4);
+  o += al(size_t(tdn::gram_parts(p.n_nodes * dim_of(p.L), p.C)) * p.C * p.C * 4);
   b.perm_src = o;
   o += al(size_t(p.n_edges) * 4);
   b.off_src = o;

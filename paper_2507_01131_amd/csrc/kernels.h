@@ -142,10 +142,10 @@ size_t edge_ef_bytes(int d, int R);
 size_t node_gemm_ws_bytes(int C);
 hipError_t launch_node_gemm(int rows, int C, const float* in, const void* W, bool w_bf16, int transpose_w,
                             float* out, void* ws, hipStream_t s);
-// grad_W[C, C] = sum_rows Z[row, :]^T G[row, :], split over gram_parts(rows)
+// grad_W[C, C] = sum_rows Z[row, :]^T G[row, :], split over gram_parts(rows, C)
 // row chunks reduced in a fixed order.  partial: [n_part, C, C] floats of
 // workspace.  bf16 = 1 rounds Z and G to bf16 for the MFMA (bf16 problems).
-int gram_parts(int rows);
+int gram_parts(int rows, int C);
 hipError_t launch_gram(int rows, int C, const float* Z, const float* G, bool bf16, float* partial, float* grad_W,
                        hipStream_t s);
 

@@ -398,12 +398,25 @@ __global__ __launch_bounds__(256) void k_gram_partial(int rows, int C, int rows_
   store_tile(acc, partial + size_t(p) * C * C, C, C, C, m0, n0);
 }
 
-__global__ void k_sum_parts(int n_part, int CC, const float* __restrict__ partial, float* __restrict__ out) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= CC) return;
+// 16 outputs per workgroup, 16 slices per output: slice k sums parts
+// k, k + 16, ... in order, then the slices are added in order (the result
+// does not depend on scheduling).
+__global__ __launch_bounds__(256) void k_sum_parts(int n_part, int CC, const float* __restrict__ partial,
+                                                   float* __restrict__ out) {
+  __shared__ float sl[16][17];
+  const int o = threadIdx.x & 15, k = threadIdx.x >> 4;
+  const int i = blockIdx.x * 16 + o;
   float s = 0.f;
-  for (int p = 0; p < n_part; ++p) s += partial[size_t(p) * CC + i];
-  out[i] = s;
+  if (i < CC)
+    for (int p = k; p < n_part; p += 16) s += partial[size_t(p) * CC + i];
+  sl[k][o] = s;
+  __syncthreads();
+  if (k == 0 && i < CC) {
+    float t = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) t += sl[j][o];
+    out[i] = t;
+  }
 }
 
 }  // namespace
@@ -444,15 +457,20 @@ hipError_t launch_node_gemm(int rows, int C, const float* in, const void* W, boo
   return hipGetLastError();
 }
 
-int gram_parts(int rows) {
-  int p = (rows + 511) / 512;
-  return p < 1 ? 1 : (p > 128 ? 128 : p);
+// Row parts of the Gram product: about 512 workgroups over the 128 x 128
+// output tiles (two per CU), each part at least 64 rows.
+int gram_parts(int rows, int C) {
+  const int tiles = ((C + kBM - 1) / kBM) * ((C + kBN - 1) / kBN);
+  int p = 512 / tiles;
+  const int by_rows = rows / 64;
+  if (p > by_rows) p = by_rows;
+  return p < 1 ? 1 : p;
 }
 
 hipError_t launch_gram(int rows, int C, const float* Z, const float* G, bool bf16, float* partial, float* grad_W,
                        hipStream_t s) {
   if (rows <= 0) return launch_zero(grad_W, size_t(C) * C * 4, s);
-  const int parts = gram_parts(rows);
+  const int parts = gram_parts(rows, C);
   int rpp = (rows + parts - 1) / parts;
   rpp = (rpp + kBK - 1) / kBK * kBK;
   const dim3 grid(parts, (C + kBM - 1) / kBM, (C + kBN - 1) / kBN);
@@ -460,7 +478,7 @@ hipError_t launch_gram(int rows, int C, const float* Z, const float* G, bool bf1
     k_gram_partial<true><<<grid, dim3(256), 0, s>>>(rows, C, rpp, Z, G, partial);
   else
     k_gram_partial<false><<<grid, dim3(256), 0, s>>>(rows, C, rpp, Z, G, partial);
-  k_sum_parts<<<dim3((C * C + 255) / 256), dim3(256), 0, s>>>(parts, C * C, partial, grad_W);
+  k_sum_parts<<<dim3((C * C + 15) / 16), dim3(256), 0, s>>>(parts, C * C, partial, grad_W);
   return hipGetLastError();
 }
 
