@@ -119,9 +119,23 @@ __global__ void k_offsets(const int32_t* __restrict__ sorted_keys, int E, int n_
   offsets[k] = lo;
 }
 
-__global__ void k_iota(int32_t* __restrict__ p, int n) {
+// Pre-sorted keys in one launch: thread i < E writes perm[i] = i, thread
+// k <= n_keys the offset of key k by binary search (as k_offsets).
+__global__ void k_iota_offsets(const int32_t* __restrict__ sorted_keys, int E, int n_keys, int32_t* __restrict__ perm,
+                               int32_t* __restrict__ offsets) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = i;
+  if (i < E) perm[i] = i;
+  if (i <= n_keys) {
+    int lo = 0, hi = E;
+    while (lo < hi) {
+      const int mid = lo + ((hi - lo) >> 1);
+      if (sorted_keys[mid] < i)
+        lo = mid + 1;
+      else
+        hi = mid;
+    }
+    offsets[i] = lo;
+  }
 }
 
 __global__ void k_fill_u32(uint32_t* __restrict__ p, size_t n) {
@@ -171,8 +185,8 @@ hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t s) {
 
 hipError_t launch_offsets_presorted(int n_keys, int E, const int32_t* sorted_keys, int32_t* perm, int32_t* offsets,
                                     hipStream_t s) {
-  if (E > 0) k_iota<<<dim3((E + 255) / 256), dim3(256), 0, s>>>(perm, E);
-  k_offsets<<<dim3((n_keys + 1 + 255) / 256), dim3(256), 0, s>>>(sorted_keys, E, n_keys, offsets);
+  const int n = E > n_keys + 1 ? E : n_keys + 1;
+  k_iota_offsets<<<dim3((n + 255) / 256), dim3(256), 0, s>>>(sorted_keys, E, n_keys, perm, offsets);
   return hipGetLastError();
 }
 
