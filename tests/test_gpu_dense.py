@@ -117,3 +117,19 @@ def test_dense_full_size_sampled(name):
     sub = perm[keep[w["edge_index"][1][perm]]]
     ref = dense_layer.forward(w["x"], w["edge_index"], w["edge_vec"], w["W"], pw, w["r_cut"], w["L"], perm=sub)
     assert rel_err(out[nodes], ref[nodes]) < TOL_F32
+
+
+@pytest.mark.parametrize("case,status", [("range", 5), ("order", 6), ("zero", 7)])
+def test_dense_validation_errors(case, status):
+    w = workloads.random_graph(12, n_nodes=10, n_edges=50, L=2, C=16, R=1, sort=True)
+    if case == "range":
+        w["edge_index"][0, 7] = 10
+    elif case == "order":
+        w["edge_index"][1, [3, 40]] = w["edge_index"][1, [40, 3]]
+    else:
+        w["edge_vec"][4] = 0
+    with pytest.raises(tdn.TdnError) as ei:
+        _run(w, _path_w(w, 1), validate=True)
+    assert ei.value.status == status
+    w2 = workloads.random_graph(12, n_nodes=10, n_edges=50, L=2, C=16, R=1, sort=True)
+    _run(w2, _path_w(w2, 1), validate=True)          # good input passes

@@ -102,3 +102,20 @@ def test_three_input_headline_size_sampled():
     ref = layer.forward3(w["x"], w["edge_index"], w["edge_vec"], A, A2, B, D, w["W"], w["radial_w"], w["r_cut"],
                          w["L"], perm=sub)
     assert rel_err(out[nodes], ref[nodes]) < TOL_F32
+
+
+@pytest.mark.parametrize("case,status", [("range", 5), ("order", 6), ("zero", 7)])
+def test_three_input_validation_errors(case, status):
+    L, R = 2, 32
+    w = workloads.random_graph(13, n_nodes=10, n_edges=50, L=L, C=16, R=R, sort=True)
+    A, B, D = random_factors(L, R, 3)
+    A2 = _a2(L, R, 4)
+    if case == "range":
+        w["edge_index"][0, 7] = 10
+    elif case == "order":
+        w["edge_index"][1, [3, 40]] = w["edge_index"][1, [40, 3]]
+    else:
+        w["edge_vec"][4] = 0
+    with pytest.raises(tdn.TdnError) as ei:
+        _run(w, A, A2, B, D, validate=True)
+    assert ei.value.status == status
