@@ -110,9 +110,3 @@ def radius_graph(pos, graph_ptr, cell, periodic, r_cut, max_neighbors=0, dst_nod
     return (np.concatenate(out_s), np.concatenate(out_d), np.concatenate(out_n).reshape(-1, 3),
             np.concatenate(out_v).reshape(-1, 3).astype(np.float32))
 
-
-def neighbour_counts(pos, graph_ptr, cell, periodic, r_cut):
-    """Number of qualifying (src, image) pairs of every destination, before
-    any cap."""
-    _, d, _, _ = radius_graph(pos, graph_ptr, cell, periodic, r_cut)
-    return np.bincount(d, minlength=np.asarray(pos).shape[0])

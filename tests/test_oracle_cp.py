@@ -82,3 +82,60 @@ def test_hosvd_truncation_within_tail_bound(L, R):
 def test_tucker_tail_vanishes_at_full_multilinear_rank():
     M = cg_tensor.cg_tensor(1)
     assert cp.tucker_tail(M, 4 ** 3) < 1e-12
+
+
+# ----- approximation_error (Sec. 4.1): closed-form cases that fix both the
+# numerator and the normaliser.  A normaliser taken from the approximation
+# instead of the exact product, or squared norms, fails each of them.
+
+@pytest.mark.parametrize("L", [1, 2, 3])
+def test_approximation_error_zero_for_exact_factors(L):
+    # Thm. 2: the rank d^2 construction reproduces M, so the error is 0
+    M = cg_tensor.cg_tensor(L)
+    D, A, B = cp.universality_factors(M)
+    rng = np.random.default_rng(10 + L)
+    x, y = rng.normal(size=(2, 50, (L + 1) ** 2))
+    app = cp.approximation_error(M, D, A, B, x, y)
+    assert np.max(app) < 1e-14
+
+
+@pytest.mark.parametrize("L", [1, 2])
+def test_approximation_error_one_for_zero_approximation(L):
+    M = cg_tensor.cg_tensor(L)
+    D, A, B = cp.universality_factors(M)
+    rng = np.random.default_rng(20 + L)
+    x, y = rng.normal(size=(2, 30, (L + 1) ** 2))
+    app = cp.approximation_error(M, np.zeros_like(D), A, B, x, y)
+    np.testing.assert_array_equal(app, np.ones(30))
+
+
+@pytest.mark.parametrize("eps", [0.5, -0.25, 1e-3, 3.0])
+def test_approximation_error_of_scaled_tensor_is_abs_eps(eps):
+    # M_hat = (1 + eps) M  =>  error = |eps| for every sample; the
+    # approximation's norm as normaliser would give |eps| / |1 + eps|, and
+    # squared norms eps^2
+    M = cg_tensor.cg_tensor(2)
+    D, A, B = cp.universality_factors(M)
+    rng = np.random.default_rng(7)
+    x, y = rng.normal(size=(2, 40, 9))
+    app = cp.approximation_error(M, (1.0 + eps) * D, A, B, x, y)
+    np.testing.assert_allclose(app, abs(eps), rtol=1e-12)
+
+
+def test_approximation_error_hand_computed_degree_one_case():
+    # L = 1 (d = 4).  The path 0 x 1 -> 1 has the identity as its CG block
+    # (<0 0; 1 m' | 1 m> = delta), so with x the unit scalar e_0 the exact
+    # product is M(e_0 (x) y) = y.  Dropping that path from the Thm. 2 factors
+    # (zeroing the columns (i = 0, j in degree 1)) leaves (y_0, 0, 0, 0).
+    # With y = (3, 0, 4, 0): error = ||(0, 0, 4, 0)|| / ||y|| = 4 / 5 exactly
+    # (the approximation's norm would give 4/3, squared norms 16/25).
+    M = cg_tensor.cg_tensor(1)
+    D, A, B = cp.universality_factors(M)
+    x = np.array([[1.0, 0.0, 0.0, 0.0]])
+    y = np.array([[3.0, 0.0, 4.0, 0.0]])
+    np.testing.assert_allclose(cg_tensor.dense_tensor_product(M, x, y), y, atol=1e-15)
+    D2 = D.copy()
+    for j in (1, 2, 3):
+        D2[:, 0 * 4 + j] = 0.0
+    app = cp.approximation_error(M, D2, A, B, x, y)
+    np.testing.assert_allclose(app, [0.8], rtol=1e-14)
