@@ -60,7 +60,9 @@ typedef enum {
   TDN_ERR_HIP = 9,                 /* a HIP call failed, see tdn_last_hip_error   */
   TDN_ERR_BAD_GEOMETRY = 10,       /* radius graph: graph_ptr, positions or box   */
   TDN_ERR_EDGE_CAPACITY = 11,      /* radius graph: more edges than buffer room   */
-  TDN_ERR_NEIGHBOUR_LIMIT = 12     /* radius graph: > 2048 candidates for an atom */
+  TDN_ERR_NEIGHBOUR_LIMIT = 12,    /* radius graph: > 2048 candidates for an atom */
+  TDN_ERR_SCRATCH_LIMIT = 13       /* no-allocation forward: workspace needed
+                                      above TDN_NOALLOC_SCRATCH_BYTES           */
 } tdn_status;
 
 typedef enum { TDN_F32 = 0, TDN_BF16 = 1 } tdn_dtype;
@@ -113,6 +115,24 @@ tdn_status tdn_cp_tp_forward(const tdn_problem* p, const void* x, const float* e
                              const float* D, const void* W, const float* radial_w, float* out,
                              float* z_save, int32_t* perm, int32_t* offsets, void* workspace,
                              size_t workspace_bytes, hipStream_t stream);
+
+/* Forward pass for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * Same arguments, results and bits as tdn_cp_tp_forward, without the
+ * workspace: the scratch space comes from a fixed area of
+ * TDN_NOALLOC_SCRATCH_BYTES that the library keeps on every device it runs
+ * on until the process ends (set up on the first call on a device).  The
+ * call allocates nothing.  A problem whose tdn_workspace_size forward bytes
+ * exceed TDN_NOALLOC_SCRATCH_BYTES is rejected with TDN_ERR_SCRATCH_LIMIT
+ * before any work is enqueued (molecules960_L3_C64_R64-sized problems fit;
+ * the 3200-node headline size does not).  Every call on a device shares that
+ * device's area, so calls that overlap on one device (other streams or host
+ * threads) race: serialise them.  Records no timing events. */
+#define TDN_NOALLOC_SCRATCH_BYTES (32u << 20)
+tdn_status tdn_cp_tp_forward_noalloc(const tdn_problem* p, const void* x, const float* edge_vec,
+                                     const int32_t* edge_index, const float* A, const float* B,
+                                     const float* D, const void* W, const float* radial_w, float* out,
+                                     float* z_save, int32_t* perm, int32_t* offsets, hipStream_t stream);
 
 /* Measurement ablation of the forward's segmented sum (Sec. 3.1: the layer
  * sums the per-edge messages into each destination node).  Same arguments,

@@ -27,7 +27,8 @@ TDN_F32, TDN_BF16 = 0, 1
 STATUS = {0: "TDN_OK", 1: "TDN_ERR_NULL_POINTER", 2: "TDN_ERR_BAD_SHAPE", 3: "TDN_ERR_BAD_DTYPE",
           4: "TDN_ERR_WORKSPACE_TOO_SMALL", 5: "TDN_ERR_INDEX_OUT_OF_RANGE", 6: "TDN_ERR_NOT_SORTED",
           7: "TDN_ERR_DEGENERATE_EDGE", 8: "TDN_ERR_UNSUPPORTED_DEVICE", 9: "TDN_ERR_HIP",
-          10: "TDN_ERR_BAD_GEOMETRY", 11: "TDN_ERR_EDGE_CAPACITY", 12: "TDN_ERR_NEIGHBOUR_LIMIT"}
+          10: "TDN_ERR_BAD_GEOMETRY", 11: "TDN_ERR_EDGE_CAPACITY", 12: "TDN_ERR_NEIGHBOUR_LIMIT",
+          13: "TDN_ERR_SCRATCH_LIMIT"}
 TDN_ERR_EDGE_CAPACITY = 11
 
 
@@ -68,6 +69,7 @@ def lib() -> ctypes.CDLL:
         L.tdn_workspace_size.argtypes = [PP, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)]
         L.tdn_cp_tp_forward.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
         L.tdn_ablation_forward_atomics.argtypes = [PP] + [_P] * 13 + [_SZ, _P]
+        L.tdn_cp_tp_forward_noalloc.argtypes = [PP] + [_P] * 13
         L.tdn_cp_tp_backward.argtypes = [PP] + [_P] * 17 + [_SZ, _P]
         L.tdn_ps_linear_workspace_size.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_SZ)]
         L.tdn_ps_linear.argtypes = [ctypes.c_int32] * 3 + [_P, _P, ctypes.c_int32, _P, _P, _SZ, _P]
@@ -87,6 +89,7 @@ def lib() -> ctypes.CDLL:
         L.tdn_status_string.restype = ctypes.c_char_p
         L.tdn_last_hip_error.restype = ctypes.c_int32
         for f in ("tdn_workspace_size", "tdn_cp_tp_forward", "tdn_ablation_forward_atomics", "tdn_cp_tp_backward",
+                  "tdn_cp_tp_forward_noalloc",
                   "tdn_sort_workspace_size", "tdn_sort_by_key", "tdn_spherical_harmonics", "tdn_timer_enable",
                   "tdn_timer_read", "tdn_radius_graph_workspace_size", "tdn_radius_graph", "tdn_dense_tp_forward",
                   "tdn_cp_tp3_forward", "tdn_ps_linear_workspace_size", "tdn_ps_linear"):
@@ -195,6 +198,40 @@ def forward(x, edge_vec, edge_index, A, B, D, W, radial_w, *, L: int, r_cut: flo
                               _ptr(D), _ptr(W), _ptr(radial_w), _ptr(out), _ptr(z), _ptr(perm), _ptr(offsets),
                               _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, name)
+    return ForwardResult(out, z, perm, offsets, p,
+                         dict(x=x, edge_vec=edge_vec, edge_index=edge_index, A=A, B=B, D=D, W=W, radial_w=radial_w))
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def forward_noalloc(x, edge_vec, edge_index, A, B, D, W, radial_w, *, L: int, r_cut: float, out, perm, offsets,
+                    z=None, edges_sorted=False, validate=False, stream=None) -> ForwardResult:
+    """Runs tdn_cp_tp_forward_noalloc: the forward with the library's fixed
+    scratch area instead of a workspace (for callers that cannot allocate).
+    The outputs out, perm, offsets (and z, optional) must be passed
+    preallocated; arguments otherwise as in forward()."""
+    dev = x.device
+    N, d, C = x.shape
+    E = edge_vec.shape[0]
+    R = A.shape[1]
+    if edge_index.dtype != torch.int32 or not edge_index.is_contiguous():
+        raise TypeError("edge_index must be contiguous int32 (no conversion happens on this path)")
+    fd = TDN_BF16 if x.dtype == torch.bfloat16 else TDN_F32
+    for t, n, dt, sh in [(x, "x", x.dtype, (N, d, C)), (edge_vec, "edge_vec", torch.float32, (E, 3)),
+                         (edge_index, "edge_index", torch.int32, (2, E)), (A, "A", torch.float32, (d, R)),
+                         (B, "B", torch.float32, (d, R)), (D, "D", torch.float32, (d, R)),
+                         (W, "W", x.dtype, (C, C)), (radial_w, "radial_w", torch.float32, (radial_w.shape[0], R)),
+                         (out, "out", torch.float32, (N, d, C)), (perm, "perm", torch.int32, (E,)),
+                         (offsets, "offsets", torch.int32, (N + 1,))]:
+        _need(t, n, dt, sh, dev)
+    if z is not None:
+        _need(z, "z", torch.float32, (N, d, C), dev)
+    p = make_problem(L, C, R, N, E, r_cut, radial_w.shape[0], fd, edges_sorted, validate)
+    st = lib().tdn_cp_tp_forward_noalloc(ctypes.byref(p), _ptr(x), _ptr(edge_vec), _ptr(edge_index), _ptr(A),
+                                         _ptr(B), _ptr(D), _ptr(W), _ptr(radial_w), _ptr(out), _ptr(z), _ptr(perm),
+                                         _ptr(offsets), _stream(stream))
+    _check(st, "tdn_cp_tp_forward_noalloc")
     return ForwardResult(out, z, perm, offsets, p,
                          dict(x=x, edge_vec=edge_vec, edge_index=edge_index, A=A, B=B, D=D, W=W, radial_w=radial_w))
 

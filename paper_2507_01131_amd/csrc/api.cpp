@@ -12,6 +12,7 @@
 #include <utility>
 #include <vector>
 
+#include "api_internal.h"
 #include "kernels.h"
 #include "tdn.h"
 
@@ -19,6 +20,8 @@
 namespace {
 
 thread_local int32_t g_last_hip = 0;
+// set while a call must not create timing events (tdn_cp_tp_forward_noalloc)
+thread_local bool g_untimed = false;
 
 size_t al(size_t b) { return (b + 255) & ~size_t(255); }
 
@@ -183,6 +186,7 @@ Timer& timer() {
 class Timed {
  public:
   Timed(const char* name, hipStream_t s) : name_(name), s_(s) {
+    if (g_untimed) return;
     Timer& t = timer();
     std::lock_guard<std::mutex> lk(t.mu);
     if (!t.on) return;
@@ -288,6 +292,8 @@ const char* tdn_status_string(tdn_status s) {
     case TDN_ERR_BAD_GEOMETRY: return "invalid graph_ptr, position or periodic box";
     case TDN_ERR_EDGE_CAPACITY: return "edge buffers smaller than the edge count";
     case TDN_ERR_NEIGHBOUR_LIMIT: return "more than 2048 neighbours of one atom within the cutoff";
+    case TDN_ERR_SCRATCH_LIMIT:
+      return "the problem needs more workspace than the no-allocation entry point's fixed scratch area holds";
   }
   return "unknown status";
 }
@@ -759,3 +765,22 @@ tdn_status tdn_timer_read(const char* kernel, double* total_ms, int32_t* launche
 }
 
 }  // extern "C"
+
+namespace tdn {
+
+tdn_status record_hip_error(hipError_t e) { return hip_fail(e); }
+
+tdn_status require_gfx950() { return check_device(); }
+
+tdn_status forward_untimed(const tdn_problem* p, const void* x, const float* edge_vec, const int32_t* edge_index,
+                           const float* A, const float* B, const float* D, const void* W, const float* radial_w,
+                           float* out, float* z_save, int32_t* perm, int32_t* offsets, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  g_untimed = true;
+  const tdn_status st = forward_impl(p, x, edge_vec, edge_index, A, B, D, W, radial_w, out, z_save, perm, offsets,
+                                     workspace, workspace_bytes, stream, false);
+  g_untimed = false;
+  return st;
+}
+
+}  // namespace tdn

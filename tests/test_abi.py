@@ -150,8 +150,8 @@ def test_radius_graph_argument_checks():
 
 
 def test_status_strings():
-    for s in range(13):
-        assert tdn.status_string(s)
+    for s in range(14):
+        assert tdn.status_string(s) not in ("", "unknown status")
     assert tdn.status_string(0) == "ok"
 
 
@@ -224,3 +224,16 @@ def test_ps_linear_argument_checks():
     assert L.tdn_ps_linear(10, 2, 64, FAKE, None, tdn.TDN_F32, FAKE, FAKE, 1 << 30, None) == 1
     assert L.tdn_ps_linear(10, 2, 64, FAKE, FAKE, tdn.TDN_F32, FAKE, None, 1 << 30, None) == 1
     assert L.tdn_ps_linear(10, 2, 64, FAKE, FAKE, tdn.TDN_F32, FAKE, FAKE, 0, None) == 4
+
+
+def test_noalloc_forward_rejects_problems_beyond_its_scratch():
+    # a host-side check made before any device work: the headline size needs
+    # more than the fixed scratch area holds
+    L = tdn.lib()
+    p = tdn.make_problem(4, 128, 128, 3200, 151118, 6.0)
+    f, _ = tdn.workspace_size(p)
+    assert f > tdn.NOALLOC_SCRATCH_BYTES
+    st = L.tdn_cp_tp_forward_noalloc(ctypes.byref(p), *([None] * 12), None)
+    assert st == 13 and tdn.STATUS[st] == "TDN_ERR_SCRATCH_LIMIT"
+    bad = tdn.make_problem(4, 100, 128, 10, 10, 6.0)     # C not a multiple of 16
+    assert L.tdn_cp_tp_forward_noalloc(ctypes.byref(bad), *([None] * 12), None) == 2
