@@ -256,6 +256,15 @@ tdn::EdgeArgs edge_args(const tdn_problem& p, const int32_t* offsets, const int3
   return a;
 }
 
+// Features of the CP edge pass: the packed fp16 split of fp32 features, or
+// the bf16 operand blocks (bf16 problems; an fp32 input is rounded).
+hipError_t edge_features(const tdn_problem& p, const void* x, bool x_is_f32, void* xt, hipStream_t s) {
+  if (feature_parts(p) == 2)
+    return tdn::launch_feature_layout_packed(p.n_nodes, dim_of(p.L), p.C, static_cast<const float*>(x), xt,
+                                             row_scales(p, xt), s);
+  return tdn::launch_feature_layout(p.n_nodes, dim_of(p.L), p.C, x, x_is_f32, 1, xt, nullptr, s);
+}
+
 // The forward edge pass Z = per-node D diag(g) A^T x sums, for either
 // feature dtype (bf16 goes through the transposed copy in the workspace).
 hipError_t forward_edge_pass(const tdn_problem& p, const int32_t* offsets, const int32_t* perm, const int32_t* src,
@@ -264,8 +273,7 @@ hipError_t forward_edge_pass(const tdn_problem& p, const int32_t* offsets, const
                              hipStream_t s, bool atomic = false) {
   {
     Timed t("feature_layout", s);
-    hipError_t e = tdn::launch_feature_layout(p.n_nodes, dim_of(p.L), p.C, x, p.feat_dtype == TDN_F32,
-                                              feature_parts(p), xt, row_scales(p, xt), s);
+    hipError_t e = edge_features(p, x, p.feat_dtype == TDN_F32, xt, s);
     if (e != hipSuccess) return e;
   }
   Timed t(atomic ? "cp_edge_fwd_atomic" : "cp_edge_fwd", s);
@@ -404,7 +412,7 @@ tdn_status tdn_cp_tp3_forward(const tdn_problem* p, const void* x, const float* 
   void* xt = ws + lay.xt;
   {
     Timed t("feature_layout", stream);
-    TDN_HIP(tdn::launch_feature_layout(N, d, C, x, true, 2, xt, row_scales(*p, xt), stream));
+    TDN_HIP(edge_features(*p, x, true, xt, stream));
   }
   {
     Timed t("cp_edge_fwd_t3", stream);
@@ -630,8 +638,7 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
     // bf16); fp32 problems on the fp16 two-part split of Gz
     {
       Timed t("feature_layout", stream);
-      TDN_HIP(tdn::launch_feature_layout(N, d, C, Gz, true, feature_parts(*p), ws + lay.xt,
-                                         row_scales(*p, ws + lay.xt), stream));
+      TDN_HIP(edge_features(*p, Gz, true, ws + lay.xt, stream));
     }
     Timed t("cp_edge_bwd_src", stream);
     TDN_HIP(tdn::launch_cp_edge(edge_args(*p, off_src, perm_src, dst, src, edge_vec, D, A, B, radial_w, ws + lay.xt,

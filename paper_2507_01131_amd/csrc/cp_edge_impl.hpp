@@ -97,7 +97,7 @@ __host__ __device__ constexpr int edge_waves_per_eu(int L, int RT, bool bf) {
                        (edge_kb((L + 1) * (L + 1)) == 2 ? 160 : 128)
                    ? 2
                    : 1)
-            : (16 * RT + 24 * edge_xp(bf) * edge_kb((L + 1) * (L + 1)) <= 160 ? 2 : 1);
+            : (16 * RT + 2 * pk_rows((L + 1) * (L + 1)) + 8 * pk_blocks((L + 1) * (L + 1)) + 32 <= 168 ? 2 : 1);
 }
 
 // Most ranges a workgroup takes: two where two workgroups share a CU (their
@@ -118,7 +118,7 @@ struct EdgeSmem {
 };
 
 // LDS regions (in floats): the factor operands, split mode
-// [KB][RT][2 parts][64 lanes] x 16 bytes of fp16, bf16 mode
+// [pk_blocks(d)][RT][64 lanes] x 16 bytes of fp16 (packed slots), bf16 mode
 // [KB][RT][64 lanes] x 32 bytes of fp32, g for a chunk of edges (rows
 // rounded up to a whole 32-row tile), harmonics, normalised edge vectors with
 // their lengths, radial basis, gathered rows, the edges' operand scales, and
@@ -130,7 +130,7 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radi
   s.Rp = RT * kTile;
   int o = 0;
   s.off_a = o;
-  o += edge_kb(d) * RT * 2 * kWave * 4;
+  o += bf ? edge_kb(d) * RT * 2 * kWave * 4 : pk_blocks(d) * RT * kWave * 4;
   s.off_g = o;
   o += (chunk + kTile - 1) / kTile * kTile * s.Rp;
   s.off_y = o;
@@ -148,7 +148,7 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radi
   o += 2 * chunk + 4;
   o = (o + 3) & ~3;
   s.off_a2 = o;
-  if (t3) o += edge_kb(d) * RT * 2 * kWave * 4;
+  if (t3) o += pk_blocks(d) * RT * kWave * 4;
   s.floats = o;
   return s;
 }
@@ -175,6 +175,9 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   constexpr int KB = edge_kb(d);
   constexpr int Rp = RT * kTile;
   constexpr int MT = (d + kTile - 1) / kTile;
+  // split mode: packed K slots (pk_rows / pk_blocks in kernels.h), PN words
+  // per lane and edge loaded as PQ quads and a PT-word tail
+  constexpr int PN = pk_rows(d), PB = pk_blocks(d), PQ = PN / 4, PT = PN % 4;
   extern __shared__ float smem[];
   const EdgeSmem S = edge_smem(RT, BF, d, a.n_radial, chunk, T3);
   u32x4* sA = reinterpret_cast<u32x4*>(smem + S.off_a);
@@ -190,6 +193,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   int* sBndKey = sBnd + chunk;                          // [chunk] that segment
   int* sMeta = sBndKey + chunk;                         // start count, first partial, last partial
 
+
   const int n_blocks = a.n_range / a.pieces_per_block;
   const int logical = xcd_remap(blockIdx.x, n_blocks * n_cgrp);
   const int slot = logical / n_cgrp, cgrp = logical - slot * n_cgrp;
@@ -197,6 +201,32 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   const int h = lane >> 5, l32 = lane & 31;
   const int C = a.C, nr = a.n_radial, R = a.R;
   const int c0 = (cgrp * waves + wave) * CT * kTile + l32;  // this lane's channel in tile 0
+
+  // Split mode: one thread per (packed K-block b, rank tile rt, lane) writes
+  // the factor operand of that block: lane (h, r) slot j = 8b + i holds, for
+  // the group j / PN and degree row h PN + j % PN, the fp16 hi part of
+  // F 2^-e_F (groups 0 and 1, against x hi and x lo) or its lo part (group 2,
+  // against x hi); zero past d, R and the three groups.
+  auto stage_packed = [&](const float* __restrict__ F, float fsc, int t, u32x4* dst) {
+    const int ln = t % kWave, brt = t / kWave;
+    const int b = brt / RT, rt = brt - b * RT;
+    const int r = rt * kTile + (ln & 31), hh = ln >> 5;
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t pr = 0;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int j = 8 * b + 2 * q + u, g = j / PN, row = hh * PN + j % PN;
+        const float v = (g < 3 && row < d && r < R) ? F[row * R + r] * fsc : 0.f;
+        const _Float16 hi = static_cast<_Float16>(v);
+        const _Float16 val = g == 2 ? static_cast<_Float16>(v - float(hi)) : hi;
+        pr |= uint32_t(__builtin_bit_cast(uint16_t, val)) << (16 * u);
+      }
+      w[q] = pr;
+    }
+    dst[brt * kWave + ln] = u32x4{w[0], w[1], w[2], w[3]};
+  };
 
   // Split mode: the power of two 2^-e_K that puts the factor's largest |KF|
   // in [2^13, 2^14) for its fp16 parts (a block maximum through sG, which
@@ -228,48 +258,77 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
     const int e = f16_split_exponent(mx);
     kf2_sc = ldexpf(1.f, -e);
     kf2_unsc = ldexpf(1.f, e);
+    for (int t = tid; t < PB * RT * kWave; t += blockDim.x) stage_packed(a.KF2, kf2_sc, t, sA2);
+  }
+  // Factor operands.  Split mode: the packed blocks above.  bf16 mode: lane
+  // (l32, h) of K-block b, rank tile rt holds KF[16b + 8h + i][rt*32 + l32],
+  // i = 0..7, zero past d and R, in fp32.  One thread per (b, rt, lane).
+  if constexpr (BF) {
     for (int t = tid; t < KB * RT * kWave; t += blockDim.x) {
       const int ln = t % kWave, brt = t / kWave;
       const int b = brt / RT, rt = brt - b * RT;
       const int r = rt * kTile + (ln & 31), k0 = 16 * b + 8 * (ln >> 5);
       float v[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = k0 + i < d && r < R ? a.KF2[(k0 + i) * R + r] : 0.f;
-      uint32_t w[2][4];
-#pragma unroll
-      for (int p = 0; p < 4; ++p) split_f16x2_pair(v[2 * p] * kf2_sc, v[2 * p + 1] * kf2_sc, w[0][p], w[1][p]);
-#pragma unroll
-      for (int s = 0; s < 2; ++s) sA2[(brt * 2 + s) * kWave + ln] = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
-    }
-  }
-  // Factor operands: lane (l32, h) of K-block b, rank tile rt holds
-  // KF[16b + 8h + i][rt*32 + l32], i = 0..7, zero past d and R, as the fp16
-  // parts of KF 2^-e_K (split mode) or in fp32 (bf16 mode).  One thread per
-  // (b, rt, lane).
-  for (int t = tid; t < KB * RT * kWave; t += blockDim.x) {
-    const int ln = t % kWave, brt = t / kWave;
-    const int b = brt / RT, rt = brt - b * RT;
-    const int r = rt * kTile + (ln & 31), k0 = 16 * b + 8 * (ln >> 5);
-    float v[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) v[i] = k0 + i < d && r < R ? a.KF[(k0 + i) * R + r] : 0.f;
-    if constexpr (BF) {
+      for (int i = 0; i < 8; ++i) v[i] = k0 + i < d && r < R ? a.KF[(k0 + i) * R + r] : 0.f;
       sAf[2 * t] = make_float4(v[0], v[1], v[2], v[3]);
       sAf[2 * t + 1] = make_float4(v[4], v[5], v[6], v[7]);
-    } else {
-      uint32_t w[XP][4];
-#pragma unroll
-      for (int p = 0; p < 4; ++p) split_f16x2_pair(v[2 * p] * kf_sc, v[2 * p + 1] * kf_sc, w[0][p], w[1][p]);
-#pragma unroll
-      for (int s = 0; s < XP; ++s) sA[(brt * XP + s) * kWave + ln] = u32x4{w[s][0], w[s][1], w[s][2], w[s][3]};
     }
+  } else {
+    for (int t = tid; t < PB * RT * kWave; t += blockDim.x) stage_packed(a.KF, kf_sc, t, sA);
   }
   __syncthreads();
   // Factor operands are read where they are used: their index goes through
   // an opaque copy (zero added in inline asm) so that the compiler does not
   // hoist all of them out of the edge loop into registers; the pointer
   // itself stays a known LDS pointer.
-  auto a_op = [&](int base, int b, int rt, int s) -> u32x4 { return sA[base + ((b * RT + rt) * XP + s) * kWave]; };
+  auto a_op = [&](int base, int b, int rt) -> u32x4 { return sA[base + (b * RT + rt) * kWave]; };
+
+  // Feature operands of one edge.  Split mode: the lane's PN packed words of
+  // the gathered row (launch_feature_layout_packed), PQ 16-byte loads and a
+  // PT-word tail, each load of the 64 lanes one contiguous run; the MFMA
+  // operand of packed block b is words 4b .. 4b+3 taken modulo PN (slots
+  // [2 PN, 3 PN) repeat the hi words, past 3 PN the factor is zero).  bf16
+  // mode: channel tile t, K-block b is the lane's 16 bytes of the operand
+  // block xs[row][tile][b].  The gathered row is wave-uniform (row base in
+  // scalar registers, one 32-bit lane offset per tile).  Channel tiles past
+  // the layout's last read that tile; their results are never stored.
+  constexpr int XB = BF ? CT : XP;  // bf16 mode: operand rows per edge
+  struct XOps {
+    u32x4 v[BF ? XB * KB : (PQ > 0 ? PQ : 1)];
+    uint32_t t[(!BF && PT > 0) ? PT : 1];
+  };
+  const char* __restrict__ xs = static_cast<const char*>(a.feat);
+  const int n_ct = (C + kTile - 1) / kTile;  // channel tiles of the layout
+  const size_t row_bytes = BF ? size_t(n_ct) * XP * KB * 1024 : size_t(n_ct) * 256 * PN;
+  uint32_t lane_off[CT];
+  uint32_t tail_off = 0;
+#pragma unroll
+  for (int t = 0; t < CT; ++t) {
+    const int ct = min((cgrp * waves + wave) * CT + t, n_ct - 1);
+    lane_off[t] = BF ? uint32_t(ct * XP * KB * 1024 + h * 512 + l32 * 16) : uint32_t(ct * 256 * PN + lane * 16);
+    if (!BF && t == 0) tail_off = uint32_t(ct * 256 * PN + PQ * 1024 + lane * 4 * PT);
+  }
+  auto load_x = [&](int row, XOps& xb) {
+    const char* p = xs + size_t(row) * row_bytes;
+    if constexpr (BF) {
+#pragma unroll
+      for (int t = 0; t < XB; ++t)
+#pragma unroll
+        for (int b = 0; b < KB; ++b)
+          xb.v[t * KB + b] = *reinterpret_cast<const u32x4*>(p + lane_off[t] + uint32_t(b * 1024));
+    } else {
+#pragma unroll
+      for (int q = 0; q < PQ; ++q) xb.v[q] = *reinterpret_cast<const u32x4*>(p + lane_off[0] + uint32_t(q * 1024));
+#pragma unroll
+      for (int t = 0; t < PT; ++t) xb.t[t] = *reinterpret_cast<const uint32_t*>(p + tail_off + uint32_t(4 * t));
+    }
+  };
+  auto xw = [&](const XOps& xb, int j) -> uint32_t { return j < 4 * PQ ? xb.v[j / 4][j % 4] : xb.t[j - 4 * PQ]; };
+  auto xop = [&](const XOps& xb, int b) -> u32x4 {
+    return u32x4{xw(xb, (4 * b) % PN), xw(xb, (4 * b + 1) % PN), xw(xb, (4 * b + 2) % PN),
+                 xw(xb, (4 * b + 3) % PN)};
+  };
 
   f32x16 acc[RT][CT];
 #pragma unroll
@@ -294,27 +353,17 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
     float* dst = (ATOM || part < 0) ? a.out + size_t(seg) * d * C : a.partial + (size_t(range) * 2 + part) * d * C;
     constexpr int P16 = BF ? 1 : 2;
     if constexpr (T3) {
-      // V = KF2^T x[seg] for this lane's rank rows and channel, from the
-      // three part products, times the two operands' scales; H *= V
-      const int n_ct = (C + kTile - 1) / kTile;
-      const int ct = min((cgrp * waves + wave) * CT, n_ct - 1);
-      const char* p = static_cast<const char*>(a.feat) + size_t(seg) * (size_t(n_ct) * 2 * KB * 1024) +
-                      ct * 2 * KB * 1024 + h * 512 + l32 * 16;
-      u32x4 xv[2][KB];
-#pragma unroll
-      for (int s = 0; s < 2; ++s)
-#pragma unroll
-        for (int b = 0; b < KB; ++b) xv[s][b] = *reinterpret_cast<const u32x4*>(p + (s * KB + b) * 1024);
+      // V = KF2^T x[seg] for this lane's rank rows and channel, one packed
+      // K-reduction per rank tile (the three part products), times the two
+      // operands' scales; H *= V
+      XOps xv;
+      load_x(seg, xv);
       const float vsc = a.row_scale[seg] * kf2_unsc;
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
         f32x16 u = f32x16{};
 #pragma unroll
-        for (int b = 0; b < KB; ++b) u = mfma_f16(sA2[((b * RT + rt) * 2 + 1) * kWave + lane], xv[0][b], u);
-#pragma unroll
-        for (int b = 0; b < KB; ++b) u = mfma_f16(sA2[((b * RT + rt) * 2 + 0) * kWave + lane], xv[1][b], u);
-#pragma unroll
-        for (int b = 0; b < KB; ++b) u = mfma_f16(sA2[((b * RT + rt) * 2 + 0) * kWave + lane], xv[0][b], u);
+        for (int b = 0; b < PB; ++b) u = mfma_f16(sA2[(b * RT + rt) * kWave + lane], xop(xv, b), u);
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[rt][0][v] *= u[v] * vsc;
       }
@@ -380,16 +429,20 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
     for (int t = 0; t < CT; ++t) {
       const int c = c0 + t * kTile;
       if (c < C) {
+        // the lane's base (row 4h, channel c) and wave-uniform row offsets,
+        // so no per-row address is kept live across the kernel
+        float* dl = dst + (4 * h) * C + c;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int m = mt * kTile + acc_row(v, h);
+            const int du = (mt * kTile + 8 * (v >> 2) + (v & 3)) * C;
             if (m < d) {
               if constexpr (ATOM)
-                unsafeAtomicAdd(dst + size_t(m) * C + c, z[t][mt][v] * zsc);  // hardware float add
+                unsafeAtomicAdd(dl + du, z[t][mt][v] * zsc);  // hardware float add
               else
-                dst[size_t(m) * C + c] = z[t][mt][v] * zsc;
+                dl[du] = z[t][mt][v] * zsc;
             }
           }
       }
@@ -400,33 +453,10 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
       for (int t = 0; t < CT; ++t) acc[rt][t] = f32x16{};
   };
 
-  // Feature operands of one edge: part s (split mode) or channel tile t
-  // (bf16 mode), K-block b is the lane's 16 bytes of the operand block
-  // xs[row][tile][s][b]: the 64 lanes of a load read one contiguous
-  // kilobyte.  The gathered row is wave-uniform (row base in scalar
-  // registers, one 32-bit lane offset per tile).  Channel tiles past the
-  // layout's last read that tile; their results are never stored.
-  constexpr int XB = BF ? CT : XP;  // operand rows per edge
-  const char* __restrict__ xs = static_cast<const char*>(a.feat);
-  const int n_ct = (C + kTile - 1) / kTile;  // channel tiles of the layout
-  uint32_t lane_off[CT];
-#pragma unroll
-  for (int t = 0; t < CT; ++t) {
-    const int ct = min((cgrp * waves + wave) * CT + t, n_ct - 1);
-    lane_off[t] = uint32_t(ct * XP * KB * 1024 + h * 512 + l32 * 16);
-  }
-  auto load_x = [&](int row, u32x4 (&xb)[XB][KB]) {
-    const char* p = xs + size_t(row) * (size_t(n_ct) * XP * KB * 1024);
-#pragma unroll
-    for (int s = 0; s < XB; ++s)
-#pragma unroll
-      for (int b = 0; b < KB; ++b)
-        xb[s][b] = BF ? *reinterpret_cast<const u32x4*>(p + lane_off[s] + uint32_t(b * 1024))
-                      : *reinterpret_cast<const u32x4*>(p + lane_off[0] + uint32_t((s * KB + b) * 1024));
-  };
-  // U_e = KF^T x[row] for one rank tile from the three part products lo hi,
-  // hi lo, hi hi (smallest first), then acc += g_e * U_e with g (which
-  // carries the operands' scales) for this lane's rows
+  // U_e = KF^T x[row] for one rank tile as one packed K-reduction of PB
+  // steps holding the three part products (hi hi, hi lo, lo hi), then
+  // acc += g_e * U_e with g (which carries the operands' scales) for this
+  // lane's rows
   // rt*32 + 8q + 4h + i read four at a time.  The rank tiles are pipelined:
   // step rt issues the LDS reads of the factor parts of tile rt+1 and of g
   // for tile rt-1, runs the MFMA chain of tile rt into one of two U buffers,
@@ -444,7 +474,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
       kf[2 * i + 1] = sAf[(i * kWave + lane) * 2 + 1];
     }
   }
-  auto edge_compute_bf = [&](int e, const u32x4 (&xb)[XB][KB]) {
+  auto edge_compute_bf = [&](int e, const XOps& xb) {
     int ab = 2 * lane;
     asm volatile("" : "+v"(ab));
     float g[RT];
@@ -460,24 +490,22 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
         const u32x4 kop = {pack_bf16x2(g[rt] * f0.x, g[rt] * f0.y), pack_bf16x2(g[rt] * f0.z, g[rt] * f0.w),
                            pack_bf16x2(g[rt] * f1.x, g[rt] * f1.y), pack_bf16x2(g[rt] * f1.z, g[rt] * f1.w)};
 #pragma unroll
-        for (int t = 0; t < CT; ++t) acc[rt][t] = mfma_bf16(kop, xb[t][b], acc[rt][t]);
+        for (int t = 0; t < CT; ++t) acc[rt][t] = mfma_bf16(kop, xb.v[t * KB + b], acc[rt][t]);
       }
   };
-  auto edge_compute = [&](int e, const u32x4 (&xb)[XB][KB]) {
+  auto edge_compute = [&](int e, const XOps& xb) {
     if constexpr (BF) {
       edge_compute_bf(e, xb);
     } else {
       int ab = lane;
       asm volatile("" : "+v"(ab));
       const float* gb = sG + e * Rp + 4 * h;
-      u32x4 am[2][XP][KB];  // [buffer][part][K-block]
-      float4 gv[4];        // [row group]
+      u32x4 am[2][PB];  // [buffer][packed K-block]
+      float4 gv[4];     // [row group]
       f32x16 U[2];
       auto load_a = [&](int rt, int buf) {
 #pragma unroll
-        for (int sp = 0; sp < XP; ++sp)
-#pragma unroll
-          for (int b = 0; b < KB; ++b) am[buf][sp][b] = a_op(ab, b, rt, sp);
+        for (int b = 0; b < PB; ++b) am[buf][b] = a_op(ab, b, rt);
       };
       auto load_g = [&](int rt) {
 #pragma unroll
@@ -486,11 +514,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
       auto chain = [&](int buf) {
         f32x16 u = f32x16{};
 #pragma unroll
-        for (int b = 0; b < KB; ++b) u = mfma_f16(am[buf][1][b], xb[0][b], u);
-#pragma unroll
-        for (int b = 0; b < KB; ++b) u = mfma_f16(am[buf][0][b], xb[1][b], u);
-#pragma unroll
-        for (int b = 0; b < KB; ++b) u = mfma_f16(am[buf][0][b], xb[0][b], u);
+        for (int b = 0; b < PB; ++b) u = mfma_f16(am[buf][b], xop(xb, b), u);
         U[buf] = u;
       };
       auto fma_rt = [&](int rt, int buf) {
@@ -628,7 +652,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
         // Two operand buffers used alternately: the loads of edge f+1 are
         // issued before the MFMAs of edge f, and the scheduling barriers keep
         // the compiler from sinking them next to their use.
-        u32x4 x0[XB][KB], x1[XB][KB];
+        XOps x0, x1;
         load_x(__builtin_amdgcn_readfirstlane(sIdx[e]), x0);
         int f = e;
         for (; f + 1 < pe; f += 2) {

@@ -77,6 +77,68 @@ __global__ __launch_bounds__(256) void k_feature_layout(int d, int C, const TI* 
   }
 }
 
+// Packed split operands of the edge pass (fp32 features; see
+// launch_feature_layout_packed): per node and 32-channel tile, lane
+// (h, c) = (lane / 32, lane % 32) holds n = pk_rows(d) 32-bit words, word j
+// packing the fp16 values 2j (low half) and 2j + 1, value p being the hi
+// part of x'[h n + p][c] for p < n and the lo part of x'[h n + p - n][c]
+// otherwise (x' = x[node] 2^-e_node, zero past d and C).  The words sit as
+// [n / 4 quads][64 lanes][4 words] and then [64 lanes][n % 4 words], so the
+// 64 lanes of each load read one contiguous run.  One block per node: its
+// [d, C] rows staged in LDS with their largest magnitude, then one thread per
+// (channel tile, quad or tail, lane).
+__device__ __forceinline__ _Float16 packed_value(const float* tile, int d, int C, int n, int h, int c, int p,
+                                                 float sc) {
+  const bool lo = p >= n;
+  const int row = h * n + (lo ? p - n : p);
+  const float v = (row < d && c < C) ? tile[row * C + c] * sc : 0.f;
+  const _Float16 hi = static_cast<_Float16>(v);
+  return lo ? static_cast<_Float16>(v - float(hi)) : hi;
+}
+
+__global__ __launch_bounds__(256) void k_feature_layout_packed(int d, int C, const float* __restrict__ x,
+                                                               uint32_t* __restrict__ xp,
+                                                               float* __restrict__ row_scale) {
+  extern __shared__ float tile[];  // [d][C], then four floats for the row maximum
+  float* red = tile + d * C;
+  const int node = blockIdx.x;
+  const float* src = x + size_t(node) * d * C;
+  float mx = 0.f;
+  for (int i = threadIdx.x; i < d * C; i += blockDim.x) {
+    const float v = src[i];
+    tile[i] = v;
+    mx = fmaxf(mx, fabsf(v));
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  const int e = f16_split_exponent(mx);
+  const float sc = ldexpf(1.f, -e);
+  if (threadIdx.x == 0) row_scale[node] = ldexpf(1.f, e);
+  const int n = pk_rows(d), nq = n / 4, nt = n % 4, groups = nq + (nt > 0);
+  const int n_ct = (C + 31) / 32;
+  uint32_t* dst = xp + size_t(node) * n_ct * 64 * n;
+  auto word = [&](int h, int c, int j) -> uint32_t {
+    const _Float16 a = packed_value(tile, d, C, n, h, c, 2 * j, sc);
+    const _Float16 b = packed_value(tile, d, C, n, h, c, 2 * j + 1, sc);
+    return uint32_t(__builtin_bit_cast(uint16_t, a)) | (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
+  };
+  for (int i = threadIdx.x; i < n_ct * groups * 64; i += blockDim.x) {
+    const int lane = i & 63, g = i >> 6;
+    const int ct = g / groups, q = g - ct * groups;
+    const int h = lane >> 5, c = ct * 32 + (lane & 31);
+    uint32_t* o = dst + size_t(ct) * 64 * n;
+    if (q < nq) {
+      *reinterpret_cast<u32x4*>(o + (q * 64 + lane) * 4) =
+          u32x4{word(h, c, 4 * q), word(h, c, 4 * q + 1), word(h, c, 4 * q + 2), word(h, c, 4 * q + 3)};
+    } else {
+      for (int t = 0; t < nt; ++t) o[nq * 256 + lane * nt + t] = word(h, c, 4 * nq + t);
+    }
+  }
+}
+
 template <int DP, int P, typename TI>
 hipError_t launch_dp(int N, int d, int C, const TI* x, uint16_t* xs, float* row_scale, hipStream_t s) {
   const size_t lds = (size_t(d) * C + 4) * 4;
@@ -181,6 +243,18 @@ hipError_t launch_direct_layout(int N, int d, int C, int Cp, const void* x, bool
   if (parts != 1) return hipErrorInvalidValue;
   return x_is_f32 ? launch_direct_p<1>(N, d, C, Cp, static_cast<const float*>(x), xd, nullptr, pm, s)
                   : launch_direct_p<1>(N, d, C, Cp, static_cast<const uint16_t*>(x), xd, nullptr, pm, s);
+}
+
+hipError_t launch_feature_layout_packed(int N, int d, int C, const float* x, void* xp, float* row_scale,
+                                        hipStream_t s) {
+  if (N == 0) return hipSuccess;
+  if (!x || !xp || !row_scale || size_t(d) * C * 4 + 16 > 160 * 1024) return hipErrorInvalidValue;
+  const size_t lds = (size_t(d) * C + 4) * 4;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_feature_layout_packed),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  if (e != hipSuccess) return e;
+  k_feature_layout_packed<<<dim3(N), dim3(256), lds, s>>>(d, C, x, static_cast<uint32_t*>(xp), row_scale);
+  return hipGetLastError();
 }
 
 hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,

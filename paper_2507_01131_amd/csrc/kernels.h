@@ -49,7 +49,8 @@ struct EdgeArgs {
   const float* Bf;           // [d, R]
   const float* radial_w;     // [n_radial, R]
   const float* KF2;          // [d, R] second node factor of the three-input product (launch_cp_edge_t3 only)
-  const void* feat;          // [n_feat_rows, d, C]
+  const void* feat;          // parts = 2: launch_feature_layout_packed's words; parts = 1: the bf16 blocks
+                             // of launch_feature_layout
   float* out;                // [n_seg, d, C]
   int n_range;               // edge ranges (EdgePlan::n_range)
   int pieces_per_block;      // ranges per workgroup (EdgePlan::per_block)
@@ -79,6 +80,23 @@ EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E, bool t3 
 int edge_kpad(int d);
 hipError_t launch_feature_layout(int N, int d, int C, const void* x, bool x_is_f32, int parts, void* xs,
                                  float* row_scale, hipStream_t s);
+// Packed split operands of the edge pass for fp32 features (the layout
+// launch_cp_edge reads when parts = 2).  With n = pk_rows(d) = ceil(d / 2),
+// lane half h of a 32x32x16 MFMA owns degree rows h n .. h n + n - 1 and gives
+// each of them three K slots: (x hi, factor hi), (x lo, factor hi),
+// (x hi, factor lo), grouped as slots [0, n), [n, 2n), [2n, 3n) of the
+// lane's 8 pk_blocks(d) slots (the rest pair with zero factor values), so
+// the three part products of the fp32-level contraction are one K-reduction
+// of pk_blocks(d) steps.  x'[node] = x[node] 2^-e_node as in
+// launch_feature_layout (row_scale[node] = 2^e_node).  Lane (h, c) of channel
+// tile ct stores n words, word j = fp16 values 2j, 2j + 1 of the sequence
+// (hi of rows h n .., then lo of rows h n ..); per node and tile the words
+// are [n / 4][64 lanes][4] then [64 lanes][n % 4]: 256 n bytes.  The slots
+// [2n, 3n) reuse the first words, so each value is loaded once.
+__host__ __device__ constexpr int pk_rows(int d) { return (d + 1) / 2; }
+__host__ __device__ constexpr int pk_blocks(int d) { return (3 * pk_rows(d) + 7) / 8; }
+hipError_t launch_feature_layout_packed(int N, int d, int C, const float* x, void* xp, float* row_scale,
+                                        hipStream_t s);
 // Features for the backward's destination kernels, blocked for contractions
 // over channels: xd [N, parts, Cp / 16, 2, d, 8] of 16-bit values, element
 // [n][p][s][h][k][i] = part p of x[n][k][c(s, h, i)] with c = 16 s + 8 h + i,
