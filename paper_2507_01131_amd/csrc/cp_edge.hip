@@ -40,10 +40,12 @@ __global__ __launch_bounds__(256) void k_range_fixup(int E, int n_range, int dC,
 
 // The output factor EF [d, R] in the operand blocks of the segment
 // epilogue's 32x32x16 MFMA: block (mt, rt, q), lane l holds
-// EF[mt*32 + l%32][rt*32 + acc_krow(q, l/32, i)], i = 0..7 (zero past d and
-// R), the ranks in the order the accumulators hold them.  P = 2: fp16 hi and
-// lo of EF 2^-e with 2^e (EF's largest |EF| to [2^13, 2^14)) to ef_scale;
-// P = 1: bf16.  One block.
+// EF[mt*32 + l%32][rt*32 + k(q, l/32, i)], i = 0..7 (zero past d and R).
+// P = 2 (fp32 features): ranks in natural order, k = 16q + 8h + i (the
+// epilogue transposes its sums through LDS), fp16 hi and lo of EF 2^-e with
+// 2^e (EF's largest |EF| to [2^13, 2^14)) to ef_scale; P = 1 (bf16): ranks
+// in the order the accumulators hold them, k = acc_krow(q, h, i), bf16.  One
+// block.
 template <int P>
 __global__ __launch_bounds__(256) void k_ef_blocks(int d, int R, int RT, int MT, const float* __restrict__ EF,
                                                    u32x4* __restrict__ out, float* __restrict__ ef_scale) {
@@ -69,7 +71,8 @@ __global__ __launch_bounds__(256) void k_ef_blocks(int d, int R, int RT, int MT,
     uint32_t w[P][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int r0 = rt * kTile + acc_krow(q, hh, 2 * i), r1 = rt * kTile + acc_krow(q, hh, 2 * i + 1);
+      const int r0 = rt * kTile + (P == 2 ? 16 * q + 8 * hh + 2 * i : acc_krow(q, hh, 2 * i));
+      const int r1 = rt * kTile + (P == 2 ? 16 * q + 8 * hh + 2 * i + 1 : acc_krow(q, hh, 2 * i + 1));
       const float v0 = (m < d && r0 < R) ? EF[m * R + r0] : 0.f;
       const float v1 = (m < d && r1 < R) ? EF[m * R + r1] : 0.f;
       if constexpr (P == 2)
@@ -113,7 +116,8 @@ EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E, bool t3)
   const int RT = (R + kTile - 1) / kTile, d = (L + 1) * (L + 1);
   const EdgeGrid gr = edge_grid(C, RT, bf16);
   // workgroups per CU: as many as the wave slots (four SIMDs) and LDS allow
-  const int lds = edge_smem(RT, bf16, d, n_radial, edge_chunk(L, RT, bf16, n_radial, t3), t3).floats * 4;
+  const int lds =
+      edge_smem(RT, bf16, d, n_radial, edge_chunk(L, RT, bf16, n_radial, t3), t3, edge_rega(L, RT, bf16)).floats * 4;
   int per_cu = 160 * 1024 / lds;
   const int by_waves = 4 * edge_waves_per_eu(L, RT, bf16) / gr.waves;
   if (per_cu > by_waves) per_cu = by_waves;

@@ -90,14 +90,22 @@ __host__ __device__ constexpr int edge_xp(bool bf) { return bf ? 1 : 2; }
 __host__ __device__ constexpr int edge_ct(bool bf, int RT) { return bf && RT <= 4 ? 2 : 1; }
 
 // Two waves per SIMD (two workgroups per CU) when the accumulators and the
-// double-buffered operands fit in 256 registers without spilling in the edge
-// loop; one otherwise.
+// operands fit in 256 registers without spilling in the edge loop; one
+// otherwise.  Split mode: accumulators 16 RT, two buffers of packed x words
+// 2 PN, two rank tiles' factor blocks 8 PB and two U tiles 32 within 168
+// (the rest holds addresses, loop state and the epilogue's temporaries).
 __host__ __device__ constexpr int edge_waves_per_eu(int L, int RT, bool bf) {
   return bf ? (16 * RT * edge_ct(bf, RT) + 8 * edge_ct(bf, RT) * edge_kb((L + 1) * (L + 1)) <=
                        (edge_kb((L + 1) * (L + 1)) == 2 ? 160 : 128)
                    ? 2
                    : 1)
             : (16 * RT + 2 * pk_rows((L + 1) * (L + 1)) + 8 * pk_blocks((L + 1) * (L + 1)) + 32 <= 168 ? 2 : 1);
+}
+// Split mode: whether all PB RT packed factor blocks stay in registers
+// across the edge loop (no factor reads from LDS per edge): up to 80
+// registers at two waves per SIMD, 160 at one.
+__host__ __device__ constexpr bool edge_rega(int L, int RT, bool bf) {
+  return !bf && 4 * pk_blocks((L + 1) * (L + 1)) * RT <= (edge_waves_per_eu(L, RT, bf) == 2 ? 80 : 160);
 }
 
 // Most ranges a workgroup takes: two where two workgroups share a CU (their
@@ -114,8 +122,14 @@ __host__ __device__ constexpr int edge_max_ranges(int L, int RT, bool bf) {
 __host__ __device__ constexpr bool edge_reg_kf(int, int) { return false; }
 
 struct EdgeSmem {
-  int Rp, off_a, off_g, off_y, off_vec, off_phi, off_idx, off_sc, off_bnd, off_a2, floats;
+  int Rp, off_a, off_g, off_y, off_vec, off_phi, off_idx, off_sc, off_bnd, off_a2, off_t, floats;
 };
+
+// Per-wave transpose area of the split-mode segment epilogue: 32 channel rows
+// of 32 ranks, row stride 36 floats (16-byte reads of eight ranks by 32
+// channels then spread over all banks).
+constexpr int kTrStride = 36;
+constexpr int kTrFloats = kTile * kTrStride;
 
 // LDS regions (in floats): the factor operands, split mode
 // [pk_blocks(d)][RT][64 lanes] x 16 bytes of fp16 (packed slots), bf16 mode
@@ -123,9 +137,11 @@ struct EdgeSmem {
 // rounded up to a whole 32-row tile), harmonics, normalised edge vectors with
 // their lengths, radial basis, gathered rows, the edges' operand scales, and
 // the segment starts of the chunk (positions, keys, count and the two
-// partial-segment flags); with t3 (the three-input product) last the second
-// node factor's operands in the layout of the first.
-__host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radial, int chunk, bool t3 = false) {
+// partial-segment flags); with t3 (the three-input product) the second node
+// factor's operands in the layout of the first; in split mode last the
+// epilogue's transpose areas, one per wave.
+__host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radial, int chunk, bool t3 = false,
+                                              bool rega = false) {
   EdgeSmem s{};
   s.Rp = RT * kTile;
   int o = 0;
@@ -149,6 +165,9 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radi
   o = (o + 3) & ~3;
   s.off_a2 = o;
   if (t3) o += pk_blocks(d) * RT * kWave * 4;
+  (void)rega;
+  s.off_t = o;
+  if (!bf) o += kMaxWavesPerBlock * kTrFloats;
   s.floats = o;
   return s;
 }
@@ -179,7 +198,8 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   // per lane and edge loaded as PQ quads and a PT-word tail
   constexpr int PN = pk_rows(d), PB = pk_blocks(d), PQ = PN / 4, PT = PN % 4;
   extern __shared__ float smem[];
-  const EdgeSmem S = edge_smem(RT, BF, d, a.n_radial, chunk, T3);
+  constexpr bool kRegA = edge_rega(L, RT, BF);
+  const EdgeSmem S = edge_smem(RT, BF, d, a.n_radial, chunk, T3, kRegA);
   u32x4* sA = reinterpret_cast<u32x4*>(smem + S.off_a);
   u32x4* sA2 = reinterpret_cast<u32x4*>(smem + S.off_a2);
   float4* sAf = reinterpret_cast<float4*>(smem + S.off_a);
@@ -278,11 +298,16 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
     for (int t = tid; t < PB * RT * kWave; t += blockDim.x) stage_packed(a.KF, kf_sc, t, sA);
   }
   __syncthreads();
-  // Factor operands are read where they are used: their index goes through
-  // an opaque copy (zero added in inline asm) so that the compiler does not
-  // hoist all of them out of the edge loop into registers; the pointer
-  // itself stays a known LDS pointer.
+  // Split mode with kRegA: every packed factor block is loaded into
+  // registers at the start of each run of edges of one segment within a chunk
+  // (areg[b * RT + rt]), so the edge loop reads no factor from LDS while the
+  // geometry phase and the segment epilogue do not hold them.  Otherwise the blocks are read from
+  // LDS where they are used.  Either way their index goes through an opaque
+  // copy (zero added in inline asm) so that the compiler does not hoist the
+  // reads out of the loops; the pointer itself stays a known LDS pointer.
+  u32x4 areg[kRegA ? PB * RT : 1];
   auto a_op = [&](int base, int b, int rt) -> u32x4 { return sA[base + (b * RT + rt) * kWave]; };
+  float* sTr = smem + S.off_t + wave * kTrFloats;  // split mode: this wave's transpose area
 
   // Feature operands of one edge.  Split mode: the lane's PN packed words of
   // the gathered row (launch_feature_layout_packed), PQ 16-byte loads and a
@@ -352,10 +377,24 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   auto finish = [&](int seg, int part) {
     float* dst = (ATOM || part < 0) ? a.out + size_t(seg) * d * C : a.partial + (size_t(range) * 2 + part) * d * C;
     constexpr int P16 = BF ? 1 : 2;
+    // EF's operand blocks of one rank tile (all mt, both K-steps q and
+    // parts), double-buffered: tile 0's loads go out first, before the scale
+    // reduction, and tile rt+1's while tile rt computes, so no step waits a
+    // full memory latency for its operand
+    u32x4 ef[2][MT][2][P16];
+    auto load_ef = [&](int rt, int buf) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int p = 0; p < P16; ++p) ef[buf][mt][q][p] = efb[((((mt * RT + rt) * 2 + q) * kWave) + lane) * P16 + p];
+    };
+    load_ef(0, 0);
     if constexpr (T3) {
-      // V = KF2^T x[seg] for this lane's rank rows and channel, one packed
-      // K-reduction per rank tile (the three part products), times the two
-      // operands' scales; H *= V
+      // V^T = x[seg]^T KF2 in the accumulators' layout (channels x ranks),
+      // one packed K-reduction per rank tile (the three part products), times
+      // the two operands' scales; H *= V
       XOps xv;
       load_x(seg, xv);
       const float vsc = a.row_scale[seg] * kf2_unsc;
@@ -363,7 +402,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
       for (int rt = 0; rt < RT; ++rt) {
         f32x16 u = f32x16{};
 #pragma unroll
-        for (int b = 0; b < PB; ++b) u = mfma_f16(sA2[(b * RT + rt) * kWave + lane], xop(xv, b), u);
+        for (int b = 0; b < PB; ++b) u = mfma_f16(xop(xv, b), sA2[(b * RT + rt) * kWave + lane], u);
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[rt][0][v] *= u[v] * vsc;
       }
@@ -388,43 +427,63 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
     for (int t = 0; t < CT; ++t)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) z[t][mt] = f32x16{};
+    if constexpr (BF) {
+      // bf16 mode: acc[rt][t] holds H (ranks x channels), so its registers
+      // 8q .. 8q+7 are a K operand as they stand (ranks in acc_krow order)
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
+      for (int rt = 0; rt < RT; ++rt) {
+        if (rt + 1 < RT) load_ef(rt + 1, (rt + 1) & 1);
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        u32x4 hp[CT][P16];
-#pragma unroll
-        for (int t = 0; t < CT; ++t) {
-          uint32_t w[P16][4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float v0 = acc[rt][t][8 * q + 2 * i] * hsc, v1 = acc[rt][t][8 * q + 2 * i + 1] * hsc;
-            if constexpr (BF)
-              w[0][i] = pack_bf16x2_rne(v0, v1);
-            else
-              split_f16x2_pair(v0, v1, w[0][i], w[1][i]);
-          }
-#pragma unroll
-          for (int p = 0; p < P16; ++p) hp[t][p] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
-        }
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          u32x4 ea[P16];
-#pragma unroll
-          for (int p = 0; p < P16; ++p) ea[p] = efb[((((mt * RT + rt) * 2 + q) * kWave) + lane) * P16 + p];
+        for (int q = 0; q < 2; ++q) {
+          u32x4 hp[CT];
 #pragma unroll
           for (int t = 0; t < CT; ++t) {
-            if constexpr (BF) {
-              z[t][mt] = mfma_bf16(ea[0], hp[t][0], z[t][mt]);
-            } else {
-              z[t][mt] = mfma_f16(ea[1], hp[t][0], z[t][mt]);
-              z[t][mt] = mfma_f16(ea[0], hp[t][1], z[t][mt]);
-              z[t][mt] = mfma_f16(ea[0], hp[t][0], z[t][mt]);
-            }
+            uint32_t w[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) w[i] = pack_bf16x2_rne(acc[rt][t][8 * q + 2 * i], acc[rt][t][8 * q + 2 * i + 1]);
+            hp[t] = u32x4{w[0], w[1], w[2], w[3]};
+          }
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int t = 0; t < CT; ++t) z[t][mt] = mfma_bf16(ef[rt & 1][mt][q][0], hp[t], z[t][mt]);
+        }
+        __builtin_amdgcn_sched_barrier(0);  // one rank tile's operands live at a time
+      }
+    } else {
+      // split mode: acc[rt][0] holds H^T (channels x ranks, lane column =
+      // rank rt*32 + l32, rows = channels 8j + 4h + i); through the wave's
+      // LDS area it becomes the K operand of ranks 16q + 8h + i for channel
+      // l32, scaled by hsc and split into fp16 hi and lo (three products
+      // against EF's parts, ranks in natural order)
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        if (rt + 1 < RT) load_ef(rt + 1, (rt + 1) & 1);
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          sTr[(8 * (v >> 2) + 4 * h + (v & 3)) * kTrStride + l32] = acc[rt][0][v] * hsc;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const float4 f0 = *reinterpret_cast<const float4*>(sTr + l32 * kTrStride + 16 * q + 8 * h);
+          const float4 f1 = *reinterpret_cast<const float4*>(sTr + l32 * kTrStride + 16 * q + 8 * h + 4);
+          uint32_t w[2][4];
+          split_f16x2_pair(f0.x, f0.y, w[0][0], w[1][0]);
+          split_f16x2_pair(f0.z, f0.w, w[0][1], w[1][1]);
+          split_f16x2_pair(f1.x, f1.y, w[0][2], w[1][2]);
+          split_f16x2_pair(f1.z, f1.w, w[0][3], w[1][3]);
+          const u32x4 hp0 = u32x4{w[0][0], w[0][1], w[0][2], w[0][3]};
+          const u32x4 hp1 = u32x4{w[1][0], w[1][1], w[1][2], w[1][3]};
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            const u32x4 e0 = ef[rt & 1][mt][q][0], e1 = ef[rt & 1][mt][q][1];
+            z[0][mt] = mfma_f16(e1, hp0, z[0][mt]);
+            z[0][mt] = mfma_f16(e0, hp1, z[0][mt]);
+            z[0][mt] = mfma_f16(e0, hp0, z[0][mt]);
           }
         }
-        __builtin_amdgcn_sched_barrier(0);  // one (rt, q) step's operands live at a time
+        __builtin_amdgcn_sched_barrier(0);  // the next tile's writes after this tile's reads
       }
+    }
 #pragma unroll
     for (int t = 0; t < CT; ++t) {
       const int c = c0 + t * kTile;
@@ -453,15 +512,16 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
       for (int t = 0; t < CT; ++t) acc[rt][t] = f32x16{};
   };
 
-  // U_e = KF^T x[row] for one rank tile as one packed K-reduction of PB
-  // steps holding the three part products (hi hi, hi lo, lo hi), then
-  // acc += g_e * U_e with g (which carries the operands' scales) for this
-  // lane's rows
-  // rt*32 + 8q + 4h + i read four at a time.  The rank tiles are pipelined:
-  // step rt issues the LDS reads of the factor parts of tile rt+1 and of g
-  // for tile rt-1, runs the MFMA chain of tile rt into one of two U buffers,
-  // and the VALU multiply-adds of tile rt-1 from the other, so that neither
-  // LDS latency nor the MFMA drain stalls the chain.
+  // Split mode: U_e^T = x[row]^T KF for one rank tile (channels x ranks,
+  // the MFMA's A operand the packed x words, its B operand the packed factor
+  // blocks) as one packed K-reduction of PB steps holding the three part
+  // products (hi hi, hi lo, lo hi), then acc += g_e[r] * U_e^T with this
+  // lane's one rank r = rt*32 + l32 (g carries the operands' scales).  The
+  // rank tiles are pipelined: step rt runs the MFMA chain of tile rt into one
+  // of two U buffers (with the factor blocks of tile rt+1 read from LDS
+  // meanwhile unless they are kept in registers) and the VALU multiply-adds
+  // of tile rt-1 from the other, so that the MFMA drain does not stall the
+  // chain.
   // bf16 mode: per (K-block, rank tile) the K operand bf16(g_e[r] KF[k][r])
   // for this lane's eight k, built once and fed to the CT channel tiles; the
   // K factor values come from registers when they fit, else from LDS.
@@ -499,44 +559,41 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
     } else {
       int ab = lane;
       asm volatile("" : "+v"(ab));
-      const float* gb = sG + e * Rp + 4 * h;
-      u32x4 am[2][PB];  // [buffer][packed K-block]
-      float4 gv[4];     // [row group]
+      u32x4 am[kRegA ? 1 : 2][kRegA ? 1 : PB];  // [buffer][packed K-block] when read from LDS
+      float gl[RT];
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) gl[rt] = sG[e * Rp + rt * kTile + l32];
       f32x16 U[2];
       auto load_a = [&](int rt, int buf) {
+        if constexpr (!kRegA) {
 #pragma unroll
-        for (int b = 0; b < PB; ++b) am[buf][b] = a_op(ab, b, rt);
+          for (int b = 0; b < PB; ++b) am[buf][b] = a_op(ab, b, rt);
+        }
       };
-      auto load_g = [&](int rt) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) gv[q] = *reinterpret_cast<const float4*>(gb + rt * kTile + 8 * q);
-      };
-      auto chain = [&](int buf) {
+      auto chain = [&](int rt, int buf) {
         f32x16 u = f32x16{};
 #pragma unroll
-        for (int b = 0; b < PB; ++b) u = mfma_f16(am[buf][b], xop(xb, b), u);
+        for (int b = 0; b < PB; ++b) {
+          if constexpr (kRegA)
+            u = mfma_f16(xop(xb, b), areg[b * RT + rt], u);
+          else
+            u = mfma_f16(xop(xb, b), am[buf][b], u);
+        }
         U[buf] = u;
       };
       auto fma_rt = [&](int rt, int buf) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          acc[rt][0][4 * q + 0] += gv[q].x * U[buf][4 * q + 0];
-          acc[rt][0][4 * q + 1] += gv[q].y * U[buf][4 * q + 1];
-          acc[rt][0][4 * q + 2] += gv[q].z * U[buf][4 * q + 2];
-          acc[rt][0][4 * q + 3] += gv[q].w * U[buf][4 * q + 3];
-        }
+        for (int v = 0; v < 16; ++v) acc[rt][0][v] += gl[rt] * U[buf][v];
       };
       load_a(0, 0);
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
         if (rt + 1 < RT) load_a(rt + 1, (rt + 1) & 1);
-        if (rt > 0) load_g(rt - 1);
         __builtin_amdgcn_sched_barrier(0);
-        chain(rt & 1);
+        chain(rt, rt & 1);
         if (rt > 0) fma_rt(rt - 1, (rt - 1) & 1);
         __builtin_amdgcn_sched_barrier(0);
       }
-      load_g(RT - 1);
       fma_rt(RT - 1, (RT - 1) & 1);
     }
   };
@@ -649,6 +706,14 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
           next = bi < nb ? __builtin_amdgcn_readfirstlane(sBnd[bi]) : n;
         }
         const int pe = next;
+        // kRegA: the factor blocks for this piece (after any epilogue, so
+        // they are not held across it or across the chunk's geometry phase)
+        if constexpr (kRegA) {
+          int ai = lane;
+          asm volatile("" : "+v"(ai));
+#pragma unroll
+          for (int i = 0; i < PB * RT; ++i) areg[i] = sA[ai + i * kWave];
+        }
         // Two operand buffers used alternately: the loads of edge f+1 are
         // issued before the MFMAs of edge f, and the scheduling barriers keep
         // the compiler from sinking them next to their use.
@@ -679,7 +744,8 @@ inline int edge_chunk(int L, int RT, bool bf, int n_radial, bool t3 = false) {
   const int d = (L + 1) * (L + 1);
   const int budget = 160 * 1024 / edge_waves_per_eu(L, RT, bf);
   int chunk = 64;
-  while (chunk > 8 && edge_smem(RT, bf, d, n_radial, chunk, t3).floats * 4 > budget) chunk >>= 1;
+  while (chunk > 8 && edge_smem(RT, bf, d, n_radial, chunk, t3, edge_rega(L, RT, bf)).floats * 4 > budget)
+    chunk >>= 1;
   return chunk;
 }
 
@@ -702,7 +768,7 @@ hipError_t launch_l_rt_m(const EdgeArgs& a, hipStream_t s) {
   const int waves = gr.waves, n_cgrp = gr.n_cgrp;
   if (a.E > 0) {
     const int chunk = edge_chunk(L, RT, BF, a.n_radial, T3);
-    const size_t lds = size_t(edge_smem(RT, BF, d, a.n_radial, chunk, T3).floats) * 4;
+    const size_t lds = size_t(edge_smem(RT, BF, d, a.n_radial, chunk, T3, edge_rega(L, RT, BF)).floats) * 4;
     auto k = k_cp_edge<L, RT, BF, ATOM, T3>;
     hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
