@@ -10,10 +10,22 @@
 
 namespace tdn {
 namespace edge_detail {
-template <int L>
-hipError_t launch_cp_edge_l(const EdgeArgs& a, hipStream_t s);
-template <int L>
-hipError_t launch_cp_edge_atomic_l(const EdgeArgs& a, hipStream_t s);
+// Instantiated in their own translation units (cp_edge_l<L>.hip,
+// cp_edge_atomic.hip, cp_edge_t3.hip); declared here so that this file does
+// not compile the kernels again.
+extern template hipError_t launch_cp_edge_l<0>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_l<1>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_l<2>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_l<3>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_l<4>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_l<5>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_l<6>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_atomic_l<2>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_atomic_l<3>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_atomic_l<4>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_t3_l<2>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_t3_l<3>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_t3_l<4>(const EdgeArgs&, hipStream_t);
 
 namespace {
 

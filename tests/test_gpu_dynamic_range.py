@@ -4,7 +4,8 @@ The float32 path runs its 16-bit MFMA contractions on two-part fp16 splits of
 operands scaled by one power of two per node row (or segment, tile or
 factor).  These tests give every node row values spread over 2^-20 .. 2^20
 across its degree rows and channels, make one node 2^40 times larger than
-every other, and draw the output cotangent the same way, so that an operand
+every other, and spread the output cotangent the same way (without the large
+node, which keeps every product inside the float32 range), so that an operand
 scaled or split with the wrong granularity loses the small values a row or a
 segment holds.  Forward output, the saved Z and grad_x are checked per node
 row, grad_edge_vec per edge against its magnitude scale, grad_W and the
