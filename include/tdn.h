@@ -70,7 +70,11 @@ typedef enum { TDN_F32 = 0, TDN_BF16 = 1 } tdn_dtype;
 typedef struct {
   int32_t L;            /* maximum degree, 0..6; d = (L+1)^2 components          */
   int32_t C;            /* channels (shared multiplicity), multiple of 16, <= 256  */
-  int32_t R;            /* CP rank, 1..256                                          */
+  int32_t R;            /* CP rank, 1..4096; ranks above 256 run as chunks of
+                           consecutive rank columns whose per-node sums are added
+                           in chunk order (the forward, backward and
+                           no-allocation forward; the three-input product and
+                           the atomics ablation take at most 256)            */
   int32_t n_nodes;      /* N >= 0                                                   */
   int32_t n_edges;      /* E >= 0 (E > 0 needs N > 0)                              */
   int32_t n_radial;     /* Gaussian radial functions, 2..16                        */

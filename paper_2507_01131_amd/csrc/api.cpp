@@ -38,12 +38,32 @@ tdn_status hip_fail(hipError_t e) {
 
 int dim_of(int L) { return (L + 1) * (L + 1); }
 
+// Ranks: the edge kernels take at most kChunkR; larger ranks (up to
+// kMaxRank, e.g. the exact rank d^2 construction of Thm. 2) run as chunks of
+// consecutive 32-rank tiles, balanced, whose per-node results are summed in
+// chunk order (the layer is linear in each rank component).
+constexpr int kChunkR = 256;
+constexpr int kMaxRank = 4096;
+int rank_chunks(int R) { return (R + kChunkR - 1) / kChunkR; }
+void chunk_range(int R, int c, int nch, int* r0, int* n) {
+  const int tiles = (R + 31) / 32, per = (tiles + nch - 1) / nch;
+  *r0 = std::min(R, c * per * 32);
+  *n = std::min(per * 32, R - *r0);
+}
+tdn_problem chunk_problem(const tdn_problem& p, int c) {
+  tdn_problem q = p;
+  int r0 = 0, n = p.R;
+  chunk_range(p.R, c, rank_chunks(p.R), &r0, &n);
+  q.R = n;
+  return q;
+}
+
 tdn_status check_problem(const tdn_problem* p) {
   if (!p) return TDN_ERR_NULL_POINTER;
   if (p->feat_dtype != TDN_F32 && p->feat_dtype != TDN_BF16) return TDN_ERR_BAD_DTYPE;
   if (p->L < 0 || p->L > 6) return TDN_ERR_BAD_SHAPE;
   if (p->C < 16 || p->C > 256 || p->C % 16 != 0) return TDN_ERR_BAD_SHAPE;
-  if (p->R < 1 || p->R > 256) return TDN_ERR_BAD_SHAPE;
+  if (p->R < 1 || p->R > kMaxRank) return TDN_ERR_BAD_SHAPE;
   if (p->n_nodes < 0 || p->n_edges < 0) return TDN_ERR_BAD_SHAPE;
   if (p->n_edges > 0 && p->n_nodes == 0) return TDN_ERR_BAD_SHAPE;
   if (p->n_radial < 2 || p->n_radial > 16) return TDN_ERR_BAD_SHAPE;
@@ -85,16 +105,26 @@ size_t xt_xc_bytes(const tdn_problem& p) {
 // the output factor's epilogue operand blocks and scale, then the partial
 // slots of the edge pass (two [d, C] rows per edge range)
 size_t ef_pad_bytes(const tdn_problem& p) { return al(tdn::edge_ef_bytes(dim_of(p.L), p.R)); }
-size_t partial_bytes(const tdn_problem& p) {
+size_t partial_bytes_one(const tdn_problem& p) {
   const bool bf16 = p.feat_dtype == TDN_BF16;
   int n_range = tdn::edge_plan(p.L, p.R, p.C, p.n_radial, bf16, p.n_edges).n_range;
   if (!bf16 && p.L >= 2 && p.L <= 4)  // the three-input product's plan may use more ranges
     n_range = std::max(n_range, tdn::edge_plan(p.L, p.R, p.C, p.n_radial, false, p.n_edges, true).n_range);
   return ef_pad_bytes(p) + size_t(n_range) * 2 * dim_of(p.L) * p.C * 4;
 }
+// the largest over the problem's rank chunks
+size_t partial_bytes(const tdn_problem& p) {
+  size_t m = 0;
+  for (int c = 0; c < rank_chunks(p.R); ++c) m = std::max(m, partial_bytes_one(chunk_problem(p, c)));
+  return m;
+}
+// rank chunks: the chunk's factor and radial-weight columns
+size_t slice_bytes(const tdn_problem& p) {
+  return rank_chunks(p.R) > 1 ? size_t(3 * dim_of(p.L) + p.n_radial) * kChunkR * 4 : 0;
+}
 
 struct FwdLayout {
-  size_t z, xt, part, sort, wp, flags, total;
+  size_t z, xt, part, sort, wp, fsl, ztmp, flags, total;
 };
 FwdLayout fwd_layout(const tdn_problem& p) {
   FwdLayout f{};
@@ -110,6 +140,10 @@ FwdLayout fwd_layout(const tdn_problem& p) {
   o += al(p.edges_sorted ? 0 : tdn::sort_plan(p.n_nodes, p.n_edges).bytes);
   f.wp = o;
   o += al(tdn::node_gemm_ws_bytes(p.C));
+  f.fsl = o;  // rank chunks: factor columns and a second Z for the chunks after the first
+  o += al(slice_bytes(p));
+  f.ztmp = o;
+  o += rank_chunks(p.R) > 1 ? al(ndc) : 0;
   f.flags = o;
   o += 256;
   f.total = o;
@@ -117,7 +151,7 @@ FwdLayout fwd_layout(const tdn_problem& p) {
 }
 
 struct BwdLayout {
-  size_t gz, z, xt, part, parts, perm_src, off_src, sort, wp, drho, wrad_part, gv, flags, total;
+  size_t gz, z, xt, part, parts, perm_src, off_src, sort, wp, drho, wrad_part, gv, fsl, gtmp, grtmp, flags, total;
 };
 BwdLayout bwd_layout(const tdn_problem& p) {
   BwdLayout b{};
@@ -141,12 +175,20 @@ BwdLayout bwd_layout(const tdn_problem& p) {
   o += al(tdn::sort_plan(p.n_nodes, p.n_edges).bytes);
   b.wp = o;
   o += al(tdn::node_gemm_ws_bytes(p.C));
+  const int rc = chunk_problem(p, 0).R;  // the largest rank chunk (p.R when not chunked)
   b.drho = o;  // radial-weight gradient: dL/drho per edge, block partials, and a
-  o += al(size_t(p.n_edges) * p.R * 4);  // grad_edge_vec stand-in when only grad_radial_w is asked for
+  o += al(size_t(p.n_edges) * rc * 4);  // grad_edge_vec stand-in when only grad_radial_w is asked for
   b.wrad_part = o;
-  o += al(size_t(tdn::radial_grad_blocks(p.n_edges)) * p.n_radial * p.R * 4);
+  o += al(size_t(tdn::radial_grad_blocks(p.n_edges)) * p.n_radial * rc * 4);
   b.gv = o;
   o += al(size_t(p.n_edges) * 12);
+  const bool chunked = rank_chunks(p.R) > 1;
+  b.fsl = o;  // rank chunks: factor columns, a chunk's grad_x or grad_edge_vec, a chunk's radial gradient
+  o += al(slice_bytes(p));
+  b.gtmp = o;
+  o += chunked ? al(std::max(ndc, size_t(p.n_edges) * 12)) : 0;
+  b.grtmp = o;
+  o += chunked ? al(size_t(p.n_radial) * rc * 4) : 0;
   b.flags = o;
   o += 256;
   b.total = o;
@@ -265,20 +307,57 @@ hipError_t edge_features(const tdn_problem& p, const void* x, bool x_is_f32, voi
   return tdn::launch_feature_layout(p.n_nodes, dim_of(p.L), p.C, x, x_is_f32, 1, xt, nullptr, s);
 }
 
+// The edge pass out[seg] = per-segment EF diag(g) KF^T feat sums over all R
+// ranks: one launch when R <= kChunkR, otherwise one per rank chunk (the
+// chunk's columns of KF, EF, B and radial_w cut into fsl), the chunks after
+// the first written to otmp and added into out in chunk order.  feat must
+// already be laid out (edge_features).
+hipError_t edge_pass_ranks(const tdn_problem& p, const int32_t* offsets, const int32_t* perm, const int32_t* gather,
+                           const int32_t* key, const float* edge_vec, const float* KF, const float* EF,
+                           const float* B, const float* radial_w, const void* feat, float* out, float* partial,
+                           float* fsl, float* otmp, hipStream_t s, bool atomic = false) {
+  const int nch = rank_chunks(p.R);
+  if (nch == 1) {
+    const tdn::EdgeArgs a = edge_args(p, offsets, perm, gather, key, edge_vec, KF, EF, B, radial_w, feat, out, partial);
+    return atomic ? tdn::launch_cp_edge_atomic(a, s) : tdn::launch_cp_edge(a, s);
+  }
+  if (atomic) return hipErrorInvalidValue;
+  const int d = dim_of(p.L);
+  float *sK = fsl, *sE = fsl + size_t(d) * kChunkR, *sB = fsl + size_t(2 * d) * kChunkR;
+  float* sW = fsl + size_t(3 * d) * kChunkR;
+  for (int c = 0; c < nch; ++c) {
+    int r0 = 0, n = 0;
+    chunk_range(p.R, c, nch, &r0, &n);
+    tdn_problem pc = p;
+    pc.R = n;
+    hipError_t e = tdn::launch_slice_cols(d, p.R, r0, n, KF, sK, s);
+    if (e == hipSuccess) e = tdn::launch_slice_cols(d, p.R, r0, n, EF, sE, s);
+    if (e == hipSuccess) e = tdn::launch_slice_cols(d, p.R, r0, n, B, sB, s);
+    if (e == hipSuccess) e = tdn::launch_slice_cols(p.n_radial, p.R, r0, n, radial_w, sW, s);
+    if (e != hipSuccess) return e;
+    float* dst = c == 0 ? out : otmp;
+    const tdn::EdgeArgs a = edge_args(pc, offsets, perm, gather, key, edge_vec, sK, sE, sB, sW, feat, dst, partial);
+    e = tdn::launch_cp_edge(a, s);
+    if (e == hipSuccess && c > 0) e = tdn::launch_accumulate(size_t(p.n_nodes) * d * p.C, otmp, out, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 // The forward edge pass Z = per-node D diag(g) A^T x sums, for either
-// feature dtype (bf16 goes through the transposed copy in the workspace).
+// feature dtype (features laid out into xt first).
 hipError_t forward_edge_pass(const tdn_problem& p, const int32_t* offsets, const int32_t* perm, const int32_t* src,
                              const int32_t* dst, const float* edge_vec, const float* A, const float* B, const float* D,
-                             const float* radial_w, const void* x, void* xt, float* partial, float* Z,
-                             hipStream_t s, bool atomic = false) {
+                             const float* radial_w, const void* x, void* xt, float* partial, float* Z, float* fsl,
+                             float* ztmp, hipStream_t s, bool atomic = false) {
   {
     Timed t("feature_layout", s);
     hipError_t e = edge_features(p, x, p.feat_dtype == TDN_F32, xt, s);
     if (e != hipSuccess) return e;
   }
   Timed t(atomic ? "cp_edge_fwd_atomic" : "cp_edge_fwd", s);
-  const tdn::EdgeArgs a = edge_args(p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, xt, Z, partial);
-  return atomic ? tdn::launch_cp_edge_atomic(a, s) : tdn::launch_cp_edge(a, s);
+  return edge_pass_ranks(p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, xt, Z, partial, fsl, ztmp, s,
+                         atomic);
 }
 
 }  // namespace
@@ -324,7 +403,7 @@ tdn_status forward_impl(const tdn_problem* p, const void* x, const float* edge_v
   tdn_status st = check_problem(p);
   if (st != TDN_OK) return st;
   if (atomic && p->feat_dtype != TDN_F32) return TDN_ERR_BAD_DTYPE;
-  if (atomic && (p->L < 2 || p->L > 4)) return TDN_ERR_BAD_SHAPE;
+  if (atomic && (p->L < 2 || p->L > 4 || p->R > kChunkR)) return TDN_ERR_BAD_SHAPE;
   const int N = p->n_nodes, E = p->n_edges, d = dim_of(p->L), C = p->C;
   if (!A || !B || !D || !W || !radial_w || !offsets || !workspace) return TDN_ERR_NULL_POINTER;
   if (N > 0 && (!x || !out)) return TDN_ERR_NULL_POINTER;
@@ -351,7 +430,8 @@ tdn_status forward_impl(const tdn_problem* p, const void* x, const float* edge_v
   float* Z = z_save ? z_save : reinterpret_cast<float*>(ws + lay.z);
   const bool bf16 = p->feat_dtype == TDN_BF16;
   TDN_HIP(forward_edge_pass(*p, offsets, perm, src, dst, edge_vec, A, B, D, radial_w, x, ws + lay.xt,
-                            reinterpret_cast<float*>(ws + lay.part), Z, stream, atomic));
+                            reinterpret_cast<float*>(ws + lay.part), Z, reinterpret_cast<float*>(ws + lay.fsl),
+                            reinterpret_cast<float*>(ws + lay.ztmp), stream, atomic));
   {
     Timed t("node_gemm", stream);
     TDN_HIP(tdn::launch_node_gemm(N * d, C, Z, W, bf16, 0, out, ws + lay.wp, stream));
@@ -384,7 +464,7 @@ tdn_status tdn_cp_tp3_forward(const tdn_problem* p, const void* x, const float* 
   tdn_status st = check_problem(p);
   if (st != TDN_OK) return st;
   if (p->feat_dtype != TDN_F32) return TDN_ERR_BAD_DTYPE;
-  if (p->L < 2 || p->L > 4) return TDN_ERR_BAD_SHAPE;
+  if (p->L < 2 || p->L > 4 || p->R > kChunkR) return TDN_ERR_BAD_SHAPE;
   const int N = p->n_nodes, E = p->n_edges, d = dim_of(p->L), C = p->C;
   if (!A || !A2 || !B || !D || !W || !radial_w || !offsets || !workspace) return TDN_ERR_NULL_POINTER;
   if (N > 0 && (!x || !out)) return TDN_ERR_NULL_POINTER;
@@ -565,66 +645,100 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
     if (!Z) {
       float* Zw = reinterpret_cast<float*>(ws + lay.z);
       TDN_HIP(forward_edge_pass(*p, offsets, perm, src, dst, edge_vec, A, B, D, radial_w, x, ws + lay.xt,
-                                reinterpret_cast<float*>(ws + lay.part), Zw, stream));
+                                reinterpret_cast<float*>(ws + lay.part), Zw, reinterpret_cast<float*>(ws + lay.fsl),
+                                reinterpret_cast<float*>(ws + lay.gtmp), stream));
       Z = Zw;
     }
     Timed t("gram", stream);
     TDN_HIP(tdn::launch_gram(N * d, C, Z, grad_out, bf16, reinterpret_cast<float*>(ws + lay.parts), grad_W, stream));
   }
+  const int nch = rank_chunks(p->R);
+  float* fsl = reinterpret_cast<float*>(ws + lay.fsl);
+  float *sA = fsl, *sB = fsl + size_t(d) * kChunkR, *sD = fsl + size_t(2 * d) * kChunkR;
+  float* sW = fsl + size_t(3 * d) * kChunkR;
+  float* gtmp = reinterpret_cast<float*>(ws + lay.gtmp);
+  // the factor and radial-weight columns of rank chunk c (the inputs
+  // themselves when the problem is one chunk)
+  auto chunk_inputs = [&](int c, int* r0, int* n, const float** cA, const float** cB, const float** cD,
+                          const float** cW) -> hipError_t {
+    chunk_range(p->R, c, nch, r0, n);
+    if (nch == 1) {
+      *cA = A, *cB = B, *cD = D, *cW = radial_w;
+      return hipSuccess;
+    }
+    hipError_t e = tdn::launch_slice_cols(d, p->R, *r0, *n, A, sA, stream);
+    if (e == hipSuccess) e = tdn::launch_slice_cols(d, p->R, *r0, *n, B, sB, stream);
+    if (e == hipSuccess) e = tdn::launch_slice_cols(d, p->R, *r0, *n, D, sD, stream);
+    if (e == hipSuccess) e = tdn::launch_slice_cols(p->n_radial, p->R, *r0, *n, radial_w, sW, stream);
+    *cA = sA, *cB = sB, *cD = sD, *cW = sW;
+    return e;
+  };
   if ((grad_edge_vec || grad_radial_w) && E > 0) {
-    tdn::BwdDstArgs a{};
-    a.n_seg = N;
-    a.E = E;
-    a.L = p->L;
-    a.d = d;
-    a.C = C;
-    a.R = p->R;
-    a.n_radial = p->n_radial;
-    a.sigma = p->r_cut / float(p->n_radial - 1);
-    a.offsets = offsets;
-    a.perm = perm;
-    a.src = src;
-    a.edge_vec = edge_vec;
-    a.A = A;
-    a.Bf = B;
-    a.D = D;
-    a.radial_w = radial_w;
-    a.x = x;
-    a.Gz = Gz;
-    a.grad_vec = grad_edge_vec ? grad_edge_vec : reinterpret_cast<float*>(ws + lay.gv);
-    a.drho = grad_radial_w ? reinterpret_cast<float*>(ws + lay.drho) : nullptr;
-    a.dst = dst;
-    const tdn::EdgePlan dp = tdn::bwd_dst_plan(p->L, p->R, C, p->n_radial, bf16, E);
-    a.n_range = dp.n_range;
-    a.pieces_per_block = dp.per_block;
-    if (a.n_range > 0) {
-      // x in parts (fp16 with row scales for fp32 problems, bf16), blocked as
-      // MFMA operands for the contraction over channels (the region is free
-      // until the grad_x pass lays out Gz there)
-      float* xscale = reinterpret_cast<float*>(ws + lay.xt + al(xc_bytes(*p)));
-      Timed t("channel_layout", stream);
-      TDN_HIP(tdn::launch_direct_layout(N, d, C, tdn::bwd_dst_cpad(C, bf16), x, !bf16, feature_parts(*p), ws + lay.xt,
-                                        bf16 ? nullptr : xscale, false, stream));
-      a.xc = ws + lay.xt;
-      a.x_scale = bf16 ? nullptr : xscale;
-    } else if (d > 32) {
-      // x in the direct kernel's operand blocks, channels in its accumulator
-      // order
-      float* xscale = reinterpret_cast<float*>(ws + lay.xt + al(xd_bytes(*p)));
-      Timed t("channel_layout", stream);
-      TDN_HIP(tdn::launch_direct_layout(N, d, C, tdn::bwd_direct_cpad(C), x, !bf16, feature_parts(*p), ws + lay.xt,
-                                        bf16 ? nullptr : xscale, true, stream));
-      a.xc = ws + lay.xt;
-      a.x_scale = bf16 ? nullptr : xscale;
-    }
-    {
-      Timed t("cp_bwd_dst", stream);
-      TDN_HIP(tdn::launch_bwd_dst(a, bf16, stream));
-    }
-    if (grad_radial_w) {
-      Timed t("radial_grad", stream);
-      TDN_HIP(tdn::launch_radial_grad(E, p->R, p->n_radial, a.sigma, edge_vec, a.drho,
-                                      reinterpret_cast<float*>(ws + lay.wrad_part), grad_radial_w, stream));
+    // dL/dr_e and dL/drho are sums over ranks: per rank chunk, the edge
+    // gradients go to the output (first chunk) or to gtmp and are added in
+    // chunk order; the radial-weight gradient of the chunk fills its columns
+    float* gv_out = grad_edge_vec ? grad_edge_vec : reinterpret_cast<float*>(ws + lay.gv);
+    for (int c = 0; c < nch; ++c) {
+      int r0 = 0, n = 0;
+      const float *cA, *cB, *cD, *cW;
+      TDN_HIP(chunk_inputs(c, &r0, &n, &cA, &cB, &cD, &cW));
+      tdn::BwdDstArgs a{};
+      a.n_seg = N;
+      a.E = E;
+      a.L = p->L;
+      a.d = d;
+      a.C = C;
+      a.R = n;
+      a.n_radial = p->n_radial;
+      a.sigma = p->r_cut / float(p->n_radial - 1);
+      a.offsets = offsets;
+      a.perm = perm;
+      a.src = src;
+      a.edge_vec = edge_vec;
+      a.A = cA;
+      a.Bf = cB;
+      a.D = cD;
+      a.radial_w = cW;
+      a.x = x;
+      a.Gz = Gz;
+      a.grad_vec = c == 0 ? gv_out : gtmp;
+      a.drho = grad_radial_w ? reinterpret_cast<float*>(ws + lay.drho) : nullptr;
+      a.dst = dst;
+      const tdn::EdgePlan dp = tdn::bwd_dst_plan(p->L, n, C, p->n_radial, bf16, E);
+      a.n_range = dp.n_range;
+      a.pieces_per_block = dp.per_block;
+      if (a.n_range > 0) {
+        // x in parts (fp16 with row scales for fp32 problems, bf16), blocked as
+        // MFMA operands for the contraction over channels (the region is free
+        // until the grad_x pass lays out Gz there)
+        float* xscale = reinterpret_cast<float*>(ws + lay.xt + al(xc_bytes(*p)));
+        Timed t("channel_layout", stream);
+        TDN_HIP(tdn::launch_direct_layout(N, d, C, tdn::bwd_dst_cpad(C, bf16), x, !bf16, feature_parts(*p),
+                                          ws + lay.xt, bf16 ? nullptr : xscale, false, stream));
+        a.xc = ws + lay.xt;
+        a.x_scale = bf16 ? nullptr : xscale;
+      } else if (d > 32) {
+        // x in the direct kernel's operand blocks, channels in its accumulator
+        // order
+        float* xscale = reinterpret_cast<float*>(ws + lay.xt + al(xd_bytes(*p)));
+        Timed t("channel_layout", stream);
+        TDN_HIP(tdn::launch_direct_layout(N, d, C, tdn::bwd_direct_cpad(C), x, !bf16, feature_parts(*p),
+                                          ws + lay.xt, bf16 ? nullptr : xscale, true, stream));
+        a.xc = ws + lay.xt;
+        a.x_scale = bf16 ? nullptr : xscale;
+      }
+      {
+        Timed t("cp_bwd_dst", stream);
+        TDN_HIP(tdn::launch_bwd_dst(a, bf16, stream));
+        if (c > 0) TDN_HIP(tdn::launch_accumulate(size_t(E) * 3, gtmp, gv_out, stream));
+      }
+      if (grad_radial_w) {
+        Timed t("radial_grad", stream);
+        float* gr = nch == 1 ? grad_radial_w : reinterpret_cast<float*>(ws + lay.grtmp);
+        TDN_HIP(tdn::launch_radial_grad(E, n, p->n_radial, a.sigma, edge_vec, a.drho,
+                                        reinterpret_cast<float*>(ws + lay.wrad_part), gr, stream));
+        if (nch > 1) TDN_HIP(tdn::launch_scatter_cols(p->n_radial, p->R, r0, n, gr, grad_radial_w, stream));
+      }
     }
   }
   if (grad_x) {
@@ -641,9 +755,8 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
       TDN_HIP(edge_features(*p, Gz, true, ws + lay.xt, stream));
     }
     Timed t("cp_edge_bwd_src", stream);
-    TDN_HIP(tdn::launch_cp_edge(edge_args(*p, off_src, perm_src, dst, src, edge_vec, D, A, B, radial_w, ws + lay.xt,
-                                          grad_x, reinterpret_cast<float*>(ws + lay.part)),
-                                stream));
+    TDN_HIP(edge_pass_ranks(*p, off_src, perm_src, dst, src, edge_vec, D, A, B, radial_w, ws + lay.xt, grad_x,
+                            reinterpret_cast<float*>(ws + lay.part), fsl, gtmp, stream));
   }
   return TDN_OK;
 }

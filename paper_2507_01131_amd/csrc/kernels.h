@@ -203,6 +203,13 @@ __host__ __device__ inline int bwd_direct_cpad(int C) { return C <= 64 ? 64 : (C
 hipError_t launch_bwd_dst(const BwdDstArgs& a, bool x_bf16, hipStream_t s);
 
 // ---------------------------------------------------------------- misc
+// Rank chunks (ranks above 256, split into column ranges):
+// dst[row][j] = src[row][r0 + j] for a row-major [rows, R] src and [rows, n] dst
+hipError_t launch_slice_cols(int rows, int R, int r0, int n, const float* src, float* dst, hipStream_t s);
+// dst[row][r0 + j] = src[row][j]
+hipError_t launch_scatter_cols(int rows, int R, int r0, int n, const float* src, float* dst, hipStream_t s);
+// dst[i] += src[i], i < n
+hipError_t launch_accumulate(size_t n, const float* src, float* dst, hipStream_t s);
 // Compute units of the current device (cached per device).
 int device_cus();
 hipError_t launch_sh(int L, int E, const float* edge_vec, float* Y, float* dY, hipStream_t s);

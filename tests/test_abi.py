@@ -56,7 +56,7 @@ def _bwd(p, ws_bytes=1 << 40, **override):
 
 @pytest.mark.parametrize("kw,status", [
     (dict(L=7), 2), (dict(L=-1), 2), (dict(C=8), 2), (dict(C=100), 2), (dict(C=512), 2), (dict(R=0), 2),
-    (dict(R=257), 2), (dict(n_nodes=-1), 2), (dict(n_edges=-5), 2), (dict(n_nodes=0, n_edges=3), 2),
+    (dict(R=4097), 2), (dict(n_nodes=-1), 2), (dict(n_edges=-5), 2), (dict(n_nodes=0, n_edges=3), 2),
     (dict(n_radial=1), 2), (dict(r_cut=0.0), 2), (dict(r_cut=float("nan")), 2), (dict(feat_dtype=7), 3),
 ])
 def test_bad_problem_is_rejected(kw, status):

@@ -232,8 +232,9 @@ def test_repeat_calls_are_bitwise_identical():
 
 
 # ------------------------------------------------------------ exact cases (no fitted factors)
-@pytest.mark.parametrize("L", [1, 2, 3])
+@pytest.mark.parametrize("L", [1, 2, 3, 4])
 def test_exact_factors_give_dense_cg_layer_and_equivariance(L):
+    # L = 4: the Thm. 2 construction has R = d^2 = 625 ranks, three rank chunks
     M = cg_tensor.cg_tensor(L)
     D, A, B = (a.astype(np.float32) for a in cp.universality_factors(M))
     R = D.shape[1]
@@ -259,6 +260,33 @@ def test_exact_factors_give_dense_cg_layer_and_equivariance(L):
     w2["x"] = np.einsum("ab,nbc->nac", Drot, w["x"].astype(np.float64)).astype(np.float32)
     out2 = _fwd(w2, A, B, D).out.cpu().numpy()
     assert rel_err(out2, np.einsum("ab,nbc->nac", Drot, out)) < 1e-5
+
+
+# ------------------------------------------------------------ ranks above 256 (rank chunks)
+@pytest.mark.parametrize("L,C,R,sort", [(3, 32, 300, False), (2, 48, 600, True), (4, 64, 257, False)])
+def test_rank_chunks_forward_and_backward(L, C, R, sort):
+    w = workloads.random_graph(60 + L, n_nodes=30, n_edges=500, L=L, C=C, R=R, sort=sort)
+    A, B, D = random_factors(L, R, 60 + L)
+    res = _fwd(w, A, B, D)
+    G = torch.from_numpy(w["grad_out"]).cuda()
+    gx, gW, gv, gr = tdn.backward(res, G, need_radial=True)
+    gx2, gW2, gv2 = tdn.backward(res, G, use_saved_z=False)
+    torch.cuda.synchronize()
+    args = (w["x"], w["edge_index"], w["edge_vec"], A, B, D, w["W"], w["radial_w"], w["r_cut"], w["L"])
+    ref, zref = layer.forward(*args, return_z=True)
+    rx, rW, rv, rr = layer.backward(*args, w["grad_out"], return_radial=True)
+    assert rel_err(res.out.cpu(), ref) < TOL_F32
+    check_rows(res.out.cpu(), ref, TOL_F32, "out")
+    check_rows(res.z.cpu(), zref, TOL_F32, "z")
+    check_rows(gx.cpu(), rx, TOL_F32, "grad_x")
+    check_scaled(gv.cpu(), rv, grad_vec_scale(w, A, B, D), TOL_F32, "grad_edge_vec")
+    assert rel_err(gv.cpu(), rv) < TOL_F32
+    assert rel_err(gW.cpu(), rW) < TOL_F32 and rel_err(gr.cpu(), rr) < TOL_F32
+    check_elementwise(gr.cpu(), rr, TOL_F32, "grad_radial_w")
+    assert torch.equal(gx, gx2) and torch.equal(gv, gv2) and rel_err(gW2.cpu(), rW) < TOL_F32
+    # fixed chunk order: repeat calls give the same bits
+    res2 = _fwd(w, A, B, D)
+    assert torch.equal(res.out, res2.out)
 
 
 # ------------------------------------------------------------ edge cases
