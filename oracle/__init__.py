@@ -21,7 +21,9 @@ Modules
             backward (Sec. 3.1 eq. approximate, Sec. 3.2)
   dense_layer
             the exact CG tensor-product layer path by path, the comparator
-            of the CP layer (Sec. 2 eq. clebsch_gordan, Sec. 3.2)
+            of the CP layer (Sec. 2 eq. clebsch_gordan, Sec. 3.2), with the
+            shared channel weight or with one channel weight per path (the
+            product without path-weight sharing)
   radius_graph
             the edges the layer consumes: every atom pair of a system (and
             its periodic images) closer than the cutoff, with an optional

@@ -22,6 +22,17 @@ too).  For every edge e = (s, t):
 The path list is cg_tensor.paths(L) in its order (the index p of Wpath);
 the CG blocks are cg.cg_real, the same real-basis blocks that build M.
 Float64 throughout.
+
+``forward_unshared`` is the product without path-weight sharing (the fully
+connected CG tensor product of Sec. 3.2, whose O(L^3) paths each carry a
+distinct multiplicity-space weight): per edge and path the degree-l3 block
+rho_e[p] CG_p(x[s], Y_e) is multiplied by that path's own channel matrix
+W_p [C_in, C_out] before the paths are summed,
+
+    m_e^(l3) = sum over paths p = (l1, l2, l3) of
+               (rho_e[p] * sum_{m1, m2} C[l3 m3; l1 m1, l2 m2] x[s]^(l1)_m1 Y_e^(l2)_m2) W_p,
+
+so that W_p = W for every p is the shared product above.
 """
 from __future__ import annotations
 
@@ -62,6 +73,39 @@ def forward(x, edge_index, edge_vec, W, path_w, r_cut, L, perm=None, return_z=Fa
     np.add.at(Z, dst[perm], z)                                        # in sorted order
     out = Z @ W
     return (out, Z) if return_z else out
+
+
+def forward_unshared(x, edge_index, edge_vec, W_paths, path_w, r_cut, L, perm=None):
+    """out [N, d, C] of the product with one channel matrix per path,
+    W_paths [P, C_in, C_out], applied to each edge's path block before the
+    paths and the edges are summed (in sorted-edge order)."""
+    x = np.asarray(x, np.float64)
+    W_paths = np.asarray(W_paths, np.float64)
+    path_w = np.asarray(path_w, np.float64)
+    N, d, C = x.shape
+    plist = paths(L)
+    assert path_w.shape[1] == len(plist) and W_paths.shape[0] == len(plist)
+    src = np.asarray(edge_index[0], np.int64)
+    dst = np.asarray(edge_index[1], np.int64)
+    if perm is None:
+        perm, _ = stable_sort_by_key(dst, N)
+    perm = np.asarray(perm, np.int64)
+    vec = np.asarray(edge_vec, np.float64)[perm]
+    Y = spherical_harmonics(L, vec)
+    phi, _ = radial_basis(np.linalg.norm(vec, axis=1), r_cut, path_w.shape[0])
+    rho = phi @ path_w
+    xs = x[src[perm]]
+    m = np.zeros((perm.shape[0], d, W_paths.shape[2]))
+    for p, (l1, l2, l3) in enumerate(plist):
+        blk = cg_real(l1, l2, l3)
+        a = slice(l1 * l1, (l1 + 1) ** 2)
+        b = slice(l2 * l2, (l2 + 1) ** 2)
+        o = slice(l3 * l3, (l3 + 1) ** 2)
+        zp = rho[:, p, None, None] * np.einsum("kij,eic,ej->ekc", blk, xs[:, a, :], Y[:, b])
+        m[:, o, :] += zp @ W_paths[p]
+    out = np.zeros((N, d, W_paths.shape[2]))
+    np.add.at(out, dst[perm], m)                                      # in sorted order
+    return out
 
 
 def exact_cp_factors(L):
