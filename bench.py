@@ -38,6 +38,10 @@ weight, and reports the CP edge pass's speed-up over it (edge kernel against
 edge kernel, whole forward against whole forward, eager launches).  Its
 algorithmic flops per launch are E (3 nnz(C) + 2 d^2 C): the per-edge matrix
 K_e = C x2 (Y_e rho_e) and its product with the gathered features.
+Its "unshared" object times tdn_dense_tp_forward_unshared, the exact
+product without path-weight sharing (one channel matrix per path, the fully
+connected product of Sec. 3.2): per-path edge sums (dense_edge_unshared) and
+the per-path channel GEMMs (path_gemm), C <= 128.
 --comparator-sweep adds the same comparison for L = 1..6 on the headline
 graph (C = 128, R = 32 ceil(7 L^2 / 32) capped at 256, random factors):
 the analogue of the paper's speed-up-against-degree figure (Sec. 4.5).
@@ -138,6 +142,35 @@ def exact_comparator(torch, tdn, L, x, vec, ei, W, r_cut, presorted, steps, n_ra
     flops = E * (3 * nnz + 2 * d * d * C)
     return {"edge_kernel_ms": k_ms, "forward_ms": f_ms, "paths": tab.n_path, "cg_nnz": nnz,
             "flops_per_launch": flops, "achieved_tflops": flops / (k_ms * 1e-3) / 1e12}
+
+
+def unshared_comparator(torch, tdn, L, x, vec, ei, r_cut, presorted, steps, n_radial, seed=0):
+    """Times tdn_dense_tp_forward_unshared (one seeded channel matrix per
+    path) on these inputs: the per-path edge sums and the path GEMM."""
+    zc = np.load(os.path.join(CG_TABLES, f"cg_L{L}.npz"))
+    tab = tdn.cg_table(zc["M"], zc["path"], x.device)
+    rng = np.random.default_rng(seed)
+    N, d, C = x.shape
+    E = vec.shape[0]
+    P = tab.n_path
+    pw = torch.from_numpy((rng.standard_normal((n_radial, P)) / np.sqrt(n_radial)).astype(np.float32)).to(x.device)
+    Wp = torch.from_numpy((rng.standard_normal((P, C, C)) / np.sqrt(C)).astype(np.float32)).to(x.device)
+    out = torch.empty((N, d, C), dtype=torch.float32, device=x.device)
+    perm = torch.empty(E, dtype=torch.int32, device=x.device)
+    off = torch.empty(N + 1, dtype=torch.int32, device=x.device)
+    ws = torch.empty(tdn.dense_unshared_workspace_size(tdn.make_problem(L, C, P, N, E, r_cut, n_radial)),
+                     dtype=torch.uint8, device=x.device)
+
+    def call():
+        return tdn.dense_forward_unshared(x, vec, ei, tab, pw, Wp, r_cut=r_cut, edges_sorted=presorted,
+                                          workspace=ws, out=out, perm=perm, offsets=off)
+
+    k_ms, f_ms = time_calls(call, torch, tdn, "dense_edge_unshared", steps)
+    g_ms, _ = time_calls(call, torch, tdn, "path_gemm", max(1, steps // 4))
+    rows = sum(2 * l3 + 1 for l1 in range(L + 1) for l2 in range(L + 1)
+               for l3 in range(abs(l1 - l2), min(l1 + l2, L) + 1))
+    del Wp, ws
+    return {"edge_kernel_ms": k_ms, "path_gemm_ms": g_ms, "forward_ms": f_ms, "paths": P, "path_rows": rows}
 
 
 def cpu_model():
@@ -388,6 +421,12 @@ def main():
                      "cp_forward_speedup": cmp_["forward_ms"] / cp_fwd_ms,
                      "frac_of_fp32_mfma_peak": cmp_["achieved_tflops"] / PEAK_FP32_MFMA_TFLOPS,
                      "launch": "eager"})
+        if C <= 128:
+            un = unshared_comparator(torch, tdn, w["L"], x, vec, ei, w["r_cut"], w["presorted"], args.steps,
+                                     w["n_radial"])
+            un.update({"kernel": "dense_edge_unshared", "cp_forward_speedup": un["forward_ms"] / cp_fwd_ms,
+                       "cp_edge_kernel_speedup": un["edge_kernel_ms"] / edge_ms, "launch": "eager"})
+            cmp_["unshared"] = un
         line["exact_cg_comparator"] = cmp_
     if args.comparator_sweep and not bf16:
         rng = np.random.default_rng(1)
@@ -407,11 +446,15 @@ def main():
 
             ck, cf = time_calls(cp_call, torch, tdn, "cp_edge_fwd", 20)
             ex = exact_comparator(torch, tdn, Ls, xs_, vec, ei, Ws, w["r_cut"], w["presorted"], 20, w["n_radial"])
+            un = unshared_comparator(torch, tdn, Ls, xs_, vec, ei, w["r_cut"], w["presorted"], 5, w["n_radial"])
             sweep.append({"L": Ls, "d": ds, "C": Cs, "R": Rs, "paths": ex["paths"], "cg_nnz": ex["cg_nnz"],
                           "cp_edge_kernel_ms": ck, "exact_edge_kernel_ms": ex["edge_kernel_ms"],
                           "cp_forward_ms": cf, "exact_forward_ms": ex["forward_ms"],
                           "cp_edge_kernel_speedup": ex["edge_kernel_ms"] / ck,
-                          "cp_forward_speedup": ex["forward_ms"] / cf})
+                          "cp_forward_speedup": ex["forward_ms"] / cf,
+                          "unshared_edge_kernel_ms": un["edge_kernel_ms"], "unshared_path_gemm_ms": un["path_gemm_ms"],
+                          "unshared_forward_ms": un["forward_ms"],
+                          "cp_forward_speedup_vs_unshared": un["forward_ms"] / cf})
             del xs_, Ws, fac, rws
         line["comparator_sweep"] = sweep
     if args.three_input and not bf16:

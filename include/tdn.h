@@ -196,6 +196,29 @@ tdn_status tdn_dense_tp_forward(const tdn_problem* p, const void* x, const float
                                 float* out, float* z_save, int32_t* perm, int32_t* offsets, void* workspace,
                                 size_t workspace_bytes, hipStream_t stream);
 
+/* The exact CG tensor product without path-weight sharing (the fully
+ * connected product of Sec. 3.2: every path carries its own channel matrix,
+ * applied to the path's block before the paths are summed):
+ *   out[n]^(l3) = sum over edges e into n, paths p = (l1, l2, l3) of
+ *                 rho_e[p] (C_p (x[src_e]^(l1) (x) Y_e^(l2))) W_paths[p],
+ *   rho_e = phi_e path_w.
+ * Since W_paths[p] acts on channels only, the kernel first sums each path's
+ * block over a node's edges (N x (sum over paths of 2 l3 + 1) x C in the
+ * workspace) and then applies the matrices per node.  Arguments as
+ * tdn_dense_tp_forward, except:
+ *   W_paths [R, C, C] f32   the channel matrix of each path, [in][out], paths
+ *                           in the order l1, then l2, then l3 ascending
+ * and no z_save.  fp32 features (TDN_ERR_BAD_DTYPE) and C <= 128
+ * (TDN_ERR_BAD_SHAPE).  The path of an entry is its degree triple (deg i,
+ * deg j, deg k); the table's path field is not read.  The workspace size is
+ * tdn_dense_tp_unshared_workspace_size's.  Deterministic. */
+tdn_status tdn_dense_tp_unshared_workspace_size(const tdn_problem* p, size_t* bytes);
+tdn_status tdn_dense_tp_forward_unshared(const tdn_problem* p, const void* x, const float* edge_vec,
+                                         const int32_t* edge_index, const int32_t* cg_row, const int32_t* cg_col,
+                                         const float* cg_val, int32_t cg_nnz, const float* path_w,
+                                         const float* W_paths, float* out, int32_t* perm, int32_t* offsets,
+                                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Backward pass for the scalar <grad_out, out>.  perm and offsets are the
  * forward's outputs; z_save is the forward's saved Z or NULL (then Z is
  * recomputed).  Each gradient pointer may be NULL to skip it; grads are f32
@@ -299,7 +322,8 @@ tdn_status tdn_spherical_harmonics(int32_t L, int32_t E, const float* edge_vec, 
  * tdn_timer_enable(1) starts recording every launch of the layer's edge
  * kernels; tdn_timer_read synchronises on the recorded events and returns
  * the summed milliseconds and launch count of the kernel named `kernel`
- * ("cp_edge_fwd", "cp_edge_fwd_atomic", "cp_edge_fwd_t3", "dense_edge_fwd", "radius_graph", "feature_layout",
+ * ("cp_edge_fwd", "cp_edge_fwd_atomic", "cp_edge_fwd_t3", "dense_edge_fwd", "dense_edge_unshared",
+ * "path_gemm", "radius_graph", "feature_layout",
  * "channel_layout", "cp_edge_bwd_src", "cp_bwd_dst", "radial_grad", "node_gemm", "gram",
  * "sort");
  * reset = 1 clears that kernel's record. */

@@ -75,6 +75,8 @@ def lib() -> ctypes.CDLL:
         L.tdn_ps_linear.argtypes = [ctypes.c_int32] * 3 + [_P, _P, ctypes.c_int32, _P, _P, _SZ, _P]
         L.tdn_cp_tp3_forward.argtypes = [PP] + [_P] * 14 + [_SZ, _P]
         L.tdn_dense_tp_forward.argtypes = [PP] + [_P] * 6 + [ctypes.c_int32] + [_P] * 7 + [_SZ, _P]
+        L.tdn_dense_tp_unshared_workspace_size.argtypes = [PP, ctypes.POINTER(_SZ)]
+        L.tdn_dense_tp_forward_unshared.argtypes = [PP] + [_P] * 6 + [ctypes.c_int32] + [_P] * 6 + [_SZ, _P]
         GP = ctypes.POINTER(GraphProblem)
         L.tdn_radius_graph_workspace_size.argtypes = [GP, ctypes.POINTER(_SZ)]
         L.tdn_radius_graph.argtypes = [GP, _P, _P, _P, ctypes.c_int64, _P, _P, _P, _P,
@@ -92,7 +94,8 @@ def lib() -> ctypes.CDLL:
                   "tdn_cp_tp_forward_noalloc",
                   "tdn_sort_workspace_size", "tdn_sort_by_key", "tdn_spherical_harmonics", "tdn_timer_enable",
                   "tdn_timer_read", "tdn_radius_graph_workspace_size", "tdn_radius_graph", "tdn_dense_tp_forward",
-                  "tdn_cp_tp3_forward", "tdn_ps_linear_workspace_size", "tdn_ps_linear"):
+                  "tdn_cp_tp3_forward", "tdn_ps_linear_workspace_size", "tdn_ps_linear",
+                  "tdn_dense_tp_unshared_workspace_size", "tdn_dense_tp_forward_unshared"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -383,6 +386,60 @@ def dense_forward(x, edge_vec, edge_index, table: CGTable, path_w, W, *, r_cut: 
     _check(st, "tdn_dense_tp_forward")
     return ForwardResult(out, z, perm, offsets, p, dict(x=x, edge_vec=edge_vec, edge_index=edge_index, W=W,
                                                         path_w=path_w))
+
+
+def dense_unshared_workspace_size(p: Problem) -> int:
+    """Workspace bytes of tdn_dense_tp_forward_unshared for this problem."""
+    nbytes = _SZ(0)
+    _check(lib().tdn_dense_tp_unshared_workspace_size(ctypes.byref(p), ctypes.byref(nbytes)),
+           "tdn_dense_tp_unshared_workspace_size")
+    return nbytes.value
+
+
+def dense_forward_unshared(x, edge_vec, edge_index, table: CGTable, path_w, W_paths, *, r_cut: float,
+                           edges_sorted=False, validate=False, workspace=None, out=None, perm=None, offsets=None,
+                           stream=None) -> ForwardResult:
+    """Runs tdn_dense_tp_forward_unshared, the exact CG tensor product with one
+    channel matrix per path (float32 features, C <= 128).  W_paths
+    [n_path, C, C] float32 ([in][out] per path); the other arguments as in
+    dense_forward()."""
+    dev = x.device
+    N, d, C = x.shape
+    E = edge_vec.shape[0]
+    L = table.L
+    P = path_w.shape[1]
+    if edge_index.dtype != torch.int32:
+        edge_index = edge_index.to(torch.int32)
+    edge_index = edge_index.contiguous()
+    for t, n, dt, sh in [(x, "x", torch.float32, (N, (L + 1) ** 2, C)), (edge_vec, "edge_vec", torch.float32, (E, 3)),
+                         (edge_index, "edge_index", torch.int32, (2, E)),
+                         (W_paths, "W_paths", torch.float32, (P, C, C)),
+                         (path_w, "path_w", torch.float32, (path_w.shape[0], P)),
+                         (table.row, "table.row", torch.int32, (d * d + 1,)),
+                         (table.col, "table.col", torch.int32, (table.col.shape[0],)),
+                         (table.val, "table.val", torch.float32, (table.col.shape[0],))]:
+        _need(t, n, dt, sh, dev)
+    p = make_problem(L, C, P, N, E, r_cut, path_w.shape[0], TDN_F32, edges_sorted, validate)
+    nbytes = dense_unshared_workspace_size(p)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    if out is None:
+        out = torch.empty((N, d, C), dtype=torch.float32, device=dev)
+    if perm is None:
+        perm = torch.empty(max(E, 1), dtype=torch.int32, device=dev)[:E]
+    if offsets is None:
+        offsets = torch.empty(N + 1, dtype=torch.int32, device=dev)
+    _need(out, "out", torch.float32, (N, d, C), dev)
+    _need(perm, "perm", torch.int32, (E,), dev)
+    _need(offsets, "offsets", torch.int32, (N + 1,), dev)
+    st = lib().tdn_dense_tp_forward_unshared(ctypes.byref(p), _ptr(x), _ptr(edge_vec), _ptr(edge_index),
+                                             _ptr(table.row), _ptr(table.col), _ptr(table.val),
+                                             int(table.col.shape[0]), _ptr(path_w), _ptr(W_paths), _ptr(out),
+                                             _ptr(perm), _ptr(offsets), _ptr(workspace), workspace.numel(),
+                                             _stream(stream))
+    _check(st, "tdn_dense_tp_forward_unshared")
+    return ForwardResult(out, None, perm, offsets, p, dict(x=x, edge_vec=edge_vec, edge_index=edge_index,
+                                                           W_paths=W_paths, path_w=path_w))
 
 
 def backward(res: ForwardResult, grad_out, *, need_x=True, need_W=True, need_vec=True, need_radial=False,

@@ -604,6 +604,96 @@ tdn_status tdn_dense_tp_forward(const tdn_problem* p, const void* x, const float
   return TDN_OK;
 }
 
+namespace {
+size_t unshared_zp_bytes(const tdn_problem& p) {
+  return size_t(p.n_nodes) * tdn::path_rows(p.L).n_rows * p.C * 4;
+}
+tdn_status check_unshared(const tdn_problem* p) {
+  const tdn_status st = check_problem(p);
+  if (st != TDN_OK) return st;
+  if (p->feat_dtype != TDN_F32) return TDN_ERR_BAD_DTYPE;
+  if (p->R != tdn::dense_path_count(p->L) || p->C > 128) return TDN_ERR_BAD_SHAPE;
+  return TDN_OK;
+}
+}  // namespace
+
+tdn_status tdn_dense_tp_unshared_workspace_size(const tdn_problem* p, size_t* bytes) {
+  const tdn_status st = check_unshared(p);
+  if (st != TDN_OK) return st;
+  if (!bytes) return TDN_ERR_NULL_POINTER;
+  *bytes = fwd_layout(*p).total + al(unshared_zp_bytes(*p));
+  return TDN_OK;
+}
+
+tdn_status tdn_dense_tp_forward_unshared(const tdn_problem* p, const void* x, const float* edge_vec,
+                                         const int32_t* edge_index, const int32_t* cg_row, const int32_t* cg_col,
+                                         const float* cg_val, int32_t cg_nnz, const float* path_w,
+                                         const float* W_paths, float* out, int32_t* perm, int32_t* offsets,
+                                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  tdn_status st = check_unshared(p);
+  if (st != TDN_OK) return st;
+  if (cg_nnz < 0) return TDN_ERR_BAD_SHAPE;
+  const int N = p->n_nodes, E = p->n_edges, d = dim_of(p->L), C = p->C;
+  if (!cg_row || (cg_nnz > 0 && (!cg_col || !cg_val)) || !path_w || !W_paths || !offsets || !workspace)
+    return TDN_ERR_NULL_POINTER;
+  if (N > 0 && (!x || !out)) return TDN_ERR_NULL_POINTER;
+  if (E > 0 && (!edge_vec || !edge_index || !perm)) return TDN_ERR_NULL_POINTER;
+  const FwdLayout lay = fwd_layout(*p);
+  if (workspace_bytes < lay.total + al(unshared_zp_bytes(*p))) return TDN_ERR_WORKSPACE_TOO_SMALL;
+  st = check_device();
+  if (st != TDN_OK) return st;
+  char* ws = static_cast<char*>(workspace);
+  if (p->validate) {
+    st = run_validation(*p, edge_index, edge_vec, ws, lay.flags, p->edges_sorted, stream);
+    if (st != TDN_OK) return st;
+  }
+  const int32_t* src = edge_index;
+  const int32_t* dst = E > 0 ? edge_index + E : nullptr;
+  {
+    Timed t("sort", stream);
+    if (p->edges_sorted || E == 0)
+      TDN_HIP(tdn::launch_offsets_presorted(N, E, dst, perm, offsets, stream));
+    else
+      TDN_HIP(tdn::launch_sort(tdn::sort_plan(N, E), dst, 1, perm, offsets, ws + lay.sort, stream));
+  }
+  if (N == 0) return TDN_OK;
+  float* zp = reinterpret_cast<float*>(ws + lay.total);
+  void* xt = ws + lay.xt;
+  {
+    Timed t("feature_layout", stream);
+    TDN_HIP(tdn::launch_feature_layout(N, d, C, x, true, 2, xt, row_scales(*p, xt), stream));
+  }
+  {
+    Timed t("dense_edge_unshared", stream);
+    tdn::DenseArgs a{};
+    a.N = N;
+    a.E = E;
+    a.L = p->L;
+    a.d = d;
+    a.C = C;
+    a.n_radial = p->n_radial;
+    a.n_path = p->R;
+    a.cg_nnz = cg_nnz;
+    a.sigma = p->r_cut / float(p->n_radial - 1);
+    a.offsets = offsets;
+    a.perm = perm;
+    a.src = src;
+    a.edge_vec = edge_vec;
+    a.cg_row = cg_row;
+    a.cg_col = cg_col;
+    a.cg_val = cg_val;
+    a.path_w = path_w;
+    a.feat = xt;
+    a.row_scale = row_scales(*p, xt);
+    TDN_HIP(tdn::launch_dense_edge_unshared(a, zp, stream));
+  }
+  {
+    Timed t("path_gemm", stream);
+    TDN_HIP(tdn::launch_path_gemm(N, p->L, C, zp, W_paths, out, stream));
+  }
+  return TDN_OK;
+}
+
 tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* edge_vec, const int32_t* edge_index,
                               const float* A, const float* B, const float* D, const void* W, const float* radial_w,
                               const int32_t* perm, const int32_t* offsets, const float* z_save,

@@ -21,6 +21,14 @@
 // The node's d x C sum is stored once.  Work per edge: nnz(C) multiply-adds
 // for K_e (independent of C) and 2 d^2 C flops of contraction (d padded to
 // 32 or 64).
+//
+// UN (the product without path-weight sharing): the output rows are the
+// paths' own blocks, row[p] + m3 over all paths (PathRows), so that each
+// path's channel matrix can be applied afterwards (launch_path_gemm).  K_e
+// then has those rows; a launch covers a chunk of dense_un_rows of them (the
+// kernel runs once per chunk), and a coefficient entry (k, i, j) goes to row
+// row[p] + m3(k) of the chunk, p the path (deg i, deg j, deg k) in the order
+// l1, l2, l3 (each ascending); the table's own path field is not used.
 #include "common.hpp"
 #include "kernels.h"
 #include "sh_device.hpp"
@@ -48,15 +56,24 @@ __host__ __device__ constexpr int dense_ks(int d) { return dense_kc(d) + 4; }
 // cost occupancy and was slower)
 __host__ __device__ constexpr int dense_eb(int d) { return d <= 9 ? 8 : (d <= 16 ? 16 : (d <= 32 ? 8 : 4)); }
 
+// UN: output row tiles per launch (the 1, 11, 51 and 156 path rows of
+// L = 0..3 in one launch; 8 at L = 4, 4 at d = 36 and 49, where the operand
+// blocks are twice as large and 8 tiles spill) and edges per batch
+__host__ __device__ constexpr int dense_un_tiles(int d) {
+  return d == 1 || d == 4 ? 1 : (d == 9 ? 2 : (d == 16 ? 5 : (d <= 32 ? 8 : 4)));
+}
+__host__ __device__ constexpr int dense_un_rows(int d) { return dense_un_tiles(d) * kTile; }
+__host__ __device__ constexpr int dense_eb_un(int) { return 2; }
+
 struct DenseSmem {
   int off_k, off_y, off_phi, off_rho, off_row, off_sc, off_ksc, off_max, floats;
 };
-__host__ __device__ inline DenseSmem dense_smem(int d, int n_path) {
-  const int eb = dense_eb(d);
+__host__ __device__ inline DenseSmem dense_smem(int d, int n_path, bool un = false) {
+  const int eb = un ? dense_eb_un(d) : dense_eb(d);
   DenseSmem s{};
   int o = 0;
   s.off_k = o;
-  o += eb * d * dense_ks(d);
+  o += eb * (un ? dense_un_rows(d) : d) * dense_ks(d);
   s.off_y = o;
   o += eb * d;
   s.off_phi = o;
@@ -75,13 +92,14 @@ __host__ __device__ inline DenseSmem dense_smem(int d, int n_path) {
   return s;
 }
 
-template <int L, int CTW>
-__global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves) {
+template <int L, int CTW, bool UN = false>
+__global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves, PathRows pt, int row0, float* zp) {
   constexpr int d = (L + 1) * (L + 1);
-  constexpr int DP = dense_dp(d), KC = dense_kc(d), KS = dense_ks(d), EB = dense_eb(d);
-  constexpr int KB = DP / 16, RK = DP / 32;
+  constexpr int DP = dense_dp(d), KC = dense_kc(d), KS = dense_ks(d), EB = UN ? dense_eb_un(d) : dense_eb(d);
+  constexpr int KB = DP / 16, RK = UN ? dense_un_tiles(d) : DP / 32;
+  constexpr int KR = UN ? dense_un_rows(d) : d;  // rows of K_e held in LDS
   extern __shared__ float smem[];
-  const DenseSmem sm = dense_smem(d, a.n_path);
+  const DenseSmem sm = dense_smem(d, a.n_path, UN);
   float* sK = smem + sm.off_k;
   float* sY = smem + sm.off_y;
   float* sPhi = smem + sm.off_phi;
@@ -100,7 +118,7 @@ __global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves) {
 
   // K's padding columns (d .. KC-1) stay zero; every (k, i) with k, i < d is
   // rewritten for each batch
-  for (int t = tid; t < EB * d * KS; t += nthr) sK[t] = 0.f;
+  for (int t = tid; t < EB * KR * KS; t += nthr) sK[t] = 0.f;
 
   f32x16 acc[RK][CTW];
 #pragma unroll
@@ -134,11 +152,12 @@ __global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves) {
     for (int r = 0; r < RK; ++r) {
       u32x4 hi[KB], lo[KB];
       const int row = r * kTile + l32;
-      const float* kp = sK + (t * d + (row < d ? row : 0)) * KS + 8 * h;
+      const float* kp = sK + (t * KR + (row < KR ? row : 0)) * KS + 8 * h;
 #pragma unroll
       for (int b = 0; b < KB; ++b) {
-        // rows >= d and column groups >= KC are zero (not stored)
-        const bool in = row < d && 16 * b + 8 * h < KC;
+        // rows >= d (UN: past the chunk) and column groups >= KC are zero
+        // (not stored)
+        const bool in = row < KR && 16 * b + 8 * h < KC;
         float4 f0 = make_float4(0.f, 0.f, 0.f, 0.f), f1 = f0;
         if (in) {
           f0 = *reinterpret_cast<const float4*>(kp + 16 * b);
@@ -202,6 +221,43 @@ __global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves) {
       float v[EB];
 #pragma unroll
       for (int e = 0; e < EB; ++e) v[e] = 0.f;
+      if constexpr (UN) {
+        // one K row per (path, m3): for k of degree l3 and i of degree l1,
+        // the rows of the paths (l1, l2, l3), l2 = |l1 - l3| .. min(l1 + l3, L),
+        // each summing the entries whose j has degree l2 (consecutive, as the
+        // row lists j in order).  Every such row position is written, zero
+        // where the table holds no entry, so no value of the previous batch
+        // stays behind; rows outside this launch's chunk are skipped.
+        const int l3k = int(sqrtf(float(k) + 0.5f)), l1i = int(sqrtf(float(i) + 0.5f));
+        const int lo2 = l1i > l3k ? l1i - l3k : l3k - l1i, hi2 = l1i + l3k < L ? l1i + l3k : L;
+        int s = s0;
+        for (int l2 = lo2; l2 <= hi2; ++l2) {
+          const int p = pt.first[l1i * (L + 1) + l2] + (l3k - (l1i > l2 ? l1i - l2 : l2 - l1i));
+#pragma unroll
+          for (int e = 0; e < EB; ++e) v[e] = 0.f;
+          for (; s < s1; ++s) {
+            const int j = a.cg_col[s] & 0xffff;
+            if (j >= d) continue;  // malformed: ignored
+            const int l2j = int(sqrtf(float(j) + 0.5f));
+            if (l2j > l2) break;
+            if (l2j < l2) continue;  // no path with this degree: ignored
+            const float cv = a.cg_val[s];
+#pragma unroll
+            for (int e = 0; e < EB; ++e)
+              if (e < nb) v[e] = fmaf(cv, sY[e * d + j] * sRho[e * P + p], v[e]);
+          }
+          const int row = pt.row[p] + (k - l3k * l3k) - row0;
+          if (row >= 0 && row < KR) {
+#pragma unroll
+            for (int e = 0; e < EB; ++e)
+              if (e < nb) {
+                sK[(e * KR + row) * KS + i] = v[e];
+                mx[e] = fmaxf(mx[e], fabsf(v[e]));
+              }
+          }
+        }
+        continue;
+      }
       // for d > 32 (rows of ~5 entries) four entries' loads issued together,
       // then applied in order; one at a time below (fewer registers, more
       // waves)
@@ -263,7 +319,7 @@ __global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves) {
     }
     if (t < nb) edge_compute(t, x0);
   }
-  // Z[n] rows k < d, channels of this wave's tiles
+  // Z[n] rows k < d (UN: the chunk's path rows), channels of this wave's tiles
 #pragma unroll
   for (int c = 0; c < CTW; ++c) {
     const int ct = wave * CTW + c;
@@ -274,7 +330,11 @@ __global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int k = r * kTile + acc_row(v, h);
-        if (k < d) a.out[(size_t(n) * d + k) * a.C + ch] = acc[r][c][v];
+        if constexpr (UN) {
+          if (row0 + k < pt.n_rows) zp[(size_t(n) * pt.n_rows + row0 + k) * a.C + ch] = acc[r][c][v];
+        } else {
+          if (k < d) a.out[(size_t(n) * d + k) * a.C + ch] = acc[r][c][v];
+        }
       }
   }
 }
@@ -287,8 +347,29 @@ hipError_t launch_l_ctw(const DenseArgs& a, int waves, hipStream_t s) {
   hipError_t e =
       hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
   if (e != hipSuccess) return e;
-  k<<<dim3(a.N), dim3(waves * kWave), lds, s>>>(a, waves);
+  PathRows none{};
+  k<<<dim3(a.N), dim3(waves * kWave), lds, s>>>(a, waves, none, 0, nullptr);
   return hipGetLastError();
+}
+
+// UN: one launch per chunk of kUnRows path rows (one 32-channel tile per
+// wave, C <= 128)
+template <int L>
+hipError_t launch_l_un(const DenseArgs& a, float* zp, hipStream_t s) {
+  constexpr int d = (L + 1) * (L + 1);
+  const int n_ct = (a.C + kTile - 1) / kTile;
+  const PathRows pt = path_rows(L);
+  const size_t lds = size_t(dense_smem(d, a.n_path, true).floats) * 4;
+  auto k = k_dense_edge<L, 1, true>;
+  hipError_t e =
+      hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  if (e != hipSuccess) return e;
+  for (int row0 = 0; row0 < pt.n_rows; row0 += dense_un_rows(d)) {
+    k<<<dim3(a.N), dim3(n_ct * kWave), lds, s>>>(a, n_ct, pt, row0, zp);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 template <int L>
@@ -308,6 +389,41 @@ int dense_path_count(int L) {
       n += hi - lo + 1;
     }
   return n;
+}
+
+PathRows path_rows(int L) {
+  PathRows t{};
+  int p = 0, row = 0;
+  for (int l1 = 0; l1 <= L; ++l1)
+    for (int l2 = 0; l2 <= L; ++l2) {
+      const int lo = l1 > l2 ? l1 - l2 : l2 - l1, hi = l1 + l2 < L ? l1 + l2 : L;
+      if (l1 * (L + 1) + l2 < kMaxDegPairs) t.first[l1 * (L + 1) + l2] = p;
+      for (int l3 = lo; l3 <= hi && p < kMaxPaths; ++l3, ++p) {
+        t.l3[p] = l3;
+        t.row[p] = row;
+        row += 2 * l3 + 1;
+      }
+    }
+  t.n_path = p;
+  t.n_rows = row;
+  return t;
+}
+
+hipError_t launch_dense_edge_unshared(const DenseArgs& a, float* zp, hipStream_t s) {
+  if (a.N == 0) return hipSuccess;
+  if (a.C < 1 || a.C > 4 * kTile || a.n_radial < 1 || a.n_radial > 16 || a.n_path != dense_path_count(a.L) ||
+      a.feat == nullptr || a.row_scale == nullptr || zp == nullptr)
+    return hipErrorInvalidValue;
+  switch (a.L) {
+    case 0: return dense_detail::launch_l_un<0>(a, zp, s);
+    case 1: return dense_detail::launch_l_un<1>(a, zp, s);
+    case 2: return dense_detail::launch_l_un<2>(a, zp, s);
+    case 3: return dense_detail::launch_l_un<3>(a, zp, s);
+    case 4: return dense_detail::launch_l_un<4>(a, zp, s);
+    case 5: return dense_detail::launch_l_un<5>(a, zp, s);
+    case 6: return dense_detail::launch_l_un<6>(a, zp, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_dense_edge(const DenseArgs& a, hipStream_t s) {

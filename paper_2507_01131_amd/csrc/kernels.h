@@ -146,6 +146,28 @@ struct DenseArgs {
 // Paths (l1, l2, l3) of the full product up to degree L.
 int dense_path_count(int L);
 hipError_t launch_dense_edge(const DenseArgs& a, hipStream_t s);
+
+// The product without path-weight sharing: every path keeps its own block of
+// output rows, path p (in the order l1, then l2, then l3 ascending) owning
+// rows row[p] .. row[p] + 2 l3[p], n_rows = sum over paths of 2 l3 + 1.
+// first[l1 (L + 1) + l2] is the index of the path (l1, l2, |l1 - l2|).
+constexpr int kMaxPaths = 176;
+constexpr int kMaxDegPairs = 49;
+struct PathRows {
+  int n_path, n_rows;
+  int l3[kMaxPaths];
+  int row[kMaxPaths];
+  int first[kMaxDegPairs];
+};
+PathRows path_rows(int L);
+// zp[n][row][c] = the sum over edges into n of the edge's path blocks,
+// zp[n][row[p] + m3] = sum_e rho_e[p] sum_{i, j} C[(l3, m3); i, j] x[s_e][i] Y_e[j]
+// for the entries of path p (fp32 features, C <= 128).
+hipError_t launch_dense_edge_unshared(const DenseArgs& a, float* zp, hipStream_t s);
+// out[n][(l3, m3)][:] = sum over paths p with degree l3 of zp[n][row[p] + m3][:] W_paths[p]
+// (W_paths [P, C, C] fp32, [in][out] per path; fp32 operands on the
+// GEMM's fp32 path).
+hipError_t launch_path_gemm(int N, int L, int C, const float* zp, const float* W_paths, float* out, hipStream_t s);
 // Workspace bytes of EdgeArgs::ef_ops: the output factor in 32x32x16 operand
 // blocks [ceil(d/32)][ceil(R/32)][2][parts][64 lanes] x 16 bytes (parts <= 2)
 // and, after them, its scale.

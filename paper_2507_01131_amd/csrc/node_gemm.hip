@@ -13,7 +13,9 @@
 // fp32 node GEMMs run on 32x32x16 fp16 MFMA over scaled two-part splits
 // (k_node_gemm_f16); the Gram products of fp32 problems use 32x32x2 fp32
 // MFMA; bf16 problems (bf16 W) use 32x32x16 bf16 MFMA with the fp32 operand
-// rounded to bf16 while it is staged.
+// rounded to bf16 while it is staged.  Without path-weight sharing, each
+// path has its own channel matrix; the path GEMM applies them to the per-path
+// node sums (they too commute with the edge sum) on 32x32x2 fp32 MFMA.
 #include "common.hpp"
 #include "kernels.h"
 
@@ -386,6 +388,24 @@ __global__ __launch_bounds__(256) void k_node_gemm(int rows, int C, const float*
 // partial[p][ci][co] = sum over rows of chunk p of Z[row][ci] G[row][co]:
 // L(m = ci, k = row) = Z[row][ci] (transposed left operand),
 // R(k = row, n = co) = G[row][co].
+// The product without path-weight sharing: out[n][k][:] = sum over the paths
+// p of degree l3 = deg k of zp[n][row[p] + k - l3^2][:] W_paths[p], one
+// (row tile, column tile, k) per block, the paths accumulated in order.
+__global__ __launch_bounds__(256) void k_path_gemm(int N, int C, int d, PathRows pt, const float* __restrict__ zp,
+                                                   const float* __restrict__ W_paths, float* __restrict__ out) {
+  __shared__ __align__(16) float smem[2 * kBM * kSF];
+  const int m0 = blockIdx.x * kBM, n0 = blockIdx.y * kBN, k = blockIdx.z;
+  int l3 = 0;
+  while ((l3 + 1) * (l3 + 1) <= k) ++l3;
+  f32x16 acc[2][2] = {{f32x16{}, f32x16{}}, {f32x16{}, f32x16{}}};
+  for (int p = 0; p < pt.n_path; ++p) {
+    if (pt.l3[p] != l3) continue;
+    gemm_tile<false, false, false>(zp + size_t(pt.row[p] + k - l3 * l3) * C, pt.n_rows * C, N,
+                                   W_paths + size_t(p) * C * C, C, C, 0, C, m0, n0, acc, smem);
+  }
+  store_tile(acc, out + size_t(k) * C, d * C, N, C, m0, n0);
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(256) void k_gram_partial(int rows, int C, int rows_per_part, const float* __restrict__ Z,
                                                       const float* __restrict__ G, float* __restrict__ partial) {
@@ -465,6 +485,15 @@ int gram_parts(int rows, int C) {
   const int by_rows = rows / 64;
   if (p > by_rows) p = by_rows;
   return p < 1 ? 1 : p;
+}
+
+hipError_t launch_path_gemm(int N, int L, int C, const float* zp, const float* W_paths, float* out, hipStream_t s) {
+  if (N == 0) return hipSuccess;
+  if (L < 0 || L > 6 || C < 1 || !zp || !W_paths || !out) return hipErrorInvalidValue;
+  const int d = (L + 1) * (L + 1);
+  const dim3 grid((N + kBM - 1) / kBM, (C + kBN - 1) / kBN, d);
+  k_path_gemm<<<grid, dim3(256), 0, s>>>(N, C, d, path_rows(L), zp, W_paths, out);
+  return hipGetLastError();
 }
 
 hipError_t launch_gram(int rows, int C, const float* Z, const float* G, bool bf16, float* partial, float* grad_W,

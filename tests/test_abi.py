@@ -187,6 +187,41 @@ def test_dense_forward_argument_checks(L, n_path):
     assert _dense(good, ws_bytes=0, nnz=0, col=None, val=None) == 4   # an empty table needs no entries
 
 
+def _dense_un(p, ws_bytes=1 << 40, nnz=100, **override):
+    args = dict(x=FAKE, vec=FAKE, ei=FAKE, row=FAKE, col=FAKE, val=FAKE, pw=FAKE, Wp=FAKE, out=FAKE,
+                perm=FAKE, off=FAKE, ws=FAKE)
+    args.update(override)
+    return tdn.lib().tdn_dense_tp_forward_unshared(None if p is None else ctypes.byref(p), args["x"], args["vec"],
+                                                   args["ei"], args["row"], args["col"], args["val"], nnz,
+                                                   args["pw"], args["Wp"], args["out"], args["perm"], args["off"],
+                                                   args["ws"], ws_bytes, None)
+
+
+@pytest.mark.parametrize("L,n_path,n_rows", [(0, 1, 1), (1, 5, 11), (2, 15, 51), (3, 34, 156), (4, 65, 375),
+                                             (5, 111, 771), (6, 175, 1421)])
+def test_dense_unshared_argument_checks_and_workspace(L, n_path, n_rows):
+    # the per-path node sums take sum over paths of (2 l3 + 1) rows per node
+    assert n_rows == sum(2 * l3 + 1 for l1 in range(L + 1) for l2 in range(L + 1)
+                         for l3 in range(abs(l1 - l2), min(l1 + l2, L) + 1))
+    good = _problem(L=L, R=n_path, C=96)
+    fwd, _ = tdn.workspace_size(good)
+    un = ctypes.c_size_t(0)
+    assert tdn.lib().tdn_dense_tp_unshared_workspace_size(ctypes.byref(good), ctypes.byref(un)) == 0
+    assert un.value >= fwd + 100 * n_rows * 96 * 4
+    assert un.value < fwd + 100 * n_rows * 96 * 4 + 4096
+    assert tdn.lib().tdn_dense_tp_unshared_workspace_size(ctypes.byref(good), None) == 1
+    assert _dense_un(good, ws_bytes=un.value - 1) == 4
+    assert _dense_un(good, ws_bytes=0) == 4
+    assert _dense_un(_problem(L=L, R=n_path + 1)) == 2
+    assert _dense_un(_problem(L=L, R=n_path, C=144)) == 2             # C <= 128
+    assert _dense_un(_problem(L=L, R=n_path, feat_dtype=tdn.TDN_BF16)) == 3
+    assert _dense_un(good, nnz=-1) == 2
+    assert _dense_un(None) == 1
+    for k in ["x", "vec", "ei", "row", "col", "val", "pw", "Wp", "out", "perm", "off", "ws"]:
+        assert _dense_un(good, **{k: None}) == 1, k
+    assert _dense_un(good, ws_bytes=0, nnz=0, col=None, val=None) == 4
+
+
 def _tp3(p, ws_bytes=1 << 40, **override):
     args = dict(x=FAKE, vec=FAKE, ei=FAKE, A=FAKE, A2=FAKE, B=FAKE, D=FAKE, W=FAKE, rw=FAKE, out=FAKE, z=None,
                 perm=FAKE, off=FAKE, ws=FAKE)
