@@ -151,7 +151,8 @@ FwdLayout fwd_layout(const tdn_problem& p) {
 }
 
 struct BwdLayout {
-  size_t gz, z, xt, part, parts, perm_src, off_src, sort, wp, drho, wrad_part, gv, fsl, gtmp, grtmp, flags, total;
+  size_t gz, z, xt, part, parts, perm_src, off_src, sort, wp, drho, wrad_part, gv, fsl, gtmp, grtmp, gzc, flags,
+      total;
 };
 BwdLayout bwd_layout(const tdn_problem& p) {
   BwdLayout b{};
@@ -178,8 +179,8 @@ BwdLayout bwd_layout(const tdn_problem& p) {
   const int rc = chunk_problem(p, 0).R;  // the largest rank chunk (p.R when not chunked)
   b.drho = o;  // radial-weight gradient: dL/drho per edge, block partials, and a
   o += al(size_t(p.n_edges) * rc * 4);  // grad_edge_vec stand-in when only grad_radial_w is asked for
-  b.wrad_part = o;
-  o += al(size_t(tdn::radial_grad_blocks(p.n_edges)) * p.n_radial * rc * 4);
+  b.wrad_part = o;  // partials of the radial_grad kernel or of the range kernel's workgroups
+  o += al(size_t(std::max(tdn::radial_grad_blocks(p.n_edges), 2 * tdn::device_cus())) * p.n_radial * rc * 4);
   b.gv = o;
   o += al(size_t(p.n_edges) * 12);
   const bool chunked = rank_chunks(p.R) > 1;
@@ -189,6 +190,8 @@ BwdLayout bwd_layout(const tdn_problem& p) {
   o += chunked ? al(std::max(ndc, size_t(p.n_edges) * 12)) : 0;
   b.grtmp = o;
   o += chunked ? al(size_t(p.n_radial) * rc * 4) : 0;
+  b.gzc = o;  // split form of the destination kernel: Gz in the layout of xc, then its row scales
+  o += tdn::bwd_dst_split(p.L, p.C, p.feat_dtype == TDN_BF16) ? al(xc_bytes(p)) + al(size_t(p.n_nodes) * 4) : 0;
   b.flags = o;
   o += 256;
   b.total = o;
@@ -768,6 +771,15 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
     // gradients go to the output (first chunk) or to gtmp and are added in
     // chunk order; the radial-weight gradient of the chunk fills its columns
     float* gv_out = grad_edge_vec ? grad_edge_vec : reinterpret_cast<float*>(ws + lay.gv);
+    // the split form takes Gz in the layout of xc (independent of the rank chunk)
+    const bool split = tdn::bwd_dst_split(p->L, C, bf16) && tdn::bwd_dst_plan(p->L, chunk_problem(*p, 0).R, C,
+                                                                               p->n_radial, bf16, E).n_range > 0;
+    float* gzscale = reinterpret_cast<float*>(ws + lay.gzc + al(xc_bytes(*p)));
+    if (split) {
+      Timed t("channel_layout", stream);
+      TDN_HIP(tdn::launch_direct_layout(N, d, C, tdn::bwd_dst_cpad(C, bf16), Gz, true, feature_parts(*p),
+                                        ws + lay.gzc, bf16 ? nullptr : gzscale, false, stream));
+    }
     for (int c = 0; c < nch; ++c) {
       int r0 = 0, n = 0;
       const float *cA, *cB, *cD, *cW;
@@ -807,6 +819,14 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
                                           ws + lay.xt, bf16 ? nullptr : xscale, false, stream));
         a.xc = ws + lay.xt;
         a.x_scale = bf16 ? nullptr : xscale;
+        // the range kernel sums the radial-weight gradient per workgroup
+        a.drho = nullptr;
+        a.wrad_part = grad_radial_w ? reinterpret_cast<float*>(ws + lay.wrad_part) : nullptr;
+        if (split) {
+          a.gzc = ws + lay.gzc;
+          a.gz_scale = bf16 ? nullptr : gzscale;
+          a.dg = reinterpret_cast<float*>(ws + lay.drho);
+        }
       } else if (d > 32) {
         // x in the direct kernel's operand blocks, channels in its accumulator
         // order
@@ -825,8 +845,11 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
       if (grad_radial_w) {
         Timed t("radial_grad", stream);
         float* gr = nch == 1 ? grad_radial_w : reinterpret_cast<float*>(ws + lay.grtmp);
-        TDN_HIP(tdn::launch_radial_grad(E, n, p->n_radial, a.sigma, edge_vec, a.drho,
-                                        reinterpret_cast<float*>(ws + lay.wrad_part), gr, stream));
+        if (a.n_range > 0)
+          TDN_HIP(tdn::launch_sum_parts(a.n_range / a.pieces_per_block, p->n_radial * n, a.wrad_part, gr, stream));
+        else
+          TDN_HIP(tdn::launch_radial_grad(E, n, p->n_radial, a.sigma, edge_vec, a.drho,
+                                          reinterpret_cast<float*>(ws + lay.wrad_part), gr, stream));
         if (nch > 1) TDN_HIP(tdn::launch_scatter_cols(p->n_radial, p->R, r0, n, gr, grad_radial_w, stream));
       }
     }

@@ -29,16 +29,21 @@ TDN_DST2_EXTERN(4)
 
 constexpr int kMinPieceEdges = 96, kMaxPieces = 2;
 
+bool bwd_dst_split(int L, int C, bool bf16) {
+  return (L + 1) * (L + 1) <= 32 && bwd2_detail::dst2_split(C, bf16);
+}
+
 EdgePlan bwd_dst_plan(int L, int R, int C, int n_radial, bool bf16, int E) {
   using namespace bwd2_detail;
   const int d = (L + 1) * (L + 1);
   const int RT = (R + kTile - 1) / kTile;
   if (E <= 0 || d > 32 || RT > 8) return EdgePlan{0, 0};
-  const int chunk = dst2_chunk(RT, bf16, d, n_radial, C);
-  const int lds = dst2_smem(RT, bf16 ? 1 : 2, d, n_radial, C, chunk).floats * 4;
+  const bool split = bwd_dst_split(L, C, bf16);
+  const int chunk = dst2_chunk(RT, bf16, d, n_radial, C, split);
+  const int lds = dst2_smem(RT, bf16 ? 1 : 2, d, n_radial, C, chunk, split).floats * 4;
   if (lds > 160 * 1024) return EdgePlan{0, 0};
   int per_cu = 160 * 1024 / lds;
-  per_cu = per_cu > 2 ? 2 : per_cu;  // eight waves per workgroup, two per SIMD
+  per_cu = per_cu > 2 ? 2 : per_cu;  // eight waves per workgroup, two (four in the split form) per SIMD
   int nb = device_cus() * per_cu;
   nb = nb < E ? nb : E;
   // several ranges per workgroup (there is no sum across ranges here) while

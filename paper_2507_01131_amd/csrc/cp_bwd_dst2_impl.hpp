@@ -87,7 +87,7 @@ struct Smem {
 // order [rank tile][4][64 lanes] x 16 bytes, the staged Gz parts
 // [32 rows][gzs halves] (gzs = P*Cp + 8: rows 16 bytes apart in bank terms),
 // and the chunk's v, rho, Y, Phi, dY, dPhi, Jacobian and per-edge records.
-__host__ __device__ inline Smem dst2_smem(int RT, int P, int d, int n_radial, int C, int chunk) {
+__host__ __device__ inline Smem dst2_smem(int RT, int P, int d, int n_radial, int C, int chunk, bool split) {
   Smem s{};
   s.Rp = RT * kTile;
   s.bs = s.Rp + 1;
@@ -98,12 +98,13 @@ __host__ __device__ inline Smem dst2_smem(int RT, int P, int d, int n_radial, in
   s.off_wr = o;
   o += n_radial * s.bs;
   o = (o + 3) & ~3;
+  // A, D and the staged Gz: only where the kernel runs the S/T contraction
   s.off_ap = o;
-  o += 2 * RT * P * kWave * 4;
+  o += split ? 0 : 2 * RT * P * kWave * 4;
   s.off_d = o;
-  o += kTile * s.Rp;
+  o += split ? 0 : kTile * s.Rp;
   s.off_gz = o;
-  o += kTile * s.gzs / 2;
+  o += split ? 0 : kTile * s.gzs / 2;
   s.off_v = o;
   o += chunk * s.bs;
   s.off_rho = o;
@@ -125,14 +126,17 @@ __host__ __device__ inline Smem dst2_smem(int RT, int P, int d, int n_radial, in
 }
 
 
-template <int L, int RT, bool BF>
-__global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_range, int chunk) {
+// SPLIT: dg of every edge comes from memory (k_bwd_dg below) instead of the
+// S/T contraction here; without A, D and Gz in LDS two workgroups share a CU.
+template <int L, int RT, bool BF, bool SPLIT>
+__global__ __launch_bounds__(kWaves* kWave) __attribute__((amdgpu_waves_per_eu(SPLIT ? 4 : 2))) void k_bwd_dst2(
+    BwdDstArgs a, int n_range, int chunk) {
   constexpr int d = (L + 1) * (L + 1);
   constexpr int P = BF ? 1 : 2;
   constexpr int KPS = dst2_kps(P);
   constexpr int Rp = RT * kTile;
   extern __shared__ float smem[];
-  const Smem S = dst2_smem(RT, P, d, a.n_radial, a.C, chunk);
+  const Smem S = dst2_smem(RT, P, d, a.n_radial, a.C, chunk, SPLIT);
   const int bs = S.bs, gzs = S.gzs;
   float* sB = smem + S.off_b;
   float* sWr = smem + S.off_wr;
@@ -172,7 +176,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
   // fp32 problems: the power of two 2^-e_A that puts A's largest |A| in
   // [2^13, 2^14) for its fp16 parts; dg carries 2^e_A back
   float a_sc = 1.f, a_unscale = 1.f;
-  if constexpr (!BF) {
+  if constexpr (!BF && !SPLIT) {
     float mx = 0.f;
     for (int i = tid; i < d * R; i += blockDim.x) mx = fmaxf(mx, fabsf(a.A[i]));
 #pragma unroll
@@ -186,7 +190,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
     a_unscale = ldexpf(1.f, e);
   }
   // sAp[((q*RT + rt)*P + p)*64 + lane'] = part p of A[t_row(q, h', i)][rt*32 + l32'], i = 0..7
-  for (int t = tid; t < 2 * RT * kWave; t += blockDim.x) {
+  for (int t = tid; t < (SPLIT ? 0 : 2 * RT * kWave); t += blockDim.x) {
     const int ln = t % kWave, qrt = t / kWave;
     const int q = qrt / RT, rt = qrt - q * RT;
     const int r = rt * kTile + (ln & 31), hh = ln >> 5;
@@ -206,7 +210,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
   }
   // sDl[(rt*4 + qq)*64 + lane'][i] = D[acc_row(4 qq + i, h')][rt*32 + l32']: the D
   // values lane' weighs its T accumulators with, one 16-byte read per quarter
-  for (int t = tid; t < RT * 4 * kWave; t += blockDim.x) {
+  for (int t = tid; t < (SPLIT ? 0 : RT * 4 * kWave); t += blockDim.x) {
     const int ln = t % kWave, rq = t / kWave;
     const int rt = rq / 4, qq = rq % 4;
     const int r = rt * kTile + (ln & 31);
@@ -220,6 +224,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
   }
 
   float gz_unscale = 1.f;  // 2^e_g of the staged Gz (fp32 problems)
+  f32x16 wacc = f32x16{};  // radial-weight gradient [n_radial rows][this wave's rank tile]
   // ---- per edge: S_e, T_e, dg -> dv, drho (in place in sV, sRho)
   // The x operand streams through a ring of kRing slots per wave, kRing - 1
   // slots ahead of the MFMA and on into the wave's next edge of the piece, so
@@ -469,8 +474,19 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
       }
       EdgeRec next{};
       load_rec(next_eid, nn, next);
+      if constexpr (SPLIT) {
+        // dg of the chunk's edges (sorted positions cb ..): dv, drho in place
+        __syncthreads();  // v/rho written
+        for (int i = tid; i < n * R; i += blockDim.x) {
+          const int e = i / R, r = i - e * R;
+          const float g = a.dg[size_t(cb + e) * R + r];
+          const float v = sV[e * bs + r], rho = sRho[e * bs + r];
+          sV[e * bs + r] = g * rho;
+          sRho[e * bs + r] = g * v;
+        }
+      }
       // ---- the chunk in segment pieces
-      for (int p0 = 0; p0 < n;) {
+      for (int p0 = 0; p0 < (SPLIT ? 0 : n);) {
         __syncthreads();  // v/rho written; the previous piece's edges done with sGz
         const int seg = __builtin_amdgcn_readfirstlane(sKey[p0]);
         int p1 = p0 + 1;
@@ -539,38 +555,58 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
           const int ee = acc_row(v, h);
           if (ee < n && l32 < K2) dstp[ee * K2 + l32] = T[v];
         }
+        // the radial-weight gradient sum_e phi_e^T drho_e, rank tile `wave`,
+        // accumulated over the workgroup's chunks (K = the chunk's edges)
+        if (wave < RT) {
+#pragma unroll
+          for (int s2 = 0; s2 < kMaxChunk / 2; ++s2) {
+            const int e = 2 * s2 + h;
+            const float av = (e < n && l32 < nr) ? sPhi[e * nr + l32] : 0.f;
+            const float bv = e < n ? sRho[e * bs + wave * kTile + l32] : 0.f;
+            wacc = mfma32(av, bv, wacc);
+          }
+        }
       }
       __syncthreads();
-      for (int t = tid; t < n; t += blockDim.x) {
-        const int eid = sEid[t];
-        const float vx = sVec[3 * t], vy = sVec[3 * t + 1], vz = sVec[3 * t + 2];
-        const float rn = sqrtf(vx * vx + vy * vy + vz * vz);
-        float gx = 0.f, gy = 0.f, gzv = 0.f;
-        for (int k = 0; k < d; ++k) {
-          const int i = t * d + k;
-          const float dy = ((sDY[i] + sDY[chunk * d + i]) + sDY[2 * chunk * d + i]) + sDY[3 * chunk * d + i];
-          gx += dy * sJ[t * 3 * d + 3 * k];
-          gy += dy * sJ[t * 3 * d + 3 * k + 1];
-          gzv += dy * sJ[t * 3 * d + 3 * k + 2];
+      // ---- the gradient per edge: sixteen threads per edge, each summing a
+      // share of the degree rows and radial functions, then combined across
+      // the sixteen lanes in a fixed order
+      {
+        constexpr int TPE = kWaves * kWave / kMaxChunk;
+        const int t = tid / TPE, sub = tid % TPE;
+        float gx = 0.f, gy = 0.f, gzv = 0.f, dr = 0.f;
+        if (t < n) {
+          const float vx = sVec[3 * t], vy = sVec[3 * t + 1], vz = sVec[3 * t + 2];
+          const float rn = sqrtf(vx * vx + vy * vy + vz * vz);
+          for (int k = sub; k < d; k += TPE) {
+            const int i = t * d + k;
+            const float dy = ((sDY[i] + sDY[chunk * d + i]) + sDY[2 * chunk * d + i]) + sDY[3 * chunk * d + i];
+            gx += dy * sJ[t * 3 * d + 3 * k];
+            gy += dy * sJ[t * 3 * d + 3 * k + 1];
+            gzv += dy * sJ[t * 3 * d + 3 * k + 2];
+          }
+          for (int q = sub; q < nr; q += TPE) {
+            const float u = (rn - float(q) * a.sigma) / a.sigma;
+            const int i = t * nr + q;
+            const float dphi =
+                ((sDPhi[i] + sDPhi[chunk * nr + i]) + sDPhi[2 * chunk * nr + i]) + sDPhi[3 * chunk * nr + i];
+            dr += dphi * (-u / a.sigma) * sPhi[i];
+          }
         }
-        float dr = 0.f;
-        for (int q = 0; q < nr; ++q) {
-          const float u = (rn - float(q) * a.sigma) / a.sigma;
-          const int i = t * nr + q;
-          const float dphi =
-              ((sDPhi[i] + sDPhi[chunk * nr + i]) + sDPhi[2 * chunk * nr + i]) + sDPhi[3 * chunk * nr + i];
-          dr += dphi * (-u / a.sigma) * sPhi[i];
+#pragma unroll
+        for (int o = TPE / 2; o > 0; o >>= 1) {
+          gx += __shfl_xor(gx, o);
+          gy += __shfl_xor(gy, o);
+          gzv += __shfl_xor(gzv, o);
+          dr += __shfl_xor(dr, o);
         }
-        const float inv = 1.f / rn;
-        a.grad_vec[3 * eid] = gx + dr * vx * inv;
-        a.grad_vec[3 * eid + 1] = gy + dr * vy * inv;
-        a.grad_vec[3 * eid + 2] = gzv + dr * vz * inv;
-      }
-      if (a.drho) {  // drho rows for the radial-weight gradient (sRho is rewritten after the next barrier)
-        const int R = a.R;
-        for (int i = tid; i < n * R; i += blockDim.x) {
-          const int t = i / R, r = i - t * R;
-          a.drho[size_t(sEid[t]) * R + r] = sRho[t * bs + r];
+        if (t < n && sub == 0) {
+          const int eid = sEid[t];
+          const float vx = sVec[3 * t], vy = sVec[3 * t + 1], vz = sVec[3 * t + 2];
+          const float inv = 1.f / sqrtf(vx * vx + vy * vy + vz * vz);
+          a.grad_vec[3 * eid] = gx + dr * vx * inv;
+          a.grad_vec[3 * eid + 1] = gy + dr * vy * inv;
+          a.grad_vec[3 * eid + 2] = gzv + dr * vz * inv;
         }
       }
       if (npc >= per_block) break;
@@ -580,23 +616,292 @@ __global__ __launch_bounds__(kWaves* kWave) void k_bwd_dst2(BwdDstArgs a, int n_
       rec = next;
     }
   }
+  // this workgroup's partial of the radial-weight gradient
+  if (a.wrad_part && wave < RT) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int q = acc_row(v, h), r = wave * kTile + l32;
+      if (q < nr && r < R) a.wrad_part[(size_t(blockIdx.x) * nr + q) * R + r] = wacc[v];
+    }
+  }
+}
+
+// ---- Split form: the S/T contraction alone, for channel counts whose Gz[t]
+// operand fits in 64 registers (at most 8 ring slots).  Each wave takes one
+// contiguous range of destination-sorted edges, with no workgroup barrier
+// after the factors are staged; x[s_e] streams through the ring as in the
+// range kernel, across edge boundaries, and Gz[t] comes in the same operand
+// blocks (launch_direct_layout of Gz, one power-of-two scale per node for
+// fp32 problems), loaded into registers when the destination changes.  The
+// edge records are fetched 64 at a time, one batch ahead.  dg is stored per
+// sorted edge position, dg[pos][r], for the range kernel's SPLIT mode.
+constexpr int kDgWaves = 4;
+__host__ __device__ inline int dg_slots(int C, int P) { return dst2_cpad(C, P) / (16 * dst2_kps(P)); }
+__host__ __device__ inline int dg_smem_floats(int RT, int P) {
+  return 2 * RT * P * kWave * 4 + RT * 4 * kWave * 4 + kDgWaves;
+}
+
+constexpr int kDgMaxSlots = 8;
+template <int L, int RT, bool BF>
+__global__ __launch_bounds__(kDgWaves* kWave) void k_bwd_dg(BwdDstArgs a, int n_wr) {
+  constexpr int d = (L + 1) * (L + 1);
+  constexpr int P = BF ? 1 : 2;
+  constexpr int KPS = dst2_kps(P);
+  constexpr int kBatch = kWave;  // edge records per batch, one per lane
+  extern __shared__ float smem[];
+  u32x4* sAp = reinterpret_cast<u32x4*>(smem);
+  f32x4* sDl = reinterpret_cast<f32x4*>(smem + 2 * RT * P * kWave * 4);
+  float* sRed = smem + 2 * RT * P * kWave * 4 + RT * 4 * kWave * 4;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int h = lane >> 5, l32 = lane & 31;
+  const int R = a.R;
+
+  // ---- A in parts (T operand order) and D (accumulator order), as in the
+  // range kernel
+  float a_sc = 1.f, a_unscale = 1.f;
+  if constexpr (!BF) {
+    float mx = 0.f;
+    for (int i = tid; i < d * R; i += blockDim.x) mx = fmaxf(mx, fabsf(a.A[i]));
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    if (lane == 0) sRed[wave] = mx;
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < kDgWaves; ++w) mx = fmaxf(mx, sRed[w]);
+    const int e = f16_split_exponent(mx);
+    a_sc = ldexpf(1.f, -e);
+    a_unscale = ldexpf(1.f, e);
+  }
+  for (int t = tid; t < 2 * RT * kWave; t += blockDim.x) {
+    const int ln = t % kWave, qrt = t / kWave;
+    const int q = qrt / RT, rt = qrt - q * RT;
+    const int r = rt * kTile + (ln & 31), hh = ln >> 5;
+    uint32_t w[P][4];
+#pragma unroll
+    for (int p2 = 0; p2 < 4; ++p2) {
+      const int k0 = t_row(q, hh, 2 * p2), k1 = t_row(q, hh, 2 * p2 + 1);
+      const float v0 = (k0 < d && r < R) ? a.A[k0 * R + r] : 0.f;
+      const float v1 = (k1 < d && r < R) ? a.A[k1 * R + r] : 0.f;
+      if constexpr (P == 2)
+        split_f16x2_pair(v0 * a_sc, v1 * a_sc, w[0][p2], w[1][p2]);
+      else
+        w[0][p2] = pack_bf16x2_rne(v0, v1);
+    }
+#pragma unroll
+    for (int p = 0; p < P; ++p) sAp[(qrt * P + p) * kWave + ln] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
+  }
+  for (int t = tid; t < RT * 4 * kWave; t += blockDim.x) {
+    const int ln = t % kWave, rq = t / kWave;
+    const int rt = rq / 4, qq = rq % 4;
+    const int r = rt * kTile + (ln & 31);
+    f32x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = acc_row(4 * qq + i, ln >> 5);
+      v[i] = (j < d && r < R) ? a.D[j * R + r] : 0.f;
+    }
+    sDl[t] = v;
+  }
+  __syncthreads();
+
+  // ---- this wave's range of sorted positions; neighbouring ranges on one XCD
+  const int w = xcd_remap(blockIdx.x, gridDim.x) * kDgWaves + wave;
+  const int e0 = int(int64_t(w) * a.E / n_wr), e1 = int(int64_t(w + 1) * a.E / n_wr);
+  if (e0 >= e1) return;
+
+  const int ns = dg_slots(a.C, P);  // 4 or 8, a multiple of kRing
+  const int Cp = ns * 16 * KPS;
+  const char* __restrict__ xc = static_cast<const char*>(a.xc);
+  const char* __restrict__ gzc = static_cast<const char*>(a.gzc);
+  const int xrow = d * P * Cp * 2;  // bytes per node, x and Gz alike
+  const int xstep = 2 * d * 16;     // bytes per operand block (part, K-step)
+  const uint32_t xoff = l32 < d ? uint32_t((h * d + l32) * 16) : 0x80000000u;
+  auto rsrc = [&](const char* base, int row, bool valid) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base) + size_t(row) * xrow, 0, valid ? xrow : 0,
+                                             kBufferWord3);
+  };
+  auto load_slot = [&](__amdgpu_buffer_rsrc_t rs, int sl, u32x4 (&xb)[KPS][P]) {
+#pragma unroll
+    for (int kk = 0; kk < KPS; ++kk)
+#pragma unroll
+      for (int p = 0; p < P; ++p)
+        xb[kk][p] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, xoff, (p * (Cp / 16) + sl * KPS + kk) * xstep, 0));
+  };
+
+  // edge records of positions b0 .. b0 + 63, one per lane
+  struct Rec {
+    int src, dst;
+    float xs, gs;
+  };
+  auto load_batch = [&](int b0) {
+    Rec r{0, -1, 1.f, 1.f};
+    const int pos = b0 + lane;
+    if (pos < e1) {
+      const int eid = a.perm[pos];
+      r.src = a.src[eid];
+      r.dst = a.dst[eid];
+      if constexpr (!BF) {
+        r.xs = a.x_scale[r.src];
+        r.gs = a.gz_scale[r.dst];
+      }
+    }
+    return r;
+  };
+  Rec cur = load_batch(e0), nxt = load_batch(e0 + kBatch);
+  int b0 = e0;
+
+  u32x4 ring[kRing][KPS][P];
+  u32x4 g[kDgMaxSlots][KPS][P];
+  int cur_t = -1;
+  float g_unscale = 1.f;
+  __amdgpu_buffer_rsrc_t rs = rsrc(xc, __builtin_amdgcn_readlane(cur.src, 0), true);
+#pragma unroll
+  for (int j = 0; j + 1 < kRing; ++j) load_slot(rs, j, ring[j]);
+
+  for (int e = e0; e < e1; ++e) {
+    const int j = e - b0;
+    const int t = __builtin_amdgcn_readlane(cur.dst, j);
+    const float xs = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cur.xs), j));
+    const bool has_next = e + 1 < e1;
+    const int sn = j + 1 < kBatch ? __builtin_amdgcn_readlane(cur.src, j + 1) : __builtin_amdgcn_readlane(nxt.src, 0);
+    const __amdgpu_buffer_rsrc_t nrs = rsrc(xc, has_next ? sn : 0, has_next);
+    if (t != cur_t) {
+      // Gz[t] into registers (rows j >= d read zeros through the range check)
+      const __amdgpu_buffer_rsrc_t grs = rsrc(gzc, t, true);
+#pragma unroll
+      for (int sl = 0; sl < kDgMaxSlots; ++sl)
+        if (sl < ns) load_slot(grs, sl, g[sl]);
+      g_unscale = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cur.gs), j));
+      cur_t = t;
+    }
+    // S_e = x[s_e] Gz[t]^T over the channels, the ring kRing - 1 slots ahead
+    f32x16 Sacc = f32x16{};
+#pragma unroll
+    for (int u = 0; u < kDgMaxSlots; ++u) {
+      if (u >= ns) break;
+      const int fs = u + kRing - 1;
+      load_slot(fs < ns ? rs : nrs, fs < ns ? fs : fs - ns, ring[fs % kRing]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kk = 0; kk < KPS; ++kk) {
+        const u32x4(&xp)[P] = ring[u % kRing][kk];
+        const u32x4(&gp)[P] = g[u][kk];
+        if constexpr (P == 2) {
+          Sacc = mfma16<BF>(xp[1], gp[0], Sacc);
+          Sacc = mfma16<BF>(xp[0], gp[1], Sacc);
+        }
+        Sacc = mfma16<BF>(xp[0], gp[0], Sacc);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // T_e = S_e^T A per rank tile and dg = colsum(D * T), as in the range kernel
+    float s_sc = 1.f, unscale = 1.f;
+    if constexpr (P == 2) {
+      float mx = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, fabsf(Sacc[v]));
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      const int es = f16_split_exponent(mx);
+      s_sc = ldexpf(1.f, -es);
+      unscale = ldexpf(xs * g_unscale * a_unscale, es);
+    }
+    u32x4 sp[2][P];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      uint32_t wd[P][4];
+#pragma unroll
+      for (int p2 = 0; p2 < 4; ++p2) {
+        const float v0 = Sacc[8 * q + 2 * p2], v1 = Sacc[8 * q + 2 * p2 + 1];
+        if constexpr (P == 2)
+          split_f16x2_pair(v0 * s_sc, v1 * s_sc, wd[0][p2], wd[1][p2]);
+        else
+          wd[0][p2] = pack_bf16x2_rne(v0, v1);
+      }
+#pragma unroll
+      for (int p = 0; p < P; ++p) sp[q][p] = u32x4{wd[p][0], wd[p][1], wd[p][2], wd[p][3]};
+    }
+    u32x4 ap[2][2][P];
+    auto load_a = [&](int rt, int b) {
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int p = 0; p < P; ++p) ap[b][q][p] = sAp[((q * RT + rt) * P + p) * kWave + lane];
+    };
+    load_a(0, 0);
+    float* dgrow = a.dg + size_t(e) * R;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      if (rt + 1 < RT) load_a(rt + 1, (rt + 1) & 1);
+      f32x4 dl[4];
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq) dl[qq] = sDl[(rt * 4 + qq) * kWave + lane];
+      f32x16 T = f32x16{};
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const u32x4(&a_)[P] = ap[rt & 1][q];
+        if constexpr (P == 2) {
+          T = mfma16<BF>(sp[q][1], a_[0], T);
+          T = mfma16<BF>(sp[q][0], a_[1], T);
+        }
+        T = mfma16<BF>(sp[q][0], a_[0], T);
+      }
+      float part = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) part += dl[v / 4][v % 4] * T[v];
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(part), __float_as_uint(part), false, false);
+      part = (__uint_as_float(sw[0]) + __uint_as_float(sw[1])) * unscale;
+      const int r = rt * kTile + l32;
+      if (h == 0 && r < R) dgrow[r] = part;
+    }
+    rs = nrs;
+    if (j + 1 == kBatch) {
+      cur = nxt;
+      b0 += kBatch;
+      nxt = load_batch(b0 + kBatch);
+    }
+  }
 }
 
 // Chunk: the largest of 32, 16, 8 edges whose layout fits the 160 KB of LDS.
-inline int dst2_chunk(int RT, bool bf, int d, int n_radial, int C) {
+inline int dst2_chunk(int RT, bool bf, int d, int n_radial, int C, bool split) {
   int chunk = kMaxChunk;
-  while (chunk > 8 && dst2_smem(RT, bf ? 1 : 2, d, n_radial, C, chunk).floats * 4 > 160 * 1024) chunk >>= 1;
+  while (chunk > 8 && dst2_smem(RT, bf ? 1 : 2, d, n_radial, C, chunk, split).floats * 4 > 160 * 1024) chunk >>= 1;
   return chunk;
+}
+
+// whether the split form applies: Gz[t] in at most 8 ring slots of registers
+inline bool dst2_split(int C, bool bf) { return dg_slots(C, bf ? 1 : 2) <= kDgMaxSlots; }
+
+template <int L, int RT, bool BF>
+hipError_t launch_dg(const BwdDstArgs& a, hipStream_t s) {
+  const size_t lds = size_t(dg_smem_floats(RT, BF ? 1 : 2)) * 4;
+  auto k = k_bwd_dg<L, RT, BF>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     int(lds));
+  if (e != hipSuccess) return e;
+  const int nb = 2 * device_cus();  // two workgroups of four waves per CU
+  k<<<dim3(nb), dim3(kDgWaves * kWave), lds, s>>>(a, nb * kDgWaves);
+  return hipGetLastError();
 }
 
 template <int L, int RT, bool BF>
 hipError_t launch_l_rt(const BwdDstArgs& a, int n_range, hipStream_t s) {
   if (a.pieces_per_block < 1 || n_range % a.pieces_per_block) return hipErrorInvalidValue;
   constexpr int d = (L + 1) * (L + 1);
-  const int chunk = dst2_chunk(RT, BF, d, a.n_radial, a.C);
-  const size_t lds = size_t(dst2_smem(RT, BF ? 1 : 2, d, a.n_radial, a.C, chunk).floats) * 4;
+  // a Gz layout given: the split form, dg first
+  const bool split = a.gzc != nullptr;
+  if (split) {
+    if (!a.dg || (!BF && !a.gz_scale) || !dst2_split(a.C, BF)) return hipErrorInvalidValue;
+    const hipError_t e = launch_dg<L, RT, BF>(a, s);
+    if (e != hipSuccess) return e;
+  }
+  const int chunk = dst2_chunk(RT, BF, d, a.n_radial, a.C, split);
+  const size_t lds = size_t(dst2_smem(RT, BF ? 1 : 2, d, a.n_radial, a.C, chunk, split).floats) * 4;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
-  auto k = k_bwd_dst2<L, RT, BF>;
+  auto k = split ? k_bwd_dst2<L, RT, BF, true> : k_bwd_dst2<L, RT, BF, false>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      int(lds));
   if (e != hipSuccess) return e;

@@ -147,6 +147,9 @@ struct DenseArgs {
 int dense_path_count(int L);
 hipError_t launch_dense_edge(const DenseArgs& a, hipStream_t s);
 
+// out[i] = sum over p = 0 .. n_part - 1 of partial[p][i] (i < n), in a fixed
+// order (sixteen strided partial sums, then those in order)
+hipError_t launch_sum_parts(int n_part, int n, const float* partial, float* out, hipStream_t s);
 // The product without path-weight sharing: every path keeps its own block of
 // output rows, path p (in the order l1, then l2, then l3 ascending) owning
 // rows row[p] .. row[p] + 2 l3[p], n_rows = sum over paths of 2 l3 + 1.
@@ -210,13 +213,22 @@ struct BwdDstArgs {
   const float* x_scale;     // fp32 problems: row_scale of launch_direct_layout
   int n_range;              // equal edge ranges (bwd_dst_plan)
   int pieces_per_block;     // ranges per workgroup
-  float* drho;              // [E, R] by edge id: dL/drho_e, or nullptr (not stored)
+  float* drho;              // [E, R] by edge id: dL/drho_e, or nullptr (not stored); per-segment kernels
+  // range kernel only:
+  float* wrad_part;         // [n_range / pieces_per_block, n_radial, R]: each workgroup's share of
+                            // grad_radial_w (sum them in order), or nullptr
+  const void* gzc;          // Gz in the layout of xc (launch_direct_layout): selects the split form
+  const float* gz_scale;    // fp32 problems: row_scale of that layout
+  float* dg;                // split form: [E, R] dL/dg by sorted edge position (written, then read)
 };
 // Edge ranges of the destination-side kernel on the current device
 // (n_range = 0 when the problem takes the per-segment kernels: d > 32 or no
 // LDS fit): per_block ranges per workgroup, workgroup b taking ranges
 // b, b + n_range / per_block, ...
 EdgePlan bwd_dst_plan(int L, int R, int C, int n_radial, bool bf16, int E);
+// whether the range kernel takes the split form for this channel count (the
+// contraction over channels in a kernel of its own, Gz[t] held in registers)
+bool bwd_dst_split(int L, int C, bool bf16);
 // channel count of its x layout: C padded to the kernel's ring turn
 int bwd_dst_cpad(int C, bool bf16);
 // Channels of the direct kernel's xd layout (d > 32): C rounded up to 64, 128

@@ -487,6 +487,13 @@ int gram_parts(int rows, int C) {
   return p < 1 ? 1 : p;
 }
 
+hipError_t launch_sum_parts(int n_part, int n, const float* partial, float* out, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  if (n_part < 1 || n < 0 || !partial || !out) return hipErrorInvalidValue;
+  k_sum_parts<<<dim3((n + 15) / 16), dim3(256), 0, s>>>(n_part, n, partial, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_path_gemm(int N, int L, int C, const float* zp, const float* W_paths, float* out, hipStream_t s) {
   if (N == 0) return hipSuccess;
   if (L < 0 || L > 6 || C < 1 || !zp || !W_paths || !out) return hipErrorInvalidValue;
