@@ -26,19 +26,63 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
 
+// x[node] ([d, C] values, dC = d C a multiple of 16) into LDS as fp32;
+// returns this thread's largest |x|.  Sixteen-byte loads, four per thread
+// issued before their LDS stores, when the rows are 16-byte aligned; single
+// values otherwise.
+template <typename TI>
+__device__ inline float stage_node(const TI* __restrict__ src, int dC, float* __restrict__ tile) {
+  float mx = 0.f;
+  if ((reinterpret_cast<uintptr_t>(src) & 15) != 0) {
+    for (int i = threadIdx.x; i < dC; i += blockDim.x) {
+      const float v = to_f32(src[i]);
+      tile[i] = v;
+      mx = fmaxf(mx, fabsf(v));
+    }
+    return mx;
+  }
+  constexpr int V = 16 / sizeof(TI);  // values per load
+  const int nv = dC / V;
+  const u32x4* s4 = reinterpret_cast<const u32x4*>(src);
+  for (int i0 = threadIdx.x; i0 < nv; i0 += 4 * blockDim.x) {
+    u32x4 r[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * blockDim.x;
+      r[u] = i < nv ? s4[i] : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * blockDim.x;
+      if (i >= nv) continue;
+      float v[V];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if constexpr (V == 4) {
+          v[j] = __uint_as_float(r[u][j]);
+        } else {
+          v[2 * j] = bf16_to_f32(uint16_t(r[u][j] & 0xffffu));
+          v[2 * j + 1] = bf16_to_f32(uint16_t(r[u][j] >> 16));
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < V; j += 4) {
+        *reinterpret_cast<float4*>(tile + i * V + j) = make_float4(v[j], v[j + 1], v[j + 2], v[j + 3]);
+        mx = fmaxf(mx, fmaxf(fmaxf(fabsf(v[j]), fabsf(v[j + 1])), fmaxf(fabsf(v[j + 2]), fabsf(v[j + 3]))));
+      }
+    }
+  }
+  return mx;
+}
+
 template <int DP, int P, typename TI>
 __global__ __launch_bounds__(256) void k_feature_layout(int d, int C, const TI* __restrict__ x,
                                                         uint16_t* __restrict__ xs, float* __restrict__ row_scale) {
-  extern __shared__ float tile[];  // [d][C], then four floats for the row maximum
+  extern __shared__ __align__(16) float tile[];  // [d][C], then four floats for the row maximum
   float* red = tile + d * C;
   const int n = blockIdx.x;
   const TI* src = x + size_t(n) * d * C;
-  float mx = 0.f;
-  for (int i = threadIdx.x; i < d * C; i += blockDim.x) {
-    const float v = to_f32(src[i]);
-    tile[i] = v;
-    mx = fmaxf(mx, fabsf(v));
-  }
+  float mx = stage_node(src, d * C, tile);
   float sc = 1.f;  // 2^-e_n: the row's largest |x| to [2^13, 2^14) (fp16 parts)
   if constexpr (P == 2) {
 #pragma unroll
@@ -99,16 +143,11 @@ __device__ __forceinline__ _Float16 packed_value(const float* tile, int d, int C
 __global__ __launch_bounds__(256) void k_feature_layout_packed(int d, int C, const float* __restrict__ x,
                                                                uint32_t* __restrict__ xp,
                                                                float* __restrict__ row_scale) {
-  extern __shared__ float tile[];  // [d][C], then four floats for the row maximum
+  extern __shared__ __align__(16) float tile[];  // [d][C], then four floats for the row maximum
   float* red = tile + d * C;
   const int node = blockIdx.x;
   const float* src = x + size_t(node) * d * C;
-  float mx = 0.f;
-  for (int i = threadIdx.x; i < d * C; i += blockDim.x) {
-    const float v = src[i];
-    tile[i] = v;
-    mx = fmaxf(mx, fabsf(v));
-  }
+  float mx = stage_node(src, d * C, tile);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
@@ -168,16 +207,11 @@ hipError_t launch_p(int N, int d, int C, const TI* x, void* xs, float* row_scale
 template <int P, typename TI, bool PERM>
 __global__ __launch_bounds__(256) void k_direct_layout(int d, int C, int Cp, const TI* __restrict__ x,
                                                        uint16_t* __restrict__ xd, float* __restrict__ row_scale) {
-  extern __shared__ float tile[];  // [d][C], then four floats for the row maximum
+  extern __shared__ __align__(16) float tile[];  // [d][C], then four floats for the row maximum
   float* red = tile + d * C;
   const int n = blockIdx.x;
   const TI* src = x + size_t(n) * d * C;
-  float mx = 0.f;
-  for (int i = threadIdx.x; i < d * C; i += blockDim.x) {
-    const float v = to_f32(src[i]);
-    tile[i] = v;
-    mx = fmaxf(mx, fabsf(v));
-  }
+  float mx = stage_node(src, d * C, tile);
   float sc = 1.f;
   if constexpr (P == 2) {
 #pragma unroll
