@@ -77,8 +77,8 @@ __device__ __forceinline__ f32x16 mfma16(u32x4 a, u32x4 b, f32x16 c) {
 __host__ __device__ constexpr int t_row(int q, int h, int i) { return 16 * q + 8 * (i / 4) + 4 * h + (i % 4); }
 
 struct Smem {
-  int Rp, bs, gzs, off_b, off_wr, off_ap, off_d, off_gz, off_v, off_rho, off_y, off_phi, off_dy, off_dphi, off_j,
-      off_idx, floats;
+  int Rp, bs, gzs, off_b, off_wr, off_ap, off_d, off_gz, off_v, off_rho, off_y, off_phi, off_dy, off_dphi, off_w,
+      off_j, off_idx, floats;
 };
 
 // LDS regions (floats): B and Wrad rows (padded stride bs so row-wise
@@ -114,9 +114,11 @@ __host__ __device__ inline Smem dst2_smem(int RT, int P, int d, int n_radial, in
   s.off_phi = o;
   o += chunk * n_radial;
   s.off_dy = o;
-  o += 4 * chunk * d;  // four rank-quarter partials
+  o += 2 * chunk * d;  // two rank-half partials
   s.off_dphi = o;
-  o += 4 * chunk * n_radial;
+  o += 2 * chunk * n_radial;  // two rank-half partials
+  s.off_w = o;  // the workgroup's radial-weight gradient [n_radial][Rp]
+  o += n_radial * s.Rp;
   s.off_j = o;
   o += chunk * 3 * d;
   s.off_idx = o;
@@ -149,6 +151,7 @@ __global__ __launch_bounds__(kWaves* kWave) __attribute__((amdgpu_waves_per_eu(S
   float* sPhi = smem + S.off_phi;
   float* sDY = smem + S.off_dy;
   float* sDPhi = smem + S.off_dphi;
+  float* sW = smem + S.off_w;
   float* sJ = smem + S.off_j;
   int* sIdx = reinterpret_cast<int*>(smem + S.off_idx);  // gathered row
   int* sEid = sIdx + chunk;                             // edge id
@@ -167,12 +170,13 @@ __global__ __launch_bounds__(kWaves* kWave) __attribute__((amdgpu_waves_per_eu(S
   const int h = lane >> 5, l32 = lane & 31;
   const int C = a.C, nr = a.n_radial, R = a.R;
 
-  // ---- factors, once per workgroup
+  // ---- factors, once per workgroup; the radial-gradient sum starts at zero
   for (int i = tid; i < (d + nr) * Rp; i += blockDim.x) {
     const int k = i / Rp, r = i - k * Rp;
     const float v = r < R ? (k < d ? a.Bf[k * R + r] : a.radial_w[(k - d) * R + r]) : 0.f;
     (k < d ? sB + k * bs : sWr + (k - d) * bs)[r] = v;
   }
+  for (int i = tid; i < nr * Rp; i += blockDim.x) sW[i] = 0.f;
   // fp32 problems: the power of two 2^-e_A that puts A's largest |A| in
   // [2^13, 2^14) for its fp16 parts; dg carries 2^e_A back
   float a_sc = 1.f, a_unscale = 1.f;
@@ -224,7 +228,6 @@ __global__ __launch_bounds__(kWaves* kWave) __attribute__((amdgpu_waves_per_eu(S
   }
 
   float gz_unscale = 1.f;  // 2^e_g of the staged Gz (fp32 problems)
-  f32x16 wacc = f32x16{};  // radial-weight gradient [n_radial rows][this wave's rank tile]
   // ---- per edge: S_e, T_e, dg -> dv, drho (in place in sV, sRho)
   // The x operand streams through a ring of kRing slots per wave, kRing - 1
   // slots ahead of the MFMA and on into the wave's next edge of the piece, so
@@ -476,13 +479,24 @@ __global__ __launch_bounds__(kWaves* kWave) __attribute__((amdgpu_waves_per_eu(S
       load_rec(next_eid, nn, next);
       if constexpr (SPLIT) {
         // dg of the chunk's edges (sorted positions cb ..): dv, drho in place
+        // (the loads issued together, then applied)
+        constexpr int kDgPer = kMaxChunk * Rp / (kWaves * kWave);
+        float g[kDgPer];
+#pragma unroll
+        for (int u = 0; u < kDgPer; ++u) {
+          const int i = tid + u * kWaves * kWave;
+          g[u] = i < n * R ? a.dg[size_t(cb) * R + i] : 0.f;
+        }
         __syncthreads();  // v/rho written
-        for (int i = tid; i < n * R; i += blockDim.x) {
-          const int e = i / R, r = i - e * R;
-          const float g = a.dg[size_t(cb + e) * R + r];
-          const float v = sV[e * bs + r], rho = sRho[e * bs + r];
-          sV[e * bs + r] = g * rho;
-          sRho[e * bs + r] = g * v;
+#pragma unroll
+        for (int u = 0; u < kDgPer; ++u) {
+          const int i = tid + u * kWaves * kWave;
+          if (i < n * R) {
+            const int e = i / R, r = i - e * R;
+            const float v = sV[e * bs + r], rho = sRho[e * bs + r];
+            sV[e * bs + r] = g[u] * rho;
+            sRho[e * bs + r] = g[u] * v;
+          }
         }
       }
       // ---- the chunk in segment pieces
@@ -531,39 +545,48 @@ __global__ __launch_bounds__(kWaves* kWave) __attribute__((amdgpu_waves_per_eu(S
         p0 = p1;
       }
       __syncthreads();
-      // ---- dY = dV B^T (k < d), dphi = dRho Wrad^T (q < nr); K = ranks,
-      // one quarter of the ranks per wave, partial products summed in a
-      // fixed order by the gradient below
+      // ---- waves 0-3: dY = dV B^T (k < d) and dphi = dRho Wrad^T (q < nr),
+      // K = ranks, one half of the ranks per wave, partial products summed in
+      // a fixed order by the gradient below.  Waves 4-7: the radial-weight
+      // gradient sum_e phi_e^T drho_e of the chunk (K = its edges) per rank
+      // tile, added to the workgroup's sum in LDS.
       {
-        static_assert(kWaves == 8 && kRing % 2 == 0, "two products x four rank quarters");
-        const bool is_y = wave < 4;
-        const int rq = wave & 3;
-        const int K2 = is_y ? d : nr;
-        const float* src = is_y ? sV : sRho;
-        const float* fac = is_y ? sB : sWr;
-        f32x16 T = f32x16{};
+        static_assert(kWaves == 8, "two products x two rank halves, four radial-gradient waves");
+        if (wave < 4) {
+          const bool is_y = wave < 2;
+          const int hf = wave & 1;
+          const int K2 = is_y ? d : nr;
+          const float* src = is_y ? sV : sRho;
+          const float* fac = is_y ? sB : sWr;
+          f32x16 T = f32x16{};
+#pragma unroll 8
+          for (int s2 = 0; s2 < RT * 8; ++s2) {
+            const int r = hf * (RT * 16) + 2 * s2 + h;
+            const float av = l32 < n ? src[l32 * bs + r] : 0.f;
+            const float bv = l32 < K2 ? fac[l32 * bs + r] : 0.f;
+            T = mfma32(av, bv, T);
+          }
+          float* dstp = is_y ? sDY + hf * chunk * d : sDPhi + hf * chunk * nr;
 #pragma unroll
-        for (int s2 = 0; s2 < RT * 4; ++s2) {
-          const int r = rq * (RT * 8) + 2 * s2 + h;
-          const float av = l32 < n ? src[l32 * bs + r] : 0.f;
-          const float bv = l32 < K2 ? fac[l32 * bs + r] : 0.f;
-          T = mfma32(av, bv, T);
-        }
-        float* dstp = is_y ? sDY + rq * chunk * d : sDPhi + rq * chunk * nr;
+          for (int v = 0; v < 16; ++v) {
+            const int ee = acc_row(v, h);
+            if (ee < n && l32 < K2) dstp[ee * K2 + l32] = T[v];
+          }
+        } else {
+          for (int rt = wave - 4; rt < RT; rt += 4) {
+            f32x16 T = f32x16{};
+#pragma unroll 4
+            for (int s2 = 0; s2 < kMaxChunk / 2; ++s2) {
+              const int e = 2 * s2 + h;
+              const float av = (e < n && l32 < nr) ? sPhi[e * nr + l32] : 0.f;
+              const float bv = e < n ? sRho[e * bs + rt * kTile + l32] : 0.f;
+              T = mfma32(av, bv, T);
+            }
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int ee = acc_row(v, h);
-          if (ee < n && l32 < K2) dstp[ee * K2 + l32] = T[v];
-        }
-        // the radial-weight gradient sum_e phi_e^T drho_e, rank tile `wave`,
-        // accumulated over the workgroup's chunks (K = the chunk's edges)
-        if (wave < RT) {
-#pragma unroll
-          for (int s2 = 0; s2 < kMaxChunk / 2; ++s2) {
-            const int e = 2 * s2 + h;
-            const float av = (e < n && l32 < nr) ? sPhi[e * nr + l32] : 0.f;
-            const float bv = e < n ? sRho[e * bs + wave * kTile + l32] : 0.f;
-            wacc = mfma32(av, bv, wacc);
+            for (int v = 0; v < 16; ++v) {
+              const int q = acc_row(v, h);
+              if (q < nr) sW[q * Rp + rt * kTile + l32] += T[v];
+            }
           }
         }
       }
@@ -580,7 +603,7 @@ __global__ __launch_bounds__(kWaves* kWave) __attribute__((amdgpu_waves_per_eu(S
           const float rn = sqrtf(vx * vx + vy * vy + vz * vz);
           for (int k = sub; k < d; k += TPE) {
             const int i = t * d + k;
-            const float dy = ((sDY[i] + sDY[chunk * d + i]) + sDY[2 * chunk * d + i]) + sDY[3 * chunk * d + i];
+            const float dy = sDY[i] + sDY[chunk * d + i];
             gx += dy * sJ[t * 3 * d + 3 * k];
             gy += dy * sJ[t * 3 * d + 3 * k + 1];
             gzv += dy * sJ[t * 3 * d + 3 * k + 2];
@@ -588,9 +611,7 @@ __global__ __launch_bounds__(kWaves* kWave) __attribute__((amdgpu_waves_per_eu(S
           for (int q = sub; q < nr; q += TPE) {
             const float u = (rn - float(q) * a.sigma) / a.sigma;
             const int i = t * nr + q;
-            const float dphi =
-                ((sDPhi[i] + sDPhi[chunk * nr + i]) + sDPhi[2 * chunk * nr + i]) + sDPhi[3 * chunk * nr + i];
-            dr += dphi * (-u / a.sigma) * sPhi[i];
+            dr += (sDPhi[i] + sDPhi[chunk * nr + i]) * (-u / a.sigma) * sPhi[i];
           }
         }
 #pragma unroll
@@ -616,14 +637,13 @@ __global__ __launch_bounds__(kWaves* kWave) __attribute__((amdgpu_waves_per_eu(S
       rec = next;
     }
   }
-  // this workgroup's partial of the radial-weight gradient
-  if (a.wrad_part && wave < RT) {
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int q = acc_row(v, h), r = wave * kTile + l32;
-      if (q < nr && r < R) a.wrad_part[(size_t(blockIdx.x) * nr + q) * R + r] = wacc[v];
+  // this workgroup's partial of the radial-weight gradient (complete since
+  // the last chunk's barrier after the dY phase)
+  if (a.wrad_part)
+    for (int i = tid; i < nr * R; i += blockDim.x) {
+      const int q = i / R, r = i - q * R;
+      a.wrad_part[size_t(blockIdx.x) * nr * R + i] = sW[q * Rp + r];
     }
-  }
 }
 
 // ---- Split form: the S/T contraction alone, for channel counts whose Gz[t]
