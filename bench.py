@@ -2,7 +2,7 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--no-cpu-baseline] [--backward] [--eager] [--radius-graph]
-                    [--ablation-atomics] [--calibrate-copy] [--no-comparator]
+                    [--ablation-atomics] [--ablations] [--calibrate-copy] [--no-comparator]
                     [--comparator-sweep] [--three-input]
 
 One step is one call of tdn_cp_tp_forward on the headline workload (64
@@ -45,6 +45,11 @@ the per-path channel GEMMs (path_gemm), C <= 128.
 --comparator-sweep adds the same comparison for L = 1..6 on the headline
 graph (C = 128, R = 32 ceil(7 L^2 / 32) capped at 256, random factors):
 the analogue of the paper's speed-up-against-degree figure (Sec. 4.5).
+--ablations adds the forward with the factor blocks read from global memory,
+with the harmonics read from a precomputed table, and with the contraction
+on the vector ALUs (tdn_ablation_forward), each timed beside the product's
+edge kernel (field "ablations"); --ablation-atomics the segmented sum
+replaced by float atomics.
 --three-input adds the three-input CP product (App. A, N = 3: source
 features, edge harmonics, destination features; tdn_cp_tp3_forward) on the
 same workload, timed beside the two-input forward.
@@ -238,6 +243,9 @@ def main():
     ap.add_argument("--backward", action="store_true",
                     help="also time tdn_cp_tp_backward with every gradient (x, W, edge vectors, radial weights; "
                          "extra field)")
+    ap.add_argument("--ablations", action="store_true",
+                    help="time the forward with the factors read from global memory, the harmonics from a "
+                         "precomputed table, and the contraction on the VALU (field 'ablations')")
     ap.add_argument("--ablation-atomics", action="store_true",
                     help="also time the atomic scatter-add forward (extra field; fp32 workloads with 2 <= L <= 4)")
     ap.add_argument("--eager", action="store_true",
@@ -495,6 +503,30 @@ def main():
             "edge_kernel_ms": a_ms / max(1, a_n), "segmented_edge_kernel_ms": edge_ms,
             "edge_kernel_slowdown": a_ms / max(1, a_n) / edge_ms,
             "ms_per_step": a_step, "value": E / (a_step * 1e-3)}
+    if args.ablations and not bf16:
+        # the other hot-path choices, each replaced in turn (tdn_ablation_forward)
+        abl = {}
+        for code, name in ((tdn.ABL_FACTORS_GLOBAL, "factors_global"), (tdn.ABL_Y_TABLE, "y_table"),
+                           (tdn.ABL_VALU, "valu_contraction")):
+            if code == tdn.ABL_VALU and (C > 128 or R > 128):
+                continue
+            pa = tdn.make_problem(w["L"], C, R, N, E, w["r_cut"], w["n_radial"], tdn.TDN_F32, w["presorted"])
+            aws = torch.empty(tdn.ablation_workspace_size(pa, code), dtype=torch.uint8, device=x.device)
+
+            def step_abl(code=code, aws=aws):
+                return tdn.forward(x, vec, ei, At, Bt, Dt, W, rw, L=w["L"], r_cut=w["r_cut"],
+                                   edges_sorted=w["presorted"], workspace=aws, out=out, z=zsave, perm=perm,
+                                   offsets=offsets, ablation=code)
+
+            k_ms, f_ms = time_calls(step_abl, torch, tdn, "cp_edge_fwd_ablation", args.steps)
+            entry = {"edge_kernel_ms": k_ms, "ms_per_step": f_ms, "value": E / (f_ms * 1e-3),
+                     "edge_kernel_slowdown": k_ms / edge_ms}
+            if code == tdn.ABL_Y_TABLE:
+                entry["table_kernel_ms"], _ = time_calls(step_abl, torch, tdn, "sh_table", max(1, args.steps // 4))
+            abl[name] = entry
+            del aws
+        abl["segmented_edge_kernel_ms"] = edge_ms
+        line["ablations"] = abl
     if args.radius_graph:
         # the edges of this workload rebuilt on the device from its atoms
         gi = workloads.graph_inputs(w["name"])

@@ -169,6 +169,34 @@ tdn_status tdn_cp_tp3_forward(const tdn_problem* p, const void* x, const float* 
                               int32_t* perm, int32_t* offsets, void* workspace, size_t workspace_bytes,
                               hipStream_t stream);
 
+/* Measurement ablations of the forward's hot-path choices: the same layer
+ * and arguments as tdn_cp_tp_forward (Sec. 3.1 eq. approximate, Sec. 3.2),
+ * with one choice of the edge pass replaced (the paper attributes its speed
+ * to this kind of kernel-level choice, Sec. 3.2 "coalesced memory access"):
+ *   TDN_ABL_FACTORS_GLOBAL  the factor's packed operand blocks read in the
+ *                           edge loop from a per-workgroup copy in global
+ *                           memory instead of registers or LDS;
+ *   TDN_ABL_Y_TABLE         the edge harmonics precomputed into a workspace
+ *                           table by a kernel of their own and read by the
+ *                           edge kernel instead of evaluated in it;
+ *   TDN_ABL_VALU            the contraction, the segment sum and D in fp32
+ *                           fused multiply-adds on the vector ALUs (one
+ *                           workgroup per destination) instead of fp16 MFMA
+ *                           over two-part splits; R <= 128, C <= 128.
+ * fp32 features (TDN_ERR_BAD_DTYPE), 2 <= L <= 4 and R <= 256
+ * (TDN_ERR_BAD_SHAPE, also for an unknown variant).  Results equal the
+ * forward's to fp32 rounding (deterministic).  The workspace is
+ * tdn_ablation_workspace_size's (the forward's plus the copies or the table).
+ * Not for production use: they exist to be timed against the forward. */
+#define TDN_ABL_FACTORS_GLOBAL 1
+#define TDN_ABL_Y_TABLE 2
+#define TDN_ABL_VALU 3
+tdn_status tdn_ablation_workspace_size(const tdn_problem* p, int32_t variant, size_t* bytes);
+tdn_status tdn_ablation_forward(const tdn_problem* p, int32_t variant, const void* x, const float* edge_vec,
+                                const int32_t* edge_index, const float* A, const float* B, const float* D,
+                                const void* W, const float* radial_w, float* out, float* z_save, int32_t* perm,
+                                int32_t* offsets, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* The exact CG tensor product over the same edges, as the comparator of the
  * CP layer (Sec. 2 eq. clebsch_gordan summed over every path (l1, l2, l3)
  * with l1, l2 <= L and |l1 - l2| <= l3 <= min(l1 + l2, L); Sec. 3.2 for the
@@ -322,7 +350,8 @@ tdn_status tdn_spherical_harmonics(int32_t L, int32_t E, const float* edge_vec, 
  * tdn_timer_enable(1) starts recording every launch of the layer's edge
  * kernels; tdn_timer_read synchronises on the recorded events and returns
  * the summed milliseconds and launch count of the kernel named `kernel`
- * ("cp_edge_fwd", "cp_edge_fwd_atomic", "cp_edge_fwd_t3", "dense_edge_fwd", "dense_edge_unshared",
+ * ("cp_edge_fwd", "cp_edge_fwd_atomic", "cp_edge_fwd_ablation", "sh_table", "cp_edge_fwd_t3",
+ * "dense_edge_fwd", "dense_edge_unshared",
  * "path_gemm", "radius_graph", "feature_layout",
  * "channel_layout", "cp_edge_bwd_src", "cp_bwd_dst", "radial_grad", "node_gemm", "gram",
  * "sort");

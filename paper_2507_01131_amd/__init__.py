@@ -76,6 +76,8 @@ def lib() -> ctypes.CDLL:
         L.tdn_cp_tp3_forward.argtypes = [PP] + [_P] * 14 + [_SZ, _P]
         L.tdn_dense_tp_forward.argtypes = [PP] + [_P] * 6 + [ctypes.c_int32] + [_P] * 7 + [_SZ, _P]
         L.tdn_dense_tp_unshared_workspace_size.argtypes = [PP, ctypes.POINTER(_SZ)]
+        L.tdn_ablation_workspace_size.argtypes = [PP, ctypes.c_int32, ctypes.POINTER(_SZ)]
+        L.tdn_ablation_forward.argtypes = [PP, ctypes.c_int32] + [_P] * 13 + [_SZ, _P]
         L.tdn_dense_tp_forward_unshared.argtypes = [PP] + [_P] * 6 + [ctypes.c_int32] + [_P] * 6 + [_SZ, _P]
         GP = ctypes.POINTER(GraphProblem)
         L.tdn_radius_graph_workspace_size.argtypes = [GP, ctypes.POINTER(_SZ)]
@@ -95,7 +97,8 @@ def lib() -> ctypes.CDLL:
                   "tdn_sort_workspace_size", "tdn_sort_by_key", "tdn_spherical_harmonics", "tdn_timer_enable",
                   "tdn_timer_read", "tdn_radius_graph_workspace_size", "tdn_radius_graph", "tdn_dense_tp_forward",
                   "tdn_cp_tp3_forward", "tdn_ps_linear_workspace_size", "tdn_ps_linear",
-                  "tdn_dense_tp_unshared_workspace_size", "tdn_dense_tp_forward_unshared"):
+                  "tdn_dense_tp_unshared_workspace_size", "tdn_dense_tp_forward_unshared",
+                  "tdn_ablation_workspace_size", "tdn_ablation_forward"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -157,13 +160,15 @@ class ForwardResult:
 
 def forward(x, edge_vec, edge_index, A, B, D, W, radial_w, *, L: int, r_cut: float, edges_sorted=False,
             validate=False, save_z=True, workspace=None, out=None, z=None, perm=None, offsets=None,
-            stream=None, atomics_ablation=False) -> ForwardResult:
+            stream=None, atomics_ablation=False, ablation=0) -> ForwardResult:
     """Runs tdn_cp_tp_forward.  x [N,d,C] and W [C,C] are float32 or bfloat16
     (both the same); edge_index [2,E] int32 (int64 is converted); everything
     else float32 on the same device.  out, z, perm, offsets and workspace may
     be passed preallocated; otherwise they are allocated here.
     atomics_ablation=True runs tdn_ablation_forward_atomics instead (the
-    per-edge atomic scatter-add the segmented sum replaces; fp32, 2 <= L <= 4)."""
+    per-edge atomic scatter-add the segmented sum replaces; fp32, 2 <= L <= 4);
+    ablation=ABL_FACTORS_GLOBAL, ABL_Y_TABLE or ABL_VALU runs
+    tdn_ablation_forward with that variant."""
     dev = x.device
     N, d, C = x.shape
     E = edge_vec.shape[0]
@@ -180,7 +185,10 @@ def forward(x, edge_vec, edge_index, A, B, D, W, radial_w, *, L: int, r_cut: flo
     if x.dtype not in (torch.float32, torch.bfloat16):
         raise TypeError("x must be float32 or bfloat16")
     p = make_problem(L, C, R, N, E, r_cut, radial_w.shape[0], fd, edges_sorted, validate)
-    fwd_bytes, _ = workspace_size(p)
+    if ablation:
+        fwd_bytes = ablation_workspace_size(p, ablation)
+    else:
+        fwd_bytes, _ = workspace_size(p)
     if workspace is None or workspace.numel() < fwd_bytes:
         workspace = torch.empty(max(fwd_bytes, 1), dtype=torch.uint8, device=dev)
     if out is None:
@@ -196,14 +204,31 @@ def forward(x, edge_vec, edge_index, A, B, D, W, radial_w, *, L: int, r_cut: flo
         _need(z, "z", torch.float32, (N, d, C), dev)
     _need(perm, "perm", torch.int32, (E,), dev)
     _need(offsets, "offsets", torch.int32, (N + 1,), dev)
-    name = "tdn_ablation_forward_atomics" if atomics_ablation else "tdn_cp_tp_forward"
-    st = getattr(lib(), name)(ctypes.byref(p), _ptr(x), _ptr(edge_vec), _ptr(edge_index), _ptr(A), _ptr(B),
-                              _ptr(D), _ptr(W), _ptr(radial_w), _ptr(out), _ptr(z), _ptr(perm), _ptr(offsets),
-                              _ptr(workspace), workspace.numel(), _stream(stream))
+    if ablation:
+        name = "tdn_ablation_forward"
+        st = lib().tdn_ablation_forward(ctypes.byref(p), int(ablation), _ptr(x), _ptr(edge_vec), _ptr(edge_index),
+                                        _ptr(A), _ptr(B), _ptr(D), _ptr(W), _ptr(radial_w), _ptr(out), _ptr(z),
+                                        _ptr(perm), _ptr(offsets), _ptr(workspace), workspace.numel(),
+                                        _stream(stream))
+    else:
+        name = "tdn_ablation_forward_atomics" if atomics_ablation else "tdn_cp_tp_forward"
+        st = getattr(lib(), name)(ctypes.byref(p), _ptr(x), _ptr(edge_vec), _ptr(edge_index), _ptr(A), _ptr(B),
+                                  _ptr(D), _ptr(W), _ptr(radial_w), _ptr(out), _ptr(z), _ptr(perm), _ptr(offsets),
+                                  _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, name)
     return ForwardResult(out, z, perm, offsets, p,
                          dict(x=x, edge_vec=edge_vec, edge_index=edge_index, A=A, B=B, D=D, W=W, radial_w=radial_w))
 
+
+ABL_FACTORS_GLOBAL, ABL_Y_TABLE, ABL_VALU = 1, 2, 3
+
+
+def ablation_workspace_size(p: Problem, variant: int) -> int:
+    """Workspace bytes of tdn_ablation_forward for this problem and variant."""
+    nb = _SZ(0)
+    _check(lib().tdn_ablation_workspace_size(ctypes.byref(p), int(variant), ctypes.byref(nb)),
+           "tdn_ablation_workspace_size")
+    return nb.value
 
 NOALLOC_SCRATCH_BYTES = 32 << 20
 

@@ -460,6 +460,91 @@ tdn_status tdn_ablation_forward_atomics(const tdn_problem* p, const void* x, con
                       workspace_bytes, stream, true);
 }
 
+namespace {
+// The measurement ablations' extra workspace after the forward's: the
+// per-workgroup factor copies, or the harmonics table.
+size_t abl_extra_bytes(const tdn_problem& p, int variant) {
+  if (variant == tdn::kAblFactorsGlobal) {
+    const tdn::EdgePlan pl = tdn::edge_plan(p.L, p.R, p.C, p.n_radial, false, p.n_edges);
+    return al(tdn::edge_abl_fa_bytes(p.L, p.R, p.C, pl.n_range, pl.per_block));
+  }
+  if (variant == tdn::kAblYTable) return al(size_t(p.n_edges) * dim_of(p.L) * 4);
+  return 0;
+}
+tdn_status check_ablation(const tdn_problem* p, int32_t variant) {
+  const tdn_status st = check_problem(p);
+  if (st != TDN_OK) return st;
+  if (variant != tdn::kAblFactorsGlobal && variant != tdn::kAblYTable && variant != tdn::kAblValu)
+    return TDN_ERR_BAD_SHAPE;
+  if (p->feat_dtype != TDN_F32) return TDN_ERR_BAD_DTYPE;
+  if (p->L < 2 || p->L > 4 || p->R > kChunkR) return TDN_ERR_BAD_SHAPE;
+  if (variant == tdn::kAblValu && (p->R > 128 || p->C > 128)) return TDN_ERR_BAD_SHAPE;
+  return TDN_OK;
+}
+}  // namespace
+
+tdn_status tdn_ablation_workspace_size(const tdn_problem* p, int32_t variant, size_t* bytes) {
+  const tdn_status st = check_ablation(p, variant);
+  if (st != TDN_OK) return st;
+  if (!bytes) return TDN_ERR_NULL_POINTER;
+  *bytes = fwd_layout(*p).total + abl_extra_bytes(*p, variant);
+  return TDN_OK;
+}
+
+tdn_status tdn_ablation_forward(const tdn_problem* p, int32_t variant, const void* x, const float* edge_vec,
+                                const int32_t* edge_index, const float* A, const float* B, const float* D,
+                                const void* W, const float* radial_w, float* out, float* z_save, int32_t* perm,
+                                int32_t* offsets, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  tdn_status st = check_ablation(p, variant);
+  if (st != TDN_OK) return st;
+  const int N = p->n_nodes, E = p->n_edges, d = dim_of(p->L), C = p->C;
+  if (!A || !B || !D || !W || !radial_w || !offsets || !workspace) return TDN_ERR_NULL_POINTER;
+  if (N > 0 && (!x || !out)) return TDN_ERR_NULL_POINTER;
+  if (E > 0 && (!edge_vec || !edge_index || !perm)) return TDN_ERR_NULL_POINTER;
+  const FwdLayout lay = fwd_layout(*p);
+  if (workspace_bytes < lay.total + abl_extra_bytes(*p, variant)) return TDN_ERR_WORKSPACE_TOO_SMALL;
+  st = check_device();
+  if (st != TDN_OK) return st;
+  char* ws = static_cast<char*>(workspace);
+  if (p->validate) {
+    st = run_validation(*p, edge_index, edge_vec, ws, lay.flags, p->edges_sorted, stream);
+    if (st != TDN_OK) return st;
+  }
+  const int32_t* src = edge_index;
+  const int32_t* dst = E > 0 ? edge_index + E : nullptr;
+  {
+    Timed t("sort", stream);
+    if (p->edges_sorted || E == 0)
+      TDN_HIP(tdn::launch_offsets_presorted(N, E, dst, perm, offsets, stream));
+    else
+      TDN_HIP(tdn::launch_sort(tdn::sort_plan(N, E), dst, 1, perm, offsets, ws + lay.sort, stream));
+  }
+  if (N == 0) return TDN_OK;
+  float* Z = z_save ? z_save : reinterpret_cast<float*>(ws + lay.z);
+  float* partial = reinterpret_cast<float*>(ws + lay.part);
+  tdn::EdgeArgs a = edge_args(*p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, ws + lay.xt, Z, partial);
+  if (variant != tdn::kAblValu) {
+    Timed t("feature_layout", stream);
+    TDN_HIP(edge_features(*p, x, true, ws + lay.xt, stream));
+  }
+  if (variant == tdn::kAblFactorsGlobal) a.fa_global = ws + lay.total;
+  if (variant == tdn::kAblYTable && E > 0) {
+    float* yt = reinterpret_cast<float*>(ws + lay.total);
+    Timed t("sh_table", stream);
+    TDN_HIP(tdn::launch_sh(p->L, E, edge_vec, yt, nullptr, stream));
+    a.y_table = yt;
+  }
+  {
+    Timed t("cp_edge_fwd_ablation", stream);
+    TDN_HIP(tdn::launch_cp_edge_ablation(a, variant, static_cast<const float*>(x), stream));
+  }
+  {
+    Timed t("node_gemm", stream);
+    TDN_HIP(tdn::launch_node_gemm(N * d, C, Z, W, false, 0, out, ws + lay.wp, stream));
+  }
+  return TDN_OK;
+}
+
 tdn_status tdn_cp_tp3_forward(const tdn_problem* p, const void* x, const float* edge_vec, const int32_t* edge_index,
                               const float* A, const float* A2, const float* B, const float* D, const void* W,
                               const float* radial_w, float* out, float* z_save, int32_t* perm, int32_t* offsets,

@@ -11,7 +11,7 @@
 namespace tdn {
 namespace edge_detail {
 // Instantiated in their own translation units (cp_edge_l<L>.hip,
-// cp_edge_atomic.hip, cp_edge_t3.hip); declared here so that this file does
+// cp_edge_ablations.hip, cp_edge_t3.hip); declared here so that this file does
 // not compile the kernels again.
 extern template hipError_t launch_cp_edge_l<0>(const EdgeArgs&, hipStream_t);
 extern template hipError_t launch_cp_edge_l<1>(const EdgeArgs&, hipStream_t);
@@ -26,6 +26,13 @@ extern template hipError_t launch_cp_edge_atomic_l<4>(const EdgeArgs&, hipStream
 extern template hipError_t launch_cp_edge_t3_l<2>(const EdgeArgs&, hipStream_t);
 extern template hipError_t launch_cp_edge_t3_l<3>(const EdgeArgs&, hipStream_t);
 extern template hipError_t launch_cp_edge_t3_l<4>(const EdgeArgs&, hipStream_t);
+#define TDN_ABL_EXTERN(LV)                                                          \
+  extern template hipError_t launch_cp_edge_abl_l<LV, 1>(const EdgeArgs&, hipStream_t); \
+  extern template hipError_t launch_cp_edge_abl_l<LV, 2>(const EdgeArgs&, hipStream_t);
+TDN_ABL_EXTERN(2)
+TDN_ABL_EXTERN(3)
+TDN_ABL_EXTERN(4)
+#undef TDN_ABL_EXTERN
 
 namespace {
 
@@ -218,6 +225,45 @@ hipError_t launch_cp_edge_t3(const EdgeArgs& a, hipStream_t s) {
     case 2: e = launch_cp_edge_t3_l<2>(a, s); break;
     case 3: e = launch_cp_edge_t3_l<3>(a, s); break;
     default: e = launch_cp_edge_t3_l<4>(a, s); break;
+  }
+  if (e != hipSuccess) return e;
+  if (a.n_seg > 0)
+    k_range_fixup<<<dim3(a.n_seg), dim3(256), 0, s>>>(a.E, a.n_range, a.d * a.C, a.offsets, a.partial, a.out);
+  return hipGetLastError();
+}
+
+size_t edge_abl_fa_bytes(int L, int R, int C, int n_range, int pieces_per_block) {
+  using namespace edge_detail;
+  const int d = (L + 1) * (L + 1), RT = (R + kTile - 1) / kTile;
+  if (pieces_per_block < 1) return 0;
+  const size_t blocks = size_t(n_range / pieces_per_block) * edge_grid(C, RT, false).n_cgrp;
+  return blocks * pk_blocks(d) * RT * kWave * 16;
+}
+
+hipError_t launch_cp_edge_ablation(const EdgeArgs& a, int variant, const float* x_f32, hipStream_t s) {
+  using namespace edge_detail;
+  if (a.L < 2 || a.L > 4) return hipErrorInvalidValue;
+  if (variant == kAblValu) return launch_cp_edge_valu(a, x_f32, s);
+  if (variant != kAblFactorsGlobal && variant != kAblYTable) return hipErrorInvalidValue;
+  if (a.parts != 2) return hipErrorInvalidValue;
+  if ((variant == kAblFactorsGlobal && !a.fa_global) || (variant == kAblYTable && a.E > 0 && !a.y_table))
+    return hipErrorInvalidValue;
+  if (a.E > 0 && (a.n_range < 1 || a.n_range > a.E || a.pieces_per_block < 1 || a.n_range % a.pieces_per_block ||
+                  !a.ef_ops || !a.ef_scale || !a.row_scale))
+    return hipErrorInvalidValue;
+  hipError_t e = hipSuccess;
+  if (a.E > 0) {
+    const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
+    k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops),
+                                                  a.ef_scale);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const bool fg = variant == kAblFactorsGlobal;
+  switch (a.L) {
+    case 2: e = fg ? launch_cp_edge_abl_l<2, 1>(a, s) : launch_cp_edge_abl_l<2, 2>(a, s); break;
+    case 3: e = fg ? launch_cp_edge_abl_l<3, 1>(a, s) : launch_cp_edge_abl_l<3, 2>(a, s); break;
+    default: e = fg ? launch_cp_edge_abl_l<4, 1>(a, s) : launch_cp_edge_abl_l<4, 2>(a, s); break;
   }
   if (e != hipSuccess) return e;
   if (a.n_seg > 0)

@@ -182,7 +182,12 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radi
 // V_t is the same for every edge of the segment, so it multiplies the
 // accumulated sum once, in the epilogue (also for partial segments: the
 // epilogue is linear in the sum).
-template <int L, int RT, bool BF, bool ATOM = false, bool T3 = false>
+//
+// ABL (measurement ablations, launch_cp_edge_ablation): 1 reads the packed
+// factor blocks in the edge loop from a per-workgroup copy in global memory
+// (written after staging) instead of registers or LDS; 2 reads the harmonics
+// from a precomputed per-edge table instead of evaluating them.
+template <int L, int RT, bool BF, bool ATOM = false, bool T3 = false, int ABL = 0>
 __global__ __launch_bounds__(kMaxWavesPerBlock* kWave)
 __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edge(EdgeArgs a, int n_cgrp, int waves,
                                                                                   int chunk) {
@@ -198,7 +203,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   // per lane and edge loaded as PQ quads and a PT-word tail
   constexpr int PN = pk_rows(d), PB = pk_blocks(d), PQ = PN / 4, PT = PN % 4;
   extern __shared__ float smem[];
-  constexpr bool kRegA = edge_rega(L, RT, BF);
+  constexpr bool kRegA = edge_rega(L, RT, BF) && ABL != 1;
   const EdgeSmem S = edge_smem(RT, BF, d, a.n_radial, chunk, T3, kRegA);
   u32x4* sA = reinterpret_cast<u32x4*>(smem + S.off_a);
   u32x4* sA2 = reinterpret_cast<u32x4*>(smem + S.off_a2);
@@ -297,6 +302,12 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   } else {
     for (int t = tid; t < PB * RT * kWave; t += blockDim.x) stage_packed(a.KF, kf_sc, t, sA);
   }
+  // ABL 1: this workgroup's copy of the staged blocks in global memory
+  u32x4* gA = ABL == 1 ? static_cast<u32x4*>(a.fa_global) + size_t(blockIdx.x) * PB * RT * kWave : nullptr;
+  if constexpr (ABL == 1) {
+    __syncthreads();
+    for (int t = tid; t < PB * RT * kWave; t += blockDim.x) gA[t] = sA[t];
+  }
   __syncthreads();
   // Split mode with kRegA: every packed factor block is loaded into
   // registers at the start of each run of edges of one segment within a chunk
@@ -306,7 +317,12 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   // copy (zero added in inline asm) so that the compiler does not hoist the
   // reads out of the loops; the pointer itself stays a known LDS pointer.
   u32x4 areg[kRegA ? PB * RT : 1];
-  auto a_op = [&](int base, int b, int rt) -> u32x4 { return sA[base + (b * RT + rt) * kWave]; };
+  auto a_op = [&](int base, int b, int rt) -> u32x4 {
+    if constexpr (ABL == 1)
+      return gA[base + (b * RT + rt) * kWave];
+    else
+      return sA[base + (b * RT + rt) * kWave];
+  };
   float* sTr = smem + S.off_t + wave * kTrFloats;  // split mode: this wave's transpose area
 
   // Feature operands of one edge.  Split mode: the lane's PN packed words of
@@ -645,9 +661,17 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
       __syncthreads();
       // harmonics: one thread per edge (all degrees, unrolled); radial basis: one
       // thread per (edge, function)
-      for (int t = tid; t < n; t += blockDim.x) {
-        const float4 u = sVec[t];
-        sh_unit_all<L>(u.x, u.y, u.z, sY + t * d);
+      if constexpr (ABL == 2) {
+        for (int t = tid; t < n; t += blockDim.x) {
+          const float* yr = a.y_table + size_t(a.perm[cb + t]) * d;
+#pragma unroll
+          for (int k = 0; k < d; ++k) sY[t * d + k] = yr[k];
+        }
+      } else {
+        for (int t = tid; t < n; t += blockDim.x) {
+          const float4 u = sVec[t];
+          sh_unit_all<L>(u.x, u.y, u.z, sY + t * d);
+        }
       }
       for (int t = tid; t < n * nr; t += blockDim.x) {
         const int e = t / nr, q = t - e * nr;
@@ -761,7 +785,7 @@ inline EdgeGrid edge_grid(int C, int RT, bool bf) {
   return EdgeGrid{waves, (wave_tiles + waves - 1) / waves};
 }
 
-template <int L, int RT, bool BF, bool ATOM = false, bool T3 = false>
+template <int L, int RT, bool BF, bool ATOM = false, bool T3 = false, int ABL = 0>
 hipError_t launch_l_rt_m(const EdgeArgs& a, hipStream_t s) {
   constexpr int d = (L + 1) * (L + 1);
   const EdgeGrid gr = edge_grid(a.C, RT, BF);
@@ -769,7 +793,7 @@ hipError_t launch_l_rt_m(const EdgeArgs& a, hipStream_t s) {
   if (a.E > 0) {
     const int chunk = edge_chunk(L, RT, BF, a.n_radial, T3);
     const size_t lds = size_t(edge_smem(RT, BF, d, a.n_radial, chunk, T3, edge_rega(L, RT, BF)).floats) * 4;
-    auto k = k_cp_edge<L, RT, BF, ATOM, T3>;
+    auto k = k_cp_edge<L, RT, BF, ATOM, T3, ABL>;
     hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
@@ -810,6 +834,22 @@ hipError_t launch_cp_edge_atomic_l(const EdgeArgs& a, hipStream_t s) {
     case 6: return launch_l_rt_m<L, 6, false, true>(a, s);
     case 7: return launch_l_rt_m<L, 7, false, true>(a, s);
     case 8: return launch_l_rt_m<L, 8, false, true>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// The ablations' dispatch on the rank tiles (fp32 features only).
+template <int L, int ABL>
+hipError_t launch_cp_edge_abl_l(const EdgeArgs& a, hipStream_t s) {
+  switch ((a.R + kTile - 1) / kTile) {
+    case 1: return launch_l_rt_m<L, 1, false, false, false, ABL>(a, s);
+    case 2: return launch_l_rt_m<L, 2, false, false, false, ABL>(a, s);
+    case 3: return launch_l_rt_m<L, 3, false, false, false, ABL>(a, s);
+    case 4: return launch_l_rt_m<L, 4, false, false, false, ABL>(a, s);
+    case 5: return launch_l_rt_m<L, 5, false, false, false, ABL>(a, s);
+    case 6: return launch_l_rt_m<L, 6, false, false, false, ABL>(a, s);
+    case 7: return launch_l_rt_m<L, 7, false, false, false, ABL>(a, s);
+    case 8: return launch_l_rt_m<L, 8, false, false, false, ABL>(a, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -60,6 +60,9 @@ struct EdgeArgs {
   float* ef_scale;           // inside ef_ops: 2^e of EF's fp16 parts (parts = 2)
   int parts;                 // 16-bit parts per feature in feat (2: fp32 features as fp16 hi + lo, 1: bf16)
   const float* row_scale;    // [n_feat_rows] 2^e of each feat row (parts = 2), from launch_feature_layout
+  // measurement ablations only (launch_cp_edge_ablation):
+  void* fa_global;           // factors from global memory: per workgroup a copy of its packed factor blocks
+  const float* y_table;      // harmonics table: [E, d] Y of each edge by edge id (launch_sh)
 };
 // Edge ranges of the pass for this problem on the current device:
 // n_range = per_block x the number of workgroups the device holds at once
@@ -113,6 +116,25 @@ hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
 // per edge and Z accumulated into `out` (zeroed first) with float atomics;
 // nondeterministic in the order of the additions.
 hipError_t launch_cp_edge_atomic(const EdgeArgs& a, hipStream_t s);
+// Measurement ablations of the edge pass (fp32 features, 2 <= L <= 4, one
+// rank chunk), each with one hot-path choice replaced:
+//   kAblFactorsGlobal: the packed factor blocks read in the edge loop from a
+//     per-workgroup copy in global memory (a.fa_global, edge_abl_fa_bytes)
+//     instead of registers or LDS;
+//   kAblYTable: the harmonics read from a precomputed table (a.y_table)
+//     instead of evaluated in the kernel;
+//   kAblValu: the contraction, the segment sum and D on the vector ALUs in
+//     fp32 (one workgroup per destination, R <= 128, C <= 128), reading x
+//     itself (x_f32 [N, d, C]) instead of the packed split words.
+// The first two keep everything else of launch_cp_edge.
+constexpr int kAblFactorsGlobal = 1, kAblYTable = 2, kAblValu = 3;
+hipError_t launch_cp_edge_ablation(const EdgeArgs& a, int variant, const float* x_f32, hipStream_t s);
+size_t edge_abl_fa_bytes(int L, int R, int C, int n_range, int pieces_per_block);
+// kAblValu's kernel: out[t] = D sum_e diag(g_e) A^T x[src_e] per destination t
+// in fp32 FMA (L <= 4, R <= 128, C <= 128), zero rows for nodes without
+// edges; a.KF = A, a.EF = D, a.Bf, a.radial_w, a.offsets, a.perm, a.gather,
+// a.edge_vec as for launch_cp_edge.
+hipError_t launch_cp_edge_valu(const EdgeArgs& a, const float* x, hipStream_t s);
 // The three-input product (App. A, N = 3: source features, edge harmonics,
 // destination features): as launch_cp_edge, with each segment's sum
 // multiplied by V_t = KF2^T x[t] (t = the segment's node, a row of feat)

@@ -272,3 +272,35 @@ def test_noalloc_forward_rejects_problems_beyond_its_scratch():
     assert st == 13 and tdn.STATUS[st] == "TDN_ERR_SCRATCH_LIMIT"
     bad = tdn.make_problem(4, 100, 128, 10, 10, 6.0)     # C not a multiple of 16
     assert L.tdn_cp_tp_forward_noalloc(ctypes.byref(bad), *([None] * 12), None) == 2
+
+
+def _abl(p, variant, ws_bytes=1 << 40, **override):
+    args = dict(x=FAKE, vec=FAKE, ei=FAKE, A=FAKE, B=FAKE, D=FAKE, W=FAKE, rw=FAKE, out=FAKE, z=None, perm=FAKE,
+                off=FAKE, ws=FAKE)
+    args.update(override)
+    return tdn.lib().tdn_ablation_forward(None if p is None else ctypes.byref(p), variant, args["x"], args["vec"],
+                                          args["ei"], args["A"], args["B"], args["D"], args["W"], args["rw"],
+                                          args["out"], args["z"], args["perm"], args["off"], args["ws"], ws_bytes,
+                                          None)
+
+
+@pytest.mark.parametrize("variant", [tdn.ABL_FACTORS_GLOBAL, tdn.ABL_Y_TABLE, tdn.ABL_VALU])
+def test_ablation_forward_argument_checks(variant):
+    good = _problem(L=4, C=128, R=128)
+    need = ctypes.c_size_t(0)
+    assert tdn.lib().tdn_ablation_workspace_size(ctypes.byref(good), variant, ctypes.byref(need)) == 0
+    fwd, _ = tdn.workspace_size(good)
+    assert need.value >= fwd
+    if variant == tdn.ABL_Y_TABLE:      # one row of d harmonics per edge
+        assert need.value >= fwd + 1000 * 25 * 4
+    assert _abl(good, variant, ws_bytes=need.value - 1) == 4
+    assert _abl(good, 0) == 2 and _abl(good, 4) == 2
+    assert _abl(_problem(L=1, R=32), variant) == 2
+    assert _abl(_problem(L=5, R=32), variant) == 2
+    assert _abl(_problem(L=4, R=300), variant) == 2
+    assert _abl(_problem(L=4, feat_dtype=tdn.TDN_BF16), variant) == 3
+    if variant == tdn.ABL_VALU:
+        assert _abl(_problem(L=4, C=160), variant) == 2   # R, C <= 128
+    assert _abl(None, variant) == 1
+    for k in ["x", "vec", "ei", "A", "B", "D", "W", "rw", "out", "perm", "off", "ws"]:
+        assert _abl(good, variant, **{k: None}) == 1, k

@@ -395,3 +395,59 @@ def test_atomics_ablation_rejects_unsupported_problems():
     with pytest.raises(tdn.TdnError) as ei:
         _fwd(w, A, B, D, atomics_ablation=True)
     assert ei.value.status == 3
+
+
+# ------------------------------------------------------------ other hot-path ablations
+ABLATIONS = [(tdn.ABL_FACTORS_GLOBAL, "factors_global"), (tdn.ABL_Y_TABLE, "y_table"), (tdn.ABL_VALU, "valu")]
+
+
+@pytest.mark.parametrize("abl", ABLATIONS, ids=lambda v: v[1])
+@pytest.mark.parametrize("cfg", ATOMIC_SMALL, ids=lambda c: f"L{c['L']}C{c['C']}R{c['R']}s{c['seed']}")
+def test_ablation_variants_small_full(cfg, abl):
+    if abl[0] == tdn.ABL_VALU and (cfg["C"] > 128 or cfg["R"] > 128):
+        pytest.skip("the VALU ablation covers R, C <= 128")
+    w, (A, B, D) = _small(cfg)
+    res = _fwd(w, A, B, D, ablation=abl[0])
+    ref, zref = layer.forward(w["x"], w["edge_index"], w["edge_vec"], A, B, D, w["W"], w["radial_w"], w["r_cut"],
+                              w["L"], return_z=True)
+    rp, ro = layer.stable_sort_by_key(w["edge_index"][1], w["N"])
+    np.testing.assert_array_equal(res.perm.cpu().numpy(), rp)
+    np.testing.assert_array_equal(res.offsets.cpu().numpy(), ro)
+    assert rel_err(res.out.cpu(), ref) < TOL_F32
+    check_rows(res.z.cpu().numpy(), zref, TOL_F32, "z")
+
+
+@pytest.mark.parametrize("abl", ABLATIONS, ids=lambda v: v[1])
+def test_ablation_variants_headline_size_sampled(abl):
+    w = workload("molecules3200_L4_C128_R128")
+    A, B, D = load_factors(w["L"], w["R"])
+    seg = _fwd(w, A, B, D)
+    res = _fwd(w, A, B, D, ablation=abl[0])
+    out = res.out.cpu().numpy()
+    assert np.all(np.isfinite(out))
+    nodes = sample_nodes(w, 24)
+    ref = layer.forward_at_nodes(nodes, w["x"], w["edge_index"], w["edge_vec"], A, B, D, w["W"], w["radial_w"],
+                                 w["r_cut"], w["L"])
+    assert rel_err(out[nodes], ref) < TOL_F32
+    check_rows(out[nodes], ref, TOL_F32, "out")
+    if abl[0] == tdn.ABL_FACTORS_GLOBAL:
+        # the same arithmetic, only the factor operands' source differs: identical bits
+        np.testing.assert_array_equal(out, seg.out.cpu().numpy())
+    else:
+        # the table's harmonics come from the stage kernel (the degree a
+        # runtime argument), the VALU variant sums in another order
+        assert rel_err(res.out.cpu(), seg.out.cpu().numpy().astype(np.float64)) < TOL_F32
+
+
+def test_ablation_variants_reject_unsupported_problems():
+    w = workloads.random_graph(13, n_nodes=10, n_edges=50, L=4, C=160, R=32)
+    A, B, D = random_factors(4, 32, 13)
+    with pytest.raises(tdn.TdnError) as ei:
+        _fwd(w, A, B, D, ablation=tdn.ABL_VALU)
+    assert ei.value.status == 2
+    w = workloads.random_graph(14, n_nodes=10, n_edges=50, L=1, C=32, R=32)
+    A, B, D = random_factors(1, 32, 14)
+    for v in (tdn.ABL_FACTORS_GLOBAL, tdn.ABL_Y_TABLE, tdn.ABL_VALU, 7):
+        with pytest.raises(tdn.TdnError) as ei:
+            _fwd(w, A, B, D, ablation=v)
+        assert ei.value.status == 2
