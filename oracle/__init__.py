@@ -24,6 +24,10 @@ Modules
             of the CP layer (Sec. 2 eq. clebsch_gordan, Sec. 3.2), with the
             shared channel weight or with one channel weight per path (the
             product without path-weight sharing)
+  attention the graph-attention block that consumes the CP messages (one
+            reading of Sec. 4.1 "Model Design": MLP attention logits from
+            invariant edge inputs, a softmax over each destination's edges
+            per head, the heads weighting channel blocks of the messages)
   radius_graph
             the edges the layer consumes: every atom pair of a system (and
             its periodic images) closer than the cutoff, with an optional
