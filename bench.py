@@ -2,7 +2,8 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--no-cpu-baseline] [--backward] [--eager] [--radius-graph]
-                    [--ablation-atomics] [--ablations] [--calibrate-copy] [--no-comparator]
+                    [--ablation-atomics] [--ablations] [--attention] [--calibrate-copy]
+                    [--no-comparator]
                     [--comparator-sweep] [--three-input]
 
 One step is one call of tdn_cp_tp_forward on the headline workload (64
@@ -50,6 +51,10 @@ with the harmonics read from a precomputed table, and with the contraction
 on the vector ALUs (tdn_ablation_forward), each timed beside the product's
 edge kernel (field "ablations"); --ablation-atomics the segmented sum
 replaced by float atomics.
+--attention adds the attention block (tdn_attention_forward: attention
+weights from invariant edge inputs, softmax per destination and head, the
+messages weighted per head inside the edge pass; 4 heads, 32 hidden units)
+timed beside the plain forward (field "attention").
 --three-input adds the three-input CP product (App. A, N = 3: source
 features, edge harmonics, destination features; tdn_cp_tp3_forward) on the
 same workload, timed beside the two-input forward.
@@ -243,6 +248,8 @@ def main():
     ap.add_argument("--backward", action="store_true",
                     help="also time tdn_cp_tp_backward with every gradient (x, W, edge vectors, radial weights; "
                          "extra field)")
+    ap.add_argument("--attention", action="store_true",
+                    help="time the attention block over the same messages (field 'attention')")
     ap.add_argument("--ablations", action="store_true",
                     help="time the forward with the factors read from global memory, the harmonics from a "
                          "precomputed table, and the contraction on the VALU (field 'ablations')")
@@ -527,6 +534,28 @@ def main():
             del aws
         abl["segmented_edge_kernel_ms"] = edge_ms
         line["ablations"] = abl
+    if args.attention and not bf16 and 1 <= w["L"] <= 4 and R <= 256 and C % 128 == 0:
+        # the attention block over the same messages: 4 heads, 32 hidden units
+        rng_a = np.random.default_rng(3)
+        H_a, F_a = 4, 32
+        W1a = t((rng_a.standard_normal((2 * C + w["n_radial"], F_a)) / np.sqrt(2 * C + w["n_radial"]))
+                .astype(np.float32))
+        w2a = t((rng_a.standard_normal((F_a, H_a)) / np.sqrt(F_a)).astype(np.float32))
+        pa = tdn.make_problem(w["L"], C, R, N, E, w["r_cut"], w["n_radial"], tdn.TDN_F32, w["presorted"])
+        aws = torch.empty(tdn.attention_workspace_size(pa, H_a, F_a), dtype=torch.uint8, device=x.device)
+        alpha_a = torch.empty((E, H_a), dtype=torch.float32, device=x.device)
+
+        def step_att():
+            return tdn.attention_forward(x, vec, ei, At, Bt, Dt, W, rw, W1a, w2a, L=w["L"], r_cut=w["r_cut"],
+                                         edges_sorted=w["presorted"], workspace=aws, out=out, alpha=alpha_a,
+                                         perm=perm, offsets=offsets)
+
+        k_ms, f_ms = time_calls(step_att, torch, tdn, "cp_edge_fwd_att", args.steps)
+        w_ms, _ = time_calls(step_att, torch, tdn, "attention_weights", max(1, args.steps // 4))
+        line["attention"] = {"heads": H_a, "hidden": F_a, "edge_kernel_ms": k_ms, "weights_ms": w_ms,
+                             "ms_per_step": f_ms, "value": E / (f_ms * 1e-3),
+                             "edge_kernel_vs_plain": k_ms / edge_ms, "launch": "eager"}
+        del aws, alpha_a
     if args.radius_graph:
         # the edges of this workload rebuilt on the device from its atoms
         gi = workloads.graph_inputs(w["name"])

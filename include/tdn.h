@@ -169,6 +169,34 @@ tdn_status tdn_cp_tp3_forward(const tdn_problem* p, const void* x, const float* 
                               int32_t* perm, int32_t* offsets, void* workspace, size_t workspace_bytes,
                               hipStream_t stream);
 
+/* The attention block that consumes the CP messages (Sec. 4.1 "Model
+ * Design": graph attention with MLP attention whose tensor products are the
+ * CP product with path-weight sharing of Sec. 3.1 and 3.2).  The paper gives
+ * no equations for the block; this is the reading implemented.  For an edge
+ * e = (s, t):
+ *   z_e  = D diag(g_e) A^T x[s]              the layer's message before W
+ *   q_e  = [x[t]^(0), x[s]^(0), phi_e]       degree-0 rows and radial basis
+ *   a_e  = LeakyReLU(q_e att_w1, 0.2) att_w2           [n_heads] logits
+ *   alpha_e[h] = exp(a_e[h]) / sum over e' into t of exp(a_e'[h])
+ *   out[t][:, c] = (sum over e into t of alpha_e[c / (C / n_heads)] z_e) W
+ * Arguments as tdn_cp_tp_forward (fp32 features only, TDN_ERR_BAD_DTYPE),
+ * and
+ *   att_w1 [2C + n_radial, n_hidden] f32  rows: x[t]^(0) channels, x[s]^(0)
+ *                                         channels, radial functions
+ *   att_w2 [n_hidden, n_heads] f32
+ *   alpha  [E, n_heads] f32 output: the weights by edge id (NULL: not stored)
+ * 1 <= L <= 4, R <= 256, 1 <= n_heads <= 8 with C a multiple of
+ * 32 n_heads, 1 <= n_hidden <= 64 (TDN_ERR_BAD_SHAPE otherwise).  The
+ * weights' softmax runs over each destination's edges in sorted order with
+ * its maximum subtracted; deterministic.  Workspace:
+ * tdn_attention_workspace_size. */
+tdn_status tdn_attention_workspace_size(const tdn_problem* p, int32_t n_heads, int32_t n_hidden, size_t* bytes);
+tdn_status tdn_attention_forward(const tdn_problem* p, int32_t n_heads, int32_t n_hidden, const float* x,
+                                 const float* edge_vec, const int32_t* edge_index, const float* A, const float* B,
+                                 const float* D, const float* W, const float* radial_w, const float* att_w1,
+                                 const float* att_w2, float* out, float* alpha, float* z_save, int32_t* perm,
+                                 int32_t* offsets, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Measurement ablations of the forward's hot-path choices: the same layer
  * and arguments as tdn_cp_tp_forward (Sec. 3.1 eq. approximate, Sec. 3.2),
  * with one choice of the edge pass replaced (the paper attributes its speed
@@ -350,7 +378,8 @@ tdn_status tdn_spherical_harmonics(int32_t L, int32_t E, const float* edge_vec, 
  * tdn_timer_enable(1) starts recording every launch of the layer's edge
  * kernels; tdn_timer_read synchronises on the recorded events and returns
  * the summed milliseconds and launch count of the kernel named `kernel`
- * ("cp_edge_fwd", "cp_edge_fwd_atomic", "cp_edge_fwd_ablation", "sh_table", "cp_edge_fwd_t3",
+ * ("cp_edge_fwd", "cp_edge_fwd_att", "attention_weights", "cp_edge_fwd_atomic", "cp_edge_fwd_ablation",
+ * "sh_table", "cp_edge_fwd_t3",
  * "dense_edge_fwd", "dense_edge_unshared",
  * "path_gemm", "radius_graph", "feature_layout",
  * "channel_layout", "cp_edge_bwd_src", "cp_bwd_dst", "radial_grad", "node_gemm", "gram",

@@ -77,6 +77,8 @@ def lib() -> ctypes.CDLL:
         L.tdn_dense_tp_forward.argtypes = [PP] + [_P] * 6 + [ctypes.c_int32] + [_P] * 7 + [_SZ, _P]
         L.tdn_dense_tp_unshared_workspace_size.argtypes = [PP, ctypes.POINTER(_SZ)]
         L.tdn_ablation_workspace_size.argtypes = [PP, ctypes.c_int32, ctypes.POINTER(_SZ)]
+        L.tdn_attention_workspace_size.argtypes = [PP, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_SZ)]
+        L.tdn_attention_forward.argtypes = [PP, ctypes.c_int32, ctypes.c_int32] + [_P] * 16 + [_SZ, _P]
         L.tdn_ablation_forward.argtypes = [PP, ctypes.c_int32] + [_P] * 13 + [_SZ, _P]
         L.tdn_dense_tp_forward_unshared.argtypes = [PP] + [_P] * 6 + [ctypes.c_int32] + [_P] * 6 + [_SZ, _P]
         GP = ctypes.POINTER(GraphProblem)
@@ -98,7 +100,8 @@ def lib() -> ctypes.CDLL:
                   "tdn_timer_read", "tdn_radius_graph_workspace_size", "tdn_radius_graph", "tdn_dense_tp_forward",
                   "tdn_cp_tp3_forward", "tdn_ps_linear_workspace_size", "tdn_ps_linear",
                   "tdn_dense_tp_unshared_workspace_size", "tdn_dense_tp_forward_unshared",
-                  "tdn_ablation_workspace_size", "tdn_ablation_forward"):
+                  "tdn_ablation_workspace_size", "tdn_ablation_forward", "tdn_attention_workspace_size",
+                  "tdn_attention_forward"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -411,6 +414,58 @@ def dense_forward(x, edge_vec, edge_index, table: CGTable, path_w, W, *, r_cut: 
     _check(st, "tdn_dense_tp_forward")
     return ForwardResult(out, z, perm, offsets, p, dict(x=x, edge_vec=edge_vec, edge_index=edge_index, W=W,
                                                         path_w=path_w))
+
+
+def attention_workspace_size(p: Problem, n_heads: int, n_hidden: int) -> int:
+    """Workspace bytes of tdn_attention_forward."""
+    nb = _SZ(0)
+    _check(lib().tdn_attention_workspace_size(ctypes.byref(p), int(n_heads), int(n_hidden), ctypes.byref(nb)),
+           "tdn_attention_workspace_size")
+    return nb.value
+
+
+def attention_forward(x, edge_vec, edge_index, A, B, D, W, radial_w, att_w1, att_w2, *, L: int, r_cut: float,
+                      edges_sorted=False, validate=False, workspace=None, out=None, z=None, alpha=None, perm=None,
+                      offsets=None, stream=None):
+    """Runs tdn_attention_forward (float32): att_w1 [2C + n_radial, F],
+    att_w2 [F, H].  Returns (ForwardResult, alpha [E, H] by edge id)."""
+    dev = x.device
+    N, d, C = x.shape
+    E = edge_vec.shape[0]
+    R = A.shape[1]
+    F, H = att_w2.shape
+    if edge_index.dtype != torch.int32:
+        edge_index = edge_index.to(torch.int32)
+    edge_index = edge_index.contiguous()
+    nr = radial_w.shape[0]
+    for t, n, sh in [(x, "x", (N, d, C)), (edge_vec, "edge_vec", (E, 3)), (A, "A", (d, R)), (B, "B", (d, R)),
+                     (D, "D", (d, R)), (W, "W", (C, C)), (radial_w, "radial_w", (nr, R)),
+                     (att_w1, "att_w1", (2 * C + nr, F)), (att_w2, "att_w2", (F, H))]:
+        _need(t, n, torch.float32, sh, dev)
+    _need(edge_index, "edge_index", torch.int32, (2, E), dev)
+    p = make_problem(L, C, R, N, E, r_cut, nr, TDN_F32, edges_sorted, validate)
+    nbytes = attention_workspace_size(p, H, F)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    if out is None:
+        out = torch.empty((N, d, C), dtype=torch.float32, device=dev)
+    if alpha is None:
+        alpha = torch.empty((E, H), dtype=torch.float32, device=dev)
+    if perm is None:
+        perm = torch.empty(max(E, 1), dtype=torch.int32, device=dev)[:E]
+    if offsets is None:
+        offsets = torch.empty(N + 1, dtype=torch.int32, device=dev)
+    _need(out, "out", torch.float32, (N, d, C), dev)
+    _need(alpha, "alpha", torch.float32, (E, H), dev)
+    if z is not None:
+        _need(z, "z", torch.float32, (N, d, C), dev)
+    st = lib().tdn_attention_forward(ctypes.byref(p), int(H), int(F), _ptr(x), _ptr(edge_vec), _ptr(edge_index),
+                                     _ptr(A), _ptr(B), _ptr(D), _ptr(W), _ptr(radial_w), _ptr(att_w1),
+                                     _ptr(att_w2), _ptr(out), _ptr(alpha), _ptr(z), _ptr(perm), _ptr(offsets),
+                                     _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "tdn_attention_forward")
+    return ForwardResult(out, z, perm, offsets, p, dict(x=x, edge_vec=edge_vec, edge_index=edge_index, A=A, B=B,
+                                                        D=D, W=W, radial_w=radial_w)), alpha
 
 
 def dense_unshared_workspace_size(p: Problem) -> int:

@@ -545,6 +545,90 @@ tdn_status tdn_ablation_forward(const tdn_problem* p, int32_t variant, const voi
   return TDN_OK;
 }
 
+namespace {
+// The attention block's workspace after the forward's: Pt and Ps [N, F], the
+// weights by sorted position [E, H].
+size_t att_extra_bytes(const tdn_problem& p, int H, int F) {
+  return al(size_t(p.n_nodes) * F * 4) * 2 + al(size_t(p.n_edges) * H * 4);
+}
+tdn_status check_attention(const tdn_problem* p, int32_t n_heads, int32_t n_hidden) {
+  const tdn_status st = check_problem(p);
+  if (st != TDN_OK) return st;
+  if (p->feat_dtype != TDN_F32) return TDN_ERR_BAD_DTYPE;
+  if (p->L < 1 || p->L > 4 || p->R > kChunkR || n_heads < 1 || n_heads > 8 || p->C % (32 * n_heads) != 0 ||
+      n_hidden < 1 || n_hidden > 64)
+    return TDN_ERR_BAD_SHAPE;
+  return TDN_OK;
+}
+}  // namespace
+
+tdn_status tdn_attention_workspace_size(const tdn_problem* p, int32_t n_heads, int32_t n_hidden, size_t* bytes) {
+  const tdn_status st = check_attention(p, n_heads, n_hidden);
+  if (st != TDN_OK) return st;
+  if (!bytes) return TDN_ERR_NULL_POINTER;
+  *bytes = fwd_layout(*p).total + att_extra_bytes(*p, n_heads, n_hidden);
+  return TDN_OK;
+}
+
+tdn_status tdn_attention_forward(const tdn_problem* p, int32_t n_heads, int32_t n_hidden, const float* x,
+                                 const float* edge_vec, const int32_t* edge_index, const float* A, const float* B,
+                                 const float* D, const float* W, const float* radial_w, const float* att_w1,
+                                 const float* att_w2, float* out, float* alpha, float* z_save, int32_t* perm,
+                                 int32_t* offsets, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  tdn_status st = check_attention(p, n_heads, n_hidden);
+  if (st != TDN_OK) return st;
+  const int N = p->n_nodes, E = p->n_edges, d = dim_of(p->L), C = p->C, F = n_hidden, H = n_heads;
+  if (!A || !B || !D || !W || !radial_w || !att_w1 || !att_w2 || !offsets || !workspace) return TDN_ERR_NULL_POINTER;
+  if (N > 0 && (!x || !out)) return TDN_ERR_NULL_POINTER;
+  if (E > 0 && (!edge_vec || !edge_index || !perm)) return TDN_ERR_NULL_POINTER;
+  const FwdLayout lay = fwd_layout(*p);
+  if (workspace_bytes < lay.total + att_extra_bytes(*p, H, F)) return TDN_ERR_WORKSPACE_TOO_SMALL;
+  st = check_device();
+  if (st != TDN_OK) return st;
+  char* ws = static_cast<char*>(workspace);
+  if (p->validate) {
+    st = run_validation(*p, edge_index, edge_vec, ws, lay.flags, p->edges_sorted, stream);
+    if (st != TDN_OK) return st;
+  }
+  const int32_t* src = edge_index;
+  const int32_t* dst = E > 0 ? edge_index + E : nullptr;
+  {
+    Timed t("sort", stream);
+    if (p->edges_sorted || E == 0)
+      TDN_HIP(tdn::launch_offsets_presorted(N, E, dst, perm, offsets, stream));
+    else
+      TDN_HIP(tdn::launch_sort(tdn::sort_plan(N, E), dst, 1, perm, offsets, ws + lay.sort, stream));
+  }
+  if (N == 0) return TDN_OK;
+  float* Pt = reinterpret_cast<float*>(ws + lay.total);
+  float* Ps = reinterpret_cast<float*>(ws + lay.total + al(size_t(N) * F * 4));
+  float* al_sorted = reinterpret_cast<float*>(ws + lay.total + 2 * al(size_t(N) * F * 4));
+  {
+    Timed t("attention_weights", stream);
+    TDN_HIP(tdn::launch_att_node(N, d, C, F, x, att_w1, Pt, Ps, stream));
+    TDN_HIP(tdn::launch_att_alpha(N, C, F, H, p->n_radial, p->r_cut / float(p->n_radial - 1), offsets, perm, src,
+                                  edge_vec, Pt, Ps, att_w1, att_w2, al_sorted, alpha, stream));
+  }
+  float* Z = z_save ? z_save : reinterpret_cast<float*>(ws + lay.z);
+  {
+    Timed t("feature_layout", stream);
+    TDN_HIP(edge_features(*p, x, true, ws + lay.xt, stream));
+  }
+  {
+    Timed t("cp_edge_fwd_att", stream);
+    tdn::EdgeArgs a = edge_args(*p, offsets, perm, src, dst, edge_vec, A, D, B, radial_w, ws + lay.xt, Z,
+                                reinterpret_cast<float*>(ws + lay.part));
+    a.alpha = al_sorted;
+    a.n_heads = H;
+    TDN_HIP(tdn::launch_cp_edge_att(a, stream));
+  }
+  {
+    Timed t("node_gemm", stream);
+    TDN_HIP(tdn::launch_node_gemm(N * d, C, Z, W, false, 0, out, ws + lay.wp, stream));
+  }
+  return TDN_OK;
+}
+
 tdn_status tdn_cp_tp3_forward(const tdn_problem* p, const void* x, const float* edge_vec, const int32_t* edge_index,
                               const float* A, const float* A2, const float* B, const float* D, const void* W,
                               const float* radial_w, float* out, float* z_save, int32_t* perm, int32_t* offsets,

@@ -33,6 +33,10 @@ TDN_ABL_EXTERN(2)
 TDN_ABL_EXTERN(3)
 TDN_ABL_EXTERN(4)
 #undef TDN_ABL_EXTERN
+extern template hipError_t launch_cp_edge_att_l<1>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_att_l<2>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_att_l<3>(const EdgeArgs&, hipStream_t);
+extern template hipError_t launch_cp_edge_att_l<4>(const EdgeArgs&, hipStream_t);
 
 namespace {
 
@@ -264,6 +268,34 @@ hipError_t launch_cp_edge_ablation(const EdgeArgs& a, int variant, const float* 
     case 2: e = fg ? launch_cp_edge_abl_l<2, 1>(a, s) : launch_cp_edge_abl_l<2, 2>(a, s); break;
     case 3: e = fg ? launch_cp_edge_abl_l<3, 1>(a, s) : launch_cp_edge_abl_l<3, 2>(a, s); break;
     default: e = fg ? launch_cp_edge_abl_l<4, 1>(a, s) : launch_cp_edge_abl_l<4, 2>(a, s); break;
+  }
+  if (e != hipSuccess) return e;
+  if (a.n_seg > 0)
+    k_range_fixup<<<dim3(a.n_seg), dim3(256), 0, s>>>(a.E, a.n_range, a.d * a.C, a.offsets, a.partial, a.out);
+  return hipGetLastError();
+}
+
+hipError_t launch_cp_edge_att(const EdgeArgs& a, hipStream_t s) {
+  using namespace edge_detail;
+  if (a.parts != 2 || a.L < 1 || a.L > 4 || a.n_heads < 1 || a.n_heads > kMaxHeads ||
+      a.C % (kTile * a.n_heads) != 0)
+    return hipErrorInvalidValue;
+  if (a.E > 0 && (a.n_range < 1 || a.n_range > a.E || a.pieces_per_block < 1 || a.n_range % a.pieces_per_block ||
+                  !a.ef_ops || !a.ef_scale || !a.row_scale || !a.alpha))
+    return hipErrorInvalidValue;
+  hipError_t e = hipSuccess;
+  if (a.E > 0) {
+    const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
+    k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops),
+                                                  a.ef_scale);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  switch (a.L) {
+    case 1: e = launch_cp_edge_att_l<1>(a, s); break;
+    case 2: e = launch_cp_edge_att_l<2>(a, s); break;
+    case 3: e = launch_cp_edge_att_l<3>(a, s); break;
+    default: e = launch_cp_edge_att_l<4>(a, s); break;
   }
   if (e != hipSuccess) return e;
   if (a.n_seg > 0)

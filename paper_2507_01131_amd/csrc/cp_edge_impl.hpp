@@ -122,8 +122,11 @@ __host__ __device__ constexpr int edge_max_ranges(int L, int RT, bool bf) {
 __host__ __device__ constexpr bool edge_reg_kf(int, int) { return false; }
 
 struct EdgeSmem {
-  int Rp, off_a, off_g, off_y, off_vec, off_phi, off_idx, off_sc, off_bnd, off_a2, off_t, floats;
+  int Rp, off_a, off_g, off_y, off_vec, off_phi, off_idx, off_sc, off_bnd, off_a2, off_al, off_t, floats;
 };
+
+// attention (ATT): most heads, and so attention weights per edge, per chunk
+constexpr int kMaxHeads = 8;
 
 // Per-wave transpose area of the split-mode segment epilogue: 32 channel rows
 // of 32 ranks, row stride 36 floats (16-byte reads of eight ranks by 32
@@ -141,7 +144,7 @@ constexpr int kTrFloats = kTile * kTrStride;
 // factor's operands in the layout of the first; in split mode last the
 // epilogue's transpose areas, one per wave.
 __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radial, int chunk, bool t3 = false,
-                                              bool rega = false) {
+                                              bool rega = false, bool att = false) {
   EdgeSmem s{};
   s.Rp = RT * kTile;
   int o = 0;
@@ -165,6 +168,8 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radi
   o = (o + 3) & ~3;
   s.off_a2 = o;
   if (t3) o += pk_blocks(d) * RT * kWave * 4;
+  s.off_al = o;  // attention: the chunk's weights [chunk][kMaxHeads]
+  if (att) o += chunk * kMaxHeads;
   (void)rega;
   s.off_t = o;
   if (!bf) o += kMaxWavesPerBlock * kTrFloats;
@@ -187,7 +192,11 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radi
 // factor blocks in the edge loop from a per-workgroup copy in global memory
 // (written after staging) instead of registers or LDS; 2 reads the harmonics
 // from a precomputed per-edge table instead of evaluating them.
-template <int L, int RT, bool BF, bool ATOM = false, bool T3 = false, int ABL = 0>
+// ATT (fp32 features, the attention block): every edge's message is weighted
+// per head by a.alpha[sorted position][head] before the segment sum; a head
+// owns C / n_heads channels, a multiple of 32, so a wave's channel tile lies
+// in one head and the weight is one factor on its g values.
+template <int L, int RT, bool BF, bool ATOM = false, bool T3 = false, int ABL = 0, bool ATT = false>
 __global__ __launch_bounds__(kMaxWavesPerBlock* kWave)
 __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edge(EdgeArgs a, int n_cgrp, int waves,
                                                                                   int chunk) {
@@ -204,7 +213,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   constexpr int PN = pk_rows(d), PB = pk_blocks(d), PQ = PN / 4, PT = PN % 4;
   extern __shared__ float smem[];
   constexpr bool kRegA = edge_rega(L, RT, BF) && ABL != 1;
-  const EdgeSmem S = edge_smem(RT, BF, d, a.n_radial, chunk, T3, kRegA);
+  const EdgeSmem S = edge_smem(RT, BF, d, a.n_radial, chunk, T3, kRegA, ATT);
   u32x4* sA = reinterpret_cast<u32x4*>(smem + S.off_a);
   u32x4* sA2 = reinterpret_cast<u32x4*>(smem + S.off_a2);
   float4* sAf = reinterpret_cast<float4*>(smem + S.off_a);
@@ -217,6 +226,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   int* sBnd = reinterpret_cast<int*>(smem + S.off_bnd);  // [chunk] chunk positions where a segment starts
   int* sBndKey = sBnd + chunk;                          // [chunk] that segment
   int* sMeta = sBndKey + chunk;                         // start count, first partial, last partial
+  float* sAl = smem + S.off_al;                         // ATT: [chunk][kMaxHeads] attention weights
 
 
   const int n_blocks = a.n_range / a.pieces_per_block;
@@ -226,6 +236,8 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   const int h = lane >> 5, l32 = lane & 31;
   const int C = a.C, nr = a.n_radial, R = a.R;
   const int c0 = (cgrp * waves + wave) * CT * kTile + l32;  // this lane's channel in tile 0
+  // ATT: the head of this wave's channel tile
+  const int my_head = ATT ? min((c0 - l32) / (C / a.n_heads), a.n_heads - 1) : 0;
 
   // Split mode: one thread per (packed K-block b, rank tile rt, lane) writes
   // the factor operand of that block: lane (h, r) slot j = 8b + i holds, for
@@ -579,6 +591,11 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
       float gl[RT];
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) gl[rt] = sG[e * Rp + rt * kTile + l32];
+      if constexpr (ATT) {
+        const float al = sAl[e * kMaxHeads + my_head];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) gl[rt] *= al;
+      }
       f32x16 U[2];
       auto load_a = [&](int rt, int buf) {
         if constexpr (!kRegA) {
@@ -637,6 +654,8 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
           sIdx[t] = row;
           if constexpr (!BF) sSc[t] = a.row_scale[row] * kf_unsc;
           key = a.key[eid];
+          if constexpr (ATT)
+            for (int hh = 0; hh < a.n_heads; ++hh) sAl[t * kMaxHeads + hh] = a.alpha[size_t(cb + t) * a.n_heads + hh];
           const float vx = a.edge_vec[3 * eid], vy = a.edge_vec[3 * eid + 1], vz = a.edge_vec[3 * eid + 2];
           const float len = sqrtf(vx * vx + vy * vy + vz * vz);
           const float inv = 1.f / len;
@@ -764,11 +783,11 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
 
 // Edge chunk of a block: the largest power of two <= 64 (at least 8) whose
 // LDS fits the block's share of the CU (160 KB over the blocks per CU).
-inline int edge_chunk(int L, int RT, bool bf, int n_radial, bool t3 = false) {
+inline int edge_chunk(int L, int RT, bool bf, int n_radial, bool t3 = false, bool att = false) {
   const int d = (L + 1) * (L + 1);
   const int budget = 160 * 1024 / edge_waves_per_eu(L, RT, bf);
   int chunk = 64;
-  while (chunk > 8 && edge_smem(RT, bf, d, n_radial, chunk, t3, edge_rega(L, RT, bf)).floats * 4 > budget)
+  while (chunk > 8 && edge_smem(RT, bf, d, n_radial, chunk, t3, edge_rega(L, RT, bf), att).floats * 4 > budget)
     chunk >>= 1;
   return chunk;
 }
@@ -785,15 +804,16 @@ inline EdgeGrid edge_grid(int C, int RT, bool bf) {
   return EdgeGrid{waves, (wave_tiles + waves - 1) / waves};
 }
 
-template <int L, int RT, bool BF, bool ATOM = false, bool T3 = false, int ABL = 0>
+template <int L, int RT, bool BF, bool ATOM = false, bool T3 = false, int ABL = 0, bool ATT = false>
 hipError_t launch_l_rt_m(const EdgeArgs& a, hipStream_t s) {
   constexpr int d = (L + 1) * (L + 1);
   const EdgeGrid gr = edge_grid(a.C, RT, BF);
   const int waves = gr.waves, n_cgrp = gr.n_cgrp;
   if (a.E > 0) {
-    const int chunk = edge_chunk(L, RT, BF, a.n_radial, T3);
-    const size_t lds = size_t(edge_smem(RT, BF, d, a.n_radial, chunk, T3, edge_rega(L, RT, BF)).floats) * 4;
-    auto k = k_cp_edge<L, RT, BF, ATOM, T3, ABL>;
+    const int chunk = edge_chunk(L, RT, BF, a.n_radial, T3, ATT);
+    const size_t lds =
+        size_t(edge_smem(RT, BF, d, a.n_radial, chunk, T3, edge_rega(L, RT, BF) && ABL != 1, ATT).floats) * 4;
+    auto k = k_cp_edge<L, RT, BF, ATOM, T3, ABL, ATT>;
     hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
@@ -850,6 +870,22 @@ hipError_t launch_cp_edge_abl_l(const EdgeArgs& a, hipStream_t s) {
     case 6: return launch_l_rt_m<L, 6, false, false, false, ABL>(a, s);
     case 7: return launch_l_rt_m<L, 7, false, false, false, ABL>(a, s);
     case 8: return launch_l_rt_m<L, 8, false, false, false, ABL>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// The attention block's dispatch on the rank tiles (fp32 features only).
+template <int L>
+hipError_t launch_cp_edge_att_l(const EdgeArgs& a, hipStream_t s) {
+  switch ((a.R + kTile - 1) / kTile) {
+    case 1: return launch_l_rt_m<L, 1, false, false, false, 0, true>(a, s);
+    case 2: return launch_l_rt_m<L, 2, false, false, false, 0, true>(a, s);
+    case 3: return launch_l_rt_m<L, 3, false, false, false, 0, true>(a, s);
+    case 4: return launch_l_rt_m<L, 4, false, false, false, 0, true>(a, s);
+    case 5: return launch_l_rt_m<L, 5, false, false, false, 0, true>(a, s);
+    case 6: return launch_l_rt_m<L, 6, false, false, false, 0, true>(a, s);
+    case 7: return launch_l_rt_m<L, 7, false, false, false, 0, true>(a, s);
+    case 8: return launch_l_rt_m<L, 8, false, false, false, 0, true>(a, s);
     default: return hipErrorInvalidValue;
   }
 }

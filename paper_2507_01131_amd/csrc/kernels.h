@@ -60,6 +60,9 @@ struct EdgeArgs {
   float* ef_scale;           // inside ef_ops: 2^e of EF's fp16 parts (parts = 2)
   int parts;                 // 16-bit parts per feature in feat (2: fp32 features as fp16 hi + lo, 1: bf16)
   const float* row_scale;    // [n_feat_rows] 2^e of each feat row (parts = 2), from launch_feature_layout
+  // attention (launch_cp_edge_att): the weights [E, n_heads] by sorted position
+  const float* alpha;
+  int n_heads;
   // measurement ablations only (launch_cp_edge_ablation):
   void* fa_global;           // factors from global memory: per workgroup a copy of its packed factor blocks
   const float* y_table;      // harmonics table: [E, d] Y of each edge by edge id (launch_sh)
@@ -116,6 +119,25 @@ hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s);
 // per edge and Z accumulated into `out` (zeroed first) with float atomics;
 // nondeterministic in the order of the additions.
 hipError_t launch_cp_edge_atomic(const EdgeArgs& a, hipStream_t s);
+// The attention block's edge pass (fp32 features, 1 <= L <= 4, one rank
+// chunk): launch_cp_edge with every edge's message weighted per head by
+// a.alpha[sorted position][head] before the segment sum (a.n_heads heads of
+// C / n_heads channels each, a multiple of 32, n_heads <= 8).
+hipError_t launch_cp_edge_att(const EdgeArgs& a, hipStream_t s);
+// Its weights.  launch_att_node: per node the hidden projections of the
+// degree-0 row, Pt[n] = x[n][0] W1[0 .. C) and Ps[n] = x[n][0] W1[C .. 2C)
+// ([N, F] each; W1 [2C + n_radial, F] row-major).  launch_att_alpha: per
+// destination (one wave), for its edges in sorted order the logits
+// a_e = LeakyReLU(Pt[t] + Ps[s_e] + phi_e W1[2C ..], 0.2) w2 (w2 [F, H]), then
+// the softmax over the destination's edges per head into alpha_sorted
+// [E, H] (sorted position) and, if not NULL, alpha_eid [E, H] (edge id).
+// F <= 64, H <= 8.
+hipError_t launch_att_node(int N, int d, int C, int F, const float* x, const float* W1, float* Pt, float* Ps,
+                           hipStream_t s);
+hipError_t launch_att_alpha(int N, int C, int F, int H, int n_radial, float sigma, const int32_t* offsets,
+                            const int32_t* perm, const int32_t* src, const float* edge_vec, const float* Pt,
+                            const float* Ps, const float* W1, const float* w2, float* alpha_sorted,
+                            float* alpha_eid, hipStream_t s);
 // Measurement ablations of the edge pass (fp32 features, 2 <= L <= 4, one
 // rank chunk), each with one hot-path choice replaced:
 //   kAblFactorsGlobal: the packed factor blocks read in the edge loop from a

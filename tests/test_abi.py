@@ -304,3 +304,31 @@ def test_ablation_forward_argument_checks(variant):
     assert _abl(None, variant) == 1
     for k in ["x", "vec", "ei", "A", "B", "D", "W", "rw", "out", "perm", "off", "ws"]:
         assert _abl(good, variant, **{k: None}) == 1, k
+
+
+def _att(p, H=2, F=8, ws_bytes=1 << 40, **override):
+    args = dict(x=FAKE, vec=FAKE, ei=FAKE, A=FAKE, B=FAKE, D=FAKE, W=FAKE, rw=FAKE, w1=FAKE, w2=FAKE, out=FAKE,
+                alpha=None, z=None, perm=FAKE, off=FAKE, ws=FAKE)
+    args.update(override)
+    return tdn.lib().tdn_attention_forward(None if p is None else ctypes.byref(p), H, F, args["x"], args["vec"],
+                                           args["ei"], args["A"], args["B"], args["D"], args["W"], args["rw"],
+                                           args["w1"], args["w2"], args["out"], args["alpha"], args["z"],
+                                           args["perm"], args["off"], args["ws"], ws_bytes, None)
+
+
+def test_attention_forward_argument_checks():
+    good = _problem(L=4, C=128, R=128)
+    need = ctypes.c_size_t(0)
+    assert tdn.lib().tdn_attention_workspace_size(ctypes.byref(good), 4, 32, ctypes.byref(need)) == 0
+    fwd, _ = tdn.workspace_size(good)
+    assert need.value >= fwd + 2 * 100 * 32 * 4 + 1000 * 4 * 4       # Pt, Ps and the sorted weights
+    assert _att(good, H=4, F=32, ws_bytes=need.value - 1) == 4
+    assert _att(good, H=3) == 2                 # C not a multiple of 32 H
+    assert _att(good, H=0) == 2 and _att(good, H=16) == 2
+    assert _att(good, F=0) == 2 and _att(good, F=65) == 2
+    assert _att(_problem(L=0, R=32)) == 2 and _att(_problem(L=5, R=32)) == 2
+    assert _att(_problem(L=4, R=300)) == 2
+    assert _att(_problem(L=4, feat_dtype=tdn.TDN_BF16)) == 3
+    assert _att(None) == 1
+    for k in ["x", "vec", "ei", "A", "B", "D", "W", "rw", "w1", "w2", "out", "perm", "off", "ws"]:
+        assert _att(good, **{k: None}) == 1, k
