@@ -69,11 +69,52 @@ __global__ __launch_bounds__(256) void k_range_fixup(int E, int n_range, int dC,
 // 2^e (EF's largest |EF| to [2^13, 2^14)) to ef_scale; P = 1 (bf16): ranks
 // in the order the accumulators hold them, k = acc_krow(q, h, i), bf16.  One
 // block.
+//
+// P = 2 also writes the node factor KF in the edge loop's packed operand
+// blocks (fp16 parts of KF 2^-e_K; kf_out [PB][RT][64 lanes], the edge
+// kernel keeps them in registers) and 2^e_K into kf_scale.
 template <int P>
 __global__ __launch_bounds__(256) void k_ef_blocks(int d, int R, int RT, int MT, const float* __restrict__ EF,
-                                                   u32x4* __restrict__ out, float* __restrict__ ef_scale) {
-  __shared__ float red[4];
+                                                   u32x4* __restrict__ out, float* __restrict__ ef_scale,
+                                                   const float* __restrict__ KF, u32x4* __restrict__ kf_out,
+                                                   float* __restrict__ kf_scale) {
+  __shared__ float red[8];
   const int tid = threadIdx.x;
+  if constexpr (P == 2) {
+    if (KF) {
+      float mx = 0.f;
+      for (int i = tid; i < d * R; i += blockDim.x) mx = fmaxf(mx, fabsf(KF[i]));
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      if ((tid & 63) == 0) red[4 + (tid >> 6)] = mx;
+      __syncthreads();
+      mx = fmaxf(fmaxf(red[4], red[5]), fmaxf(red[6], red[7]));
+      const int e = f16_split_exponent(mx);
+      const float ksc = ldexpf(1.f, -e);
+      if (tid == 0) *kf_scale = ldexpf(1.f, e);
+      const int PN = pk_rows(d), PB = pk_blocks(d);
+      for (int t = tid; t < PB * RT * kWave; t += blockDim.x) {
+        const int ln = t % kWave, brt = t / kWave;
+        const int b = brt / RT, rt = brt - b * RT;
+        const int r = rt * kTile + (ln & 31), hh = ln >> 5;
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint32_t pr = 0;
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            const int j = 8 * b + 2 * q + u, g = j / PN, row = hh * PN + j % PN;
+            const float v = (g < 3 && row < d && r < R) ? KF[row * R + r] * ksc : 0.f;
+            const _Float16 hi = static_cast<_Float16>(v);
+            const _Float16 val = g == 2 ? static_cast<_Float16>(v - float(hi)) : hi;
+            pr |= uint32_t(__builtin_bit_cast(uint16_t, val)) << (16 * u);
+          }
+          w[q] = pr;
+        }
+        kf_out[brt * kWave + ln] = u32x4{w[0], w[1], w[2], w[3]};
+      }
+    }
+  }
   float sc = 1.f;
   if constexpr (P == 2) {
     float mx = 0.f;
@@ -110,6 +151,12 @@ __global__ __launch_bounds__(256) void k_ef_blocks(int d, int R, int RT, int MT,
 
 constexpr int kMinRangeEdges = 48;
 
+// the node factor's packed blocks and scale inside ef_ops (after EF's blocks)
+u32x4* kf_blocks(const EdgeArgs& a) {
+  return reinterpret_cast<u32x4*>(static_cast<char*>(a.ef_ops) + edge_ef_blocks_bytes(a.d, a.R));
+}
+float* kf_scale(const EdgeArgs& a) { return a.ef_scale + 1; }
+
 }  // namespace
 }  // namespace edge_detail
 
@@ -129,8 +176,8 @@ int device_cus() {
 }
 
 size_t edge_ef_bytes(int d, int R) {
-  const size_t blocks = size_t((d + kTile - 1) / kTile) * ((R + kTile - 1) / kTile) * 2 * 2 * kWave * 16;
-  return blocks + 256;
+  const size_t kf = size_t(pk_blocks(d)) * ((R + kTile - 1) / kTile) * kWave * 16;
+  return edge_ef_blocks_bytes(d, R) + kf + 256;
 }
 
 EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E, bool t3) {
@@ -166,9 +213,11 @@ hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s) {
     const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
     u32x4* blocks = static_cast<u32x4*>(a.ef_ops);
     if (a.parts == 2)
-      k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, blocks, a.ef_scale);
+      k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, blocks, a.ef_scale, a.KF,
+                                                    kf_blocks(a), kf_scale(a));
     else
-      k_ef_blocks<1><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, blocks, a.ef_scale);
+      k_ef_blocks<1><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, blocks, a.ef_scale, nullptr, nullptr,
+                                                    nullptr);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -197,7 +246,8 @@ hipError_t launch_cp_edge_atomic(const EdgeArgs& a, hipStream_t s) {
   hipError_t e = launch_zero(a.out, size_t(a.n_seg) * a.d * a.C * 4, s);
   if (e != hipSuccess || a.E == 0) return e;
   const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
-  k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops), a.ef_scale);
+  k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops), a.ef_scale,
+                                                a.KF, kf_blocks(a), kf_scale(a));
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   switch (a.L) {
@@ -221,7 +271,7 @@ hipError_t launch_cp_edge_t3(const EdgeArgs& a, hipStream_t s) {
   if (a.E > 0) {
     const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
     k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops),
-                                                  a.ef_scale);
+                                                  a.ef_scale, a.KF, kf_blocks(a), kf_scale(a));
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -259,7 +309,7 @@ hipError_t launch_cp_edge_ablation(const EdgeArgs& a, int variant, const float* 
   if (a.E > 0) {
     const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
     k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops),
-                                                  a.ef_scale);
+                                                  a.ef_scale, a.KF, kf_blocks(a), kf_scale(a));
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -287,7 +337,7 @@ hipError_t launch_cp_edge_att(const EdgeArgs& a, hipStream_t s) {
   if (a.E > 0) {
     const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
     k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops),
-                                                  a.ef_scale);
+                                                  a.ef_scale, a.KF, kf_blocks(a), kf_scale(a));
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -148,8 +148,8 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radi
   EdgeSmem s{};
   s.Rp = RT * kTile;
   int o = 0;
-  s.off_a = o;
-  o += bf ? edge_kb(d) * RT * 2 * kWave * 4 : pk_blocks(d) * RT * kWave * 4;
+  s.off_a = o;  // split mode with rega: none (the blocks come from ef_ops)
+  o += bf ? edge_kb(d) * RT * 2 * kWave * 4 : (rega ? 0 : pk_blocks(d) * RT * kWave * 4);
   s.off_g = o;
   o += (chunk + kTile - 1) / kTile * kTile * s.Rp;
   s.off_y = o;
@@ -270,7 +270,10 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   // the chunk loop overwrites only after its first barrier); the edges' g
   // carry 2^e_K back.
   float kf_sc = 1.f, kf_unsc = 1.f;
-  if constexpr (!BF) {
+  if constexpr (!BF && kRegA) {
+    // the blocks and their scale were written by the launch's block kernel
+    kf_unsc = a.ef_scale[1];
+  } else if constexpr (!BF) {
     float mx = 0.f;
     for (int i = tid; i < d * R; i += blockDim.x) mx = fmaxf(mx, fabsf(a.KF[i]));
 #pragma unroll
@@ -311,7 +314,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
       sAf[2 * t] = make_float4(v[0], v[1], v[2], v[3]);
       sAf[2 * t + 1] = make_float4(v[4], v[5], v[6], v[7]);
     }
-  } else {
+  } else if constexpr (!kRegA) {
     for (int t = tid; t < PB * RT * kWave; t += blockDim.x) stage_packed(a.KF, kf_sc, t, sA);
   }
   // ABL 1: this workgroup's copy of the staged blocks in global memory
@@ -323,12 +326,18 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   __syncthreads();
   // Split mode with kRegA: every packed factor block is loaded into
   // registers at the start of each run of edges of one segment within a chunk
-  // (areg[b * RT + rt]), so the edge loop reads no factor from LDS while the
-  // geometry phase and the segment epilogue do not hold them.  Otherwise the blocks are read from
-  // LDS where they are used.  Either way their index goes through an opaque
-  // copy (zero added in inline asm) so that the compiler does not hoist the
-  // reads out of the loops; the pointer itself stays a known LDS pointer.
+  // (areg[b * RT + rt]) from the copy the launch's block kernel wrote in
+  // global memory (20 KB at R = 128, cache resident; no LDS for the factor,
+  // which leaves room for 64-edge chunks at two workgroups per CU), so the
+  // edge loop reads no factor while the geometry phase and the segment
+  // epilogue do not hold them.  Otherwise the blocks are read from LDS where
+  // they are used.  Either way their index goes through an opaque copy (zero
+  // added in inline asm) so that the compiler does not hoist the reads out of
+  // the loops.
   u32x4 areg[kRegA ? PB * RT : 1];
+  // kRegA: the packed blocks written by the launch (k_ef_blocks), after EF's
+  const u32x4* __restrict__ kfg = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.ef_ops) +
+                                                                edge_ef_blocks_bytes(d, R));
   auto a_op = [&](int base, int b, int rt) -> u32x4 {
     if constexpr (ABL == 1)
       return gA[base + (b * RT + rt) * kWave];
@@ -755,7 +764,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
           int ai = lane;
           asm volatile("" : "+v"(ai));
 #pragma unroll
-          for (int i = 0; i < PB * RT; ++i) areg[i] = sA[ai + i * kWave];
+          for (int i = 0; i < PB * RT; ++i) areg[i] = kfg[ai + i * kWave];
         }
         // Two operand buffers used alternately: the loads of edge f+1 are
         // issued before the MFMAs of edge f, and the scheduling barriers keep

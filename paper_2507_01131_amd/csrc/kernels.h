@@ -217,7 +217,12 @@ hipError_t launch_dense_edge_unshared(const DenseArgs& a, float* zp, hipStream_t
 hipError_t launch_path_gemm(int N, int L, int C, const float* zp, const float* W_paths, float* out, hipStream_t s);
 // Workspace bytes of EdgeArgs::ef_ops: the output factor in 32x32x16 operand
 // blocks [ceil(d/32)][ceil(R/32)][2][parts][64 lanes] x 16 bytes (parts <= 2)
-// and, after them, its scale.
+// (edge_ef_blocks_bytes), the node factor in the edge loop's packed blocks
+// [pk_blocks(d)][ceil(R/32)][64 lanes] x 16 bytes (fp32 features), then 256
+// bytes holding the two scales (EF's, then KF's).
+__host__ __device__ inline size_t edge_ef_blocks_bytes(int d, int R) {
+  return size_t((d + 31) / 32) * ((R + 31) / 32) * 2 * 2 * 64 * 16;
+}
 size_t edge_ef_bytes(int d, int R);
 
 // ---------------------------------------------------------------- node GEMMs
