@@ -67,12 +67,34 @@ __global__ __launch_bounds__(256) void k_range_fixup(int E, int n_range, int dC,
 // P = 2 (fp32 features): ranks in natural order, k = 16q + 8h + i (the
 // epilogue transposes its sums through LDS), fp16 hi and lo of EF 2^-e with
 // 2^e (EF's largest |EF| to [2^13, 2^14)) to ef_scale; P = 1 (bf16): ranks
-// in the order the accumulators hold them, k = acc_krow(q, h, i), bf16.  One
-// block.
+// in the order the accumulators hold them, k = acc_krow(q, h, i), bf16.
 //
 // P = 2 also writes the node factor KF in the edge loop's packed operand
 // blocks (fp16 parts of KF 2^-e_K; kf_out [PB][RT][64 lanes], the edge
 // kernel keeps them in registers) and 2^e_K into kf_scale.
+//
+// One thread per 16-byte output entry, KF's entries first; every workgroup
+// takes the two largest magnitudes over the whole factors itself (a few KB
+// from L2), so the workgroups need no exchange and agree exactly.
+__device__ __forceinline__ float block_abs_max(const float* __restrict__ v, int n, float* red) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  // eight independent loads in flight per thread
+  float m[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  int i = tid;
+  for (; i + 7 * nt < n; i += 8 * nt)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) m[u] = fmaxf(m[u], fabsf(v[i + u * nt]));
+  for (; i < n; i += nt) m[0] = fmaxf(m[0], fabsf(v[i]));
+  float mx = fmaxf(fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3])), fmaxf(fmaxf(m[4], m[5]), fmaxf(m[6], m[7])));
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  if ((tid & 63) == 0) red[tid >> 6] = mx;
+  __syncthreads();
+  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+__host__ __device__ inline int ef_kf_entries(int d, int RT, bool kf) { return kf ? pk_blocks(d) * RT * kWave : 0; }
+
 template <int P>
 __global__ __launch_bounds__(256) void k_ef_blocks(int d, int R, int RT, int MT, const float* __restrict__ EF,
                                                    u32x4* __restrict__ out, float* __restrict__ ef_scale,
@@ -80,20 +102,17 @@ __global__ __launch_bounds__(256) void k_ef_blocks(int d, int R, int RT, int MT,
                                                    float* __restrict__ kf_scale) {
   __shared__ float red[8];
   const int tid = threadIdx.x;
+  const int t = blockIdx.x * blockDim.x + tid;
+  const int n_kf = ef_kf_entries(d, RT, P == 2 && KF != nullptr);
+  const int n_ef = MT * RT * 2 * kWave;
   if constexpr (P == 2) {
     if (KF) {
-      float mx = 0.f;
-      for (int i = tid; i < d * R; i += blockDim.x) mx = fmaxf(mx, fabsf(KF[i]));
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-      if ((tid & 63) == 0) red[4 + (tid >> 6)] = mx;
-      __syncthreads();
-      mx = fmaxf(fmaxf(red[4], red[5]), fmaxf(red[6], red[7]));
+      const float mx = block_abs_max(KF, d * R, red + 4);
       const int e = f16_split_exponent(mx);
       const float ksc = ldexpf(1.f, -e);
-      if (tid == 0) *kf_scale = ldexpf(1.f, e);
-      const int PN = pk_rows(d), PB = pk_blocks(d);
-      for (int t = tid; t < PB * RT * kWave; t += blockDim.x) {
+      if (t == 0) *kf_scale = ldexpf(1.f, e);
+      const int PN = pk_rows(d);
+      if (t < n_kf) {
         const int ln = t % kWave, brt = t / kWave;
         const int b = brt / RT, rt = brt - b * RT;
         const int r = rt * kTile + (ln & 31), hh = ln >> 5;
@@ -117,19 +136,14 @@ __global__ __launch_bounds__(256) void k_ef_blocks(int d, int R, int RT, int MT,
   }
   float sc = 1.f;
   if constexpr (P == 2) {
-    float mx = 0.f;
-    for (int i = tid; i < d * R; i += blockDim.x) mx = fmaxf(mx, fabsf(EF[i]));
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-    if ((tid & 63) == 0) red[tid >> 6] = mx;
-    __syncthreads();
-    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    const float mx = block_abs_max(EF, d * R, red);
     const int e = f16_split_exponent(mx);
     sc = ldexpf(1.f, -e);
-    if (tid == 0) *ef_scale = ldexpf(1.f, e);
+    if (t == 0) *ef_scale = ldexpf(1.f, e);
   }
-  for (int t = tid; t < MT * RT * 2 * kWave; t += blockDim.x) {
-    const int ln = t % kWave, blk = t / kWave;
+  const int te = t - n_kf;
+  if (te >= 0 && te < n_ef) {
+    const int ln = te % kWave, blk = te / kWave;
     const int q = blk % 2, rt = (blk / 2) % RT, mt = blk / (2 * RT);
     const int m = mt * kTile + (ln & 31), hh = ln >> 5;
     uint32_t w[P][4];
@@ -145,8 +159,18 @@ __global__ __launch_bounds__(256) void k_ef_blocks(int d, int R, int RT, int MT,
         w[0][i] = pack_bf16x2_rne(v0, v1);
     }
 #pragma unroll
-    for (int p = 0; p < P; ++p) out[t * P + p] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
+    for (int p = 0; p < P; ++p) out[te * P + p] = u32x4{w[p][0], w[p][1], w[p][2], w[p][3]};
   }
+}
+
+// the launch of k_ef_blocks: one 256-thread workgroup per 256 output entries
+template <int P>
+hipError_t launch_ef_blocks(int d, int R, const float* EF, u32x4* out, float* ef_scale, const float* KF,
+                            u32x4* kf_out, float* kf_scale, hipStream_t s) {
+  const int RT = (R + kTile - 1) / kTile, MT = (d + kTile - 1) / kTile;
+  const int n = ef_kf_entries(d, RT, P == 2 && KF != nullptr) + MT * RT * 2 * kWave;
+  k_ef_blocks<P><<<dim3((n + 255) / 256), dim3(256), 0, s>>>(d, R, RT, MT, EF, out, ef_scale, KF, kf_out, kf_scale);
+  return hipGetLastError();
 }
 
 constexpr int kMinRangeEdges = 48;
@@ -210,15 +234,11 @@ hipError_t launch_cp_edge(const EdgeArgs& a, hipStream_t s) {
     return hipErrorInvalidValue;
   hipError_t e = hipSuccess;
   if (a.E > 0) {
-    const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
     u32x4* blocks = static_cast<u32x4*>(a.ef_ops);
     if (a.parts == 2)
-      k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, blocks, a.ef_scale, a.KF,
-                                                    kf_blocks(a), kf_scale(a));
+      e = launch_ef_blocks<2>(a.d, a.R, a.EF, blocks, a.ef_scale, a.KF, kf_blocks(a), kf_scale(a), s);
     else
-      k_ef_blocks<1><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, blocks, a.ef_scale, nullptr, nullptr,
-                                                    nullptr);
-    e = hipGetLastError();
+      e = launch_ef_blocks<1>(a.d, a.R, a.EF, blocks, a.ef_scale, nullptr, nullptr, nullptr, s);
     if (e != hipSuccess) return e;
   }
   switch (a.L) {
@@ -245,10 +265,8 @@ hipError_t launch_cp_edge_atomic(const EdgeArgs& a, hipStream_t s) {
     return hipErrorInvalidValue;
   hipError_t e = launch_zero(a.out, size_t(a.n_seg) * a.d * a.C * 4, s);
   if (e != hipSuccess || a.E == 0) return e;
-  const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
-  k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops), a.ef_scale,
-                                                a.KF, kf_blocks(a), kf_scale(a));
-  e = hipGetLastError();
+  e = launch_ef_blocks<2>(a.d, a.R, a.EF, static_cast<u32x4*>(a.ef_ops), a.ef_scale, a.KF, kf_blocks(a),
+                          kf_scale(a), s);
   if (e != hipSuccess) return e;
   switch (a.L) {
     case 2: return launch_cp_edge_atomic_l<2>(a, s);
@@ -269,10 +287,8 @@ hipError_t launch_cp_edge_t3(const EdgeArgs& a, hipStream_t s) {
     return hipErrorInvalidValue;
   hipError_t e = hipSuccess;
   if (a.E > 0) {
-    const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
-    k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops),
-                                                  a.ef_scale, a.KF, kf_blocks(a), kf_scale(a));
-    e = hipGetLastError();
+    e = launch_ef_blocks<2>(a.d, a.R, a.EF, static_cast<u32x4*>(a.ef_ops), a.ef_scale, a.KF, kf_blocks(a),
+                            kf_scale(a), s);
     if (e != hipSuccess) return e;
   }
   switch (a.L) {
@@ -307,10 +323,8 @@ hipError_t launch_cp_edge_ablation(const EdgeArgs& a, int variant, const float* 
     return hipErrorInvalidValue;
   hipError_t e = hipSuccess;
   if (a.E > 0) {
-    const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
-    k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops),
-                                                  a.ef_scale, a.KF, kf_blocks(a), kf_scale(a));
-    e = hipGetLastError();
+    e = launch_ef_blocks<2>(a.d, a.R, a.EF, static_cast<u32x4*>(a.ef_ops), a.ef_scale, a.KF, kf_blocks(a),
+                            kf_scale(a), s);
     if (e != hipSuccess) return e;
   }
   const bool fg = variant == kAblFactorsGlobal;
@@ -335,10 +349,8 @@ hipError_t launch_cp_edge_att(const EdgeArgs& a, hipStream_t s) {
     return hipErrorInvalidValue;
   hipError_t e = hipSuccess;
   if (a.E > 0) {
-    const int RT = (a.R + kTile - 1) / kTile, MT = (a.d + kTile - 1) / kTile;
-    k_ef_blocks<2><<<dim3(1), dim3(256), 0, s>>>(a.d, a.R, RT, MT, a.EF, static_cast<u32x4*>(a.ef_ops),
-                                                  a.ef_scale, a.KF, kf_blocks(a), kf_scale(a));
-    e = hipGetLastError();
+    e = launch_ef_blocks<2>(a.d, a.R, a.EF, static_cast<u32x4*>(a.ef_ops), a.ef_scale, a.KF, kf_blocks(a),
+                            kf_scale(a), s);
     if (e != hipSuccess) return e;
   }
   switch (a.L) {

@@ -108,12 +108,10 @@ __host__ __device__ constexpr bool edge_rega(int L, int RT, bool bf) {
   return !bf && 4 * pk_blocks((L + 1) * (L + 1)) * RT <= (edge_waves_per_eu(L, RT, bf) == 2 ? 80 : 160);
 }
 
-// Most ranges a workgroup takes: two where two workgroups share a CU (their
-// gathered rows then stay in L2), one otherwise (the extra loop level costs
-// registers that a one-wave kernel spends on accumulators).
-__host__ __device__ constexpr int edge_max_ranges(int L, int RT, bool bf) {
-  return edge_waves_per_eu(L, RT, bf) == 2 ? 2 : 1;
-}
+// Most ranges a workgroup takes: one.  (Two ranges per workgroup, dealt so
+// that an XCD's workgroups work on neighbouring edges, ran as fast but write
+// twice the partial rows of the segments that cross range ends.)
+__host__ __device__ constexpr int edge_max_ranges(int, int, bool) { return 1; }
 
 // bf16 mode: whether this lane's K factor values (KB * RT * 8 floats) stay
 // in registers instead of LDS.  Never: two waves per SIMD, which the registers

@@ -192,8 +192,10 @@ int dense_path_count(int L);
 hipError_t launch_dense_edge(const DenseArgs& a, hipStream_t s);
 
 // out[i] = sum over p = 0 .. n_part - 1 of partial[p][i] (i < n), in a fixed
-// order (sixteen strided partial sums, then those in order)
-hipError_t launch_sum_parts(int n_part, int n, const float* partial, float* out, hipStream_t s);
+// order (sixteen strided partial sums, then those in order; above 256 parts
+// first the groups of 64 consecutive parts, each written over its first
+// part, so partial is overwritten then)
+hipError_t launch_sum_parts(int n_part, int n, float* partial, float* out, hipStream_t s);
 // The product without path-weight sharing: every path keeps its own block of
 // output rows, path p (in the order l1, then l2, then l3 ascending) owning
 // rows row[p] .. row[p] + 2 l3[p], n_rows = sum over paths of 2 l3 + 1.

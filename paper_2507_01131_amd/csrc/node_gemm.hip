@@ -419,16 +419,16 @@ __global__ __launch_bounds__(256) void k_gram_partial(int rows, int C, int rows_
 }
 
 // 16 outputs per workgroup, 16 slices per output: slice k sums parts
-// k, k + 16, ... in order, then the slices are added in order (the result
-// does not depend on scheduling).
-__global__ __launch_bounds__(256) void k_sum_parts(int n_part, int CC, const float* __restrict__ partial,
+// k, k + 16, ... in order (part p at row p * stride), then the slices are
+// added in order (the result does not depend on scheduling).
+__global__ __launch_bounds__(256) void k_sum_parts(int n_part, int CC, int stride, const float* __restrict__ partial,
                                                    float* __restrict__ out) {
   __shared__ float sl[16][17];
   const int o = threadIdx.x & 15, k = threadIdx.x >> 4;
   const int i = blockIdx.x * 16 + o;
   float s = 0.f;
   if (i < CC)
-    for (int p = k; p < n_part; p += 16) s += partial[size_t(p) * CC + i];
+    for (int p = k; p < n_part; p += 16) s += partial[size_t(p) * stride * CC + i];
   sl[k][o] = s;
   __syncthreads();
   if (k == 0 && i < CC) {
@@ -437,6 +437,20 @@ __global__ __launch_bounds__(256) void k_sum_parts(int n_part, int CC, const flo
     for (int j = 0; j < 16; ++j) t += sl[j][o];
     out[i] = t;
   }
+}
+
+// First stage for many parts: group g (parts g kGroup .. g kGroup + kGroup
+// - 1) summed in order by one thread per output, the sum written over the
+// group's first part (each entry read and written by its one thread).
+constexpr int kGroup = 64;
+__global__ __launch_bounds__(256) void k_sum_groups(int n_part, int CC, float* __restrict__ partial) {
+  const int i = blockIdx.x * 256 + threadIdx.x, g = blockIdx.y;
+  if (i >= CC) return;
+  const int p0 = g * kGroup, p1 = min(p0 + kGroup, n_part);
+  float s = 0.f;
+#pragma unroll 8
+  for (int p = p0; p < p1; ++p) s += partial[size_t(p) * CC + i];
+  partial[size_t(p0) * CC + i] = s;
 }
 
 }  // namespace
@@ -487,10 +501,19 @@ int gram_parts(int rows, int C) {
   return p < 1 ? 1 : p;
 }
 
-hipError_t launch_sum_parts(int n_part, int n, const float* partial, float* out, hipStream_t s) {
+hipError_t launch_sum_parts(int n_part, int n, float* partial, float* out, hipStream_t s) {
   if (n == 0) return hipSuccess;
   if (n_part < 1 || n < 0 || !partial || !out) return hipErrorInvalidValue;
-  k_sum_parts<<<dim3((n + 15) / 16), dim3(256), 0, s>>>(n_part, n, partial, out);
+  if (n_part > 4 * kGroup) {
+    // many parts: groups of kGroup summed in place first, then the groups
+    const int groups = (n_part + kGroup - 1) / kGroup;
+    k_sum_groups<<<dim3((n + 255) / 256, groups), dim3(256), 0, s>>>(n_part, n, partial);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    k_sum_parts<<<dim3((n + 15) / 16), dim3(256), 0, s>>>(groups, n, kGroup, partial, out);
+    return hipGetLastError();
+  }
+  k_sum_parts<<<dim3((n + 15) / 16), dim3(256), 0, s>>>(n_part, n, 1, partial, out);
   return hipGetLastError();
 }
 
@@ -514,7 +537,7 @@ hipError_t launch_gram(int rows, int C, const float* Z, const float* G, bool bf1
     k_gram_partial<true><<<grid, dim3(256), 0, s>>>(rows, C, rpp, Z, G, partial);
   else
     k_gram_partial<false><<<grid, dim3(256), 0, s>>>(rows, C, rpp, Z, G, partial);
-  k_sum_parts<<<dim3((C * C + 15) / 16), dim3(256), 0, s>>>(parts, C * C, partial, grad_W);
+  k_sum_parts<<<dim3((C * C + 15) / 16), dim3(256), 0, s>>>(parts, C * C, 1, partial, grad_W);
   return hipGetLastError();
 }
 

@@ -7,8 +7,8 @@
 // most 2048) in chunks of 64:
 // phi for the chunk into LDS, then fp32 MFMA (rows: radial functions, columns:
 // ranks, contraction over the chunk's edges, two per step), one 32-rank tile
-// per wave (two for R > 128).  The partial sums are added in block order by a
-// second kernel, so the result does not depend on scheduling.
+// per wave (two for R > 128).  The partial sums are added in a fixed order
+// (launch_sum_parts), so the result does not depend on scheduling.
 #include "common.hpp"
 #include "kernels.h"
 #include "sh_device.hpp"
@@ -75,26 +75,6 @@ __global__ __launch_bounds__(256) void k_wrad_partial(int E, int n_blocks, int R
   }
 }
 
-// 16 outputs per workgroup, 16 slices per output: slice k sums the partials
-// of blocks k, k + 16, ... in order, then the slices are added in order.
-__global__ __launch_bounds__(256) void k_wrad_reduce(int n_blocks, int n_out, const float* __restrict__ partial,
-                                                     float* __restrict__ grad) {
-  __shared__ float sSum[16][17];
-  const int o = threadIdx.x & 15, k = threadIdx.x >> 4;
-  const int i = blockIdx.x * 16 + o;
-  float s = 0.f;
-  if (i < n_out)
-    for (int b = k; b < n_blocks; b += 16) s += partial[size_t(b) * n_out + i];
-  sSum[k][o] = s;
-  __syncthreads();
-  if (k == 0 && i < n_out) {
-    float t = 0.f;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) t += sSum[j][o];
-    grad[i] = t;
-  }
-}
-
 }  // namespace
 
 int radial_grad_blocks(int E) {
@@ -109,8 +89,9 @@ hipError_t launch_radial_grad(int E, int R, int n_radial, float sigma, const flo
   if (E == 0) return launch_zero(grad_radial_w, size_t(n_out) * 4, s);
   const int nb = radial_grad_blocks(E);
   k_wrad_partial<<<dim3(nb), dim3(256), 0, s>>>(E, nb, R, n_radial, sigma, edge_vec, drho, partial);
-  k_wrad_reduce<<<dim3((n_out + 15) / 16), dim3(256), 0, s>>>(nb, n_out, partial, grad_radial_w);
-  return hipGetLastError();
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_sum_parts(nb, n_out, partial, grad_radial_w, s);
 }
 
 }  // namespace tdn

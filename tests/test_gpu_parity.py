@@ -84,6 +84,9 @@ SMALL = [
     dict(seed=8, N=33, E=600, L=5, C=48, R=40, sort=False),
     dict(seed=9, N=30, E=500, L=5, C=96, R=100, sort=True, feat_dtype="bf16"),
     dict(seed=10, N=20, E=300, L=6, C=160, R=64, sort=False),
+    # d > 32 with four rank tiles per wave (R a multiple of 128, C <= 128)
+    dict(seed=11, N=24, E=450, L=6, C=128, R=256, sort=False),
+    dict(seed=12, N=30, E=500, L=5, C=80, R=128, sort=True),
 ]
 
 
