@@ -151,7 +151,7 @@ FwdLayout fwd_layout(const tdn_problem& p) {
 }
 
 struct BwdLayout {
-  size_t gz, z, xt, part, parts, perm_src, off_src, sort, wp, drho, wrad_part, gv, fsl, gtmp, grtmp, gzc, flags,
+  size_t gz, z, xt, part, parts, perm_src, off_src, sort, wp, drho, wrad_part, gv, fsl, gtmp, grtmp, bt, gzc, flags,
       total;
 };
 BwdLayout bwd_layout(const tdn_problem& p) {
@@ -190,6 +190,8 @@ BwdLayout bwd_layout(const tdn_problem& p) {
   o += chunked ? al(std::max(ndc, size_t(p.n_edges) * 12)) : 0;
   b.grtmp = o;
   o += chunked ? al(size_t(p.n_radial) * rc * 4) : 0;
+  b.bt = o;  // direct destination kernel (d > 32): B^T and Wrad^T of a rank chunk
+  o += dim_of(p.L) > 32 ? al(size_t(dim_of(p.L) + p.n_radial) * rc * 4) : 0;
   b.gzc = o;  // split form of the destination kernel: Gz in the layout of xc, then its row scales
   o += tdn::bwd_dst_split(p.L, p.C, p.feat_dtype == TDN_BF16) ? al(xc_bytes(p)) + al(size_t(p.n_nodes) * 4) : 0;
   b.flags = o;
@@ -1005,6 +1007,7 @@ tdn_status tdn_cp_tp_backward(const tdn_problem* p, const void* x, const float* 
                                           ws + lay.xt, bf16 ? nullptr : xscale, true, stream));
         a.xc = ws + lay.xt;
         a.x_scale = bf16 ? nullptr : xscale;
+        a.bt = reinterpret_cast<float*>(ws + lay.bt);
       }
       {
         Timed t("cp_bwd_dst", stream);

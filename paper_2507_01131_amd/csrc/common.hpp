@@ -22,6 +22,12 @@ __device__ __forceinline__ f32x16 mfma32(float a, float b, f32x16 c) {
 
 __device__ __forceinline__ int acc_row(int v, int half) { return 8 * (v >> 2) + 4 * half + (v & 3); }
 
+// One 16x16x4 fp32 MFMA.  Lane l supplies a = A[l%16][l/16] and
+// b = B[l/16][l%16]; register i of lane l holds row 4(l/16) + i, column l%16.
+__device__ __forceinline__ f32x4 mfma16f32(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }
 
 template <typename T>

@@ -35,25 +35,26 @@ namespace tdn {
 
 namespace bwd_detail {
 
-constexpr int kChunk = 16;  // edges per chunk
-static_assert(kChunk <= kTile, "a chunk's edges fit one 32-row MFMA tile");
+constexpr int kChunk = 16;  // edges per chunk: the rows of one 16x16x4 MFMA tile
+constexpr int kPy = 80;     // per edge: 64 dY columns (k < d <= 64) and 16 dphi columns (n_radial <= 16)
 
 struct DstSmem {
-  int Rp, off_b, off_v, off_rho, off_dg, off_y, off_phi, off_dy, off_dphi, off_j, off_idx, off_sc, floats;
+  int Rp, Rs, off_b, off_v, off_rho, off_dg, off_y, off_phi, off_dy, off_dphi, off_j, off_idx, off_sc, floats;
 };
 
 __host__ __device__ inline DstSmem dst_smem(int RT, int MT, int d, int n_radial, int C) {
   DstSmem s{};
   s.Rp = RT * kTile;
+  s.Rs = s.Rp + 4;  // row stride of v, rho and dg: the dY products read columns of them
   int o = 0;
   s.off_b = o;  // A in accumulator order: [MT][RT][4][64 lanes] x float4
   o += MT * RT * 4 * kWave * 4;
   s.off_v = o;
-  o += kChunk * s.Rp;
+  o += kChunk * s.Rs;
   s.off_rho = o;
-  o += kChunk * s.Rp;
+  o += kChunk * s.Rs;
   s.off_dg = o;
-  o += MT * kChunk * s.Rp;
+  o += MT * kChunk * s.Rs;
   if (o < s.off_v + d * C) o = s.off_v + d * C;  // the region also holds Gz[seg] while Gh^T is formed
   s.off_y = o;
   o += kChunk * d;
@@ -97,11 +98,11 @@ __global__ __launch_bounds__(direct_waves(MT, RT)* kWave) void k_bwd_dst(BwdDstA
   constexpr int NW = direct_waves(MT, RT);
   extern __shared__ float smem[];
   const DstSmem S = dst_smem(RT, MT, a.d, a.n_radial, a.C);
-  constexpr int Rp = RT * kTile;
+  constexpr int Rp = RT * kTile, Rs = Rp + 4;
   f32x4* sAl = reinterpret_cast<f32x4*>(smem + S.off_b);
   float* sV = smem + S.off_v;
   float* sRho = smem + S.off_rho;
-  float* sDG = smem + S.off_dg;  // [MT][kChunk][Rp]: dg over each k tile
+  float* sDG = smem + S.off_dg;  // [MT][kChunk][Rs]: dg over each k tile
   float* sY = smem + S.off_y;
   float* sPhi = smem + S.off_phi;
   float* sDY = smem + S.off_dy;
@@ -117,6 +118,7 @@ __global__ __launch_bounds__(direct_waves(MT, RT)* kWave) void k_bwd_dst(BwdDstA
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, l32 = lane & 31;
+  const int g4 = lane >> 4, l16 = lane & 15;  // 16x16x4 MFMA operand coordinates
   const int d = a.d, C = a.C, nr = a.n_radial, R = a.R;
   // the P_e tiles of this wave: k tile kt, rank tiles 2j and 2j + 1
   const int kt = wave % MT, pj = wave / MT;
@@ -243,32 +245,42 @@ __global__ __launch_bounds__(direct_waves(MT, RT)* kWave) void k_bwd_dst(BwdDstA
       sSc[t] = BF ? 1.f : a.x_scale[row];
     }
     __syncthreads();
-    // v = Y B and rho = Phi Wrad per rank tile on fp32 MFMA (rows: the chunk's
-    // edges, padded to a 32-row tile), one rank tile per wave at a time
+    // v = Y B and rho = Phi Wrad on 16x16x4 fp32 MFMA (rows: the chunk's 16
+    // edges; columns: two 16-rank halves of one 32-rank tile per wave at a
+    // time; contraction over k < d, then over the radial functions)
     for (int rt = wave; rt < RT; rt += NW) {
-      const int r = rt * kTile + l32;
-      f32x16 tv = f32x16{}, tr = f32x16{};
+      f32x4 tv[2] = {f32x4{}, f32x4{}}, tr[2] = {f32x4{}, f32x4{}};
 #pragma unroll 4
-      for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
-        const int k = 2 * s2 + h;
-        const float av = (l32 < n && k < d) ? sY[l32 * d + k] : 0.f;
-        const float bv = (k < d && r < R) ? a.Bf[k * R + r] : 0.f;
-        tv = mfma32(av, bv, tv);
-      }
-      for (int s2 = 0; s2 < (nr + 1) / 2; ++s2) {
-        const int q = 2 * s2 + h;
-        const float av = (l32 < n && q < nr) ? sPhi[l32 * nr + q] : 0.f;
-        const float bv = (q < nr && r < R) ? a.radial_w[q * R + r] : 0.f;
-        tr = mfma32(av, bv, tr);
-      }
+      for (int s4 = 0; s4 < (d + 3) / 4; ++s4) {
+        const int k = 4 * s4 + g4;
+        const float av = (l16 < n && k < d) ? sY[l16 * d + k] : 0.f;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int e = acc_row(v, h);
-        if (e < n) {
-          sV[e * Rp + r] = tv[v];
-          sRho[e * Rp + r] = tr[v];
+        for (int c2 = 0; c2 < 2; ++c2) {
+          const int r = rt * kTile + 16 * c2 + l16;
+          const float bv = (k < d && r < R) ? a.Bf[k * R + r] : 0.f;
+          tv[c2] = mfma16f32(av, bv, tv[c2]);
         }
       }
+      for (int s4 = 0; s4 < (nr + 3) / 4; ++s4) {
+        const int q = 4 * s4 + g4;
+        const float av = (l16 < n && q < nr) ? sPhi[l16 * nr + q] : 0.f;
+#pragma unroll
+        for (int c2 = 0; c2 < 2; ++c2) {
+          const int r = rt * kTile + 16 * c2 + l16;
+          const float bv = (q < nr && r < R) ? a.radial_w[q * R + r] : 0.f;
+          tr[c2] = mfma16f32(av, bv, tr[c2]);
+        }
+      }
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = 4 * g4 + i, r = rt * kTile + 16 * c2 + l16;
+          if (e < n) {
+            sV[e * Rs + r] = tv[c2][i];
+            sRho[e * Rs + r] = tr[c2][i];
+          }
+        }
     }
 
     // P_e tiles and dg over this wave's k tile, edges in pairs so that the
@@ -328,7 +340,7 @@ __global__ __launch_bounds__(direct_waves(MT, RT)* kWave) void k_bwd_dst(BwdDstA
               }
               part += __shfl_xor(part, 32);
               if (h == 0 && (t == 0 || has2))
-                sDG[(kt * kChunk + e) * Rp + rtw[t] * kTile + l32] = part * (sc * gh_unscale[t]);
+                sDG[(kt * kChunk + e) * Rs + rtw[t] * kTile + l32] = part * (sc * gh_unscale[t]);
             }
           }
         }
@@ -336,61 +348,66 @@ __global__ __launch_bounds__(direct_waves(MT, RT)* kWave) void k_bwd_dst(BwdDstA
     }
     __syncthreads();
     for (int i = tid; i < n * Rp; i += blockDim.x) {
-      float dg = sDG[i];
+      const int e = i / Rp, r = i - e * Rp, j = e * Rs + r;
+      float dg = sDG[j];
 #pragma unroll
-      for (int k2 = 1; k2 < MT; ++k2) dg += sDG[k2 * kChunk * Rp + i];
-      const float dv = dg * sRho[i], drho = dg * sV[i];
-      sV[i] = dv;
-      sRho[i] = drho;
-      if (a.drho) {  // drho rows for the radial-weight gradient
-        const int e = i / Rp, r = i - e * Rp;
-        if (r < R) a.drho[size_t(sEid[e]) * R + r] = drho;
-      }
+      for (int k2 = 1; k2 < MT; ++k2) dg += sDG[k2 * kChunk * Rs + j];
+      const float dv = dg * sRho[j], drho = dg * sV[j];
+      sV[j] = dv;
+      sRho[j] = drho;
+      if (a.drho && r < R) a.drho[size_t(sEid[e]) * R + r] = drho;  // for the radial-weight gradient
     }
     __syncthreads();
-    // dY = dV B^T (k < d <= 64: two output tiles) and dphi = dRho Wrad^T (one
-    // tile) on fp32 MFMA with one rank tile as the contraction range; the
-    // per-tile partials (RT tiles x 3 outputs x kChunk rows x 32 floats =
-    // 3 kChunk Rp) go to the v/rho/dg region ((2 + MT) kChunk Rp floats) and
-    // are summed over the rank tiles in a fixed order.
+    // dY = dV B^T (columns k < d <= 64: four 16-column tiles) and dphi =
+    // dRho Wrad^T (columns q < n_radial <= 16: one tile) on 16x16x4 fp32
+    // MFMA, contraction over one rank tile of 32 per wave (eight steps), B
+    // and Wrad read from their transposed copies (a quarter-wave's operands
+    // then lie in one row: coalesced loads); the per-tile partials
+    // ([RT][kChunk][kPy] floats) go to the v/rho/dg region ((2 + MT) kChunk
+    // Rs floats) and are summed over the rank tiles in a fixed order.
     {
-      f32x16 py[3] = {f32x16{}, f32x16{}, f32x16{}};
+      f32x4 py[5] = {f32x4{}, f32x4{}, f32x4{}, f32x4{}, f32x4{}};
       const int rt = wave;  // RT <= NW: one rank tile per wave at most
+      const float* __restrict__ BT = a.bt;            // [R][d]
+      const float* __restrict__ WT = a.bt + d * R;    // [R][n_radial]
       if (rt < RT) {
 #pragma unroll 4
-        for (int s2 = 0; s2 < kTile / 2; ++s2) {
-          const int rr = rt * kTile + 2 * s2 + h;
-          const float a_v = l32 < n ? sV[l32 * Rp + rr] : 0.f;
-          const float a_r = l32 < n ? sRho[l32 * Rp + rr] : 0.f;
+        for (int s4 = 0; s4 < kTile / 4; ++s4) {
+          const int rr = rt * kTile + 4 * s4 + g4;
           const bool rok = rr < R;
-          const float b0 = (rok && l32 < d) ? a.Bf[l32 * R + rr] : 0.f;
-          const float b1 = (rok && kTile + l32 < d) ? a.Bf[(kTile + l32) * R + rr] : 0.f;
-          const float b2 = (rok && l32 < nr) ? a.radial_w[l32 * R + rr] : 0.f;
-          py[0] = mfma32(a_v, b0, py[0]);
-          py[1] = mfma32(a_v, b1, py[1]);
-          py[2] = mfma32(a_r, b2, py[2]);
+          const float a_v = l16 < n ? sV[l16 * Rs + rr] : 0.f;
+          const float a_r = l16 < n ? sRho[l16 * Rs + rr] : 0.f;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            if (16 * t >= d) break;
+            const int k = 16 * t + l16;
+            const float bv = (rok && k < d) ? BT[rr * d + k] : 0.f;
+            py[t] = mfma16f32(a_v, bv, py[t]);
+          }
+          const float bw = (rok && l16 < nr) ? WT[rr * nr + l16] : 0.f;
+          py[4] = mfma16f32(a_r, bw, py[4]);
         }
       }
       __syncthreads();  // every wave has read dv and drho
       float* sPart = sV;
       if (rt < RT) {
 #pragma unroll
-        for (int t3 = 0; t3 < 3; ++t3)
+        for (int t = 0; t < 5; ++t)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int e = acc_row(v, h);
-            if (e < n) sPart[((rt * 3 + t3) * kChunk + e) * kTile + l32] = py[t3][v];
+          for (int i = 0; i < 4; ++i) {
+            const int e = 4 * g4 + i;
+            if (e < n) sPart[(rt * kChunk + e) * kPy + 16 * t + l16] = py[t][i];
           }
       }
       __syncthreads();
-      for (int i = tid; i < n * 3 * kTile; i += blockDim.x) {
-        const int e = i / (3 * kTile), c = i - e * 3 * kTile, t3 = c / kTile, col = c - t3 * kTile;
+      for (int i = tid; i < n * kPy; i += blockDim.x) {
+        const int e = i / kPy, c = i - e * kPy;
         float sum = 0.f;
-        for (int w = 0; w < RT; ++w) sum += sPart[((w * 3 + t3) * kChunk + e) * kTile + col];
-        if (t3 < 2) {
-          if (t3 * kTile + col < d) sDY[e * d + t3 * kTile + col] = sum;
-        } else if (col < nr) {
-          sDPhi[e * nr + col] = sum;
+        for (int w = 0; w < RT; ++w) sum += sPart[(w * kChunk + e) * kPy + c];
+        if (c < 64) {
+          if (c < d) sDY[e * d + c] = sum;
+        } else if (c - 64 < nr) {
+          sDPhi[e * nr + c - 64] = sum;
         }
       }
     }
@@ -419,10 +436,24 @@ __global__ __launch_bounds__(direct_waves(MT, RT)* kWave) void k_bwd_dst(BwdDstA
   }
 }
 
+namespace {
+// out[c][r] = in[r][c] for an [rows, cols] row-major input
+__global__ __launch_bounds__(256) void k_transpose(int rows, int cols, const float* __restrict__ in,
+                                                   float* __restrict__ out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * cols) return;
+  const int c = i / rows, r = i - c * rows;
+  out[i] = in[size_t(r) * cols + c];
+}
+}  // namespace
+
 template <int MT, int RT, int NCT, bool BF>
 hipError_t launch_k(const BwdDstArgs& a, hipStream_t s) {
   const size_t lds = size_t(dst_smem(RT, MT, a.d, a.n_radial, a.C).floats) * 4;
-  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  if (lds > 160 * 1024 || !a.bt) return hipErrorInvalidValue;
+  k_transpose<<<dim3((a.d * a.R + 255) / 256), dim3(256), 0, s>>>(a.d, a.R, a.Bf, a.bt);
+  k_transpose<<<dim3((a.n_radial * a.R + 255) / 256), dim3(256), 0, s>>>(a.n_radial, a.R, a.radial_w,
+                                                                           a.bt + size_t(a.d) * a.R);
   auto k = k_bwd_dst<MT, RT, NCT, BF>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      int(lds));

@@ -265,6 +265,8 @@ struct BwdDstArgs {
   int n_range;              // equal edge ranges (bwd_dst_plan)
   int pieces_per_block;     // ranges per workgroup
   float* drho;              // [E, R] by edge id: dL/drho_e, or nullptr (not stored); per-segment kernels
+  float* bt;                // direct kernel (d > 32): workspace of (d + n_radial) R floats for B^T
+                            // [R, d] and Wrad^T [R, n_radial], written by its launch
   // range kernel only:
   float* wrad_part;         // [n_range / pieces_per_block, n_radial, R]: each workgroup's share of
                             // grad_radial_w (sum them in order), or nullptr
