@@ -706,28 +706,42 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
       __syncthreads();
       // g = (Y B) * (Phi Wrad) for the chunk's edges (rows) and all ranks
       // (columns): two small fp32 MFMA GEMMs per 32x32 tile, one rank tile per
-      // wave, with B and Wrad read from global memory (cached).  Rows beyond n
-      // hold zeros (their A operand is masked) and are never read.
+      // wave, with B and Wrad read from global memory (cached; n_radial <= 16,
+      // so Wrad's operands are at most 8 steps).  Rows beyond n hold zeros
+      // (their A operand is masked) and are never read.
       const int n_et = (n + kTile - 1) / kTile;
       for (int item = wave; item < n_et * RT; item += waves) {
         const int et = item / RT, rt = item - et * RT;
         const int er = et * kTile + l32;  // this lane's edge row
         const bool row_ok = er < n;
         const int r = rt * kTile + l32, rc = r < R ? r : R - 1;
-        f32x16 Tr = f32x16{}, Ty = f32x16{};
-  #pragma unroll 1
-        for (int s2 = 0; s2 < (nr + 1) / 2; ++s2) {
+        // every B and Wrad operand of the two chains loaded before the first
+        // product (one memory latency per item instead of one per step)
+        constexpr int KY = (d + 1) / 2;
+        float bq[8], by[KY];
+#pragma unroll
+        for (int s2 = 0; s2 < 8; ++s2) {
           const int q = 2 * s2 + h, qc = q < nr ? q : nr - 1;
-          const float av = (row_ok && q < nr) ? sPhi[er * nr + q] : 0.f;
-          const float bw = a.radial_w[qc * R + rc];
-          Tr = mfma32(av, (q < nr && r < R) ? bw : 0.f, Tr);
+          bq[s2] = 2 * s2 < nr ? a.radial_w[qc * R + rc] : 0.f;
         }
-  #pragma unroll
-        for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
+#pragma unroll
+        for (int s2 = 0; s2 < KY; ++s2) {
           const int k = 2 * s2 + h, kc = k < d ? k : d - 1;
+          by[s2] = a.Bf[kc * R + rc];
+        }
+        f32x16 Tr = f32x16{}, Ty = f32x16{};
+#pragma unroll
+        for (int s2 = 0; s2 < 8; ++s2) {
+          if (2 * s2 >= nr) break;
+          const int q = 2 * s2 + h;
+          const float av = (row_ok && q < nr) ? sPhi[er * nr + q] : 0.f;
+          Tr = mfma32(av, (q < nr && r < R) ? bq[s2] : 0.f, Tr);
+        }
+#pragma unroll
+        for (int s2 = 0; s2 < KY; ++s2) {
+          const int k = 2 * s2 + h;
           const float av = (row_ok && k < d) ? sY[er * d + k] : 0.f;
-          const float bw = a.Bf[kc * R + rc];
-          Ty = mfma32(av, (k < d && r < R) ? bw : 0.f, Ty);
+          Ty = mfma32(av, (k < d && r < R) ? by[s2] : 0.f, Ty);
         }
   #pragma unroll
         for (int v = 0; v < 16; ++v) {
