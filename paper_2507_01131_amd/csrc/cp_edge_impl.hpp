@@ -108,10 +108,16 @@ __host__ __device__ constexpr bool edge_rega(int L, int RT, bool bf) {
   return !bf && 4 * pk_blocks((L + 1) * (L + 1)) * RT <= (edge_waves_per_eu(L, RT, bf) == 2 ? 80 : 160);
 }
 
-// Most ranges a workgroup takes: one.  (Two ranges per workgroup, dealt so
-// that an XCD's workgroups work on neighbouring edges, ran as fast but write
-// twice the partial rows of the segments that cross range ends.)
-__host__ __device__ constexpr int edge_max_ranges(int, int, bool) { return 1; }
+// Most ranges a workgroup takes: two where two workgroups share a CU (taken
+// as ranges b and b + n_blocks, so that at any time an XCD's workgroups
+// gather from a window of neighbouring nodes that fits its L2: one range
+// per workgroup ran 1-3 % faster at the headline shape, its misses served
+// from the MALL, but read five times the bytes past L2), one otherwise (the
+// extra loop level costs registers that a one-wave kernel spends on
+// accumulators).
+__host__ __device__ constexpr int edge_max_ranges(int L, int RT, bool bf) {
+  return edge_waves_per_eu(L, RT, bf) == 2 ? 2 : 1;
+}
 
 // bf16 mode: whether this lane's K factor values (KB * RT * 8 floats) stay
 // in registers instead of LDS.  Never: two waves per SIMD, which the registers
@@ -715,35 +721,55 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
         const int er = et * kTile + l32;  // this lane's edge row
         const bool row_ok = er < n;
         const int r = rt * kTile + l32, rc = r < R ? r : R - 1;
-        // every B and Wrad operand of the two chains loaded before the first
-        // product (one memory latency per item instead of one per step)
-        constexpr int KY = (d + 1) / 2;
-        float bq[8], by[KY];
-#pragma unroll
-        for (int s2 = 0; s2 < 8; ++s2) {
-          const int q = 2 * s2 + h, qc = q < nr ? q : nr - 1;
-          bq[s2] = 2 * s2 < nr ? a.radial_w[qc * R + rc] : 0.f;
-        }
-#pragma unroll
-        for (int s2 = 0; s2 < KY; ++s2) {
-          const int k = 2 * s2 + h, kc = k < d ? k : d - 1;
-          by[s2] = a.Bf[kc * R + rc];
-        }
         f32x16 Tr = f32x16{}, Ty = f32x16{};
+        if constexpr (edge_waves_per_eu(L, RT, BF) == 1) {
+          // one wave per SIMD (registers to spare): every B and Wrad operand
+          // of the two chains loaded before the first product, one memory
+          // latency per item instead of one per radial step
+          constexpr int KY = (d + 1) / 2;
+          float bq[8], by[KY];
 #pragma unroll
-        for (int s2 = 0; s2 < 8; ++s2) {
-          if (2 * s2 >= nr) break;
-          const int q = 2 * s2 + h;
-          const float av = (row_ok && q < nr) ? sPhi[er * nr + q] : 0.f;
-          Tr = mfma32(av, (q < nr && r < R) ? bq[s2] : 0.f, Tr);
+          for (int s2 = 0; s2 < 8; ++s2) {
+            const int q = 2 * s2 + h, qc = q < nr ? q : nr - 1;
+            bq[s2] = 2 * s2 < nr ? a.radial_w[qc * R + rc] : 0.f;
+          }
+#pragma unroll
+          for (int s2 = 0; s2 < KY; ++s2) {
+            const int k = 2 * s2 + h, kc = k < d ? k : d - 1;
+            by[s2] = a.Bf[kc * R + rc];
+          }
+#pragma unroll
+          for (int s2 = 0; s2 < 8; ++s2) {
+            if (2 * s2 >= nr) break;
+            const int q = 2 * s2 + h;
+            const float av = (row_ok && q < nr) ? sPhi[er * nr + q] : 0.f;
+            Tr = mfma32(av, (q < nr && r < R) ? bq[s2] : 0.f, Tr);
+          }
+#pragma unroll
+          for (int s2 = 0; s2 < KY; ++s2) {
+            const int k = 2 * s2 + h;
+            const float av = (row_ok && k < d) ? sY[er * d + k] : 0.f;
+            Ty = mfma32(av, (k < d && r < R) ? by[s2] : 0.f, Ty);
+          }
+        } else {
+          // two waves per SIMD: the loads inside the chains (hoisting them
+          // spilled registers of the edge loop)
+#pragma unroll 1
+          for (int s2 = 0; s2 < (nr + 1) / 2; ++s2) {
+            const int q = 2 * s2 + h, qc = q < nr ? q : nr - 1;
+            const float av = (row_ok && q < nr) ? sPhi[er * nr + q] : 0.f;
+            const float bw = a.radial_w[qc * R + rc];
+            Tr = mfma32(av, (q < nr && r < R) ? bw : 0.f, Tr);
+          }
+#pragma unroll
+          for (int s2 = 0; s2 < (d + 1) / 2; ++s2) {
+            const int k = 2 * s2 + h, kc = k < d ? k : d - 1;
+            const float av = (row_ok && k < d) ? sY[er * d + k] : 0.f;
+            const float bw = a.Bf[kc * R + rc];
+            Ty = mfma32(av, (k < d && r < R) ? bw : 0.f, Ty);
+          }
         }
 #pragma unroll
-        for (int s2 = 0; s2 < KY; ++s2) {
-          const int k = 2 * s2 + h;
-          const float av = (row_ok && k < d) ? sY[er * d + k] : 0.f;
-          Ty = mfma32(av, (k < d && r < R) ? by[s2] : 0.f, Ty);
-        }
-  #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int e = et * kTile + acc_row(v, h);
           sG[e * Rp + rt * kTile + l32] = BF ? Tr[v] * Ty[v] : Tr[v] * Ty[v] * (e < n ? sSc[e] : 0.f);
