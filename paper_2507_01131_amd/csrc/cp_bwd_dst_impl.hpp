@@ -9,8 +9,9 @@
 // and then  dv = dg * rho,  drho = dg * v,  dY = B dv,  dphi = Wrad drho,
 //   grad r_e = J_Y(r_e)^T dY + (sum_q dphi_q phi'_q(|r_e|)) r_e/|r_e|.
 //
-// One workgroup per destination segment, one wave per 32-rank tile.  Each
-// wave forms its Gh^T tiles once (fp32 MFMA, K = d); in accumulator layout
+// One workgroup per destination segment; each wave takes one 32-row k tile
+// and a pair of 32-rank tiles.  Each wave forms its two Gh^T tiles once
+// (fp32 MFMA, K = d); in accumulator layout
 // lane l holds Gh^T[ct*32 + acc_row(v, l/32)][rt*32 + l%32], so registers
 // 8q .. 8q+7 are the B operand of one 32x32x16 step of P_e = x[s_e] Gh^T
 // that contracts channels ct*32 + 16q + 8(i/4) + 4h + i%4 (i = 0..7) in
@@ -23,8 +24,14 @@
 // parts each (to 2^-22) and P_e sums the three part products with i + j <= 3
 // on v_mfma_f32_32x32x16_f16, fp32 accumulation; dg carries both scales back
 // (exactly).  bf16 problems: x is bf16 and Gh^T is rounded to bf16, one
-// product on v_mfma_f32_32x32x16_bf16.  dg is a 32-term dot product with A
-// held in registers plus one cross-half add.
+// product on v_mfma_f32_32x32x16_bf16.  dg over the wave's k tile is a
+// 32-term dot product with A (from LDS, in accumulator order) plus one
+// cross-half add; the two k tiles' parts are added in a fixed order.
+//
+// Per chunk of 16 edges the small products v = Y B, rho = Phi Wrad, dY =
+// dV B^T and dphi = dRho Wrad^T run on 16x16x4 fp32 MFMA (the chunk's edges
+// are one tile's rows), dY and dphi reading B and Wrad from transposed
+// copies that the launch writes (coalesced operand loads).
 #pragma once
 
 #include "common.hpp"
