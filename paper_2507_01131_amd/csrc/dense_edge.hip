@@ -66,7 +66,7 @@ __host__ __device__ constexpr int dense_un_rows(int d) { return dense_un_tiles(d
 __host__ __device__ constexpr int dense_eb_un(int) { return 2; }
 
 struct DenseSmem {
-  int off_k, off_y, off_phi, off_rho, off_row, off_sc, off_ksc, off_max, floats;
+  int off_k, off_y, off_phi, off_rho, off_row, off_sc, off_ksc, off_max, off_pre, floats;
 };
 __host__ __device__ inline DenseSmem dense_smem(int d, int n_path, bool un = false) {
   const int eb = un ? dense_eb_un(d) : dense_eb(d);
@@ -88,12 +88,15 @@ __host__ __device__ inline DenseSmem dense_smem(int d, int n_path, bool un = fal
   o += eb;
   s.off_max = o;
   o += kMaxWaves * eb;
+  s.off_pre = o;  // UN: first item of each of the launch's paths
+  o += un ? kMaxPaths + 1 : 0;
   s.floats = o;
   return s;
 }
 
 template <int L, int CTW, bool UN = false>
-__global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves, PathRows pt, int row0, float* zp) {
+__global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves, PathRows pt, int row0, int p_lo, int p_hi,
+                                                    float* zp) {
   constexpr int d = (L + 1) * (L + 1);
   constexpr int DP = dense_dp(d), KC = dense_kc(d), KS = dense_ks(d), EB = UN ? dense_eb_un(d) : dense_eb(d);
   constexpr int KB = DP / 16, RK = UN ? dense_un_tiles(d) : DP / 32;
@@ -119,6 +122,19 @@ __global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves, Path
   // K's padding columns (d .. KC-1) stay zero; every (k, i) with k, i < d is
   // rewritten for each batch
   for (int t = tid; t < EB * KR * KS; t += nthr) sK[t] = 0.f;
+  // UN over part of the paths (several launches): the launch's (path, m3,
+  // m1) items, path p_lo + u from item pre[u]; over all paths (one launch):
+  // the (k, i) rows, each walked once
+  const bool un_items = UN && p_hi - p_lo < pt.n_path;
+  int* sPre = reinterpret_cast<int*>(smem + sm.off_pre);
+  if (un_items && tid == 0) {
+    int acc = 0;
+    for (int p = p_lo; p < p_hi; ++p) {
+      sPre[p - p_lo] = acc;
+      acc += (2 * pt.l3[p] + 1) * (2 * pt.l1[p] + 1);
+    }
+    sPre[p_hi - p_lo] = acc;
+  }
 
   f32x16 acc[RK][CTW];
 #pragma unroll
@@ -213,7 +229,46 @@ __global__ __launch_bounds__(256) void k_dense_edge(DenseArgs a, int waves, Path
     float mx[EB];
 #pragma unroll
     for (int e = 0; e < EB; ++e) mx[e] = 0.f;
-    for (int q = tid; q < d * d; q += nthr) {
+    if (un_items) {
+      // item (p, m3, m1) sums the entries of row (k, i) = (l3^2 + m3,
+      // l1^2 + m1) whose j has degree l2 and writes row row[p] + m3 - row0,
+      // column i, zero where the table holds no entry (every row position of
+      // the launch's paths is written; rows outside the chunk are skipped)
+      const int n_item = sPre[p_hi - p_lo];
+      for (int it = tid; it < n_item; it += nthr) {
+        int u = 0;  // the path of item it: the last u with pre[u] <= it
+        for (int step = 128; step > 0; step >>= 1)  // kMaxPaths <= 256
+          if (u + step < p_hi - p_lo && sPre[u + step] <= it) u += step;
+        const int p = p_lo + u, r = it - sPre[u];
+        const int l1 = pt.l1[p], l2 = pt.l2[p], l3 = pt.l3[p];
+        const int m3 = r / (2 * l1 + 1), m1 = r - m3 * (2 * l1 + 1);
+        const int row = pt.row[p] + m3 - row0;
+        if (row < 0 || row >= KR) continue;
+        const int k = l3 * l3 + m3, i = l1 * l1 + m1, q = k * d + i;
+        int s0 = a.cg_row[q], s1 = a.cg_row[q + 1];
+        s0 = max(0, min(s0, a.cg_nnz));
+        s1 = max(s0, min(s1, a.cg_nnz));
+        float v[EB];
+#pragma unroll
+        for (int e = 0; e < EB; ++e) v[e] = 0.f;
+        for (int s = s0; s < s1; ++s) {
+          const int j = a.cg_col[s] & 0xffff;
+          if (j >= (l2 + 1) * (l2 + 1)) break;
+          if (j < l2 * l2) continue;
+          const float cv = a.cg_val[s];
+#pragma unroll
+          for (int e = 0; e < EB; ++e)
+            if (e < nb) v[e] = fmaf(cv, sY[e * d + j] * sRho[e * P + p], v[e]);
+        }
+#pragma unroll
+        for (int e = 0; e < EB; ++e)
+          if (e < nb) {
+            sK[(e * KR + row) * KS + i] = v[e];
+            mx[e] = fmaxf(mx[e], fabsf(v[e]));
+          }
+      }
+    }
+    for (int q = tid; q < (un_items ? 0 : d * d); q += nthr) {
       const int k = q / d, i = q - k * d;
       int s0 = a.cg_row[q], s1 = a.cg_row[q + 1];
       s0 = max(0, min(s0, a.cg_nnz));
@@ -348,7 +403,7 @@ hipError_t launch_l_ctw(const DenseArgs& a, int waves, hipStream_t s) {
       hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
   if (e != hipSuccess) return e;
   PathRows none{};
-  k<<<dim3(a.N), dim3(waves * kWave), lds, s>>>(a, waves, none, 0, nullptr);
+  k<<<dim3(a.N), dim3(waves * kWave), lds, s>>>(a, waves, none, 0, 0, 0, nullptr);
   return hipGetLastError();
 }
 
@@ -365,7 +420,12 @@ hipError_t launch_l_un(const DenseArgs& a, float* zp, hipStream_t s) {
       hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
   if (e != hipSuccess) return e;
   for (int row0 = 0; row0 < pt.n_rows; row0 += dense_un_rows(d)) {
-    k<<<dim3(a.N), dim3(n_ct * kWave), lds, s>>>(a, n_ct, pt, row0, zp);
+    // the paths whose rows meet [row0, row0 + rows of a launch)
+    int p_lo = 0;
+    while (p_lo < pt.n_path && pt.row[p_lo] + 2 * pt.l3[p_lo] + 1 <= row0) ++p_lo;
+    int p_hi = p_lo;
+    while (p_hi < pt.n_path && pt.row[p_hi] < row0 + dense_un_rows(d)) ++p_hi;
+    k<<<dim3(a.N), dim3(n_ct * kWave), lds, s>>>(a, n_ct, pt, row0, p_lo, p_hi, zp);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -399,6 +459,8 @@ PathRows path_rows(int L) {
       const int lo = l1 > l2 ? l1 - l2 : l2 - l1, hi = l1 + l2 < L ? l1 + l2 : L;
       if (l1 * (L + 1) + l2 < kMaxDegPairs) t.first[l1 * (L + 1) + l2] = p;
       for (int l3 = lo; l3 <= hi && p < kMaxPaths; ++l3, ++p) {
+        t.l1[p] = l1;
+        t.l2[p] = l2;
         t.l3[p] = l3;
         t.row[p] = row;
         row += 2 * l3 + 1;

@@ -204,7 +204,7 @@ constexpr int kMaxPaths = 176;
 constexpr int kMaxDegPairs = 49;
 struct PathRows {
   int n_path, n_rows;
-  int l3[kMaxPaths];
+  int l1[kMaxPaths], l2[kMaxPaths], l3[kMaxPaths];
   int row[kMaxPaths];
   int first[kMaxDegPairs];
 };
