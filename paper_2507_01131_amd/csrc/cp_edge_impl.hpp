@@ -107,6 +107,29 @@ __host__ __device__ constexpr int edge_waves_per_eu(int L, int RT, bool bf) {
 __host__ __device__ constexpr bool edge_rega(int L, int RT, bool bf) {
   return !bf && 4 * pk_blocks((L + 1) * (L + 1)) * RT <= (edge_waves_per_eu(L, RT, bf) == 2 ? 80 : 160);
 }
+// Split mode: rank tiles whose factor blocks stay in registers through a run
+// of edges.  All of them with edge_rega; otherwise, at one wave per SIMD, as
+// many as 80 registers hold (the other tiles' blocks are read from LDS per
+// edge): at L = 6, R = 256 two of eight tiles, which took the slab edge pass
+// from 3.18-3.21 to 3.04-3.06 ms (three tiles: 3.08; four spilled).
+__host__ __device__ constexpr int edge_reg_tiles(int L, int RT, bool bf) {
+  return bf ? 0
+            : edge_rega(L, RT, bf)
+                  ? RT
+                  : (edge_waves_per_eu(L, RT, bf) == 1
+                         ? (RT < 80 / (4 * pk_blocks((L + 1) * (L + 1))) ? RT : 80 / (4 * pk_blocks((L + 1) * (L + 1))))
+                         : 0);
+}
+// Split mode: the rank tile at position p of an edge's sequence of NRA
+// register tiles (0 .. NRA-1) and RT - NRA LDS tiles (NRA .. RT-1): a
+// register tile first, then the two kinds alternate while both last, so
+// that the LDS reads of the next LDS tile overlap two MFMA chains instead of
+// one; identity when all tiles or none are in registers.
+__host__ __device__ constexpr int edge_tile_at(int p, int RT, int NRA) {
+  const int NL = RT - NRA, m = NRA < NL ? NRA : NL;
+  if (p < 2 * m) return (p & 1) ? NRA + p / 2 : p / 2;
+  return NRA > NL ? p - m : p;
+}
 
 // Most ranges a workgroup takes: two where two workgroups share a CU (taken
 // as ranges b and b + n_blocks, so that at any time an XCD's workgroups
@@ -217,6 +240,8 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   constexpr int PN = pk_rows(d), PB = pk_blocks(d), PQ = PN / 4, PT = PN % 4;
   extern __shared__ float smem[];
   constexpr bool kRegA = edge_rega(L, RT, BF) && ABL != 1;
+  // split mode: rank tiles 0 .. NRA-1 take their factor blocks from registers
+  constexpr int NRA = ABL == 1 ? 0 : edge_reg_tiles(L, RT, BF);
   const EdgeSmem S = edge_smem(RT, BF, d, a.n_radial, chunk, T3, kRegA, ATT);
   u32x4* sA = reinterpret_cast<u32x4*>(smem + S.off_a);
   u32x4* sA2 = reinterpret_cast<u32x4*>(smem + S.off_a2);
@@ -330,15 +355,16 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   __syncthreads();
   // Split mode with kRegA: every packed factor block is loaded into
   // registers at the start of each run of edges of one segment within a chunk
-  // (areg[b * RT + rt]) from the copy the launch's block kernel wrote in
-  // global memory (20 KB at R = 128, cache resident; no LDS for the factor,
-  // which leaves room for 64-edge chunks at two workgroups per CU), so the
-  // edge loop reads no factor while the geometry phase and the segment
-  // epilogue do not hold them.  Otherwise the blocks are read from LDS where
+  // (areg[b * NRA + rt], NRA = RT) from the copy the launch's block kernel
+  // wrote in global memory (20 KB at R = 128, cache resident; no LDS for the
+  // factor, which leaves room for 64-edge chunks at two workgroups per CU), so
+  // the edge loop reads no factor while the geometry phase and the segment
+  // epilogue do not hold them.  Otherwise the blocks of rank tiles below NRA
+  // are loaded the same way from LDS, and the rest are read from LDS where
   // they are used.  Either way their index goes through an opaque copy (zero
   // added in inline asm) so that the compiler does not hoist the reads out of
   // the loops.
-  u32x4 areg[kRegA ? PB * RT : 1];
+  u32x4 areg[NRA > 0 ? PB * NRA : 1];
   // kRegA: the packed blocks written by the launch (k_ef_blocks), after EF's
   const u32x4* __restrict__ kfg = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.ef_ops) +
                                                                 edge_ef_blocks_bytes(d, R));
@@ -412,7 +438,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   // multiplied back into Z; bf16 problems: H and EF rounded to bf16, one
   // product.  part < 0 writes the segment's output row, part 0 or 1 the
   // range's partial slot; the accumulators restart from zero.
-  const u32x4* __restrict__ efb = static_cast<const u32x4*>(a.ef_ops);
+  const char* __restrict__ efb = static_cast<const char*>(a.ef_ops);
   const float ef_unscale = BF ? 1.f : *a.ef_scale;
   int range = 0;
   auto finish = [&](int seg, int part) {
@@ -422,14 +448,22 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
     // parts), double-buffered: tile 0's loads go out first, before the scale
     // reduction, and tile rt+1's while tile rt computes, so no step waits a
     // full memory latency for its operand
+    // (32-bit byte offsets from an opaque lane term: as 64-bit addresses the
+    // compiler kept all MT * RT * 2 * P16 of them live across the edge loop,
+    // which at L = 4 spilled 18 registers per lane and slowed the edge pass by
+    // 3-4 %)
     u32x4 ef[2][MT][2][P16];
+    uint32_t ef_lane = uint32_t(lane) * P16 * 16;
+    asm volatile("" : "+v"(ef_lane));
     auto load_ef = [&](int rt, int buf) {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int q = 0; q < 2; ++q)
 #pragma unroll
-          for (int p = 0; p < P16; ++p) ef[buf][mt][q][p] = efb[((((mt * RT + rt) * 2 + q) * kWave) + lane) * P16 + p];
+          for (int p = 0; p < P16; ++p)
+            ef[buf][mt][q][p] = *reinterpret_cast<const u32x4*>(
+                efb + (ef_lane + uint32_t(((((mt * RT + rt) * 2 + q) * kWave) * P16 + p) * 16)));
     };
     load_ef(0, 0);
     if constexpr (T3) {
@@ -600,7 +634,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
     } else {
       int ab = lane;
       asm volatile("" : "+v"(ab));
-      u32x4 am[kRegA ? 1 : 2][kRegA ? 1 : PB];  // [buffer][packed K-block] when read from LDS
+      u32x4 am[NRA == RT ? 1 : 2][NRA == RT ? 1 : PB];  // [buffer][packed K-block] of the LDS tiles
       float gl[RT];
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) gl[rt] = sG[e * Rp + rt * kTile + l32];
@@ -611,7 +645,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
       }
       f32x16 U[2];
       auto load_a = [&](int rt, int buf) {
-        if constexpr (!kRegA) {
+        if constexpr (NRA < RT) {
 #pragma unroll
           for (int b = 0; b < PB; ++b) am[buf][b] = a_op(ab, b, rt);
         }
@@ -620,10 +654,10 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
         f32x16 u = f32x16{};
 #pragma unroll
         for (int b = 0; b < PB; ++b) {
-          if constexpr (kRegA)
-            u = mfma_f16(xop(xb, b), areg[b * RT + rt], u);
+          if (rt < NRA)
+            u = mfma_f16(xop(xb, b), areg[b * NRA + (rt < NRA ? rt : 0)], u);
           else
-            u = mfma_f16(xop(xb, b), am[buf][b], u);
+            u = mfma_f16(xop(xb, b), am[NRA == RT ? 0 : (rt - NRA) & 1][b], u);
         }
         U[buf] = u;
       };
@@ -631,16 +665,20 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[rt][0][v] += gl[rt] * U[buf][v];
       };
-      load_a(0, 0);
+      // positions p in the order edge_tile_at gives; an LDS tile's blocks are
+      // read while the chains before it run (the first LDS tile's from the
+      // edge's start, the next one's from the previous LDS tile's chain on)
+      if (NRA < RT) load_a(NRA, 0);
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        if (rt + 1 < RT) load_a(rt + 1, (rt + 1) & 1);
+      for (int p = 0; p < RT; ++p) {
+        const int rt = edge_tile_at(p, RT, NRA);
+        if (rt >= NRA && rt + 1 < RT) load_a(rt + 1, (rt + 1 - NRA) & 1);
         __builtin_amdgcn_sched_barrier(0);
-        chain(rt, rt & 1);
-        if (rt > 0) fma_rt(rt - 1, (rt - 1) & 1);
+        chain(rt, p & 1);
+        if (p > 0) fma_rt(edge_tile_at(p - 1, RT, NRA), (p - 1) & 1);
         __builtin_amdgcn_sched_barrier(0);
       }
-      fma_rt(RT - 1, (RT - 1) & 1);
+      fma_rt(edge_tile_at(RT - 1, RT, NRA), (RT - 1) & 1);
     }
   };
 
@@ -803,6 +841,13 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
           asm volatile("" : "+v"(ai));
 #pragma unroll
           for (int i = 0; i < PB * RT; ++i) areg[i] = kfg[ai + i * kWave];
+        } else if constexpr (NRA > 0) {
+          int ai = lane;
+          asm volatile("" : "+v"(ai));
+#pragma unroll
+          for (int b = 0; b < PB; ++b)
+#pragma unroll
+            for (int rt = 0; rt < NRA; ++rt) areg[b * NRA + rt] = sA[ai + (b * RT + rt) * kWave];
         }
         // Two operand buffers used alternately: the loads of edge f+1 are
         // issued before the MFMAs of edge f, and the scheduling barriers keep
