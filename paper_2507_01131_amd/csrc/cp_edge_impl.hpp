@@ -760,10 +760,12 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
         const bool row_ok = er < n;
         const int r = rt * kTile + l32, rc = r < R ? r : R - 1;
         f32x16 Tr = f32x16{}, Ty = f32x16{};
-        if constexpr (edge_waves_per_eu(L, RT, BF) == 1) {
-          // one wave per SIMD (registers to spare): every B and Wrad operand
-          // of the two chains loaded before the first product, one memory
-          // latency per item instead of one per radial step
+        if constexpr (edge_waves_per_eu(L, RT, BF) == 1 || L >= 4) {
+          // one wave per SIMD, or L >= 4: every B and Wrad operand of the two
+          // chains loaded before the first product, one memory latency per
+          // item instead of one per radial step (at L = 4 and two waves per
+          // SIMD this holds since the epilogue's addresses stopped taking
+          // registers: headline edge pass 0.409-0.411 -> 0.398-0.399 ms)
           constexpr int KY = (d + 1) / 2;
           float bq[8], by[KY];
 #pragma unroll
@@ -790,8 +792,8 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
             Ty = mfma32(av, (k < d && r < R) ? by[s2] : 0.f, Ty);
           }
         } else {
-          // two waves per SIMD: the loads inside the chains (hoisting them
-          // spilled registers of the edge loop)
+          // L <= 3 at two or more waves per SIMD: the loads inside the chains
+          // (hoisted, they would cost L = 3 its third wave per SIMD)
 #pragma unroll 1
           for (int s2 = 0; s2 < (nr + 1) / 2; ++s2) {
             const int q = 2 * s2 + h, qc = q < nr ? q : nr - 1;
