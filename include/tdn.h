@@ -93,7 +93,11 @@ typedef struct {
 } tdn_problem;
 
 /* Workspace bytes needed by tdn_cp_tp_forward (*fwd_bytes) and
- * tdn_cp_tp_backward (*bwd_bytes); either pointer may be NULL.  The sizes
+ * tdn_cp_tp_backward (*bwd_bytes); either pointer may be NULL.  The
+ * workspace holds the intermediates of the CP layer of Sec. 3.1 and 3.2
+ * (the per-node sums H_t and Z_t = D H_t, the operands in their MFMA
+ * layouts, the destination sort) and of its backward, so its size follows
+ * from N, E, L, C, R and n_radial alone.  The sizes
  * assume z_save == NULL (forward) and z_save == NULL (backward), i.e. the
  * largest case. */
 tdn_status tdn_workspace_size(const tdn_problem* p, size_t* fwd_bytes, size_t* bwd_bytes);
@@ -345,7 +349,12 @@ tdn_status tdn_radius_graph(const tdn_graph_problem* g, const float* pos, const 
                             float* edge_vec, int32_t* edge_image, int32_t* offsets, int64_t* n_edges,
                             void* workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* Stable sort of E integer keys in [0, n_keys): perm[p] = original index of
+/* The grouping step of the layer's sum into destination nodes (the
+ * out[t] sum above, taken over each destination's edges as one contiguous
+ * segment so that the per-edge products of Sec. 3.1 eq. approximate are
+ * summed in registers): a stable sort of the edges by destination,
+ * exported for callers that sort once and pass edges_sorted = 1.
+ * Stable sort of E integer keys in [0, n_keys): perm[p] = original index of
  * the p-th smallest key (equal keys keep their original order), offsets[k] =
  * number of keys < k, offsets[n_keys] = E.  Keys outside the range give
  * undefined perm/offsets (no memory fault).  Workspace from
@@ -368,7 +377,11 @@ tdn_status tdn_ps_linear_workspace_size(int32_t C, int32_t w_dtype, size_t* byte
 tdn_status tdn_ps_linear(int32_t n_nodes, int32_t L, int32_t C, const float* x, const void* W, int32_t w_dtype,
                          float* y, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* Real spherical harmonics of edge directions (basis as above):
+/* Real spherical harmonics of edge directions (basis as above; the
+ * harmonics input of the tensor product, Sec. 2, which the CP layer
+ * contracts with its factor B, Sec. 3.1 eq. approximate), and their
+ * Jacobian, which the backward uses for the gradient with respect to the
+ * edge vectors:
  *   Y  [E, d]     Y(r_e/|r_e|)
  *   dY [E, d, 3]  dY/dr_e (or NULL) */
 tdn_status tdn_spherical_harmonics(int32_t L, int32_t E, const float* edge_vec, float* Y,

@@ -1,4 +1,4 @@
-// Destination-side backward on bf16 MFMA (d <= 32) instantiated for L = 0.
+// Split-form destination-side backward (d <= 32: dg per edge, then geometry and gradients per edge), instantiated for L = 0; fp32 features run on fp16 MFMA with two-part splits, bf16 features on bf16 MFMA.
 #include "cp_bwd_dst2_impl.hpp"
 
 template hipError_t tdn::bwd2_detail::launch_l<0, false>(const tdn::BwdDstArgs&, int, hipStream_t);
