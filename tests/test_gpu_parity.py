@@ -87,6 +87,10 @@ SMALL = [
     # d > 32 with four rank tiles per wave (R a multiple of 128, C <= 128)
     dict(seed=11, N=24, E=450, L=6, C=128, R=256, sort=False),
     dict(seed=12, N=30, E=500, L=5, C=80, R=128, sort=True),
+    # one wave per SIMD with some rank tiles' factor blocks in registers and
+    # the rest from LDS (six and five rank tiles, the last one ragged)
+    dict(seed=13, N=28, E=520, L=5, C=64, R=192, sort=False),
+    dict(seed=14, N=26, E=480, L=6, C=96, R=150, sort=True),
 ]
 
 
