@@ -211,7 +211,7 @@ EdgePlan edge_plan(int L, int R, int C, int n_radial, bool bf16, int E, bool t3)
   const EdgeGrid gr = edge_grid(C, RT, bf16);
   // workgroups per CU: as many as the wave slots (four SIMDs) and LDS allow
   const int lds =
-      edge_smem(RT, bf16, d, n_radial, edge_chunk(L, RT, bf16, n_radial, t3), t3, edge_rega(L, RT, bf16)).floats * 4;
+      edge_smem(RT, bf16, d, n_radial, edge_chunk(L, RT, bf16, n_radial, t3), t3, edge_lds_tiles(L, RT, bf16)).floats * 4;
   int per_cu = 160 * 1024 / lds;
   const int by_waves = 4 * edge_waves_per_eu(L, RT, bf16) / gr.waves;
   if (per_cu > by_waves) per_cu = by_waves;

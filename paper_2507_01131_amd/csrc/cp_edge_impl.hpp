@@ -111,7 +111,9 @@ __host__ __device__ constexpr bool edge_rega(int L, int RT, bool bf) {
 // of edges.  All of them with edge_rega; otherwise, at one wave per SIMD, as
 // many as 80 registers hold (the other tiles' blocks are read from LDS per
 // edge): at L = 6, R = 256 two of eight tiles, which took the slab edge pass
-// from 3.18-3.21 to 3.04-3.06 ms (three tiles: 3.08; four spilled).
+// from 3.18-3.21 to 3.04-3.06 ms (three tiles: 3.08; four spilled).  The LDS
+// then holds only the other tiles' blocks, which at L = 6, R = 256 leaves
+// room for 64-edge chunks instead of 32 (3.10-3.17 -> 2.95-2.96 ms).
 __host__ __device__ constexpr int edge_reg_tiles(int L, int RT, bool bf) {
   return bf ? 0
             : edge_rega(L, RT, bf)
@@ -119,6 +121,12 @@ __host__ __device__ constexpr int edge_reg_tiles(int L, int RT, bool bf) {
                   : (edge_waves_per_eu(L, RT, bf) == 1
                          ? (RT < 80 / (4 * pk_blocks((L + 1) * (L + 1))) ? RT : 80 / (4 * pk_blocks((L + 1) * (L + 1))))
                          : 0);
+}
+// Rank tiles whose factor blocks a workgroup stages in LDS: bf16 mode all of
+// them (as fp32 K values); split mode those not held in registers (all of
+// them for the measurement ablation that reads them from a global copy).
+__host__ __device__ constexpr int edge_lds_tiles(int L, int RT, bool bf, bool abl1 = false) {
+  return bf || abl1 ? RT : RT - edge_reg_tiles(L, RT, bf);
 }
 // Split mode: the rank tile at position p of an edge's sequence of NRA
 // register tiles (0 .. NRA-1) and RT - NRA LDS tiles (NRA .. RT-1): a
@@ -162,25 +170,29 @@ constexpr int kTrStride = 36;
 constexpr int kTrFloats = kTile * kTrStride;
 
 // LDS regions (in floats): the factor operands, split mode
-// [pk_blocks(d)][RT][64 lanes] x 16 bytes of fp16 (packed slots), bf16 mode
+// [pk_blocks(d)][a_tiles][64 lanes] x 16 bytes of fp16 (packed slots) for the
+// a_tiles rank tiles read from LDS, bf16 mode
 // [KB][RT][64 lanes] x 32 bytes of fp32, g for a chunk of edges (rows
 // rounded up to a whole 32-row tile), harmonics, normalised edge vectors with
 // their lengths, radial basis, gathered rows, the edges' operand scales, and
 // the segment starts of the chunk (positions, keys, count and the two
 // partial-segment flags); with t3 (the three-input product) the second node
-// factor's operands in the layout of the first; in split mode last the
-// epilogue's transpose areas, one per wave.
-__host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radial, int chunk, bool t3 = false,
-                                              bool rega = false, bool att = false) {
+// factor's operands in the layout of the first.  In split mode the
+// epilogue's transpose areas (one per wave) share the harmonics' region:
+// the harmonics are read only by the chunk's g products, which end at a
+// barrier before any epilogue, and written only after the next chunk's
+// first barrier.
+__host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radial, int chunk, bool t3, int a_tiles,
+                                              bool att = false) {
   EdgeSmem s{};
   s.Rp = RT * kTile;
   int o = 0;
-  s.off_a = o;  // split mode with rega: none (the blocks come from ef_ops)
-  o += bf ? edge_kb(d) * RT * 2 * kWave * 4 : (rega ? 0 : pk_blocks(d) * RT * kWave * 4);
+  s.off_a = o;
+  o += bf ? edge_kb(d) * RT * 2 * kWave * 4 : pk_blocks(d) * a_tiles * kWave * 4;
   s.off_g = o;
   o += (chunk + kTile - 1) / kTile * kTile * s.Rp;
   s.off_y = o;
-  o += chunk * d;
+  o += bf ? chunk * d : (chunk * d > kMaxWavesPerBlock * kTrFloats ? chunk * d : kMaxWavesPerBlock * kTrFloats);
   o = (o + 3) & ~3;  // float4 rows
   s.off_vec = o;
   o += chunk * 4;
@@ -197,9 +209,7 @@ __host__ __device__ inline EdgeSmem edge_smem(int RT, bool bf, int d, int n_radi
   if (t3) o += pk_blocks(d) * RT * kWave * 4;
   s.off_al = o;  // attention: the chunk's weights [chunk][kMaxHeads]
   if (att) o += chunk * kMaxHeads;
-  (void)rega;
-  s.off_t = o;
-  if (!bf) o += kMaxWavesPerBlock * kTrFloats;
+  s.off_t = bf ? o : s.off_y;
   s.floats = o;
   return s;
 }
@@ -242,7 +252,8 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   constexpr bool kRegA = edge_rega(L, RT, BF) && ABL != 1;
   // split mode: rank tiles 0 .. NRA-1 take their factor blocks from registers
   constexpr int NRA = ABL == 1 ? 0 : edge_reg_tiles(L, RT, BF);
-  const EdgeSmem S = edge_smem(RT, BF, d, a.n_radial, chunk, T3, kRegA, ATT);
+  constexpr int NL = edge_lds_tiles(L, RT, BF, ABL == 1);  // split mode: RT - NRA
+  const EdgeSmem S = edge_smem(RT, BF, d, a.n_radial, chunk, T3, NL, ATT);
   u32x4* sA = reinterpret_cast<u32x4*>(smem + S.off_a);
   u32x4* sA2 = reinterpret_cast<u32x4*>(smem + S.off_a2);
   float4* sAf = reinterpret_cast<float4*>(smem + S.off_a);
@@ -299,7 +310,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   // the chunk loop overwrites only after its first barrier); the edges' g
   // carry 2^e_K back.
   float kf_sc = 1.f, kf_unsc = 1.f;
-  if constexpr (!BF && kRegA) {
+  if constexpr (!BF && NRA > 0) {
     // the blocks and their scale were written by the launch's block kernel
     kf_unsc = a.ef_scale[1];
   } else if constexpr (!BF) {
@@ -343,6 +354,14 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
       sAf[2 * t] = make_float4(v[0], v[1], v[2], v[3]);
       sAf[2 * t + 1] = make_float4(v[4], v[5], v[6], v[7]);
     }
+  } else if constexpr (!kRegA && NRA > 0) {
+    // the LDS tiles' blocks from the launch's packed copy (its scale above)
+    const u32x4* __restrict__ kg =
+        reinterpret_cast<const u32x4*>(static_cast<const char*>(a.ef_ops) + edge_ef_blocks_bytes(d, R));
+    for (int t = tid; t < PB * NL * kWave; t += blockDim.x) {
+      const int ln = t % kWave, bl = t / kWave, b = bl / NL, rt = NRA + (bl - b * NL);
+      sA[t] = kg[(b * RT + rt) * kWave + ln];
+    }
   } else if constexpr (!kRegA) {
     for (int t = tid; t < PB * RT * kWave; t += blockDim.x) stage_packed(a.KF, kf_sc, t, sA);
   }
@@ -360,8 +379,9 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   // factor, which leaves room for 64-edge chunks at two workgroups per CU), so
   // the edge loop reads no factor while the geometry phase and the segment
   // epilogue do not hold them.  Otherwise the blocks of rank tiles below NRA
-  // are loaded the same way from LDS, and the rest are read from LDS where
-  // they are used.  Either way their index goes through an opaque copy (zero
+  // are loaded the same way, and only the other tiles' blocks are staged in
+  // LDS (copied from the same global copy), read from there where they are
+  // used.  Either way their index goes through an opaque copy (zero
   // added in inline asm) so that the compiler does not hoist the reads out of
   // the loops.
   u32x4 areg[NRA > 0 ? PB * NRA : 1];
@@ -372,7 +392,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
     if constexpr (ABL == 1)
       return gA[base + (b * RT + rt) * kWave];
     else
-      return sA[base + (b * RT + rt) * kWave];
+      return sA[base + (b * NL + rt - NRA) * kWave];
   };
   float* sTr = smem + S.off_t + wave * kTrFloats;  // split mode: this wave's transpose area
 
@@ -849,7 +869,7 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
 #pragma unroll
           for (int b = 0; b < PB; ++b)
 #pragma unroll
-            for (int rt = 0; rt < NRA; ++rt) areg[b * NRA + rt] = sA[ai + (b * RT + rt) * kWave];
+            for (int rt = 0; rt < NRA; ++rt) areg[b * NRA + rt] = kfg[ai + (b * RT + rt) * kWave];
         }
         // Two operand buffers used alternately: the loads of edge f+1 are
         // issued before the MFMAs of edge f, and the scheduling barriers keep
@@ -881,7 +901,7 @@ inline int edge_chunk(int L, int RT, bool bf, int n_radial, bool t3 = false, boo
   const int d = (L + 1) * (L + 1);
   const int budget = 160 * 1024 / edge_waves_per_eu(L, RT, bf);
   int chunk = 64;
-  while (chunk > 8 && edge_smem(RT, bf, d, n_radial, chunk, t3, edge_rega(L, RT, bf), att).floats * 4 > budget)
+  while (chunk > 8 && edge_smem(RT, bf, d, n_radial, chunk, t3, edge_lds_tiles(L, RT, bf), att).floats * 4 > budget)
     chunk >>= 1;
   return chunk;
 }
@@ -906,7 +926,7 @@ hipError_t launch_l_rt_m(const EdgeArgs& a, hipStream_t s) {
   if (a.E > 0) {
     const int chunk = edge_chunk(L, RT, BF, a.n_radial, T3, ATT);
     const size_t lds =
-        size_t(edge_smem(RT, BF, d, a.n_radial, chunk, T3, edge_rega(L, RT, BF) && ABL != 1, ATT).floats) * 4;
+        size_t(edge_smem(RT, BF, d, a.n_radial, chunk, T3, edge_lds_tiles(L, RT, BF, ABL == 1), ATT).floats) * 4;
     auto k = k_cp_edge<L, RT, BF, ATOM, T3, ABL, ATT>;
     hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
