@@ -385,7 +385,8 @@ __attribute__((amdgpu_waves_per_eu(edge_waves_per_eu(L, RT, BF)))) void k_cp_edg
   // added in inline asm) so that the compiler does not hoist the reads out of
   // the loops.
   u32x4 areg[NRA > 0 ? PB * NRA : 1];
-  // kRegA: the packed blocks written by the launch (k_ef_blocks), after EF's
+  // the packed blocks written by the launch (k_ef_blocks), after EF's: the
+  // register tiles' source
   const u32x4* __restrict__ kfg = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.ef_ops) +
                                                                 edge_ef_blocks_bytes(d, R));
   auto a_op = [&](int base, int b, int rt) -> u32x4 {
