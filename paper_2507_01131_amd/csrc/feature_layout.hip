@@ -26,17 +26,18 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
 
-// x[node] ([d, C] values, dC = d C a multiple of 16) into LDS as fp32;
-// returns this thread's largest |x|.  Sixteen-byte loads, four per thread
+// x[node] ([d, C] values, dC = d C a multiple of 16) into LDS as fp32, rows
+// contiguous, or C + 1 floats apart when C > 0 is given; returns this
+// thread's largest |x|.  Sixteen-byte loads, four per thread
 // issued before their LDS stores, when the rows are 16-byte aligned; single
 // values otherwise.
 template <typename TI>
-__device__ inline float stage_node(const TI* __restrict__ src, int dC, float* __restrict__ tile) {
+__device__ inline float stage_node(const TI* __restrict__ src, int dC, float* __restrict__ tile, int C = 0) {
   float mx = 0.f;
   if ((reinterpret_cast<uintptr_t>(src) & 15) != 0) {
     for (int i = threadIdx.x; i < dC; i += blockDim.x) {
       const float v = to_f32(src[i]);
-      tile[i] = v;
+      tile[C > 0 ? i + i / C : i] = v;
       mx = fmaxf(mx, fabsf(v));
     }
     return mx;
@@ -67,7 +68,14 @@ __device__ inline float stage_node(const TI* __restrict__ src, int dC, float* __
       }
 #pragma unroll
       for (int j = 0; j < V; j += 4) {
-        *reinterpret_cast<float4*>(tile + i * V + j) = make_float4(v[j], v[j + 1], v[j + 2], v[j + 3]);
+        if (C > 0) {
+          // rows C + 1 floats apart (C a multiple of 16: the run lies in one row)
+          float* o = tile + i * V + j + (i * V) / C;
+#pragma unroll
+          for (int u2 = 0; u2 < 4; ++u2) o[u2] = v[j + u2];
+        } else {
+          *reinterpret_cast<float4*>(tile + i * V + j) = make_float4(v[j], v[j + 1], v[j + 2], v[j + 3]);
+        }
         mx = fmaxf(mx, fmaxf(fmaxf(fabsf(v[j]), fabsf(v[j + 1])), fmaxf(fabsf(v[j + 2]), fabsf(v[j + 3]))));
       }
     }
@@ -231,15 +239,19 @@ hipError_t launch_p(int N, int d, int C, const TI* x, void* xs, float* row_scale
 // direct kernel holds Gh^T in accumulator registers.  P = 2: fp16 hi and lo of x[n] 2^-e_n with
 // 2^e_n (the row's largest |x| to [2^13, 2^14)) in row_scale[n]; P = 1:
 // bf16.  One block per node: its [d, C] rows staged in LDS with their
-// maximum, then one thread per (s, h, k) run of eight channels.
+// maximum, then one thread per (s, h, k) run of eight channels.  The staged
+// rows are C + 1 floats apart: the threads of a wave read one channel of
+// consecutive rows, which with rows C floats apart (C a multiple of 16) all
+// fell in one or two LDS banks.
 template <int P, typename TI, bool PERM>
 __global__ __launch_bounds__(256) void k_direct_layout(int d, int C, int Cp, const TI* __restrict__ x,
                                                        uint16_t* __restrict__ xd, float* __restrict__ row_scale) {
-  extern __shared__ __align__(16) float tile[];  // [d][C], then four floats for the row maximum
-  float* red = tile + d * C;
+  extern __shared__ __align__(16) float tile[];  // [d][C + 1], then four floats for the row maximum
+  const int S = C + 1;
+  float* red = tile + d * S;
   const int n = blockIdx.x;
   const TI* src = x + size_t(n) * d * C;
-  float mx = stage_node(src, d * C, tile);
+  float mx = stage_node(src, d * C, tile, C);  // row k at k (C + 1)
   float sc = 1.f;
   if constexpr (P == 2) {
 #pragma unroll
@@ -263,8 +275,8 @@ __global__ __launch_bounds__(256) void k_direct_layout(int d, int C, int Cp, con
     for (int q = 0; q < 4; ++q) {
       const int i0 = 2 * q;  // elements i0, i0 + 1 of the run
       const int c0 = PERM ? 16 * st + 8 * (i0 / 4) + 4 * h + i0 % 4 : 16 * st + 8 * h + i0;
-      const float v0 = c0 < C ? tile[k * C + c0] : 0.f;
-      const float v1 = c0 + 1 < C ? tile[k * C + c0 + 1] : 0.f;
+      const float v0 = c0 < C ? tile[k * S + c0] : 0.f;
+      const float v1 = c0 + 1 < C ? tile[k * S + c0 + 1] : 0.f;
       if constexpr (P == 2)
         split_f16x2_pair(v0 * sc, v1 * sc, w[0][q], w[1][q]);
       else
@@ -280,7 +292,7 @@ __global__ __launch_bounds__(256) void k_direct_layout(int d, int C, int Cp, con
 template <int P, typename TI>
 hipError_t launch_direct_p(int N, int d, int C, int Cp, const TI* x, void* xd, float* row_scale, bool perm,
                            hipStream_t s) {
-  const size_t lds = (size_t(d) * C + 4) * 4;
+  const size_t lds = (size_t(d) * (C + 1) + 4) * 4;
   auto k = perm ? k_direct_layout<P, TI, true> : k_direct_layout<P, TI, false>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      int(lds));
@@ -296,7 +308,7 @@ int edge_kpad(int d) { return d <= 32 ? 32 : 64; }
 hipError_t launch_direct_layout(int N, int d, int C, int Cp, const void* x, bool x_is_f32, int parts, void* xd,
                                 float* row_scale, bool perm_channels, hipStream_t s) {
   if (N == 0) return hipSuccess;
-  if (Cp < C || Cp % 16 || size_t(d) * C * 4 + 16 > 160 * 1024) return hipErrorInvalidValue;
+  if (Cp < C || Cp % 16 || size_t(d) * (C + 1) * 4 + 16 > 160 * 1024) return hipErrorInvalidValue;
   const bool pm = perm_channels;
   if (parts == 2) {
     if (!x_is_f32 || !row_scale) return hipErrorInvalidValue;
