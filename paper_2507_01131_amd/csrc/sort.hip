@@ -146,38 +146,47 @@ __global__ __launch_bounds__(kSortThreads) void k_digit_scatter(const int32_t* _
   }
 }
 
-// offsets[k] = first index i with sorted_keys[i] >= k, for k in [0, n_keys].
-__global__ void k_offsets(const int32_t* __restrict__ sorted_keys, int E, int n_keys, int32_t* __restrict__ offsets) {
-  const int k = blockIdx.x * blockDim.x + threadIdx.x;
-  if (k > n_keys) return;
-  int lo = 0, hi = E;
-  while (lo < hi) {
-    const int mid = lo + ((hi - lo) >> 1);
-    if (sorted_keys[mid] < k)
-      lo = mid + 1;
-    else
-      hi = mid;
+// offsets[k] = first index i with sorted_keys[i] >= k (E if none), for k in
+// [0, n_keys]: one wave per key, a 64-way search.  Each round the 64 lanes
+// compare the keys at 64 positions spread over the remaining range and the
+// count of keys below k (a ballot) narrows it 65-fold, so 151 k edges take
+// three dependent loads instead of the 17 of a binary search; once at most
+// 64 positions remain, one load per lane settles it.  For keys that are not
+// sorted the result is still some index in [0, E].
+__device__ __forceinline__ void wave_lower_bound(const int32_t* __restrict__ sorted_keys, int E, int k, int lane,
+                                                 int32_t* __restrict__ out) {
+  int lo = 0, hi = E;  // the answer lies in [lo, hi]
+  while (hi - lo > kWave) {
+    const int q = lo + int(int64_t(hi - lo) * (lane + 1) / (kWave + 1));  // lo <= q < hi
+    const unsigned long long below = __ballot(sorted_keys[q] < k);
+    const int c = __popcll(below);
+    const int q_lo = lo + int(int64_t(hi - lo) * c / (kWave + 1));  // probe c - 1 (c > 0)
+    const int q_hi = lo + int(int64_t(hi - lo) * (c + 1) / (kWave + 1));  // probe c (c < 64)
+    const int nlo = c > 0 ? q_lo + 1 : lo;
+    const int nhi = c < kWave ? q_hi : hi;
+    lo = nlo;
+    hi = nhi;
   }
-  offsets[k] = lo;
+  const bool below = lo + lane < hi && sorted_keys[lo + lane] < k;
+  const int c = __popcll(__ballot(below));
+  if (lane == 0) *out = lo + c;
 }
 
-// Pre-sorted keys in one launch: thread i < E writes perm[i] = i, thread
-// k <= n_keys the offset of key k by binary search (as k_offsets).
+__global__ void k_offsets(const int32_t* __restrict__ sorted_keys, int E, int n_keys, int32_t* __restrict__ offsets) {
+  const int k = int((size_t(blockIdx.x) * blockDim.x + threadIdx.x) / kWave);
+  if (k > n_keys) return;  // whole waves
+  wave_lower_bound(sorted_keys, E, k, threadIdx.x % kWave, offsets + k);
+}
+
+// Pre-sorted keys in one launch: perm[i] = i for every i < E (grid-stride),
+// and the offsets as in k_offsets, one wave per key.
 __global__ void k_iota_offsets(const int32_t* __restrict__ sorted_keys, int E, int n_keys, int32_t* __restrict__ perm,
                                int32_t* __restrict__ offsets) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < E) perm[i] = i;
-  if (i <= n_keys) {
-    int lo = 0, hi = E;
-    while (lo < hi) {
-      const int mid = lo + ((hi - lo) >> 1);
-      if (sorted_keys[mid] < i)
-        lo = mid + 1;
-      else
-        hi = mid;
-    }
-    offsets[i] = lo;
-  }
+  const size_t gid = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  for (size_t i = gid; i < size_t(E); i += size_t(gridDim.x) * blockDim.x) perm[i] = int32_t(i);
+  const int k = int(gid / kWave);
+  if (k > n_keys) return;
+  wave_lower_bound(sorted_keys, E, k, threadIdx.x % kWave, offsets + k);
 }
 
 __global__ void k_fill_u32(uint32_t* __restrict__ p, size_t n) {
@@ -227,8 +236,9 @@ hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t s) {
 
 hipError_t launch_offsets_presorted(int n_keys, int E, const int32_t* sorted_keys, int32_t* perm, int32_t* offsets,
                                     hipStream_t s) {
-  const int n = E > n_keys + 1 ? E : n_keys + 1;
-  k_iota_offsets<<<dim3((n + 255) / 256), dim3(256), 0, s>>>(sorted_keys, E, n_keys, perm, offsets);
+  // one wave per key (n_keys + 1 of them); the perm writes stride over the grid
+  const size_t threads = size_t(n_keys + 1) * kWave;
+  k_iota_offsets<<<dim3(unsigned((threads + 255) / 256)), dim3(256), 0, s>>>(sorted_keys, E, n_keys, perm, offsets);
   return hipGetLastError();
 }
 
@@ -258,7 +268,8 @@ hipError_t launch_sort(const SortPlan& plan, const int32_t* keys, int /*key_stri
     kin = kout;
     vin = vout;
   }
-  k_offsets<<<dim3((plan.n_keys + 1 + 255) / 256), dim3(256), 0, s>>>(kin, E, plan.n_keys, offsets);
+  k_offsets<<<dim3(unsigned((size_t(plan.n_keys + 1) * kWave + 255) / 256)), dim3(256), 0, s>>>(kin, E, plan.n_keys,
+                                                                                                offsets);
   return hipGetLastError();
 }
 
